@@ -1,0 +1,227 @@
+"""Seeded synthetic inputs for the fused 3S operator.
+
+This module holds input generators only: graphs as CSR (int32 row_ptr,
+col_idx) and fp16 Q, K, V drawn from N(0, 1).  It contains none of the
+operator's arithmetic, and both the oracle and the HIP path consume exactly
+the arrays it returns.
+
+The five workloads stand in for the paper's evaluation inputs (Section 4.1,
+Table 6 single graphs, the batched LRGB/OGB graphs, and the sparse-transformer
+masks of Section 2.1), none of which are available here:
+
+1. ``er``        Erdos-Renyi, N=1024, ~16 neighbours/row incl. self-loop, d=64
+2. ``cl21``      Chung-Lu power law, N=65,536, exponent 2.1, mean degree 20,
+                 weights capped at 4096, self-loops, d=64
+3. ``cl25``      Chung-Lu, N=1,048,576, exponent 2.5, mean degree 16, cap
+                 4096, self-loops, node ids randomly permuted, d=128
+4. ``molecules`` 4096 graphs of 15-45 nodes: uniform random labelled tree
+                 (Pruefer code) plus 10% extra edges, undirected, self-loops,
+                 block-diagonal, d=64
+5. ``seqwin``    sequence length 32,768: local window [i-128, i+127] plus 64
+                 distinct uniformly drawn keys outside the window, d=64
+
+Every generator is deterministic in its seed: one child stream of
+``numpy.random.SeedSequence(seed)`` draws the graph, a second draws Q, K, V
+(float32 N(0,1) rounded to fp16 with round-to-nearest-even).
+"""
+import math
+
+import numpy as np
+
+CONFIGS = {
+    1: dict(name="er", N=1024, d=64),
+    2: dict(name="cl21", N=65536, d=64),
+    3: dict(name="cl25", N=1048576, d=128),
+    4: dict(name="molecules", N=None, d=64),
+    5: dict(name="seqwin", N=32768, d=64),
+}
+
+
+def _streams(seed):
+    g, f = np.random.SeedSequence(seed).spawn(2)
+    return np.random.default_rng(g), np.random.default_rng(f)
+
+
+def csr_from_edges(N, src, dst, self_loops=True, symmetric=True):
+    """Binary CSR (sorted, duplicate-free columns) from an edge list."""
+    src = np.asarray(src, dtype=np.int64)
+    dst = np.asarray(dst, dtype=np.int64)
+    if symmetric:
+        src, dst = np.concatenate([src, dst]), np.concatenate([dst, src])
+    if self_loops:
+        ids = np.arange(N, dtype=np.int64)
+        src, dst = np.concatenate([src, ids]), np.concatenate([dst, ids])
+    key = np.unique(src * N + dst)
+    rows = key // N
+    cols = (key % N).astype(np.int32)
+    row_ptr = np.zeros(N + 1, dtype=np.int64)
+    np.cumsum(np.bincount(rows, minlength=N), out=row_ptr[1:])
+    return row_ptr.astype(np.int32), cols
+
+
+def features(rng, N, d):
+    """Q, K, V: float32 N(0,1) rounded to fp16 (RNE)."""
+    out = []
+    for _ in range(3):
+        out.append(rng.standard_normal((N, d), dtype=np.float32).astype(np.float16))
+    return tuple(out)
+
+
+def erdos_renyi(rng, N=1024, avg_nbrs=15.0):
+    """Undirected G(N, p) with p = avg_nbrs / (N-1) over pairs i < j."""
+    p = avg_nbrs / (N - 1)
+    iu, ju = np.triu_indices(N, k=1)
+    keep = rng.random(iu.shape[0]) < p
+    return csr_from_edges(N, iu[keep], ju[keep])
+
+
+def chung_lu_weights(N, gamma, mean_deg, cap):
+    """Power-law expected degrees w_i = w_min (1 - (i+1/2)/N)^(-1/(gamma-1)),
+    capped at ``cap``, with w_min bisected so that mean(w) = mean_deg."""
+    base = (1.0 - (np.arange(N) + 0.5) / N) ** (-1.0 / (gamma - 1.0))
+    lo, hi = 1e-6, float(mean_deg)
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if np.minimum(mid * base, cap).mean() < mean_deg:
+            lo = mid
+        else:
+            hi = mid
+    return np.minimum(0.5 * (lo + hi) * base, cap)
+
+
+def chung_lu(rng, N, gamma, mean_deg, cap, permute):
+    """Chung-Lu graph by endpoint sampling: N*mean_deg/2 pairs, both ends
+    drawn independently with probability proportional to w; self-pairs are
+    dropped and repeats merged (so the realised mean degree is a little below
+    the target); undirected; self-loops added; ids optionally permuted."""
+    w = chung_lu_weights(N, gamma, mean_deg, cap)
+    cdf = np.cumsum(w)
+    cdf /= cdf[-1]
+    M = int(round(N * mean_deg / 2))
+    a = np.searchsorted(cdf, rng.random(M), side="right")
+    b = np.searchsorted(cdf, rng.random(M), side="right")
+    a = np.minimum(a, N - 1)
+    b = np.minimum(b, N - 1)
+    keep = a != b
+    a, b = a[keep], b[keep]
+    if permute:
+        perm = rng.permutation(N)
+        a, b = perm[a], perm[b]
+    return csr_from_edges(N, a, b)
+
+
+def _pruefer_tree(rng, n):
+    """Uniform random labelled tree on n >= 2 nodes via a Pruefer sequence."""
+    if n == 2:
+        return [(0, 1)]
+    seq = rng.integers(0, n, size=n - 2)
+    degree = np.ones(n, dtype=np.int64)
+    np.add.at(degree, seq, 1)
+    edges = []
+    import heapq
+    leaves = [i for i in range(n) if degree[i] == 1]
+    heapq.heapify(leaves)
+    for v in seq:
+        leaf = heapq.heappop(leaves)
+        edges.append((leaf, int(v)))
+        degree[v] -= 1
+        if degree[v] == 1:
+            heapq.heappush(leaves, int(v))
+    u = heapq.heappop(leaves)
+    v = heapq.heappop(leaves)
+    edges.append((u, v))
+    return edges
+
+
+def molecules(rng, n_graphs=4096, n_min=15, n_max=45, extra=0.10):
+    """Batched molecule-like graphs as one block-diagonal CSR."""
+    src, dst = [], []
+    base = 0
+    for _ in range(n_graphs):
+        n = int(rng.integers(n_min, n_max + 1))
+        tree = _pruefer_tree(rng, n)
+        present = set((min(a, b), max(a, b)) for a, b in tree)
+        want = int(round(extra * (n - 1)))
+        added = 0
+        while added < want:
+            a, b = (int(x) for x in rng.integers(0, n, size=2))
+            if a == b:
+                continue
+            e = (min(a, b), max(a, b))
+            if e in present:
+                continue
+            present.add(e)
+            added += 1
+        for a, b in present:
+            src.append(base + a)
+            dst.append(base + b)
+        base += n
+    return csr_from_edges(base, np.array(src), np.array(dst))
+
+
+def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
+    """Sparse-sequence mask: keys [i-before, i+after] (clipped) plus n_rand
+    distinct keys drawn uniformly from outside that window, per query."""
+    rows, cols = [], []
+    idx = np.arange(L, dtype=np.int64)
+    lo = np.maximum(idx - before, 0)
+    hi = np.minimum(idx + after, L - 1)
+    for i in range(L):
+        win = np.arange(lo[i], hi[i] + 1, dtype=np.int64)
+        outside = L - win.size
+        r = rng.choice(outside, size=min(n_rand, outside), replace=False)
+        r = np.where(r < lo[i], r, r + win.size)
+        c = np.concatenate([win, r])
+        rows.append(np.full(c.size, i, dtype=np.int64))
+        cols.append(c)
+    return csr_from_edges(L, np.concatenate(rows), np.concatenate(cols),
+                          self_loops=False, symmetric=False)
+
+
+def make_config(k, seed=0, with_features=True):
+    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V)."""
+    if k not in CONFIGS:
+        raise ValueError(f"unknown workload {k}")
+    cfg = CONFIGS[k]
+    g, f = _streams(seed)
+    if k == 1:
+        rp, ci = erdos_renyi(g, N=1024, avg_nbrs=15.0)
+    elif k == 2:
+        rp, ci = chung_lu(g, 65536, 2.1, 20.0, 4096.0, permute=False)
+    elif k == 3:
+        rp, ci = chung_lu(g, 1048576, 2.5, 16.0, 4096.0, permute=True)
+    elif k == 4:
+        rp, ci = molecules(g)
+    else:
+        rp, ci = sequence_window_random(g)
+    N = len(rp) - 1
+    d = cfg["d"]
+    out = dict(name=cfg["name"], N=N, d=d, scale=1.0 / math.sqrt(d),
+               row_ptr=rp, col_idx=ci)
+    if with_features:
+        out["Q"], out["K"], out["V"] = features(f, N, d)
+    return out
+
+
+def random_csr(rng, N, max_deg, empty_frac=0.0, dup_frac=0.0, shuffle=True):
+    """Small adversarial CSR: random degrees in [0, max_deg], optional empty
+    rows, optional repeated entries, columns in random order."""
+    rows = []
+    for i in range(N):
+        if rng.random() < empty_frac:
+            rows.append(np.zeros(0, dtype=np.int32))
+            continue
+        deg = int(rng.integers(1, max_deg + 1))
+        c = rng.choice(N, size=min(deg, N), replace=False).astype(np.int32)
+        if dup_frac > 0 and c.size:
+            nd = int(math.ceil(dup_frac * c.size))
+            c = np.concatenate([c, rng.choice(c, size=nd)])
+        if shuffle:
+            rng.shuffle(c)
+        else:
+            c.sort()
+        rows.append(c)
+    row_ptr = np.zeros(N + 1, dtype=np.int64)
+    row_ptr[1:] = np.cumsum([r.size for r in rows])
+    col_idx = np.concatenate(rows) if rows else np.zeros(0, dtype=np.int32)
+    return row_ptr.astype(np.int32), col_idx.astype(np.int32)
