@@ -1,0 +1,210 @@
+"""Benchmark of the fused 3S operator on one MI355X.
+
+Default workload: the 1,048,576-node Chung-Lu graph (exponent 2.5, mean
+degree 16, permuted ids, d = 128): the largest graph workload, on which the
+HBM-bandwidth target is set.  One "step" is one f3s_run call (the whole
+operator: block scores, mask, online softmax, value product, normalisation)
+over device-resident inputs.
+
+Prints ONE JSON line.  `value` is effective GFLOP/s = 4 * nnz * d / time,
+with nnz the distinct (row, column) pairs.  `roofline` prices the fused
+kernel against HBM bandwidth with the algorithmic bytes of one launch;
+`cpu_baseline` times the fp64 oracle on a bounded row sample on the host.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16 MFMA, published
+METRIC = "ms per fused 3S call and effective GFLOP/s (4*nnz*d) at 1 MI355X"
+COUNTERS_FILE = os.path.join(HERE, "profiles", "fused3s_cl25_d128_counters.json")
+KERNEL_SOURCES = [os.path.join(HERE, "paper_2505_08098_amd", "csrc", f)
+                  for f in ("fused3s.hip", "f3s_internal.h")]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(info, d):
+    """Bytes one launch must move at minimum without cache reuse: Q read and
+    O written once (6*N*d), the K and V rows of every distinct (window,
+    column) pair (4*d per pair), 64 B of column ids + 32 B of bitmap per
+    block, 16 B per work item."""
+    return (6 * info["N"] * d + 4 * d * info["n_unique"] + 96 * info["n_blocks"]
+            + 16 * info["n_items"])
+
+
+def traffic_from_counters(d):
+    """HBM bytes per launch measured by rocprofv3 counters, if they were taken
+    on the current kernel source; otherwise None."""
+    try:
+        with open(COUNTERS_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != kernel_source_hash() or rec.get("d") != d:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(c, O_gpu, sample_rows):
+    import numpy as np
+    import oracle
+    threads = min(16, len(os.sched_getaffinity(0)))
+    r1 = min(c["N"], sample_rows)
+    t0 = time.perf_counter()
+    ref = oracle.attention_rows_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                                    c["scale"], 0, r1, threads=threads)
+    dt = time.perf_counter() - t0
+    rp = c["row_ptr"]
+    nnz_sample = 0
+    ci = c["col_idx"]
+    for lo in range(0, r1, 65536):
+        hi = min(r1, lo + 65536)
+        rows = np.repeat(np.arange(lo, hi), np.diff(rp[lo:hi + 1]))
+        key = rows.astype(np.int64) * c["N"] + ci[rp[lo]:rp[hi]]
+        nnz_sample += np.unique(key).size
+    flops = 4.0 * nnz_sample * c["d"]
+    got = O_gpu[:r1].astype(np.float64)
+    diff = got - ref
+    parity = dict(rows=r1, max_abs=float(np.abs(diff).max()),
+                  rel_fro=float(np.linalg.norm(diff) / np.linalg.norm(ref)))
+    return dict(value=flops / dt / 1e9, unit="GFLOP/s", cores=threads, kind="oracle",
+                sample=f"rows 0..{r1} of the same workload ({nnz_sample} nnz, "
+                       f"{dt:.2f} s wall, fp64)",
+                ms=dt * 1e3), parity
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--cpu-rows", type=int, default=262144,
+                    help="rows of the workload in the oracle baseline sample")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2505_08098_amd as f3s
+    from paper_2505_08098_amd import workloads as W
+
+    f3s.load_library()
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    c = W.make_config(args.workload, seed=args.seed)
+    gen_s = time.perf_counter() - t0
+    N, d = c["N"], c["d"]
+    rp = torch.from_numpy(c["row_ptr"]).to(dev)
+    ci = torch.from_numpy(c["col_idx"]).to(dev)
+    Q = torch.from_numpy(c["Q"]).to(dev)
+    K = torch.from_numpy(c["K"]).to(dev)
+    V = torch.from_numpy(c["V"]).to(dev)
+    O = torch.empty((N, d), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    plan = f3s.Plan(rp, ci, N)
+    info = plan.info
+    stream = torch.cuda.current_stream(dev)
+
+    for _ in range(args.warmup):
+        f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
+    torch.cuda.synchronize()
+    # timed region: events on the launch stream around each call
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
+    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    ms = float(per.mean())
+
+    flops_eff = 4.0 * info["nnz"] * d
+    value = flops_eff / (ms * 1e-3) / 1e9
+    alg_bytes = algorithmic_bytes(info, d)
+    achieved = alg_bytes / (ms * 1e-3) / 1e9
+    issued = 1024.0 * d * info["n_blocks"]  # MFMA flops incl. zero padding
+    traffic = traffic_from_counters(d)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{c['name']}: " + {
+                1: "Erdos-Renyi N=1024, ~16 nbrs/row incl. self-loop, d=64",
+                2: "Chung-Lu N=65536, exponent 2.1, mean degree 20, cap 4096, self-loops, d=64",
+                3: "Chung-Lu N=1048576, exponent 2.5, mean degree 16, cap 4096, "
+                   "self-loops, permuted ids, d=128",
+                4: "4096 molecule-like graphs of 15-45 nodes, block-diagonal, d=64",
+                5: "sequence L=32768, window 256 + 64 random keys per query, d=64",
+            }[args.workload],
+            "N": N, "nnz": info["nnz"], "d": d, "scale": c["scale"], "seed": args.seed,
+            "parallelism": "single GPU",
+        },
+        "ms_p10": round(float(np.percentile(per, 10)), 5),
+        "ms_median": round(float(np.median(per)), 5),
+        "ms_p90": round(float(np.percentile(per, 90)), 5),
+        "wall_ms_per_step": round(wall_ms, 5),
+        "plan_ms": round(info["build_ms"], 3),
+        "plan": {k: info[k] for k in ("n_windows", "n_unique", "n_blocks", "max_blocks",
+                                      "piece_blocks", "n_items", "n_split", "n_pieces")},
+        "launches_per_call": 1 + (info["n_split"] > 0),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg_bytes,
+            "kernel": "k_fused3s<%d>" % d,
+            "mfma_issued_frac": round(issued / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+        },
+        "gen_s": round(gen_s, 1),
+    }
+    if not args.no_cpu:
+        torch.cuda.synchronize()
+        O_host = O.cpu().numpy()
+        base, parity = cpu_baseline(c, O_host, args.cpu_rows)
+        out["cpu_baseline"] = base
+        out["parity_sample"] = parity
+    else:
+        out["cpu_baseline"] = None
+    plan.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,129 @@
+/*
+ * f3s.h -- fused sparse attention (3S) on AMD MI355X (gfx950).
+ *
+ * The operator (Fused3S, Section 2.1, Eq. 1, with the masked reading of the
+ * element-wise product and the max-stabilised online softmax of Section 3.5):
+ *
+ *     O = softmax_rows( mask_A( scale * Q K^T ) ) V
+ *
+ * A is a binary N x N pattern given as CSR.  For row i only the columns j
+ * with A[i][j] != 0 enter the softmax; a row without any such column gives
+ * O[i,:] = 0.  Precisions follow Table 5: Q, K, V fp16, scores and softmax
+ * fp32, the normalised scores cast to fp16 for the second product, O fp32.
+ *
+ * Two calls:
+ *   f3s_plan  builds, on the GPU, the Binary Sparse Block layout of
+ *             Section 3.1 (16-row windows, all-zero columns removed, 16x16
+ *             blocks with one 256-bit bitmap each) and the heavy-first work
+ *             list of Section 3.2 (with heavy windows split into pieces).
+ *   f3s_run   evaluates the operator with the fused kernel of Algorithm 1
+ *             (score block, mask, online softmax, fp16 probabilities, value
+ *             product, final normalisation; scores never reach HBM).
+ *
+ * Threading: calls are thread-safe except that one plan must not be used by
+ * two f3s_run calls that overlap in time (they share the plan's partial-result
+ * scratch).  Different plans may run concurrently.
+ */
+#ifndef F3S_H
+#define F3S_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    F3S_OK = 0,
+    F3S_ERR_INVALID_VALUE = 1, /* null/misaligned pointer, bad size, aliasing   */
+    F3S_ERR_INVALID_CSR = 2,   /* row_ptr[0] != 0, decreasing, column not in [0,N) */
+    F3S_ERR_UNSUPPORTED = 3,   /* d not a multiple of 32 in [32, 256]           */
+    F3S_ERR_OUT_OF_MEMORY = 4, /* a device allocation failed                    */
+    F3S_ERR_HIP = 5            /* any other HIP runtime error                   */
+} f3s_status_t;
+
+typedef struct f3s_plan_s *f3s_plan_t;
+
+typedef struct {
+    int32_t N;             /* rows (= columns) of A                              */
+    int32_t n_windows;     /* T_r = ceil(N / 16)  (Algorithm 1)                  */
+    int64_t nnz_csr;       /* entries in the CSR, repeats included               */
+    int64_t nnz;           /* distinct (row, column) pairs: the non-zeros of A   */
+    int64_t n_unique;      /* sum over windows of distinct columns (bc, Table 3) */
+    int64_t n_blocks;      /* 16x16 blocks (b, Table 3)                          */
+    int32_t max_blocks;    /* largest block count of one window                  */
+    int32_t piece_blocks;  /* windows with more blocks are split into pieces     */
+    int32_t n_items;       /* work items (windows or pieces) in the work list    */
+    int32_t n_split;       /* windows that were split                            */
+    int32_t n_pieces;      /* pieces in total (partial-result slots)             */
+    int32_t reserved;
+    int64_t bsb_bytes;     /* window offsets + column lists + bitmaps            */
+    int64_t device_bytes;  /* everything the plan holds on the device            */
+    double build_ms;       /* wall time of f3s_plan                              */
+} f3s_plan_info_t;
+
+/*
+ * Build a plan from a CSR pattern that lives in DEVICE memory.
+ *   row_ptr  int32[N+1], row_ptr[0] == 0, non-decreasing
+ *   col_idx  int32[row_ptr[N]], every entry in [0, N); order inside a row is
+ *            free and repeated entries count once (A is binary, Section 3.1)
+ *   N        >= 0; N == 0 gives a valid empty plan
+ * The plan copies what it needs: the caller may free the CSR on return.
+ * Synchronous on the current device's null stream.  Returns NULL on error;
+ * f3s_last_error() then tells why (F3S_ERR_INVALID_CSR for a malformed
+ * pattern, nothing is leaked).
+ */
+f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N);
+
+/*
+ * O = softmax_rows(mask_A(scale * Q K^T)) V  (Algorithm 1, Section 3).
+ *   Q, K, V  device, fp16, N x d row-major, contiguous, 16-byte aligned; they
+ *            may alias each other (Q = K = V as in AGNN, Section 2.1)
+ *   O        device, fp32, N x d row-major, 16-byte aligned, must not overlap
+ *            Q, K or V; every row is overwritten (empty rows with 0)
+ *   d        multiple of 32, 32 <= d <= 256
+ *   scale    finite; multiplies the fp32 dot products
+ *   stream   HIP stream; the call is asynchronous on it, allocates nothing
+ *            and copies nothing between host and device
+ * Inputs must be finite.  Returns F3S_OK or an error code (no launch happens
+ * on an argument error).
+ */
+f3s_status_t f3s_run(f3s_plan_t plan, const void *Q, const void *K, const void *V,
+                     void *O, int32_t d, float scale, hipStream_t stream);
+
+/* Release a plan and all its device memory.  NULL is a no-op. */
+void f3s_destroy(f3s_plan_t plan);
+
+/* Sizes and statistics of a plan (host struct filled on return). */
+f3s_status_t f3s_plan_info(f3s_plan_t plan, f3s_plan_info_t *out);
+
+/*
+ * Copy the plan's layout to HOST buffers (for inspection and tests).  Any
+ * pointer may be NULL to skip that array.  Sizes come from f3s_plan_info:
+ *   blk_off  int32[n_windows + 1]  first block of each window (the tro array)
+ *   cols     int32[16 * n_blocks]  original column of each compacted block
+ *                                  column (the sptd gather list), -1 = padding
+ *   mask     uint32[8 * n_blocks]  bitmap of each block: the non-zero at
+ *                                  window row r, block column c is bit
+ *                                  k = 4*(r + 16*(c/4)) + c%4, i.e. bit k%32 of
+ *                                  word k/32
+ *   items    int32[4 * n_items]    work list in launch order: window, first
+ *                                  block, end block, partial slot (-1 = none)
+ *   merges   int32[3 * n_split]    split windows: window, first slot, pieces
+ * Synchronous.
+ */
+f3s_status_t f3s_plan_export(f3s_plan_t plan, int32_t *blk_off, int32_t *cols,
+                             uint32_t *mask, int32_t *items, int32_t *merges);
+
+/* Status of the last failing call on this thread (F3S_OK if none). */
+f3s_status_t f3s_last_error(void);
+
+/* Static, human-readable name of a status code. */
+const char *f3s_status_string(f3s_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* F3S_H */

@@ -59,6 +59,19 @@ static double half_bits_to_double(uint16_t h)
 
 double oracle_half_to_double(uint16_t h) { return half_bits_to_double(h); }
 
+/* Decoding table: entry h is half_bits_to_double(h) (filled once). */
+static double g_half_table[65536];
+static int g_half_table_ready = 0;
+
+static void fill_half_table(void)
+{
+    if (g_half_table_ready) return;
+    for (int h = 0; h < 65536; ++h) g_half_table[h] = half_bits_to_double((uint16_t)h);
+    g_half_table_ready = 1;
+}
+
+#define H2D(h) (g_half_table[(h)])
+
 static int cmp_int32(const void *a, const void *b)
 {
     int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
@@ -102,6 +115,7 @@ int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
     int rc = oracle_check_csr(N, row_ptr, col_idx);
     if (rc) return rc;
     if (d <= 0) return -5;
+    fill_half_table();
 #ifdef _OPENMP
     if (nthreads > 0) omp_set_num_threads(nthreads);
 #else
@@ -135,7 +149,7 @@ int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
             const uint16_t *kr = K + (int64_t)nb[a] * d;
             double acc = 0.0;
             for (int32_t k = 0; k < d; ++k)
-                acc += half_bits_to_double(q[k]) * half_bits_to_double(kr[k]);
+                acc += H2D(q[k]) * H2D(kr[k]);
             s[a] = scale * acc;
         }
         /* 3. row max */
@@ -152,7 +166,7 @@ int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
         for (int64_t a = 0; a < u; ++a) {
             double p = s[a] / l;
             const uint16_t *vr = V + (int64_t)nb[a] * d;
-            for (int32_t k = 0; k < d; ++k) o[k] += p * half_bits_to_double(vr[k]);
+            for (int32_t k = 0; k < d; ++k) o[k] += p * H2D(vr[k]);
             if (P) {
                 for (int64_t k = beg; k < end; ++k)
                     if (col_idx[k] == nb[a]) { P[k] = p; break; }

@@ -1,0 +1,212 @@
+"""ctypes binding of libf3s.so: argument marshalling only.
+
+Every step of the operator runs in the HIP library; this module passes device
+pointers, sizes and the current HIP stream.  torch is used for device memory
+and streams.  A missing or unloadable library is an error: there is no
+fallback path of any kind.
+"""
+import ctypes
+import math
+import os
+
+import torch  # noqa: F401  (loads torch's HIP runtime before libf3s.so; see _load)
+
+from . import build as _build
+
+F3S_OK = 0
+_STATUS = {0: "F3S_OK", 1: "F3S_ERR_INVALID_VALUE", 2: "F3S_ERR_INVALID_CSR",
+           3: "F3S_ERR_UNSUPPORTED", 4: "F3S_ERR_OUT_OF_MEMORY", 5: "F3S_ERR_HIP"}
+
+
+class F3SError(RuntimeError):
+    def __init__(self, code, what):
+        self.code = code
+        super().__init__(f"{what}: {_STATUS.get(code, code)}")
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("N", ctypes.c_int32), ("n_windows", ctypes.c_int32),
+        ("nnz_csr", ctypes.c_int64), ("nnz", ctypes.c_int64),
+        ("n_unique", ctypes.c_int64), ("n_blocks", ctypes.c_int64),
+        ("max_blocks", ctypes.c_int32), ("piece_blocks", ctypes.c_int32),
+        ("n_items", ctypes.c_int32), ("n_split", ctypes.c_int32),
+        ("n_pieces", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("bsb_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
+        ("build_ms", ctypes.c_double),
+    ]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+
+
+_LIB = None
+
+
+def _hip_runtimes_mapped():
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64" in line:
+                    paths.add(os.path.realpath(line.split()[-1]))
+    except OSError:
+        pass
+    return paths
+
+
+def load_library():
+    """Load libf3s.so (raises if it is missing or not loadable).
+
+    torch is imported first so that its HIP runtime is the one libf3s.so
+    binds to (both carry the soname libamdhip64.so.7); a second runtime in
+    the process would make torch's stream handles meaningless to the library.
+    """
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(_build.LIB):
+        raise RuntimeError(
+            f"{_build.LIB} is missing: build it with "
+            "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(_build.LIB)
+    runtimes = _hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise RuntimeError(f"two HIP runtimes mapped in one process: {sorted(runtimes)}")
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    L.f3s_plan.argtypes = [vp, vp, i32]
+    L.f3s_plan.restype = vp
+    L.f3s_run.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp]
+    L.f3s_run.restype = ctypes.c_int
+    L.f3s_destroy.argtypes = [vp]
+    L.f3s_destroy.restype = None
+    L.f3s_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
+    L.f3s_plan_info.restype = ctypes.c_int
+    L.f3s_plan_export.argtypes = [vp, vp, vp, vp, vp, vp]
+    L.f3s_plan_export.restype = ctypes.c_int
+    L.f3s_last_error.argtypes = []
+    L.f3s_last_error.restype = ctypes.c_int
+    L.f3s_status_string.argtypes = [ctypes.c_int]
+    L.f3s_status_string.restype = ctypes.c_char_p
+    _LIB = L
+    return L
+
+
+def status_string(code):
+    return load_library().f3s_status_string(int(code)).decode()
+
+
+def _check_device_tensor(t, name, dtype):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class Plan:
+    """f3s_plan on a device CSR (int32 row_ptr[N+1], int32 col_idx[nnz])."""
+
+    def __init__(self, row_ptr, col_idx, N):
+        L = load_library()
+        _check_device_tensor(row_ptr, "row_ptr", torch.int32)
+        _check_device_tensor(col_idx, "col_idx", torch.int32)
+        if row_ptr.numel() != int(N) + 1:
+            raise ValueError("row_ptr must hold N + 1 entries")
+        with torch.cuda.device(row_ptr.device):
+            torch.cuda.current_stream().synchronize()
+            h = L.f3s_plan(row_ptr.data_ptr(), col_idx.data_ptr() if col_idx.numel() else None,
+                           int(N))
+        if not h:
+            raise F3SError(L.f3s_last_error(), "f3s_plan")
+        self._h = h
+        self.device = row_ptr.device
+        self.N = int(N)
+        self.info = self._info()
+
+    def _info(self):
+        inf = PlanInfo()
+        rc = load_library().f3s_plan_info(self._h, ctypes.byref(inf))
+        if rc != F3S_OK:
+            raise F3SError(rc, "f3s_plan_info")
+        return inf.as_dict()
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise RuntimeError("plan was destroyed")
+        return self._h
+
+    def export(self):
+        """The plan's arrays copied to host numpy arrays."""
+        import numpy as np
+        inf = self.info
+        T, B = inf["n_windows"], inf["n_blocks"]
+        blk_off = np.empty(T + 1, dtype=np.int32)
+        cols = np.empty(max(16 * B, 1), dtype=np.int32)
+        mask = np.empty(max(8 * B, 1), dtype=np.uint32)
+        items = np.empty(max(4 * inf["n_items"], 1), dtype=np.int32)
+        merges = np.empty(max(3 * inf["n_split"], 1), dtype=np.int32)
+        ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+        rc = load_library().f3s_plan_export(self.handle, ptr(blk_off), ptr(cols), ptr(mask),
+                                            ptr(items), ptr(merges))
+        if rc != F3S_OK:
+            raise F3SError(rc, "f3s_plan_export")
+        return dict(blk_off=blk_off, cols=cols[: 16 * B], mask=mask[: 8 * B],
+                    items=items[: 4 * inf["n_items"]].reshape(-1, 4),
+                    merges=merges[: 3 * inf["n_split"]].reshape(-1, 3))
+
+    def close(self):
+        if self._h is not None:
+            load_library().f3s_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def run(plan, Q, K, V, scale=None, out=None, stream=None):
+    """O = softmax_rows(mask_A(scale Q K^T)) V through f3s_run.
+
+    Q, K, V: fp16 device tensors [N, d]; out: optional fp32 [N, d]; the call is
+    asynchronous on ``stream`` (default: torch's current stream).
+    """
+    L = load_library()
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check_device_tensor(t, n, torch.float16)
+        if t.dim() != 2 or t.shape[0] != plan.N:
+            raise ValueError(f"{n} must be [N, d] with N = {plan.N}")
+    d = Q.shape[1]
+    if K.shape[1] != d or V.shape[1] != d:
+        raise ValueError("Q, K, V must share d")
+    if out is None:
+        out = torch.empty((plan.N, d), dtype=torch.float32, device=Q.device)
+    else:
+        _check_device_tensor(out, "out", torch.float32)
+        if tuple(out.shape) != (plan.N, d):
+            raise ValueError("out must be [N, d]")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if stream is None:
+        stream = torch.cuda.current_stream(Q.device)
+    rc = L.f3s_run(plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(),
+                   int(d), float(scale), ctypes.c_void_p(stream.cuda_stream))
+    if rc != F3S_OK:
+        raise F3SError(rc, "f3s_run")
+    return out
+
+
+def run_raw(plan, q_ptr, k_ptr, v_ptr, o_ptr, d, scale, stream_handle):
+    """f3s_run on raw device addresses (returns the status code)."""
+    return load_library().f3s_run(plan.handle, q_ptr, k_ptr, v_ptr, o_ptr, int(d),
+                                  float(scale), ctypes.c_void_p(stream_handle))

@@ -1,0 +1,379 @@
+// C ABI of the f3s library: argument checks, plan orchestration, dispatch.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <chrono>
+#include <new>
+#include <vector>
+
+#include "f3s_internal.h"
+
+namespace {
+
+thread_local f3s_status_t g_last_error = F3S_OK;
+
+f3s_status_t fail(f3s_status_t s)
+{
+    g_last_error = s;
+    return s;
+}
+
+f3s_status_t from_hip(hipError_t e)
+{
+    if (e == hipSuccess) return F3S_OK;
+    return e == hipErrorOutOfMemory ? F3S_ERR_OUT_OF_MEMORY : F3S_ERR_HIP;
+}
+
+// Device scratch owned by one f3s_plan call; freed on every exit path.
+struct Scratch {
+    std::vector<void *> ptrs;
+    ~Scratch()
+    {
+        for (void *p : ptrs) (void)hipFree(p);
+    }
+    template <typename T>
+    hipError_t alloc(T **out, int64_t count)
+    {
+        *out = nullptr;
+        if (count <= 0) count = 1;
+        void *p = nullptr;
+        hipError_t e = hipMalloc(&p, (size_t)count * sizeof(T));
+        if (e != hipSuccess) return e;
+        ptrs.push_back(p);
+        *out = static_cast<T *>(p);
+        return hipSuccess;
+    }
+};
+
+template <typename T>
+hipError_t plan_alloc(f3s_plan_s *p, T **out, int64_t count)
+{
+    *out = nullptr;
+    if (count <= 0) count = 1;
+    void *ptr = nullptr;
+    hipError_t e = hipMalloc(&ptr, (size_t)count * sizeof(T));
+    if (e != hipSuccess) return e;
+    *out = static_cast<T *>(ptr);
+    p->device_bytes += (int64_t)((size_t)count * sizeof(T));
+    return hipSuccess;
+}
+
+void free_plan_arrays(f3s_plan_s *p)
+{
+    void *arrs[] = {p->blk_off, p->cols, p->mask, p->items, p->merges, p->part_o,
+                    p->part_ml};
+    for (void *a : arrs)
+        if (a) (void)hipFree(a);
+    p->blk_off = nullptr;
+    p->cols = nullptr;
+    p->mask = nullptr;
+    p->items = nullptr;
+    p->merges = nullptr;
+    p->part_o = nullptr;
+    p->part_ml = nullptr;
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *v = getenv(name);
+    if (!v || !*v) return dflt;
+    return atoi(v);
+}
+
+#define HIP_TRY(expr)                                          \
+    do {                                                       \
+        hipError_t e_ = (expr);                                \
+        if (e_ != hipSuccess) return from_hip(e_);             \
+    } while (0)
+
+template <typename T>
+hipError_t read_scalar(T *host, const T *dev)
+{
+    return hipMemcpy(host, dev, sizeof(T), hipMemcpyDeviceToHost);
+}
+
+// Work-list piece size: aim for at most one piece's worth of blocks per
+// wavefront slot so the tail of the launch stays short; even, >= 16.
+int choose_piece(int64_t n_blocks, int device)
+{
+    int env = env_int("F3S_PIECE_BLOCKS", 0);
+    if (env >= 2) return env & ~1;
+    int cus = 256;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) == hipSuccess && prop.multiProcessorCount > 0)
+        cus = prop.multiProcessorCount;
+    const int64_t slots = (int64_t)cus * 8;
+    int64_t piece = (n_blocks + slots - 1) / slots;
+    if (piece < 16) piece = 16;
+    if (piece > (1 << 20)) piece = 1 << 20;
+    return (int)((piece + 1) & ~1LL);
+}
+
+f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *col_idx)
+{
+    using namespace f3s;
+    const hipStream_t s = nullptr;
+    const int32_t N = p->N;
+    const int32_t T = p->T;
+    Scratch tmp;
+
+    // ---- 1. nnz and row_ptr validation --------------------------------
+    int32_t ends[2] = {0, 0};
+    HIP_TRY(hipMemcpy(&ends[0], row_ptr, sizeof(int32_t), hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&ends[1], row_ptr + N, sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (ends[0] != 0 || ends[1] < 0) return F3S_ERR_INVALID_CSR;
+    const int32_t nnz = ends[1];
+    if (nnz > 0 && !col_idx) return F3S_ERR_INVALID_VALUE;
+    p->nnz_csr = nnz;
+
+    int32_t *err = nullptr;
+    HIP_TRY(tmp.alloc(&err, 4));
+    HIP_TRY(hipMemset(err, 0, 4 * sizeof(int32_t)));
+    HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, err, s));
+    int32_t herr = 0;
+    HIP_TRY(read_scalar(&herr, err));
+    if (herr) return F3S_ERR_INVALID_CSR;
+
+    // ---- 2. distinct columns per window -------------------------------
+    int32_t *tmp_cols = nullptr, *u = nullptr, *heavy = nullptr, *n_heavy = err + 1;
+    HIP_TRY(tmp.alloc(&tmp_cols, nnz));
+    HIP_TRY(tmp.alloc(&u, T));
+    HIP_TRY(tmp.alloc(&heavy, T));
+    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, T, tmp_cols, u, heavy, n_heavy,
+                               err, s));
+    int32_t hh[2] = {0, 0};
+    HIP_TRY(hipMemcpy(hh, err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (hh[0]) return F3S_ERR_INVALID_CSR;
+    const int32_t n_heavy_h = hh[1];
+    if (n_heavy_h > 0) {
+        const int32_t words = (N + 31) / 32;
+        const int64_t budget = 256ll << 20;  // bitmap workspace per batch
+        int64_t per = (int64_t)words * 4;
+        int32_t batch = (int32_t)(budget / per);
+        if (batch < 1) batch = 1;
+        if (batch > n_heavy_h) batch = n_heavy_h;
+        uint32_t *bitmap = nullptr;
+        HIP_TRY(tmp.alloc(&bitmap, (int64_t)batch * words));
+        for (int32_t first = 0; first < n_heavy_h; first += batch) {
+            const int32_t cnt = n_heavy_h - first < batch ? n_heavy_h - first : batch;
+            HIP_TRY(hipMemsetAsync(bitmap, 0, (size_t)cnt * words * 4, s));
+            HIP_TRY(launch_heavy_compact(row_ptr, col_idx, N, heavy + first, cnt,
+                                         bitmap, words, tmp_cols, u, err, s));
+        }
+        HIP_TRY(read_scalar(&herr, err));
+        if (herr) return F3S_ERR_INVALID_CSR;
+    }
+
+    // ---- 3. blocks per window and their prefix (tro) ------------------
+    int32_t *nb = nullptr;
+    HIP_TRY(tmp.alloc(&nb, T));
+    HIP_TRY(plan_alloc(p, &p->blk_off, (int64_t)T + 1));
+    HIP_TRY(launch_blocks_per_window(u, T, nb, s));
+    HIP_TRY(launch_scan(nb, p->blk_off, T, s));
+    int32_t B = 0;
+    HIP_TRY(read_scalar(&B, p->blk_off + T));
+    p->n_blocks = B;
+
+    unsigned long long *acc = nullptr;
+    HIP_TRY(tmp.alloc(&acc, 2));
+    HIP_TRY(hipMemset(acc, 0, 2 * sizeof(unsigned long long)));
+    HIP_TRY(launch_sum_i32(u, T, acc, s));
+    HIP_TRY(hipMemset(err + 2, 0, sizeof(int32_t)));
+    HIP_TRY(launch_max_i32(nb, T, err + 2, s));
+
+    // ---- 4. column lists and bitmaps ----------------------------------
+    HIP_TRY(plan_alloc(p, &p->cols, (int64_t)kBlockCols * B));
+    HIP_TRY(plan_alloc(p, &p->mask, (int64_t)kMaskWords * B));
+    HIP_TRY(hipMemsetAsync(p->mask, 0, (size_t)kMaskWords * B * 4, s));
+    HIP_TRY(launch_fill_windows(row_ptr, col_idx, N, T, tmp_cols, u, p->blk_off,
+                                p->cols, p->mask, s));
+    HIP_TRY(launch_count_bits(p->mask, (int64_t)kMaskWords * B, acc + 1, s));
+    unsigned long long hacc[2] = {0, 0};
+    HIP_TRY(hipMemcpy(hacc, acc, sizeof(hacc), hipMemcpyDeviceToHost));
+    p->n_unique = (int64_t)hacc[0];
+    p->nnz = (int64_t)hacc[1];
+    HIP_TRY(read_scalar(&p->max_blocks, err + 2));
+    p->bsb_bytes = 4ll * (T + 1) + 4ll * kBlockCols * B + 4ll * kMaskWords * B;
+
+    // ---- 5. heavy-first work list -------------------------------------
+    const int32_t piece = choose_piece(B, p->device);
+    p->piece = piece;
+    int32_t *npieces, *key, *split_pieces, *split_one;
+    HIP_TRY(tmp.alloc(&npieces, T));
+    HIP_TRY(tmp.alloc(&key, T));
+    HIP_TRY(tmp.alloc(&split_pieces, (int64_t)T + 1));
+    HIP_TRY(tmp.alloc(&split_one, (int64_t)T + 1));
+    HIP_TRY(launch_bin_keys(nb, T, piece, npieces, key, split_pieces, split_one, s));
+    HIP_TRY(launch_scan(split_pieces, split_pieces, T, s));  // -> slot base
+    HIP_TRY(launch_scan(split_one, split_one, T, s));        // -> split index
+    int32_t tot[2];
+    HIP_TRY(read_scalar(&tot[0], split_pieces + T));
+    HIP_TRY(read_scalar(&tot[1], split_one + T));
+    p->n_pieces = tot[0];
+    p->n_split = tot[1];
+
+    const int32_t chunk = 64;
+    const int32_t nchunks = (T + chunk - 1) / chunk;
+    const int64_t cells = (int64_t)(piece + 1) * nchunks;
+    if (cells >= INT32_MAX) return F3S_ERR_UNSUPPORTED;
+    int32_t *hist = nullptr;
+    HIP_TRY(tmp.alloc(&hist, cells + 1));
+    HIP_TRY(hipMemsetAsync(hist, 0, (size_t)(cells + 1) * 4, s));
+    HIP_TRY(launch_bin_hist(npieces, key, T, piece, chunk, nchunks, hist, s));
+    HIP_TRY(launch_scan(hist, hist, (int32_t)cells, s));
+    int32_t n_items = 0;
+    HIP_TRY(read_scalar(&n_items, hist + cells));
+    p->n_items = n_items;
+    HIP_TRY(plan_alloc(p, &p->items, n_items));
+    HIP_TRY(plan_alloc(p, &p->merges, 3ll * p->n_split));
+    HIP_TRY(launch_bin_scatter(nb, p->blk_off, npieces, key, split_pieces, split_one,
+                               T, piece, chunk, nchunks, hist, p->items, p->merges, s));
+    if (p->n_pieces > 0) {
+        HIP_TRY(plan_alloc(p, &p->part_o, (int64_t)p->n_pieces * kWindowRows * kMaxD));
+        HIP_TRY(plan_alloc(p, &p->part_ml, (int64_t)p->n_pieces * 32));
+    }
+    // ---- 6. integrity check of the finished plan ------------------------
+    HIP_TRY(hipMemset(err, 0, sizeof(int32_t)));
+    HIP_TRY(launch_validate_plan(*p, err, s));
+    HIP_TRY(read_scalar(&herr, err));
+    if (herr) return F3S_ERR_HIP;
+    return F3S_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlaps(const void *a, size_t na, const void *b, size_t nb)
+{
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *f3s_status_string(f3s_status_t status)
+{
+    switch (status) {
+    case F3S_OK: return "F3S_OK";
+    case F3S_ERR_INVALID_VALUE: return "F3S_ERR_INVALID_VALUE";
+    case F3S_ERR_INVALID_CSR: return "F3S_ERR_INVALID_CSR";
+    case F3S_ERR_UNSUPPORTED: return "F3S_ERR_UNSUPPORTED";
+    case F3S_ERR_OUT_OF_MEMORY: return "F3S_ERR_OUT_OF_MEMORY";
+    case F3S_ERR_HIP: return "F3S_ERR_HIP";
+    }
+    return "F3S_ERR_UNKNOWN";
+}
+
+f3s_status_t f3s_last_error(void) { return g_last_error; }
+
+f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N)
+{
+    const auto t0 = std::chrono::steady_clock::now();
+    if (N < 0 || (N > 0 && !row_ptr)) {
+        fail(F3S_ERR_INVALID_VALUE);
+        return nullptr;
+    }
+    f3s_plan_s *p = new (std::nothrow) f3s_plan_s();
+    if (!p) {
+        fail(F3S_ERR_OUT_OF_MEMORY);
+        return nullptr;
+    }
+    p->N = N;
+    p->T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
+    f3s_status_t st = from_hip(hipGetDevice(&p->device));
+    if (st == F3S_OK) {
+        if (N == 0) {
+            st = from_hip(plan_alloc(p, &p->blk_off, 1));
+            if (st == F3S_OK) st = from_hip(hipMemset(p->blk_off, 0, sizeof(int32_t)));
+            p->piece = 16;
+        } else {
+            st = build_plan(p, row_ptr, col_idx);
+        }
+    }
+    if (st != F3S_OK) {
+        (void)hipDeviceSynchronize();
+        (void)hipGetLastError();
+        free_plan_arrays(p);
+        delete p;
+        fail(st);
+        return nullptr;
+    }
+    p->build_ms = std::chrono::duration<double, std::milli>(
+                      std::chrono::steady_clock::now() - t0).count();
+    return p;
+}
+
+void f3s_destroy(f3s_plan_t plan)
+{
+    if (!plan) return;
+    free_plan_arrays(plan);
+    delete plan;
+}
+
+f3s_status_t f3s_plan_info(f3s_plan_t p, f3s_plan_info_t *out)
+{
+    if (!p || !out) return fail(F3S_ERR_INVALID_VALUE);
+    memset(out, 0, sizeof(*out));
+    out->N = p->N;
+    out->n_windows = p->T;
+    out->nnz_csr = p->nnz_csr;
+    out->nnz = p->nnz;
+    out->n_unique = p->n_unique;
+    out->n_blocks = p->n_blocks;
+    out->max_blocks = p->max_blocks;
+    out->piece_blocks = p->piece;
+    out->n_items = p->n_items;
+    out->n_split = p->n_split;
+    out->n_pieces = p->n_pieces;
+    out->bsb_bytes = p->bsb_bytes;
+    out->device_bytes = p->device_bytes;
+    out->build_ms = p->build_ms;
+    return F3S_OK;
+}
+
+f3s_status_t f3s_plan_export(f3s_plan_t p, int32_t *blk_off, int32_t *cols,
+                             uint32_t *mask, int32_t *items, int32_t *merges)
+{
+    if (!p) return fail(F3S_ERR_INVALID_VALUE);
+    struct {
+        void *dst;
+        const void *src;
+        size_t bytes;
+    } cp[] = {
+        {blk_off, p->blk_off, 4ull * (p->T + 1)},
+        {cols, p->cols, 4ull * f3s::kBlockCols * p->n_blocks},
+        {mask, p->mask, 4ull * f3s::kMaskWords * p->n_blocks},
+        {items, p->items, sizeof(f3s::WorkItem) * p->n_items},
+        {merges, p->merges, 12ull * p->n_split},
+    };
+    for (auto &c : cp) {
+        if (!c.dst || c.bytes == 0) continue;
+        f3s_status_t st = from_hip(hipMemcpy(c.dst, c.src, c.bytes, hipMemcpyDeviceToHost));
+        if (st != F3S_OK) return fail(st);
+    }
+    return F3S_OK;
+}
+
+f3s_status_t f3s_run(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                     void *O, int32_t d, float scale, hipStream_t stream)
+{
+    if (!p) return fail(F3S_ERR_INVALID_VALUE);
+    if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
+    if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
+    if (p->N == 0) return F3S_OK;
+    if (!Q || !K || !V || !O) return fail(F3S_ERR_INVALID_VALUE);
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O))
+        return fail(F3S_ERR_INVALID_VALUE);
+    const size_t in_bytes = (size_t)p->N * d * 2, out_bytes = (size_t)p->N * d * 4;
+    if (overlaps(O, out_bytes, Q, in_bytes) || overlaps(O, out_bytes, K, in_bytes) ||
+        overlaps(O, out_bytes, V, in_bytes))
+        return fail(F3S_ERR_INVALID_VALUE);
+    // base-2 softmax: 2^(x * scale * log2 e) == e^(x * scale)
+    const float sl2 = (float)((double)scale * 1.4426950408889634);
+    f3s_status_t st = from_hip(f3s::launch_fused(*p, Q, K, V, O, d, sl2, stream));
+    return st == F3S_OK ? F3S_OK : fail(st);
+}
+
+}  // extern "C"

@@ -1,0 +1,107 @@
+// Internal declarations shared by the f3s HIP sources (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "f3s.h"
+
+namespace f3s {
+
+constexpr int kWindowRows = 16;   // r: rows per row window (Section 3.1)
+constexpr int kBlockCols = 16;    // c: compacted columns per block
+constexpr int kMaskWords = 8;     // 256-bit bitmap per 16x16 block
+constexpr int kMaxD = 256;        // largest supported feature dimension
+
+// One unit of work for the fused kernel: a whole row window or one piece of
+// a split window.  Blocks are absolute indices into the plan's block arrays.
+struct WorkItem {
+    int32_t window;
+    int32_t blk_begin;
+    int32_t blk_end;
+    int32_t slot;  // partial-result slot of a piece, -1 for a whole window
+};
+static_assert(sizeof(WorkItem) == 16, "WorkItem must be 16 bytes");
+
+}  // namespace f3s
+
+struct f3s_plan_s {
+    int device = 0;
+    int32_t N = 0;
+    int32_t T = 0;               // row windows
+    int64_t nnz_csr = 0;
+    int64_t nnz = 0;             // distinct (row, col) pairs
+    int64_t n_unique = 0;
+    int64_t n_blocks = 0;
+    int32_t max_blocks = 0;
+    int32_t piece = 0;
+    int32_t n_items = 0;
+    int32_t n_split = 0;
+    int32_t n_pieces = 0;
+    int32_t *blk_off = nullptr;  // [T + 1]
+    int32_t *cols = nullptr;     // [16 * n_blocks]
+    uint32_t *mask = nullptr;    // [8 * n_blocks]
+    f3s::WorkItem *items = nullptr;  // [n_items]
+    int32_t *merges = nullptr;   // [3 * n_split]
+    float *part_o = nullptr;     // [n_pieces * 16 * kMaxD]
+    float *part_ml = nullptr;    // [n_pieces * 32]: 16 maxima then 16 sums
+    int64_t device_bytes = 0;
+    int64_t bsb_bytes = 0;
+    double build_ms = 0.0;
+};
+
+namespace f3s {
+
+// ---- plan kernels (plan_kernels.hip) ------------------------------------
+hipError_t launch_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
+                                int32_t *err, hipStream_t s);
+// Per window: sorted distinct columns into tmp_cols at the window's CSR
+// offset, count into u; windows above the LDS capacity are queued as heavy.
+hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
+                              int32_t N, int32_t T, int32_t *tmp_cols,
+                              int32_t *u, int32_t *heavy, int32_t *n_heavy,
+                              int32_t *err, hipStream_t s);
+// Heavy windows heavy[first .. first+count): column bitmap of N bits each in
+// `bitmap` (zeroed by the caller), then popcount compaction.
+hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
+                                int32_t N, const int32_t *heavy, int32_t count,
+                                uint32_t *bitmap, int32_t words,
+                                int32_t *tmp_cols, int32_t *u, int32_t *err,
+                                hipStream_t s);
+hipError_t launch_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb,
+                                    hipStream_t s);
+// Exclusive scan of n int32 into out[0..n], out[n] = total (in == out ok).
+hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, hipStream_t s);
+hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *col_idx,
+                               int32_t N, int32_t T, const int32_t *tmp_cols,
+                               const int32_t *u, const int32_t *blk_off,
+                               int32_t *cols, uint32_t *mask, hipStream_t s);
+hipError_t launch_count_bits(const uint32_t *mask, int64_t words,
+                             unsigned long long *out, hipStream_t s);
+hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
+                          hipStream_t s);
+hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,
+                          hipStream_t s);
+// Work list: per window piece count, bucket key, split flags.
+hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece,
+                           int32_t *npieces, int32_t *key, int32_t *split_pieces,
+                           int32_t *split_one, hipStream_t s);
+hipError_t launch_bin_hist(const int32_t *npieces, const int32_t *key, int32_t T,
+                           int32_t piece, int32_t chunk, int32_t nchunks,
+                           int32_t *hist, hipStream_t s);
+hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
+                              const int32_t *npieces, const int32_t *key,
+                              const int32_t *slot_base, const int32_t *split_idx,
+                              int32_t T, int32_t piece, int32_t chunk,
+                              int32_t nchunks, int32_t *offs, WorkItem *items,
+                              int32_t *merges, hipStream_t s);
+
+// Sets *err when a finished plan is internally inconsistent.
+hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s);
+
+// ---- fused operator (fused3s.hip) ---------------------------------------
+hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
+                        const void *V, void *O, int32_t d, float scale_log2,
+                        hipStream_t s);
+
+}  // namespace f3s

@@ -1,0 +1,314 @@
+// Fused 3S kernel for CDNA4 (gfx950): Algorithm 1 of Fused3S with the
+// tensor-core tiling re-derived for 64-wide wavefronts and the
+// v_mfma_f32_16x16x32_f16 matrix instruction.
+//
+// One wavefront owns one work item (a 16-row window, or a piece of one) and
+// walks its 16x16 blocks two at a time (32 compacted columns = the K depth of
+// one MFMA for the value product).  Per block pair:
+//
+//   scores   S^T = K_hat * Q_i^T     (A = gathered K rows, straight from HBM
+//                                     into VGPRs; B = the window's Q rows,
+//                                     held in VGPRs for the whole item)
+//            With S^T as the product, MFMA's accumulator layout gives every
+//            lane ONE query row (lane % 16) and 4 neighbours per block, so
+//            the row softmax needs only a 4-lane reduction and the fp16
+//            probabilities already sit in the B-operand layout of the next
+//            product: no shuffle of P at all.
+//   mask     bitmap bit off -> -inf (Algorithm 1: "apply bitmap")
+//   softmax  online, base 2, fp32 (Section 3.5): running max m, running
+//            lane-partial sum l, rescale factor alpha = 2^(m_old - m_new)
+//   P        fp32 -> fp16 with round-to-nearest-even; the SAME rounded values
+//            are summed into l, so the effective probabilities of a row sum
+//            to one
+//   values   O_i^T += V_hat^T * P^T  (A = gathered V rows staged row-major in
+//            LDS and read transposed; B = P from registers; the accumulator
+//            lane layout again has lane % 16 = query row, so the alpha
+//            rescale is a per-lane multiply)
+//
+// The gather order within a row (the reduction index of the score product)
+// is permuted so each lane reads 16 contiguous bytes per load and the four
+// lanes of a row cover 64 contiguous bytes: any consistent permutation of the
+// reduction index leaves Q K^T unchanged (the register remapping of
+// Section 3.4).  The loads of the next block pair are issued before the
+// softmax and value product of the current pair (one pair in flight).
+//
+// Scores and probabilities never leave registers; only O (fp32) and, for
+// split windows, the (m, l, unnormalised O) partials are written.
+#include "f3s_internal.h"
+
+namespace f3s {
+namespace {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ h8 load16(const _Float16 *p)
+{
+    return *reinterpret_cast<const h8 *>(p);
+}
+
+// Orders this wave's LDS accesses (one wave per workgroup).
+__device__ __forceinline__ void wave_lds_fence()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <int D>
+__global__ __launch_bounds__(64) void k_fused3s(
+    const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
+    const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
+    const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
+    float *__restrict__ O, float *__restrict__ part_o,
+    float *__restrict__ part_ml, int32_t N, float sl2)
+{
+    constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
+    constexpr int NT = D / 16;  // 16-wide output tiles of the value product
+    constexpr int LS = D + 4;   // LDS row stride (halves) of staged V rows
+    __shared__ __attribute__((aligned(16))) _Float16 vs[32 * LS];
+
+    const int lane = threadIdx.x;
+    const int i = lane & 15;  // query row (accumulators) / operand row index
+    const int g = lane >> 4;  // lane group: selects the reduction slots
+    const WorkItem it = items[blockIdx.x];
+    const int row = it.window * kWindowRows + i;
+    const int b0 = it.blk_begin, b1 = it.blk_end;
+
+    // Q_i: lane (i, g) holds Q[row][32c + 8g .. +7] for each chunk c.  Pad
+    // rows (>= N) of the last window read row N-1: their results are never
+    // written and rows do not interact, so any finite values do.
+    h8 q[NC];
+    {
+        const _Float16 *qp = Q + (int64_t)min(row, N - 1) * D + 8 * g;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) q[c] = load16(qp + 32 * c);
+    }
+
+    f4 o[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) o[t] = f4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -__builtin_inff();
+    float l_run = 0.f;
+
+    // Pipeline state: columns and operands of the pair being loaded.  All
+    // loads are unconditional (no divergent branches, so the wait counters
+    // can keep the next pair in flight): a padding slot (column -1) or the
+    // absent second block of an odd tail gathers the block's first column
+    // instead, whose bitmap bit is clear, so its probability is exactly 0
+    // and it adds 0 * (finite V) = 0.
+    h8 ka[NC], kb[NC], va[NC], vb[NC];
+    uint32_t mwa = 0, mwb = 0;
+    int na = 0, nb = 0;  // raw columns (-1 = padding) of the next pair
+
+    // Raw column ids of pair (b, b+1); clamped block index so the reads stay
+    // inside this item even past its end (those values are never used).
+    auto load_cols = [&](int b) {
+        na = cols[(int64_t)kBlockCols * min(b, b1 - 1) + i];
+        nb = cols[(int64_t)kBlockCols * min(b + 1, b1 - 1) + i];
+    };
+    // Issue the K, V and bitmap loads of pair (b, b+1) from na/nb.  Lane 0
+    // holds slot 0 of a block, which is never padding; the wave is fully
+    // active here, so readfirstlane returns lane 0's column.
+    auto load_pair = [&](int b) {
+        const int fa = __builtin_amdgcn_readfirstlane(na);
+        const int fb = __builtin_amdgcn_readfirstlane(nb);
+        const int ca = na < 0 ? fa : na;
+        const int cb = b + 1 < b1 ? (nb < 0 ? fb : nb) : ca;
+        const _Float16 *kpa = K + (int64_t)ca * D + 8 * g;
+        const _Float16 *kpb = K + (int64_t)cb * D + 8 * g;
+        const _Float16 *vpa = V + (int64_t)ca * D + 8 * g;
+        const _Float16 *vpb = V + (int64_t)cb * D + 8 * g;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            ka[c] = load16(kpa + 32 * c);
+            kb[c] = load16(kpb + 32 * c);
+        }
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            va[c] = load16(vpa + 32 * c);
+            vb[c] = load16(vpb + 32 * c);
+        }
+        mwa = mask[(int64_t)kMaskWords * b + (lane >> 3)];
+        mwb = mask[(int64_t)kMaskWords * min(b + 1, b1 - 1) + (lane >> 3)];
+    };
+
+    const int nib_shift = 4 * (lane & 7);
+    // One block pair: scores, mask, online softmax, value product.  With
+    // `prefetch`, the loads of the pair after it are issued as soon as this
+    // pair's operand registers are consumed.
+    auto step = [&](int b, bool prefetch) {
+        // ---- scores of the two blocks (S^T: lane = row i, nbrs 4g+r) ----
+        f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            s0 = mfma16x16x32(ka[c], q[c], s0);
+            s1 = mfma16x16x32(kb[c], q[c], s1);
+        }
+        // ---- stage this pair's V rows in LDS (row-major, slot = nbr) ----
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            *reinterpret_cast<h8 *>(&vs[i * LS + 32 * c + 8 * g]) = va[c];
+            *reinterpret_cast<h8 *>(&vs[(16 + i) * LS + 32 * c + 8 * g]) = vb[c];
+        }
+        const uint32_t nib0 = (mwa >> nib_shift) & 15u;
+        // (an odd tail's absent second block re-read block b: mask it off)
+        const uint32_t nib1 = b + 1 < b1 ? (mwb >> nib_shift) & 15u : 0u;
+        // ---- issue the next pair's loads (registers are free now) ----
+        if (prefetch) {
+            load_pair(b + 2);
+            load_cols(b + 4);
+        }
+        // ---- mask + online softmax (base 2) ----
+        float x[8];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            x[r] = (nib0 >> r) & 1u ? s0[r] * sl2 : -__builtin_inff();
+            x[4 + r] = (nib1 >> r) & 1u ? s1[r] * sl2 : -__builtin_inff();
+        }
+        float mloc = x[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mloc = fmaxf(mloc, x[e]);
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float m_new = fmaxf(m_run, mloc);
+        const float m_ref = m_new == -__builtin_inff() ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+        h8 p;
+        float psum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const _Float16 ph = (_Float16)__builtin_amdgcn_exp2f(x[e] - m_ref);
+            p[e] = ph;
+            psum += (float)ph;
+        }
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) o[t] *= alpha;
+        wave_lds_fence();
+        // ---- value product: A[m][slot] = V_hat[slot][16t + m] ----
+        // slot order of lane group g: 4g..4g+3 (block 0), 16+4g..+3 (block 1)
+        const _Float16 *va0 = vs + (4 * g) * LS + i;
+        const _Float16 *vb0 = vs + (16 + 4 * g) * LS + i;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            h8 a;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                a[e] = va0[e * LS + 16 * t];
+                a[4 + e] = vb0[e * LS + 16 * t];
+            }
+            o[t] = mfma16x16x32(a, p, o[t]);
+        }
+        wave_lds_fence();
+    };
+
+    if (b0 < b1) {
+        load_cols(b0);
+        load_pair(b0);
+        load_cols(b0 + 2);
+        int b = b0;
+        for (; b + 2 < b1; b += 2) step(b, true);
+        step(b, false);
+    }
+
+    // ---- finalise: full row sums, normalise, write (Algorithm 1 end) ----
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (it.slot < 0) {
+        if (row < N) {
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            float *op = O + (int64_t)row * D + 4 * g;
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                *reinterpret_cast<f4 *>(op + 16 * t) = o[t] * inv;
+        }
+    } else {
+        float *op = part_o + (int64_t)it.slot * kWindowRows * D + i * D + 4 * g;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) *reinterpret_cast<f4 *>(op + 16 * t) = o[t];
+        if (g == 0) {
+            part_ml[(int64_t)it.slot * 32 + i] = m_run;
+            part_ml[(int64_t)it.slot * 32 + 16 + i] = l_tot;
+        }
+    }
+}
+
+// Combines the pieces of one split window (fixed piece order, so the result
+// is deterministic): m = max m_p, l = sum 2^(m_p - m) l_p,
+// O = sum 2^(m_p - m) O_p / l.
+template <int D>
+__global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merges,
+                                               const float *__restrict__ part_o,
+                                               const float *__restrict__ part_ml,
+                                               float *__restrict__ O, int32_t N)
+{
+    const int s = blockIdx.x;
+    const int w = merges[3 * s], first = merges[3 * s + 1], np = merges[3 * s + 2];
+    for (int e = threadIdx.x; e < kWindowRows * D; e += blockDim.x) {
+        const int r = e / D, col = e % D;
+        const int row = w * kWindowRows + r;
+        if (row >= N) continue;
+        float m = -__builtin_inff();
+        for (int k = 0; k < np; ++k) m = fmaxf(m, part_ml[(int64_t)(first + k) * 32 + r]);
+        float out = 0.f;
+        if (m != -__builtin_inff()) {
+            float l = 0.f, acc = 0.f;
+            for (int k = 0; k < np; ++k) {
+                const int64_t sl = first + k;
+                const float sc = __builtin_amdgcn_exp2f(part_ml[sl * 32 + r] - m);
+                l += sc * part_ml[sl * 32 + 16 + r];
+                acc += sc * part_o[sl * kWindowRows * D + r * D + col];
+            }
+            out = l > 0.f ? acc / l : 0.f;
+        }
+        O[(int64_t)row * D + col] = out;
+    }
+}
+
+template <int D>
+hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
+                    const void *V, void *O, float sl2, hipStream_t s)
+{
+    if (p.n_items > 0) {
+        k_fused3s<D><<<p.n_items, 64, 0, s>>>(
+            p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
+            static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V),
+            static_cast<float *>(O), p.part_o, p.part_ml, p.N, sl2);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (p.n_split > 0) {
+        k_merge<D><<<p.n_split, 256, 0, s>>>(p.merges, p.part_o, p.part_ml,
+                                             static_cast<float *>(O), p.N);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
+                        const void *V, void *O, int32_t d, float sl2,
+                        hipStream_t s)
+{
+    switch (d) {
+    case 32: return launch_d<32>(p, Q, K, V, O, sl2, s);
+    case 64: return launch_d<64>(p, Q, K, V, O, sl2, s);
+    case 96: return launch_d<96>(p, Q, K, V, O, sl2, s);
+    case 128: return launch_d<128>(p, Q, K, V, O, sl2, s);
+    case 160: return launch_d<160>(p, Q, K, V, O, sl2, s);
+    case 192: return launch_d<192>(p, Q, K, V, O, sl2, s);
+    case 224: return launch_d<224>(p, Q, K, V, O, sl2, s);
+    case 256: return launch_d<256>(p, Q, K, V, O, sl2, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace f3s

@@ -1,0 +1,68 @@
+"""The C-ABI library loads and exports every function include/f3s.h declares
+(CPU only: no compute call is made)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "f3s.h")
+LIB = os.path.join(ROOT, "paper_2505_08098_amd", "libf3s.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(f3s_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        pytest.fail("libf3s.so is not built (run __graft_entry__.build())")
+    import torch  # noqa: F401  (same load order as the binding)
+    return ctypes.CDLL(LIB)
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("f3s_plan", "f3s_run", "f3s_destroy", "f3s_plan_info",
+              "f3s_plan_export", "f3s_last_error", "f3s_status_string"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_exports_are_c_symbols():
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if " T " in line)
+    for n in declared_functions():
+        assert n in exported, n
+
+
+def test_status_strings_are_host_only(lib):
+    lib.f3s_status_string.restype = ctypes.c_char_p
+    lib.f3s_status_string.argtypes = [ctypes.c_int]
+    assert lib.f3s_status_string(0) == b"F3S_OK"
+    assert lib.f3s_status_string(2) == b"F3S_ERR_INVALID_CSR"
+    assert lib.f3s_status_string(99) == b"F3S_ERR_UNKNOWN"
+    lib.f3s_last_error.restype = ctypes.c_int
+    assert lib.f3s_last_error() == 0
+
+
+def test_null_handles_are_rejected_without_a_device(lib):
+    lib.f3s_destroy.argtypes = [ctypes.c_void_p]
+    lib.f3s_destroy(None)  # no-op
+    lib.f3s_plan_info.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.f3s_plan_info.restype = ctypes.c_int
+    assert lib.f3s_plan_info(None, None) == 1
+    lib.f3s_run.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_float,
+                                                    ctypes.c_void_p]
+    lib.f3s_run.restype = ctypes.c_int
+    assert lib.f3s_run(None, None, None, None, None, 64, 1.0, None) == 1

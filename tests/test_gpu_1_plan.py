@@ -1,0 +1,112 @@
+"""GPU plan (CSR -> BSB layout + work list) against the oracle, bit for bit.
+
+Section 3.1 (layout) and Section 3.2 (reordered work list) define integer
+results; the plan built by the HIP kernels must equal the oracle's exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2505_08098_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _plan(f3s, rp, ci, N):
+    dev = torch.device("cuda:0")
+    return f3s.Plan(torch.from_numpy(np.ascontiguousarray(rp)).to(dev),
+                    torch.from_numpy(np.ascontiguousarray(ci)).to(dev), N)
+
+
+def _check_plan_against_oracle(f3s, oracle, rp, ci, N):
+    print(f"plan check N={N} nnz={int(rp[-1])}", flush=True)
+    plan = _plan(f3s, rp, ci, N)
+    got = plan.export()
+    ref = oracle.bsb(rp, ci, N)
+    info = plan.info
+    assert info["n_windows"] == (N + 15) // 16
+    assert np.array_equal(got["blk_off"], ref["blk_off"])
+    assert np.array_equal(got["cols"], ref["cols"])
+    assert np.array_equal(got["mask"], ref["mask"])
+    assert info["n_blocks"] == int(ref["blk_off"][-1])
+    assert info["n_unique"] == int(ref["u"].sum())
+    assert info["max_blocks"] == (int(ref["nb"].max()) if len(ref["nb"]) else 0)
+    # distinct (row, col) pairs = set bits of all bitmaps
+    assert info["nnz"] == int(np.unpackbits(ref["mask"].view(np.uint8)).sum())
+    items, merges = oracle.worklist(ref["nb"], ref["blk_off"], info["piece_blocks"])
+    assert np.array_equal(got["items"], items)
+    assert np.array_equal(got["merges"], merges)
+    assert info["n_items"] == len(items) and info["n_split"] == len(merges)
+    assert info["n_pieces"] == int((items[:, 3] >= 0).sum())
+    assert info["bsb_bytes"] == 4 * (info["n_windows"] + 1) + 64 * info["n_blocks"] \
+        + 32 * info["n_blocks"]
+    plan.close()
+    return info
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_plan_matches_oracle_on_workloads(gpu, oracle, k):
+    c = W.make_config(k, with_features=False)
+    info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
+    print(k, info, flush=True)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_plan_matches_oracle_on_random_patterns(gpu, oracle, seed):
+    rng = np.random.default_rng(1000 + seed)
+    N = int(rng.integers(1, 300))
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 60), empty_frac=0.2, dup_frac=0.3)
+    _check_plan_against_oracle(gpu, oracle, rp, ci, N)
+
+
+def test_plan_heavy_window_above_lds_capacity(gpu, oracle):
+    """A window with more entries than the LDS sort holds takes the bitmap path."""
+    rng = np.random.default_rng(7)
+    N = 40000
+    rows = [rng.choice(N, size=600, replace=True) if i < 16 else
+            rng.choice(N, size=3, replace=False) for i in range(N)]
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([len(r) for r in rows])
+    ci = np.concatenate(rows).astype(np.int32)
+    info = _check_plan_against_oracle(gpu, oracle, rp, ci, N)
+    assert info["max_blocks"] > 256
+
+
+def test_plan_split_windows(gpu, oracle, monkeypatch):
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
+    c = W.make_config(2, with_features=False)
+    info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
+    assert info["piece_blocks"] == 4 and info["n_split"] > 100
+
+
+def test_plan_empty_and_degenerate(gpu, oracle):
+    # N = 0
+    plan = _plan(gpu, np.zeros(1, dtype=np.int32), np.zeros(0, dtype=np.int32), 0)
+    assert plan.info["n_windows"] == 0 and plan.info["n_items"] == 0
+    plan.close()
+    # all rows empty
+    _check_plan_against_oracle(gpu, oracle, np.zeros(50, dtype=np.int32),
+                               np.zeros(0, dtype=np.int32), 49)
+    # single node with a self loop
+    _check_plan_against_oracle(gpu, oracle, np.array([0, 1], dtype=np.int32),
+                               np.array([0], dtype=np.int32), 1)
+
+
+@pytest.mark.parametrize("rp,ci,N", [
+    ([1, 1], [0], 1),                 # row_ptr[0] != 0
+    ([0, 2, 1], [0, 1], 2),           # decreasing row_ptr
+    ([0, 1, 2], [0, 2], 2),           # column == N
+    ([0, 1, 2], [0, -1], 2),          # negative column
+])
+def test_plan_rejects_malformed_csr(gpu, rp, ci, N):
+    with pytest.raises(gpu.F3SError) as e:
+        _plan(gpu, np.array(rp, dtype=np.int32), np.array(ci, dtype=np.int32), N)
+    assert e.value.code == 2  # F3S_ERR_INVALID_CSR
+
+
+def test_plan_is_deterministic(gpu):
+    c = W.make_config(2, with_features=False)
+    a = _plan(gpu, c["row_ptr"], c["col_idx"], c["N"]).export()
+    b = _plan(gpu, c["row_ptr"], c["col_idx"], c["N"]).export()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k

@@ -1,0 +1,256 @@
+"""Fused 3S on the GPU against the fp64 oracle, element by element.
+
+Tolerance (fixed by the operator's precision scheme, Table 5: fp16 inputs,
+fp32 scores and softmax, probabilities rounded to fp16 before the value
+product, fp32 output): max-abs error <= 5e-3 and relative Frobenius error
+<= 1e-3, no non-finite outputs.  The dominant error is the fp16 rounding of
+the probabilities (unit roundoff 2^-11), which gives a relative Frobenius
+error near 3e-4 on N(0,1) inputs.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2505_08098_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 5e-3
+REL_FRO = 1e-3
+DEV = torch.device("cuda:0")
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _errors(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    diff = got - ref
+    max_abs = float(np.abs(diff).max()) if diff.size else 0.0
+    nref = float(np.linalg.norm(ref))
+    rel = float(np.linalg.norm(diff)) / nref if nref > 0 else float(np.linalg.norm(diff))
+    return max_abs, rel
+
+
+def _assert_parity(got, ref, max_abs=MAX_ABS, rel_fro=REL_FRO):
+    assert np.all(np.isfinite(got)), "non-finite output"
+    ma, rf = _errors(got, ref)
+    print(f"  max_abs={ma:.3e} rel_fro={rf:.3e}", flush=True)
+    assert ma <= max_abs and rf <= rel_fro, (ma, rf)
+    return ma, rf
+
+
+def _run(f3s, rp, ci, N, Q, K, V, scale, plan=None, out=None, stream=None):
+    if plan is None:
+        plan = f3s.Plan(_dev(rp), _dev(ci), N)
+    O = f3s.run(plan, _dev(Q), _dev(K), _dev(V), scale=scale, out=out, stream=stream)
+    torch.cuda.synchronize()
+    return O.cpu().numpy(), plan
+
+
+def _qkv(rng, N, d, scale=1.0):
+    return tuple((scale * rng.standard_normal((N, d))).astype(np.float16) for _ in range(3))
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_workload_parity(gpu, oracle, k):
+    c = W.make_config(k)
+    print(f"workload {k} ({c['name']}) N={c['N']} nnz={int(c['row_ptr'][-1])} d={c['d']}",
+          flush=True)
+    O, plan = _run(gpu, c["row_ptr"], c["col_idx"], c["N"], c["Q"], c["K"], c["V"],
+                   c["scale"])
+    ref = oracle.attention_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                               c["scale"])
+    print(f"  plan {plan.info}", flush=True)
+    _assert_parity(O, ref)
+
+
+@pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
+@pytest.mark.parametrize("N", [1, 17, 200])
+def test_feature_sizes_and_ragged_windows(gpu, oracle, d, N):
+    rng = np.random.default_rng(d * 1000 + N)
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 70), empty_frac=0.1, dup_frac=0.2)
+    Q, K, V = _qkv(rng, N, d)
+    scale = 1 / math.sqrt(d)
+    O, _ = _run(gpu, rp, ci, N, Q, K, V, scale)
+    _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, scale))
+
+
+def test_single_neighbour_rows_are_exact(gpu):
+    rng = np.random.default_rng(1)
+    N, d = 333, 64
+    j = rng.integers(0, N, size=N).astype(np.int32)
+    rp = np.arange(N + 1, dtype=np.int32)
+    Q, K, V = _qkv(rng, N, d, scale=4.0)
+    O, _ = _run(gpu, rp, j, N, Q, K, V, 0.3)
+    assert np.array_equal(O, V[j].astype(np.float32))
+
+
+def test_zero_queries_average_neighbours(gpu, oracle):
+    rng = np.random.default_rng(2)
+    N, d = 500, 128
+    rp, ci = W.random_csr(rng, N, max_deg=90)
+    _, K, V = _qkv(rng, N, d)
+    Q = np.zeros((N, d), dtype=np.float16)
+    O, _ = _run(gpu, rp, ci, N, Q, K, V, 0.1)
+    _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, 0.1), max_abs=1e-5, rel_fro=1e-6)
+
+
+def test_constant_values_are_reproduced(gpu):
+    rng = np.random.default_rng(3)
+    N, d = 400, 64
+    rp, ci = W.random_csr(rng, N, max_deg=50, empty_frac=0.1)
+    Q, K, _ = _qkv(rng, N, d, scale=2.0)
+    V = np.full((N, d), -1.75, dtype=np.float16)
+    O, _ = _run(gpu, rp, ci, N, Q, K, V, 0.25)
+    nonempty = np.diff(rp) > 0
+    # the fp16 probabilities are summed into the normaliser, so they sum to 1
+    # up to fp32 rounding
+    np.testing.assert_allclose(O[nonempty], -1.75, rtol=1e-5)
+    assert np.all(O[~nonempty] == 0)
+
+
+@pytest.mark.parametrize("gap", [30.0, 1000.0])
+def test_dominant_score_and_overflow_safety(gpu, oracle, gap):
+    """One neighbour scores `gap` above the rest; gap = 1000 would overflow a
+    naive softmax (e^89 is the fp32 limit)."""
+    rng = np.random.default_rng(4)
+    N, d = 64, 32
+    rp = np.arange(0, N * N + 1, N, dtype=np.int32)   # dense rows
+    ci = np.tile(np.arange(N, dtype=np.int32), N)
+    Q = np.zeros((N, d), dtype=np.float16)
+    K = np.zeros((N, d), dtype=np.float16)
+    Q[:, 0] = 1.0
+    K[np.arange(N) % 7 == 3, 0] = 1.0   # several equal winners per row
+    V = rng.standard_normal((N, d)).astype(np.float16)
+    O, _ = _run(gpu, rp, ci, N, Q, K, V, gap)
+    _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, gap))
+
+
+def test_repeated_and_unsorted_entries(gpu, oracle):
+    rng = np.random.default_rng(5)
+    N, d = 300, 64
+    rp, ci = W.random_csr(rng, N, max_deg=40, dup_frac=1.0, shuffle=True)
+    Q, K, V = _qkv(rng, N, d)
+    O, _ = _run(gpu, rp, ci, N, Q, K, V, 0.125)
+    _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, 0.125))
+    # the deduplicated, sorted pattern gives the bit-identical result
+    rows = [np.unique(ci[rp[i]:rp[i + 1]]) for i in range(N)]
+    rp2 = np.zeros(N + 1, dtype=np.int32)
+    rp2[1:] = np.cumsum([r.size for r in rows])
+    O2, _ = _run(gpu, rp2, np.concatenate(rows).astype(np.int32), N, Q, K, V, 0.125)
+    assert np.array_equal(O, O2)
+
+
+def test_empty_rows_and_all_empty(gpu):
+    rng = np.random.default_rng(6)
+    N, d = 77, 64
+    rp, ci = W.random_csr(rng, N, max_deg=10, empty_frac=0.6)
+    Q, K, V = _qkv(rng, N, d)
+    O, _ = _run(gpu, rp, ci, N, Q, K, V, 0.5)
+    assert np.all(O[np.diff(rp) == 0] == 0)
+    rp0 = np.zeros(N + 1, dtype=np.int32)
+    O0, _ = _run(gpu, rp0, np.zeros(0, dtype=np.int32), N, Q, K, V, 0.5)
+    assert np.all(O0 == 0)
+
+
+def test_hub_window_above_lds_capacity(gpu, oracle):
+    rng = np.random.default_rng(8)
+    N, d = 30000, 64
+    rows = [rng.choice(N, size=2000, replace=False) if i < 5 else
+            rng.choice(N, size=4, replace=False) for i in range(N)]
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([len(r) for r in rows])
+    ci = np.concatenate(rows).astype(np.int32)
+    Q, K, V = _qkv(rng, N, d)
+    O, plan = _run(gpu, rp, ci, N, Q, K, V, 0.125)
+    assert plan.info["max_blocks"] > 256
+    _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, 0.125))
+
+
+@pytest.mark.parametrize("piece", [2, 4, 16])
+def test_split_windows_merge(gpu, oracle, monkeypatch, piece):
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", str(piece))
+    c = W.make_config(2)
+    O, plan = _run(gpu, c["row_ptr"], c["col_idx"], c["N"], c["Q"], c["K"], c["V"],
+                   c["scale"])
+    assert plan.info["n_split"] > 0
+    ref = oracle.attention_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                               c["scale"])
+    _assert_parity(O, ref)
+
+
+def test_relabelling_equivariance(gpu, oracle):
+    c = W.make_config(4)
+    N = c["N"]
+    rng = np.random.default_rng(9)
+    pi = rng.permutation(N)
+    inv = np.argsort(pi)
+    rp, ci = c["row_ptr"], c["col_idx"]
+    cols = [pi[ci[rp[o]:rp[o + 1]]] for o in inv]
+    rp2 = np.zeros(N + 1, dtype=np.int32)
+    rp2[1:] = np.cumsum([x.size for x in cols])
+    ci2 = np.concatenate(cols).astype(np.int32)
+    O1, _ = _run(gpu, rp, ci, N, c["Q"], c["K"], c["V"], c["scale"])
+    O2, _ = _run(gpu, rp2, ci2, N, c["Q"][inv], c["K"][inv], c["V"][inv], c["scale"])
+    _assert_parity(O2, O1[inv].astype(np.float64))
+
+
+def test_deterministic_and_every_row_written(gpu):
+    c = W.make_config(2)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    Q, K, V = _dev(c["Q"]), _dev(c["K"]), _dev(c["V"])
+    out = torch.full((c["N"], c["d"]), float("nan"), device=DEV)
+    a = gpu.run(plan, Q, K, V, scale=c["scale"], out=out).clone()
+    b = gpu.run(plan, Q, K, V, scale=c["scale"])
+    torch.cuda.synchronize()
+    assert torch.isfinite(a).all()
+    assert torch.equal(a, b)
+
+
+def test_non_default_stream(gpu, oracle):
+    c = W.make_config(1)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    Q, K, V = _dev(c["Q"]), _dev(c["K"]), _dev(c["V"])
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        O = gpu.run(plan, Q, K, V, scale=c["scale"], stream=s)
+    s.synchronize()
+    ref = oracle.attention_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                               c["scale"])
+    _assert_parity(O.cpu().numpy(), ref)
+
+
+def test_aliased_q_k_v(gpu, oracle):
+    """AGNN form (Section 2.1): Q = K = V = H in one buffer."""
+    rng = np.random.default_rng(10)
+    N, d = 1000, 64
+    rp, ci = W.random_csr(rng, N, max_deg=30)
+    H = rng.standard_normal((N, d)).astype(np.float16)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    Hd = _dev(H)
+    O = gpu.run(plan, Hd, Hd, Hd, scale=0.2)
+    torch.cuda.synchronize()
+    _assert_parity(O.cpu().numpy(), oracle.attention_f64(rp, ci, H, H, H, 0.2))
+
+
+def test_run_argument_errors(gpu):
+    c = W.make_config(1)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    Q = _dev(c["Q"])
+    O = torch.empty((c["N"], c["d"]), dtype=torch.float32, device=DEV)
+    s = torch.cuda.current_stream().cuda_stream
+    base = Q.data_ptr()
+    assert gpu.run_raw(plan, base, base, base, O.data_ptr(), 48, 0.1, s) == 3  # d
+    assert gpu.run_raw(plan, base, base, base, O.data_ptr(), 288, 0.1, s) == 3
+    assert gpu.run_raw(plan, base + 2, base, base, O.data_ptr(), 64, 0.1, s) == 1
+    assert gpu.run_raw(plan, 0, base, base, O.data_ptr(), 64, 0.1, s) == 1
+    assert gpu.run_raw(plan, base, base, base, O.data_ptr(), 64, float("inf"), s) == 1
+    # O overlapping an input
+    assert gpu.run_raw(plan, base, base, base, base, 64, 0.1, s) == 1
+    assert gpu.load_library().f3s_last_error() == 1
+    assert gpu.status_string(2) == "F3S_ERR_INVALID_CSR"
