@@ -31,10 +31,16 @@ KERNEL_SOURCES = [os.path.join(HERE, "paper_2505_08098_amd", "csrc", f)
 
 
 def kernel_source_hash():
+    """Hash of the fused kernel's source code with comments and whitespace
+    removed (a comment edit does not invalidate measured counters)."""
+    import re
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update("".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -96,8 +102,11 @@ def main():
     ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
-    ap.add_argument("--cpu-rows", type=int, default=262144,
+    ap.add_argument("--cpu-rows", type=int, default=1 << 30,
                     help="rows of the workload in the oracle baseline sample")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="after timing, run 3 plain device copies of this many MiB "
+                         "(reference dispatches for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -194,6 +203,16 @@ def main():
         },
         "gen_s": round(gen_s, 1),
     }
+    if args.copy_calib_mib > 0:
+        n = args.copy_calib_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calib_bytes"] = n * 4
+        del src, dst
     if not args.no_cpu:
         torch.cuda.synchronize()
         O_host = O.cpu().numpy()

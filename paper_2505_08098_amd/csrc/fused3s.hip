@@ -14,7 +14,7 @@
 //            the row softmax needs only a 4-lane reduction and the fp16
 //            probabilities already sit in the B-operand layout of the next
 //            product: no shuffle of P at all.
-//   mask     bitmap bit off -> -inf (Algorithm 1: "apply bitmap")
+//   mask     bitmap bit clear -> score -inf (the bitmap mask of Algorithm 1)
 //   softmax  online, base 2, fp32 (Section 3.5): running max m, running
 //            lane-partial sum l, rescale factor alpha = 2^(m_old - m_new)
 //   P        fp32 -> fp16 with round-to-nearest-even; the SAME rounded values
@@ -40,7 +40,10 @@ namespace f3s {
 namespace {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s4 lds_s4;
 
 __device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
 {
@@ -50,6 +53,17 @@ __device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
 __device__ __forceinline__ h8 load16(const _Float16 *p)
 {
     return *reinterpret_cast<const h8 *>(p);
+}
+
+// Transposed LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane j of the group returns element k = 0..3 taken from the 8-byte chunk
+// addressed by group lane 4k + j/4, at position j%4 of that chunk.  So if
+// group lane s points at row (R + s/4), columns C + 4(s%4) .. +3 of a
+// row-major fp16 tile, lane j receives rows R..R+3 of column C + j: one
+// column of a 4 x 16 sub-tile, i.e. 4 reduction slots of an MFMA operand.
+__device__ __forceinline__ h4 lds_read_tr(const _Float16 *p)
+{
+    return __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)p));
 }
 
 // Orders this wave's LDS accesses (one wave per workgroup).
@@ -70,7 +84,9 @@ __global__ __launch_bounds__(64) void k_fused3s(
 {
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
-    constexpr int LS = D + 4;   // LDS row stride (halves) of staged V rows
+    // LDS row stride (halves) of staged V rows: D/2 + 8 dwords is 8 times an
+    // odd number, so 8 consecutive rows start in 8 disjoint 8-bank ranges
+    constexpr int LS = D + 16;
     __shared__ __attribute__((aligned(16))) _Float16 vs[32 * LS];
 
     const int lane = threadIdx.x;
@@ -194,16 +210,16 @@ __global__ __launch_bounds__(64) void k_fused3s(
         wave_lds_fence();
         // ---- value product: A[m][slot] = V_hat[slot][16t + m] ----
         // slot order of lane group g: 4g..4g+3 (block 0), 16+4g..+3 (block 1)
-        const _Float16 *va0 = vs + (4 * g) * LS + i;
-        const _Float16 *vb0 = vs + (16 + 4 * g) * LS + i;
+        // -- the neighbours this lane's P values belong to.  Group lane s
+        // addresses row 4g + s/4, columns 16t + 4(s%4).., so the transposed
+        // read hands lane (m = i, g) the column 16t + m of rows 4g..4g+3.
+        const _Float16 *ta = vs + (4 * g + (i >> 2)) * LS + 4 * (i & 3);
+        const _Float16 *tb = ta + 16 * LS;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            h8 a;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                a[e] = va0[e * LS + 16 * t];
-                a[4 + e] = vb0[e * LS + 16 * t];
-            }
+            const h4 lo = lds_read_tr(ta + 16 * t);
+            const h4 hi = lds_read_tr(tb + 16 * t);
+            const h8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             o[t] = mfma16x16x32(a, p, o[t]);
         }
         wave_lds_fence();
