@@ -17,6 +17,8 @@
 //   mask     bitmap bit clear -> score -inf (the bitmap mask of Algorithm 1)
 //   softmax  online, base 2, fp32 (Section 3.5): running max m, running
 //            lane-partial sum l, rescale factor alpha = 2^(m_old - m_new)
+//            applied every pair (a branch around a rarely needed rescale
+//            measured slower: it splits the loop body for the scheduler)
 //   P        fp32 -> fp16 with round-to-nearest-even; the SAME rounded values
 //            are summed into l, so the effective probabilities of a row sum
 //            to one
@@ -74,8 +76,21 @@ __device__ __forceinline__ void wave_lds_fence()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Occupancy target (waves per SIMD) per feature size: the most waves whose
+// registers fit without spilling; more resident waves = more gathers in
+// flight, which is what bounds this kernel.
+template <int D> struct WavesPerSimd { static constexpr int value = 1; };
+template <> struct WavesPerSimd<32> { static constexpr int value = 6; };
+template <> struct WavesPerSimd<64> { static constexpr int value = 4; };
+template <> struct WavesPerSimd<96> { static constexpr int value = 3; };
+template <> struct WavesPerSimd<128> { static constexpr int value = 3; };
+template <> struct WavesPerSimd<160> { static constexpr int value = 2; };
+template <> struct WavesPerSimd<192> { static constexpr int value = 2; };
+template <> struct WavesPerSimd<224> { static constexpr int value = 2; };
+
 template <int D>
-__global__ __launch_bounds__(64) void k_fused3s(
+__global__ __launch_bounds__(64)
+__attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
     const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
@@ -258,7 +273,8 @@ __global__ __launch_bounds__(64) void k_fused3s(
 
 // Combines the pieces of one split window (fixed piece order, so the result
 // is deterministic): m = max m_p, l = sum 2^(m_p - m) l_p,
-// O = sum 2^(m_p - m) O_p / l.
+// O = sum 2^(m_p - m) O_p / l.  16 threads per row, float4 columns; the
+// piece loops are unrolled so a thread keeps several loads in flight.
 template <int D>
 __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merges,
                                                const float *__restrict__ part_o,
@@ -267,24 +283,32 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
 {
     const int s = blockIdx.x;
     const int w = merges[3 * s], first = merges[3 * s + 1], np = merges[3 * s + 2];
-    for (int e = threadIdx.x; e < kWindowRows * D; e += blockDim.x) {
-        const int r = e / D, col = e % D;
-        const int row = w * kWindowRows + r;
-        if (row >= N) continue;
-        float m = -__builtin_inff();
-        for (int k = 0; k < np; ++k) m = fmaxf(m, part_ml[(int64_t)(first + k) * 32 + r]);
-        float out = 0.f;
+    const int r = threadIdx.x >> 4, q = threadIdx.x & 15;
+    const int row = w * kWindowRows + r;
+    if (row >= N) return;
+    const float *ml = part_ml + (int64_t)first * 32;
+    float m = -__builtin_inff();
+#pragma unroll 4
+    for (int k = 0; k < np; ++k) m = fmaxf(m, ml[k * 32 + r]);
+    float l = 0.f;
+    if (m != -__builtin_inff()) {
+#pragma unroll 4
+        for (int k = 0; k < np; ++k)
+            l += __builtin_amdgcn_exp2f(ml[k * 32 + r] - m) * ml[k * 32 + 16 + r];
+    }
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const float *po = part_o + (int64_t)first * kWindowRows * D + r * D;
+    for (int c4 = q; c4 < D / 4; c4 += 16) {
+        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
         if (m != -__builtin_inff()) {
-            float l = 0.f, acc = 0.f;
+#pragma unroll 4
             for (int k = 0; k < np; ++k) {
-                const int64_t sl = first + k;
-                const float sc = __builtin_amdgcn_exp2f(part_ml[sl * 32 + r] - m);
-                l += sc * part_ml[sl * 32 + 16 + r];
-                acc += sc * part_o[sl * kWindowRows * D + r * D + col];
+                const float sc = __builtin_amdgcn_exp2f(ml[k * 32 + r] - m);
+                acc += sc * *reinterpret_cast<const f4 *>(po + (int64_t)k * kWindowRows * D
+                                                          + 4 * c4);
             }
-            out = l > 0.f ? acc / l : 0.f;
         }
-        O[(int64_t)row * D + col] = out;
+        *reinterpret_cast<f4 *>(O + (int64_t)row * D + 4 * c4) = acc * inv;
     }
 }
 
