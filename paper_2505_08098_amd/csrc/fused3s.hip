@@ -6,9 +6,9 @@
 // walks its 16x16 blocks two at a time (32 compacted columns = the K depth of
 // one MFMA for the value product).  Per block pair:
 //
-//   scores   S^T = K_hat * Q_i^T     (A = gathered K rows, straight from HBM
-//                                     into VGPRs; B = the window's Q rows,
-//                                     held in VGPRs for the whole item)
+//   scores   S^T = K_hat * Q_i^T     (A = gathered K rows, read from LDS in
+//                                     the operand layout; B = the window's
+//                                     Q rows, in VGPRs for the whole item)
 //            With S^T as the product, MFMA's accumulator layout gives every
 //            lane ONE query row (lane % 16) and 4 neighbours per block, so
 //            the row softmax needs only a 4-lane reduction and the fp16
@@ -33,6 +33,8 @@
 // reduction index leaves Q K^T unchanged (the register remapping of
 // Section 3.4).  The loads of the next block pair are issued before the
 // softmax and value product of the current pair (one pair in flight).
+// K and V rows are gathered with row-contiguous lanes and staged through
+// LDS (see the pipeline comment in the kernel).
 //
 // Scores and probabilities never leave registers; only O (fp32) and, for
 // split windows, the (m, l, unnormalised O) partials are written.
@@ -55,6 +57,11 @@ __device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
 __device__ __forceinline__ h8 load16(const _Float16 *p)
 {
     return *reinterpret_cast<const h8 *>(p);
+}
+
+__device__ __forceinline__ h8 load16_off(const _Float16 *base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const h8 *>(reinterpret_cast<const char *>(base) + byte_off);
 }
 
 // Transposed LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
@@ -83,12 +90,11 @@ template <int D> struct WavesPerSimd { static constexpr int value = 1; };
 template <> struct WavesPerSimd<32> { static constexpr int value = 6; };
 template <> struct WavesPerSimd<64> { static constexpr int value = 4; };
 template <> struct WavesPerSimd<96> { static constexpr int value = 3; };
-template <> struct WavesPerSimd<128> { static constexpr int value = 3; };
+template <> struct WavesPerSimd<128> { static constexpr int value = 2; };
 template <> struct WavesPerSimd<160> { static constexpr int value = 2; };
-template <> struct WavesPerSimd<192> { static constexpr int value = 2; };
-template <> struct WavesPerSimd<224> { static constexpr int value = 2; };
 
-template <int D>
+// kWide: Q/K/V may exceed 4 GiB, so gathers use 64-bit addresses.
+template <int D, bool kWide>
 __global__ __launch_bounds__(64)
 __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
@@ -99,10 +105,14 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
 {
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
-    // LDS row stride (halves) of staged V rows: D/2 + 8 dwords is 8 times an
-    // odd number, so 8 consecutive rows start in 8 disjoint 8-bank ranges
-    constexpr int LS = D + 16;
-    __shared__ __attribute__((aligned(16))) _Float16 vs[32 * LS];
+    // One LDS tile per wave, used twice per block pair with two row strides
+    // (halves).  K phase: D/2 + 4 dwords = 4 x odd, so the 16 rows read by a
+    // 16-lane pass start in 16 disjoint 4-bank ranges.  V phase: D/2 + 8
+    // dwords = 8 x odd, so the 8 rows of a transposed read start in disjoint
+    // 8-bank ranges.
+    constexpr int LSK = D + 8;
+    constexpr int LSV = D + 16;
+    __shared__ __attribute__((aligned(16))) _Float16 tile[32 * LSV];
 
     const int lane = threadIdx.x;
     const int i = lane & 15;  // query row (accumulators) / operand row index
@@ -127,43 +137,53 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     float m_run = -__builtin_inff();
     float l_run = 0.f;
 
-    // Pipeline state: columns and operands of the pair being loaded.  All
-    // loads are unconditional (no divergent branches, so the wait counters
-    // can keep the next pair in flight): a padding slot (column -1) or the
-    // absent second block of an odd tail gathers the block's first column
-    // instead, whose bitmap bit is clear, so its probability is exactly 0
-    // and it adds 0 * (finite V) = 0.
-    h8 ka[NC], kb[NC], va[NC], vb[NC];
+    // Pipeline state.  The 32 K rows and 32 V rows of a block pair are
+    // gathered "row-contiguous": the pair tile's 16-byte chunks are spread
+    // flat over the lanes (chunk f = lane + 64 j, row f / LPR, chunk f % LPR),
+    // so every 4-lane quad reads 64 contiguous bytes of ONE row; the texture
+    // addresser then spends one cycle per quad instead of four (an MFMA
+    // operand layout puts consecutive lanes on different rows).  The rows go
+    // through LDS: K rows are read back in the MFMA A layout, V rows with
+    // the transposed read.  Loads are unconditional: a padding slot (column
+    // -1) or the absent second block of an odd tail gathers a real column of
+    // the same block, whose bitmap bit is clear, so its probability is
+    // exactly 0 and it adds 0 * (finite V) = 0.
+    constexpr int LPR = D / 8;   // lanes (16-byte chunks) per row
+    constexpr int NI = D / 16;   // chunks per lane per tile
+    h8 kst[NI], vst[NI];         // staged K and V chunks of the pair in flight
     uint32_t mwa = 0, mwb = 0;
-    int na = 0, nb = 0;  // raw columns (-1 = padding) of the next pair
+    int ncol = 0;                // lanes 0..31: raw column of slot `lane` of the next pair
 
-    // Raw column ids of pair (b, b+1); clamped block index so the reads stay
-    // inside this item even past its end (those values are never used).
+    // Raw column ids of pair (b, b+1): lane l (mod 32) takes slot l; block
+    // indices clamped so reads stay inside this item (values past its end
+    // are never used).
     auto load_cols = [&](int b) {
-        na = cols[(int64_t)kBlockCols * min(b, b1 - 1) + i];
-        nb = cols[(int64_t)kBlockCols * min(b + 1, b1 - 1) + i];
+        const int slot = lane & 31;
+        const int blk = slot < 16 ? min(b, b1 - 1) : min(b + 1, b1 - 1);
+        ncol = cols[(int64_t)kBlockCols * blk + (slot & 15)];
     };
-    // Issue the K, V and bitmap loads of pair (b, b+1) from na/nb.  Lane 0
-    // holds slot 0 of a block, which is never padding; the wave is fully
-    // active here, so readfirstlane returns lane 0's column.
+    // Issue the K, V and bitmap loads of pair (b, b+1).  Slots 0 and 16 are
+    // never padding (the first slot of a block); the wave is fully active
+    // here, so readlane sees them.
     auto load_pair = [&](int b) {
-        const int fa = __builtin_amdgcn_readfirstlane(na);
-        const int fb = __builtin_amdgcn_readfirstlane(nb);
-        const int ca = na < 0 ? fa : na;
-        const int cb = b + 1 < b1 ? (nb < 0 ? fb : nb) : ca;
-        const _Float16 *kpa = K + (int64_t)ca * D + 8 * g;
-        const _Float16 *kpb = K + (int64_t)cb * D + 8 * g;
-        const _Float16 *vpa = V + (int64_t)ca * D + 8 * g;
-        const _Float16 *vpb = V + (int64_t)cb * D + 8 * g;
+        const int f0 = __builtin_amdgcn_readlane(ncol, 0);
+        const int f1 = __builtin_amdgcn_readlane(ncol, 16);
+        const int c = ncol < 0 ? ((lane & 16) ? f1 : f0) : ncol;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            ka[c] = load16(kpa + 32 * c);
-            kb[c] = load16(kpb + 32 * c);
-        }
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            va[c] = load16(vpa + 32 * c);
-            vb[c] = load16(vpb + 32 * c);
+        for (int j = 0; j < NI; ++j) {
+            const int f = lane + 64 * j;
+            const int col = __shfl(c, f / LPR);
+            if constexpr (kWide) {
+                const int64_t off = (int64_t)col * D + 8 * (f % LPR);
+                kst[j] = load16(K + off);
+                vst[j] = load16(V + off);
+            } else {
+                // byte offset < 2^32 (checked on the host): the load takes
+                // the uniform base from SGPRs and a 32-bit VGPR offset
+                const uint32_t off = (uint32_t)col * (uint32_t)(2 * D) + 16u * (f % LPR);
+                kst[j] = load16_off(K, off);
+                vst[j] = load16_off(V, off);
+            }
         }
         mwa = mask[(int64_t)kMaskWords * b + (lane >> 3)];
         mwb = mask[(int64_t)kMaskWords * min(b + 1, b1 - 1) + (lane >> 3)];
@@ -172,8 +192,21 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     const int nib_shift = 4 * (lane & 7);
     // One block pair: scores, mask, online softmax, value product.  With
     // `prefetch`, the loads of the pair after it are issued as soon as this
-    // pair's operand registers are consumed.
+    // pair's staging registers are in LDS.
     auto step = [&](int b, bool prefetch) {
+        // ---- K rows -> LDS (stride LSK), read back as MFMA A operands ----
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int f = lane + 64 * j;
+            *reinterpret_cast<h8 *>(&tile[(f / LPR) * LSK + 8 * (f % LPR)]) = kst[j];
+        }
+        wave_lds_fence();
+        h8 ka[NC], kb[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            ka[c] = *reinterpret_cast<const h8 *>(&tile[i * LSK + 32 * c + 8 * g]);
+            kb[c] = *reinterpret_cast<const h8 *>(&tile[(16 + i) * LSK + 32 * c + 8 * g]);
+        }
         // ---- scores of the two blocks (S^T: lane = row i, nbrs 4g+r) ----
         f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -181,16 +214,17 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
             s0 = mfma16x16x32(ka[c], q[c], s0);
             s1 = mfma16x16x32(kb[c], q[c], s1);
         }
-        // ---- stage this pair's V rows in LDS (row-major, slot = nbr) ----
+        wave_lds_fence();
+        // ---- V rows -> the same LDS tile (stride LSV, slot = neighbour) ----
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            *reinterpret_cast<h8 *>(&vs[i * LS + 32 * c + 8 * g]) = va[c];
-            *reinterpret_cast<h8 *>(&vs[(16 + i) * LS + 32 * c + 8 * g]) = vb[c];
+        for (int j = 0; j < NI; ++j) {
+            const int f = lane + 64 * j;
+            *reinterpret_cast<h8 *>(&tile[(f / LPR) * LSV + 8 * (f % LPR)]) = vst[j];
         }
         const uint32_t nib0 = (mwa >> nib_shift) & 15u;
         // (an odd tail's absent second block re-read block b: mask it off)
         const uint32_t nib1 = b + 1 < b1 ? (mwb >> nib_shift) & 15u : 0u;
-        // ---- issue the next pair's loads (registers are free now) ----
+        // ---- issue the next pair's loads (staging registers are free) ----
         if (prefetch) {
             load_pair(b + 2);
             load_cols(b + 4);
@@ -228,8 +262,8 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
         // -- the neighbours this lane's P values belong to.  Group lane s
         // addresses row 4g + s/4, columns 16t + 4(s%4).., so the transposed
         // read hands lane (m = i, g) the column 16t + m of rows 4g..4g+3.
-        const _Float16 *ta = vs + (4 * g + (i >> 2)) * LS + 4 * (i & 3);
-        const _Float16 *tb = ta + 16 * LS;
+        const _Float16 *ta = tile + (4 * g + (i >> 2)) * LSV + 4 * (i & 3);
+        const _Float16 *tb = ta + 16 * LSV;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const h4 lo = lds_read_tr(ta + 16 * t);
@@ -317,7 +351,9 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                     const void *V, void *O, float sl2, hipStream_t s)
 {
     if (p.n_items > 0) {
-        k_fused3s<D><<<p.n_items, 64, 0, s>>>(
+        const bool wide = (uint64_t)p.N * D * 2 > 0xFFFFFFF0ull;
+        auto kern = wide ? k_fused3s<D, true> : k_fused3s<D, false>;
+        kern<<<p.n_items, 64, 0, s>>>(
             p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
             static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V),
             static_cast<float *>(O), p.part_o, p.part_ml, p.N, sl2);
