@@ -44,13 +44,14 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(info, d):
+def algorithmic_bytes(info, d, heads=1):
     """Bytes one launch must move at minimum without cache reuse: Q read and
-    O written once (6*N*d), the K and V rows of every distinct (window,
-    column) pair (4*d per pair), 64 B of column ids + 32 B of bitmap per
-    block, 16 B per work item."""
-    return (6 * info["N"] * d + 4 * d * info["n_unique"] + 96 * info["n_blocks"]
-            + 16 * info["n_items"])
+    O written once (6*N*d per head), the K and V rows of every distinct
+    (window, column) pair (4*d per pair and head), 64 B of column ids + 32 B
+    of bitmap per block, 16 B per work item (plan data counted once: the
+    heads of a window share it)."""
+    return (heads * (6 * info["N"] * d + 4 * d * info["n_unique"])
+            + 96 * info["n_blocks"] + 16 * info["n_items"])
 
 
 def traffic_from_counters(d):
@@ -101,6 +102,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--heads", type=int, default=1,
+                    help="heads sharing the plan (Q, K, V of shape [N, heads, d]; "
+                         "fresh seeded N(0,1) features)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--cpu-rows", type=int, default=1 << 30,
                     help="rows of the workload in the oracle baseline sample")
@@ -123,12 +127,17 @@ def main():
     c = W.make_config(args.workload, seed=args.seed)
     gen_s = time.perf_counter() - t0
     N, d = c["N"], c["d"]
+    H = args.heads
+    if H > 1:
+        rng = np.random.default_rng(np.random.SeedSequence(args.seed).spawn(3)[2])
+        for key in ("Q", "K", "V"):
+            c[key] = rng.standard_normal((N, H, d), dtype=np.float32).astype(np.float16)
     rp = torch.from_numpy(c["row_ptr"]).to(dev)
     ci = torch.from_numpy(c["col_idx"]).to(dev)
     Q = torch.from_numpy(c["Q"]).to(dev)
     K = torch.from_numpy(c["K"]).to(dev)
     V = torch.from_numpy(c["V"]).to(dev)
-    O = torch.empty((N, d), dtype=torch.float32, device=dev)
+    O = torch.empty(tuple(c["Q"].shape), dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
     plan = f3s.Plan(rp, ci, N)
     info = plan.info
@@ -151,12 +160,12 @@ def main():
     per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
     ms = float(per.mean())
 
-    flops_eff = 4.0 * info["nnz"] * d
+    flops_eff = 4.0 * info["nnz"] * d * H
     value = flops_eff / (ms * 1e-3) / 1e9
-    alg_bytes = algorithmic_bytes(info, d)
+    alg_bytes = algorithmic_bytes(info, d, H)
     achieved = alg_bytes / (ms * 1e-3) / 1e9
-    issued = 1024.0 * d * info["n_blocks"]  # MFMA flops incl. zero padding
-    traffic = traffic_from_counters(d)
+    issued = 1024.0 * d * H * info["n_blocks"]  # MFMA flops incl. zero padding
+    traffic = traffic_from_counters(d) if H == 1 else None
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -179,7 +188,8 @@ def main():
                 4: "4096 molecule-like graphs of 15-45 nodes, block-diagonal, d=64",
                 5: "sequence L=32768, window 256 + 64 random keys per query, d=64",
             }[args.workload],
-            "N": N, "nnz": info["nnz"], "d": d, "scale": c["scale"], "seed": args.seed,
+            "N": N, "nnz": info["nnz"], "d": d, "heads": H, "scale": c["scale"],
+            "seed": args.seed,
             "parallelism": "single GPU",
         },
         "ms_p10": round(float(np.percentile(per, 10)), 5),
@@ -198,7 +208,7 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_bytes,
-            "kernel": "k_fused3s<%d>" % d,
+            "kernel": "k_fused3s<%d>" % d + (" x %d heads" % H if H > 1 else ""),
             "mfma_issued_frac": round(issued / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
         },
         "gen_s": round(gen_s, 1),
@@ -213,7 +223,9 @@ def main():
         torch.cuda.synchronize()
         out["copy_calib_bytes"] = n * 4
         del src, dst
-    if not args.no_cpu:
+    if not args.no_cpu and H > 1:
+        out["cpu_baseline"] = None  # the oracle baseline is defined for one head
+    elif not args.no_cpu:
         torch.cuda.synchronize()
         O_host = O.cpu().numpy()
         base, parity = cpu_baseline(c, O_host, args.cpu_rows)

@@ -92,6 +92,19 @@ f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N);
 f3s_status_t f3s_run(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                      void *O, int32_t d, float scale, hipStream_t stream);
 
+/*
+ * Multi-head form: n_heads independent operators that share one pattern A
+ * (the attention layer of a Graph Transformer, Section 2.1 Eq. 4, has one
+ * per head).  Q, K, V are fp16 [N, n_heads, d] row-major (row i holds head h
+ * at elements (i*n_heads + h)*d ...), O is fp32 [N, n_heads, d]; head h of O
+ * is the single-head operator applied to head h of Q, K, V.  Same pointer,
+ * alignment, d, scale and stream rules as f3s_run; n_heads >= 1 and
+ * n_items * n_heads < 2^31.  f3s_run is f3s_run_mh with n_heads = 1.
+ */
+f3s_status_t f3s_run_mh(f3s_plan_t plan, const void *Q, const void *K, const void *V,
+                        void *O, int32_t n_heads, int32_t d, float scale,
+                        hipStream_t stream);
+
 /* Release a plan and all its device memory.  NULL is a no-op. */
 void f3s_destroy(f3s_plan_t plan);
 

@@ -78,6 +78,8 @@ def load_library():
     L.f3s_plan.restype = vp
     L.f3s_run.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp]
     L.f3s_run.restype = ctypes.c_int
+    L.f3s_run_mh.argtypes = [vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp]
+    L.f3s_run_mh.restype = ctypes.c_int
     L.f3s_destroy.argtypes = [vp]
     L.f3s_destroy.restype = None
     L.f3s_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
@@ -176,33 +178,37 @@ class Plan:
 
 
 def run(plan, Q, K, V, scale=None, out=None, stream=None):
-    """O = softmax_rows(mask_A(scale Q K^T)) V through f3s_run.
+    """O = softmax_rows(mask_A(scale Q K^T)) V through f3s_run / f3s_run_mh.
 
-    Q, K, V: fp16 device tensors [N, d]; out: optional fp32 [N, d]; the call is
-    asynchronous on ``stream`` (default: torch's current stream).
+    Q, K, V: fp16 device tensors [N, d] (one head) or [N, H, d] (H heads
+    sharing the plan); out: optional fp32 tensor of the same shape; the call
+    is asynchronous on ``stream`` (default: torch's current stream).
     """
     L = load_library()
+    shape = tuple(Q.shape)
     for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
         _check_device_tensor(t, n, torch.float16)
-        if t.dim() != 2 or t.shape[0] != plan.N:
-            raise ValueError(f"{n} must be [N, d] with N = {plan.N}")
-    d = Q.shape[1]
-    if K.shape[1] != d or V.shape[1] != d:
-        raise ValueError("Q, K, V must share d")
+        if t.dim() not in (2, 3) or t.shape[0] != plan.N:
+            raise ValueError(f"{n} must be [N, d] or [N, H, d] with N = {plan.N}")
+        if tuple(t.shape) != shape:
+            raise ValueError("Q, K, V must share one shape")
+    H = shape[1] if len(shape) == 3 else 1
+    d = shape[-1]
     if out is None:
-        out = torch.empty((plan.N, d), dtype=torch.float32, device=Q.device)
+        out = torch.empty(shape, dtype=torch.float32, device=Q.device)
     else:
         _check_device_tensor(out, "out", torch.float32)
-        if tuple(out.shape) != (plan.N, d):
-            raise ValueError("out must be [N, d]")
+        if tuple(out.shape) != shape:
+            raise ValueError("out must have the shape of Q")
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     if stream is None:
         stream = torch.cuda.current_stream(Q.device)
-    rc = L.f3s_run(plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(),
-                   int(d), float(scale), ctypes.c_void_p(stream.cuda_stream))
+    rc = L.f3s_run_mh(plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(),
+                      out.data_ptr(), int(H), int(d), float(scale),
+                      ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
-        raise F3SError(rc, "f3s_run")
+        raise F3SError(rc, "f3s_run_mh")
     return out
 
 

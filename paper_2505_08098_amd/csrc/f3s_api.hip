@@ -231,7 +231,10 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
                                T, piece, chunk, nchunks, hist, p->items, p->merges, s));
     if (p->n_pieces > 0) {
         HIP_TRY(plan_alloc(p, &p->part_o, (int64_t)p->n_pieces * kWindowRows * kMaxD));
-        HIP_TRY(plan_alloc(p, &p->part_ml, (int64_t)p->n_pieces * 32));
+        // one (m, l) record of 16 + 16 floats per piece and head of a launch
+        // group; a group holds at most kMaxD / 32 heads (nh * d <= kMaxD)
+        HIP_TRY(plan_alloc(p, &p->part_ml,
+                           (int64_t)p->n_pieces * 32 * (kMaxD / 32)));
     }
     // ---- 6. integrity check of the finished plan ------------------------
     HIP_TRY(hipMemset(err, 0, sizeof(int32_t)));
@@ -356,24 +359,35 @@ f3s_status_t f3s_plan_export(f3s_plan_t p, int32_t *blk_off, int32_t *cols,
     return F3S_OK;
 }
 
-f3s_status_t f3s_run(f3s_plan_t p, const void *Q, const void *K, const void *V,
-                     void *O, int32_t d, float scale, hipStream_t stream)
+f3s_status_t f3s_run_mh(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                        void *O, int32_t n_heads, int32_t d, float scale,
+                        hipStream_t stream)
 {
-    if (!p) return fail(F3S_ERR_INVALID_VALUE);
+    if (!p || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
     if (!Q || !K || !V || !O) return fail(F3S_ERR_INVALID_VALUE);
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O))
         return fail(F3S_ERR_INVALID_VALUE);
-    const size_t in_bytes = (size_t)p->N * d * 2, out_bytes = (size_t)p->N * d * 4;
+    if ((uint64_t)p->n_items * (uint64_t)n_heads > 0x7FFFFFFFull)
+        return fail(F3S_ERR_UNSUPPORTED);
+    const size_t elems = (size_t)p->N * (size_t)n_heads * (size_t)d;
+    const size_t in_bytes = elems * 2, out_bytes = elems * 4;
     if (overlaps(O, out_bytes, Q, in_bytes) || overlaps(O, out_bytes, K, in_bytes) ||
         overlaps(O, out_bytes, V, in_bytes))
         return fail(F3S_ERR_INVALID_VALUE);
     // base-2 softmax: 2^(x * scale * log2 e) == e^(x * scale)
     const float sl2 = (float)((double)scale * 1.4426950408889634);
-    f3s_status_t st = from_hip(f3s::launch_fused(*p, Q, K, V, O, d, sl2, stream));
+    f3s_status_t st =
+        from_hip(f3s::launch_fused(*p, Q, K, V, O, n_heads, d, sl2, stream));
     return st == F3S_OK ? F3S_OK : fail(st);
+}
+
+f3s_status_t f3s_run(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                     void *O, int32_t d, float scale, hipStream_t stream)
+{
+    return f3s_run_mh(p, Q, K, V, O, 1, d, scale, stream);
 }
 
 }  // extern "C"

@@ -43,8 +43,10 @@ struct f3s_plan_s {
     uint32_t *mask = nullptr;    // [8 * n_blocks]
     f3s::WorkItem *items = nullptr;  // [n_items]
     int32_t *merges = nullptr;   // [3 * n_split]
+    // Partial results of split windows for one launch group of nh heads
+    // (nh * d <= kMaxD): slot (piece, head) = piece * nh + head.
     float *part_o = nullptr;     // [n_pieces * 16 * kMaxD]
-    float *part_ml = nullptr;    // [n_pieces * 32]: 16 maxima then 16 sums
+    float *part_ml = nullptr;    // [n_pieces * (kMaxD/32) * 32]: 16 maxima, 16 sums
     int64_t device_bytes = 0;
     int64_t bsb_bytes = 0;
     double build_ms = 0.0;
@@ -100,8 +102,9 @@ hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
 hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s);
 
 // ---- fused operator (fused3s.hip) ---------------------------------------
+// H heads of size d; Q, K, V, O rows hold the heads back to back (stride H*d).
 hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
-                        const void *V, void *O, int32_t d, float scale_log2,
-                        hipStream_t s);
+                        const void *V, void *O, int32_t H, int32_t d,
+                        float scale_log2, hipStream_t s);
 
 }  // namespace f3s

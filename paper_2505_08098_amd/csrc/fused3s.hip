@@ -101,7 +101,8 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
     const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
     float *__restrict__ O, float *__restrict__ part_o,
-    float *__restrict__ part_ml, int32_t N, float sl2)
+    float *__restrict__ part_ml, int32_t N, int32_t ld, int32_t h0, int32_t nh,
+    float sl2)
 {
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
@@ -117,7 +118,16 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     const int lane = threadIdx.x;
     const int i = lane & 15;  // query row (accumulators) / operand row index
     const int g = lane >> 4;  // lane group: selects the reduction slots
-    const WorkItem it = items[blockIdx.x];
+    // Workgroups walk the work list item-major, head-minor: the heads of one
+    // window run back to back and share its column lists and bitmaps.
+    const int item = blockIdx.x / nh, hl = blockIdx.x - item * nh;
+    const int head = h0 + hl;
+    const WorkItem it = items[item];
+    // Row r of head h starts at r * ld + h * D (elements) in Q, K, V and O.
+    Q += (int64_t)head * D;
+    K += (int64_t)head * D;
+    V += (int64_t)head * D;
+    O += (int64_t)head * D;
     const int row = it.window * kWindowRows + i;
     const int b0 = it.blk_begin, b1 = it.blk_end;
 
@@ -126,7 +136,7 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     // written and rows do not interact, so any finite values do.
     h8 q[NC];
     {
-        const _Float16 *qp = Q + (int64_t)min(row, N - 1) * D + 8 * g;
+        const _Float16 *qp = Q + (int64_t)min(row, N - 1) * ld + 8 * g;
 #pragma unroll
         for (int c = 0; c < NC; ++c) q[c] = load16(qp + 32 * c);
     }
@@ -174,13 +184,13 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
             const int f = lane + 64 * j;
             const int col = __shfl(c, f / LPR);
             if constexpr (kWide) {
-                const int64_t off = (int64_t)col * D + 8 * (f % LPR);
+                const int64_t off = (int64_t)col * ld + 8 * (f % LPR);
                 kst[j] = load16(K + off);
                 vst[j] = load16(V + off);
             } else {
                 // byte offset < 2^32 (checked on the host): the load takes
                 // the uniform base from SGPRs and a 32-bit VGPR offset
-                const uint32_t off = (uint32_t)col * (uint32_t)(2 * D) + 16u * (f % LPR);
+                const uint32_t off = (uint32_t)col * (uint32_t)(2 * ld) + 16u * (f % LPR);
                 kst[j] = load16_off(K, off);
                 vst[j] = load16_off(V, off);
             }
@@ -289,18 +299,20 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     if (it.slot < 0) {
         if (row < N) {
             const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            float *op = O + (int64_t)row * D + 4 * g;
+            float *op = O + (int64_t)row * ld + 4 * g;
 #pragma unroll
             for (int t = 0; t < NT; ++t)
                 *reinterpret_cast<f4 *>(op + 16 * t) = o[t] * inv;
         }
     } else {
-        float *op = part_o + (int64_t)it.slot * kWindowRows * D + i * D + 4 * g;
+        // partial slot of (piece, head): slot * nh + head offset
+        const int64_t ps = (int64_t)it.slot * nh + hl;
+        float *op = part_o + ps * kWindowRows * D + i * D + 4 * g;
 #pragma unroll
         for (int t = 0; t < NT; ++t) *reinterpret_cast<f4 *>(op + 16 * t) = o[t];
         if (g == 0) {
-            part_ml[(int64_t)it.slot * 32 + i] = m_run;
-            part_ml[(int64_t)it.slot * 32 + 16 + i] = l_tot;
+            part_ml[ps * 32 + i] = m_run;
+            part_ml[ps * 32 + 16 + i] = l_tot;
         }
     }
 }
@@ -313,57 +325,74 @@ template <int D>
 __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merges,
                                                const float *__restrict__ part_o,
                                                const float *__restrict__ part_ml,
-                                               float *__restrict__ O, int32_t N)
+                                               float *__restrict__ O, int32_t N,
+                                               int32_t ld, int32_t h0, int32_t nh)
 {
-    const int s = blockIdx.x;
+    const int s = blockIdx.x / nh, hl = blockIdx.x - (blockIdx.x / nh) * nh;
     const int w = merges[3 * s], first = merges[3 * s + 1], np = merges[3 * s + 2];
     const int r = threadIdx.x >> 4, q = threadIdx.x & 15;
     const int row = w * kWindowRows + r;
     if (row >= N) return;
-    const float *ml = part_ml + (int64_t)first * 32;
+    // partial slot of (piece k, head) = (first + k) * nh + hl
+    const float *ml = part_ml + ((int64_t)first * nh + hl) * 32;
+    const int64_t mstride = (int64_t)nh * 32;
     float m = -__builtin_inff();
 #pragma unroll 4
-    for (int k = 0; k < np; ++k) m = fmaxf(m, ml[k * 32 + r]);
+    for (int k = 0; k < np; ++k) m = fmaxf(m, ml[k * mstride + r]);
     float l = 0.f;
     if (m != -__builtin_inff()) {
 #pragma unroll 4
         for (int k = 0; k < np; ++k)
-            l += __builtin_amdgcn_exp2f(ml[k * 32 + r] - m) * ml[k * 32 + 16 + r];
+            l += __builtin_amdgcn_exp2f(ml[k * mstride + r] - m) * ml[k * mstride + 16 + r];
     }
     const float inv = l > 0.f ? 1.f / l : 0.f;
-    const float *po = part_o + (int64_t)first * kWindowRows * D + r * D;
+    const float *po = part_o + ((int64_t)first * nh + hl) * kWindowRows * D + r * D;
+    const int64_t ostride = (int64_t)nh * kWindowRows * D;
+    float *orow = O + (int64_t)row * ld + (int64_t)(h0 + hl) * D;
     for (int c4 = q; c4 < D / 4; c4 += 16) {
         f4 acc = f4{0.f, 0.f, 0.f, 0.f};
         if (m != -__builtin_inff()) {
 #pragma unroll 4
             for (int k = 0; k < np; ++k) {
-                const float sc = __builtin_amdgcn_exp2f(ml[k * 32 + r] - m);
-                acc += sc * *reinterpret_cast<const f4 *>(po + (int64_t)k * kWindowRows * D
-                                                          + 4 * c4);
+                const float sc = __builtin_amdgcn_exp2f(ml[k * mstride + r] - m);
+                acc += sc * *reinterpret_cast<const f4 *>(po + k * ostride + 4 * c4);
             }
         }
-        *reinterpret_cast<f4 *>(O + (int64_t)row * D + 4 * c4) = acc * inv;
+        *reinterpret_cast<f4 *>(orow + 4 * c4) = acc * inv;
     }
 }
 
+// Heads are launched in groups whose partial results fit the plan's scratch
+// (nh * D <= 256 floats per piece row); without split windows all heads go
+// in one launch.
 template <int D>
 hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
-                    const void *V, void *O, float sl2, hipStream_t s)
+                    const void *V, void *O, int32_t H, float sl2, hipStream_t s)
 {
-    if (p.n_items > 0) {
-        const bool wide = (uint64_t)p.N * D * 2 > 0xFFFFFFF0ull;
-        auto kern = wide ? k_fused3s<D, true> : k_fused3s<D, false>;
-        kern<<<p.n_items, 64, 0, s>>>(
-            p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
-            static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V),
-            static_cast<float *>(O), p.part_o, p.part_ml, p.N, sl2);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if (p.n_split > 0) {
-        k_merge<D><<<p.n_split, 256, 0, s>>>(p.merges, p.part_o, p.part_ml,
-                                             static_cast<float *>(O), p.N);
-        return hipGetLastError();
+    const int32_t ld = H * D;
+    const bool wide = (uint64_t)p.N * ld * 2 > 0xFFFFFFF0ull;
+    auto kern = wide ? k_fused3s<D, true> : k_fused3s<D, false>;
+    const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
+    for (int32_t h0 = 0; h0 < H; h0 += group) {
+        const int32_t nh = H - h0 < group ? H - h0 : group;
+        // the plan's partial buffers hold n_pieces * kMaxD / D head slots
+        if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
+        if (p.n_items > 0) {
+            const uint64_t grid = (uint64_t)p.n_items * nh;
+            if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+            kern<<<(unsigned)grid, 64, 0, s>>>(
+                p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
+                static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V),
+                static_cast<float *>(O), p.part_o, p.part_ml, p.N, ld, h0, nh, sl2);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        if (p.n_split > 0) {
+            k_merge<D><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.part_o, p.part_ml,
+                                                     static_cast<float *>(O), p.N, ld, h0, nh);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
     }
     return hipSuccess;
 }
@@ -371,18 +400,18 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
 }  // namespace
 
 hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
-                        const void *V, void *O, int32_t d, float sl2,
+                        const void *V, void *O, int32_t H, int32_t d, float sl2,
                         hipStream_t s)
 {
     switch (d) {
-    case 32: return launch_d<32>(p, Q, K, V, O, sl2, s);
-    case 64: return launch_d<64>(p, Q, K, V, O, sl2, s);
-    case 96: return launch_d<96>(p, Q, K, V, O, sl2, s);
-    case 128: return launch_d<128>(p, Q, K, V, O, sl2, s);
-    case 160: return launch_d<160>(p, Q, K, V, O, sl2, s);
-    case 192: return launch_d<192>(p, Q, K, V, O, sl2, s);
-    case 224: return launch_d<224>(p, Q, K, V, O, sl2, s);
-    case 256: return launch_d<256>(p, Q, K, V, O, sl2, s);
+    case 32: return launch_d<32>(p, Q, K, V, O, H, sl2, s);
+    case 64: return launch_d<64>(p, Q, K, V, O, H, sl2, s);
+    case 96: return launch_d<96>(p, Q, K, V, O, H, sl2, s);
+    case 128: return launch_d<128>(p, Q, K, V, O, H, sl2, s);
+    case 160: return launch_d<160>(p, Q, K, V, O, H, sl2, s);
+    case 192: return launch_d<192>(p, Q, K, V, O, H, sl2, s);
+    case 224: return launch_d<224>(p, Q, K, V, O, H, sl2, s);
+    case 256: return launch_d<256>(p, Q, K, V, O, H, sl2, s);
     default: return hipErrorInvalidValue;
     }
 }

@@ -254,3 +254,62 @@ def test_run_argument_errors(gpu):
     assert gpu.run_raw(plan, base, base, base, base, 64, 0.1, s) == 1
     assert gpu.load_library().f3s_last_error() == 1
     assert gpu.status_string(2) == "F3S_ERR_INVALID_CSR"
+
+
+@pytest.mark.parametrize("H,d", [(2, 64), (4, 32), (8, 64), (3, 128)])
+def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d):
+    """f3s_run_mh: H heads sharing one plan (Section 2.1, Eq. 4 per head)."""
+    rng = np.random.default_rng(100 + H * d)
+    N = 700
+    rp, ci = W.random_csr(rng, N, max_deg=60, empty_frac=0.05, dup_frac=0.1)
+    Q, K, V = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(3))
+    scale = 1 / math.sqrt(d)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    O = gpu.run(plan, _dev(Q), _dev(K), _dev(V), scale=scale)
+    torch.cuda.synchronize()
+    O = O.cpu().numpy()
+    for h in range(H):
+        ref = oracle.attention_f64(rp, ci, Q[:, h], K[:, h], V[:, h], scale)
+        _assert_parity(O[:, h], ref)
+
+
+@pytest.mark.parametrize("piece", [4, 1000000])
+def test_multi_head_equals_single_head_runs(gpu, monkeypatch, piece):
+    """Head h of the multi-head call is bit-identical to a single-head call on
+    the head's slice, with and without split windows (H * d > 256 also
+    exercises the head groups that bound the partial-result scratch)."""
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", str(piece))
+    c = W.make_config(2, with_features=False)
+    N, H, d = c["N"], 6, 64
+    rng = np.random.default_rng(5)
+    Q, K, V = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(3))
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), N)
+    if piece == 4:
+        assert plan.info["n_split"] > 0
+    O = gpu.run(plan, _dev(Q), _dev(K), _dev(V), scale=0.125)
+    for h in (0, 3, 5):
+        Oh = gpu.run(plan, _dev(np.ascontiguousarray(Q[:, h])), _dev(np.ascontiguousarray(K[:, h])),
+                     _dev(np.ascontiguousarray(V[:, h])), scale=0.125)
+        torch.cuda.synchronize()
+        assert torch.equal(O[:, h], Oh)
+
+
+def test_multi_head_argument_errors(gpu):
+    c = W.make_config(1)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    Q = torch.zeros((c["N"], 2, 64), dtype=torch.float16, device=DEV)
+    O = torch.empty((c["N"], 2, 64), dtype=torch.float32, device=DEV)
+    L = gpu.load_library()
+    s = ctypes_stream()
+    assert L.f3s_run_mh(plan.handle, Q.data_ptr(), Q.data_ptr(), Q.data_ptr(), O.data_ptr(),
+                        0, 64, 0.1, s) == 1
+    assert L.f3s_run_mh(plan.handle, Q.data_ptr(), Q.data_ptr(), Q.data_ptr(), O.data_ptr(),
+                        2, 40, 0.1, s) == 3
+    assert L.f3s_run_mh(plan.handle, Q.data_ptr(), Q.data_ptr(), Q.data_ptr(), O.data_ptr(),
+                        2, 64, 0.1, s) == 0
+    torch.cuda.synchronize()
+
+
+def ctypes_stream():
+    import ctypes
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
