@@ -163,7 +163,7 @@ def bsb(row_ptr, col_idx, N):
                 mask=mask[: 8 * B])
 
 
-def worklist(nb, blk_off, piece):
+def worklist(nb, blk_off, piece, reorder=True):
     """Reordered work list (Section 3.2) with heavy windows split in pieces.
 
     Definition, in the order it is applied:
@@ -177,7 +177,9 @@ def worklist(nb, blk_off, piece):
        piece) and the sort key ``piece``.  Window w gets one merge record
        ``(w, first_slot, np)``.
     3. Items are listed window by window, piece by piece, then stably sorted
-       by key, largest first (the paper's decreasing block count).
+       by key, largest first (the paper's decreasing block count).  With
+       ``reorder=False`` (the ablation without row-window reordering) the
+       listing order is kept.
 
     Returns ``items`` (n x 4 int32: window, first block, end block, slot or
     -1) and ``merges`` (m x 3 int32).
@@ -199,6 +201,6 @@ def worklist(nb, blk_off, piece):
             b = ((k + 1) * pairs) // npieces
             raw.append((piece, (w, b0 + 2 * a, b0 + min(n, 2 * b), slot)))
             slot += 1
-    ordered = sorted(raw, key=lambda kv: -kv[0])  # sorted() is stable
+    ordered = sorted(raw, key=lambda kv: -kv[0]) if reorder else raw  # stable
     items = np.array([it for _, it in ordered], dtype=np.int32).reshape(-1, 4)
     return items, np.array(merges, dtype=np.int32).reshape(-1, 3)

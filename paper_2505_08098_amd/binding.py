@@ -31,13 +31,13 @@ class PlanInfo(ctypes.Structure):
         ("n_unique", ctypes.c_int64), ("n_blocks", ctypes.c_int64),
         ("max_blocks", ctypes.c_int32), ("piece_blocks", ctypes.c_int32),
         ("n_items", ctypes.c_int32), ("n_split", ctypes.c_int32),
-        ("n_pieces", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("n_pieces", ctypes.c_int32), ("flags", ctypes.c_int32),
         ("bsb_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
         ("build_ms", ctypes.c_double),
     ]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 _LIB = None

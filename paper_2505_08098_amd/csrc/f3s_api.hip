@@ -204,7 +204,10 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(tmp.alloc(&key, T));
     HIP_TRY(tmp.alloc(&split_pieces, (int64_t)T + 1));
     HIP_TRY(tmp.alloc(&split_one, (int64_t)T + 1));
-    HIP_TRY(launch_bin_keys(nb, T, piece, npieces, key, split_pieces, split_one, s));
+    const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
+    p->flags = reorder ? 0 : 1;
+    HIP_TRY(launch_bin_keys(nb, T, piece, reorder, npieces, key, split_pieces,
+                            split_one, s));
     HIP_TRY(launch_scan(split_pieces, split_pieces, T, s));  // -> slot base
     HIP_TRY(launch_scan(split_one, split_one, T, s));        // -> split index
     int32_t tot[2];
@@ -330,6 +333,7 @@ f3s_status_t f3s_plan_info(f3s_plan_t p, f3s_plan_info_t *out)
     out->n_items = p->n_items;
     out->n_split = p->n_split;
     out->n_pieces = p->n_pieces;
+    out->flags = p->flags;
     out->bsb_bytes = p->bsb_bytes;
     out->device_bytes = p->device_bytes;
     out->build_ms = p->build_ms;

@@ -38,6 +38,7 @@ struct f3s_plan_s {
     int32_t n_items = 0;
     int32_t n_split = 0;
     int32_t n_pieces = 0;
+    int32_t flags = 0;           // bit 0: work list in window order
     int32_t *blk_off = nullptr;  // [T + 1]
     int32_t *cols = nullptr;     // [16 * n_blocks]
     uint32_t *mask = nullptr;    // [8 * n_blocks]
@@ -85,7 +86,8 @@ hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
 hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,
                           hipStream_t s);
 // Work list: per window piece count, bucket key, split flags.
-hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece,
+// reorder == false gives every window the same key (window order kept).
+hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
                            int32_t *npieces, int32_t *key, int32_t *split_pieces,
                            int32_t *split_one, hipStream_t s);
 hipError_t launch_bin_hist(const int32_t *npieces, const int32_t *key, int32_t T,

@@ -263,7 +263,7 @@ __global__ void k_max_i32(const int32_t *in, int32_t n, int32_t *out)
     atomicMax(out, acc);
 }
 
-__global__ void k_bin_keys(const int32_t *nb, int32_t T, int32_t piece,
+__global__ void k_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
                            int32_t *npieces, int32_t *key, int32_t *split_pieces,
                            int32_t *split_one)
 {
@@ -273,7 +273,7 @@ __global__ void k_bin_keys(const int32_t *nb, int32_t T, int32_t piece,
     const bool split = n > piece;
     const int np = split ? (n + piece - 1) / piece : 1;
     npieces[w] = np;
-    key[w] = split ? piece : n;
+    key[w] = reorder ? (split ? piece : n) : 0;
     split_pieces[w] = split ? np : 0;
     split_one[w] = split ? 1 : 0;
 }
@@ -447,12 +447,12 @@ hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,
     return hipGetLastError();
 }
 
-hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece,
+hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
                            int32_t *npieces, int32_t *key, int32_t *split_pieces,
                            int32_t *split_one, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_bin_keys<<<grid_for(T, 256), 256, 0, s>>>(nb, T, piece, npieces, key,
+    k_bin_keys<<<grid_for(T, 256), 256, 0, s>>>(nb, T, piece, reorder, npieces, key,
                                                split_pieces, split_one);
     return hipGetLastError();
 }

@@ -133,3 +133,13 @@ def test_worklist_properties(oracle, piece):
     # heavy first: keys never increase along the list
     keys = [piece if s >= 0 else b1 - b0 for _, b0, b1, s in items.tolist()]
     assert all(a >= b for a, b in zip(keys, keys[1:]))
+
+
+def test_worklist_without_reordering_keeps_window_order(oracle):
+    nb = np.array([3, 0, 40, 7, 2])
+    blk_off = np.concatenate([[0], np.cumsum(nb)])
+    items, merges = oracle.worklist(nb, blk_off, 16, reorder=False)
+    assert items[:, 0].tolist() == [0, 1, 2, 2, 2, 3, 4]
+    assert merges.tolist() == [[2, 0, 3]]
+    sorted_items, _ = oracle.worklist(nb, blk_off, 16)
+    assert sorted_items[:, 0].tolist() == [2, 2, 2, 3, 0, 4, 1]

@@ -33,7 +33,8 @@ def _check_plan_against_oracle(f3s, oracle, rp, ci, N):
     assert info["max_blocks"] == (int(ref["nb"].max()) if len(ref["nb"]) else 0)
     # distinct (row, col) pairs = set bits of all bitmaps
     assert info["nnz"] == int(np.unpackbits(ref["mask"].view(np.uint8)).sum())
-    items, merges = oracle.worklist(ref["nb"], ref["blk_off"], info["piece_blocks"])
+    items, merges = oracle.worklist(ref["nb"], ref["blk_off"], info["piece_blocks"],
+                                    reorder=not (info["flags"] & 1))
     assert np.array_equal(got["items"], items)
     assert np.array_equal(got["merges"], merges)
     assert info["n_items"] == len(items) and info["n_split"] == len(merges)
@@ -110,3 +111,11 @@ def test_plan_is_deterministic(gpu):
     b = _plan(gpu, c["row_ptr"], c["col_idx"], c["N"]).export()
     for k in a:
         assert np.array_equal(a[k], b[k]), k
+
+
+def test_plan_without_reordering(gpu, oracle, monkeypatch):
+    """Ablation switch: the work list keeps window order (Section 3.2 off)."""
+    monkeypatch.setenv("F3S_NO_REORDER", "1")
+    c = W.make_config(2, with_features=False)
+    info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
+    assert info["flags"] & 1
