@@ -14,6 +14,9 @@ Functions and the passages they follow:
 * :func:`bsb` -- Section 3.1, the Binary Sparse Block construction (row
   windows of 16 rows, all-zero columns removed, 16x16 blocks, one bitmap per
   block; Table 3 gives its footprint).
+* :func:`attention_bwd_f64` -- gradients of the operator (the backward pass
+  the paper names as the next step): softmax Jacobian applied to dO V^T on
+  the pattern, then the two products back through K and Q, and P^T dO.
 * :func:`worklist` -- Section 3.2, row-window reordering (windows in
   decreasing order of block count), extended by splitting windows with more
   than ``piece`` blocks into pieces (the future-work remedy of Section 4.2).
@@ -47,6 +50,12 @@ def lib():
         L.oracle_check_csr.restype = ctypes.c_int
         L.oracle_3s_f64.argtypes = [i32, vp, vp, i32, vp, vp, vp, dbl, vp, vp, vp, i32]
         L.oracle_3s_f64.restype = ctypes.c_int
+        L.oracle_3s_f64d.argtypes = [i32, vp, vp, i32, vp, vp, vp, dbl, vp, vp, vp, i32]
+        L.oracle_3s_f64d.restype = ctypes.c_int
+        L.oracle_3s_bwd_f64.argtypes = [i32, vp, vp, i32, vp, vp, vp, vp, dbl, vp, vp, vp]
+        L.oracle_3s_bwd_f64.restype = ctypes.c_int
+        L.oracle_3s_bwd_f64d.argtypes = [i32, vp, vp, i32, vp, vp, vp, vp, dbl, vp, vp, vp]
+        L.oracle_3s_bwd_f64d.restype = ctypes.c_int
         L.oracle_3s_f64_rows.argtypes = [i32, vp, vp, i32, vp, vp, vp, dbl, i32, i32, vp, i32]
         L.oracle_3s_f64_rows.restype = ctypes.c_int
         L.oracle_num_windows.argtypes = [i32]
@@ -117,6 +126,43 @@ def attention_f64(row_ptr, col_idx, Q, K, V, scale, want_lse=False,
     if want_p:
         out.append(P[: int(rp[-1])])
     return out[0] if len(out) == 1 else tuple(out)
+
+
+def attention_f64_exact(row_ptr, col_idx, Q, K, V, scale, want_lse=False):
+    """The same operator on float64 inputs (used by the finite-difference
+    pins of the gradients)."""
+    rp, ci = _csr(row_ptr, col_idx)
+    q, k, v = (np.ascontiguousarray(x, dtype=np.float64) for x in (Q, K, V))
+    N, d = q.shape
+    O = np.empty((N, d), dtype=np.float64)
+    lse = np.empty(N, dtype=np.float64) if want_lse else None
+    rc = lib().oracle_3s_f64d(N, _ptr(rp), _ptr(ci), d, _ptr(q), _ptr(k), _ptr(v),
+                              float(scale), _ptr(O),
+                              _ptr(lse) if lse is not None else None, None, 0)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the input (code {rc})")
+    return (O, lse) if want_lse else O
+
+
+def attention_bwd_f64(row_ptr, col_idx, Q, K, V, G, scale):
+    """Gradients (dQ, dK, dV) of sum(O * G) for O = the 3S operator, fp64.
+
+    Q, K, V, G are N x d arrays: binary16 (exactly widened) or float64.
+    """
+    rp, ci = _csr(row_ptr, col_idx)
+    if np.asarray(Q).dtype == np.float64:
+        arrs = [np.ascontiguousarray(x, dtype=np.float64) for x in (Q, K, V, G)]
+        fn = lib().oracle_3s_bwd_f64d
+    else:
+        arrs = [_half_bits(x) for x in (Q, K, V, G)]
+        fn = lib().oracle_3s_bwd_f64
+    N, d = arrs[0].shape
+    outs = [np.empty((N, d), dtype=np.float64) for _ in range(3)]
+    rc = fn(N, _ptr(rp), _ptr(ci), d, *[_ptr(a) for a in arrs], float(scale),
+            *[_ptr(o) for o in outs])
+    if rc != 0:
+        raise ValueError(f"oracle rejected the input (code {rc})")
+    return tuple(outs)
 
 
 def attention_rows_f64(row_ptr, col_idx, Q, K, V, scale, r0, r1, threads=0):

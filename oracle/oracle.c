@@ -91,9 +91,10 @@ int oracle_check_csr(int32_t N, const int32_t *row_ptr, const int32_t *col_idx)
 }
 
 /*
- * The 3S operator, fp64 throughout (inputs widened exactly from binary16).
+ * The 3S operator, fp64 throughout, on fp64 inputs (the binary16 entry point
+ * below widens its inputs exactly and calls this one).
  *
- * Q, K, V: N x d row-major binary16 bit patterns.  O: N x d fp64 output.
+ * Q, K, V: N x d row-major.  O: N x d output.
  * lse (may be NULL): per row m + log(l), -inf for an empty row.
  * P   (may be NULL): per CSR entry k, the probability of its column, written
  *     at the FIRST occurrence of that column in the row; 0 at repeats.
@@ -107,15 +108,13 @@ int oracle_check_csr(int32_t N, const int32_t *row_ptr, const int32_t *col_idx)
  *   4. e_j   = exp(s_j - m),  l = sum_j e_j,  P_ij = e_j / l
  *   5. O[i,:] = sum_j P_ij V[j,:]                     (SpMM)
  */
-int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
-                  int32_t d, const uint16_t *Q, const uint16_t *K,
-                  const uint16_t *V, double scale, double *O, double *lse,
-                  double *P, int32_t nthreads)
+int oracle_3s_f64d(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
+                   int32_t d, const double *Q, const double *K, const double *V,
+                   double scale, double *O, double *lse, double *P, int32_t nthreads)
 {
     int rc = oracle_check_csr(N, row_ptr, col_idx);
     if (rc) return rc;
     if (d <= 0) return -5;
-    fill_half_table();
 #ifdef _OPENMP
     if (nthreads > 0) omp_set_num_threads(nthreads);
 #else
@@ -145,11 +144,10 @@ int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
             if (k == 0 || nb[k] != nb[k - 1]) nb[u++] = nb[k];
         /* 2. scores */
         for (int64_t a = 0; a < u; ++a) {
-            const uint16_t *q = Q + (int64_t)i * d;
-            const uint16_t *kr = K + (int64_t)nb[a] * d;
+            const double *q = Q + (int64_t)i * d;
+            const double *kr = K + (int64_t)nb[a] * d;
             double acc = 0.0;
-            for (int32_t k = 0; k < d; ++k)
-                acc += H2D(q[k]) * H2D(kr[k]);
+            for (int32_t k = 0; k < d; ++k) acc += q[k] * kr[k];
             s[a] = scale * acc;
         }
         /* 3. row max */
@@ -165,8 +163,8 @@ int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
         /* 5. weighted sum of neighbour V rows */
         for (int64_t a = 0; a < u; ++a) {
             double p = s[a] / l;
-            const uint16_t *vr = V + (int64_t)nb[a] * d;
-            for (int32_t k = 0; k < d; ++k) o[k] += p * H2D(vr[k]);
+            const double *vr = V + (int64_t)nb[a] * d;
+            for (int32_t k = 0; k < d; ++k) o[k] += p * vr[k];
             if (P) {
                 for (int64_t k = beg; k < end; ++k)
                     if (col_idx[k] == nb[a]) { P[k] = p; break; }
@@ -177,6 +175,137 @@ int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
         free(s);
     }
     return bad ? -6 : 0;
+}
+
+/* N x d binary16 bit patterns -> fp64 (exact). */
+static double *widen(const uint16_t *h, int64_t count)
+{
+    double *out = (double *)malloc(sizeof(double) * (count > 0 ? count : 1));
+    if (!out) return NULL;
+    for (int64_t k = 0; k < count; ++k) out[k] = H2D(h[k]);
+    return out;
+}
+
+/* The 3S operator on binary16 inputs (see oracle_3s_f64d). */
+int oracle_3s_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
+                  int32_t d, const uint16_t *Q, const uint16_t *K,
+                  const uint16_t *V, double scale, double *O, double *lse,
+                  double *P, int32_t nthreads)
+{
+    if (d <= 0 || N < 0) return -5;
+    fill_half_table();
+    int64_t count = (int64_t)N * d;
+    double *q = widen(Q, count), *k = widen(K, count), *v = widen(V, count);
+    int rc = -6;
+    if (q && k && v)
+        rc = oracle_3s_f64d(N, row_ptr, col_idx, d, q, k, v, scale, O, lse, P, nthreads);
+    free(q);
+    free(k);
+    free(v);
+    return rc;
+}
+
+/*
+ * Gradients of the 3S operator (the backward pass the paper names as the
+ * next step), fp64, on fp64 inputs.  With P_ij the probabilities of the
+ * forward (masked, Eq. 1 / Eq. 7) and G = dL/dO:
+ *   dV_j   = sum_i P_ij G_i                      (i over rows holding column j)
+ *   dP_ij  = G_i . V_j
+ *   D_i    = sum_j P_ij dP_ij  (= G_i . O_i)
+ *   dS_ij  = P_ij (dP_ij - D_i)                  (softmax Jacobian)
+ *   dQ_i   = scale * sum_j dS_ij K_j
+ *   dK_j   = scale * sum_i dS_ij Q_i
+ * Rows are visited in order and the column sums are accumulated in that
+ * order (sequential; no threads).  Empty rows contribute nothing.
+ */
+int oracle_3s_bwd_f64d(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
+                       int32_t d, const double *Q, const double *K, const double *V,
+                       const double *G, double scale, double *dQ, double *dK,
+                       double *dV)
+{
+    int rc = oracle_check_csr(N, row_ptr, col_idx);
+    if (rc) return rc;
+    if (d <= 0) return -5;
+    int64_t count = (int64_t)N * d;
+    for (int64_t k = 0; k < count; ++k) dQ[k] = dK[k] = dV[k] = 0.0;
+    int64_t maxn = 0;
+    for (int32_t i = 0; i < N; ++i)
+        if (row_ptr[i + 1] - row_ptr[i] > maxn) maxn = row_ptr[i + 1] - row_ptr[i];
+    int32_t *nb = (int32_t *)malloc(sizeof(int32_t) * (maxn > 0 ? maxn : 1));
+    double *p = (double *)malloc(sizeof(double) * (maxn > 0 ? maxn : 1));
+    double *dp = (double *)malloc(sizeof(double) * (maxn > 0 ? maxn : 1));
+    if (!nb || !p || !dp) { free(nb); free(p); free(dp); return -6; }
+    for (int32_t i = 0; i < N; ++i) {
+        int64_t beg = row_ptr[i], n = row_ptr[i + 1] - beg;
+        if (n == 0) continue;
+        memcpy(nb, col_idx + beg, sizeof(int32_t) * n);
+        qsort(nb, n, sizeof(int32_t), cmp_int32);
+        int64_t u = 0;
+        for (int64_t k = 0; k < n; ++k)
+            if (k == 0 || nb[k] != nb[k - 1]) nb[u++] = nb[k];
+        const double *q = Q + (int64_t)i * d, *g = G + (int64_t)i * d;
+        /* forward probabilities of row i */
+        double m = -INFINITY;
+        for (int64_t a = 0; a < u; ++a) {
+            const double *kr = K + (int64_t)nb[a] * d;
+            double acc = 0.0;
+            for (int32_t k = 0; k < d; ++k) acc += q[k] * kr[k];
+            p[a] = scale * acc;
+            if (p[a] > m) m = p[a];
+        }
+        double l = 0.0;
+        for (int64_t a = 0; a < u; ++a) {
+            p[a] = exp(p[a] - m);
+            l += p[a];
+        }
+        for (int64_t a = 0; a < u; ++a) p[a] /= l;
+        /* dP and D */
+        double D = 0.0;
+        for (int64_t a = 0; a < u; ++a) {
+            const double *vr = V + (int64_t)nb[a] * d;
+            double acc = 0.0;
+            for (int32_t k = 0; k < d; ++k) acc += g[k] * vr[k];
+            dp[a] = acc;
+            D += p[a] * acc;
+        }
+        /* accumulate */
+        for (int64_t a = 0; a < u; ++a) {
+            const int64_t j = nb[a];
+            const double ds = p[a] * (dp[a] - D);
+            const double *kr = K + j * d;
+            double *dq = dQ + (int64_t)i * d, *dk = dK + j * d, *dv = dV + j * d;
+            for (int32_t k = 0; k < d; ++k) {
+                dq[k] += scale * ds * kr[k];
+                dk[k] += scale * ds * q[k];
+                dv[k] += p[a] * g[k];
+            }
+        }
+    }
+    free(nb);
+    free(p);
+    free(dp);
+    return 0;
+}
+
+/* Gradients on binary16 inputs (G = dL/dO given as binary16 too). */
+int oracle_3s_bwd_f64(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
+                      int32_t d, const uint16_t *Q, const uint16_t *K,
+                      const uint16_t *V, const uint16_t *G, double scale, double *dQ,
+                      double *dK, double *dV)
+{
+    if (d <= 0 || N < 0) return -5;
+    fill_half_table();
+    int64_t count = (int64_t)N * d;
+    double *q = widen(Q, count), *k = widen(K, count), *v = widen(V, count),
+           *g = widen(G, count);
+    int rc = -6;
+    if (q && k && v && g)
+        rc = oracle_3s_bwd_f64d(N, row_ptr, col_idx, d, q, k, v, g, scale, dQ, dK, dV);
+    free(q);
+    free(k);
+    free(v);
+    free(g);
+    return rc;
 }
 
 /* Same as oracle_3s_f64 on the row range [r0, r1) only (bounded samples). */
