@@ -108,6 +108,48 @@ f3s_status_t f3s_run_mh(f3s_plan_t plan, const void *Q, const void *K, const voi
                         void *O, int32_t n_heads, int32_t d, float scale,
                         hipStream_t stream);
 
+/*
+ * Forward with the per-row log-sum-exp kept for a later backward call.
+ *   lse  device fp32 [N, n_heads] (4-byte aligned) or NULL: for row i, head h,
+ *        lse = log(sum_j exp(scale * Q_i . K_j)) over the row's columns
+ *        (natural log; -inf for an empty row)
+ * Everything else as f3s_run_mh (which is f3s_forward with lse = NULL).
+ */
+f3s_status_t f3s_forward(f3s_plan_t plan, const void *Q, const void *K, const void *V,
+                         void *O, float *lse, int32_t n_heads, int32_t d, float scale,
+                         hipStream_t stream);
+
+/*
+ * Plan of the transposed pattern A^T, built on the GPU from `plan` alone
+ * (its bitmaps list A's entries).  Needed by f3s_backward: the gradients of
+ * K and V are sums over the rows that attend to a key, i.e. over the rows of
+ * A^T, so each window of A^T owns its keys' gradients (no atomics).
+ * Synchronous; NULL on error (f3s_last_error).  Destroy with f3s_destroy.
+ */
+f3s_plan_t f3s_plan_transpose(f3s_plan_t plan);
+
+/*
+ * Gradients of L with respect to Q, K, V given G = dL/dO (the backward pass
+ * the paper leaves to future work).  With P the forward probabilities:
+ *   delta_i = G_i . O_i,  dS_ij = P_ij (G_i . V_j - delta_i)  on the pattern,
+ *   dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T G.
+ *   plan, plan_t  a plan and f3s_plan_transpose(plan)
+ *   Q, K, V, dO   device fp16 [N, n_heads, d] (the forward's inputs, and G)
+ *   O, lse        device fp32: the forward's output [N, n_heads, d] and
+ *                 log-sum-exp [N, n_heads] from f3s_forward
+ *   delta         device fp32 [N, n_heads], written (G_i . O_i)
+ *   dQ, dK, dV    device fp32 [N, n_heads, d], every element written
+ *   d             32, 64, 96 or 128
+ * P and dS enter the products as fp16 (round to nearest even).  Outputs must
+ * not overlap each other or any input; 16-byte aligned (lse, delta: 4).
+ * Asynchronous on `stream`, no allocation.  Deterministic (no atomics).
+ */
+f3s_status_t f3s_backward(f3s_plan_t plan, f3s_plan_t plan_t, const void *Q,
+                          const void *K, const void *V, const float *O, const void *dO,
+                          const float *lse, float *delta, float *dQ, float *dK,
+                          float *dV, int32_t n_heads, int32_t d, float scale,
+                          hipStream_t stream);
+
 /* Release a plan and all its device memory.  NULL is a no-op. */
 void f3s_destroy(f3s_plan_t plan);
 

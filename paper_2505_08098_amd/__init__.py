@@ -7,5 +7,5 @@
 The compute path is the HIP library only (see ``binding``); ``workloads``
 holds the seeded synthetic inputs.
 """
-from .binding import (F3SError, Plan, PlanInfo, load_library, run, run_raw,  # noqa: F401
-                      status_string)
+from .binding import (F3SError, Plan, PlanInfo, backward, forward,  # noqa: F401
+                      load_library, run, run_raw, status_string)

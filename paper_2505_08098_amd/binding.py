@@ -80,6 +80,12 @@ def load_library():
     L.f3s_run.restype = ctypes.c_int
     L.f3s_run_mh.argtypes = [vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp]
     L.f3s_run_mh.restype = ctypes.c_int
+    L.f3s_forward.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp]
+    L.f3s_forward.restype = ctypes.c_int
+    L.f3s_plan_transpose.argtypes = [vp]
+    L.f3s_plan_transpose.restype = vp
+    L.f3s_backward.argtypes = [vp, vp] + [vp] * 10 + [i32, i32, ctypes.c_float, vp]
+    L.f3s_backward.restype = ctypes.c_int
     L.f3s_destroy.argtypes = [vp]
     L.f3s_destroy.restype = None
     L.f3s_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
@@ -109,6 +115,24 @@ def _check_device_tensor(t, name, dtype):
 
 class Plan:
     """f3s_plan on a device CSR (int32 row_ptr[N+1], int32 col_idx[nnz])."""
+
+    @classmethod
+    def _from_handle(cls, h, device, N):
+        self = cls.__new__(cls)
+        self._h = h
+        self.device = device
+        self.N = int(N)
+        self.info = self._info()
+        return self
+
+    def transpose(self):
+        """Plan of the transposed pattern (f3s_plan_transpose)."""
+        L = load_library()
+        with torch.cuda.device(self.device):
+            h = L.f3s_plan_transpose(self.handle)
+        if not h:
+            raise F3SError(L.f3s_last_error(), "f3s_plan_transpose")
+        return Plan._from_handle(h, self.device, self.N)
 
     def __init__(self, row_ptr, col_idx, N):
         L = load_library()
@@ -210,6 +234,63 @@ def run(plan, Q, K, V, scale=None, out=None, stream=None):
     if rc != F3S_OK:
         raise F3SError(rc, "f3s_run_mh")
     return out
+
+
+def forward(plan, Q, K, V, scale=None, out=None, lse=None, stream=None):
+    """f3s_forward: returns (O, lse) with lse fp32 [N] or [N, H]."""
+    shape = tuple(Q.shape)
+    H = shape[1] if len(shape) == 3 else 1
+    if lse is None:
+        lse = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
+    _check_device_tensor(lse, "lse", torch.float32)
+    if lse.numel() != plan.N * H:
+        raise ValueError("lse must hold N * H values")
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=Q.device)
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check_device_tensor(t, n, torch.float16)
+        if tuple(t.shape) != shape or shape[0] != plan.N:
+            raise ValueError("Q, K, V must share one [N, d] / [N, H, d] shape")
+    _check_device_tensor(out, "out", torch.float32)
+    d = shape[-1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if stream is None:
+        stream = torch.cuda.current_stream(Q.device)
+    rc = load_library().f3s_forward(plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(),
+                                    out.data_ptr(), lse.data_ptr(), int(H), int(d),
+                                    float(scale), ctypes.c_void_p(stream.cuda_stream))
+    if rc != F3S_OK:
+        raise F3SError(rc, "f3s_forward")
+    return out, lse
+
+
+def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
+    """f3s_backward: returns (dQ, dK, dV) fp32 (and writes a delta buffer)."""
+    shape = tuple(Q.shape)
+    H = shape[1] if len(shape) == 3 else 1
+    d = shape[-1]
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V"), (dO, "dO")):
+        _check_device_tensor(t, n, torch.float16)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{n} must have the shape of Q")
+    _check_device_tensor(O, "O", torch.float32)
+    _check_device_tensor(lse, "lse", torch.float32)
+    if tuple(O.shape) != shape or lse.numel() != plan.N * H:
+        raise ValueError("O must match Q; lse must hold N * H values")
+    dQ, dK, dV = (torch.empty(shape, dtype=torch.float32, device=Q.device) for _ in range(3))
+    delta = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if stream is None:
+        stream = torch.cuda.current_stream(Q.device)
+    rc = load_library().f3s_backward(
+        plan.handle, plan_t.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), O.data_ptr(),
+        dO.data_ptr(), lse.data_ptr(), delta.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
+        dV.data_ptr(), int(H), int(d), float(scale), ctypes.c_void_p(stream.cuda_stream))
+    if rc != F3S_OK:
+        raise F3SError(rc, "f3s_backward")
+    return dQ, dK, dV
 
 
 def run_raw(plan, q_ptr, k_ptr, v_ptr, o_ptr, d, scale, stream_handle):

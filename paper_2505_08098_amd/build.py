@@ -10,7 +10,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libf3s.so")
-SOURCES = ["f3s_api.hip", "plan_kernels.hip", "fused3s.hip"]
+SOURCES = ["f3s_api.hip", "plan_kernels.hip", "fused3s.hip", "backward.hip"]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",

@@ -3,6 +3,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <chrono>
 #include <new>
 #include <vector>
@@ -12,6 +13,7 @@
 namespace {
 
 thread_local f3s_status_t g_last_error = F3S_OK;
+std::atomic<uint64_t> g_next_plan_id{1};
 
 f3s_status_t fail(f3s_status_t s)
 {
@@ -288,6 +290,7 @@ f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N)
     }
     p->N = N;
     p->T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
+    p->id = g_next_plan_id.fetch_add(1);
     f3s_status_t st = from_hip(hipGetDevice(&p->device));
     if (st == F3S_OK) {
         if (N == 0) {
@@ -309,6 +312,53 @@ f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N)
     p->build_ms = std::chrono::duration<double, std::milli>(
                       std::chrono::steady_clock::now() - t0).count();
     return p;
+}
+
+f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
+{
+    const auto t0 = std::chrono::steady_clock::now();
+    if (!src) {
+        fail(F3S_ERR_INVALID_VALUE);
+        return nullptr;
+    }
+    const int32_t N = src->N;
+    int32_t *rp = nullptr, *ci = nullptr, *cursor = nullptr;
+    f3s_status_t st = F3S_OK;
+    auto step = [&](hipError_t e) {
+        if (st == F3S_OK && e != hipSuccess) st = from_hip(e);
+    };
+    int prev_device = 0;
+    step(hipGetDevice(&prev_device));
+    step(hipSetDevice(src->device));
+    step(hipMalloc(&rp, sizeof(int32_t) * ((size_t)N + 1)));
+    step(hipMalloc(&cursor, sizeof(int32_t) * ((size_t)N + 1)));
+    step(hipMalloc(&ci, sizeof(int32_t) * (size_t)(src->nnz > 0 ? src->nnz : 1)));
+    if (st == F3S_OK) {
+        step(hipMemset(cursor, 0, sizeof(int32_t) * ((size_t)N + 1)));
+        step(f3s::launch_transpose_entries(*src, cursor, nullptr, nullptr));
+        step(f3s::launch_scan(cursor, rp, N, nullptr));
+        step(hipMemcpy(cursor, rp, sizeof(int32_t) * (size_t)N, hipMemcpyDeviceToDevice));
+        step(f3s::launch_transpose_entries(*src, cursor, ci, nullptr));
+        step(hipDeviceSynchronize());
+    }
+    f3s_plan_t t = nullptr;
+    if (st == F3S_OK) {
+        t = f3s_plan(rp, ci, N);
+        if (!t) st = g_last_error;
+    }
+    if (rp) (void)hipFree(rp);
+    if (ci) (void)hipFree(ci);
+    if (cursor) (void)hipFree(cursor);
+    (void)hipSetDevice(prev_device);
+    if (st != F3S_OK) {
+        f3s_destroy(t);
+        fail(st);
+        return nullptr;
+    }
+    t->transpose_of = src->id;
+    t->build_ms = std::chrono::duration<double, std::milli>(
+                      std::chrono::steady_clock::now() - t0).count();
+    return t;
 }
 
 void f3s_destroy(f3s_plan_t plan)
@@ -363,9 +413,9 @@ f3s_status_t f3s_plan_export(f3s_plan_t p, int32_t *blk_off, int32_t *cols,
     return F3S_OK;
 }
 
-f3s_status_t f3s_run_mh(f3s_plan_t p, const void *Q, const void *K, const void *V,
-                        void *O, int32_t n_heads, int32_t d, float scale,
-                        hipStream_t stream)
+f3s_status_t f3s_forward(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                         void *O, float *lse, int32_t n_heads, int32_t d, float scale,
+                         hipStream_t stream)
 {
     if (!p || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
@@ -383,8 +433,60 @@ f3s_status_t f3s_run_mh(f3s_plan_t p, const void *Q, const void *K, const void *
         return fail(F3S_ERR_INVALID_VALUE);
     // base-2 softmax: 2^(x * scale * log2 e) == e^(x * scale)
     const float sl2 = (float)((double)scale * 1.4426950408889634);
+    if (lse && (((uintptr_t)lse & 3u) ||
+                overlaps(lse, (size_t)p->N * n_heads * 4, O, out_bytes) ||
+                overlaps(lse, (size_t)p->N * n_heads * 4, Q, in_bytes) ||
+                overlaps(lse, (size_t)p->N * n_heads * 4, K, in_bytes) ||
+                overlaps(lse, (size_t)p->N * n_heads * 4, V, in_bytes)))
+        return fail(F3S_ERR_INVALID_VALUE);
     f3s_status_t st =
-        from_hip(f3s::launch_fused(*p, Q, K, V, O, n_heads, d, sl2, stream));
+        from_hip(f3s::launch_fused(*p, Q, K, V, O, lse, n_heads, d, sl2, stream));
+    return st == F3S_OK ? F3S_OK : fail(st);
+}
+
+f3s_status_t f3s_run_mh(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                        void *O, int32_t n_heads, int32_t d, float scale,
+                        hipStream_t stream)
+{
+    return f3s_forward(p, Q, K, V, O, nullptr, n_heads, d, scale, stream);
+}
+
+f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void *K,
+                          const void *V, const float *O, const void *dO, const float *lse,
+                          float *delta, float *dQ, float *dK, float *dV, int32_t n_heads,
+                          int32_t d, float scale, hipStream_t stream)
+{
+    if (!p || !pt || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
+    if (pt->transpose_of != p->id || pt->N != p->N) return fail(F3S_ERR_INVALID_VALUE);
+    if (d < 32 || d > 128 || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
+    if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
+    if (p->N == 0) return F3S_OK;
+    const void *ins[] = {Q, K, V, dO};
+    void *outs[] = {dQ, dK, dV};
+    for (const void *x : ins)
+        if (!x || !aligned16(x)) return fail(F3S_ERR_INVALID_VALUE);
+    for (void *x : outs)
+        if (!x || !aligned16(x)) return fail(F3S_ERR_INVALID_VALUE);
+    if (!O || !aligned16(O) || !lse || !delta || ((uintptr_t)lse & 3u) ||
+        ((uintptr_t)delta & 3u))
+        return fail(F3S_ERR_INVALID_VALUE);
+    if ((uint64_t)p->n_items * n_heads > 0x7FFFFFFFull ||
+        (uint64_t)pt->n_items * n_heads > 0x7FFFFFFFull)
+        return fail(F3S_ERR_UNSUPPORTED);
+    const size_t elems = (size_t)p->N * n_heads * d;
+    const size_t h16 = elems * 2, f32 = elems * 4, rowv = (size_t)p->N * n_heads * 4;
+    // outputs must not overlap each other or any input
+    struct Span { const void *p; size_t n; };
+    const Span in_spans[] = {{Q, h16}, {K, h16}, {V, h16}, {dO, h16}, {O, f32}, {lse, rowv}};
+    const Span out_spans[] = {{dQ, f32}, {dK, f32}, {dV, f32}, {delta, rowv}};
+    for (const Span &o : out_spans) {
+        for (const Span &x : in_spans)
+            if (overlaps(o.p, o.n, x.p, x.n)) return fail(F3S_ERR_INVALID_VALUE);
+        for (const Span &x : out_spans)
+            if (&x != &o && overlaps(o.p, o.n, x.p, x.n)) return fail(F3S_ERR_INVALID_VALUE);
+    }
+    f3s_status_t st = from_hip(f3s::launch_backward(*p, *pt, Q, K, V, O, dO, lse, delta, dQ,
+                                                    dK, dV, n_heads, d, scale, stream));
     return st == F3S_OK ? F3S_OK : fail(st);
 }
 

@@ -39,6 +39,8 @@ struct f3s_plan_s {
     int32_t n_split = 0;
     int32_t n_pieces = 0;
     int32_t flags = 0;           // bit 0: work list in window order
+    uint64_t id = 0;             // process-unique plan id
+    uint64_t transpose_of = 0;   // id of the plan this one transposes (0: none)
     int32_t *blk_off = nullptr;  // [T + 1]
     int32_t *cols = nullptr;     // [16 * n_blocks]
     uint32_t *mask = nullptr;    // [8 * n_blocks]
@@ -100,13 +102,25 @@ hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
                               int32_t nchunks, int32_t *offs, WorkItem *items,
                               int32_t *merges, hipStream_t s);
 
+// Transposed pattern from a plan: with out == null, cursor[col] += entries
+// of column col; otherwise out[cursor[col]++] = row for every entry.
+hipError_t launch_transpose_entries(const f3s_plan_s &p, int32_t *cursor, int32_t *out,
+                                   hipStream_t s);
+
 // Sets *err when a finished plan is internally inconsistent.
 hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s);
 
 // ---- fused operator (fused3s.hip) ---------------------------------------
 // H heads of size d; Q, K, V, O rows hold the heads back to back (stride H*d).
+// lse (may be null): [N, H] natural-log log-sum-exp of each row's scores.
 hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
-                        const void *V, void *O, int32_t H, int32_t d,
+                        const void *V, void *O, float *lse, int32_t H, int32_t d,
                         float scale_log2, hipStream_t s);
+
+// Gradients (see backward.hip).  pt is the plan of the transposed pattern.
+hipError_t launch_backward(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q,
+                           const void *K, const void *V, const float *O, const void *G,
+                           const float *lse, float *delta, float *dQ, float *dK, float *dV,
+                           int32_t H, int32_t d, float scale, hipStream_t s);
 
 }  // namespace f3s

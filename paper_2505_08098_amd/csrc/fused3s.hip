@@ -38,50 +38,12 @@
 //
 // Scores and probabilities never leave registers; only O (fp32) and, for
 // split windows, the (m, l, unnormalised O) partials are written.
-#include "f3s_internal.h"
+#include "kernel_common.h"
 
 namespace f3s {
 namespace {
 
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef short s4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s4 lds_s4;
-
-__device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ h8 load16(const _Float16 *p)
-{
-    return *reinterpret_cast<const h8 *>(p);
-}
-
-__device__ __forceinline__ h8 load16_off(const _Float16 *base, uint32_t byte_off)
-{
-    return *reinterpret_cast<const h8 *>(reinterpret_cast<const char *>(base) + byte_off);
-}
-
-// Transposed LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
-// lane j of the group returns element k = 0..3 taken from the 8-byte chunk
-// addressed by group lane 4k + j/4, at position j%4 of that chunk.  So if
-// group lane s points at row (R + s/4), columns C + 4(s%4) .. +3 of a
-// row-major fp16 tile, lane j receives rows R..R+3 of column C + j: one
-// column of a 4 x 16 sub-tile, i.e. 4 reduction slots of an MFMA operand.
-__device__ __forceinline__ h4 lds_read_tr(const _Float16 *p)
-{
-    return __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)p));
-}
-
-// Orders this wave's LDS accesses (one wave per workgroup).
-__device__ __forceinline__ void wave_lds_fence()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
+constexpr float kLn2 = 0.6931471805599453f;
 
 // Occupancy target (waves per SIMD) per feature size: the most waves whose
 // registers fit without spilling; more resident waves = more gathers in
@@ -101,8 +63,8 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
     const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
     float *__restrict__ O, float *__restrict__ part_o,
-    float *__restrict__ part_ml, int32_t N, int32_t ld, int32_t h0, int32_t nh,
-    float sl2)
+    float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
+    int32_t h0, int32_t nh, float sl2)
 {
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
@@ -303,6 +265,10 @@ __attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
 #pragma unroll
             for (int t = 0; t < NT; ++t)
                 *reinterpret_cast<f4 *>(op + 16 * t) = o[t] * inv;
+            // natural-log log-sum-exp of the row's scaled scores
+            if (lse && g == 0)
+                lse[(int64_t)row * (ld / D) + head] =
+                    l_tot > 0.f ? kLn2 * (m_run + __log2f(l_tot)) : -__builtin_inff();
         }
     } else {
         // partial slot of (piece, head): slot * nh + head offset
@@ -325,7 +291,8 @@ template <int D>
 __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merges,
                                                const float *__restrict__ part_o,
                                                const float *__restrict__ part_ml,
-                                               float *__restrict__ O, int32_t N,
+                                               float *__restrict__ O,
+                                               float *__restrict__ lse, int32_t N,
                                                int32_t ld, int32_t h0, int32_t nh)
 {
     const int s = blockIdx.x / nh, hl = blockIdx.x - (blockIdx.x / nh) * nh;
@@ -346,6 +313,9 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
             l += __builtin_amdgcn_exp2f(ml[k * mstride + r] - m) * ml[k * mstride + 16 + r];
     }
     const float inv = l > 0.f ? 1.f / l : 0.f;
+    if (lse && q == 0)
+        lse[(int64_t)row * (ld / D) + h0 + hl] =
+            l > 0.f ? kLn2 * (m + __log2f(l)) : -__builtin_inff();
     const float *po = part_o + ((int64_t)first * nh + hl) * kWindowRows * D + r * D;
     const int64_t ostride = (int64_t)nh * kWindowRows * D;
     float *orow = O + (int64_t)row * ld + (int64_t)(h0 + hl) * D;
@@ -367,7 +337,8 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
 // in one launch.
 template <int D>
 hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
-                    const void *V, void *O, int32_t H, float sl2, hipStream_t s)
+                    const void *V, void *O, float *lse, int32_t H, float sl2,
+                    hipStream_t s)
 {
     const int32_t ld = H * D;
     const bool wide = (uint64_t)p.N * ld * 2 > 0xFFFFFFF0ull;
@@ -383,13 +354,14 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
             kern<<<(unsigned)grid, 64, 0, s>>>(
                 p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
                 static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V),
-                static_cast<float *>(O), p.part_o, p.part_ml, p.N, ld, h0, nh, sl2);
+                static_cast<float *>(O), p.part_o, p.part_ml, lse, p.N, ld, h0, nh, sl2);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
         if (p.n_split > 0) {
             k_merge<D><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.part_o, p.part_ml,
-                                                     static_cast<float *>(O), p.N, ld, h0, nh);
+                                                     static_cast<float *>(O), lse, p.N, ld,
+                                                     h0, nh);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
@@ -400,18 +372,18 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
 }  // namespace
 
 hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
-                        const void *V, void *O, int32_t H, int32_t d, float sl2,
-                        hipStream_t s)
+                        const void *V, void *O, float *lse, int32_t H, int32_t d,
+                        float sl2, hipStream_t s)
 {
     switch (d) {
-    case 32: return launch_d<32>(p, Q, K, V, O, H, sl2, s);
-    case 64: return launch_d<64>(p, Q, K, V, O, H, sl2, s);
-    case 96: return launch_d<96>(p, Q, K, V, O, H, sl2, s);
-    case 128: return launch_d<128>(p, Q, K, V, O, H, sl2, s);
-    case 160: return launch_d<160>(p, Q, K, V, O, H, sl2, s);
-    case 192: return launch_d<192>(p, Q, K, V, O, H, sl2, s);
-    case 224: return launch_d<224>(p, Q, K, V, O, H, sl2, s);
-    case 256: return launch_d<256>(p, Q, K, V, O, H, sl2, s);
+    case 32: return launch_d<32>(p, Q, K, V, O, lse, H, sl2, s);
+    case 64: return launch_d<64>(p, Q, K, V, O, lse, H, sl2, s);
+    case 96: return launch_d<96>(p, Q, K, V, O, lse, H, sl2, s);
+    case 128: return launch_d<128>(p, Q, K, V, O, lse, H, sl2, s);
+    case 160: return launch_d<160>(p, Q, K, V, O, lse, H, sl2, s);
+    case 192: return launch_d<192>(p, Q, K, V, O, lse, H, sl2, s);
+    case 224: return launch_d<224>(p, Q, K, V, O, lse, H, sl2, s);
+    case 256: return launch_d<256>(p, Q, K, V, O, lse, H, sl2, s);
     default: return hipErrorInvalidValue;
     }
 }

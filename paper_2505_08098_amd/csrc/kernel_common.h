@@ -1,0 +1,56 @@
+// Device helpers shared by the forward and backward kernels (CDNA4, gfx950).
+#pragma once
+
+#include "f3s_internal.h"
+
+namespace f3s {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s4 lds_s4;
+
+// D(16x16, fp32) += A(16x32, fp16) * B(32x16, fp16).  Lane l holds A row
+// l%16 and B column l%16 with 8 reduction slots chosen by l/16, and D rows
+// 4(l/16)..+3 of column l%16 (layout probed on the GPU).
+__device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ h8 load16(const _Float16 *p)
+{
+    return *reinterpret_cast<const h8 *>(p);
+}
+
+__device__ __forceinline__ h8 load16_off(const _Float16 *base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const h8 *>(reinterpret_cast<const char *>(base) + byte_off);
+}
+
+// Transposed LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane j of the group returns element k = 0..3 taken from the 8-byte chunk
+// addressed by group lane 4k + j/4, at position j%4 of that chunk.  So if
+// group lane s points at row (R + s/4), columns C + 4(s%4) .. +3 of a
+// row-major fp16 tile, lane j receives rows R..R+3 of column C + j: one
+// column of a 4 x 16 sub-tile, i.e. 4 reduction slots of an MFMA operand.
+__device__ __forceinline__ h4 lds_read_tr(const _Float16 *p)
+{
+    return __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)p));
+}
+
+// Orders this wave's LDS accesses (one wave per workgroup).
+__device__ __forceinline__ void wave_lds_fence()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ h8 cat44(h4 lo, h4 hi)
+{
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+}  // namespace f3s

@@ -357,6 +357,34 @@ __global__ void k_validate_plan(const int32_t *blk_off, int32_t T, const int32_t
     if (bad) atomicOr(err, 1);
 }
 
+// Entries of the pattern read back from a plan (every set bitmap bit is a
+// distinct (row, col) of A), one workgroup per window.  Without `out`, counts
+// the entries of each column; with it, scatters the row of each entry to
+// position cursor[col]++ of the transposed CSR (order inside a transposed row
+// is arbitrary: a plan built from it sorts its columns anyway).
+__global__ __launch_bounds__(256) void k_transpose_entries(const int32_t *blk_off,
+                                                           const int32_t *cols,
+                                                           const uint32_t *mask,
+                                                           int32_t *cursor, int32_t *out)
+{
+    const int w = blockIdx.x;
+    const int64_t w0 = (int64_t)blk_off[w] * kMaskWords, w1 = (int64_t)blk_off[w + 1] * kMaskWords;
+    for (int64_t t = w0 + threadIdx.x; t < w1; t += blockDim.x) {
+        const int64_t blk = t / kMaskWords;
+        const int word = (int)(t % kMaskWords);
+        uint32_t x = mask[t];
+        while (x) {
+            const int k = 32 * word + __ffs(x) - 1;
+            x &= x - 1;
+            const int r = (k >> 2) & 15;           // window row
+            const int c = 4 * (k >> 6) + (k & 3);  // block column
+            const int col = cols[kBlockCols * blk + c];
+            const int pos = atomicAdd(&cursor[col], 1);
+            if (out) out[pos] = w * kWindowRows + r;
+        }
+    }
+}
+
 inline unsigned grid_for(int64_t n, int threads)
 {
     int64_t g = (n + threads - 1) / threads;
@@ -490,6 +518,14 @@ hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s
     k_validate_plan<<<grid_for(n, 256), 256, 0, s>>>(p.blk_off, p.T, p.cols, p.n_blocks,
                                                     p.items, p.n_items, p.merges,
                                                     p.n_split, p.n_pieces, p.N, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_entries(const f3s_plan_s &p, int32_t *cursor, int32_t *out,
+                                   hipStream_t s)
+{
+    if (p.T == 0) return hipSuccess;
+    k_transpose_entries<<<p.T, 256, 0, s>>>(p.blk_off, p.cols, p.mask, cursor, out);
     return hipGetLastError();
 }
 

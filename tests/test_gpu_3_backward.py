@@ -1,0 +1,168 @@
+"""Backward pass on the GPU against the fp64 oracle's gradients.
+
+Tolerance for gradients (fp16 inputs; P and dS rounded to fp16 before the
+products, unit roundoff 2^-11; P recomputed from an lse whose normaliser
+summed fp16-rounded probabilities): relative Frobenius error <= 1e-3 per
+gradient and max-abs error <= 5e-3 * max(1, max |reference|).  Measured:
+rel-Fro ~2e-4 (the fp16 rounding of P and dS, 2^-11 relative, averaged).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2505_08098_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+REL_FRO = 1e-3
+MAX_ABS_REL = 5e-3
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _check(name, got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite"
+    diff = got - ref
+    nref = float(np.linalg.norm(ref))
+    rel = float(np.linalg.norm(diff)) / nref if nref > 0 else float(np.linalg.norm(diff))
+    ma = float(np.abs(diff).max()) if diff.size else 0.0
+    bound = MAX_ABS_REL * max(1.0, float(np.abs(ref).max()) if ref.size else 1.0)
+    print(f"  {name}: rel_fro={rel:.2e} max_abs={ma:.2e} (bound {bound:.2e})", flush=True)
+    assert rel <= REL_FRO and ma <= bound, (name, rel, ma)
+
+
+def _transpose_csr(rp, ci, N):
+    rows = np.repeat(np.arange(N, dtype=np.int64), np.diff(rp))
+    key = np.unique(ci.astype(np.int64) * N + rows)   # (col, row), deduplicated
+    r2 = (key // N).astype(np.int64)
+    c2 = (key % N).astype(np.int32)
+    rp2 = np.zeros(N + 1, dtype=np.int64)
+    np.cumsum(np.bincount(r2, minlength=N), out=rp2[1:])
+    return rp2.astype(np.int32), c2
+
+
+def _grad_case(f3s, oracle, rp, ci, N, Q, K, V, G, scale):
+    plan = f3s.Plan(_dev(rp), _dev(ci), N)
+    plan_t = plan.transpose()
+    q, k, v, g = _dev(Q), _dev(K), _dev(V), _dev(G)
+    O, lse = f3s.forward(plan, q, k, v, scale=scale)
+    dQ, dK, dV = f3s.backward(plan, plan_t, q, k, v, O, g, lse, scale=scale)
+    torch.cuda.synchronize()
+    H = Q.shape[1] if Q.ndim == 3 else 1
+    for h in range(H):
+        sl = (slice(None), h) if Q.ndim == 3 else (slice(None),)
+        ref = oracle.attention_bwd_f64(rp, ci, Q[sl], K[sl], V[sl], G[sl], scale)
+        for name, got, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
+            _check(f"{name}[h{h}]", got.cpu().numpy()[sl], r)
+    return plan, plan_t
+
+
+def test_forward_lse_matches_oracle(gpu, oracle, monkeypatch):
+    for piece in ("4", "1000000"):
+        monkeypatch.setenv("F3S_PIECE_BLOCKS", piece)
+        c = W.make_config(2)
+        plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+        O, lse = gpu.forward(plan, _dev(c["Q"]), _dev(c["K"]), _dev(c["V"]), scale=c["scale"])
+        torch.cuda.synchronize()
+        refO, reflse = oracle.attention_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                                            c["scale"], want_lse=True)
+        assert np.abs(lse.cpu().numpy() - reflse).max() < 2e-3
+        assert np.abs(O.cpu().numpy() - refO).max() < 5e-3
+
+
+def test_empty_rows_have_minus_inf_lse(gpu):
+    rng = np.random.default_rng(1)
+    N = 50
+    rp, ci = W.random_csr(rng, N, max_deg=5, empty_frac=0.5)
+    Q = _dev(rng.standard_normal((N, 32)).astype(np.float16))
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    _, lse = gpu.forward(plan, Q, Q, Q, scale=0.2)
+    lse = lse.cpu().numpy()
+    empty = np.diff(rp) == 0
+    assert np.all(np.isneginf(lse[empty])) and np.all(np.isfinite(lse[~empty]))
+
+
+@pytest.mark.parametrize("k", [1, 2, 4])
+def test_transposed_plan_is_the_plan_of_the_transpose(gpu, oracle, k):
+    c = W.make_config(k, with_features=False)
+    N = c["N"]
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), N)
+    got = plan.transpose().export()
+    rp2, ci2 = _transpose_csr(c["row_ptr"], c["col_idx"], N)
+    ref = gpu.Plan(_dev(rp2), _dev(ci2), N).export()
+    for key in ref:
+        assert np.array_equal(got[key], ref[key]), key
+    b = oracle.bsb(rp2, ci2, N)
+    assert np.array_equal(got["cols"], b["cols"]) and np.array_equal(got["mask"], b["mask"])
+
+
+@pytest.mark.parametrize("d", [32, 64, 96, 128])
+@pytest.mark.parametrize("N", [1, 17, 300])
+def test_gradients_random_patterns(gpu, oracle, d, N):
+    rng = np.random.default_rng(d + 7 * N)
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 50), empty_frac=0.1, dup_frac=0.2)
+    Q, K, V, G = (rng.standard_normal((N, d)).astype(np.float16) for _ in range(4))
+    print(f"random N={N} d={d}", flush=True)
+    _grad_case(gpu, oracle, rp, ci, N, Q, K, V, G, 1 / math.sqrt(d))
+
+
+@pytest.mark.parametrize("k", [1, 4, 2])
+def test_gradients_workloads(gpu, oracle, k):
+    c = W.make_config(k)
+    rng = np.random.default_rng(11)
+    G = rng.standard_normal(c["Q"].shape).astype(np.float16)
+    print(f"workload {k} N={c['N']}", flush=True)
+    _grad_case(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"], c["Q"], c["K"], c["V"], G,
+               c["scale"])
+
+
+def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch):
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
+    rng = np.random.default_rng(12)
+    N, H, d = 3000, 3, 64
+    rows = [rng.choice(N, size=300, replace=False) if i < 20 else
+            rng.choice(N, size=6, replace=False) for i in range(N)]
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([len(r) for r in rows])
+    ci = np.concatenate(rows).astype(np.int32)
+    Q, K, V, G = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(4))
+    plan, plan_t = _grad_case(gpu, oracle, rp, ci, N, Q, K, V, G, 0.125)
+    assert plan.info["n_split"] > 0 and plan_t.info["n_split"] > 0
+
+
+def test_backward_is_deterministic(gpu):
+    c = W.make_config(2)
+    rng = np.random.default_rng(13)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    plan_t = plan.transpose()
+    q, k, v = _dev(c["Q"]), _dev(c["K"]), _dev(c["V"])
+    g = _dev(rng.standard_normal(c["Q"].shape).astype(np.float16))
+    O, lse = gpu.forward(plan, q, k, v)
+    a = gpu.backward(plan, plan_t, q, k, v, O, g, lse)
+    b = gpu.backward(plan, plan_t, q, k, v, O, g, lse)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_backward_argument_errors(gpu):
+    c = W.make_config(1)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    other = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    q, k, v = _dev(c["Q"]), _dev(c["K"]), _dev(c["V"])
+    O, lse = gpu.forward(plan, q, k, v)
+    with pytest.raises(gpu.F3SError) as e:   # not the transpose of `plan`
+        gpu.backward(plan, other, q, k, v, O, q, lse)
+    assert e.value.code == 1
+    plan_t = plan.transpose()
+    big = torch.zeros((c["N"], 160), dtype=torch.float16, device=DEV)
+    Ob = torch.zeros((c["N"], 160), dtype=torch.float32, device=DEV)
+    with pytest.raises(gpu.F3SError) as e:   # d above 128
+        gpu.backward(plan, plan_t, big, big, big, Ob, big, lse)
+    assert e.value.code == 3
