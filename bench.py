@@ -27,7 +27,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16 MFMA, published
 METRIC = "ms per fused 3S call and effective GFLOP/s (4*nnz*d) at 1 MI355X"
 COUNTERS_FILE = os.path.join(HERE, "profiles", "fused3s_cl25_d128_counters.json")
 KERNEL_SOURCES = [os.path.join(HERE, "paper_2505_08098_amd", "csrc", f)
-                  for f in ("fused3s.hip", "f3s_internal.h")]
+                  for f in ("fused3s.hip", "kernel_common.h", "f3s_internal.h")]
 
 
 def kernel_source_hash():
@@ -95,6 +95,73 @@ def cpu_baseline(c, O_gpu, sample_rows):
                 ms=dt * 1e3), parity
 
 
+def backward_bytes(info, info_t, d, heads=1):
+    """Algorithmic bytes of one f3s_backward: delta (G and O read, delta
+    written), the dQ pass over windows of A (Q and G rows, K and V rows per
+    distinct window column, dQ written, plan data, lse and delta of the
+    rows) and the dK/dV pass over windows of A^T (K and V rows, Q and G rows
+    per distinct window column plus their lse and delta, dK and dV written,
+    plan data)."""
+    N = info["N"]
+    per_head = (6 * N * d + 4 * N
+                + 4 * N * d + 4 * d * info["n_unique"] + 4 * N * d + 8 * N
+                + 4 * N * d + 4 * d * info_t["n_unique"] + 8 * info_t["n_unique"]
+                + 8 * N * d)
+    plan_bytes = 96 * (info["n_blocks"] + info_t["n_blocks"]) + 16 * (
+        info["n_items"] + info_t["n_items"])
+    return heads * per_head + plan_bytes
+
+
+def bench_backward(args, c, plan, Q, K, V, stream, dev):
+    import numpy as np
+    import torch
+    import paper_2505_08098_amd as f3s
+    d, H = c["d"], args.heads
+    t0 = time.perf_counter()
+    plan_t = plan.transpose()
+    transpose_ms = (time.perf_counter() - t0) * 1e3
+    rng = np.random.default_rng(np.random.SeedSequence(args.seed).spawn(4)[3])
+    G = torch.from_numpy(rng.standard_normal(tuple(Q.shape), dtype=np.float32)
+                         .astype(np.float16)).to(dev)
+    O, lse = f3s.forward(plan, Q, K, V, scale=c["scale"], stream=stream)
+    for _ in range(args.warmup):
+        f3s.backward(plan, plan_t, Q, K, V, O, G, lse, scale=c["scale"], stream=stream)
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for k in range(args.steps):
+        starts[k].record(stream)
+        f3s.backward(plan, plan_t, Q, K, V, O, G, lse, scale=c["scale"], stream=stream)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
+    ms = float(per.mean())
+    info, info_t = plan.info, plan_t.info
+    flops = 10.0 * info["nnz"] * d * H  # scores recomputed + 4 products
+    nbytes = backward_bytes(info, info_t, d, H)
+    out = {
+        "metric": "ms per fused 3S backward call (dQ, dK, dV) and effective GFLOP/s "
+                  "(10*nnz*d) at 1 MI355X",
+        "value": round(flops / (ms * 1e-3) / 1e9, 2), "unit": "GFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": c["name"], "N": c["N"], "nnz": info["nnz"], "d": d,
+                   "heads": H},
+        "ms_median": round(float(np.median(per)), 5),
+        "transpose_plan_ms": round(transpose_ms, 3),
+        "roofline": {"bound": "hbm", "achieved": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "algorithmic_bytes_per_call": nbytes,
+                     "kernel": "k_bwd_dq (with delta) + k_bwd_dkdv"},
+        "cpu_baseline": None,
+    }
+    plan_t.close()
+    plan.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +175,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--cpu-rows", type=int, default=1 << 30,
                     help="rows of the workload in the oracle baseline sample")
+    ap.add_argument("--backward", action="store_true",
+                    help="time f3s_backward (dQ, dK, dV) instead of the forward call")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run 3 plain device copies of this many MiB "
                          "(reference dispatches for scaling HBM byte counters)")
@@ -143,6 +212,8 @@ def main():
     info = plan.info
     stream = torch.cuda.current_stream(dev)
 
+    if args.backward:
+        return bench_backward(args, c, plan, Q, K, V, stream, dev)
     for _ in range(args.warmup):
         f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
     torch.cuda.synchronize()

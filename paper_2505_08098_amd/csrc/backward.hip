@@ -5,9 +5,9 @@
 //
 // With P the forward probabilities (recomputed from the stored log-sum-exp,
 // so nothing of size nnz is kept between the passes) and G = dL/dO:
-//   delta_i = G_i . O_i                           k_delta
+//   delta_i = G_i . O_i                           k_bwd_dq   (windows of A)
 //   dP_ij   = G_i . V_j,  dS_ij = P_ij (dP_ij - delta_i)
-//   dQ_i    = scale sum_j dS_ij K_j               k_bwd_dq   (windows of A)
+//   dQ_i    = scale sum_j dS_ij K_j               k_bwd_dq
 //   dV_j    = sum_i P_ij G_i                      k_bwd_dkdv (windows of A^T)
 //   dK_j    = scale sum_i dS_ij Q_i               k_bwd_dkdv
 // dK and dV are owned by the windows of the transposed pattern, so no
@@ -24,6 +24,7 @@ template <int D> struct BwdWaves { static constexpr int value = 1; };
 template <> struct BwdWaves<32> { static constexpr int value = 4; };
 template <> struct BwdWaves<64> { static constexpr int value = 2; };
 template <> struct BwdWaves<96> { static constexpr int value = 2; };
+template <> struct BwdWaves<128> { static constexpr int value = 2; };
 
 // Row-contiguous gather of the 32 rows (two blocks) of a block pair from two
 // row-major fp16 matrices A and B (same rows): chunk f = lane + 64 j is row
@@ -70,25 +71,6 @@ __device__ __forceinline__ int sanitize_slot(int ncol, int lane)
     return ncol < 0 ? ((lane & 16) ? f1 : f0) : ncol;
 }
 
-__global__ void k_delta(const _Float16 *__restrict__ G, const float *__restrict__ O,
-                        float *__restrict__ delta, int64_t rows, int32_t d)
-{
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= rows) return;
-    const _Float16 *g = G + t * d;
-    const float *o = O + t * d;
-    float acc = 0.f;
-    for (int k = 0; k < d; k += 8) {
-        const h8 gv = load16(g + k);
-        const f4 o0 = *reinterpret_cast<const f4 *>(o + k);
-        const f4 o1 = *reinterpret_cast<const f4 *>(o + k + 4);
-        acc += (float)gv[0] * o0[0] + (float)gv[1] * o0[1] + (float)gv[2] * o0[2] +
-               (float)gv[3] * o0[3] + (float)gv[4] * o1[0] + (float)gv[5] * o1[1] +
-               (float)gv[6] * o1[2] + (float)gv[7] * o1[3];
-    }
-    delta[t] = acc;
-}
-
 // dQ over the row windows of A.  Lane (i, g): query row i of the window;
 // scores and dP as in the forward (S^T = K_hat Q^T, dP^T = V_hat G^T), then
 // dQ^T += K_hat^T dS^T with K_hat read transposed from LDS.
@@ -98,9 +80,10 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
     const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
-    const _Float16 *__restrict__ G, const float *__restrict__ lse,
-    const float *__restrict__ delta, float *__restrict__ dQ, float *__restrict__ part,
-    int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2, float scale)
+    const _Float16 *__restrict__ G, const float *__restrict__ O,
+    const float *__restrict__ lse, float *__restrict__ delta, float *__restrict__ dQ,
+    float *__restrict__ part, int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2,
+    float scale)
 {
     constexpr int NC = D / 32, NT = D / 16, NI = D / 16;
     constexpr int LSK = D + 16;  // K tile: operand reads and transposed reads
@@ -116,6 +99,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     K += (int64_t)head * D;
     V += (int64_t)head * D;
     G += (int64_t)head * D;
+    O += (int64_t)head * D;
     dQ += (int64_t)head * D;
     const int row = it.window * kWindowRows + i;
     const int rrow = min(row, N - 1);
@@ -128,7 +112,22 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
         gq[c] = load16(G + (int64_t)rrow * ld + 32 * c + 8 * g);
     }
     const float lse2 = lse[(int64_t)rrow * H + head] * kLog2e;
-    const float dl = delta[(int64_t)rrow * H + head];
+    // delta_i = G_i . O_i from the G values this lane holds and the matching
+    // O values; the four lanes of a row together cover all d.  Every piece
+    // of a split window writes the same value; the dK/dV pass reads it.
+    float dl = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const float *orow = O + (int64_t)rrow * ld + 32 * c + 8 * g;
+        const f4 o0 = *reinterpret_cast<const f4 *>(orow);
+        const f4 o1 = *reinterpret_cast<const f4 *>(orow + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            dl += (float)gq[c][e] * o0[e] + (float)gq[c][4 + e] * o1[e];
+    }
+    dl += __shfl_xor(dl, 16);
+    dl += __shfl_xor(dl, 32);
+    if (g == 0 && row < N) delta[(int64_t)row * H + head] = dl;
 
     f4 acc[NT];
 #pragma unroll
@@ -404,10 +403,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     const auto *k = static_cast<const _Float16 *>(K);
     const auto *v = static_cast<const _Float16 *>(V);
     const auto *gr = static_cast<const _Float16 *>(G);
-    const int64_t rows = (int64_t)p.N * H;
-    k_delta<<<(unsigned)((rows + 255) / 256), 256, 0, s>>>(gr, O, delta, rows, D);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
         auto kern = wide ? k_bwd_dq<D, true> : k_bwd_dq<D, false>;
@@ -417,8 +413,8 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
             if (p.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)p.n_items * nh), 64, 0, s>>>(
-                    p.items, p.cols, p.mask, q, k, v, gr, lse, delta, dQ, p.part_o, p.N, ld,
-                    h0, nh, sl2, scale);
+                    p.items, p.cols, p.mask, q, k, v, gr, O, lse, delta, dQ, p.part_o, p.N,
+                    ld, h0, nh, sl2, scale);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (p.n_split > 0) {
