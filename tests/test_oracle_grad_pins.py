@@ -91,3 +91,54 @@ def test_binary16_entry_widens_exactly(oracle):
     b = oracle.attention_bwd_f64(rp, ci, *[x.astype(np.float64) for x in X], 0.5)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+def test_constant_values_give_zero_score_gradients(oracle):
+    """All V rows equal: O_i = V for every non-empty row whatever P is, so
+    dP_ij = G_i . V is the same for all j of a row and equals delta_i: dS = 0,
+    hence dQ = dK = 0, while dV still receives sum_i P_ij G_i."""
+    rng = np.random.default_rng(7)
+    N, d = 50, 6
+    rp, ci = W.random_csr(rng, N, max_deg=10, empty_frac=0.1)
+    Q, K, G = (rng.standard_normal((N, d)) for _ in range(3))
+    V = np.tile(rng.standard_normal(d), (N, 1))
+    dQ, dK, dV = oracle.attention_bwd_f64(rp, ci, Q, K, V, G, 0.8)
+    assert np.abs(dQ).max() < 1e-12 and np.abs(dK).max() < 1e-12
+    # dV sums to the sum of G over non-empty rows (each P row sums to one)
+    nonempty = np.diff(rp) > 0
+    np.testing.assert_allclose(dV.sum(axis=0), G[nonempty].sum(axis=0), atol=1e-11)
+
+
+def test_scale_derivative_identity(oracle):
+    """The scores are scale * Q_i . K_j, so dL/dscale = sum dS_ij Q_i . K_j,
+    which equals <dQ, Q> / scale and <dK, K> / scale; the derivative is
+    checked against a central difference in the scale itself."""
+    rng = np.random.default_rng(8)
+    N, d = 25, 4
+    rp, ci = W.random_csr(rng, N, max_deg=8, empty_frac=0.1)
+    Q, K, V, G = (rng.standard_normal((N, d)) for _ in range(4))
+    s = 0.6
+    dQ, dK, _ = oracle.attention_bwd_f64(rp, ci, Q, K, V, G, s)
+    h = 1e-6
+    fd = ((oracle.attention_f64_exact(rp, ci, Q, K, V, s + h) * G).sum()
+          - (oracle.attention_f64_exact(rp, ci, Q, K, V, s - h) * G).sum()) / (2 * h)
+    assert abs((dQ * Q).sum() / s - fd) < 1e-7
+    assert abs((dK * K).sum() / s - fd) < 1e-7
+
+
+def test_empty_rows_and_unreferenced_columns(oracle):
+    """An empty row has O = 0 independent of its Q, so its dQ row is 0; a
+    node no row points at contributes to no output, so its dK and dV rows
+    are 0."""
+    rng = np.random.default_rng(9)
+    N, d = 40, 5
+    rp, ci = W.random_csr(rng, N, max_deg=6, empty_frac=0.3)
+    ci = np.where(ci < 3, ci + 3, ci).astype(np.int32)   # nodes 0, 1, 2 unreferenced
+    Q, K, V, G = (rng.standard_normal((N, d)) for _ in range(4))
+    dQ, dK, dV = oracle.attention_bwd_f64(rp, ci, Q, K, V, G, 0.5)
+    empty = np.diff(rp) == 0
+    assert empty.any() and np.all(dQ[empty] == 0)
+    unref = np.ones(N, dtype=bool)
+    unref[ci] = False
+    assert unref.any()
+    assert np.all(dK[unref] == 0) and np.all(dV[unref] == 0)
