@@ -27,7 +27,8 @@ MFMA_F16_PEAK_TFLOPS = 2500.0  # dense fp16 MFMA, published
 METRIC = "ms per fused 3S call and effective GFLOP/s (4*nnz*d) at 1 MI355X"
 COUNTERS_FILE = os.path.join(HERE, "profiles", "fused3s_cl25_d128_counters.json")
 KERNEL_SOURCES = [os.path.join(HERE, "paper_2505_08098_amd", "csrc", f)
-                  for f in ("fused3s.hip", "kernel_common.h", "f3s_internal.h")]
+                  for f in ("fused3s.hip", "fused3s_kernel.h", "kernel_common.h",
+                            "f3s_internal.h")]
 
 
 def kernel_source_hash():
@@ -44,13 +45,15 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(info, d, heads=1):
+def algorithmic_bytes(info, d, heads=1, in_size=2, out_size=4):
     """Bytes one launch must move at minimum without cache reuse: Q read and
-    O written once (6*N*d per head), the K and V rows of every distinct
-    (window, column) pair (4*d per pair and head), 64 B of column ids + 32 B
-    of bitmap per block, 16 B per work item (plan data counted once: the
-    heads of a window share it)."""
-    return (heads * (6 * info["N"] * d + 4 * d * info["n_unique"])
+    O written once ((in_size + out_size)*N*d per head: 6*N*d for fp16 in,
+    fp32 out), the K and V rows of every distinct (window, column) pair
+    (2*in_size*d per pair and head), 64 B of column ids + 32 B of bitmap per
+    block, 16 B per work item (plan data counted once: the heads of a window
+    share it)."""
+    return (heads * ((in_size + out_size) * info["N"] * d
+                     + 2 * in_size * d * info["n_unique"])
             + 96 * info["n_blocks"] + 16 * info["n_items"])
 
 
@@ -177,10 +180,17 @@ def main():
                     help="rows of the workload in the oracle baseline sample")
     ap.add_argument("--backward", action="store_true",
                     help="time f3s_backward (dQ, dK, dV) instead of the forward call")
+    ap.add_argument("--in-dtype", default="f16", choices=["f16", "bf16"],
+                    help="storage type of Q, K, V (bf16: f3s_forward_typed)")
+    ap.add_argument("--out-dtype", default="f32", choices=["f32", "f16"],
+                    help="type of O (f16: f3s_forward_typed)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run 3 plain device copies of this many MiB "
                          "(reference dispatches for scaling HBM byte counters)")
     args = ap.parse_args()
+    if args.backward and (args.in_dtype != "f16" or args.out_dtype != "f32"):
+        print(json.dumps({"error": "the backward pass takes fp16 inputs and fp32 outputs"}))
+        sys.exit(2)
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -193,20 +203,34 @@ def main():
     f3s.load_library()
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
-    c = W.make_config(args.workload, seed=args.seed)
+    c = W.make_config(args.workload, seed=args.seed, dtype=args.in_dtype)
     gen_s = time.perf_counter() - t0
     N, d = c["N"], c["d"]
     H = args.heads
     if H > 1:
         rng = np.random.default_rng(np.random.SeedSequence(args.seed).spawn(3)[2])
         for key in ("Q", "K", "V"):
-            c[key] = rng.standard_normal((N, H, d), dtype=np.float32).astype(np.float16)
+            x = rng.standard_normal((N, H, d), dtype=np.float32)
+            c[key] = x.astype(np.float16) if args.in_dtype == "f16" else W.to_bf16_bits(x)
     rp = torch.from_numpy(c["row_ptr"]).to(dev)
     ci = torch.from_numpy(c["col_idx"]).to(dev)
-    Q = torch.from_numpy(c["Q"]).to(dev)
-    K = torch.from_numpy(c["K"]).to(dev)
-    V = torch.from_numpy(c["V"]).to(dev)
-    O = torch.empty(tuple(c["Q"].shape), dtype=torch.float32, device=dev)
+
+    def to_dev(a):
+        t = torch.from_numpy(a)
+        return t.to(dev) if args.in_dtype == "f16" else t.view(torch.int16).to(dev).view(
+            torch.bfloat16)
+
+    Q, K, V = to_dev(c["Q"]), to_dev(c["K"]), to_dev(c["V"])
+    out_dt = torch.float32 if args.out_dtype == "f32" else torch.float16
+    O = torch.empty(tuple(c["Q"].shape), dtype=out_dt, device=dev)
+    typed = args.in_dtype != "f16" or args.out_dtype != "f32"
+
+    def call():
+        if typed:
+            f3s.forward_typed(plan, Q, K, V, out_dtype=out_dt, scale=c["scale"], out=O,
+                              stream=stream)
+        else:
+            f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
     torch.cuda.synchronize()
     plan = f3s.Plan(rp, ci, N)
     info = plan.info
@@ -215,7 +239,7 @@ def main():
     if args.backward:
         return bench_backward(args, c, plan, Q, K, V, stream, dev)
     for _ in range(args.warmup):
-        f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
+        call()
     torch.cuda.synchronize()
     # timed region: events on the launch stream around each call
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -224,7 +248,7 @@ def main():
     w0 = time.perf_counter()
     for k in range(args.steps):
         starts[k].record(stream)
-        f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
+        call()
         ends[k].record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
@@ -233,10 +257,10 @@ def main():
 
     flops_eff = 4.0 * info["nnz"] * d * H
     value = flops_eff / (ms * 1e-3) / 1e9
-    alg_bytes = algorithmic_bytes(info, d, H)
+    alg_bytes = algorithmic_bytes(info, d, H, 2, 4 if args.out_dtype == "f32" else 2)
     achieved = alg_bytes / (ms * 1e-3) / 1e9
     issued = 1024.0 * d * H * info["n_blocks"]  # MFMA flops incl. zero padding
-    traffic = traffic_from_counters(d) if H == 1 else None
+    traffic = traffic_from_counters(d) if H == 1 and not typed else None
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -248,7 +272,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": args.in_dtype,
         "data": "synthetic",
         "config": {
             "workload": f"{c['name']}: " + {
@@ -260,6 +284,7 @@ def main():
                 5: "sequence L=32768, window 256 + 64 random keys per query, d=64",
             }[args.workload],
             "N": N, "nnz": info["nnz"], "d": d, "heads": H, "scale": c["scale"],
+            "in_dtype": args.in_dtype, "out_dtype": args.out_dtype,
             "seed": args.seed,
             "parallelism": "single GPU",
         },
@@ -279,7 +304,9 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_bytes,
-            "kernel": "k_fused3s<%d>" % d + (" x %d heads" % H if H > 1 else ""),
+            "kernel": "k_fused3s<%d>" % d + (" %s->%s" % (args.in_dtype, args.out_dtype)
+                                              if typed else "")
+                      + (" x %d heads" % H if H > 1 else ""),
             "mfma_issued_frac": round(issued / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
         },
         "gen_s": round(gen_s, 1),
@@ -294,8 +321,9 @@ def main():
         torch.cuda.synchronize()
         out["copy_calib_bytes"] = n * 4
         del src, dst
-    if not args.no_cpu and H > 1:
-        out["cpu_baseline"] = None  # the oracle baseline is defined for one head
+    if not args.no_cpu and (H > 1 or typed):
+        # the oracle baseline is timed on the one-head fp16 -> fp32 workload
+        out["cpu_baseline"] = None
     elif not args.no_cpu:
         torch.cuda.synchronize()
         O_host = O.cpu().numpy()

@@ -119,6 +119,32 @@ f3s_status_t f3s_forward(f3s_plan_t plan, const void *Q, const void *K, const vo
                          void *O, float *lse, int32_t n_heads, int32_t d, float scale,
                          hipStream_t stream);
 
+/* Element types of the typed forward. */
+typedef enum {
+    F3S_DTYPE_F16 = 0,   /* IEEE 754 binary16 */
+    F3S_DTYPE_BF16 = 1,  /* bfloat16: the upper 16 bits of an IEEE binary32 */
+    F3S_DTYPE_F32 = 2    /* IEEE 754 binary32 */
+} f3s_dtype_t;
+
+/*
+ * Forward with a choice of storage types (the precision variants beside
+ * Table 5's scheme).
+ *   in_dtype   type of Q, K, V: F3S_DTYPE_F16 (Table 5) or F3S_DTYPE_BF16.
+ *              With bf16 inputs the scores use the bf16 matrix product and
+ *              the probabilities enter the value product as two bf16 terms
+ *              (about 16 significant bits), so the error stays within the
+ *              fp16 scheme's bound.
+ *   out_dtype  type of O: F3S_DTYPE_F32 (Table 5) or F3S_DTYPE_F16 (the
+ *              normalised fp32 result rounded to nearest even).
+ * Other types give F3S_ERR_UNSUPPORTED.  Layouts, alignment, d, scale, lse
+ * and stream rules as f3s_forward, with element sizes taken from the types.
+ * f3s_forward is this call with (F3S_DTYPE_F16, F3S_DTYPE_F32).
+ */
+f3s_status_t f3s_forward_typed(f3s_plan_t plan, const void *Q, const void *K, const void *V,
+                               f3s_dtype_t in_dtype, void *O, f3s_dtype_t out_dtype,
+                               float *lse, int32_t n_heads, int32_t d, float scale,
+                               hipStream_t stream);
+
 /*
  * Plan of the transposed pattern A^T, built on the GPU from `plan` alone
  * (its bitmaps list A's entries).  Needed by f3s_backward: the gradients of

@@ -14,6 +14,9 @@ Functions and the passages they follow:
 * :func:`bsb` -- Section 3.1, the Binary Sparse Block construction (row
   windows of 16 rows, all-zero columns removed, 16x16 blocks, one bitmap per
   block; Table 3 gives its footprint).
+* :func:`attention_bf16_f64` -- the same definition on bfloat16 inputs
+  (exact widening with the oracle's own bfloat16 decoder; the precision
+  variant beside Table 5's fp16 scheme).
 * :func:`attention_bwd_f64` -- gradients of the operator (the backward pass
   the paper names as the next step): softmax Jacobian applied to dO V^T on
   the pattern, then the two products back through K and Q, and P^T dO.
@@ -46,6 +49,10 @@ def lib():
         vp = ctypes.c_void_p
         L.oracle_half_to_double.argtypes = [ctypes.c_uint16]
         L.oracle_half_to_double.restype = dbl
+        L.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+        L.oracle_bf16_to_double.restype = dbl
+        L.oracle_widen_bf16.argtypes = [ctypes.c_int64, vp, vp]
+        L.oracle_widen_bf16.restype = None
         L.oracle_check_csr.argtypes = [i32, vp, vp]
         L.oracle_check_csr.restype = ctypes.c_int
         L.oracle_3s_f64.argtypes = [i32, vp, vp, i32, vp, vp, vp, dbl, vp, vp, vp, i32]
@@ -92,6 +99,28 @@ def _half_bits(x):
 def half_to_double(bits):
     """Decode one binary16 bit pattern with the oracle's own decoder."""
     return lib().oracle_half_to_double(int(bits) & 0xFFFF)
+
+
+def bf16_to_double(bits):
+    """Decode one bfloat16 bit pattern with the oracle's own decoder."""
+    return lib().oracle_bf16_to_double(int(bits) & 0xFFFF)
+
+
+def widen_bf16(bits):
+    """bfloat16 bit patterns (uint16 array) -> float64, exactly."""
+    a = np.ascontiguousarray(bits)
+    if a.dtype != np.uint16:
+        raise TypeError("expected bfloat16 bit patterns as uint16")
+    out = np.empty(a.shape, dtype=np.float64)
+    lib().oracle_widen_bf16(a.size, _ptr(a), _ptr(out))
+    return out
+
+
+def attention_bf16_f64(row_ptr, col_idx, Q, K, V, scale, want_lse=False):
+    """The operator on bfloat16 inputs (uint16 bit patterns), in fp64: the
+    inputs are widened exactly and the fp64 definition is applied."""
+    return attention_f64_exact(row_ptr, col_idx, widen_bf16(Q), widen_bf16(K),
+                               widen_bf16(V), scale, want_lse=want_lse)
 
 
 def check_csr(row_ptr, col_idx, N):

@@ -59,6 +59,34 @@ static double half_bits_to_double(uint16_t h)
 
 double oracle_half_to_double(uint16_t h) { return half_bits_to_double(h); }
 
+/* ---------------------------------------------------------------------- */
+/* bfloat16 -> double, from the format definition: 1 sign bit, 8 exponent  */
+/* bits (bias 127, as binary32), 7 fraction bits.  Exact in double.        */
+/* ---------------------------------------------------------------------- */
+static double bf16_bits_to_double(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int expo = (h >> 7) & 0xff;
+    int frac = h & 0x7f;
+    double v;
+    if (expo == 0) {
+        v = ldexp((double)frac, -133);           /* subnormal: frac * 2^-133 */
+    } else if (expo == 255) {
+        v = frac ? NAN : INFINITY;
+    } else {
+        v = ldexp((double)(frac + 128), expo - 134); /* (1 + f/128) 2^(e-127) */
+    }
+    return sign ? -v : v;
+}
+
+double oracle_bf16_to_double(uint16_t h) { return bf16_bits_to_double(h); }
+
+/* count bfloat16 bit patterns -> fp64 (exact). */
+void oracle_widen_bf16(int64_t count, const uint16_t *h, double *out)
+{
+    for (int64_t k = 0; k < count; ++k) out[k] = bf16_bits_to_double(h[k]);
+}
+
 /* Decoding table: entry h is half_bits_to_double(h) (filled once). */
 static double g_half_table[65536];
 static int g_half_table_ready = 0;

@@ -82,6 +82,9 @@ def load_library():
     L.f3s_run_mh.restype = ctypes.c_int
     L.f3s_forward.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp]
     L.f3s_forward.restype = ctypes.c_int
+    L.f3s_forward_typed.argtypes = [vp, vp, vp, vp, i32, vp, i32, vp, i32, i32,
+                                    ctypes.c_float, vp]
+    L.f3s_forward_typed.restype = ctypes.c_int
     L.f3s_plan_transpose.argtypes = [vp]
     L.f3s_plan_transpose.restype = vp
     L.f3s_backward.argtypes = [vp, vp] + [vp] * 10 + [i32, i32, ctypes.c_float, vp]
@@ -262,6 +265,49 @@ def forward(plan, Q, K, V, scale=None, out=None, lse=None, stream=None):
                                     float(scale), ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
         raise F3SError(rc, "f3s_forward")
+    return out, lse
+
+
+# f3s_dtype_t codes
+_DTYPE_CODE = {torch.float16: 0, torch.bfloat16: 1, torch.float32: 2}
+
+
+def forward_typed(plan, Q, K, V, out_dtype=torch.float32, scale=None, out=None,
+                  lse=None, want_lse=False, stream=None):
+    """f3s_forward_typed: Q, K, V fp16 or bf16 ([N, d] or [N, H, d]); O of
+    ``out_dtype`` (fp32 or fp16).  Returns (O, lse) with lse None unless
+    ``want_lse`` or an ``lse`` tensor is given."""
+    shape = tuple(Q.shape)
+    H = shape[1] if len(shape) == 3 else 1
+    if Q.dtype not in (torch.float16, torch.bfloat16):
+        raise TypeError(f"Q must be float16 or bfloat16, got {Q.dtype}")
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check_device_tensor(t, n, Q.dtype)
+        if tuple(t.shape) != shape or shape[0] != plan.N:
+            raise ValueError("Q, K, V must share one [N, d] / [N, H, d] shape")
+    if out is None:
+        out = torch.empty(shape, dtype=out_dtype, device=Q.device)
+    _check_device_tensor(out, "out", out_dtype)
+    if tuple(out.shape) != shape:
+        raise ValueError("out must have the shape of Q")
+    if lse is None and want_lse:
+        lse = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
+    if lse is not None:
+        _check_device_tensor(lse, "lse", torch.float32)
+        if lse.numel() != plan.N * H:
+            raise ValueError("lse must hold N * H values")
+    d = shape[-1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if stream is None:
+        stream = torch.cuda.current_stream(Q.device)
+    rc = load_library().f3s_forward_typed(
+        plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), _DTYPE_CODE[Q.dtype],
+        out.data_ptr(), _DTYPE_CODE.get(out_dtype, -1),
+        lse.data_ptr() if lse is not None else None, int(H), int(d), float(scale),
+        ctypes.c_void_p(stream.cuda_stream))
+    if rc != F3S_OK:
+        raise F3SError(rc, "f3s_forward_typed")
     return out, lse
 
 

@@ -413,12 +413,17 @@ f3s_status_t f3s_plan_export(f3s_plan_t p, int32_t *blk_off, int32_t *cols,
     return F3S_OK;
 }
 
-f3s_status_t f3s_forward(f3s_plan_t p, const void *Q, const void *K, const void *V,
-                         void *O, float *lse, int32_t n_heads, int32_t d, float scale,
-                         hipStream_t stream)
+f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                               f3s_dtype_t in_dtype, void *O, f3s_dtype_t out_dtype,
+                               float *lse, int32_t n_heads, int32_t d, float scale,
+                               hipStream_t stream)
 {
     if (!p || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
+    if (in_dtype != F3S_DTYPE_F16 && in_dtype != F3S_DTYPE_BF16)
+        return fail(F3S_ERR_UNSUPPORTED);
+    if (out_dtype != F3S_DTYPE_F32 && out_dtype != F3S_DTYPE_F16)
+        return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
     if (!Q || !K || !V || !O) return fail(F3S_ERR_INVALID_VALUE);
@@ -427,7 +432,8 @@ f3s_status_t f3s_forward(f3s_plan_t p, const void *Q, const void *K, const void 
     if ((uint64_t)p->n_items * (uint64_t)n_heads > 0x7FFFFFFFull)
         return fail(F3S_ERR_UNSUPPORTED);
     const size_t elems = (size_t)p->N * (size_t)n_heads * (size_t)d;
-    const size_t in_bytes = elems * 2, out_bytes = elems * 4;
+    const size_t in_bytes = elems * 2;
+    const size_t out_bytes = elems * (out_dtype == F3S_DTYPE_F32 ? 4 : 2);
     if (overlaps(O, out_bytes, Q, in_bytes) || overlaps(O, out_bytes, K, in_bytes) ||
         overlaps(O, out_bytes, V, in_bytes))
         return fail(F3S_ERR_INVALID_VALUE);
@@ -439,9 +445,19 @@ f3s_status_t f3s_forward(f3s_plan_t p, const void *Q, const void *K, const void 
                 overlaps(lse, (size_t)p->N * n_heads * 4, K, in_bytes) ||
                 overlaps(lse, (size_t)p->N * n_heads * 4, V, in_bytes)))
         return fail(F3S_ERR_INVALID_VALUE);
-    f3s_status_t st =
-        from_hip(f3s::launch_fused(*p, Q, K, V, O, lse, n_heads, d, sl2, stream));
+    const int in_type = in_dtype == F3S_DTYPE_BF16 ? f3s::kInBF16 : f3s::kInF16;
+    f3s_status_t st = from_hip(f3s::launch_fused(*p, Q, K, V, in_type, O,
+                                                 out_dtype == F3S_DTYPE_F16, lse, n_heads, d,
+                                                 sl2, stream));
     return st == F3S_OK ? F3S_OK : fail(st);
+}
+
+f3s_status_t f3s_forward(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                         void *O, float *lse, int32_t n_heads, int32_t d, float scale,
+                         hipStream_t stream)
+{
+    return f3s_forward_typed(p, Q, K, V, F3S_DTYPE_F16, O, F3S_DTYPE_F32, lse, n_heads, d,
+                             scale, stream);
 }
 
 f3s_status_t f3s_run_mh(f3s_plan_t p, const void *Q, const void *K, const void *V,

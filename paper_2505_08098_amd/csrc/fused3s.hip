@@ -1,391 +1,17 @@
-// Fused 3S kernel for CDNA4 (gfx950): Algorithm 1 of Fused3S with the
-// tensor-core tiling re-derived for 64-wide wavefronts and the
-// v_mfma_f32_16x16x32_f16 matrix instruction.
-//
-// One wavefront owns one work item (a 16-row window, or a piece of one) and
-// walks its 16x16 blocks two at a time (32 compacted columns = the K depth of
-// one MFMA for the value product).  Per block pair:
-//
-//   scores   S^T = K_hat * Q_i^T     (A = gathered K rows, read from LDS in
-//                                     the operand layout; B = the window's
-//                                     Q rows, in VGPRs for the whole item)
-//            With S^T as the product, MFMA's accumulator layout gives every
-//            lane ONE query row (lane % 16) and 4 neighbours per block, so
-//            the row softmax needs only a 4-lane reduction and the fp16
-//            probabilities already sit in the B-operand layout of the next
-//            product: no shuffle of P at all.
-//   mask     bitmap bit clear -> score -inf (the bitmap mask of Algorithm 1)
-//   softmax  online, base 2, fp32 (Section 3.5): running max m, running
-//            lane-partial sum l, rescale factor alpha = 2^(m_old - m_new)
-//            applied every pair (a branch around a rarely needed rescale
-//            measured slower: it splits the loop body for the scheduler)
-//   P        fp32 -> fp16 with round-to-nearest-even; the SAME rounded values
-//            are summed into l, so the effective probabilities of a row sum
-//            to one
-//   values   O_i^T += V_hat^T * P^T  (A = gathered V rows staged row-major in
-//            LDS and read transposed; B = P from registers; the accumulator
-//            lane layout again has lane % 16 = query row, so the alpha
-//            rescale is a per-lane multiply)
-//
-// The gather order within a row (the reduction index of the score product)
-// is permuted so each lane reads 16 contiguous bytes per load and the four
-// lanes of a row cover 64 contiguous bytes: any consistent permutation of the
-// reduction index leaves Q K^T unchanged (the register remapping of
-// Section 3.4).  The loads of the next block pair are issued before the
-// softmax and value product of the current pair (one pair in flight).
-// K and V rows are gathered with row-contiguous lanes and staged through
-// LDS (see the pipeline comment in the kernel).
-//
-// Scores and probabilities never leave registers; only O (fp32) and, for
-// split windows, the (m, l, unnormalised O) partials are written.
-#include "kernel_common.h"
+// Fused 3S forward, fp16 inputs (the precision scheme of Table 5), and the
+// dispatch over input storage types.  The kernels are in fused3s_kernel.h.
+#include "fused3s_kernel.h"
 
 namespace f3s {
-namespace {
-
-constexpr float kLn2 = 0.6931471805599453f;
-
-// Occupancy target (waves per SIMD) per feature size: the most waves whose
-// registers fit without spilling; more resident waves = more gathers in
-// flight, which is what bounds this kernel.
-template <int D> struct WavesPerSimd { static constexpr int value = 1; };
-template <> struct WavesPerSimd<32> { static constexpr int value = 6; };
-template <> struct WavesPerSimd<64> { static constexpr int value = 4; };
-template <> struct WavesPerSimd<96> { static constexpr int value = 3; };
-template <> struct WavesPerSimd<128> { static constexpr int value = 2; };
-template <> struct WavesPerSimd<160> { static constexpr int value = 2; };
-
-// kWide: Q/K/V may exceed 4 GiB, so gathers use 64-bit addresses.
-template <int D, bool kWide>
-__global__ __launch_bounds__(64)
-__attribute__((amdgpu_waves_per_eu(WavesPerSimd<D>::value, 8))) void k_fused3s(
-    const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
-    const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
-    const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
-    float *__restrict__ O, float *__restrict__ part_o,
-    float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
-    int32_t h0, int32_t nh, float sl2)
-{
-    constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
-    constexpr int NT = D / 16;  // 16-wide output tiles of the value product
-    // One LDS tile per wave, used twice per block pair with two row strides
-    // (halves).  K phase: D/2 + 4 dwords = 4 x odd, so the 16 rows read by a
-    // 16-lane pass start in 16 disjoint 4-bank ranges.  V phase: D/2 + 8
-    // dwords = 8 x odd, so the 8 rows of a transposed read start in disjoint
-    // 8-bank ranges.
-    constexpr int LSK = D + 8;
-    constexpr int LSV = D + 16;
-    __shared__ __attribute__((aligned(16))) _Float16 tile[32 * LSV];
-
-    const int lane = threadIdx.x;
-    const int i = lane & 15;  // query row (accumulators) / operand row index
-    const int g = lane >> 4;  // lane group: selects the reduction slots
-    // Workgroups walk the work list item-major, head-minor: the heads of one
-    // window run back to back and share its column lists and bitmaps.
-    const int item = blockIdx.x / nh, hl = blockIdx.x - item * nh;
-    const int head = h0 + hl;
-    const WorkItem it = items[item];
-    // Row r of head h starts at r * ld + h * D (elements) in Q, K, V and O.
-    Q += (int64_t)head * D;
-    K += (int64_t)head * D;
-    V += (int64_t)head * D;
-    O += (int64_t)head * D;
-    const int row = it.window * kWindowRows + i;
-    const int b0 = it.blk_begin, b1 = it.blk_end;
-
-    // Q_i: lane (i, g) holds Q[row][32c + 8g .. +7] for each chunk c.  Pad
-    // rows (>= N) of the last window read row N-1: their results are never
-    // written and rows do not interact, so any finite values do.
-    h8 q[NC];
-    {
-        const _Float16 *qp = Q + (int64_t)min(row, N - 1) * ld + 8 * g;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) q[c] = load16(qp + 32 * c);
-    }
-
-    f4 o[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) o[t] = f4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -__builtin_inff();
-    float l_run = 0.f;
-
-    // Pipeline state.  The 32 K rows and 32 V rows of a block pair are
-    // gathered "row-contiguous": the pair tile's 16-byte chunks are spread
-    // flat over the lanes (chunk f = lane + 64 j, row f / LPR, chunk f % LPR),
-    // so every 4-lane quad reads 64 contiguous bytes of ONE row; the texture
-    // addresser then spends one cycle per quad instead of four (an MFMA
-    // operand layout puts consecutive lanes on different rows).  The rows go
-    // through LDS: K rows are read back in the MFMA A layout, V rows with
-    // the transposed read.  Loads are unconditional: a padding slot (column
-    // -1) or the absent second block of an odd tail gathers a real column of
-    // the same block, whose bitmap bit is clear, so its probability is
-    // exactly 0 and it adds 0 * (finite V) = 0.
-    constexpr int LPR = D / 8;   // lanes (16-byte chunks) per row
-    constexpr int NI = D / 16;   // chunks per lane per tile
-    h8 kst[NI], vst[NI];         // staged K and V chunks of the pair in flight
-    uint32_t mwa = 0, mwb = 0;
-    int ncol = 0;                // lanes 0..31: raw column of slot `lane` of the next pair
-
-    // Raw column ids of pair (b, b+1): lane l (mod 32) takes slot l; block
-    // indices clamped so reads stay inside this item (values past its end
-    // are never used).
-    auto load_cols = [&](int b) {
-        const int slot = lane & 31;
-        const int blk = slot < 16 ? min(b, b1 - 1) : min(b + 1, b1 - 1);
-        ncol = cols[(int64_t)kBlockCols * blk + (slot & 15)];
-    };
-    // Issue the K, V and bitmap loads of pair (b, b+1).  Slots 0 and 16 are
-    // never padding (the first slot of a block); the wave is fully active
-    // here, so readlane sees them.
-    auto load_pair = [&](int b) {
-        const int f0 = __builtin_amdgcn_readlane(ncol, 0);
-        const int f1 = __builtin_amdgcn_readlane(ncol, 16);
-        const int c = ncol < 0 ? ((lane & 16) ? f1 : f0) : ncol;
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-            const int f = lane + 64 * j;
-            const int col = __shfl(c, f / LPR);
-            if constexpr (kWide) {
-                const int64_t off = (int64_t)col * ld + 8 * (f % LPR);
-                kst[j] = load16(K + off);
-                vst[j] = load16(V + off);
-            } else {
-                // byte offset < 2^32 (checked on the host): the load takes
-                // the uniform base from SGPRs and a 32-bit VGPR offset
-                const uint32_t off = (uint32_t)col * (uint32_t)(2 * ld) + 16u * (f % LPR);
-                kst[j] = load16_off(K, off);
-                vst[j] = load16_off(V, off);
-            }
-        }
-        mwa = mask[(int64_t)kMaskWords * b + (lane >> 3)];
-        mwb = mask[(int64_t)kMaskWords * min(b + 1, b1 - 1) + (lane >> 3)];
-    };
-
-    const int nib_shift = 4 * (lane & 7);
-    // One block pair: scores, mask, online softmax, value product.  With
-    // `prefetch`, the loads of the pair after it are issued as soon as this
-    // pair's staging registers are in LDS.
-    auto step = [&](int b, bool prefetch) {
-        // ---- K rows -> LDS (stride LSK), read back as MFMA A operands ----
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-            const int f = lane + 64 * j;
-            *reinterpret_cast<h8 *>(&tile[(f / LPR) * LSK + 8 * (f % LPR)]) = kst[j];
-        }
-        wave_lds_fence();
-        h8 ka[NC], kb[NC];
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            ka[c] = *reinterpret_cast<const h8 *>(&tile[i * LSK + 32 * c + 8 * g]);
-            kb[c] = *reinterpret_cast<const h8 *>(&tile[(16 + i) * LSK + 32 * c + 8 * g]);
-        }
-        // ---- scores of the two blocks (S^T: lane = row i, nbrs 4g+r) ----
-        f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            s0 = mfma16x16x32(ka[c], q[c], s0);
-            s1 = mfma16x16x32(kb[c], q[c], s1);
-        }
-        wave_lds_fence();
-        // ---- V rows -> the same LDS tile (stride LSV, slot = neighbour) ----
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-            const int f = lane + 64 * j;
-            *reinterpret_cast<h8 *>(&tile[(f / LPR) * LSV + 8 * (f % LPR)]) = vst[j];
-        }
-        const uint32_t nib0 = (mwa >> nib_shift) & 15u;
-        // (an odd tail's absent second block re-read block b: mask it off)
-        const uint32_t nib1 = b + 1 < b1 ? (mwb >> nib_shift) & 15u : 0u;
-        // ---- issue the next pair's loads (staging registers are free) ----
-        if (prefetch) {
-            load_pair(b + 2);
-            load_cols(b + 4);
-        }
-        // ---- mask + online softmax (base 2) ----
-        float x[8];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            x[r] = (nib0 >> r) & 1u ? s0[r] * sl2 : -__builtin_inff();
-            x[4 + r] = (nib1 >> r) & 1u ? s1[r] * sl2 : -__builtin_inff();
-        }
-        float mloc = x[0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mloc = fmaxf(mloc, x[e]);
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-        const float m_new = fmaxf(m_run, mloc);
-        const float m_ref = m_new == -__builtin_inff() ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
-        h8 p;
-        float psum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const _Float16 ph = (_Float16)__builtin_amdgcn_exp2f(x[e] - m_ref);
-            p[e] = ph;
-            psum += (float)ph;
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) o[t] *= alpha;
-        wave_lds_fence();
-        // ---- value product: A[m][slot] = V_hat[slot][16t + m] ----
-        // slot order of lane group g: 4g..4g+3 (block 0), 16+4g..+3 (block 1)
-        // -- the neighbours this lane's P values belong to.  Group lane s
-        // addresses row 4g + s/4, columns 16t + 4(s%4).., so the transposed
-        // read hands lane (m = i, g) the column 16t + m of rows 4g..4g+3.
-        const _Float16 *ta = tile + (4 * g + (i >> 2)) * LSV + 4 * (i & 3);
-        const _Float16 *tb = ta + 16 * LSV;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const h4 lo = lds_read_tr(ta + 16 * t);
-            const h4 hi = lds_read_tr(tb + 16 * t);
-            const h8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            o[t] = mfma16x16x32(a, p, o[t]);
-        }
-        wave_lds_fence();
-    };
-
-    if (b0 < b1) {
-        load_cols(b0);
-        load_pair(b0);
-        load_cols(b0 + 2);
-        int b = b0;
-        for (; b + 2 < b1; b += 2) step(b, true);
-        step(b, false);
-    }
-
-    // ---- finalise: full row sums, normalise, write (Algorithm 1 end) ----
-    float l_tot = l_run + __shfl_xor(l_run, 16);
-    l_tot += __shfl_xor(l_tot, 32);
-    if (it.slot < 0) {
-        if (row < N) {
-            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            float *op = O + (int64_t)row * ld + 4 * g;
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-                *reinterpret_cast<f4 *>(op + 16 * t) = o[t] * inv;
-            // natural-log log-sum-exp of the row's scaled scores
-            if (lse && g == 0)
-                lse[(int64_t)row * (ld / D) + head] =
-                    l_tot > 0.f ? kLn2 * (m_run + __log2f(l_tot)) : -__builtin_inff();
-        }
-    } else {
-        // partial slot of (piece, head): slot * nh + head offset
-        const int64_t ps = (int64_t)it.slot * nh + hl;
-        float *op = part_o + ps * kWindowRows * D + i * D + 4 * g;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) *reinterpret_cast<f4 *>(op + 16 * t) = o[t];
-        if (g == 0) {
-            part_ml[ps * 32 + i] = m_run;
-            part_ml[ps * 32 + 16 + i] = l_tot;
-        }
-    }
-}
-
-// Combines the pieces of one split window (fixed piece order, so the result
-// is deterministic): m = max m_p, l = sum 2^(m_p - m) l_p,
-// O = sum 2^(m_p - m) O_p / l.  16 threads per row, float4 columns; the
-// piece loops are unrolled so a thread keeps several loads in flight.
-template <int D>
-__global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merges,
-                                               const float *__restrict__ part_o,
-                                               const float *__restrict__ part_ml,
-                                               float *__restrict__ O,
-                                               float *__restrict__ lse, int32_t N,
-                                               int32_t ld, int32_t h0, int32_t nh)
-{
-    const int s = blockIdx.x / nh, hl = blockIdx.x - (blockIdx.x / nh) * nh;
-    const int w = merges[3 * s], first = merges[3 * s + 1], np = merges[3 * s + 2];
-    const int r = threadIdx.x >> 4, q = threadIdx.x & 15;
-    const int row = w * kWindowRows + r;
-    if (row >= N) return;
-    // partial slot of (piece k, head) = (first + k) * nh + hl
-    const float *ml = part_ml + ((int64_t)first * nh + hl) * 32;
-    const int64_t mstride = (int64_t)nh * 32;
-    float m = -__builtin_inff();
-#pragma unroll 4
-    for (int k = 0; k < np; ++k) m = fmaxf(m, ml[k * mstride + r]);
-    float l = 0.f;
-    if (m != -__builtin_inff()) {
-#pragma unroll 4
-        for (int k = 0; k < np; ++k)
-            l += __builtin_amdgcn_exp2f(ml[k * mstride + r] - m) * ml[k * mstride + 16 + r];
-    }
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    if (lse && q == 0)
-        lse[(int64_t)row * (ld / D) + h0 + hl] =
-            l > 0.f ? kLn2 * (m + __log2f(l)) : -__builtin_inff();
-    const float *po = part_o + ((int64_t)first * nh + hl) * kWindowRows * D + r * D;
-    const int64_t ostride = (int64_t)nh * kWindowRows * D;
-    float *orow = O + (int64_t)row * ld + (int64_t)(h0 + hl) * D;
-    for (int c4 = q; c4 < D / 4; c4 += 16) {
-        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
-        if (m != -__builtin_inff()) {
-#pragma unroll 4
-            for (int k = 0; k < np; ++k) {
-                const float sc = __builtin_amdgcn_exp2f(ml[k * mstride + r] - m);
-                acc += sc * *reinterpret_cast<const f4 *>(po + k * ostride + 4 * c4);
-            }
-        }
-        *reinterpret_cast<f4 *>(orow + 4 * c4) = acc * inv;
-    }
-}
-
-// Heads are launched in groups whose partial results fit the plan's scratch
-// (nh * D <= 256 floats per piece row); without split windows all heads go
-// in one launch.
-template <int D>
-hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
-                    const void *V, void *O, float *lse, int32_t H, float sl2,
-                    hipStream_t s)
-{
-    const int32_t ld = H * D;
-    const bool wide = (uint64_t)p.N * ld * 2 > 0xFFFFFFF0ull;
-    auto kern = wide ? k_fused3s<D, true> : k_fused3s<D, false>;
-    const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
-    for (int32_t h0 = 0; h0 < H; h0 += group) {
-        const int32_t nh = H - h0 < group ? H - h0 : group;
-        // the plan's partial buffers hold n_pieces * kMaxD / D head slots
-        if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
-        if (p.n_items > 0) {
-            const uint64_t grid = (uint64_t)p.n_items * nh;
-            if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-            kern<<<(unsigned)grid, 64, 0, s>>>(
-                p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
-                static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V),
-                static_cast<float *>(O), p.part_o, p.part_ml, lse, p.N, ld, h0, nh, sl2);
-            hipError_t e = hipGetLastError();
-            if (e != hipSuccess) return e;
-        }
-        if (p.n_split > 0) {
-            k_merge<D><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.part_o, p.part_ml,
-                                                     static_cast<float *>(O), lse, p.N, ld,
-                                                     h0, nh);
-            hipError_t e = hipGetLastError();
-            if (e != hipSuccess) return e;
-        }
-    }
-    return hipSuccess;
-}
-
-}  // namespace
 
 hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
-                        const void *V, void *O, float *lse, int32_t H, int32_t d,
-                        float sl2, hipStream_t s)
+                        const void *V, int in_type, void *O, bool out_f16, float *lse,
+                        int32_t H, int32_t d, float sl2, hipStream_t s)
 {
-    switch (d) {
-    case 32: return launch_d<32>(p, Q, K, V, O, lse, H, sl2, s);
-    case 64: return launch_d<64>(p, Q, K, V, O, lse, H, sl2, s);
-    case 96: return launch_d<96>(p, Q, K, V, O, lse, H, sl2, s);
-    case 128: return launch_d<128>(p, Q, K, V, O, lse, H, sl2, s);
-    case 160: return launch_d<160>(p, Q, K, V, O, lse, H, sl2, s);
-    case 192: return launch_d<192>(p, Q, K, V, O, lse, H, sl2, s);
-    case 224: return launch_d<224>(p, Q, K, V, O, lse, H, sl2, s);
-    case 256: return launch_d<256>(p, Q, K, V, O, lse, H, sl2, s);
-    default: return hipErrorInvalidValue;
-    }
+    if (in_type == kInBF16) return launch_fused_bf16(p, Q, K, V, O, out_f16, lse, H, d, sl2, s);
+    if (in_type != kInF16) return hipErrorInvalidValue;
+    return out_f16 ? launch_in<kInF16, true>(p, Q, K, V, O, lse, H, d, sl2, s)
+                   : launch_in<kInF16, false>(p, Q, K, V, O, lse, H, d, sl2, s);
 }
 
 }  // namespace f3s

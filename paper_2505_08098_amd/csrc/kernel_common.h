@@ -19,6 +19,14 @@ __device__ __forceinline__ f4 mfma16x16x32(h8 a, h8 b, f4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
+// The same product with bfloat16 operands (raw 16-bit patterns in h8).
+__device__ __forceinline__ f4 mfma16x16x32_bf16(h8 a, h8 b, f4 c)
+{
+    typedef __bf16 b8 __attribute__((ext_vector_type(8)));
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(b8, a),
+                                                   __builtin_bit_cast(b8, b), c, 0, 0, 0);
+}
+
 __device__ __forceinline__ h8 load16(const _Float16 *p)
 {
     return *reinterpret_cast<const h8 *>(p);

@@ -59,12 +59,22 @@ def csr_from_edges(N, src, dst, self_loops=True, symmetric=True):
     return row_ptr.astype(np.int32), cols
 
 
-def features(rng, N, d):
-    """Q, K, V: float32 N(0,1) rounded to fp16 (RNE)."""
+def features(rng, N, d, dtype="f16"):
+    """Q, K, V: float32 N(0,1) rounded (RNE) to fp16 (numpy float16 arrays)
+    or, with dtype="bf16", to bfloat16 (uint16 bit patterns)."""
     out = []
     for _ in range(3):
-        out.append(rng.standard_normal((N, d), dtype=np.float32).astype(np.float16))
+        x = rng.standard_normal((N, d), dtype=np.float32)
+        out.append(x.astype(np.float16) if dtype == "f16" else to_bf16_bits(x))
     return tuple(out)
+
+
+def to_bf16_bits(x):
+    """float32 array -> bfloat16 bit patterns (uint16), round to nearest even
+    (torch's CPU conversion)."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
 
 
 def erdos_renyi(rng, N=1024, avg_nbrs=15.0):
@@ -178,8 +188,9 @@ def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
                           self_loops=False, symmetric=False)
 
 
-def make_config(k, seed=0, with_features=True):
-    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V)."""
+def make_config(k, seed=0, with_features=True, dtype="f16"):
+    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V);
+    dtype "f16" (default) or "bf16" selects the feature storage type."""
     if k not in CONFIGS:
         raise ValueError(f"unknown workload {k}")
     cfg = CONFIGS[k]
@@ -199,7 +210,7 @@ def make_config(k, seed=0, with_features=True):
     out = dict(name=cfg["name"], N=N, d=d, scale=1.0 / math.sqrt(d),
                row_ptr=rp, col_idx=ci)
     if with_features:
-        out["Q"], out["K"], out["V"] = features(f, N, d)
+        out["Q"], out["K"], out["V"] = features(f, N, d, dtype)
     return out
 
 
