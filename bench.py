@@ -180,7 +180,7 @@ def main():
                     help="rows of the workload in the oracle baseline sample")
     ap.add_argument("--backward", action="store_true",
                     help="time f3s_backward (dQ, dK, dV) instead of the forward call")
-    ap.add_argument("--in-dtype", default="f16", choices=["f16", "bf16"],
+    ap.add_argument("--in-dtype", default="f16", choices=["f16", "bf16", "fp8"],
                     help="storage type of Q, K, V (bf16: f3s_forward_typed)")
     ap.add_argument("--out-dtype", default="f32", choices=["f32", "f16"],
                     help="type of O (f16: f3s_forward_typed)")
@@ -211,14 +211,16 @@ def main():
         rng = np.random.default_rng(np.random.SeedSequence(args.seed).spawn(3)[2])
         for key in ("Q", "K", "V"):
             x = rng.standard_normal((N, H, d), dtype=np.float32)
-            c[key] = x.astype(np.float16) if args.in_dtype == "f16" else W.to_bf16_bits(x)
+            c[key] = {"f16": lambda a: a.astype(np.float16), "bf16": W.to_bf16_bits,
+                      "fp8": W.to_e4m3_bits}[args.in_dtype](x)
     rp = torch.from_numpy(c["row_ptr"]).to(dev)
     ci = torch.from_numpy(c["col_idx"]).to(dev)
 
     def to_dev(a):
-        t = torch.from_numpy(a)
-        return t.to(dev) if args.in_dtype == "f16" else t.view(torch.int16).to(dev).view(
-            torch.bfloat16)
+        t = torch.from_numpy(a).to(dev)
+        if args.in_dtype == "bf16":
+            return t.view(torch.int16).view(torch.bfloat16)
+        return t.view(torch.float8_e4m3fn) if args.in_dtype == "fp8" else t
 
     Q, K, V = to_dev(c["Q"]), to_dev(c["K"]), to_dev(c["V"])
     out_dt = torch.float32 if args.out_dtype == "f32" else torch.float16
@@ -257,7 +259,8 @@ def main():
 
     flops_eff = 4.0 * info["nnz"] * d * H
     value = flops_eff / (ms * 1e-3) / 1e9
-    alg_bytes = algorithmic_bytes(info, d, H, 2, 4 if args.out_dtype == "f32" else 2)
+    alg_bytes = algorithmic_bytes(info, d, H, 1 if args.in_dtype == "fp8" else 2,
+                                  4 if args.out_dtype == "f32" else 2)
     achieved = alg_bytes / (ms * 1e-3) / 1e9
     issued = 1024.0 * d * H * info["n_blocks"]  # MFMA flops incl. zero padding
     traffic = traffic_from_counters(d) if H == 1 and not typed else None

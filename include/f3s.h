@@ -123,17 +123,22 @@ f3s_status_t f3s_forward(f3s_plan_t plan, const void *Q, const void *K, const vo
 typedef enum {
     F3S_DTYPE_F16 = 0,   /* IEEE 754 binary16 */
     F3S_DTYPE_BF16 = 1,  /* bfloat16: the upper 16 bits of an IEEE binary32 */
-    F3S_DTYPE_F32 = 2    /* IEEE 754 binary32 */
+    F3S_DTYPE_F32 = 2,   /* IEEE 754 binary32 */
+    F3S_DTYPE_FP8_E4M3 = 3  /* OCP 8-bit float e4m3 (bias 7, finite to 448, no inf) */
 } f3s_dtype_t;
 
 /*
  * Forward with a choice of storage types (the precision variants beside
  * Table 5's scheme).
- *   in_dtype   type of Q, K, V: F3S_DTYPE_F16 (Table 5) or F3S_DTYPE_BF16.
- *              With bf16 inputs the scores use the bf16 matrix product and
- *              the probabilities enter the value product as two bf16 terms
- *              (about 16 significant bits), so the error stays within the
- *              fp16 scheme's bound.
+ *   in_dtype   type of Q, K, V: F3S_DTYPE_F16 (Table 5), F3S_DTYPE_BF16 or
+ *              F3S_DTYPE_FP8_E4M3 (the 8-bit inputs the paper's future work
+ *              names).  With bf16 inputs the scores use the bf16 matrix
+ *              product and the probabilities enter the value product as two
+ *              bf16 terms (about 16 significant bits), so the error stays
+ *              within the fp16 scheme's bound.  fp8 inputs are widened to
+ *              fp16 exactly as they are loaded and then follow the fp16
+ *              scheme; any per-tensor dequantisation factor of Q and K folds
+ *              into `scale`, and one of V multiplies O afterwards.
  *   out_dtype  type of O: F3S_DTYPE_F32 (Table 5) or F3S_DTYPE_F16 (the
  *              normalised fp32 result rounded to nearest even).
  * Other types give F3S_ERR_UNSUPPORTED.  Layouts, alignment, d, scale, lse

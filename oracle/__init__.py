@@ -17,6 +17,8 @@ Functions and the passages they follow:
 * :func:`attention_bf16_f64` -- the same definition on bfloat16 inputs
   (exact widening with the oracle's own bfloat16 decoder; the precision
   variant beside Table 5's fp16 scheme).
+* :func:`attention_e4m3_f64` -- the same on 8-bit float (OCP e4m3) inputs,
+  the low-precision inputs the paper's future work names.
 * :func:`attention_bwd_f64` -- gradients of the operator (the backward pass
   the paper names as the next step): softmax Jacobian applied to dO V^T on
   the pattern, then the two products back through K and Q, and P^T dO.
@@ -53,6 +55,10 @@ def lib():
         L.oracle_bf16_to_double.restype = dbl
         L.oracle_widen_bf16.argtypes = [ctypes.c_int64, vp, vp]
         L.oracle_widen_bf16.restype = None
+        L.oracle_e4m3_to_double.argtypes = [ctypes.c_uint8]
+        L.oracle_e4m3_to_double.restype = dbl
+        L.oracle_widen_e4m3.argtypes = [ctypes.c_int64, vp, vp]
+        L.oracle_widen_e4m3.restype = None
         L.oracle_check_csr.argtypes = [i32, vp, vp]
         L.oracle_check_csr.restype = ctypes.c_int
         L.oracle_3s_f64.argtypes = [i32, vp, vp, i32, vp, vp, vp, dbl, vp, vp, vp, i32]
@@ -121,6 +127,28 @@ def attention_bf16_f64(row_ptr, col_idx, Q, K, V, scale, want_lse=False):
     inputs are widened exactly and the fp64 definition is applied."""
     return attention_f64_exact(row_ptr, col_idx, widen_bf16(Q), widen_bf16(K),
                                widen_bf16(V), scale, want_lse=want_lse)
+
+
+def e4m3_to_double(bits):
+    """Decode one OCP e4m3 byte with the oracle's own decoder."""
+    return lib().oracle_e4m3_to_double(int(bits) & 0xFF)
+
+
+def widen_e4m3(bits):
+    """OCP e4m3 bytes (uint8 array) -> float64, exactly."""
+    a = np.ascontiguousarray(bits)
+    if a.dtype != np.uint8:
+        raise TypeError("expected e4m3 bytes as uint8")
+    out = np.empty(a.shape, dtype=np.float64)
+    lib().oracle_widen_e4m3(a.size, _ptr(a), _ptr(out))
+    return out
+
+
+def attention_e4m3_f64(row_ptr, col_idx, Q, K, V, scale, want_lse=False):
+    """The operator on fp8 e4m3 inputs (uint8 bytes), in fp64: exact
+    widening, then the fp64 definition."""
+    return attention_f64_exact(row_ptr, col_idx, widen_e4m3(Q), widen_e4m3(K),
+                               widen_e4m3(V), scale, want_lse=want_lse)
 
 
 def check_csr(row_ptr, col_idx, N):

@@ -87,6 +87,35 @@ void oracle_widen_bf16(int64_t count, const uint16_t *h, double *out)
     for (int64_t k = 0; k < count; ++k) out[k] = bf16_bits_to_double(h[k]);
 }
 
+/* ---------------------------------------------------------------------- */
+/* OCP 8-bit float e4m3 -> double, from the format definition: 1 sign bit, */
+/* 4 exponent bits (bias 7), 3 fraction bits; no infinities, the all-ones  */
+/* exponent with all-ones fraction is NaN.  Exact in double.               */
+/* ---------------------------------------------------------------------- */
+static double e4m3_bits_to_double(uint8_t b)
+{
+    int sign = (b >> 7) & 1;
+    int expo = (b >> 3) & 0xf;
+    int frac = b & 0x7;
+    double v;
+    if (expo == 0) {
+        v = ldexp((double)frac, -9);             /* subnormal: frac * 2^-9 */
+    } else if (expo == 15 && frac == 7) {
+        v = NAN;
+    } else {
+        v = ldexp((double)(frac + 8), expo - 10); /* (1 + f/8) 2^(e-7) */
+    }
+    return sign ? -v : v;
+}
+
+double oracle_e4m3_to_double(uint8_t b) { return e4m3_bits_to_double(b); }
+
+/* count e4m3 bytes -> fp64 (exact). */
+void oracle_widen_e4m3(int64_t count, const uint8_t *b, double *out)
+{
+    for (int64_t k = 0; k < count; ++k) out[k] = e4m3_bits_to_double(b[k]);
+}
+
 /* Decoding table: entry h is half_bits_to_double(h) (filled once). */
 static double g_half_table[65536];
 static int g_half_table_ready = 0;

@@ -269,18 +269,19 @@ def forward(plan, Q, K, V, scale=None, out=None, lse=None, stream=None):
 
 
 # f3s_dtype_t codes
-_DTYPE_CODE = {torch.float16: 0, torch.bfloat16: 1, torch.float32: 2}
+_DTYPE_CODE = {torch.float16: 0, torch.bfloat16: 1, torch.float32: 2,
+               torch.float8_e4m3fn: 3}
 
 
 def forward_typed(plan, Q, K, V, out_dtype=torch.float32, scale=None, out=None,
                   lse=None, want_lse=False, stream=None):
-    """f3s_forward_typed: Q, K, V fp16 or bf16 ([N, d] or [N, H, d]); O of
-    ``out_dtype`` (fp32 or fp16).  Returns (O, lse) with lse None unless
-    ``want_lse`` or an ``lse`` tensor is given."""
+    """f3s_forward_typed: Q, K, V fp16, bf16 or float8_e4m3fn ([N, d] or
+    [N, H, d]); O of ``out_dtype`` (fp32 or fp16).  Returns (O, lse) with lse
+    None unless ``want_lse`` or an ``lse`` tensor is given."""
     shape = tuple(Q.shape)
     H = shape[1] if len(shape) == 3 else 1
-    if Q.dtype not in (torch.float16, torch.bfloat16):
-        raise TypeError(f"Q must be float16 or bfloat16, got {Q.dtype}")
+    if Q.dtype not in (torch.float16, torch.bfloat16, torch.float8_e4m3fn):
+        raise TypeError(f"Q must be float16, bfloat16 or float8_e4m3fn, got {Q.dtype}")
     for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
         _check_device_tensor(t, n, Q.dtype)
         if tuple(t.shape) != shape or shape[0] != plan.N:

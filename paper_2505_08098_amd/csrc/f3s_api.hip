@@ -420,7 +420,8 @@ f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const
 {
     if (!p || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
-    if (in_dtype != F3S_DTYPE_F16 && in_dtype != F3S_DTYPE_BF16)
+    if (in_dtype != F3S_DTYPE_F16 && in_dtype != F3S_DTYPE_BF16 &&
+        in_dtype != F3S_DTYPE_FP8_E4M3)
         return fail(F3S_ERR_UNSUPPORTED);
     if (out_dtype != F3S_DTYPE_F32 && out_dtype != F3S_DTYPE_F16)
         return fail(F3S_ERR_UNSUPPORTED);
@@ -432,7 +433,7 @@ f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const
     if ((uint64_t)p->n_items * (uint64_t)n_heads > 0x7FFFFFFFull)
         return fail(F3S_ERR_UNSUPPORTED);
     const size_t elems = (size_t)p->N * (size_t)n_heads * (size_t)d;
-    const size_t in_bytes = elems * 2;
+    const size_t in_bytes = elems * (in_dtype == F3S_DTYPE_FP8_E4M3 ? 1 : 2);
     const size_t out_bytes = elems * (out_dtype == F3S_DTYPE_F32 ? 4 : 2);
     if (overlaps(O, out_bytes, Q, in_bytes) || overlaps(O, out_bytes, K, in_bytes) ||
         overlaps(O, out_bytes, V, in_bytes))
@@ -445,7 +446,9 @@ f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const
                 overlaps(lse, (size_t)p->N * n_heads * 4, K, in_bytes) ||
                 overlaps(lse, (size_t)p->N * n_heads * 4, V, in_bytes)))
         return fail(F3S_ERR_INVALID_VALUE);
-    const int in_type = in_dtype == F3S_DTYPE_BF16 ? f3s::kInBF16 : f3s::kInF16;
+    const int in_type = in_dtype == F3S_DTYPE_BF16       ? f3s::kInBF16
+                        : in_dtype == F3S_DTYPE_FP8_E4M3 ? f3s::kInFP8
+                                                         : f3s::kInF16;
     f3s_status_t st = from_hip(f3s::launch_fused(*p, Q, K, V, in_type, O,
                                                  out_dtype == F3S_DTYPE_F16, lse, n_heads, d,
                                                  sl2, stream));

@@ -16,6 +16,7 @@ constexpr int kMaxD = 256;        // largest supported feature dimension
 // Storage type of Q, K, V in the forward kernels.
 constexpr int kInF16 = 0;
 constexpr int kInBF16 = 1;
+constexpr int kInFP8 = 2;     // OCP e4m3 (finite values up to 448)
 
 // One unit of work for the fused kernel: a whole row window or one piece of
 // a split window.  Blocks are absolute indices into the plan's block arrays.
@@ -117,13 +118,16 @@ hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s
 // ---- fused operator (fused3s.hip) ---------------------------------------
 // H heads of size d; Q, K, V, O rows hold the heads back to back (stride H*d).
 // lse (may be null): [N, H] natural-log log-sum-exp of each row's scores.
-// in_type: kInF16 or kInBF16; out_f16: O is fp16 instead of fp32.
+// in_type: kInF16, kInBF16 or kInFP8; out_f16: O is fp16 instead of fp32.
 hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
                         const void *V, int in_type, void *O, bool out_f16, float *lse,
                         int32_t H, int32_t d, float scale_log2, hipStream_t s);
 hipError_t launch_fused_bf16(const f3s_plan_s &p, const void *Q, const void *K,
                              const void *V, void *O, bool out_f16, float *lse, int32_t H,
                              int32_t d, float scale_log2, hipStream_t s);
+hipError_t launch_fused_fp8(const f3s_plan_s &p, const void *Q, const void *K,
+                            const void *V, void *O, bool out_f16, float *lse, int32_t H,
+                            int32_t d, float scale_log2, hipStream_t s);
 
 // Gradients (see backward.hip).  pt is the plan of the transposed pattern.
 hipError_t launch_backward(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q,

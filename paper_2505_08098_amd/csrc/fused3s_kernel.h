@@ -1,7 +1,8 @@
 // Fused 3S kernel for CDNA4 (gfx950): Algorithm 1 of Fused3S with the
 // tensor-core tiling re-derived for 64-wide wavefronts and the 16x16x32
 // matrix instructions.  Included by one source file per input storage type
-// (fused3s.hip: fp16, fused3s_bf16.hip: bfloat16), each instantiating the
+// (fused3s.hip: fp16, fused3s_bf16.hip: bfloat16, fused3s_fp8.hip: fp8
+// e4m3), each instantiating the
 // templates for every feature size.
 //
 // One wavefront owns one work item (a 16-row window, or a piece of one) and
@@ -79,6 +80,47 @@ __device__ __forceinline__ f4 mma_in(h8 a, h8 b, f4 c)
         return mfma16x16x32(a, b, c);
 }
 
+// Bytes per stored element of Q, K, V.
+template <int kIn> constexpr int elem_bytes() { return kIn == kInFP8 ? 1 : 2; }
+
+// 16 stored bytes (8 fp16/bf16 elements, or 16 fp8 e4m3 elements) -> the
+// compute type: unchanged for 16-bit storage; for fp8 the two fp16 halves
+// (e4m3 -> fp16 is exact).
+__device__ __forceinline__ void widen_fp8x16(h8 raw, h8 &lo, h8 &hi)
+{
+    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+    const u4 w = __builtin_bit_cast(u4, raw);
+    h8 out[2];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const h2 a = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w[k], 1.0f, false);
+        const h2 b = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w[k], 1.0f, true);
+        out[k >> 1][4 * (k & 1) + 0] = a[0];
+        out[k >> 1][4 * (k & 1) + 1] = a[1];
+        out[k >> 1][4 * (k & 1) + 2] = b[0];
+        out[k >> 1][4 * (k & 1) + 3] = b[1];
+    }
+    lo = out[0];
+    hi = out[1];
+}
+
+// 8 stored fp8 bytes -> 8 fp16.
+__device__ __forceinline__ h8 widen_fp8x8(uint64_t raw)
+{
+    h8 r;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const uint32_t w = (uint32_t)(raw >> (32 * k));
+        const h2 a = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, false);
+        const h2 b = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, true);
+        r[4 * k + 0] = a[0];
+        r[4 * k + 1] = a[1];
+        r[4 * k + 2] = b[0];
+        r[4 * k + 3] = b[1];
+    }
+    return r;
+}
+
 // Four fp32 results -> the output type at p (16-byte or 8-byte store).
 template <bool kOutH>
 __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
@@ -93,15 +135,16 @@ __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
     }
 }
 
-// kIn: storage type of Q, K, V (kInF16 or kInBF16; 16-bit raw bits either
-// way).  kOutH: O is fp16 instead of fp32.  kWide: Q/K/V may exceed 4 GiB,
-// so gathers use 64-bit addresses.
+// kIn: storage type of Q, K, V (kInF16, kInBF16: 16-bit raw bits; kInFP8:
+// e4m3 bytes, widened to fp16 on the way into registers / LDS, so the
+// products are the fp16 ones).  kOutH: O is fp16 instead of fp32.  kWide:
+// Q/K/V may exceed 4 GiB, so gathers use 64-bit addresses.
 template <int D, bool kWide, int kIn, bool kOutH>
 __global__ __launch_bounds__(64)
 __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
-    const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
-    const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
+    const uint32_t *__restrict__ mask, const void *__restrict__ Qv,
+    const void *__restrict__ Kv, const void *__restrict__ Vv,
     void *__restrict__ O, float *__restrict__ part_o,
     float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
     int32_t h0, int32_t nh, float sl2)
@@ -126,9 +169,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     const int head = h0 + hl;
     const WorkItem it = items[item];
     // Row r of head h starts at r * ld + h * D (elements) in Q, K, V and O.
-    Q += (int64_t)head * D;
-    K += (int64_t)head * D;
-    V += (int64_t)head * D;
+    constexpr int EB = elem_bytes<kIn>();
+    const char *Q = static_cast<const char *>(Qv) + (int64_t)head * D * EB;
+    const char *K = static_cast<const char *>(Kv) + (int64_t)head * D * EB;
+    const char *V = static_cast<const char *>(Vv) + (int64_t)head * D * EB;
     const int64_t ohead = (int64_t)head * D;
     const int row = it.window * kWindowRows + i;
     const int b0 = it.blk_begin, b1 = it.blk_end;
@@ -138,9 +182,14 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     // written and rows do not interact, so any finite values do.
     h8 q[NC];
     {
-        const _Float16 *qp = Q + (int64_t)min(row, N - 1) * ld + 8 * g;
+        const char *qp = Q + ((int64_t)min(row, N - 1) * ld + 8 * g) * EB;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) q[c] = load16(qp + 32 * c);
+        for (int c = 0; c < NC; ++c) {
+            if constexpr (EB == 1)
+                q[c] = widen_fp8x8(*reinterpret_cast<const uint64_t *>(qp + 32 * c));
+            else
+                q[c] = *reinterpret_cast<const h8 *>(qp + 64 * c);
+        }
     }
 
     f4 o[NT];
@@ -160,9 +209,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     // -1) or the absent second block of an odd tail gathers a real column of
     // the same block, whose bitmap bit is clear, so its probability is
     // exactly 0 and it adds 0 * (finite V) = 0.
-    constexpr int LPR = D / 8;   // lanes (16-byte chunks) per row
-    constexpr int NI = D / 16;   // chunks per lane per tile
-    h8 kst[NI], vst[NI];         // staged K and V chunks of the pair in flight
+    constexpr int LPR = D * EB / 16;  // lanes (16-byte chunks) per row
+    constexpr int NI = D * EB / 32;   // chunks per lane per tile
+    constexpr int CE = 16 / EB;       // elements per chunk
+    h8 kst[NI], vst[NI];              // staged K and V chunks of the pair in flight
     uint32_t mwa = 0, mwb = 0;
     int ncol = 0;                // lanes 0..31: raw column of slot `lane` of the next pair
 
@@ -186,15 +236,15 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
             const int f = lane + 64 * j;
             const int col = __shfl(c, f / LPR);
             if constexpr (kWide) {
-                const int64_t off = (int64_t)col * ld + 8 * (f % LPR);
-                kst[j] = load16(K + off);
-                vst[j] = load16(V + off);
+                const int64_t off = (int64_t)col * ld * EB + 16 * (f % LPR);
+                kst[j] = *reinterpret_cast<const h8 *>(K + off);
+                vst[j] = *reinterpret_cast<const h8 *>(V + off);
             } else {
                 // byte offset < 2^32 (checked on the host): the load takes
                 // the uniform base from SGPRs and a 32-bit VGPR offset
-                const uint32_t off = (uint32_t)col * (uint32_t)(2 * ld) + 16u * (f % LPR);
-                kst[j] = load16_off(K, off);
-                vst[j] = load16_off(V, off);
+                const uint32_t off = (uint32_t)col * (uint32_t)(EB * ld) + 16u * (f % LPR);
+                kst[j] = load16_off(reinterpret_cast<const _Float16 *>(K), off);
+                vst[j] = load16_off(reinterpret_cast<const _Float16 *>(V), off);
             }
         }
         mwa = mask[(int64_t)kMaskWords * b + (lane >> 3)];
@@ -210,7 +260,15 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int f = lane + 64 * j;
-            *reinterpret_cast<h8 *>(&tile[(f / LPR) * LSK + 8 * (f % LPR)]) = kst[j];
+            _Float16 *dst = &tile[(f / LPR) * LSK + CE * (f % LPR)];
+            if constexpr (EB == 1) {
+                h8 lo, hi;
+                widen_fp8x16(kst[j], lo, hi);
+                *reinterpret_cast<h8 *>(dst) = lo;
+                *reinterpret_cast<h8 *>(dst + 8) = hi;
+            } else {
+                *reinterpret_cast<h8 *>(dst) = kst[j];
+            }
         }
         wave_lds_fence();
         h8 ka[NC], kb[NC];
@@ -231,7 +289,15 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int f = lane + 64 * j;
-            *reinterpret_cast<h8 *>(&tile[(f / LPR) * LSV + 8 * (f % LPR)]) = vst[j];
+            _Float16 *dst = &tile[(f / LPR) * LSV + CE * (f % LPR)];
+            if constexpr (EB == 1) {
+                h8 lo, hi;
+                widen_fp8x16(vst[j], lo, hi);
+                *reinterpret_cast<h8 *>(dst) = lo;
+                *reinterpret_cast<h8 *>(dst + 8) = hi;
+            } else {
+                *reinterpret_cast<h8 *>(dst) = vst[j];
+            }
         }
         const uint32_t nib0 = (mwa >> nib_shift) & 15u;
         // (an odd tail's absent second block re-read block b: mask it off)
@@ -399,7 +465,7 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                     hipStream_t s)
 {
     const int32_t ld = H * D;
-    const bool wide = (uint64_t)p.N * ld * 2 > 0xFFFFFFF0ull;
+    const bool wide = (uint64_t)p.N * ld * elem_bytes<kIn>() > 0xFFFFFFF0ull;
     auto kern = wide ? k_fused3s<D, true, kIn, kOutH> : k_fused3s<D, false, kIn, kOutH>;
     const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
     for (int32_t h0 = 0; h0 < H; h0 += group) {
@@ -409,10 +475,9 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
         if (p.n_items > 0) {
             const uint64_t grid = (uint64_t)p.n_items * nh;
             if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
-            kern<<<(unsigned)grid, 64, 0, s>>>(
-                p.items, p.cols, p.mask, static_cast<const _Float16 *>(Q),
-                static_cast<const _Float16 *>(K), static_cast<const _Float16 *>(V), O,
-                p.part_o, p.part_ml, lse, p.N, ld, h0, nh, sl2);
+            kern<<<(unsigned)grid, 64, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
+                                               p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
+                                               sl2);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }

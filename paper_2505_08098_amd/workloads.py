@@ -60,13 +60,27 @@ def csr_from_edges(N, src, dst, self_loops=True, symmetric=True):
 
 
 def features(rng, N, d, dtype="f16"):
-    """Q, K, V: float32 N(0,1) rounded (RNE) to fp16 (numpy float16 arrays)
-    or, with dtype="bf16", to bfloat16 (uint16 bit patterns)."""
+    """Q, K, V: float32 N(0,1) rounded (RNE) to fp16 (numpy float16 arrays),
+    with dtype="bf16" to bfloat16 (uint16 bit patterns), with dtype="fp8" to
+    OCP e4m3 (uint8 bytes)."""
     out = []
     for _ in range(3):
         x = rng.standard_normal((N, d), dtype=np.float32)
-        out.append(x.astype(np.float16) if dtype == "f16" else to_bf16_bits(x))
+        if dtype == "f16":
+            out.append(x.astype(np.float16))
+        elif dtype == "bf16":
+            out.append(to_bf16_bits(x))
+        else:
+            out.append(to_e4m3_bits(x))
     return tuple(out)
+
+
+def to_e4m3_bits(x):
+    """float32 array -> OCP e4m3 bytes (uint8), round to nearest even
+    (torch's CPU conversion; |x| must stay below 464)."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float8_e4m3fn)
+    return t.view(torch.uint8).numpy()
 
 
 def to_bf16_bits(x):
@@ -190,7 +204,7 @@ def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
 
 def make_config(k, seed=0, with_features=True, dtype="f16"):
     """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V);
-    dtype "f16" (default) or "bf16" selects the feature storage type."""
+    dtype "f16" (default), "bf16" or "fp8" selects the feature storage type."""
     if k not in CONFIGS:
         raise ValueError(f"unknown workload {k}")
     cfg = CONFIGS[k]

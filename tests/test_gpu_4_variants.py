@@ -1,5 +1,5 @@
-"""Precision variants of the forward (bfloat16 inputs, fp16 output) on the
-GPU against the fp64 oracle.
+"""Precision variants of the forward (bfloat16 and fp8 e4m3 inputs, fp16
+output) on the GPU against the fp64 oracle.
 
 Tolerances.  fp16 output adds one rounding of O (half an ulp: at most
 2^-11 |O| relative) to the fp16 scheme's error, which stays inside the same
@@ -9,7 +9,9 @@ probability error is <= 2^-11 * max|V| ~ 2.8e-3 and the output rounding
 bfloat16 inputs the probabilities carry ~16 significant bits (two bf16
 terms), so the error is fp32 accumulation only; the test asserts a relative
 Frobenius error below 1e-4, ten times under the bar, which a single bf16
-probability term (8 bits, ~2e-3) could not meet.
+probability term (8 bits, ~2e-3) could not meet.  fp8 (e4m3) inputs are
+widened to fp16 exactly before any product, so the fp16 scheme's bar applies
+unchanged and the fp8 result equals the fp16 kernel's on the widened values.
 """
 import ctypes
 import math
@@ -170,10 +172,67 @@ def test_typed_argument_errors(gpu):
     L = gpu.load_library()
     s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     O = torch.empty((c["N"], 64), dtype=torch.float32, device=DEV)
-    for ind, outd in ((2, 2), (7, 2), (0, 1), (0, 9), (-1, 2)):
+    for ind, outd in ((2, 2), (7, 2), (0, 1), (0, 9), (-1, 2), (3, 3), (0, 3)):
         assert L.f3s_forward_typed(plan.handle, q.data_ptr(), q.data_ptr(), q.data_ptr(),
                                    ind, O.data_ptr(), outd, None, 1, 64, 0.1, s) == 3
     with pytest.raises(gpu.F3SError) as e:
         gpu.forward_typed(plan, q, q, q, out_dtype=torch.bfloat16)
     assert e.value.code == 3
     torch.cuda.synchronize()
+
+
+def _fp8_dev(bits):
+    return _dev(bits).view(torch.float8_e4m3fn)
+
+
+@pytest.mark.parametrize("k", [1, 2, 4, 5])
+def test_fp8_inputs_workloads(gpu, oracle, k):
+    c = W.make_config(k, dtype="fp8")
+    print(f"workload {k} fp8 N={c['N']} d={c['d']}", flush=True)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    q, kk, v = (_fp8_dev(c[x]) for x in ("Q", "K", "V"))
+    O, lse = gpu.forward_typed(plan, q, kk, v, scale=c["scale"], want_lse=True)
+    torch.cuda.synchronize()
+    ref, reflse = oracle.attention_e4m3_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"],
+                                            c["V"], c["scale"], want_lse=True)
+    _check(O.cpu().numpy(), ref)
+    assert np.abs(lse.cpu().numpy() - reflse).max() < 2e-3
+
+
+@pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
+def test_fp8_equals_f16_on_widened_inputs(gpu, oracle, d):
+    """e4m3 -> fp16 is exact and the fp8 kernel widens before any product,
+    so its output must equal the fp16 kernel's on the widened inputs bit for
+    bit (fp32 and fp16 outputs, split windows included)."""
+    rng = np.random.default_rng(300 + d)
+    N = 333
+    rp, ci = W.random_csr(rng, N, max_deg=90, empty_frac=0.05, dup_frac=0.1)
+    X = [W.to_e4m3_bits(2 * rng.standard_normal((N, d), dtype=np.float32)) for _ in range(3)]
+    H = [oracle.widen_e4m3(x).astype(np.float16) for x in X]
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    for out_dtype in (torch.float32, torch.float16):
+        a, la = gpu.forward_typed(plan, *(_fp8_dev(x) for x in X), out_dtype=out_dtype,
+                                  scale=1 / math.sqrt(d), want_lse=True)
+        b, lb = gpu.forward_typed(plan, *(_dev(h) for h in H), out_dtype=out_dtype,
+                                  scale=1 / math.sqrt(d), want_lse=True)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b) and torch.equal(la, lb)
+    ref = oracle.attention_e4m3_f64(rp, ci, *X, 1 / math.sqrt(d))
+    _check(a.float().cpu().numpy(), ref)
+
+
+def test_fp8_multi_head_split_windows(gpu, oracle, monkeypatch):
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
+    c = W.make_config(2, with_features=False)
+    N, H, d = c["N"], 3, 64
+    rng = np.random.default_rng(31)
+    X = [W.to_e4m3_bits(rng.standard_normal((N, H, d), dtype=np.float32)) for _ in range(3)]
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), N)
+    assert plan.info["n_split"] > 0
+    O, _ = gpu.forward_typed(plan, *(_fp8_dev(x) for x in X), scale=0.125)
+    torch.cuda.synchronize()
+    O = O.cpu().numpy()
+    for h in range(H):
+        ref = oracle.attention_e4m3_f64(c["row_ptr"], c["col_idx"],
+                                        *(np.ascontiguousarray(x[:, h]) for x in X), 0.125)
+        _check(O[:, h], ref)

@@ -1,10 +1,13 @@
-"""Pins for the oracle's bfloat16 entry (CPU only).
+"""Pins for the oracle's bfloat16 and fp8 (e4m3) entries (CPU only).
 
 bfloat16 is the upper half of an IEEE binary32, so its decoder is checked
 against torch's bfloat16 -> float64 conversion (a library routine) on all
 65,536 bit patterns; the operator on bfloat16 inputs is checked against the
 binary16 entry on inputs that both formats represent exactly (the two
-entries then see identical values and must agree to rounding of fp64)."""
+entries then see identical values and must agree to rounding of fp64).  The
+e4m3 decoder is checked against torch.float8_e4m3fn on all 256 codes, and
+since every finite e4m3 value is exact in binary16 the fp8 entry must agree
+with the binary16 entry on the widened values."""
 import numpy as np
 import torch
 
@@ -49,3 +52,31 @@ def test_bf16_generator_rounds_to_nearest_even():
     # ties go to the even neighbour: 1 + 2^-8 -> 1, 1 + 3*2^-8 -> 1 + 2^-6
     assert b[0] == 0x3F80 and b[1] == 0x3F80 and b[2] == 0x3F82
     assert b[3] == 0xFF62 and b[4] != 0
+
+
+def test_e4m3_decoder_matches_torch_on_every_byte(oracle):
+    """OCP e4m3 (torch.float8_e4m3fn, a library routine) on all 256 codes."""
+    b = np.arange(256, dtype=np.uint8)
+    got = oracle.widen_e4m3(b)
+    ref = torch.from_numpy(b).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert nan.sum() == 2 and np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert oracle.e4m3_to_double(0x7E) == 448.0 and oracle.e4m3_to_double(0x01) == 2.0 ** -9
+
+
+def test_e4m3_entry_equals_f16_entry(oracle):
+    """Every finite e4m3 value is exact in binary16, so the fp8 entry must
+    agree with the fp16 entry on the same values, for any inputs."""
+    rng = np.random.default_rng(22)
+    N, d = 80, 32
+    rp, ci = W.random_csr(rng, N, max_deg=25, empty_frac=0.1, dup_frac=0.2)
+    X = [W.to_e4m3_bits(3 * rng.standard_normal((N, d), dtype=np.float32)) for _ in range(3)]
+    H = [oracle.widen_e4m3(x).astype(np.float16) for x in X]
+    for x, h in zip(X, H):
+        assert np.array_equal(h.astype(np.float64), oracle.widen_e4m3(x))
+    O1, l1 = oracle.attention_f64(rp, ci, *H, 0.4, want_lse=True)
+    O2, l2 = oracle.attention_e4m3_f64(rp, ci, *X, 0.4, want_lse=True)
+    np.testing.assert_allclose(O2, O1, rtol=0, atol=1e-13)
+    fin = np.isfinite(l1)
+    np.testing.assert_allclose(l2[fin], l1[fin], rtol=0, atol=1e-13)
