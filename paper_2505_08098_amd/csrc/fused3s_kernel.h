@@ -79,6 +79,8 @@ __device__ __forceinline__ f4 mma_in(h8 a, h8 b, f4 c)
         return mfma16x16x32(a, b, c);
 }
 
+template <bool B> struct Tag { static constexpr bool value = B; };
+
 // Bytes per stored element of Q, K, V.
 template <int kIn> constexpr int elem_bytes() { return kIn == kInFP8 ? 1 : 2; }
 
@@ -178,31 +180,54 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     const char *Kb = static_cast<const char *>(Kv);
     const char *Vb = static_cast<const char *>(Vv);
 
+    // The body runs in one of two forms: kMulti = false for a workgroup with
+    // one item (read with a scalar load; the pair loop has no item
+    // bookkeeping, which keeps the steady state branch-free), kMulti = true
+    // for a light workgroup of several items.
+    auto body = [&](auto multi_tag) {
+    constexpr bool kMulti = decltype(multi_tag)::value;
     // ---- this wavefront's items: lane k (< nk) holds item k's descriptor --
     const int wg = blockIdx.x;
-    const int v0 = wg < n_single ? wg : n_single + (wg - n_single) * group;
-    const int nk = wg < n_single ? 1 : min(group, total - v0);   // 1 <= nk <= 64
+    const int v0 = kMulti ? n_single + (wg - n_single) * group : wg;
+    const int nk = kMulti ? min(group, total - v0) : 1;   // 1 <= nk <= 64
     int dwin = 0, db0 = 0, db1 = 0, dslot = -1, dhl = 0;
-    if (lane < nk) {
-        const int v = v0 + lane;
-        const int item = v / nh;
-        const WorkItem it = items[item];
+    if constexpr (kMulti) {
+        if (lane < nk) {
+            const int v = v0 + lane;
+            const int item = v / nh;
+            const WorkItem it = items[item];
+            dwin = it.window;
+            db0 = it.blk_begin;
+            db1 = it.blk_end;
+            dslot = it.slot;
+            dhl = v - item * nh;
+        }
+    } else {
+        const int item = v0 / nh;
+        const WorkItem it = items[item];   // uniform: a scalar load
         dwin = it.window;
         db0 = it.blk_begin;
         db1 = it.blk_end;
         dslot = it.slot;
-        dhl = v - item * nh;
+        dhl = v0 - item * nh;
     }
     // uniform reads of item k's fields
-    auto WIN = [&](int k) { return __builtin_amdgcn_readlane(dwin, k); };
-    auto B0 = [&](int k) { return __builtin_amdgcn_readlane(db0, k); };
-    auto B1 = [&](int k) { return __builtin_amdgcn_readlane(db1, k); };
-    auto SLOT = [&](int k) { return __builtin_amdgcn_readlane(dslot, k); };
-    auto HL = [&](int k) { return __builtin_amdgcn_readlane(dhl, k); };
+    auto RL = [&](int x, int k) {
+        if constexpr (kMulti)
+            return __builtin_amdgcn_readlane(x, k);
+        else
+            return x;
+    };
+    auto WIN = [&](int k) { return RL(dwin, k); };
+    auto B0 = [&](int k) { return RL(db0, k); };
+    auto B1 = [&](int k) { return RL(db1, k); };
+    auto SLOT = [&](int k) { return RL(dslot, k); };
+    auto HL = [&](int k) { return RL(dhl, k); };
 
     // Items without blocks (all 16 rows empty; never a piece): O rows = 0,
     // lse = -inf (Algorithm 1's division by l = 0 read as 0).
-    const uint64_t nonempty = __ballot(lane < nk && db0 < db1);
+    const uint64_t nonempty =
+        kMulti ? (uint64_t)__ballot(lane < nk && db0 < db1) : (db0 < db1 ? 1ull : 0ull);
     for (int k = 0; k < nk; ++k) {
         if ((nonempty >> k) & 1) continue;
         const int row = WIN(k) * kWindowRows + i;
@@ -217,10 +242,13 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     if (nonempty == 0) return;
     const int k_first = __builtin_ctzll(nonempty);
     const int k_last = 63 - __builtin_clzll(nonempty);
-    int npairs_lane = lane < nk ? (db1 - db0 + 1) >> 1 : 0;
+    int npairs = (db1 - db0 + 1) >> 1;
+    if constexpr (kMulti) {
+        int npairs_lane = lane < nk ? npairs : 0;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) npairs_lane += __shfl_xor(npairs_lane, off);
-    const int npairs = __builtin_amdgcn_readfirstlane(npairs_lane);
+        for (int off = 32; off > 0; off >>= 1) npairs_lane += __shfl_xor(npairs_lane, off);
+        npairs = __builtin_amdgcn_readfirstlane(npairs_lane);
+    }
 
     // Stream cursor (item k, first block b of the pair).  Past the last pair
     // k = 64; loads for such a cursor re-read the first pair of the last
@@ -231,9 +259,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     };
     auto advance = [&](int &k, int &b) {
         b += 2;
-        if (b >= B1(k)) {
-            k = next_item(k);
-            b = k < 64 ? B0(k) : 0;
+        if constexpr (kMulti) {
+            if (b >= B1(k)) {
+                k = next_item(k);
+                b = k < 64 ? B0(k) : 0;
+            }
         }
     };
 
@@ -285,7 +315,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     // indices clamped so reads stay inside the item (values past its end are
     // never used).
     auto load_cols = [&](int k, int b) {
-        if (k >= 64) {
+        if (kMulti && k >= 64) {
             k = k_last;
             b = B0(k_last);
         }
@@ -393,8 +423,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
             s1 = mma_in<kIn>(kb[c], q[c], s1);
         }
         // the next pair starts another item: its Q rows replace this one's
-        const bool item_end = pk != ck;
-        if (prefetch && item_end) load_q(pk);
+        const bool item_end = kMulti ? pk != ck : !prefetch;
+        if constexpr (kMulti) {
+            if (prefetch && item_end) load_q(pk);
+        }
         wave_lds_fence();
         // ---- V rows -> the same LDS tile (stride LSV, slot = neighbour) ----
 #pragma unroll
@@ -500,6 +532,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     load_cols(pk, pb);
     for (int sidx = 0; sidx + 1 < npairs; ++sidx) step(true);
     step(false);
+    };
+    if ((int)blockIdx.x < n_single)
+        body(Tag<false>{});
+    else
+        body(Tag<true>{});
 }
 
 // Combines the pieces of one split window in their fixed order (so the
