@@ -61,19 +61,13 @@ typedef struct {
     int64_t bsb_bytes;     /* window offsets + column lists + bitmaps            */
     int64_t device_bytes;  /* everything the plan holds on the device            */
     double build_ms;       /* wall time of f3s_plan                              */
-    int32_t n_light;       /* light items (<= light_blocks blocks) at the end of
-                              the work list; a wavefront takes several of them  */
-    int32_t light_blocks;  /* block-count bound of a light item                 */
 } f3s_plan_info_t;
 
 /*
  * Build a plan from a CSR pattern that lives in DEVICE memory.
  * Environment (read at plan time; for ablations): F3S_PIECE_BLOCKS=<even n>
  * overrides the piece size of split windows; F3S_NO_REORDER=1 keeps the work
- * list in window order instead of decreasing block count (Section 3.2);
- * F3S_LIGHT_GROUP=<n> (1..64) fixes how many light windows one wavefront
- * runs back to back (default: enough to cover the light tail in one round of
- * resident wavefronts; 1 = one window per wavefront).
+ * list in window order instead of decreasing block count (Section 3.2).
  *   row_ptr  int32[N+1], row_ptr[0] == 0, non-decreasing
  *   col_idx  int32[row_ptr[N]], every entry in [0, N); order inside a row is
  *            free and repeated entries count once (A is binary, Section 3.1)

@@ -34,7 +34,6 @@ class PlanInfo(ctypes.Structure):
         ("n_pieces", ctypes.c_int32), ("flags", ctypes.c_int32),
         ("bsb_bytes", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
         ("build_ms", ctypes.c_double),
-        ("n_light", ctypes.c_int32), ("light_blocks", ctypes.c_int32),
     ]
 
     def as_dict(self):

@@ -207,7 +207,6 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(tmp.alloc(&split_pieces, (int64_t)T + 1));
     HIP_TRY(tmp.alloc(&split_one, (int64_t)T + 1));
     const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
-    p->light_group = env_int("F3S_LIGHT_GROUP", 0);
     p->flags = reorder ? 0 : 1;
     HIP_TRY(launch_bin_keys(nb, T, piece, reorder, npieces, key, split_pieces,
                             split_one, s));
@@ -231,15 +230,6 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     int32_t n_items = 0;
     HIP_TRY(read_scalar(&n_items, hist + cells));
     p->n_items = n_items;
-    // items of key <= kLightBlocks (row piece - kLightBlocks onwards of the
-    // key-descending histogram) form the end of the list
-    if (reorder) {
-        int32_t first_light = 0;
-        if (piece > kLightBlocks)
-            HIP_TRY(read_scalar(&first_light,
-                                hist + (int64_t)(piece - kLightBlocks) * nchunks));
-        p->n_light = n_items - first_light;
-    }
     HIP_TRY(plan_alloc(p, &p->items, n_items));
     HIP_TRY(plan_alloc(p, &p->merges, 3ll * p->n_split));
     HIP_TRY(launch_bin_scatter(nb, p->blk_off, npieces, key, split_pieces, split_one,
@@ -397,8 +387,6 @@ f3s_status_t f3s_plan_info(f3s_plan_t p, f3s_plan_info_t *out)
     out->bsb_bytes = p->bsb_bytes;
     out->device_bytes = p->device_bytes;
     out->build_ms = p->build_ms;
-    out->n_light = p->n_light;
-    out->light_blocks = f3s::kLightBlocks;
     return F3S_OK;
 }
 

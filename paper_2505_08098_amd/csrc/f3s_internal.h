@@ -12,11 +12,6 @@ constexpr int kWindowRows = 16;   // r: rows per row window (Section 3.1)
 constexpr int kBlockCols = 16;    // c: compacted columns per block
 constexpr int kMaskWords = 8;     // 256-bit bitmap per 16x16 block
 constexpr int kMaxD = 256;        // largest supported feature dimension
-// Whole windows of at most this many blocks (two block pairs) are "light":
-// they sit at the end of the heavy-first work list, and the fused kernel
-// lets one wavefront run several of them back to back with its load
-// pipeline crossing from one to the next.
-constexpr int kLightBlocks = 4;
 
 // Storage type of Q, K, V in the forward kernels.
 constexpr int kInF16 = 0;
@@ -48,8 +43,6 @@ struct f3s_plan_s {
     int32_t n_items = 0;
     int32_t n_split = 0;
     int32_t n_pieces = 0;
-    int32_t n_light = 0;         // light items: the last n_light of the work list
-    int32_t light_group = 0;     // items per light wavefront (0: chosen per launch)
     int32_t flags = 0;           // bit 0: work list in window order
     uint64_t id = 0;             // process-unique plan id
     uint64_t transpose_of = 0;   // id of the plan this one transposes (0: none)

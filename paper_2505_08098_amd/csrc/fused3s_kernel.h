@@ -58,15 +58,16 @@ constexpr float kLn2 = 0.6931471805599453f;
 // registers fit without spilling; more resident waves = more gathers in
 // flight, which is what bounds this kernel.
 template <int D> struct WavesPerSimd { static constexpr int value = 1; };
-template <> struct WavesPerSimd<32> { static constexpr int value = 5; };
+template <> struct WavesPerSimd<32> { static constexpr int value = 6; };
 template <> struct WavesPerSimd<64> { static constexpr int value = 4; };
 template <> struct WavesPerSimd<96> { static constexpr int value = 3; };
 template <> struct WavesPerSimd<128> { static constexpr int value = 2; };
 template <> struct WavesPerSimd<160> { static constexpr int value = 2; };
+// The bf16 variant holds the second probability term: one wave less at d=32.
 template <int D, int kIn>
 constexpr int waves_per_simd()
 {
-    return WavesPerSimd<D>::value;
+    return WavesPerSimd<D>::value - (kIn == kInBF16 && D == 32 ? 1 : 0);
 }
 
 // Score product for the input storage type (16-bit operands as raw bits).
@@ -78,8 +79,6 @@ __device__ __forceinline__ f4 mma_in(h8 a, h8 b, f4 c)
     else
         return mfma16x16x32(a, b, c);
 }
-
-template <bool B> struct Tag { static constexpr bool value = B; };
 
 // Bytes per stored element of Q, K, V.
 template <int kIn> constexpr int elem_bytes() { return kIn == kInFP8 ? 1 : 2; }
@@ -140,17 +139,6 @@ __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
 // e4m3 bytes, widened to fp16 on the way into registers / LDS, so the
 // products are the fp16 ones).  kOutH: O is fp16 instead of fp32.  kWide:
 // Q/K/V may exceed 4 GiB, so gathers use 64-bit addresses.
-//
-// Work assignment.  Virtual item v = item * nh + head (heads of one window
-// back to back: they share its column lists and bitmaps).  Workgroups
-// below n_single take one virtual item each (the heavy and mid part of the
-// heavy-first list, balanced by the hardware's dynamic dispatch); each later
-// workgroup takes `group` consecutive virtual items of the light tail
-// (consecutive in the sorted list = similar sizes).  A wavefront runs its
-// items as one stream of block pairs: the loads of the next pair -- which
-// may belong to the next item -- are in flight while the current pair is
-// computed, and the next item's Q rows are fetched right after the current
-// item's last score product.
 template <int D, bool kWide, int kIn, bool kOutH>
 __global__ __launch_bounds__(64)
 __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s(
@@ -159,7 +147,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     const void *__restrict__ Kv, const void *__restrict__ Vv,
     void *__restrict__ O, float *__restrict__ part_o,
     float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
-    int32_t h0, int32_t nh, int32_t n_single, int32_t group, int32_t total, float sl2)
+    int32_t h0, int32_t nh, float sl2)
 {
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
@@ -175,106 +163,26 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     const int lane = threadIdx.x;
     const int i = lane & 15;  // query row (accumulators) / operand row index
     const int g = lane >> 4;  // lane group: selects the reduction slots
+    // Workgroups walk the work list item-major, head-minor: the heads of one
+    // window run back to back and share its column lists and bitmaps.
+    const int item = blockIdx.x / nh, hl = blockIdx.x - item * nh;
+    const int head = h0 + hl;
+    const WorkItem it = items[item];
+    // Row r of head h starts at r * ld + h * D (elements) in Q, K, V and O.
     constexpr int EB = elem_bytes<kIn>();
-    const char *Qb = static_cast<const char *>(Qv);
-    const char *Kb = static_cast<const char *>(Kv);
-    const char *Vb = static_cast<const char *>(Vv);
+    const char *Q = static_cast<const char *>(Qv) + (int64_t)head * D * EB;
+    const char *K = static_cast<const char *>(Kv) + (int64_t)head * D * EB;
+    const char *V = static_cast<const char *>(Vv) + (int64_t)head * D * EB;
+    const int64_t ohead = (int64_t)head * D;
+    const int row = it.window * kWindowRows + i;
+    const int b0 = it.blk_begin, b1 = it.blk_end;
 
-    // The body runs in one of two forms: kMulti = false for a workgroup with
-    // one item (read with a scalar load; the pair loop has no item
-    // bookkeeping, which keeps the steady state branch-free), kMulti = true
-    // for a light workgroup of several items.
-    auto body = [&](auto multi_tag) {
-    constexpr bool kMulti = decltype(multi_tag)::value;
-    // ---- this wavefront's items: lane k (< nk) holds item k's descriptor --
-    const int wg = blockIdx.x;
-    const int v0 = kMulti ? n_single + (wg - n_single) * group : wg;
-    const int nk = kMulti ? min(group, total - v0) : 1;   // 1 <= nk <= 64
-    int dwin = 0, db0 = 0, db1 = 0, dslot = -1, dhl = 0;
-    if constexpr (kMulti) {
-        if (lane < nk) {
-            const int v = v0 + lane;
-            const int item = v / nh;
-            const WorkItem it = items[item];
-            dwin = it.window;
-            db0 = it.blk_begin;
-            db1 = it.blk_end;
-            dslot = it.slot;
-            dhl = v - item * nh;
-        }
-    } else {
-        const int item = v0 / nh;
-        const WorkItem it = items[item];   // uniform: a scalar load
-        dwin = it.window;
-        db0 = it.blk_begin;
-        db1 = it.blk_end;
-        dslot = it.slot;
-        dhl = v0 - item * nh;
-    }
-    // uniform reads of item k's fields
-    auto RL = [&](int x, int k) {
-        if constexpr (kMulti)
-            return __builtin_amdgcn_readlane(x, k);
-        else
-            return x;
-    };
-    auto WIN = [&](int k) { return RL(dwin, k); };
-    auto B0 = [&](int k) { return RL(db0, k); };
-    auto B1 = [&](int k) { return RL(db1, k); };
-    auto SLOT = [&](int k) { return RL(dslot, k); };
-    auto HL = [&](int k) { return RL(dhl, k); };
-
-    // Items without blocks (all 16 rows empty; never a piece): O rows = 0,
-    // lse = -inf (Algorithm 1's division by l = 0 read as 0).
-    const uint64_t nonempty =
-        kMulti ? (uint64_t)__ballot(lane < nk && db0 < db1) : (db0 < db1 ? 1ull : 0ull);
-    for (int k = 0; k < nk; ++k) {
-        if ((nonempty >> k) & 1) continue;
-        const int row = WIN(k) * kWindowRows + i;
-        if (SLOT(k) < 0 && row < N) {
-            const int head = h0 + HL(k);
-            const int64_t ob = (int64_t)row * ld + (int64_t)head * D + 4 * g;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) store4<kOutH>(O, ob + 16 * t, f4{0.f, 0.f, 0.f, 0.f});
-            if (lse && g == 0) lse[(int64_t)row * (ld / D) + head] = -__builtin_inff();
-        }
-    }
-    if (nonempty == 0) return;
-    const int k_first = __builtin_ctzll(nonempty);
-    const int k_last = 63 - __builtin_clzll(nonempty);
-    int npairs = (db1 - db0 + 1) >> 1;
-    if constexpr (kMulti) {
-        int npairs_lane = lane < nk ? npairs : 0;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) npairs_lane += __shfl_xor(npairs_lane, off);
-        npairs = __builtin_amdgcn_readfirstlane(npairs_lane);
-    }
-
-    // Stream cursor (item k, first block b of the pair).  Past the last pair
-    // k = 64; loads for such a cursor re-read the first pair of the last
-    // item (in bounds, never used).
-    auto next_item = [&](int k) {
-        const uint64_t rest = k >= 63 ? 0ull : nonempty & ~((2ull << k) - 1ull);
-        return rest ? __builtin_ctzll(rest) : 64;
-    };
-    auto advance = [&](int &k, int &b) {
-        b += 2;
-        if constexpr (kMulti) {
-            if (b >= B1(k)) {
-                k = next_item(k);
-                b = k < 64 ? B0(k) : 0;
-            }
-        }
-    };
-
+    // Q_i: lane (i, g) holds Q[row][32c + 8g .. +7] for each chunk c.  Pad
+    // rows (>= N) of the last window read row N-1: their results are never
+    // written and rows do not interact, so any finite values do.
     h8 q[NC];
-    // Q_i of item k: lane (i, g) holds Q[row][32c + 8g .. +7] for each chunk
-    // c.  Pad rows (>= N) of the last window read row N-1: their results are
-    // never written and rows do not interact, so any finite values do.
-    auto load_q = [&](int k) {
-        const int row = WIN(k) * kWindowRows + i;
-        const int head = h0 + HL(k);
-        const char *qp = Qb + ((int64_t)min(row, N - 1) * ld + (int64_t)head * D + 8 * g) * EB;
+    {
+        const char *qp = Q + ((int64_t)min(row, N - 1) * ld + 8 * g) * EB;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             if constexpr (EB == 1)
@@ -282,16 +190,13 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
             else
                 q[c] = *reinterpret_cast<const h8 *>(qp + 64 * c);
         }
-    };
+    }
 
     f4 o[NT];
-    float m_run, l_run;
-    auto reset = [&]() {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) o[t] = f4{0.f, 0.f, 0.f, 0.f};
-        m_run = -__builtin_inff();
-        l_run = 0.f;
-    };
+    for (int t = 0; t < NT; ++t) o[t] = f4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -__builtin_inff();
+    float l_run = 0.f;
 
     // Pipeline state.  The 32 K rows and 32 V rows of a block pair are
     // gathered "row-contiguous": the pair tile's 16-byte chunks are spread
@@ -309,29 +214,20 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
     constexpr int CE = 16 / EB;       // elements per chunk
     h8 kst[NI], vst[NI];              // staged K and V chunks of the pair in flight
     uint32_t mwa = 0, mwb = 0;
-    int ncol = 0;                     // lanes 0..31: raw column of slot `lane` of a pair
+    int ncol = 0;                // lanes 0..31: raw column of slot `lane` of the next pair
 
-    // Raw column ids of pair (k, b): lane l (mod 32) takes slot l; block
-    // indices clamped so reads stay inside the item (values past its end are
-    // never used).
-    auto load_cols = [&](int k, int b) {
-        if (kMulti && k >= 64) {
-            k = k_last;
-            b = B0(k_last);
-        }
-        const int b1 = B1(k);
+    // Raw column ids of pair (b, b+1): lane l (mod 32) takes slot l; block
+    // indices clamped so reads stay inside this item (values past its end
+    // are never used).
+    auto load_cols = [&](int b) {
         const int slot = lane & 31;
         const int blk = slot < 16 ? min(b, b1 - 1) : min(b + 1, b1 - 1);
         ncol = cols[(int64_t)kBlockCols * blk + (slot & 15)];
     };
-    // Issue the K, V and bitmap loads of pair (k, b), whose column ids are in
-    // ncol.  Slots 0 and 16 are never padding (the first slot of a block);
-    // the wave is fully active here, so readlane sees them.
-    auto load_pair = [&](int k, int b) {
-        const int b1 = B1(k);
-        const int64_t hoff = (int64_t)(h0 + HL(k)) * D * EB;
-        const char *K = Kb + hoff;
-        const char *V = Vb + hoff;
+    // Issue the K, V and bitmap loads of pair (b, b+1).  Slots 0 and 16 are
+    // never padding (the first slot of a block); the wave is fully active
+    // here, so readlane sees them.
+    auto load_pair = [&](int b) {
         const int f0 = __builtin_amdgcn_readlane(ncol, 0);
         const int f1 = __builtin_amdgcn_readlane(ncol, 16);
         const int c = ncol < 0 ? ((lane & 16) ? f1 : f0) : ncol;
@@ -355,45 +251,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
         mwb = mask[(int64_t)kMaskWords * min(b + 1, b1 - 1) + (lane >> 3)];
     };
 
-    // Item k done: full row sums, normalise, write (Algorithm 1 end), or
-    // write the unnormalised partial of a piece.
-    auto finish = [&](int k) {
-        float l_tot = l_run + __shfl_xor(l_run, 16);
-        l_tot += __shfl_xor(l_tot, 32);
-        const int row = WIN(k) * kWindowRows + i;
-        const int slot = SLOT(k);
-        const int hl = HL(k);
-        if (slot < 0) {
-            if (row < N) {
-                const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-                const int64_t ob = (int64_t)row * ld + (int64_t)(h0 + hl) * D + 4 * g;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) store4<kOutH>(O, ob + 16 * t, o[t] * inv);
-                // natural-log log-sum-exp of the row's scaled scores
-                if (lse && g == 0)
-                    lse[(int64_t)row * (ld / D) + h0 + hl] =
-                        l_tot > 0.f ? kLn2 * (m_run + __log2f(l_tot)) : -__builtin_inff();
-            }
-        } else {
-            // partial slot of (piece, head): slot * nh + head offset
-            const int64_t ps = (int64_t)slot * nh + hl;
-            float *op = part_o + ps * kWindowRows * D + i * D + 4 * g;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) *reinterpret_cast<f4 *>(op + 16 * t) = o[t];
-            if (g == 0) {
-                part_ml[ps * 32 + i] = m_run;
-                part_ml[ps * 32 + 16 + i] = l_tot;
-            }
-        }
-    };
-
     const int nib_shift = 4 * (lane & 7);
-    int ck = k_first, cb = B0(k_first);   // pair being computed
-    int pk = ck, pb = cb;                 // next pair (its column ids in flight)
     // One block pair: scores, mask, online softmax, value product.  With
     // `prefetch`, the loads of the pair after it are issued as soon as this
     // pair's staging registers are in LDS.
-    auto step = [&](bool prefetch) {
+    auto step = [&](int b, bool prefetch) {
         // ---- K rows -> LDS (stride LSK), read back as MFMA A operands ----
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
@@ -422,11 +284,6 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
             s0 = mma_in<kIn>(ka[c], q[c], s0);
             s1 = mma_in<kIn>(kb[c], q[c], s1);
         }
-        // the next pair starts another item: its Q rows replace this one's
-        const bool item_end = kMulti ? pk != ck : !prefetch;
-        if constexpr (kMulti) {
-            if (prefetch && item_end) load_q(pk);
-        }
         wave_lds_fence();
         // ---- V rows -> the same LDS tile (stride LSV, slot = neighbour) ----
 #pragma unroll
@@ -444,13 +301,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
         }
         const uint32_t nib0 = (mwa >> nib_shift) & 15u;
         // (an odd tail's absent second block re-read block b: mask it off)
-        const uint32_t nib1 = cb + 1 < B1(ck) ? (mwb >> nib_shift) & 15u : 0u;
+        const uint32_t nib1 = b + 1 < b1 ? (mwb >> nib_shift) & 15u : 0u;
         // ---- issue the next pair's loads (staging registers are free) ----
-        int nk2 = pk, nb2 = pb;
         if (prefetch) {
-            load_pair(pk, pb);
-            advance(nk2, nb2);
-            load_cols(nk2, nb2);
+            load_pair(b + 2);
+            load_cols(b + 4);
         }
         // ---- mask + online softmax (base 2) ----
         float x[8];
@@ -514,29 +369,42 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
             }
         }
         wave_lds_fence();
-        if (item_end) {
-            finish(ck);
-            reset();
-        }
-        ck = pk;
-        cb = pb;
-        pk = nk2;
-        pb = nb2;
     };
 
-    reset();
-    load_q(ck);
-    load_cols(ck, cb);
-    load_pair(ck, cb);
-    advance(pk, pb);
-    load_cols(pk, pb);
-    for (int sidx = 0; sidx + 1 < npairs; ++sidx) step(true);
-    step(false);
-    };
-    if ((int)blockIdx.x < n_single)
-        body(Tag<false>{});
-    else
-        body(Tag<true>{});
+    if (b0 < b1) {
+        load_cols(b0);
+        load_pair(b0);
+        load_cols(b0 + 2);
+        int b = b0;
+        for (; b + 2 < b1; b += 2) step(b, true);
+        step(b, false);
+    }
+
+    // ---- finalise: full row sums, normalise, write (Algorithm 1 end) ----
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (it.slot < 0) {
+        if (row < N) {
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            const int64_t ob = (int64_t)row * ld + ohead + 4 * g;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) store4<kOutH>(O, ob + 16 * t, o[t] * inv);
+            // natural-log log-sum-exp of the row's scaled scores
+            if (lse && g == 0)
+                lse[(int64_t)row * (ld / D) + head] =
+                    l_tot > 0.f ? kLn2 * (m_run + __log2f(l_tot)) : -__builtin_inff();
+        }
+    } else {
+        // partial slot of (piece, head): slot * nh + head offset
+        const int64_t ps = (int64_t)it.slot * nh + hl;
+        float *op = part_o + ps * kWindowRows * D + i * D + 4 * g;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) *reinterpret_cast<f4 *>(op + 16 * t) = o[t];
+        if (g == 0) {
+            part_ml[ps * 32 + i] = m_run;
+            part_ml[ps * 32 + 16 + i] = l_tot;
+        }
+    }
 }
 
 // Combines the pieces of one split window in their fixed order (so the
@@ -613,38 +481,9 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
 // Heads are launched in groups whose partial results fit the plan's scratch
 // (nh * D <= 256 floats per piece row); without split windows all heads go
 // in one launch.
-// Resident wavefronts of a kernel on the current device (occupancy x CUs),
-// cached per device.
-template <typename Kern>
-int resident_waves(Kern kern)
-{
-    static int cache[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cache[dev] == 0) {
-        int per_cu = 0, cus = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 64, 0) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
-                hipSuccess)
-            return 0;
-        cache[dev] = per_cu * cus;
-    }
-    return cache[dev];
-}
-
-// Items per light workgroup: spread the light tail over one round of the
-// resident wavefronts (at most 64 items: one descriptor per lane); a plan
-// built with F3S_LIGHT_GROUP=<n> fixes it (1 = one item per wavefront).
-inline int32_t light_group(const f3s_plan_s &p, int64_t light_virtual, int resident)
-{
-    int64_t gsz = p.light_group > 0
-                      ? p.light_group
-                      : (resident > 0 ? (light_virtual + resident - 1) / resident : 1);
-    if (gsz < 1) gsz = 1;
-    if (gsz > 64) gsz = 64;
-    return (int32_t)gsz;
-}
-
+// Heads are launched in groups whose partial results fit the plan's scratch
+// (nh * D <= 256 floats per piece row); without split windows all heads go
+// in one launch.
 template <int D, int kIn, bool kOutH>
 hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                     const void *V, void *O, float *lse, int32_t H, float sl2,
@@ -659,15 +498,11 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
         // the plan's partial buffers hold n_pieces * kMaxD / D head slots
         if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
         if (p.n_items > 0) {
-            const int64_t total = (int64_t)p.n_items * nh;
-            const int64_t light = (int64_t)p.n_light * nh;
-            const int64_t single = total - light;
-            const int32_t lg = light > 0 ? light_group(p, light, resident_waves(kern)) : 1;
-            const int64_t grid = single + (light + lg - 1) / lg;
-            if (total > 0x7FFFFFFFll) return hipErrorInvalidConfiguration;
+            const uint64_t grid = (uint64_t)p.n_items * nh;
+            if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
             kern<<<(unsigned)grid, 64, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
-                                               (int32_t)single, lg, (int32_t)total, sl2);
+                                               sl2);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }

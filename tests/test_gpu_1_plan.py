@@ -39,16 +39,6 @@ def _check_plan_against_oracle(f3s, oracle, rp, ci, N):
     assert np.array_equal(got["merges"], merges)
     assert info["n_items"] == len(items) and info["n_split"] == len(merges)
     assert info["n_pieces"] == int((items[:, 3] >= 0).sum())
-    # light tail: items of key <= light_blocks (key = block count of a whole
-    # window, the piece size for a piece) close the heavy-first list
-    if info["flags"] & 1:
-        assert info["n_light"] == 0
-    else:
-        keys = np.where(items[:, 3] >= 0, info["piece_blocks"], items[:, 2] - items[:, 1])
-        light = keys <= info["light_blocks"]
-        n_light = int(light.sum())
-        assert info["n_light"] == n_light
-        assert np.all(light[len(items) - n_light:])
     assert info["bsb_bytes"] == 4 * (info["n_windows"] + 1) + 64 * info["n_blocks"] \
         + 32 * info["n_blocks"]
     plan.close()

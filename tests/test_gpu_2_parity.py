@@ -315,47 +315,27 @@ def ctypes_stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-@pytest.mark.parametrize("case", ["molecules", "empty_windows_heads", "split_fp8"])
-def test_light_grouping_is_bit_identical(gpu, monkeypatch, case):
-    """Several light windows per wavefront (with the load pipeline running
-    across them) change nothing in any window's arithmetic: the output is
-    bit-identical for every group size, 1 (one window per wavefront) included."""
-    H, dt, piece = 1, torch.float16, None
-    if case == "molecules":
-        c = W.make_config(4)
-        rp, ci, N, feats = c["row_ptr"], c["col_idx"], c["N"], [c["Q"], c["K"], c["V"]]
-        d = c["d"]
-    else:
-        rng = np.random.default_rng(41)
-        N, d = 2000, 64
-        rp, ci = W.random_csr(rng, N, max_deg=6, empty_frac=0.6, dup_frac=0.1)
-        if case == "empty_windows_heads":
-            # whole empty windows: rows 160..479 without entries
-            deg = np.diff(rp)
-            deg[160:480] = 0
-            keep = np.repeat(np.arange(N), np.diff(rp))
-            mask = (keep < 160) | (keep >= 480)
-            ci = ci[mask]
-            rp = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
-            H = 3
-        else:
-            dt, piece = torch.float8_e4m3fn, "2"
-        feats = [rng.standard_normal((N, H, d) if H > 1 else (N, d), dtype=np.float32)
-                 for _ in range(3)]
-    if piece:
-        monkeypatch.setenv("F3S_PIECE_BLOCKS", piece)
-    x = [torch.from_numpy(np.asarray(f, dtype=np.float32)).to(dt).to(DEV) for f in feats]
-    outs = []
-    for grp in ("0", "1", "2", "7", "64"):
-        monkeypatch.setenv("F3S_LIGHT_GROUP", grp)
-        plan = gpu.Plan(_dev(rp), _dev(ci), N)
-        if grp == "0":
-            print(f"  {case}: n_items={plan.info['n_items']} n_light={plan.info['n_light']}",
-                  flush=True)
-            assert plan.info["n_light"] > 0
-        O, lse = gpu.forward_typed(plan, *x, scale=1 / math.sqrt(d), want_lse=True)
-        torch.cuda.synchronize()
-        outs.append((O, lse))
-        plan.close()
-    for O, lse in outs[1:]:
-        assert torch.equal(O, outs[0][0]) and torch.equal(lse, outs[0][1])
+@pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
+def test_split_windows_merge_all_feature_sizes(gpu, oracle, monkeypatch, d):
+    """Pieces of 2 blocks: every window above 2 blocks is split and merged
+    (the merge kernel's column coverage differs for d = 32, 96, 160, 224);
+    two heads share each launch where 2 * d <= 256."""
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "2")
+    rng = np.random.default_rng(500 + d)
+    N, H = 300, 2
+    rp, ci = W.random_csr(rng, N, max_deg=80, empty_frac=0.05, dup_frac=0.1)
+    Q, K, V = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(3))
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    assert plan.info["n_split"] > 0
+    O, lse = gpu.forward(plan, _dev(Q), _dev(K), _dev(V), scale=1 / math.sqrt(d))
+    torch.cuda.synchronize()
+    O, lse = O.cpu().numpy(), lse.cpu().numpy()
+    for h in range(H):
+        ref, reflse = oracle.attention_f64(rp, ci, np.ascontiguousarray(Q[:, h]),
+                                           np.ascontiguousarray(K[:, h]),
+                                           np.ascontiguousarray(V[:, h]), 1 / math.sqrt(d),
+                                           want_lse=True)
+        _assert_parity(O[:, h], ref)
+        fin = np.isfinite(reflse)
+        assert np.array_equal(np.isfinite(lse[:, h]), fin)
+        assert np.abs(lse[fin, h] - reflse[fin]).max() < 2e-3
