@@ -99,20 +99,38 @@ def cpu_baseline(c, O_gpu, sample_rows):
 
 
 def backward_bytes(info, info_t, d, heads=1):
-    """Algorithmic bytes of one f3s_backward: delta (G and O read, delta
-    written), the dQ pass over windows of A (Q and G rows, K and V rows per
-    distinct window column, dQ written, plan data, lse and delta of the
-    rows) and the dK/dV pass over windows of A^T (K and V rows, Q and G rows
-    per distinct window column plus their lse and delta, dK and dV written,
-    plan data)."""
+    """Algorithmic bytes of one f3s_backward.  dQ pass over windows of A:
+    Q, G and O rows of the window (delta = G.O is formed there) and their
+    lse, the K and V rows of every distinct window column, dQ written and
+    one (lse, delta) record per row written.  dK/dV pass over windows of
+    A^T: K and V rows of the window, the Q and G rows and the (lse, delta)
+    record of every distinct window column, dK and dV written.  Plan data:
+    96 B per block, 16 B per item of both plans."""
     N = info["N"]
-    per_head = (6 * N * d + 4 * N
-                + 4 * N * d + 4 * d * info["n_unique"] + 4 * N * d + 8 * N
-                + 4 * N * d + 4 * d * info_t["n_unique"] + 8 * info_t["n_unique"]
-                + 8 * N * d)
+    dq = 2 * N * d + 2 * N * d + 4 * N * d + 4 * N + 4 * d * info["n_unique"] \
+        + 4 * N * d + 8 * N
+    dkdv = 4 * N * d + 4 * d * info_t["n_unique"] + 8 * info_t["n_unique"] + 8 * N * d
     plan_bytes = 96 * (info["n_blocks"] + info_t["n_blocks"]) + 16 * (
         info["n_items"] + info_t["n_items"])
-    return heads * per_head + plan_bytes
+    return heads * (dq + dkdv) + plan_bytes
+
+
+def copy_calibration(args, out, dev):
+    """Three plain device copies of --copy-calib-mib MiB after the timed
+    region: reference dispatches of known size for scaling HBM byte
+    counters (FETCH_SIZE, WRITE_SIZE) taken over the same process."""
+    if args.copy_calib_mib <= 0:
+        return
+    import torch
+    n = args.copy_calib_mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    out["copy_calib_bytes"] = n * 4
+    del src, dst
 
 
 def bench_backward(args, c, plan, Q, K, V, stream, dev):
@@ -157,9 +175,10 @@ def bench_backward(args, c, plan, Q, K, V, stream, dev):
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": None, "algorithmic_bytes_per_call": nbytes,
-                     "kernel": "k_bwd_dq (with delta) + k_bwd_dkdv"},
+                     "kernel": "k_bwd_dq + k_bwd_dkdv"},
         "cpu_baseline": None,
     }
+    copy_calibration(args, out, dev)
     plan_t.close()
     plan.close()
     print(json.dumps(out), flush=True)
@@ -314,16 +333,7 @@ def main():
         },
         "gen_s": round(gen_s, 1),
     }
-    if args.copy_calib_mib > 0:
-        n = args.copy_calib_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        out["copy_calib_bytes"] = n * 4
-        del src, dst
+    copy_calibration(args, out, dev)
     if not args.no_cpu and (H > 1 or typed):
         # the oracle baseline is timed on the one-head fp16 -> fp32 workload
         out["cpu_baseline"] = None

@@ -168,16 +168,19 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t plan);
  *   Q, K, V, dO   device fp16 [N, n_heads, d] (the forward's inputs, and G)
  *   O, lse        device fp32: the forward's output [N, n_heads, d] and
  *                 log-sum-exp [N, n_heads] from f3s_forward
- *   delta         device fp32 [N, n_heads], written (G_i . O_i)
+ *   row_stats     device fp32 [N, n_heads, 2], written: per row and head the
+ *                 base-2 log-sum-exp (lse * log2 e) and delta_i = G_i . O_i;
+ *                 8-byte aligned.  The dK/dV pass gathers this one 8-byte
+ *                 record for every row attending to a key.
  *   dQ, dK, dV    device fp32 [N, n_heads, d], every element written
  *   d             32, 64, 96 or 128
  * P and dS enter the products as fp16 (round to nearest even).  Outputs must
- * not overlap each other or any input; 16-byte aligned (lse, delta: 4).
+ * not overlap each other or any input; 16-byte aligned (lse: 4, row_stats: 8).
  * Asynchronous on `stream`, no allocation.  Deterministic (no atomics).
  */
 f3s_status_t f3s_backward(f3s_plan_t plan, f3s_plan_t plan_t, const void *Q,
                           const void *K, const void *V, const float *O, const void *dO,
-                          const float *lse, float *delta, float *dQ, float *dK,
+                          const float *lse, float *row_stats, float *dQ, float *dK,
                           float *dV, int32_t n_heads, int32_t d, float scale,
                           hipStream_t stream);
 

@@ -313,7 +313,8 @@ def forward_typed(plan, Q, K, V, out_dtype=torch.float32, scale=None, out=None,
 
 
 def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
-    """f3s_backward: returns (dQ, dK, dV) fp32 (and writes a delta buffer)."""
+    """f3s_backward: returns (dQ, dK, dV) fp32 (the per-row (lse, delta)
+    records it needs go to a buffer allocated here)."""
     shape = tuple(Q.shape)
     H = shape[1] if len(shape) == 3 else 1
     d = shape[-1]
@@ -326,14 +327,14 @@ def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
     if tuple(O.shape) != shape or lse.numel() != plan.N * H:
         raise ValueError("O must match Q; lse must hold N * H values")
     dQ, dK, dV = (torch.empty(shape, dtype=torch.float32, device=Q.device) for _ in range(3))
-    delta = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
+    row_stats = torch.empty(shape[:-1] + (2,), dtype=torch.float32, device=Q.device)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     if stream is None:
         stream = torch.cuda.current_stream(Q.device)
     rc = load_library().f3s_backward(
         plan.handle, plan_t.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), O.data_ptr(),
-        dO.data_ptr(), lse.data_ptr(), delta.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
+        dO.data_ptr(), lse.data_ptr(), row_stats.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
         dV.data_ptr(), int(H), int(d), float(scale), ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
         raise F3SError(rc, "f3s_backward")

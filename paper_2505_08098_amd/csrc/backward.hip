@@ -81,7 +81,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
     const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
     const _Float16 *__restrict__ G, const float *__restrict__ O,
-    const float *__restrict__ lse, float *__restrict__ delta, float *__restrict__ dQ,
+    const float *__restrict__ lse, float2 *__restrict__ stats, float *__restrict__ dQ,
     float *__restrict__ part, int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2,
     float scale)
 {
@@ -127,7 +127,9 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     }
     dl += __shfl_xor(dl, 16);
     dl += __shfl_xor(dl, 32);
-    if (g == 0 && row < N) delta[(int64_t)row * H + head] = dl;
+    // one 8-byte record per row and head for the dK/dV pass, which gathers
+    // it for every attending row: (base-2 log-sum-exp, delta)
+    if (g == 0 && row < N) stats[(int64_t)row * H + head] = float2{lse2, dl};
 
     f4 acc[NT];
 #pragma unroll
@@ -222,8 +224,8 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
     const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
-    const _Float16 *__restrict__ G, const float *__restrict__ lse,
-    const float *__restrict__ delta, float *__restrict__ dK, float *__restrict__ dV,
+    const _Float16 *__restrict__ G, const float2 *__restrict__ stats,
+    float *__restrict__ dK, float *__restrict__ dV,
     float *__restrict__ part, int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2,
     float scale)
 {
@@ -269,8 +271,9 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     auto load_pair = [&](int b) {
         const int c = sanitize_slot(ncol, lane);
         gather_pair<D, kWide>(Q, G, c, ld, lane, qst, gst);
-        lsev = lse[(int64_t)c * H + head];
-        delv = delta[(int64_t)c * H + head];
+        const float2 st = stats[(int64_t)c * H + head];
+        lsev = st.x;
+        delv = st.y;
         mwa = mask[(int64_t)kMaskWords * b + (lane >> 3)];
         mwb = mask[(int64_t)kMaskWords * min(b + 1, b1 - 1) + (lane >> 3)];
     };
@@ -279,7 +282,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
         stage_pair<D>(tQ, LS, lane, qst);
         stage_pair<D>(tG, LS, lane, gst);
         if (lane < 32) {
-            slse[lane] = lsev * kLog2e;
+            slse[lane] = lsev;
             sdel[lane] = delv;
         }
         wave_lds_fence();
@@ -383,9 +386,20 @@ __global__ __launch_bounds__(256) void k_merge_sum(const int32_t *__restrict__ m
         const float *src = part + ((int64_t)first * nh + hl) * slot_floats +
                            (int64_t)pidx * kWindowRows * D + (int64_t)r * D;
         for (int c4 = q; c4 < D / 4; c4 += 16) {
+            // pieces summed in order; the loads of 8 pieces are issued
+            // together (indices past the last piece re-read it, unused)
             f4 acc = f4{0.f, 0.f, 0.f, 0.f};
-            for (int k = 0; k < np; ++k)
-                acc += *reinterpret_cast<const f4 *>(src + k * nh * slot_floats + 4 * c4);
+            for (int k0 = 0; k0 < np; k0 += 8) {
+                f4 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int k = min(k0 + u, np - 1);
+                    v[u] = *reinterpret_cast<const f4 *>(src + k * nh * slot_floats + 4 * c4);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (k0 + u < np) acc += v[u];
+            }
             *reinterpret_cast<f4 *>(out + 4 * c4) = acc;
         }
     }
@@ -394,9 +408,10 @@ __global__ __launch_bounds__(256) void k_merge_sum(const int32_t *__restrict__ m
 template <int D>
 hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q,
                         const void *K, const void *V, const float *O, const void *G,
-                        const float *lse, float *delta, float *dQ, float *dK, float *dV,
+                        const float *lse, float *row_stats, float *dQ, float *dK, float *dV,
                         int32_t H, float sl2, float scale, hipStream_t s)
 {
+    float2 *stats = reinterpret_cast<float2 *>(row_stats);
     const int32_t ld = H * D;
     const bool wide = (uint64_t)p.N * ld * 2 > 0xFFFFFFF0ull;
     const auto *q = static_cast<const _Float16 *>(Q);
@@ -413,7 +428,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
             if (p.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)p.n_items * nh), 64, 0, s>>>(
-                    p.items, p.cols, p.mask, q, k, v, gr, O, lse, delta, dQ, p.part_o, p.N,
+                    p.items, p.cols, p.mask, q, k, v, gr, O, lse, stats, dQ, p.part_o, p.N,
                     ld, h0, nh, sl2, scale);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
@@ -434,7 +449,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (pt.n_split > 0 && (int64_t)nh * 2 * D > kMaxD) return hipErrorInvalidValue;
             if (pt.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)pt.n_items * nh), 64, 0, s>>>(
-                    pt.items, pt.cols, pt.mask, q, k, v, gr, lse, delta, dK, dV, pt.part_o,
+                    pt.items, pt.cols, pt.mask, q, k, v, gr, stats, dK, dV, pt.part_o,
                     pt.N, ld, h0, nh, sl2, scale);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
@@ -452,15 +467,15 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
 
 hipError_t launch_backward(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q,
                            const void *K, const void *V, const float *O, const void *G,
-                           const float *lse, float *delta, float *dQ, float *dK, float *dV,
+                           const float *lse, float *row_stats, float *dQ, float *dK, float *dV,
                            int32_t H, int32_t d, float scale, hipStream_t s)
 {
     const float sl2 = scale * kLog2e;
     switch (d) {
-    case 32: return launch_bwd_d<32>(p, pt, Q, K, V, O, G, lse, delta, dQ, dK, dV, H, sl2, scale, s);
-    case 64: return launch_bwd_d<64>(p, pt, Q, K, V, O, G, lse, delta, dQ, dK, dV, H, sl2, scale, s);
-    case 96: return launch_bwd_d<96>(p, pt, Q, K, V, O, G, lse, delta, dQ, dK, dV, H, sl2, scale, s);
-    case 128: return launch_bwd_d<128>(p, pt, Q, K, V, O, G, lse, delta, dQ, dK, dV, H, sl2, scale, s);
+    case 32: return launch_bwd_d<32>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 64: return launch_bwd_d<64>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 96: return launch_bwd_d<96>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 128: return launch_bwd_d<128>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
     default: return hipErrorInvalidValue;
     }
 }

@@ -472,7 +472,7 @@ f3s_status_t f3s_run_mh(f3s_plan_t p, const void *Q, const void *K, const void *
 
 f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void *K,
                           const void *V, const float *O, const void *dO, const float *lse,
-                          float *delta, float *dQ, float *dK, float *dV, int32_t n_heads,
+                          float *row_stats, float *dQ, float *dK, float *dV, int32_t n_heads,
                           int32_t d, float scale, hipStream_t stream)
 {
     if (!p || !pt || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
@@ -486,8 +486,8 @@ f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void
         if (!x || !aligned16(x)) return fail(F3S_ERR_INVALID_VALUE);
     for (void *x : outs)
         if (!x || !aligned16(x)) return fail(F3S_ERR_INVALID_VALUE);
-    if (!O || !aligned16(O) || !lse || !delta || ((uintptr_t)lse & 3u) ||
-        ((uintptr_t)delta & 3u))
+    if (!O || !aligned16(O) || !lse || !row_stats || ((uintptr_t)lse & 3u) ||
+        ((uintptr_t)row_stats & 7u))
         return fail(F3S_ERR_INVALID_VALUE);
     if ((uint64_t)p->n_items * n_heads > 0x7FFFFFFFull ||
         (uint64_t)pt->n_items * n_heads > 0x7FFFFFFFull)
@@ -497,14 +497,14 @@ f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void
     // outputs must not overlap each other or any input
     struct Span { const void *p; size_t n; };
     const Span in_spans[] = {{Q, h16}, {K, h16}, {V, h16}, {dO, h16}, {O, f32}, {lse, rowv}};
-    const Span out_spans[] = {{dQ, f32}, {dK, f32}, {dV, f32}, {delta, rowv}};
+    const Span out_spans[] = {{dQ, f32}, {dK, f32}, {dV, f32}, {row_stats, 2 * rowv}};
     for (const Span &o : out_spans) {
         for (const Span &x : in_spans)
             if (overlaps(o.p, o.n, x.p, x.n)) return fail(F3S_ERR_INVALID_VALUE);
         for (const Span &x : out_spans)
             if (&x != &o && overlaps(o.p, o.n, x.p, x.n)) return fail(F3S_ERR_INVALID_VALUE);
     }
-    f3s_status_t st = from_hip(f3s::launch_backward(*p, *pt, Q, K, V, O, dO, lse, delta, dQ,
+    f3s_status_t st = from_hip(f3s::launch_backward(*p, *pt, Q, K, V, O, dO, lse, row_stats, dQ,
                                                     dK, dV, n_heads, d, scale, stream));
     return st == F3S_OK ? F3S_OK : fail(st);
 }
