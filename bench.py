@@ -31,14 +31,21 @@ KERNEL_SOURCES = [os.path.join(HERE, "paper_2505_08098_amd", "csrc", f)
                             "f3s_internal.h")]
 
 
-def kernel_source_hash():
+def kernel_source_hash(root=None):
     """Hash of the fused kernel's source code with comments and whitespace
-    removed (a comment edit does not invalidate measured counters)."""
+    removed (a comment edit does not invalidate measured counters).  Of the
+    internal header only the part the kernel uses counts: the constants, the
+    work item and the plan struct, i.e. everything before the launcher
+    declarations."""
     import re
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
+        if root is not None:
+            p = os.path.join(root, os.path.relpath(p, HERE))
         with open(p) as f:
             text = f.read()
+        if p.endswith("f3s_internal.h"):
+            text = text.split("// ---- plan kernels")[0]
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         text = re.sub(r"//[^\n]*", "", text)
         h.update("".join(text.split()).encode())
