@@ -66,7 +66,7 @@ typedef struct {
 /*
  * Build a plan from a CSR pattern that lives in DEVICE memory.
  * Environment (read at plan time; for ablations): F3S_PIECE_BLOCKS=<even n>
- * overrides the piece size of split windows; F3S_NO_REORDER=1 keeps the work
+ * overrides the piece size of split windows (capped at the largest window); F3S_NO_REORDER=1 keeps the work
  * list in window order instead of decreasing block count (Section 3.2).
  *   row_ptr  int32[N+1], row_ptr[0] == 0, non-decreasing
  *   col_idx  int32[row_ptr[N]], every entry in [0, N); order inside a row is

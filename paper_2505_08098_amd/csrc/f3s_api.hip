@@ -97,19 +97,29 @@ hipError_t read_scalar(T *host, const T *dev)
 
 // Work-list piece size: aim for at most one piece's worth of blocks per
 // wavefront slot so the tail of the launch stays short; even, >= 16.
-int choose_piece(int64_t n_blocks, int device)
+// Piece size (even): about n_blocks / (8 x CUs) blocks, so the work list has
+// of the order of 8 items per CU, at least 4 blocks (measured: on a 64-window
+// graph, pieces of 4 beat 2 and 8 and whole windows).  Never above the
+// largest window (a larger value splits nothing and only widens the bucket
+// histogram of the work-list sort).
+int choose_piece(int64_t n_blocks, int32_t max_blocks, int device)
 {
-    int env = env_int("F3S_PIECE_BLOCKS", 0);
-    if (env >= 2) return env & ~1;
-    int cus = 256;
-    hipDeviceProp_t prop;
-    if (hipGetDeviceProperties(&prop, device) == hipSuccess && prop.multiProcessorCount > 0)
-        cus = prop.multiProcessorCount;
-    const int64_t slots = (int64_t)cus * 8;
-    int64_t piece = (n_blocks + slots - 1) / slots;
-    if (piece < 16) piece = 16;
-    if (piece > (1 << 20)) piece = 1 << 20;
-    return (int)((piece + 1) & ~1LL);
+    const int64_t cap = ((int64_t)(max_blocks > 2 ? max_blocks : 2) + 1) & ~1LL;
+    int64_t piece;
+    const int env = env_int("F3S_PIECE_BLOCKS", 0);
+    if (env >= 2) {
+        piece = env & ~1;
+    } else {
+        int cus = 256;
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, device) == hipSuccess && prop.multiProcessorCount > 0)
+            cus = prop.multiProcessorCount;
+        const int64_t slots = (int64_t)cus * 8;
+        piece = (n_blocks + slots - 1) / slots;
+        if (piece < 4) piece = 4;
+        piece = (piece + 1) & ~1LL;
+    }
+    return (int)(piece < cap ? piece : cap);
 }
 
 f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *col_idx)
@@ -199,7 +209,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     p->bsb_bytes = 4ll * (T + 1) + 4ll * kBlockCols * B + 4ll * kMaskWords * B;
 
     // ---- 5. heavy-first work list -------------------------------------
-    const int32_t piece = choose_piece(B, p->device);
+    const int32_t piece = choose_piece(B, p->max_blocks, p->device);
     p->piece = piece;
     int32_t *npieces, *key, *split_pieces, *split_one;
     HIP_TRY(tmp.alloc(&npieces, T));
