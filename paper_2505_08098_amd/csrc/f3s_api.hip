@@ -98,10 +98,10 @@ hipError_t read_scalar(T *host, const T *dev)
 // Work-list piece size: aim for at most one piece's worth of blocks per
 // wavefront slot so the tail of the launch stays short; even, >= 16.
 // Piece size (even): about n_blocks / (8 x CUs) blocks, so the work list has
-// of the order of 8 items per CU, at least 4 blocks (measured: on a 64-window
-// graph, pieces of 4 beat 2 and 8 and whole windows).  Never above the
-// largest window (a larger value splits nothing and only widens the bucket
-// histogram of the work-list sort).
+// of the order of 8 items per CU, at least 16 blocks (smaller pieces help
+// the forward on tiny graphs a little but add merge launches to the
+// backward).  Never above the largest window (a larger value splits nothing
+// and only widens the bucket histogram of the work-list sort).
 int choose_piece(int64_t n_blocks, int32_t max_blocks, int device)
 {
     const int64_t cap = ((int64_t)(max_blocks > 2 ? max_blocks : 2) + 1) & ~1LL;
@@ -116,7 +116,7 @@ int choose_piece(int64_t n_blocks, int32_t max_blocks, int device)
             cus = prop.multiProcessorCount;
         const int64_t slots = (int64_t)cus * 8;
         piece = (n_blocks + slots - 1) / slots;
-        if (piece < 4) piece = 4;
+        if (piece < 16) piece = 16;
         piece = (piece + 1) & ~1LL;
     }
     return (int)(piece < cap ? piece : cap);
