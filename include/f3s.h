@@ -57,7 +57,8 @@ typedef struct {
     int32_t n_items;       /* work items (windows or pieces) in the work list    */
     int32_t n_split;       /* windows that were split                            */
     int32_t n_pieces;      /* pieces in total (partial-result slots)             */
-    int32_t flags;         /* bit 0: work list left in window order (no reorder) */
+    int32_t flags;         /* bit 0: work list left in window order (no reorder);
+                              bit 1: narrow K/V gathers (ablation)                */
     int64_t bsb_bytes;     /* window offsets + column lists + bitmaps            */
     int64_t device_bytes;  /* everything the plan holds on the device            */
     double build_ms;       /* wall time of f3s_plan                              */
@@ -65,9 +66,16 @@ typedef struct {
 
 /*
  * Build a plan from a CSR pattern that lives in DEVICE memory.
- * Environment (read at plan time; for ablations): F3S_PIECE_BLOCKS=<even n>
- * overrides the piece size of split windows (capped at the largest window); F3S_NO_REORDER=1 keeps the work
- * list in window order instead of decreasing block count (Section 3.2).
+ * Environment (read at plan time; for ablations):
+ *   F3S_PIECE_BLOCKS=<even n>  piece size of split windows (capped at the
+ *                              largest window)
+ *   F3S_NO_REORDER=1           work list in window order instead of
+ *                              decreasing block count (Section 3.2)
+ *   F3S_NARROW_GATHER=1        the fp16 -> fp32 forward gathers K and V rows
+ *                              in 4-byte words instead of 16-byte chunks (the
+ *                              access granularity without the register
+ *                              remapping of Section 3.4); other type pairs
+ *                              then return F3S_ERR_UNSUPPORTED
  *   row_ptr  int32[N+1], row_ptr[0] == 0, non-decreasing
  *   col_idx  int32[row_ptr[N]], every entry in [0, N); order inside a row is
  *            free and repeated entries count once (A is binary, Section 3.1)

@@ -217,7 +217,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(tmp.alloc(&split_pieces, (int64_t)T + 1));
     HIP_TRY(tmp.alloc(&split_one, (int64_t)T + 1));
     const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
-    p->flags = reorder ? 0 : 1;
+    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0);
     HIP_TRY(launch_bin_keys(nb, T, piece, reorder, npieces, key, split_pieces,
                             split_one, s));
     HIP_TRY(launch_scan(split_pieces, split_pieces, T, s));  // -> slot base
@@ -434,6 +434,9 @@ f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const
         in_dtype != F3S_DTYPE_FP8_E4M3)
         return fail(F3S_ERR_UNSUPPORTED);
     if (out_dtype != F3S_DTYPE_F32 && out_dtype != F3S_DTYPE_F16)
+        return fail(F3S_ERR_UNSUPPORTED);
+    // the narrow-gather ablation exists for fp16 -> fp32 only
+    if ((p->flags & 2) && (in_dtype != F3S_DTYPE_F16 || out_dtype != F3S_DTYPE_F32))
         return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;

@@ -43,7 +43,7 @@ struct f3s_plan_s {
     int32_t n_items = 0;
     int32_t n_split = 0;
     int32_t n_pieces = 0;
-    int32_t flags = 0;           // bit 0: work list in window order
+    int32_t flags = 0;           // bit 0: work list in window order; bit 1: narrow gathers
     uint64_t id = 0;             // process-unique plan id
     uint64_t transpose_of = 0;   // id of the plan this one transposes (0: none)
     int32_t *blk_off = nullptr;  // [T + 1]
@@ -125,6 +125,10 @@ hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
 hipError_t launch_fused_bf16(const f3s_plan_s &p, const void *Q, const void *K,
                              const void *V, void *O, bool out_f16, float *lse, int32_t H,
                              int32_t d, float scale_log2, hipStream_t s);
+// Ablation: fp16 -> fp32 forward with 4-byte K/V gathers (plan flag bit 1).
+hipError_t launch_fused_narrow(const f3s_plan_s &p, const void *Q, const void *K,
+                               const void *V, void *O, float *lse, int32_t H, int32_t d,
+                               float scale_log2, hipStream_t s);
 hipError_t launch_fused_fp8(const f3s_plan_s &p, const void *Q, const void *K,
                             const void *V, void *O, bool out_f16, float *lse, int32_t H,
                             int32_t d, float scale_log2, hipStream_t s);

@@ -11,6 +11,10 @@ hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
     if (in_type == kInBF16) return launch_fused_bf16(p, Q, K, V, O, out_f16, lse, H, d, sl2, s);
     if (in_type == kInFP8) return launch_fused_fp8(p, Q, K, V, O, out_f16, lse, H, d, sl2, s);
     if (in_type != kInF16) return hipErrorInvalidValue;
+    if (p.flags & 2) {
+        if (out_f16) return hipErrorInvalidValue;
+        return launch_fused_narrow(p, Q, K, V, O, lse, H, d, sl2, s);
+    }
     return out_f16 ? launch_in<kInF16, true>(p, Q, K, V, O, lse, H, d, sl2, s)
                    : launch_in<kInF16, false>(p, Q, K, V, O, lse, H, d, sl2, s);
 }

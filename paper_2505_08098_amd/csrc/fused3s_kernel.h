@@ -63,11 +63,14 @@ template <> struct WavesPerSimd<64> { static constexpr int value = 4; };
 template <> struct WavesPerSimd<96> { static constexpr int value = 3; };
 template <> struct WavesPerSimd<128> { static constexpr int value = 2; };
 template <> struct WavesPerSimd<160> { static constexpr int value = 2; };
-// The bf16 variant holds the second probability term: one wave less at d=32.
-template <int D, int kIn>
+// The bf16 variant holds the second probability term: one wave less at
+// d = 32.  The narrow-gather ablation holds an address per 4-byte word: one
+// wave less where it would otherwise spill (d = 64, 96, 160).
+template <int D, int kIn, bool kNarrow = false>
 constexpr int waves_per_simd()
 {
-    return WavesPerSimd<D>::value - (kIn == kInBF16 && D == 32 ? 1 : 0);
+    return WavesPerSimd<D>::value - (kIn == kInBF16 && D == 32 ? 1 : 0) -
+           (kNarrow && (D == 64 || D == 96 || D == 160) ? 1 : 0);
 }
 
 // Score product for the input storage type (16-bit operands as raw bits).
@@ -121,6 +124,18 @@ __device__ __forceinline__ h8 widen_fp8x8(uint64_t raw)
     return r;
 }
 
+// Narrow-gather staging: word cc of `w` is word (m & 3) of chunk
+// (m & ~3) + cc of the row starting at `row`.
+__device__ __forceinline__ void stage_words(_Float16 *row, int m, h8 w)
+{
+    typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+    const u4v words = __builtin_bit_cast(u4v, w);
+    const int m0 = m & ~3, qd = m & 3;
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc)
+        *reinterpret_cast<uint32_t *>(row + 8 * (m0 + cc) + 2 * qd) = words[cc];
+}
+
 // Four fp32 results -> the output type at p (16-byte or 8-byte store).
 template <bool kOutH>
 __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
@@ -138,10 +153,15 @@ __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
 // kIn: storage type of Q, K, V (kInF16, kInBF16: 16-bit raw bits; kInFP8:
 // e4m3 bytes, widened to fp16 on the way into registers / LDS, so the
 // products are the fp16 ones).  kOutH: O is fp16 instead of fp32.  kWide:
-// Q/K/V may exceed 4 GiB, so gathers use 64-bit addresses.
-template <int D, bool kWide, int kIn, bool kOutH>
+// Q/K/V may exceed 4 GiB, so gathers use 64-bit addresses.  kNarrow (an
+// ablation of the coalescing layout, fp16 inputs only): K and V are
+// gathered in 4-byte words -- consecutive lanes of a quad read consecutive
+// words of a row, each lane taking one word of each of the quad's four
+// 16-byte chunks -- instead of one 16-byte chunk per lane, i.e. the access
+// granularity without the register remapping of Section 3.4.
+template <int D, bool kWide, int kIn, bool kOutH, bool kNarrow = false>
 __global__ __launch_bounds__(64)
-__attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s(
+__attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const void *__restrict__ Qv,
     const void *__restrict__ Kv, const void *__restrict__ Vv,
@@ -235,7 +255,29 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
         for (int j = 0; j < NI; ++j) {
             const int f = lane + 64 * j;
             const int col = __shfl(c, f / LPR);
-            if constexpr (kWide) {
+            if constexpr (kNarrow) {
+                // word qd of chunks m0 .. m0+3 (the quad's chunks: LPR is a
+                // multiple of 4, so the quad lies in one row)
+                static_assert(EB == 2, "narrow gathers are defined for 16-bit inputs");
+                typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+                const int m = f % LPR, m0 = m & ~3, qd = m & 3;
+                u4v wk, wv;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+                    if constexpr (kWide) {
+                        const int64_t off = (int64_t)col * ld * EB + 16 * (m0 + cc) + 4 * qd;
+                        wk[cc] = *reinterpret_cast<const uint32_t *>(K + off);
+                        wv[cc] = *reinterpret_cast<const uint32_t *>(V + off);
+                    } else {
+                        const uint32_t off = (uint32_t)col * (uint32_t)(EB * ld) +
+                                             16u * (m0 + cc) + 4u * qd;
+                        wk[cc] = *reinterpret_cast<const uint32_t *>(K + off);
+                        wv[cc] = *reinterpret_cast<const uint32_t *>(V + off);
+                    }
+                }
+                kst[j] = __builtin_bit_cast(h8, wk);
+                vst[j] = __builtin_bit_cast(h8, wv);
+            } else if constexpr (kWide) {
                 const int64_t off = (int64_t)col * ld * EB + 16 * (f % LPR);
                 kst[j] = *reinterpret_cast<const h8 *>(K + off);
                 vst[j] = *reinterpret_cast<const h8 *>(V + off);
@@ -261,7 +303,9 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
         for (int j = 0; j < NI; ++j) {
             const int f = lane + 64 * j;
             _Float16 *dst = &tile[(f / LPR) * LSK + CE * (f % LPR)];
-            if constexpr (EB == 1) {
+            if constexpr (kNarrow) {
+                stage_words(&tile[(f / LPR) * LSK], f % LPR, kst[j]);
+            } else if constexpr (EB == 1) {
                 h8 lo, hi;
                 widen_fp8x16(kst[j], lo, hi);
                 *reinterpret_cast<h8 *>(dst) = lo;
@@ -290,7 +334,9 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn>(), 8))) void k_fused3s
         for (int j = 0; j < NI; ++j) {
             const int f = lane + 64 * j;
             _Float16 *dst = &tile[(f / LPR) * LSV + CE * (f % LPR)];
-            if constexpr (EB == 1) {
+            if constexpr (kNarrow) {
+                stage_words(&tile[(f / LPR) * LSV], f % LPR, vst[j]);
+            } else if constexpr (EB == 1) {
                 h8 lo, hi;
                 widen_fp8x16(vst[j], lo, hi);
                 *reinterpret_cast<h8 *>(dst) = lo;
@@ -484,14 +530,15 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
 // Heads are launched in groups whose partial results fit the plan's scratch
 // (nh * D <= 256 floats per piece row); without split windows all heads go
 // in one launch.
-template <int D, int kIn, bool kOutH>
+template <int D, int kIn, bool kOutH, bool kNarrow = false>
 hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                     const void *V, void *O, float *lse, int32_t H, float sl2,
                     hipStream_t s)
 {
     const int32_t ld = H * D;
     const bool wide = (uint64_t)p.N * ld * elem_bytes<kIn>() > 0xFFFFFFF0ull;
-    auto kern = wide ? k_fused3s<D, true, kIn, kOutH> : k_fused3s<D, false, kIn, kOutH>;
+    auto kern = wide ? k_fused3s<D, true, kIn, kOutH, kNarrow>
+                     : k_fused3s<D, false, kIn, kOutH, kNarrow>;
     const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
     for (int32_t h0 = 0; h0 < H; h0 += group) {
         const int32_t nh = H - h0 < group ? H - h0 : group;
@@ -517,19 +564,19 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
 }
 
 // Dispatch over the feature size for one input storage type.
-template <int kIn, bool kOutH>
+template <int kIn, bool kOutH, bool kNarrow = false>
 hipError_t launch_in(const f3s_plan_s &p, const void *Q, const void *K, const void *V,
                      void *O, float *lse, int32_t H, int32_t d, float sl2, hipStream_t s)
 {
     switch (d) {
-    case 32: return launch_d<32, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 64: return launch_d<64, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 96: return launch_d<96, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 128: return launch_d<128, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 160: return launch_d<160, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 192: return launch_d<192, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 224: return launch_d<224, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
-    case 256: return launch_d<256, kIn, kOutH>(p, Q, K, V, O, lse, H, sl2, s);
+    case 32: return launch_d<32, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 64: return launch_d<64, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 96: return launch_d<96, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 128: return launch_d<128, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 160: return launch_d<160, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 192: return launch_d<192, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 224: return launch_d<224, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 256: return launch_d<256, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
     default: return hipErrorInvalidValue;
     }
 }

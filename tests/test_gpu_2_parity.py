@@ -339,3 +339,23 @@ def test_split_windows_merge_all_feature_sizes(gpu, oracle, monkeypatch, d):
         fin = np.isfinite(reflse)
         assert np.array_equal(np.isfinite(lse[:, h]), fin)
         assert np.abs(lse[fin, h] - reflse[fin]).max() < 2e-3
+
+
+@pytest.mark.parametrize("k", [1, 2, 4])
+def test_narrow_gather_ablation_is_bit_identical(gpu, monkeypatch, k):
+    """F3S_NARROW_GATHER=1 only changes how K and V rows reach LDS (4-byte
+    words instead of 16-byte chunks): same tiles, same arithmetic, so the
+    output is bit-identical; other type pairs are refused."""
+    c = W.make_config(k)
+    q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    ref, ref_lse = gpu.forward(plan, q, kk, v, scale=c["scale"])
+    monkeypatch.setenv("F3S_NARROW_GATHER", "1")
+    narrow = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    assert narrow.info["flags"] & 2
+    got, got_lse = gpu.forward(narrow, q, kk, v, scale=c["scale"])
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref) and torch.equal(got_lse, ref_lse)
+    with pytest.raises(gpu.F3SError) as e:
+        gpu.forward_typed(narrow, q, kk, v, out_dtype=torch.float16)
+    assert e.value.code == 3
