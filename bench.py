@@ -122,6 +122,28 @@ def backward_bytes(info, info_t, d, heads=1):
     return heads * (dq + dkdv) + plan_bytes
 
 
+def cold_mall_ms(args, call, stream, dev):
+    """Mean ms of --cold-steps calls, each after writing a 1 GiB scrub buffer
+    (4x the Infinity Cache), timed with events around the call only."""
+    if args.cold_steps <= 0:
+        return None
+    import numpy as np
+    import torch
+    scrub = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    times = []
+    for k in range(args.cold_steps):
+        scrub.fill_(float(k))
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        call()
+        b.record(stream)
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    del scrub
+    return round(float(np.mean(times)), 5)
+
+
 def copy_calibration(args, out, dev):
     """Three plain device copies of --copy-calib-mib MiB after the timed
     region: reference dispatches of known size for scaling HBM byte
@@ -210,6 +232,10 @@ def main():
                     help="storage type of Q, K, V (bf16: f3s_forward_typed)")
     ap.add_argument("--out-dtype", default="f32", choices=["f32", "f16"],
                     help="type of O (f16: f3s_forward_typed)")
+    ap.add_argument("--cold-steps", type=int, default=5,
+                    help="after the timed region, calls timed one by one after a 1 GiB "
+                         "scrub write each (L2 and the 256 MB Infinity Cache cold); "
+                         "reported as ms_cold_mall, not in value")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run 3 plain device copies of this many MiB "
                          "(reference dispatches for scaling HBM byte counters)")
@@ -282,6 +308,7 @@ def main():
     wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
     per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
     ms = float(per.mean())
+    cold = cold_mall_ms(args, call, stream, dev)
 
     flops_eff = 4.0 * info["nnz"] * d * H
     value = flops_eff / (ms * 1e-3) / 1e9
@@ -321,6 +348,7 @@ def main():
         "ms_median": round(float(np.median(per)), 5),
         "ms_p90": round(float(np.percentile(per, 90)), 5),
         "wall_ms_per_step": round(wall_ms, 5),
+        "ms_cold_mall": cold,
         "plan_ms": round(info["build_ms"], 3),
         "plan": {k: info[k] for k in ("n_windows", "n_unique", "n_blocks", "max_blocks",
                                       "piece_blocks", "n_items", "n_split", "n_pieces")},
