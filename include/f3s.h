@@ -181,7 +181,7 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t plan);
  *                 8-byte aligned.  The dK/dV pass gathers this one 8-byte
  *                 record for every row attending to a key.
  *   dQ, dK, dV    device fp32 [N, n_heads, d], every element written
- *   d             32, 64, 96 or 128
+ *   d             multiple of 32, 32 <= d <= 256 (as the forward)
  * P and dS enter the products as fp16 (round to nearest even).  Outputs must
  * not overlap each other or any input; 16-byte aligned (lse: 4, row_stats: 8).
  * Asynchronous on `stream`, no allocation.  Deterministic (no atomics).

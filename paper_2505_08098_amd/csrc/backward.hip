@@ -20,6 +20,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Waves per SIMD (d >= 160: one wave, the accumulators spill into AGPRs).
 template <int D> struct BwdWaves { static constexpr int value = 1; };
 template <> struct BwdWaves<32> { static constexpr int value = 4; };
 template <> struct BwdWaves<64> { static constexpr int value = 2; };
@@ -442,11 +443,13 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     // dK, dV: windows of A^T; partials need 2*16*D floats per (piece, head)
     {
         auto kern = wide ? k_bwd_dkdv<D, true> : k_bwd_dkdv<D, false>;
-        const int32_t cap = kMaxD / (2 * D);
+        // the transposed plan's partial rows hold part_row floats
+        const int32_t cap = pt.part_row / (2 * D);
+        if (pt.n_split > 0 && cap < 1) return hipErrorInvalidValue;
         const int32_t group = pt.n_split > 0 ? (cap < H ? cap : H) : H;
         for (int32_t h0 = 0; h0 < H; h0 += group) {
             const int32_t nh = H - h0 < group ? H - h0 : group;
-            if (pt.n_split > 0 && (int64_t)nh * 2 * D > kMaxD) return hipErrorInvalidValue;
+            if (pt.n_split > 0 && (int64_t)nh * 2 * D > pt.part_row) return hipErrorInvalidValue;
             if (pt.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)pt.n_items * nh), 64, 0, s>>>(
                     pt.items, pt.cols, pt.mask, q, k, v, gr, stats, dK, dV, pt.part_o,
@@ -476,6 +479,10 @@ hipError_t launch_backward(const f3s_plan_s &p, const f3s_plan_s &pt, const void
     case 64: return launch_bwd_d<64>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
     case 96: return launch_bwd_d<96>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
     case 128: return launch_bwd_d<128>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 160: return launch_bwd_d<160>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 192: return launch_bwd_d<192>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 224: return launch_bwd_d<224>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
+    case 256: return launch_bwd_d<256>(p, pt, Q, K, V, O, G, lse, row_stats, dQ, dK, dV, H, sl2, scale, s);
     default: return hipErrorInvalidValue;
     }
 }

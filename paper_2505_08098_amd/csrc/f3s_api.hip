@@ -366,6 +366,27 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
         return nullptr;
     }
     t->transpose_of = src->id;
+    // the dK/dV pass keeps two partials (dK, dV) per piece row: double the
+    // partial buffer so a launch group still holds heads with nh * d <= kMaxD
+    if (t->n_pieces > 0) {
+        int prev = 0;
+        hipError_t e = hipGetDevice(&prev);
+        if (e == hipSuccess) e = hipSetDevice(t->device);
+        if (e == hipSuccess) {
+            (void)hipFree(t->part_o);
+            t->device_bytes -= (int64_t)t->n_pieces * f3s::kWindowRows * t->part_row * 4;
+            t->part_o = nullptr;
+            e = plan_alloc(t, &t->part_o,
+                           (int64_t)t->n_pieces * f3s::kWindowRows * 2 * f3s::kMaxD);
+            if (e == hipSuccess) t->part_row = 2 * f3s::kMaxD;
+        }
+        (void)hipSetDevice(prev);
+        if (e != hipSuccess) {
+            f3s_destroy(t);
+            fail(from_hip(e));
+            return nullptr;
+        }
+    }
     t->build_ms = std::chrono::duration<double, std::milli>(
                       std::chrono::steady_clock::now() - t0).count();
     return t;
@@ -490,7 +511,7 @@ f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void
 {
     if (!p || !pt || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (pt->transpose_of != p->id || pt->N != p->N) return fail(F3S_ERR_INVALID_VALUE);
-    if (d < 32 || d > 128 || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
+    if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
     const void *ins[] = {Q, K, V, dO};

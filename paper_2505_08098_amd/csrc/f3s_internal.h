@@ -53,7 +53,9 @@ struct f3s_plan_s {
     int32_t *merges = nullptr;   // [3 * n_split]
     // Partial results of split windows for one launch group of nh heads
     // (nh * d <= kMaxD): slot (piece, head) = piece * nh + head.
-    float *part_o = nullptr;     // [n_pieces * 16 * kMaxD]
+    float *part_o = nullptr;     // [n_pieces * 16 * part_row]
+    int32_t part_row = f3s::kMaxD;  // floats per piece row of part_o (transposed plans:
+                                 // 2 * kMaxD, for the dK and dV partials)
     float *part_ml = nullptr;    // [n_pieces * (kMaxD/32) * 32]: 16 maxima, 16 sums
     int64_t device_bytes = 0;
     int64_t bsb_bytes = 0;

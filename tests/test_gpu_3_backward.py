@@ -102,7 +102,7 @@ def test_transposed_plan_is_the_plan_of_the_transpose(gpu, oracle, k):
     assert np.array_equal(got["cols"], b["cols"]) and np.array_equal(got["mask"], b["mask"])
 
 
-@pytest.mark.parametrize("d", [32, 64, 96, 128])
+@pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
 @pytest.mark.parametrize("N", [1, 17, 300])
 def test_gradients_random_patterns(gpu, oracle, d, N):
     rng = np.random.default_rng(d + 7 * N)
@@ -122,10 +122,13 @@ def test_gradients_workloads(gpu, oracle, k):
                c["scale"])
 
 
-def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch):
+@pytest.mark.parametrize("H,d", [(3, 64), (2, 160), (2, 256)])
+def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d):
+    """Split windows in both plans; for d > 128 the dK/dV partials of one
+    head fill a whole (double-width) partial row of the transposed plan."""
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
     rng = np.random.default_rng(12)
-    N, H, d = 3000, 3, 64
+    N = 3000
     rows = [rng.choice(N, size=300, replace=False) if i < 20 else
             rng.choice(N, size=6, replace=False) for i in range(N)]
     rp = np.zeros(N + 1, dtype=np.int32)
@@ -161,8 +164,8 @@ def test_backward_argument_errors(gpu):
         gpu.backward(plan, other, q, k, v, O, q, lse)
     assert e.value.code == 1
     plan_t = plan.transpose()
-    big = torch.zeros((c["N"], 160), dtype=torch.float16, device=DEV)
-    Ob = torch.zeros((c["N"], 160), dtype=torch.float32, device=DEV)
-    with pytest.raises(gpu.F3SError) as e:   # d above 128
+    big = torch.zeros((c["N"], 288), dtype=torch.float16, device=DEV)
+    Ob = torch.zeros((c["N"], 288), dtype=torch.float32, device=DEV)
+    with pytest.raises(gpu.F3SError) as e:   # d above 256
         gpu.backward(plan, plan_t, big, big, big, Ob, big, lse)
     assert e.value.code == 3
