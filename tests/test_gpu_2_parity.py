@@ -359,3 +359,51 @@ def test_narrow_gather_ablation_is_bit_identical(gpu, monkeypatch, k):
     with pytest.raises(gpu.F3SError) as e:
         gpu.forward_typed(narrow, q, kk, v, out_dtype=torch.float16)
     assert e.value.code == 3
+
+
+def _sample_rows_reference(oracle, rp, ci, S, Q, K, V, scale):
+    """Oracle rows S of a large problem: the rows S and their neighbours are
+    copied into a small problem (neighbour-only rows empty) and the oracle
+    runs on that; rows of S come back in order."""
+    rp = rp.cpu().numpy().astype(np.int64)
+    nb = {int(i): ci[int(rp[i]):int(rp[i + 1])].cpu().numpy() for i in S}
+    U = sorted(set(int(i) for i in S) | set(int(j) for a in nb.values() for j in a))
+    loc = {u: k for k, u in enumerate(U)}
+    rows = [[loc[int(j)] for j in nb[u]] if u in nb else [] for u in U]
+    mrp = np.zeros(len(U) + 1, dtype=np.int32)
+    mrp[1:] = np.cumsum([len(r) for r in rows])
+    mci = np.array([c for r in rows for c in r], dtype=np.int32)
+    idx = torch.tensor(U, device=DEV)
+    q, k, v = (x.index_select(0, idx).cpu().numpy() for x in (Q, K, V))
+    ref = oracle.attention_f64(mrp, mci, q, k, v, scale)
+    return ref[[loc[int(i)] for i in S]]
+
+
+def test_wide_addressing_above_4gib(gpu, oracle):
+    """Q, K, V of more than 4 GiB each (N = 9,000,000 rows, d = 256: gathers
+    switch to 64-bit addresses): sampled rows, including the last ones and
+    rows whose neighbours sit at the top of the arrays, against the oracle."""
+    N, d = 9_000_000, 256
+    assert N * d * 2 > 2 ** 32
+    i = torch.arange(N, dtype=torch.int64, device=DEV)
+    cols = torch.stack([i, (i * 7919 + 13) % N, N - 1 - i], dim=1)
+    ci = cols.reshape(-1).to(torch.int32)
+    rp = (torch.arange(N + 1, dtype=torch.int64, device=DEV) * 3).to(torch.int32)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(7)
+    Q, K, V = (torch.randn((N, d), generator=g, device=DEV, dtype=torch.float32).half()
+               for _ in range(3))
+    plan = gpu.Plan(rp, ci, N)
+    O = gpu.run(plan, Q, K, V, scale=1 / 16)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(8)
+    S = np.unique(np.concatenate([[0, 1, N // 2, N - 2, N - 1],
+                                  rng.integers(0, N, size=120),
+                                  N - 1 - rng.integers(0, 1000, size=40)]))
+    ref = _sample_rows_reference(oracle, rp, ci, S, Q, K, V, 1 / 16)
+    got = O.index_select(0, torch.tensor(S, device=DEV)).cpu().numpy()
+    print(f"  {len(S)} sampled rows", flush=True)
+    _assert_parity(got, ref)
+    plan.close()
+    del Q, K, V, O
+    torch.cuda.empty_cache()

@@ -169,3 +169,52 @@ def test_backward_argument_errors(gpu):
     with pytest.raises(gpu.F3SError) as e:   # d above 256
         gpu.backward(plan, plan_t, big, big, big, Ob, big, lse)
     assert e.value.code == 3
+
+
+def test_backward_wide_addressing_above_4gib(gpu, oracle):
+    """Gradients with Q, K, V, dO of more than 4 GiB each (N = 9,000,000,
+    d = 256: 64-bit gathers in both passes).  Checked on sampled keys: the
+    small oracle problem holds the sampled rows and every row attending to
+    them (with their full neighbour lists), so dQ, dK and dV of the sampled
+    rows are exact there."""
+    N, d, scale = 9_000_000, 256, 1 / 16
+    assert N * d * 2 > 2 ** 32
+    i = torch.arange(N, dtype=torch.int64, device=DEV)
+    ci = torch.stack([i, (i * 7919 + 13) % N, N - 1 - i], dim=1).reshape(-1).to(torch.int32)
+    rp = (torch.arange(N + 1, dtype=torch.int64, device=DEV) * 3).to(torch.int32)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(9)
+    Q, K, V, G = (torch.randn((N, d), generator=gen, device=DEV, dtype=torch.float32).half()
+                  for _ in range(4))
+    plan = gpu.Plan(rp, ci, N)
+    plan_t = plan.transpose()
+    O, lse = gpu.forward(plan, Q, K, V, scale=scale)
+    dQ, dK, dV = gpu.backward(plan, plan_t, Q, K, V, O, G, lse, scale=scale)
+    torch.cuda.synchronize()
+    del O, lse
+    rng = np.random.default_rng(10)
+    S = np.unique(np.concatenate([[0, N - 1, N // 3], rng.integers(0, N, size=20),
+                                  N - 1 - rng.integers(0, 500, size=10)]))
+    St = torch.tensor(S, dtype=torch.int32, device=DEV)
+    attending = (torch.isin(ci, St).nonzero().reshape(-1) // 3).cpu().numpy()
+    R = sorted(set(S.tolist()) | set(attending.tolist()))
+    rpn = rp.cpu().numpy().astype(np.int64)
+    nb = {r: ci[int(rpn[r]):int(rpn[r + 1])].cpu().numpy() for r in R}
+    U = sorted(set(R) | set(int(j) for a in nb.values() for j in a))
+    loc = {u: k for k, u in enumerate(U)}
+    rows = [[loc[int(j)] for j in nb[u]] if u in nb else [] for u in U]
+    mrp = np.zeros(len(U) + 1, dtype=np.int32)
+    mrp[1:] = np.cumsum([len(r) for r in rows])
+    mci = np.array([c for r in rows for c in r], dtype=np.int32)
+    idx = torch.tensor(U, device=DEV)
+    q, k, v, gg = (x.index_select(0, idx).cpu().numpy() for x in (Q, K, V, G))
+    gg[[loc[u] for u in U if u not in nb]] = 0    # rows outside R contribute nothing
+    ref = oracle.attention_bwd_f64(mrp, mci, q, k, v, gg, scale)
+    sel = torch.tensor(S, device=DEV)
+    print(f"  {len(S)} sampled keys, {len(R)} rows in the small problem", flush=True)
+    for name, got, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
+        _check(name, got.index_select(0, sel).cpu().numpy(), r[[loc[int(s)] for s in S]])
+    plan.close()
+    plan_t.close()
+    del Q, K, V, G, dQ, dK, dV
+    torch.cuda.empty_cache()
