@@ -236,3 +236,40 @@ def test_fp8_multi_head_split_windows(gpu, oracle, monkeypatch):
         ref = oracle.attention_e4m3_f64(c["row_ptr"], c["col_idx"],
                                         *(np.ascontiguousarray(x[:, h]) for x in X), 0.125)
         _check(O[:, h], ref)
+
+
+def test_fp8_wide_addressing_above_4gib(gpu, oracle):
+    """fp8 Q, K, V of more than 4 GiB each (N = 17,000,000, d = 256: one byte
+    per element, so 64-bit gathers start above 16.7M rows), sampled rows
+    against the oracle's e4m3 entry."""
+    N, d, scale = 17_000_000, 256, 1 / 16
+    assert N * d > 2 ** 32
+    i = torch.arange(N, dtype=torch.int64, device=DEV)
+    ci = torch.stack([i, (i * 7919 + 13) % N, N - 1 - i], dim=1).reshape(-1).to(torch.int32)
+    rp = (torch.arange(N + 1, dtype=torch.int64, device=DEV) * 3).to(torch.int32)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(11)
+    X = [torch.randn((N, d), generator=gen, device=DEV, dtype=torch.float32)
+         .to(torch.float8_e4m3fn) for _ in range(3)]
+    plan = gpu.Plan(rp, ci, N)
+    O, _ = gpu.forward_typed(plan, *X, scale=scale)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(12)
+    S = np.unique(np.concatenate([[0, N - 1], rng.integers(0, N, size=60),
+                                  N - 1 - rng.integers(0, 300, size=20)]))
+    rpn = rp.cpu().numpy().astype(np.int64)
+    nb = {int(r): ci[int(rpn[r]):int(rpn[r + 1])].cpu().numpy() for r in S}
+    U = sorted(set(int(s) for s in S) | set(int(j) for a in nb.values() for j in a))
+    loc = {u: k for k, u in enumerate(U)}
+    rows = [[loc[int(j)] for j in nb[u]] if u in nb else [] for u in U]
+    mrp = np.zeros(len(U) + 1, dtype=np.int32)
+    mrp[1:] = np.cumsum([len(r) for r in rows])
+    mci = np.array([c for r in rows for c in r], dtype=np.int32)
+    idx = torch.tensor(U, device=DEV)
+    q, k, v = (x.index_select(0, idx).view(torch.uint8).cpu().numpy() for x in X)
+    ref = oracle.attention_e4m3_f64(mrp, mci, q, k, v, scale)[[loc[int(s)] for s in S]]
+    got = O.index_select(0, torch.tensor(S, device=DEV)).cpu().numpy()
+    _check(got, ref)
+    plan.close()
+    del X, O
+    torch.cuda.empty_cache()
