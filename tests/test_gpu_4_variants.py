@@ -266,7 +266,7 @@ def test_fp8_wide_addressing_above_4gib(gpu, oracle):
     mrp[1:] = np.cumsum([len(r) for r in rows])
     mci = np.array([c for r in rows for c in r], dtype=np.int32)
     idx = torch.tensor(U, device=DEV)
-    q, k, v = (x.index_select(0, idx).view(torch.uint8).cpu().numpy() for x in X)
+    q, k, v = (x.view(torch.uint8).index_select(0, idx).cpu().numpy() for x in X)
     ref = oracle.attention_e4m3_f64(mrp, mci, q, k, v, scale)[[loc[int(s)] for s in S]]
     got = O.index_select(0, torch.tensor(S, device=DEV)).cpu().numpy()
     _check(got, ref)
