@@ -67,3 +67,15 @@ def test_null_handles_are_rejected_without_a_device(lib):
                                                     ctypes.c_void_p]
     lib.f3s_run.restype = ctypes.c_int
     assert lib.f3s_run(None, None, None, None, None, 64, 1.0, None) == 1
+
+
+def test_plain_c_program_builds_against_the_header():
+    """A C11 translation unit including only include/f3s.h (and the HIP
+    runtime API it names) compiles and links against libf3s.so (the GPU test
+    runs the program)."""
+    import sys
+    sys.path.insert(0, ROOT)
+    import __graft_entry__ as ge
+    path = ge.build_c_driver()
+    out = subprocess.run(["ldd", path], capture_output=True, text=True, check=True).stdout
+    assert "libf3s.so" in out
