@@ -136,6 +136,14 @@ __device__ __forceinline__ void stage_words(_Float16 *row, int m, h8 w)
         *reinterpret_cast<uint32_t *>(row + 8 * (m0 + cc) + 2 * qd) = words[cc];
 }
 
+// v where sel is all ones, -inf where sel is zero (one bit-select).
+__device__ __forceinline__ float masked_score(float v, int sel)
+{
+    const uint32_t ninf = 0xff800000u;
+    return __builtin_bit_cast(float, (__builtin_bit_cast(uint32_t, v) & (uint32_t)sel) |
+                                         (ninf & ~(uint32_t)sel));
+}
+
 // Four fp32 results -> the output type at p (16-byte or 8-byte store).
 template <bool kOutH>
 __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
@@ -354,17 +362,19 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
             load_cols(b + 4);
         }
         // ---- mask + online softmax (base 2) ----
+        // bit r of the nibble -> all-ones / zero word (signed bit-field
+        // extract), then a bit-select between the score and -inf
         float x[8];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            x[r] = (nib0 >> r) & 1u ? s0[r] * sl2 : -__builtin_inff();
-            x[4 + r] = (nib1 >> r) & 1u ? s1[r] * sl2 : -__builtin_inff();
+            x[r] = masked_score(s0[r] * sl2, __builtin_amdgcn_sbfe((int)nib0, r, 1));
+            x[4 + r] = masked_score(s1[r] * sl2, __builtin_amdgcn_sbfe((int)nib1, r, 1));
         }
         float mloc = x[0];
 #pragma unroll
         for (int e = 1; e < 8; ++e) mloc = fmaxf(mloc, x[e]);
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        mloc = max_xor16(mloc);
+        mloc = max_xor32(mloc);
         const float m_new = fmaxf(m_run, mloc);
         const float m_ref = m_new == -__builtin_inff() ? 0.f : m_new;
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
@@ -384,11 +394,13 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
             }
         } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const _Float16 ph = (_Float16)__builtin_amdgcn_exp2f(x[e] - m_ref);
-                p[e] = ph;
-                psum += (float)ph;
-            }
+            for (int e = 0; e < 8; ++e)
+                p[e] = (_Float16)__builtin_amdgcn_exp2f(x[e] - m_ref);
+            // the sum of the rounded values, two at a time (dot with 1, 1)
+            const h2 one = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+            for (int e = 0; e < 8; e += 2)
+                psum = __builtin_amdgcn_fdot2(h2{p[e], p[e + 1]}, one, psum, false);
         }
         l_run = l_run * alpha + psum;
         m_run = m_new;

@@ -49,6 +49,23 @@ __device__ __forceinline__ h4 lds_read_tr(const _Float16 *p)
     return __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)p));
 }
 
+// Max / sum of v over lanes l and l ^ 16, and over l and l ^ 32, with the
+// cross-row swap instructions (VALU, no LDS round trip): called with the
+// same value twice, v_permlane16_swap / v_permlane32_swap leave in each lane
+// the pair {v[l], v[l ^ 16]} / {v[l], v[l ^ 32]} (checked on the GPU).
+__device__ __forceinline__ float max_xor16(float v)
+{
+    const int b = __builtin_bit_cast(int, v);
+    const auto r = __builtin_amdgcn_permlane16_swap(b, b, false, false);
+    return fmaxf(__builtin_bit_cast(float, (int)r[0]), __builtin_bit_cast(float, (int)r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v)
+{
+    const int b = __builtin_bit_cast(int, v);
+    const auto r = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+    return fmaxf(__builtin_bit_cast(float, (int)r[0]), __builtin_bit_cast(float, (int)r[1]));
+}
+
 // Orders this wave's LDS accesses (one wave per workgroup).
 __device__ __forceinline__ void wave_lds_fence()
 {
