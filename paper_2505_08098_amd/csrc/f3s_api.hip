@@ -27,46 +27,41 @@ f3s_status_t from_hip(hipError_t e)
     return e == hipErrorOutOfMemory ? F3S_ERR_OUT_OF_MEMORY : F3S_ERR_HIP;
 }
 
-// Device scratch owned by one f3s_plan call; freed on every exit path.
-struct Scratch {
-    std::vector<void *> ptrs;
-    ~Scratch()
-    {
-        for (void *p : ptrs) (void)hipFree(p);
-    }
+// One device allocation carved into 256-byte aligned pieces (the scratch of
+// one f3s_plan call, or a plan's arrays); sizing pass first (add), then one
+// hipMalloc (alloc), then the pieces in the same order (take).
+struct Arena {
+    char *base = nullptr;
+    size_t used = 0, cap = 0;
+    static size_t round(size_t b) { return (b + 255) & ~(size_t)255; }
     template <typename T>
-    hipError_t alloc(T **out, int64_t count)
+    void add(int64_t count)
     {
-        *out = nullptr;
-        if (count <= 0) count = 1;
-        void *p = nullptr;
-        hipError_t e = hipMalloc(&p, (size_t)count * sizeof(T));
-        if (e != hipSuccess) return e;
-        ptrs.push_back(p);
-        *out = static_cast<T *>(p);
-        return hipSuccess;
+        cap += round((size_t)(count > 0 ? count : 1) * sizeof(T));
+    }
+    hipError_t alloc() { return hipMalloc((void **)&base, cap ? cap : 256); }
+    template <typename T>
+    T *take(int64_t count)
+    {
+        T *p = reinterpret_cast<T *>(base + used);
+        used += round((size_t)(count > 0 ? count : 1) * sizeof(T));
+        return p;
     }
 };
 
-template <typename T>
-hipError_t plan_alloc(f3s_plan_s *p, T **out, int64_t count)
-{
-    *out = nullptr;
-    if (count <= 0) count = 1;
-    void *ptr = nullptr;
-    hipError_t e = hipMalloc(&ptr, (size_t)count * sizeof(T));
-    if (e != hipSuccess) return e;
-    *out = static_cast<T *>(ptr);
-    p->device_bytes += (int64_t)((size_t)count * sizeof(T));
-    return hipSuccess;
-}
+// Scratch arena freed on every exit path of a plan build.
+struct ScratchArena : Arena {
+    ~ScratchArena()
+    {
+        if (base) (void)hipFree(base);
+    }
+};
 
 void free_plan_arrays(f3s_plan_s *p)
 {
-    void *arrs[] = {p->blk_off, p->cols, p->mask, p->items, p->merges, p->part_o,
-                    p->part_ml};
-    for (void *a : arrs)
-        if (a) (void)hipFree(a);
+    if (p->store) (void)hipFree(p->store);
+    if (p->part_store) (void)hipFree(p->part_store);
+    p->store = p->part_store = nullptr;
     p->blk_off = nullptr;
     p->cols = nullptr;
     p->mask = nullptr;
@@ -74,6 +69,35 @@ void free_plan_arrays(f3s_plan_s *p)
     p->merges = nullptr;
     p->part_o = nullptr;
     p->part_ml = nullptr;
+}
+
+// Partial-result buffers of split windows: part_row floats per piece row
+// for O (kMaxD for a plan, 2 * kMaxD for a transposed plan, which holds the
+// dK and dV partials), and the (m, l) records.  Replaces any previous ones.
+hipError_t alloc_parts(f3s_plan_s *p, int32_t part_row)
+{
+    if (p->part_store) {
+        (void)hipFree(p->part_store);
+        p->device_bytes -= (int64_t)p->part_bytes;
+        p->part_store = nullptr;
+        p->part_o = p->part_ml = nullptr;
+        p->part_bytes = 0;
+    }
+    p->part_row = part_row;
+    if (p->n_pieces == 0) return hipSuccess;
+    Arena a;
+    a.add<float>((int64_t)p->n_pieces * f3s::kWindowRows * part_row);
+    // one (m, l) record of 16 + 16 floats per piece and head of a launch
+    // group; a group holds at most kMaxD / 32 heads (nh * d <= kMaxD)
+    a.add<float>((int64_t)p->n_pieces * 32 * (f3s::kMaxD / 32));
+    hipError_t e = a.alloc();
+    if (e != hipSuccess) return e;
+    p->part_store = a.base;
+    p->part_bytes = (int64_t)a.cap;
+    p->device_bytes += (int64_t)a.cap;
+    p->part_o = a.take<float>((int64_t)p->n_pieces * f3s::kWindowRows * part_row);
+    p->part_ml = a.take<float>((int64_t)p->n_pieces * 32 * (f3s::kMaxD / 32));
+    return hipSuccess;
 }
 
 int env_int(const char *name, int dflt)
@@ -122,140 +146,158 @@ int choose_piece(int64_t n_blocks, int32_t max_blocks, int device)
     return (int)(piece < cap ? piece : cap);
 }
 
-f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *col_idx)
+// Device-side statistics of a plan build, read back with one copy each
+// time the host needs them.
+struct BuildStats {
+    unsigned long long n_unique;  // sum of distinct columns over windows
+    unsigned long long nnz;       // set bits of all bitmaps
+    int32_t err;                  // malformed CSR
+    int32_t n_heavy;              // windows too large for the LDS sort
+    int32_t max_blocks;
+    int32_t n_blocks;
+    int32_t n_pieces;
+    int32_t n_split;
+    int32_t n_items;              // total of the work-list histogram
+    int32_t invalid;              // plan integrity check
+};
+
+f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *col_idx,
+                        int32_t part_row)
 {
     using namespace f3s;
     const hipStream_t s = nullptr;
     const int32_t N = p->N;
     const int32_t T = p->T;
-    Scratch tmp;
 
-    // ---- 1. nnz and row_ptr validation --------------------------------
-    int32_t ends[2] = {0, 0};
-    HIP_TRY(hipMemcpy(&ends[0], row_ptr, sizeof(int32_t), hipMemcpyDeviceToHost));
-    HIP_TRY(hipMemcpy(&ends[1], row_ptr + N, sizeof(int32_t), hipMemcpyDeviceToHost));
-    if (ends[0] != 0 || ends[1] < 0) return F3S_ERR_INVALID_CSR;
-    const int32_t nnz = ends[1];
+    // ---- 1. nnz (row_ptr[0] == 0 and monotonicity are checked on the GPU)
+    int32_t nnz = 0;
+    HIP_TRY(hipMemcpy(&nnz, row_ptr + N, sizeof(int32_t), hipMemcpyDeviceToHost));
+    if (nnz < 0) return F3S_ERR_INVALID_CSR;
     if (nnz > 0 && !col_idx) return F3S_ERR_INVALID_VALUE;
     p->nnz_csr = nnz;
 
-    int32_t *err = nullptr;
-    HIP_TRY(tmp.alloc(&err, 4));
-    HIP_TRY(hipMemset(err, 0, 4 * sizeof(int32_t)));
-    HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, err, s));
-    int32_t herr = 0;
-    HIP_TRY(read_scalar(&herr, err));
-    if (herr) return F3S_ERR_INVALID_CSR;
+    // all scratch of the build in one allocation
+    ScratchArena tmp;
+    tmp.add<BuildStats>(1);
+    tmp.add<int32_t>(nnz);               // sorted distinct columns per window
+    for (int k = 0; k < 5; ++k) tmp.add<int32_t>(T);  // u, heavy, nb, npieces, key
+    for (int k = 0; k < 3; ++k) tmp.add<int32_t>((int64_t)T + 1);  // tro, splits
+    tmp.add<int32_t>(scan_tmp_ints(T));
+    HIP_TRY(tmp.alloc());
+    BuildStats *st = tmp.take<BuildStats>(1);
+    int32_t *tmp_cols = tmp.take<int32_t>(nnz);
+    int32_t *u = tmp.take<int32_t>(T), *heavy = tmp.take<int32_t>(T);
+    int32_t *nb = tmp.take<int32_t>(T), *npieces = tmp.take<int32_t>(T);
+    int32_t *key = tmp.take<int32_t>(T);
+    int32_t *tro = tmp.take<int32_t>((int64_t)T + 1);
+    int32_t *split_pieces = tmp.take<int32_t>((int64_t)T + 1);
+    int32_t *split_one = tmp.take<int32_t>((int64_t)T + 1);
+    int32_t *scan_tmp = tmp.take<int32_t>(scan_tmp_ints(T));
+    BuildStats hs;
+    HIP_TRY(hipMemsetAsync(st, 0, sizeof(BuildStats), s));
 
-    // ---- 2. distinct columns per window -------------------------------
-    int32_t *tmp_cols = nullptr, *u = nullptr, *heavy = nullptr, *n_heavy = err + 1;
-    HIP_TRY(tmp.alloc(&tmp_cols, nnz));
-    HIP_TRY(tmp.alloc(&u, T));
-    HIP_TRY(tmp.alloc(&heavy, T));
-    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, T, tmp_cols, u, heavy, n_heavy,
-                               err, s));
-    int32_t hh[2] = {0, 0};
-    HIP_TRY(hipMemcpy(hh, err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost));
-    if (hh[0]) return F3S_ERR_INVALID_CSR;
-    const int32_t n_heavy_h = hh[1];
-    if (n_heavy_h > 0) {
+    // ---- 2. CSR check and distinct columns per window ------------------
+    HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
+    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, T, tmp_cols, u, heavy, &st->n_heavy,
+                               &st->err, s));
+    HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
+    if (hs.err) return F3S_ERR_INVALID_CSR;
+    if (hs.n_heavy > 0) {
         const int32_t words = (N + 31) / 32;
         const int64_t budget = 256ll << 20;  // bitmap workspace per batch
         int64_t per = (int64_t)words * 4;
         int32_t batch = (int32_t)(budget / per);
         if (batch < 1) batch = 1;
-        if (batch > n_heavy_h) batch = n_heavy_h;
-        uint32_t *bitmap = nullptr;
-        HIP_TRY(tmp.alloc(&bitmap, (int64_t)batch * words));
-        for (int32_t first = 0; first < n_heavy_h; first += batch) {
-            const int32_t cnt = n_heavy_h - first < batch ? n_heavy_h - first : batch;
+        if (batch > hs.n_heavy) batch = hs.n_heavy;
+        ScratchArena bm;
+        bm.add<uint32_t>((int64_t)batch * words);
+        HIP_TRY(bm.alloc());
+        uint32_t *bitmap = bm.take<uint32_t>((int64_t)batch * words);
+        for (int32_t first = 0; first < hs.n_heavy; first += batch) {
+            const int32_t cnt = hs.n_heavy - first < batch ? hs.n_heavy - first : batch;
             HIP_TRY(hipMemsetAsync(bitmap, 0, (size_t)cnt * words * 4, s));
-            HIP_TRY(launch_heavy_compact(row_ptr, col_idx, N, heavy + first, cnt,
-                                         bitmap, words, tmp_cols, u, err, s));
+            HIP_TRY(launch_heavy_compact(row_ptr, col_idx, N, heavy + first, cnt, bitmap,
+                                         words, tmp_cols, u, &st->err, s));
         }
-        HIP_TRY(read_scalar(&herr, err));
-        if (herr) return F3S_ERR_INVALID_CSR;
+        HIP_TRY(hipStreamSynchronize(s));  // the bitmap workspace is freed here
     }
 
-    // ---- 3. blocks per window and their prefix (tro) ------------------
-    int32_t *nb = nullptr;
-    HIP_TRY(tmp.alloc(&nb, T));
-    HIP_TRY(plan_alloc(p, &p->blk_off, (int64_t)T + 1));
+    // ---- 3. blocks per window, their prefix (tro), statistics -----------
     HIP_TRY(launch_blocks_per_window(u, T, nb, s));
-    HIP_TRY(launch_scan(nb, p->blk_off, T, s));
-    int32_t B = 0;
-    HIP_TRY(read_scalar(&B, p->blk_off + T));
+    HIP_TRY(launch_scan(nb, tro, T, scan_tmp, &st->n_blocks, s));
+    HIP_TRY(launch_sum_i32(u, T, &st->n_unique, s));
+    HIP_TRY(launch_max_i32(nb, T, &st->max_blocks, s));
+    HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
+    if (hs.err) return F3S_ERR_INVALID_CSR;
+    const int32_t B = hs.n_blocks;
     p->n_blocks = B;
-
-    unsigned long long *acc = nullptr;
-    HIP_TRY(tmp.alloc(&acc, 2));
-    HIP_TRY(hipMemset(acc, 0, 2 * sizeof(unsigned long long)));
-    HIP_TRY(launch_sum_i32(u, T, acc, s));
-    HIP_TRY(hipMemset(err + 2, 0, sizeof(int32_t)));
-    HIP_TRY(launch_max_i32(nb, T, err + 2, s));
-
-    // ---- 4. column lists and bitmaps ----------------------------------
-    HIP_TRY(plan_alloc(p, &p->cols, (int64_t)kBlockCols * B));
-    HIP_TRY(plan_alloc(p, &p->mask, (int64_t)kMaskWords * B));
-    HIP_TRY(hipMemsetAsync(p->mask, 0, (size_t)kMaskWords * B * 4, s));
-    HIP_TRY(launch_fill_windows(row_ptr, col_idx, N, T, tmp_cols, u, p->blk_off,
-                                p->cols, p->mask, s));
-    HIP_TRY(launch_count_bits(p->mask, (int64_t)kMaskWords * B, acc + 1, s));
-    unsigned long long hacc[2] = {0, 0};
-    HIP_TRY(hipMemcpy(hacc, acc, sizeof(hacc), hipMemcpyDeviceToHost));
-    p->n_unique = (int64_t)hacc[0];
-    p->nnz = (int64_t)hacc[1];
-    HIP_TRY(read_scalar(&p->max_blocks, err + 2));
+    p->n_unique = (int64_t)hs.n_unique;
+    p->max_blocks = hs.max_blocks;
     p->bsb_bytes = 4ll * (T + 1) + 4ll * kBlockCols * B + 4ll * kMaskWords * B;
 
-    // ---- 5. heavy-first work list -------------------------------------
+    // ---- 4. work-list shape: piece size, split windows, item count ------
     const int32_t piece = choose_piece(B, p->max_blocks, p->device);
     p->piece = piece;
-    int32_t *npieces, *key, *split_pieces, *split_one;
-    HIP_TRY(tmp.alloc(&npieces, T));
-    HIP_TRY(tmp.alloc(&key, T));
-    HIP_TRY(tmp.alloc(&split_pieces, (int64_t)T + 1));
-    HIP_TRY(tmp.alloc(&split_one, (int64_t)T + 1));
     const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
     p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0);
     HIP_TRY(launch_bin_keys(nb, T, piece, reorder, npieces, key, split_pieces,
                             split_one, s));
-    HIP_TRY(launch_scan(split_pieces, split_pieces, T, s));  // -> slot base
-    HIP_TRY(launch_scan(split_one, split_one, T, s));        // -> split index
-    int32_t tot[2];
-    HIP_TRY(read_scalar(&tot[0], split_pieces + T));
-    HIP_TRY(read_scalar(&tot[1], split_one + T));
-    p->n_pieces = tot[0];
-    p->n_split = tot[1];
+    HIP_TRY(launch_scan(split_pieces, split_pieces, T, scan_tmp, &st->n_pieces, s));
+    HIP_TRY(launch_scan(split_one, split_one, T, scan_tmp, &st->n_split, s));
+    HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
+    p->n_pieces = hs.n_pieces;
+    p->n_split = hs.n_split;
+    const int64_t n_items = (int64_t)T - p->n_split + p->n_pieces;
+    if (n_items > INT32_MAX) return F3S_ERR_UNSUPPORTED;
+    p->n_items = (int32_t)n_items;
 
+    // ---- 5. the plan's arrays: one allocation, plus the partial buffers --
+    {
+        Arena a;
+        a.add<int32_t>((int64_t)T + 1);
+        a.add<int32_t>((int64_t)kBlockCols * B);
+        a.add<uint32_t>((int64_t)kMaskWords * B);
+        a.add<WorkItem>(p->n_items);
+        a.add<int32_t>(3ll * p->n_split);
+        HIP_TRY(a.alloc());
+        p->store = a.base;
+        p->device_bytes += (int64_t)a.cap;
+        p->blk_off = a.take<int32_t>((int64_t)T + 1);
+        p->cols = a.take<int32_t>((int64_t)kBlockCols * B);
+        p->mask = a.take<uint32_t>((int64_t)kMaskWords * B);
+        p->items = a.take<WorkItem>(p->n_items);
+        p->merges = a.take<int32_t>(3ll * p->n_split);
+    }
+    HIP_TRY(alloc_parts(p, part_row));
+    HIP_TRY(hipMemcpyAsync(p->blk_off, tro, sizeof(int32_t) * ((size_t)T + 1),
+                           hipMemcpyDeviceToDevice, s));
+
+    // ---- 6. column lists and bitmaps (and the distinct-pair count) ------
+    HIP_TRY(launch_fill_windows(row_ptr, col_idx, N, T, tmp_cols, u, p->blk_off, p->cols,
+                                p->mask, &st->nnz, s));
+
+    // ---- 7. heavy-first work list: histogram over (key, chunk), scan, scatter
     const int32_t chunk = 64;
     const int32_t nchunks = (T + chunk - 1) / chunk;
     const int64_t cells = (int64_t)(piece + 1) * nchunks;
     if (cells >= INT32_MAX) return F3S_ERR_UNSUPPORTED;
-    int32_t *hist = nullptr;
-    HIP_TRY(tmp.alloc(&hist, cells + 1));
+    ScratchArena hist_arena;
+    hist_arena.add<int32_t>(cells + 1);
+    hist_arena.add<int32_t>(scan_tmp_ints(cells));
+    HIP_TRY(hist_arena.alloc());
+    int32_t *hist = hist_arena.take<int32_t>(cells + 1);
+    int32_t *hist_tmp = hist_arena.take<int32_t>(scan_tmp_ints(cells));
     HIP_TRY(hipMemsetAsync(hist, 0, (size_t)(cells + 1) * 4, s));
     HIP_TRY(launch_bin_hist(npieces, key, T, piece, chunk, nchunks, hist, s));
-    HIP_TRY(launch_scan(hist, hist, (int32_t)cells, s));
-    int32_t n_items = 0;
-    HIP_TRY(read_scalar(&n_items, hist + cells));
-    p->n_items = n_items;
-    HIP_TRY(plan_alloc(p, &p->items, n_items));
-    HIP_TRY(plan_alloc(p, &p->merges, 3ll * p->n_split));
+    HIP_TRY(launch_scan(hist, hist, (int32_t)cells, hist_tmp, &st->n_items, s));
     HIP_TRY(launch_bin_scatter(nb, p->blk_off, npieces, key, split_pieces, split_one,
                                T, piece, chunk, nchunks, hist, p->items, p->merges, s));
-    if (p->n_pieces > 0) {
-        HIP_TRY(plan_alloc(p, &p->part_o, (int64_t)p->n_pieces * kWindowRows * kMaxD));
-        // one (m, l) record of 16 + 16 floats per piece and head of a launch
-        // group; a group holds at most kMaxD / 32 heads (nh * d <= kMaxD)
-        HIP_TRY(plan_alloc(p, &p->part_ml,
-                           (int64_t)p->n_pieces * 32 * (kMaxD / 32)));
-    }
-    // ---- 6. integrity check of the finished plan ------------------------
-    HIP_TRY(hipMemset(err, 0, sizeof(int32_t)));
-    HIP_TRY(launch_validate_plan(*p, err, s));
-    HIP_TRY(read_scalar(&herr, err));
-    if (herr) return F3S_ERR_HIP;
+
+    // ---- 8. integrity check of the finished plan ------------------------
+    HIP_TRY(launch_validate_plan(*p, &st->invalid, s));
+    HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
+    p->nnz = (int64_t)hs.nnz;
+    if (hs.invalid || hs.n_items != p->n_items) return F3S_ERR_HIP;
     return F3S_OK;
 }
 
@@ -265,6 +307,54 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb)
 {
     const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
     return x < y + nb && y < x + na;
+}
+
+// Builds a plan whose split-window partials hold part_row floats per row.
+f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                     int32_t part_row)
+{
+    const auto t0 = std::chrono::steady_clock::now();
+    if (N < 0 || (N > 0 && !row_ptr)) {
+        fail(F3S_ERR_INVALID_VALUE);
+        return nullptr;
+    }
+    f3s_plan_s *p = new (std::nothrow) f3s_plan_s();
+    if (!p) {
+        fail(F3S_ERR_OUT_OF_MEMORY);
+        return nullptr;
+    }
+    p->N = N;
+    p->T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
+    p->id = g_next_plan_id.fetch_add(1);
+    f3s_status_t st = from_hip(hipGetDevice(&p->device));
+    if (st == F3S_OK) {
+        if (N == 0) {
+            Arena a;
+            a.add<int32_t>(1);
+            st = from_hip(a.alloc());
+            if (st == F3S_OK) {
+                p->store = a.base;
+                p->device_bytes += (int64_t)a.cap;
+                p->blk_off = a.take<int32_t>(1);
+                st = from_hip(hipMemset(p->blk_off, 0, sizeof(int32_t)));
+            }
+            p->piece = 16;
+            p->part_row = part_row;
+        } else {
+            st = build_plan(p, row_ptr, col_idx, part_row);
+        }
+    }
+    if (st != F3S_OK) {
+        (void)hipDeviceSynchronize();
+        (void)hipGetLastError();
+        free_plan_arrays(p);
+        delete p;
+        fail(st);
+        return nullptr;
+    }
+    p->build_ms = std::chrono::duration<double, std::milli>(
+                      std::chrono::steady_clock::now() - t0).count();
+    return p;
 }
 
 }  // namespace
@@ -288,40 +378,7 @@ f3s_status_t f3s_last_error(void) { return g_last_error; }
 
 f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N)
 {
-    const auto t0 = std::chrono::steady_clock::now();
-    if (N < 0 || (N > 0 && !row_ptr)) {
-        fail(F3S_ERR_INVALID_VALUE);
-        return nullptr;
-    }
-    f3s_plan_s *p = new (std::nothrow) f3s_plan_s();
-    if (!p) {
-        fail(F3S_ERR_OUT_OF_MEMORY);
-        return nullptr;
-    }
-    p->N = N;
-    p->T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
-    p->id = g_next_plan_id.fetch_add(1);
-    f3s_status_t st = from_hip(hipGetDevice(&p->device));
-    if (st == F3S_OK) {
-        if (N == 0) {
-            st = from_hip(plan_alloc(p, &p->blk_off, 1));
-            if (st == F3S_OK) st = from_hip(hipMemset(p->blk_off, 0, sizeof(int32_t)));
-            p->piece = 16;
-        } else {
-            st = build_plan(p, row_ptr, col_idx);
-        }
-    }
-    if (st != F3S_OK) {
-        (void)hipDeviceSynchronize();
-        (void)hipGetLastError();
-        free_plan_arrays(p);
-        delete p;
-        fail(st);
-        return nullptr;
-    }
-    p->build_ms = std::chrono::duration<double, std::milli>(
-                      std::chrono::steady_clock::now() - t0).count();
-    return p;
+    return make_plan(row_ptr, col_idx, N, f3s::kMaxD);
 }
 
 f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
@@ -332,7 +389,6 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
         return nullptr;
     }
     const int32_t N = src->N;
-    int32_t *rp = nullptr, *ci = nullptr, *cursor = nullptr;
     f3s_status_t st = F3S_OK;
     auto step = [&](hipError_t e) {
         if (st == F3S_OK && e != hipSuccess) st = from_hip(e);
@@ -340,25 +396,35 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
     int prev_device = 0;
     step(hipGetDevice(&prev_device));
     step(hipSetDevice(src->device));
-    step(hipMalloc(&rp, sizeof(int32_t) * ((size_t)N + 1)));
-    step(hipMalloc(&cursor, sizeof(int32_t) * ((size_t)N + 1)));
-    step(hipMalloc(&ci, sizeof(int32_t) * (size_t)(src->nnz > 0 ? src->nnz : 1)));
-    if (st == F3S_OK) {
-        step(hipMemset(cursor, 0, sizeof(int32_t) * ((size_t)N + 1)));
-        step(f3s::launch_transpose_entries(*src, cursor, nullptr, nullptr));
-        step(f3s::launch_scan(cursor, rp, N, nullptr));
-        step(hipMemcpy(cursor, rp, sizeof(int32_t) * (size_t)N, hipMemcpyDeviceToDevice));
-        step(f3s::launch_transpose_entries(*src, cursor, ci, nullptr));
-        step(hipDeviceSynchronize());
-    }
     f3s_plan_t t = nullptr;
-    if (st == F3S_OK) {
-        t = f3s_plan(rp, ci, N);
-        if (!t) st = g_last_error;
+    {
+        // CSR of A^T: count entries per column, scan, scatter (columns of a
+        // row come out in window order, which the plan build does not need)
+        ScratchArena tmp;
+        tmp.add<int32_t>((int64_t)N + 1);  // rp
+        tmp.add<int32_t>((int64_t)N + 1);  // cursor
+        tmp.add<int32_t>(src->nnz);        // ci
+        tmp.add<int32_t>(f3s::scan_tmp_ints(N));
+        if (st == F3S_OK) step(tmp.alloc());
+        if (st == F3S_OK) {
+            int32_t *rp = tmp.take<int32_t>((int64_t)N + 1);
+            int32_t *cursor = tmp.take<int32_t>((int64_t)N + 1);
+            int32_t *ci = tmp.take<int32_t>(src->nnz);
+            int32_t *scan_tmp = tmp.take<int32_t>(f3s::scan_tmp_ints(N));
+            step(hipMemsetAsync(cursor, 0, sizeof(int32_t) * ((size_t)N + 1), nullptr));
+            step(f3s::launch_transpose_entries(*src, cursor, nullptr, nullptr));
+            step(f3s::launch_scan(cursor, rp, N, scan_tmp, nullptr, nullptr));
+            step(hipMemcpyAsync(cursor, rp, sizeof(int32_t) * (size_t)N,
+                                hipMemcpyDeviceToDevice, nullptr));
+            step(f3s::launch_transpose_entries(*src, cursor, ci, nullptr));
+            // the dK/dV pass keeps two partials (dK, dV) per piece row, so a
+            // launch group still holds heads with nh * d <= kMaxD
+            if (st == F3S_OK) {
+                t = make_plan(rp, ci, N, 2 * f3s::kMaxD);
+                if (!t) st = g_last_error;
+            }
+        }
     }
-    if (rp) (void)hipFree(rp);
-    if (ci) (void)hipFree(ci);
-    if (cursor) (void)hipFree(cursor);
     (void)hipSetDevice(prev_device);
     if (st != F3S_OK) {
         f3s_destroy(t);
@@ -366,27 +432,6 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
         return nullptr;
     }
     t->transpose_of = src->id;
-    // the dK/dV pass keeps two partials (dK, dV) per piece row: double the
-    // partial buffer so a launch group still holds heads with nh * d <= kMaxD
-    if (t->n_pieces > 0) {
-        int prev = 0;
-        hipError_t e = hipGetDevice(&prev);
-        if (e == hipSuccess) e = hipSetDevice(t->device);
-        if (e == hipSuccess) {
-            (void)hipFree(t->part_o);
-            t->device_bytes -= (int64_t)t->n_pieces * f3s::kWindowRows * t->part_row * 4;
-            t->part_o = nullptr;
-            e = plan_alloc(t, &t->part_o,
-                           (int64_t)t->n_pieces * f3s::kWindowRows * 2 * f3s::kMaxD);
-            if (e == hipSuccess) t->part_row = 2 * f3s::kMaxD;
-        }
-        (void)hipSetDevice(prev);
-        if (e != hipSuccess) {
-            f3s_destroy(t);
-            fail(from_hip(e));
-            return nullptr;
-        }
-    }
     t->build_ms = std::chrono::duration<double, std::milli>(
                       std::chrono::steady_clock::now() - t0).count();
     return t;

@@ -46,6 +46,9 @@ struct f3s_plan_s {
     int32_t flags = 0;           // bit 0: work list in window order; bit 1: narrow gathers
     uint64_t id = 0;             // process-unique plan id
     uint64_t transpose_of = 0;   // id of the plan this one transposes (0: none)
+    void *store = nullptr;       // one allocation: blk_off, cols, mask, items, merges
+    void *part_store = nullptr;  // one allocation: part_o, part_ml
+    int64_t part_bytes = 0;
     int32_t *blk_off = nullptr;  // [T + 1]
     int32_t *cols = nullptr;     // [16 * n_blocks]
     uint32_t *mask = nullptr;    // [8 * n_blocks]
@@ -82,14 +85,18 @@ hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
                                 hipStream_t s);
 hipError_t launch_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb,
                                     hipStream_t s);
-// Exclusive scan of n int32 into out[0..n], out[n] = total (in == out ok).
-hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, hipStream_t s);
+// Exclusive scan of n int32 into out[0..n], out[n] = total (in == out ok);
+// tmp: scan_tmp_ints(n) ints of workspace; total_out (may be null) also
+// receives the total.
+int64_t scan_tmp_ints(int64_t n);
+hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
+                       int32_t *total_out, hipStream_t s);
+// Also adds the number of set bits (distinct (row, col) pairs) to *nnz_out.
 hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *col_idx,
                                int32_t N, int32_t T, const int32_t *tmp_cols,
                                const int32_t *u, const int32_t *blk_off,
-                               int32_t *cols, uint32_t *mask, hipStream_t s);
-hipError_t launch_count_bits(const uint32_t *mask, int64_t words,
-                             unsigned long long *out, hipStream_t s);
+                               int32_t *cols, uint32_t *mask,
+                               unsigned long long *nnz_out, hipStream_t s);
 hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
                           hipStream_t s);
 hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,

@@ -5,7 +5,8 @@
 //  2. per row window: sorted distinct columns (LDS bitonic sort; windows too
 //     large for LDS use an N-bit column bitmap and popcount compaction)
 //  3. blocks per window (ceil(u/16)) and their exclusive prefix (tro)
-//  4. padded column lists (sptd) and one 256-bit bitmap per 16x16 block
+//  4. padded column lists (sptd) and one 256-bit bitmap per 16x16 block,
+//     built in LDS per window
 //  5. work list: windows stably sorted by block count, largest first, with
 //     windows above `piece` blocks split into pieces of whole block pairs
 //
@@ -58,6 +59,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_window_sort(
 {
     __shared__ int32_t keys[kSortCap];
     __shared__ int scan[kPlanThreads];
+    // k_check_row_ptr ran before on the same stream: a malformed row_ptr
+    // stops every block here, before any column is read
+    if (*(volatile int32_t *)err) return;
     const int tid = threadIdx.x;
     const int w = blockIdx.x;
     const int r0 = w * kWindowRows;
@@ -136,7 +140,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_heavy_compact(
         }
         atomicOr(&bm[c >> 5], 1u << (c & 31));
     }
-    __threadfence();
+    // the atomics and the loads below are issued by this workgroup alone and
+    // performed at the L2: workgroup-scope ordering is enough (a device-scope
+    // fence would write back the whole L2 for every block)
+    __threadfence_block();
     __syncthreads();
     const int ch = (words + kPlanThreads - 1) / kPlanThreads;
     const int lo = min(tid * ch, words), hi = min(lo + ch, words);
@@ -166,19 +173,28 @@ __global__ void k_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb)
 
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 4;
+constexpr int kScanTile = kScanThreads * kScanItems;
 
-__global__ __launch_bounds__(kScanThreads) void k_scan(const int32_t *in,
-                                                       int32_t *out, int32_t n)
+// Exclusive scan of one tile of kScanTile ints per workgroup, in place or
+// not; the tile's total goes to tile_sums[tile] (when given).  With one
+// workgroup and n > kScanTile it walks the tiles in order with a carry
+// (used for the short array of tile totals), and writes out[n] = total.
+__global__ __launch_bounds__(kScanThreads) void k_scan(const int32_t *in, int32_t *out,
+                                                       int32_t n, int32_t *tile_sums,
+                                                       int32_t *total_out)
 {
     __shared__ int32_t sh[kScanThreads];
     const int tid = threadIdx.x;
+    const bool whole = gridDim.x == 1;
     int carry = 0;
-    for (int64_t base = 0; base < n; base += kScanThreads * kScanItems) {
+    const int64_t first = whole ? 0 : (int64_t)blockIdx.x * kScanTile;
+    const int64_t last = whole ? n : min((int64_t)n, first + kScanTile);
+    for (int64_t base = first; base < last; base += kScanTile) {
         int v[kScanItems];
         int s = 0;
         for (int j = 0; j < kScanItems; ++j) {
             const int64_t idx = base + (int64_t)tid * kScanItems + j;
-            v[j] = idx < n ? in[idx] : 0;
+            v[j] = idx < last ? in[idx] : 0;
             s += v[j];
         }
         sh[tid] = s;
@@ -194,55 +210,116 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(const int32_t *in,
         __syncthreads();
         for (int j = 0; j < kScanItems; ++j) {
             const int64_t idx = base + (int64_t)tid * kScanItems + j;
-            if (idx < n) out[idx] = run;
+            if (idx < last) out[idx] = run;
             run += v[j];
         }
         carry += tile_total;
     }
-    if (tid == 0) out[n] = carry;
-}
-
-__global__ __launch_bounds__(kPlanThreads) void k_fill_windows(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-    const int32_t *tmp_cols, const int32_t *u, const int32_t *blk_off,
-    int32_t *cols, uint32_t *mask)
-{
-    const int tid = threadIdx.x;
-    const int w = blockIdx.x;
-    const int r0 = w * kWindowRows;
-    const int r1 = min(r0 + kWindowRows, N);
-    const int32_t *uc = tmp_cols + row_ptr[r0];
-    const int uw = u[w];
-    const int ob = blk_off[w];
-    const int slots = kBlockCols * (blk_off[w + 1] - ob);
-    for (int k = tid; k < slots; k += kPlanThreads)
-        cols[(int64_t)kBlockCols * ob + k] = k < uw ? uc[k] : -1;
-    for (int r = r0; r < r1; ++r) {
-        for (int e = row_ptr[r] + tid; e < row_ptr[r + 1]; e += kPlanThreads) {
-            const int c = col_idx[e];
-            int lo = 0, hi = uw;
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (uc[mid] < c) lo = mid + 1;
-                else hi = mid;
-            }
-            if (lo >= uw || uc[lo] != c) continue;  // unreachable on valid CSR
-            const int64_t blk = ob + lo / kBlockCols;
-            const int cc = lo % kBlockCols, rr = r - r0;
-            const int bit = 4 * (rr + 16 * (cc / 4)) + (cc % 4);
-            atomicOr(&mask[kMaskWords * blk + bit / 32], 1u << (bit % 32));
+    if (tid == 0) {
+        if (whole) {
+            out[n] = carry;
+            if (total_out) *total_out = carry;
+        } else {
+            tile_sums[blockIdx.x] = carry;
         }
     }
 }
 
-__global__ void k_count_bits(const uint32_t *mask, int64_t words,
-                             unsigned long long *out)
+// Adds the scanned tile offsets to every tile after the first and writes
+// the total.
+__global__ __launch_bounds__(256) void k_scan_add(int32_t *out, int32_t n,
+                                                  const int32_t *tile_offs, int32_t ntiles,
+                                                  int32_t *total_out)
 {
-    unsigned long long acc = 0;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < words;
-         k += (int64_t)gridDim.x * blockDim.x)
-        acc += __popc(mask[k]);
-    if (acc) atomicAdd(out, acc);
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) {
+        const int64_t tile = i / kScanTile;
+        if (tile > 0) out[i] += tile_offs[tile];
+    }
+    if (i == 0) {
+        out[n] = tile_offs[ntiles];
+        if (total_out) *total_out = tile_offs[ntiles];
+    }
+}
+
+// Column lists (sptd, padded with -1) and block bitmaps of one window per
+// workgroup.  The window's sorted distinct columns and its bitmaps are held
+// in LDS: each CSR entry finds its row among the 16 row starts and its
+// compacted column by binary search, sets its bit with an LDS atomic OR, and
+// the block arrays are written out once, coalesced.  The set bits are
+// counted on the way out (distinct (row, col) pairs of A).  A window with
+// more distinct columns than the LDS holds (from the heavy path) works on
+// its own global bitmaps instead, zeroed first.
+__global__ __launch_bounds__(kPlanThreads) void k_fill_windows(
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+    const int32_t *tmp_cols, const int32_t *u, const int32_t *blk_off,
+    int32_t *cols, uint32_t *mask, unsigned long long *nnz_out)
+{
+    __shared__ int32_t s_uc[kSortCap];
+    __shared__ uint32_t s_mask[kSortCap / kBlockCols * kMaskWords];
+    __shared__ int32_t s_rp[kWindowRows + 1];
+    __shared__ unsigned long long s_cnt;
+    const int tid = threadIdx.x;
+    const int w = blockIdx.x;
+    const int r0 = w * kWindowRows;
+    const int nr = min(r0 + kWindowRows, N) - r0;
+    if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
+    if (tid == 0) s_cnt = 0;
+    const int32_t *uc = tmp_cols + row_ptr[r0];
+    const int uw = u[w];
+    const int ob = blk_off[w];
+    const int nbw = blk_off[w + 1] - ob;
+    const bool in_lds = uw <= kSortCap;
+    uint32_t *gmask = mask + (int64_t)kMaskWords * ob;
+    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads) {
+        if (in_lds) s_mask[k] = 0;
+        else gmask[k] = 0;
+    }
+    if (in_lds)
+        for (int k = tid; k < uw; k += kPlanThreads) s_uc[k] = uc[k];
+    __threadfence_block();
+    __syncthreads();
+    const int beg = s_rp[0], n = s_rp[nr] - beg;
+    for (int e = tid; e < n; e += kPlanThreads) {
+        // row of entry e: the last row start <= beg + e
+        int rlo = 0, rhi = nr;
+        while (rhi - rlo > 1) {
+            const int mid = (rlo + rhi) >> 1;
+            if (s_rp[mid] <= beg + e) rlo = mid;
+            else rhi = mid;
+        }
+        const int c = col_idx[beg + e];
+        int lo = 0, hi = uw;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if ((in_lds ? s_uc[mid] : uc[mid]) < c) lo = mid + 1;
+            else hi = mid;
+        }
+        if (lo >= uw || (in_lds ? s_uc[lo] : uc[lo]) != c) continue;  // unreachable on valid CSR
+        const int cc = lo % kBlockCols;
+        const int bit = 4 * (rlo + 16 * (cc / 4)) + (cc % 4);
+        const int word = kMaskWords * (lo / kBlockCols) + bit / 32;
+        if (in_lds) atomicOr(&s_mask[word], 1u << (bit % 32));
+        else atomicOr(&gmask[word], 1u << (bit % 32));
+    }
+    __threadfence_block();  // as in k_heavy_compact: one workgroup, L2 atomics
+    __syncthreads();
+    for (int k = tid; k < kBlockCols * nbw; k += kPlanThreads)
+        cols[(int64_t)kBlockCols * ob + k] = k < uw ? (in_lds ? s_uc[k] : uc[k]) : -1;
+    unsigned long long cnt = 0;
+    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads) {
+        uint32_t m;
+        if (in_lds) {
+            m = s_mask[k];
+            gmask[k] = m;
+        } else {
+            m = __hip_atomic_load(&gmask[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        cnt += __popc(m);
+    }
+    if (cnt) atomicAdd(&s_cnt, cnt);
+    __syncthreads();
+    if (tid == 0 && s_cnt) atomicAdd(nnz_out, s_cnt);
 }
 
 __global__ void k_sum_i32(const int32_t *in, int32_t n, unsigned long long *out)
@@ -431,29 +508,34 @@ hipError_t launch_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb,
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, hipStream_t s)
+int64_t scan_tmp_ints(int64_t n)
 {
-    k_scan<<<1, kScanThreads, 0, s>>>(in, out, n);
+    return n <= kScanTile ? 1 : (n + kScanTile - 1) / kScanTile + 1;
+}
+
+hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
+                       int32_t *total_out, hipStream_t s)
+{
+    if (n <= kScanTile) {
+        k_scan<<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total_out);
+        return hipGetLastError();
+    }
+    const int32_t ntiles = (int32_t)((n + kScanTile - 1) / kScanTile);
+    k_scan<<<ntiles, kScanThreads, 0, s>>>(in, out, n, tmp, nullptr);
+    k_scan<<<1, kScanThreads, 0, s>>>(tmp, tmp, ntiles, nullptr, nullptr);
+    k_scan_add<<<grid_for(n, 256), 256, 0, s>>>(out, n, tmp, ntiles, total_out);
     return hipGetLastError();
 }
 
 hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *col_idx,
                                int32_t N, int32_t T, const int32_t *tmp_cols,
                                const int32_t *u, const int32_t *blk_off,
-                               int32_t *cols, uint32_t *mask, hipStream_t s)
+                               int32_t *cols, uint32_t *mask,
+                               unsigned long long *nnz_out, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
     k_fill_windows<<<T, kPlanThreads, 0, s>>>(row_ptr, col_idx, N, tmp_cols, u,
-                                              blk_off, cols, mask);
-    return hipGetLastError();
-}
-
-hipError_t launch_count_bits(const uint32_t *mask, int64_t words,
-                             unsigned long long *out, hipStream_t s)
-{
-    if (words == 0) return hipSuccess;
-    const unsigned g = grid_for(words, 256);
-    k_count_bits<<<g < 4096 ? g : 4096, 256, 0, s>>>(mask, words, out);
+                                              blk_off, cols, mask, nnz_out);
     return hipGetLastError();
 }
 
