@@ -152,6 +152,7 @@ struct BuildStats {
     unsigned long long n_unique;  // sum of distinct columns over windows
     unsigned long long nnz;       // set bits of all bitmaps
     int32_t err;                  // malformed CSR
+    int32_t n_big;                // windows too large for one wavefront
     int32_t n_heavy;              // windows too large for the LDS sort
     int32_t max_blocks;
     int32_t n_blocks;
@@ -177,16 +178,22 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     p->nnz_csr = nnz;
 
     // all scratch of the build in one allocation
+    const int64_t stage_words = mask_stage_words(nnz, T);
     ScratchArena tmp;
     tmp.add<BuildStats>(1);
     tmp.add<int32_t>(nnz);               // sorted distinct columns per window
-    for (int k = 0; k < 5; ++k) tmp.add<int32_t>(T);  // u, heavy, nb, npieces, key
+    tmp.add<uint32_t>(stage_words);      // block bitmaps per window
+    // u, big, is_big, bits, heavy, nb, npieces, key
+    for (int k = 0; k < 8; ++k) tmp.add<int32_t>(T);
     for (int k = 0; k < 3; ++k) tmp.add<int32_t>((int64_t)T + 1);  // tro, splits
     tmp.add<int32_t>(scan_tmp_ints(T));
     HIP_TRY(tmp.alloc());
     BuildStats *st = tmp.take<BuildStats>(1);
     int32_t *tmp_cols = tmp.take<int32_t>(nnz);
-    int32_t *u = tmp.take<int32_t>(T), *heavy = tmp.take<int32_t>(T);
+    uint32_t *tmp_mask = tmp.take<uint32_t>(stage_words);
+    int32_t *u = tmp.take<int32_t>(T), *big = tmp.take<int32_t>(T);
+    int32_t *is_big = tmp.take<int32_t>(T), *bits = tmp.take<int32_t>(T);
+    int32_t *heavy = tmp.take<int32_t>(T);
     int32_t *nb = tmp.take<int32_t>(T), *npieces = tmp.take<int32_t>(T);
     int32_t *key = tmp.take<int32_t>(T);
     int32_t *tro = tmp.take<int32_t>((int64_t)T + 1);
@@ -196,12 +203,20 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     BuildStats hs;
     HIP_TRY(hipMemsetAsync(st, 0, sizeof(BuildStats), s));
 
-    // ---- 2. CSR check and distinct columns per window ------------------
+    // ---- 2. CSR check, distinct columns and bitmaps per window ----------
     HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
-    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, T, tmp_cols, u, heavy, &st->n_heavy,
-                               &st->err, s));
+    HIP_TRY(launch_window_wave(row_ptr, col_idx, N, T, tmp_cols, tmp_mask, u, is_big,
+                               bits, &st->err, s));
+    HIP_TRY(launch_scan(is_big, tro, T, scan_tmp, &st->n_big, s));  // tro as scratch
+    HIP_TRY(launch_compact_big(is_big, tro, T, big, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
+    if (hs.n_big > 0) {
+        HIP_TRY(launch_window_sort(row_ptr, col_idx, N, big, hs.n_big, tmp_cols, tmp_mask,
+                                   u, bits, heavy, &st->n_heavy, &st->err, s));
+        HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
+        if (hs.err) return F3S_ERR_INVALID_CSR;
+    }
     if (hs.n_heavy > 0) {
         const int32_t words = (N + 31) / 32;
         const int64_t budget = 256ll << 20;  // bitmap workspace per batch
@@ -221,6 +236,9 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
         }
         HIP_TRY(hipStreamSynchronize(s));  // the bitmap workspace is freed here
     }
+    HIP_TRY(launch_heavy_masks(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, u,
+                             tmp_mask, bits, s));
+    HIP_TRY(launch_sum_i32(bits, T, &st->nnz, s));
 
     // ---- 3. blocks per window, their prefix (tro), statistics -----------
     HIP_TRY(launch_blocks_per_window(u, T, nb, s));
@@ -272,9 +290,9 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(hipMemcpyAsync(p->blk_off, tro, sizeof(int32_t) * ((size_t)T + 1),
                            hipMemcpyDeviceToDevice, s));
 
-    // ---- 6. column lists and bitmaps (and the distinct-pair count) ------
-    HIP_TRY(launch_fill_windows(row_ptr, col_idx, N, T, tmp_cols, u, p->blk_off, p->cols,
-                                p->mask, &st->nnz, s));
+    // ---- 6. column lists and bitmaps into their blocks --------------------
+    HIP_TRY(launch_fill_windows(row_ptr, T, tmp_cols, tmp_mask, u, p->blk_off, p->cols,
+                                p->mask, s));
 
     // ---- 7. heavy-first work list: histogram over (key, chunk), scan, scatter
     const int32_t chunk = 64;
@@ -398,25 +416,20 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
     step(hipSetDevice(src->device));
     f3s_plan_t t = nullptr;
     {
-        // CSR of A^T: count entries per column, scan, scatter (columns of a
-        // row come out in window order, which the plan build does not need)
+        // CSR of A^T from the plan's bitmaps (radix sort of the entries by
+        // column)
+        size_t tr_bytes = 0;
+        step(f3s::transpose_scratch_bytes(*src, &tr_bytes));
         ScratchArena tmp;
         tmp.add<int32_t>((int64_t)N + 1);  // rp
-        tmp.add<int32_t>((int64_t)N + 1);  // cursor
         tmp.add<int32_t>(src->nnz);        // ci
-        tmp.add<int32_t>(f3s::scan_tmp_ints(N));
+        tmp.add<char>((int64_t)tr_bytes);
         if (st == F3S_OK) step(tmp.alloc());
         if (st == F3S_OK) {
             int32_t *rp = tmp.take<int32_t>((int64_t)N + 1);
-            int32_t *cursor = tmp.take<int32_t>((int64_t)N + 1);
             int32_t *ci = tmp.take<int32_t>(src->nnz);
-            int32_t *scan_tmp = tmp.take<int32_t>(f3s::scan_tmp_ints(N));
-            step(hipMemsetAsync(cursor, 0, sizeof(int32_t) * ((size_t)N + 1), nullptr));
-            step(f3s::launch_transpose_entries(*src, cursor, nullptr, nullptr));
-            step(f3s::launch_scan(cursor, rp, N, scan_tmp, nullptr, nullptr));
-            step(hipMemcpyAsync(cursor, rp, sizeof(int32_t) * (size_t)N,
-                                hipMemcpyDeviceToDevice, nullptr));
-            step(f3s::launch_transpose_entries(*src, cursor, ci, nullptr));
+            void *tr = tmp.take<char>((int64_t)tr_bytes);
+            step(f3s::launch_transpose_csr(*src, tr, tr_bytes, rp, ci, nullptr));
             // the dK/dV pass keeps two partials (dK, dV) per piece row, so a
             // launch group still holds heads with nh * d <= kMaxD
             if (st == F3S_OK) {

@@ -70,12 +70,33 @@ namespace f3s {
 // ---- plan kernels (plan_kernels.hip) ------------------------------------
 hipError_t launch_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
                                 int32_t *err, hipStream_t s);
-// Per window: sorted distinct columns into tmp_cols at the window's CSR
-// offset, count into u; windows above the LDS capacity are queued as heavy.
+// Staging area of the window bitmaps, in 32-bit words, for nnz CSR entries.
+int64_t mask_stage_words(int64_t nnz, int32_t T);
+// Per window of at most 512 entries (one wavefront each): sorted distinct
+// columns into tmp_cols at the window's CSR offset, their count into u, the
+// block bitmaps into the staging area, their set bits into bits.  Larger
+// windows get is_big = 1 and are left to launch_window_sort.
+hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                              int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
+                              int32_t *u, int32_t *is_big, int32_t *bits, int32_t *err,
+                              hipStream_t s);
+// big[pos[w]] = w for every window with is_big[w] (pos: exclusive scan).
+hipError_t launch_compact_big(const int32_t *is_big, const int32_t *pos, int32_t T,
+                              int32_t *big, hipStream_t s);
+// The windows big[0 .. n_big): sorted distinct columns, u, bitmaps and bits
+// as above (one wavefront with 16 keys per lane up to 1024 entries, else an
+// LDS sort); windows above the LDS capacity are queued as heavy.
 hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
-                              int32_t N, int32_t T, int32_t *tmp_cols,
-                              int32_t *u, int32_t *heavy, int32_t *n_heavy,
+                              int32_t N, const int32_t *big, int32_t n_big,
+                              int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+                              int32_t *bits, int32_t *heavy, int32_t *n_heavy,
                               int32_t *err, hipStream_t s);
+// Block bitmaps and bits of the windows list[0 .. count) once their columns
+// are known (the heavy windows).
+hipError_t launch_heavy_masks(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                            const int32_t *list, int32_t count, const int32_t *tmp_cols,
+                            const int32_t *u, uint32_t *tmp_mask, int32_t *bits,
+                            hipStream_t s);
 // Heavy windows heavy[first .. first+count): column bitmap of N bits each in
 // `bitmap` (zeroed by the caller), then popcount compaction.
 hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
@@ -91,12 +112,11 @@ hipError_t launch_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb,
 int64_t scan_tmp_ints(int64_t n);
 hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
                        int32_t *total_out, hipStream_t s);
-// Also adds the number of set bits (distinct (row, col) pairs) to *nnz_out.
-hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *col_idx,
-                               int32_t N, int32_t T, const int32_t *tmp_cols,
-                               const int32_t *u, const int32_t *blk_off,
-                               int32_t *cols, uint32_t *mask,
-                               unsigned long long *nnz_out, hipStream_t s);
+// Padded column lists and block bitmaps of the plan from the staging areas.
+hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,
+                               const uint32_t *tmp_mask, const int32_t *u,
+                               const int32_t *blk_off, int32_t *cols, uint32_t *mask,
+                               hipStream_t s);
 hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
                           hipStream_t s);
 hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,
@@ -116,10 +136,12 @@ hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
                               int32_t nchunks, int32_t *offs, WorkItem *items,
                               int32_t *merges, hipStream_t s);
 
-// Transposed pattern from a plan: with out == null, cursor[col] += entries
-// of column col; otherwise out[cursor[col]++] = row for every entry.
-hipError_t launch_transpose_entries(const f3s_plan_s &p, int32_t *cursor, int32_t *out,
-                                   hipStream_t s);
+// ---- transposed pattern (transpose.hip) ----------------------------------
+// CSR of A^T (rp[N+1], ci[nnz]) from a plan's bitmaps; scratch of
+// transpose_scratch_bytes(p) bytes.
+hipError_t transpose_scratch_bytes(const f3s_plan_s &p, size_t *bytes);
+hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scratch_bytes,
+                                int32_t *rp, int32_t *ci, hipStream_t s);
 
 // Sets *err when a finished plan is internally inconsistent.
 hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s);

@@ -2,11 +2,13 @@
 // (Section 3.1) and the heavy-first work list (Section 3.2).
 //
 //  1. row_ptr validation
-//  2. per row window: sorted distinct columns (LDS bitonic sort; windows too
-//     large for LDS use an N-bit column bitmap and popcount compaction)
+//  2. per row window: sorted distinct columns and the window's 256-bit block
+//     bitmaps, staged at offsets fixed by the CSR (one wavefront per window
+//     with a register bitonic sort; larger windows a workgroup LDS sort;
+//     windows too large for LDS an N-bit column bitmap and popcount
+//     compaction)
 //  3. blocks per window (ceil(u/16)) and their exclusive prefix (tro)
-//  4. padded column lists (sptd) and one 256-bit bitmap per 16x16 block,
-//     built in LDS per window
+//  4. padded column lists (sptd) and bitmaps copied to their final blocks
 //  5. work list: windows stably sorted by block count, largest first, with
 //     windows above `piece` blocks split into pieces of whole block pairs
 //
@@ -41,6 +43,238 @@ __device__ int block_exclusive_scan256(int v, int *lds, int *total)
     return incl - v;
 }
 
+// Staging offset (in 32-bit words) of window w's bitmaps, whose CSR entries
+// start at beg.  A window with n entries has at most ceil(n/16) blocks, 8n/16
+// + 8 words at most, and the next window's offset lies at least n/2 + 8
+// words further on, so the regions never overlap; all of them fit in
+// nnz/2 + 8T + 8 words.
+__device__ __forceinline__ int64_t mask_stage(int32_t beg, int32_t w)
+{
+    return (int64_t)(beg >> 1) + 8 * (int64_t)w;
+}
+
+// Orders the LDS accesses of one wavefront (the wave's LDS operations run in
+// issue order, so only the compiler has to be kept from moving them).
+__device__ __forceinline__ void wave_lds_order()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int wave_excl_scan(int v, int lane, int *total)
+{
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    *total = __shfl(incl, 63);
+    return incl - v;
+}
+
+// Bitonic sorting network, ascending, over the 64*E keys of one wavefront:
+// key t = E*lane + i sits in x[i] of lane `lane`.  Compare distances below E
+// stay inside a lane, larger ones pair lanes lane and lane ^ (j/E).
+template <int E>
+__device__ __forceinline__ void wave_bitonic(int (&x)[E], int lane)
+{
+#pragma unroll
+    for (int k = 2; k <= 64 * E; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= E) {
+                const bool lower = (lane & (j / E)) == 0;
+#pragma unroll
+                for (int i = 0; i < E; ++i) {
+                    const bool up = ((E * lane + i) & k) == 0;
+                    const int o = __shfl_xor(x[i], j / E);
+                    x[i] = lower == up ? min(x[i], o) : max(x[i], o);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < E; ++i) {
+                    if (i & j) continue;
+                    const bool up = ((E * lane + i) & k) == 0;
+                    const int a = x[i], b = x[i | j];
+                    x[i] = up ? min(a, b) : max(a, b);
+                    x[i | j] = up ? max(a, b) : min(a, b);
+                }
+            }
+        }
+    }
+}
+
+// Entries a window may have for the one-wave path over all windows (8 keys
+// per lane); windows up to kWaveCap16 entries get a second one-wave pass with
+// 16 keys per lane, launched over the larger windows only (its registers
+// would cut the occupancy of the first pass threefold).
+constexpr int kWaveCap = 512;
+constexpr int kWaveCap16 = 1024;
+
+// Window of n <= 64*E entries starting at CSR offset beg; lanes 0..nr of rp
+// hold the window's row starts (INT_MAX above).  Writes the sorted distinct
+// columns to tmp_cols[beg..), the block bitmaps to their staging region, u[w]
+// and the number of set bits to bits[w].
+template <int E>
+__device__ void window_wave(const int32_t *col_idx, int32_t N, int32_t w, int32_t beg,
+                            int32_t n, int32_t rp, int lane, int32_t *s_cols,
+                            uint32_t *s_mask, int32_t *tmp_cols, uint32_t *tmp_mask,
+                            int32_t *u, int32_t *bits_out, int32_t *err)
+{
+    int x[E];
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        const int e = 64 * i + lane;  // coalesced loads; a sort input's order is free
+        int v = INT_MAX;
+        if (e < n) {
+            v = col_idx[beg + e];
+            if (v < 0 || v >= N) {
+                atomicOr(err, 1);
+                v = INT_MAX;
+            }
+        }
+        x[i] = v;
+    }
+    wave_bitonic<E>(x, lane);
+
+    // distinct keys in sorted order, compacted by a wave prefix sum
+    const int before = __shfl_up(x[E - 1], 1);
+    uint32_t first = 0;
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        const int prev = i ? x[i - 1] : before;
+        if (x[i] != INT_MAX && ((lane == 0 && i == 0) || x[i] != prev)) first |= 1u << i;
+    }
+    int total;
+    int off = wave_excl_scan(__popc(first), lane, &total);
+#pragma unroll
+    for (int i = 0; i < E; ++i)
+        if (first & (1u << i)) {
+            tmp_cols[beg + off] = x[i];
+            s_cols[off] = x[i];
+            ++off;
+        }
+    const int nbw = (total + kBlockCols - 1) / kBlockCols;
+    for (int k = lane; k < kMaskWords * nbw; k += 64) s_mask[k] = 0;
+    wave_lds_order();
+
+    // one bit per entry: row from the row starts, compacted column by binary
+    // search in the distinct list
+    int starts[kWindowRows - 1];  // wave-uniform: scalar registers
+#pragma unroll
+    for (int r = 1; r < kWindowRows; ++r) starts[r - 1] = __builtin_amdgcn_readlane(rp, r);
+#pragma unroll
+    for (int i = 0; i < E; ++i) {
+        const int e = 64 * i + lane;
+        if (e >= n) continue;
+        const int c = col_idx[beg + e];  // again (cache-resident) to spare registers
+        if (c < 0 || c >= N) continue;
+        int row = 0;
+#pragma unroll
+        for (int r = 1; r < kWindowRows; ++r) row += beg + e >= starts[r - 1];
+        int lo = 0, hi = total;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (s_cols[mid] < c) lo = mid + 1;
+            else hi = mid;
+        }
+        if (lo >= total) continue;  // every valid column is in the list
+        const int cc = lo % kBlockCols;
+        const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
+        atomicOr(&s_mask[kMaskWords * (lo / kBlockCols) + bit / 32], 1u << (bit % 32));
+    }
+    wave_lds_order();
+    uint32_t *gm = tmp_mask + mask_stage(beg, w);
+    int bits = 0;
+    for (int k = lane; k < kMaskWords * nbw; k += 64) {
+        const uint32_t m = s_mask[k];
+        gm[k] = m;
+        bits += __popc(m);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) bits += __shfl_xor(bits, o);
+    if (lane == 0) {
+        u[w] = total;
+        bits_out[w] = bits;
+    }
+}
+
+// Loads a window's row starts into lanes 0..nr of the wave (INT_MAX above).
+__device__ __forceinline__ int32_t window_row_starts(const int32_t *row_ptr, int32_t N,
+                                                     int32_t w, int lane, int32_t *beg,
+                                                     int32_t *n)
+{
+    const int r0 = w * kWindowRows;
+    const int nr = min(kWindowRows, N - r0);
+    const int32_t rp = lane <= nr ? row_ptr[r0 + lane] : INT_MAX;
+    *beg = __shfl(rp, 0);
+    *n = __shfl(rp, nr) - *beg;
+    return rp;
+}
+
+// One wavefront (one workgroup) per window.  Windows with more than kWaveCap
+// entries are flagged in is_big for the later passes.  (No counter shared by
+// all windows: atomics on one address serialise, tens of ns each.)
+__global__ __launch_bounds__(64) void k_window_wave(
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, int32_t *tmp_cols,
+    uint32_t *tmp_mask, int32_t *u, int32_t *is_big, int32_t *bits_out, int32_t *err)
+{
+    __shared__ int32_t s_cols[kWaveCap];
+    __shared__ uint32_t s_mask[kWaveCap / kBlockCols * kMaskWords];
+    const int lane = threadIdx.x;
+    const int w = blockIdx.x;
+    // k_check_row_ptr ran before on the same stream: a malformed row_ptr
+    // stops every wave here, before any column is read (is_big stays valid
+    // for the scan that follows)
+    if (*(volatile int32_t *)err) {
+        if (lane == 0) is_big[w] = 0;
+        return;
+    }
+    int32_t beg, n;
+    const int32_t rp = window_row_starts(row_ptr, N, w, lane, &beg, &n);
+    if (lane == 0) is_big[w] = n > kWaveCap;
+    if (n > kWaveCap) return;
+    if (n <= 64)
+        window_wave<1>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols,
+                       tmp_mask, u, bits_out, err);
+    else if (n <= 128)
+        window_wave<2>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols,
+                       tmp_mask, u, bits_out, err);
+    else if (n <= 256)
+        window_wave<4>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols,
+                       tmp_mask, u, bits_out, err);
+    else
+        window_wave<8>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols,
+                       tmp_mask, u, bits_out, err);
+}
+
+// The windows of `big` with kWaveCap < n <= kWaveCap16 entries, one wavefront
+// each with 16 keys per lane; the others are left to k_window_sort.
+__global__ __launch_bounds__(64) void k_window_wave16(
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *big,
+    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
+{
+    __shared__ int32_t s_cols[kWaveCap16];
+    __shared__ uint32_t s_mask[kWaveCap16 / kBlockCols * kMaskWords];
+    const int lane = threadIdx.x;
+    const int w = big[blockIdx.x];
+    int32_t beg, n;
+    const int32_t rp = window_row_starts(row_ptr, N, w, lane, &beg, &n);
+    if (n <= kWaveCap || n > kWaveCap16) return;
+    window_wave<16>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols, tmp_mask,
+                    u, bits_out, err);
+}
+
+// big[pos[w]] = w for the flagged windows (pos: exclusive scan of is_big).
+__global__ void k_compact_big(const int32_t *is_big, const int32_t *pos, int32_t T,
+                              int32_t *big)
+{
+    const int w = blockIdx.x * blockDim.x + threadIdx.x;
+    if (w < T && is_big[w] && pos[w] < T) big[pos[w]] = w;
+}
+
 __global__ void k_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
                                 int32_t *err)
 {
@@ -53,21 +287,48 @@ __global__ void k_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
     if (bad) atomicOr(err, 1);
 }
 
-__global__ __launch_bounds__(kPlanThreads) void k_window_sort(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, int32_t *tmp_cols,
-    int32_t *u, int32_t *heavy, int32_t *n_heavy, int32_t *err)
+// Windows of the list `big` with more than kWaveCap16 entries, one
+// workgroup each: LDS bitonic sort and compaction into tmp_cols and u, then
+// the block bitmaps assembled in LDS and stored to the staging area, their
+// set bits to bits[w].  Windows above the LDS capacity are queued as heavy.
+constexpr int kSortThreads = 1024;
+
+// Exclusive scan of one int per thread over a workgroup of kSortThreads.
+__device__ int block_excl_scan_sort(int v, int *lds, int *total)
 {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    int wt;
+    const int x = wave_excl_scan(v, lane, &wt);
+    if (lane == 0) lds[wv] = wt;
+    __syncthreads();
+    int before = 0, all = 0;
+    for (int k = 0; k < kSortThreads / 64; ++k) {
+        const int c = lds[k];
+        before += k < wv ? c : 0;
+        all += c;
+    }
+    *total = all;
+    __syncthreads();
+    return before + x;
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_window_sort(
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *big,
+    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *heavy,
+    int32_t *n_heavy, int32_t *err)
+{
+    constexpr int kChunk = kSortCap / kSortThreads;  // sorted keys per thread
     __shared__ int32_t keys[kSortCap];
-    __shared__ int scan[kPlanThreads];
-    // k_check_row_ptr ran before on the same stream: a malformed row_ptr
-    // stops every block here, before any column is read
-    if (*(volatile int32_t *)err) return;
+    __shared__ int scan[kSortThreads / 64];
+    __shared__ uint32_t s_mask[kSortCap / kBlockCols * kMaskWords];
+    __shared__ int32_t s_rp[kWindowRows + 1];
     const int tid = threadIdx.x;
-    const int w = blockIdx.x;
+    const int w = big[blockIdx.x];
     const int r0 = w * kWindowRows;
-    const int r1 = min(r0 + kWindowRows, N);
+    const int nr = min(r0 + kWindowRows, N) - r0;
     const int beg = row_ptr[r0];
-    const int n = row_ptr[r1] - beg;
+    const int n = row_ptr[r0 + nr] - beg;
+    if (n <= kWaveCap16) return;  // sorted by k_window_wave16
     if (n > kSortCap) {
         if (tid == 0) {
             heavy[atomicAdd(n_heavy, 1)] = w;
@@ -75,9 +336,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_window_sort(
         }
         return;
     }
+    if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
     int p2 = 1;
     while (p2 < n) p2 <<= 1;
-    for (int t = tid; t < p2; t += kPlanThreads) {
+    for (int t = tid; t < p2; t += kSortThreads) {
         int v = INT_MAX;
         if (t < n) {
             v = col_idx[beg + t];
@@ -92,7 +354,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_window_sort(
     // bitonic sort, ascending
     for (int k = 2; k <= p2; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int t = tid; t < p2; t += kPlanThreads) {
+            for (int t = tid; t < p2; t += kSortThreads) {
                 const int x = t ^ j;
                 if (x > t) {
                     const int a = keys[t], b = keys[x];
@@ -106,18 +368,63 @@ __global__ __launch_bounds__(kPlanThreads) void k_window_sort(
             __syncthreads();
         }
     }
-    // distinct values, written in order at the window's CSR offset
-    const int ch = (p2 + kPlanThreads - 1) / kPlanThreads;
+    // distinct values, written in order at the window's CSR offset and
+    // compacted to the front of keys (read into registers first: the scan's
+    // barriers separate every read from the compacting writes)
+    const int ch = (p2 + kSortThreads - 1) / kSortThreads;
     const int lo = min(tid * ch, n), hi = min(lo + ch, n);
-    int cnt = 0;
-    for (int k = lo; k < hi; ++k)
-        cnt += keys[k] != INT_MAX && (k == 0 || keys[k] != keys[k - 1]);
+    int v[kChunk];
+    uint32_t first = 0;
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        const int k = lo + j;
+        v[j] = k < hi ? keys[k] : INT_MAX;
+        if (k < hi && v[j] != INT_MAX && (k == 0 || v[j] != keys[k - 1])) first |= 1u << j;
+    }
     int total;
-    int off = block_exclusive_scan256(cnt, scan, &total);
-    for (int k = lo; k < hi; ++k)
-        if (keys[k] != INT_MAX && (k == 0 || keys[k] != keys[k - 1]))
-            tmp_cols[beg + off++] = keys[k];
-    if (tid == 0) u[w] = total;
+    int off = block_excl_scan_sort(__popc(first), scan, &total);
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j)
+        if (first & (1u << j)) {
+            tmp_cols[beg + off] = v[j];
+            keys[off] = v[j];
+            ++off;
+        }
+    const int nbw = (total + kBlockCols - 1) / kBlockCols;
+    for (int k = tid; k < kMaskWords * nbw; k += kSortThreads) s_mask[k] = 0;
+    __syncthreads();
+    // one bit per entry: row among the row starts, compacted column by binary
+    // search in the distinct list
+    for (int e = tid; e < n; e += kSortThreads) {
+        const int c = col_idx[beg + e];
+        if (c < 0 || c >= N) continue;
+        int row = 0;
+        for (int r = 1; r < nr; ++r) row += beg + e >= s_rp[r];
+        int a = 0, b = total;
+        while (a < b) {
+            const int mid = (a + b) >> 1;
+            if (keys[mid] < c) a = mid + 1;
+            else b = mid;
+        }
+        if (a >= total) continue;  // every valid column is in the list
+        const int cc = a % kBlockCols;
+        const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
+        atomicOr(&s_mask[kMaskWords * (a / kBlockCols) + bit / 32], 1u << (bit % 32));
+    }
+    __syncthreads();
+    uint32_t *gm = tmp_mask + mask_stage(beg, w);
+    int cnt = 0;
+    for (int k = tid; k < kMaskWords * nbw; k += kSortThreads) {
+        const uint32_t m = s_mask[k];
+        gm[k] = m;
+        cnt += __popc(m);
+    }
+    int nbits;
+    (void)block_excl_scan_sort(cnt, scan, &nbits);
+    if (tid == 0) {
+        u[w] = total;
+        bits_out[w] = nbits;
+    }
 }
 
 __global__ __launch_bounds__(kPlanThreads) void k_heavy_compact(
@@ -242,102 +549,127 @@ __global__ __launch_bounds__(256) void k_scan_add(int32_t *out, int32_t n,
     }
 }
 
-// Column lists (sptd, padded with -1) and block bitmaps of one window per
-// workgroup.  The window's sorted distinct columns and its bitmaps are held
-// in LDS: each CSR entry finds its row among the 16 row starts and its
-// compacted column by binary search, sets its bit with an LDS atomic OR, and
-// the block arrays are written out once, coalesced.  The set bits are
-// counted on the way out (distinct (row, col) pairs of A).  A window with
-// more distinct columns than the LDS holds (from the heavy path) works on
-// its own global bitmaps instead, zeroed first.
-__global__ __launch_bounds__(kPlanThreads) void k_fill_windows(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-    const int32_t *tmp_cols, const int32_t *u, const int32_t *blk_off,
-    int32_t *cols, uint32_t *mask, unsigned long long *nnz_out)
+// Bitmaps of the heavy windows, one workgroup each, built with atomics in the
+// window's staging region: each
+// entry finds its row among the row starts and its compacted column by
+// binary search in the window's distinct columns.  The set bits go to
+// bits[w].
+__global__ __launch_bounds__(kPlanThreads) void k_heavy_masks(
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *list,
+    const int32_t *tmp_cols, const int32_t *u, uint32_t *tmp_mask, int32_t *bits_out)
 {
-    __shared__ int32_t s_uc[kSortCap];
-    __shared__ uint32_t s_mask[kSortCap / kBlockCols * kMaskWords];
     __shared__ int32_t s_rp[kWindowRows + 1];
-    __shared__ unsigned long long s_cnt;
+    __shared__ int32_t s_cnt;
     const int tid = threadIdx.x;
-    const int w = blockIdx.x;
+    const int w = list[blockIdx.x];
     const int r0 = w * kWindowRows;
     const int nr = min(r0 + kWindowRows, N) - r0;
     if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
     if (tid == 0) s_cnt = 0;
-    const int32_t *uc = tmp_cols + row_ptr[r0];
+    const int32_t beg0 = row_ptr[r0];
+    const int32_t *uc = tmp_cols + beg0;
     const int uw = u[w];
-    const int ob = blk_off[w];
-    const int nbw = blk_off[w + 1] - ob;
-    const bool in_lds = uw <= kSortCap;
-    uint32_t *gmask = mask + (int64_t)kMaskWords * ob;
-    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads) {
-        if (in_lds) s_mask[k] = 0;
-        else gmask[k] = 0;
-    }
-    if (in_lds)
-        for (int k = tid; k < uw; k += kPlanThreads) s_uc[k] = uc[k];
+    const int nbw = (uw + kBlockCols - 1) / kBlockCols;
+    uint32_t *gm = tmp_mask + mask_stage(beg0, w);
+    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads) gm[k] = 0;
+    // the stores, atomics and loads on gm are all this workgroup's and are
+    // performed at the L2: workgroup-scope ordering is enough
     __threadfence_block();
     __syncthreads();
     const int beg = s_rp[0], n = s_rp[nr] - beg;
     for (int e = tid; e < n; e += kPlanThreads) {
-        // row of entry e: the last row start <= beg + e
-        int rlo = 0, rhi = nr;
+        int rlo = 0, rhi = nr;  // row of entry e: the last row start <= beg + e
         while (rhi - rlo > 1) {
             const int mid = (rlo + rhi) >> 1;
             if (s_rp[mid] <= beg + e) rlo = mid;
             else rhi = mid;
         }
         const int c = col_idx[beg + e];
+        if (c < 0 || c >= N) continue;  // reported by the sort
         int lo = 0, hi = uw;
         while (lo < hi) {
             const int mid = (lo + hi) >> 1;
-            if ((in_lds ? s_uc[mid] : uc[mid]) < c) lo = mid + 1;
+            if (uc[mid] < c) lo = mid + 1;
             else hi = mid;
         }
-        if (lo >= uw || (in_lds ? s_uc[lo] : uc[lo]) != c) continue;  // unreachable on valid CSR
+        if (lo >= uw) continue;  // every valid column is in the list
         const int cc = lo % kBlockCols;
         const int bit = 4 * (rlo + 16 * (cc / 4)) + (cc % 4);
-        const int word = kMaskWords * (lo / kBlockCols) + bit / 32;
-        if (in_lds) atomicOr(&s_mask[word], 1u << (bit % 32));
-        else atomicOr(&gmask[word], 1u << (bit % 32));
+        atomicOr(&gm[kMaskWords * (lo / kBlockCols) + bit / 32], 1u << (bit % 32));
     }
-    __threadfence_block();  // as in k_heavy_compact: one workgroup, L2 atomics
+    __threadfence_block();
     __syncthreads();
-    for (int k = tid; k < kBlockCols * nbw; k += kPlanThreads)
-        cols[(int64_t)kBlockCols * ob + k] = k < uw ? (in_lds ? s_uc[k] : uc[k]) : -1;
-    unsigned long long cnt = 0;
-    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads) {
-        uint32_t m;
-        if (in_lds) {
-            m = s_mask[k];
-            gmask[k] = m;
-        } else {
-            m = __hip_atomic_load(&gmask[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        cnt += __popc(m);
-    }
-    if (cnt) atomicAdd(&s_cnt, cnt);
+    int cnt = 0;
+    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads)
+        cnt += __popc(__hip_atomic_load(&gm[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    if (cnt) atomicAdd(&s_cnt, cnt);  // LDS
     __syncthreads();
-    if (tid == 0 && s_cnt) atomicAdd(nnz_out, s_cnt);
+    if (tid == 0) bits_out[w] = s_cnt;
 }
 
-__global__ void k_sum_i32(const int32_t *in, int32_t n, unsigned long long *out)
+// Padded column lists (sptd, -1 past the window's distinct columns) and the
+// block bitmaps copied from the staging areas to the window's blocks; one
+// wavefront per window, four per workgroup.
+__global__ __launch_bounds__(256) void k_fill_windows(
+    const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols, const uint32_t *tmp_mask,
+    const int32_t *u, const int32_t *blk_off, int32_t *cols, uint32_t *mask)
 {
+    const int lane = threadIdx.x & 63;
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= T) return;
+    const int32_t beg = row_ptr[w * kWindowRows];
+    const int uw = u[w];
+    const int64_t ob = blk_off[w];
+    const int nbw = blk_off[w + 1] - blk_off[w];
+    const int32_t *src = tmp_cols + beg;
+    const uint32_t *msrc = tmp_mask + mask_stage(beg, w);
+    int32_t *dst = cols + kBlockCols * ob;
+    uint32_t *mdst = mask + kMaskWords * ob;
+    for (int k = lane; k < kBlockCols * nbw; k += 64) dst[k] = k < uw ? src[k] : -1;
+    for (int k = lane; k < kMaskWords * nbw; k += 64) mdst[k] = msrc[k];
+}
+
+// Sum and maximum over n ints: grid-stride, then a workgroup reduction and
+// one atomic per workgroup (a few dozen workgroups).
+constexpr int kReduceThreads = 256;
+constexpr int kReduceBlocks = 64;
+
+__global__ __launch_bounds__(kReduceThreads) void k_sum_i32(const int32_t *in, int32_t n,
+                                                            unsigned long long *out)
+{
+    __shared__ unsigned long long part[kReduceThreads / 64];
     unsigned long long acc = 0;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
          k += (int64_t)gridDim.x * blockDim.x)
         acc += (unsigned long long)in[k];
-    if (acc) atomicAdd(out, acc);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+        for (int k = 0; k < kReduceThreads / 64; ++k) t += part[k];
+        if (t) atomicAdd(out, t);
+    }
 }
 
-__global__ void k_max_i32(const int32_t *in, int32_t n, int32_t *out)
+__global__ __launch_bounds__(kReduceThreads) void k_max_i32(const int32_t *in, int32_t n,
+                                                            int32_t *out)
 {
+    __shared__ int32_t part[kReduceThreads / 64];
     int32_t acc = 0;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
          k += (int64_t)gridDim.x * blockDim.x)
         acc = max(acc, in[k]);
-    atomicMax(out, acc);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc = max(acc, __shfl_xor(acc, o));
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t t = 0;
+        for (int k = 0; k < kReduceThreads / 64; ++k) t = max(t, part[k]);
+        if (t) atomicMax(out, t);
+    }
 }
 
 __global__ void k_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
@@ -434,34 +766,6 @@ __global__ void k_validate_plan(const int32_t *blk_off, int32_t T, const int32_t
     if (bad) atomicOr(err, 1);
 }
 
-// Entries of the pattern read back from a plan (every set bitmap bit is a
-// distinct (row, col) of A), one workgroup per window.  Without `out`, counts
-// the entries of each column; with it, scatters the row of each entry to
-// position cursor[col]++ of the transposed CSR (order inside a transposed row
-// is arbitrary: a plan built from it sorts its columns anyway).
-__global__ __launch_bounds__(256) void k_transpose_entries(const int32_t *blk_off,
-                                                           const int32_t *cols,
-                                                           const uint32_t *mask,
-                                                           int32_t *cursor, int32_t *out)
-{
-    const int w = blockIdx.x;
-    const int64_t w0 = (int64_t)blk_off[w] * kMaskWords, w1 = (int64_t)blk_off[w + 1] * kMaskWords;
-    for (int64_t t = w0 + threadIdx.x; t < w1; t += blockDim.x) {
-        const int64_t blk = t / kMaskWords;
-        const int word = (int)(t % kMaskWords);
-        uint32_t x = mask[t];
-        while (x) {
-            const int k = 32 * word + __ffs(x) - 1;
-            x &= x - 1;
-            const int r = (k >> 2) & 15;           // window row
-            const int c = 4 * (k >> 6) + (k & 3);  // block column
-            const int col = cols[kBlockCols * blk + c];
-            const int pos = atomicAdd(&cursor[col], 1);
-            if (out) out[pos] = w * kWindowRows + r;
-        }
-    }
-}
-
 inline unsigned grid_for(int64_t n, int threads)
 {
     int64_t g = (n + threads - 1) / threads;
@@ -477,14 +781,49 @@ hipError_t launch_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
     return hipGetLastError();
 }
 
-hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
-                              int32_t N, int32_t T, int32_t *tmp_cols,
-                              int32_t *u, int32_t *heavy, int32_t *n_heavy,
-                              int32_t *err, hipStream_t s)
+int64_t mask_stage_words(int64_t nnz, int32_t T) { return (nnz >> 1) + 8ll * T + 8; }
+
+hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                              int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
+                              int32_t *u, int32_t *is_big, int32_t *bits, int32_t *err,
+                              hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_window_sort<<<T, kPlanThreads, 0, s>>>(row_ptr, col_idx, N, tmp_cols, u,
-                                             heavy, n_heavy, err);
+    k_window_wave<<<T, 64, 0, s>>>(row_ptr, col_idx, N, tmp_cols, tmp_mask, u, is_big,
+                                   bits, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact_big(const int32_t *is_big, const int32_t *pos, int32_t T,
+                              int32_t *big, hipStream_t s)
+{
+    if (T == 0) return hipSuccess;
+    k_compact_big<<<grid_for(T, 256), 256, 0, s>>>(is_big, pos, T, big);
+    return hipGetLastError();
+}
+
+hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
+                              int32_t N, const int32_t *big, int32_t n_big,
+                              int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+                              int32_t *bits, int32_t *heavy, int32_t *n_heavy,
+                              int32_t *err, hipStream_t s)
+{
+    if (n_big == 0) return hipSuccess;
+    k_window_wave16<<<n_big, 64, 0, s>>>(row_ptr, col_idx, N, big, tmp_cols, tmp_mask, u,
+                                         bits, err);
+    k_window_sort<<<n_big, kSortThreads, 0, s>>>(row_ptr, col_idx, N, big, tmp_cols,
+                                                 tmp_mask, u, bits, heavy, n_heavy, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_heavy_masks(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                            const int32_t *list, int32_t count, const int32_t *tmp_cols,
+                            const int32_t *u, uint32_t *tmp_mask, int32_t *bits,
+                            hipStream_t s)
+{
+    if (count == 0) return hipSuccess;
+    k_heavy_masks<<<count, kPlanThreads, 0, s>>>(row_ptr, col_idx, N, list, tmp_cols, u,
+                                               tmp_mask, bits);
     return hipGetLastError();
 }
 
@@ -527,15 +866,14 @@ hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
     return hipGetLastError();
 }
 
-hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *col_idx,
-                               int32_t N, int32_t T, const int32_t *tmp_cols,
-                               const int32_t *u, const int32_t *blk_off,
-                               int32_t *cols, uint32_t *mask,
-                               unsigned long long *nnz_out, hipStream_t s)
+hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,
+                               const uint32_t *tmp_mask, const int32_t *u,
+                               const int32_t *blk_off, int32_t *cols, uint32_t *mask,
+                               hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_fill_windows<<<T, kPlanThreads, 0, s>>>(row_ptr, col_idx, N, tmp_cols, u,
-                                              blk_off, cols, mask, nnz_out);
+    k_fill_windows<<<grid_for(T, 4), 256, 0, s>>>(row_ptr, T, tmp_cols, tmp_mask, u,
+                                                  blk_off, cols, mask);
     return hipGetLastError();
 }
 
@@ -543,17 +881,16 @@ hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
                           hipStream_t s)
 {
     if (n == 0) return hipSuccess;
-    const unsigned g = grid_for(n, 256);
-    k_sum_i32<<<g < 4096 ? g : 4096, 256, 0, s>>>(in, n, out);
+    const unsigned g = grid_for(n, kReduceThreads);
+    k_sum_i32<<<g < kReduceBlocks ? g : kReduceBlocks, kReduceThreads, 0, s>>>(in, n, out);
     return hipGetLastError();
 }
 
-hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,
-                          hipStream_t s)
+hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out, hipStream_t s)
 {
     if (n == 0) return hipSuccess;
-    const unsigned g = grid_for(n, 256);
-    k_max_i32<<<g < 4096 ? g : 4096, 256, 0, s>>>(in, n, out);
+    const unsigned g = grid_for(n, kReduceThreads);
+    k_max_i32<<<g < kReduceBlocks ? g : kReduceBlocks, kReduceThreads, 0, s>>>(in, n, out);
     return hipGetLastError();
 }
 
@@ -603,12 +940,5 @@ hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s
     return hipGetLastError();
 }
 
-hipError_t launch_transpose_entries(const f3s_plan_s &p, int32_t *cursor, int32_t *out,
-                                   hipStream_t s)
-{
-    if (p.T == 0) return hipSuccess;
-    k_transpose_entries<<<p.T, 256, 0, s>>>(p.blk_off, p.cols, p.mask, cursor, out);
-    return hipGetLastError();
-}
 
 }  // namespace f3s

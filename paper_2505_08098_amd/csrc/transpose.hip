@@ -1,0 +1,160 @@
+// CSR of the transposed pattern A^T from a plan, on the GPU, without atomics:
+// the plan's block bitmaps are decoded into (column, row) pairs, the pairs
+// are radix-sorted by column (hipCUB, stable), and the row pointers of A^T
+// follow from the sorted columns by binary search.  The pattern a plan holds
+// is A with duplicates merged (Section 3.1's bitmaps), so A^T has one entry
+// per set bit.
+#include <hipcub/hipcub.hpp>
+
+#include "f3s_internal.h"
+
+namespace f3s {
+namespace {
+
+__device__ __forceinline__ int wave_excl_scan_t(int v, int lane, int *total)
+{
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    *total = __shfl(incl, 63);
+    return incl - v;
+}
+
+// Set bits of each window's bitmaps; one wavefront per window.
+__global__ __launch_bounds__(256) void k_window_bits(const int32_t *blk_off,
+                                                     const uint32_t *mask, int32_t T,
+                                                     int32_t *cnt)
+{
+    const int lane = threadIdx.x & 63;
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= T) return;
+    const int64_t k0 = (int64_t)kMaskWords * blk_off[w];
+    const int64_t k1 = (int64_t)kMaskWords * blk_off[w + 1];
+    int c = 0;
+    for (int64_t k = k0 + lane; k < k1; k += 64) c += __popc(mask[k]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+    if (lane == 0) cnt[w] = c;
+}
+
+// (column, row) of every set bit of window w, written from off[w] on in bit
+// order; one wavefront per window.
+__global__ __launch_bounds__(256) void k_window_pairs(const int32_t *blk_off,
+                                                      const int32_t *cols,
+                                                      const uint32_t *mask, int32_t T,
+                                                      const int32_t *off, uint32_t *keys,
+                                                      int32_t *rows)
+{
+    const int lane = threadIdx.x & 63;
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= T) return;
+    const int64_t k0 = (int64_t)kMaskWords * blk_off[w];
+    const int64_t k1 = (int64_t)kMaskWords * blk_off[w + 1];
+    int64_t base = off[w];
+    for (int64_t kb = k0; kb < k1; kb += 64) {
+        const int64_t k = kb + lane;
+        uint32_t m = k < k1 ? mask[k] : 0u;
+        int total;
+        int64_t pos = base + wave_excl_scan_t(__popc(m), lane, &total);
+        const int64_t blk = k / kMaskWords;
+        const int word = (int)(k % kMaskWords);
+        while (m) {
+            const int bit = 32 * word + __ffs(m) - 1;
+            m &= m - 1;
+            const int r = (bit >> 2) & 15;             // window row
+            const int c = 4 * (bit >> 6) + (bit & 3);  // block column
+            keys[pos] = (uint32_t)cols[kBlockCols * blk + c];
+            rows[pos] = w * kWindowRows + r;
+            ++pos;
+        }
+        base += total;
+    }
+}
+
+// rp[c] = number of sorted keys below c, for c = 0 .. N.
+__global__ void k_rows_from_sorted(const uint32_t *keys, int32_t n, int32_t N, int32_t *rp)
+{
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c > N) return;
+    int lo = 0, hi = n;
+    while (lo < hi) {
+        const int mid = (int)(((int64_t)lo + hi) >> 1);
+        if ((int64_t)keys[mid] < c) lo = mid + 1;
+        else hi = mid;
+    }
+    rp[c] = lo;
+}
+
+int key_bits(int32_t N)
+{
+    int b = 1;
+    while (b < 31 && (1ll << b) < N) ++b;
+    return b;
+}
+
+}  // namespace
+
+// Scratch of launch_transpose_csr: keys in and out, rows in, per-window
+// counts and offsets, the scan's workspace and the radix sort's storage.
+hipError_t transpose_scratch_bytes(const f3s_plan_s &p, size_t *bytes)
+{
+    const int32_t n = (int32_t)p.nnz;
+    size_t sort_bytes = 0;
+    hipError_t e = hipcub::DeviceRadixSort::SortPairs(
+        nullptr, sort_bytes, (const uint32_t *)nullptr, (uint32_t *)nullptr,
+        (const int32_t *)nullptr, (int32_t *)nullptr, n, 0, key_bits(p.N));
+    if (e != hipSuccess) return e;
+    auto r = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    const size_t pairs = (size_t)(n > 0 ? n : 1);
+    *bytes = 3 * r(4 * pairs) + 2 * r(4 * ((size_t)p.T + 1)) +
+             r(4 * (size_t)scan_tmp_ints(p.T)) + r(sort_bytes);
+    return hipSuccess;
+}
+
+hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scratch_bytes,
+                                int32_t *rp, int32_t *ci, hipStream_t s)
+{
+    const int32_t n = (int32_t)p.nnz;
+    const int32_t T = p.T;
+    auto r = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    const size_t pairs = (size_t)(n > 0 ? n : 1);
+    char *at = static_cast<char *>(scratch);
+    auto take = [&](size_t b) {
+        char *q = at;
+        at += r(b);
+        return q;
+    };
+    uint32_t *keys_in = (uint32_t *)take(4 * pairs);
+    uint32_t *keys_out = (uint32_t *)take(4 * pairs);
+    int32_t *rows_in = (int32_t *)take(4 * pairs);
+    int32_t *cnt = (int32_t *)take(4 * ((size_t)T + 1));
+    int32_t *off = (int32_t *)take(4 * ((size_t)T + 1));
+    int32_t *scan_tmp = (int32_t *)take(4 * (size_t)scan_tmp_ints(T));
+    const size_t used = (size_t)(at - static_cast<char *>(scratch));
+    if (used > scratch_bytes) return hipErrorInvalidValue;
+    size_t sort_bytes = scratch_bytes - used;
+    if (T > 0) {
+        k_window_bits<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.mask, T, cnt);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        e = launch_scan(cnt, off, T, scan_tmp, nullptr, s);
+        if (e != hipSuccess) return e;
+        k_window_pairs<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.cols, p.mask, T, off,
+                                                   keys_in, rows_in);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (n > 0) {
+        hipError_t e = hipcub::DeviceRadixSort::SortPairs(at, sort_bytes, keys_in, keys_out,
+                                                          rows_in, ci, n, 0, key_bits(p.N), s);
+        if (e != hipSuccess) return e;
+    }
+    k_rows_from_sorted<<<(unsigned)(((int64_t)p.N + 1 + 255) / 256), 256, 0, s>>>(
+        keys_out, n, p.N, rp);
+    return hipGetLastError();
+}
+
+}  // namespace f3s

@@ -73,6 +73,49 @@ def test_plan_heavy_window_above_lds_capacity(gpu, oracle):
     assert info["max_blocks"] > 256
 
 
+def _windows_of_sizes(rng, sizes, N, dup_frac=0.3):
+    """CSR whose window w holds sizes[w] entries spread over its 16 rows, with
+    duplicates and unsorted columns; the remaining rows are empty."""
+    rows = [[] for _ in range(N)]
+    for w, n in enumerate(sizes):
+        pool = rng.choice(N, size=max(1, int(n * (1 - dup_frac))), replace=False)
+        cols = rng.choice(pool, size=n, replace=True)
+        which = rng.integers(0, 16, size=n)
+        for r in range(16):
+            rows[16 * w + r] = cols[which == r].tolist()
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([len(r) for r in rows])
+    ci = np.array([c for r in rows for c in r], dtype=np.int32)
+    return rp, ci
+
+
+def test_plan_window_size_classes(gpu, oracle):
+    """Every sorting path of the plan: one wavefront with 1, 2, 4, 8 or 16 keys
+    per lane (up to 64, 128, 256, 512, 1024 entries), the workgroup LDS sort
+    (up to 4096) and the column-bitmap path above it, each at its edges."""
+    rng = np.random.default_rng(11)
+    sizes = [0, 1, 17, 64, 65, 100, 128, 129, 256, 257, 400, 512, 513, 1000,
+             1024, 1025, 4096, 4097, 6000, 3, 0, 64]
+    N = 9000
+    rp, ci = _windows_of_sizes(rng, sizes, N)
+    _check_plan_against_oracle(gpu, oracle, rp, ci, N)
+
+
+@pytest.mark.parametrize("size", [100, 600, 2000, 5000])
+def test_plan_rejects_bad_column_in_each_path(gpu, size):
+    """An out-of-range column is reported whichever path sorts its window."""
+    rng = np.random.default_rng(size)
+    N = 9000
+    rp, ci = _windows_of_sizes(rng, [50, size, 20], N)
+    lo, hi = int(rp[16]), int(rp[32])
+    for bad in (N, -1):
+        c2 = ci.copy()
+        c2[(lo + hi) // 2] = bad
+        with pytest.raises(gpu.F3SError) as e:
+            _plan(gpu, rp, c2, N)
+        assert e.value.code == 2  # F3S_ERR_INVALID_CSR
+
+
 def test_plan_split_windows(gpu, oracle, monkeypatch):
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
     c = W.make_config(2, with_features=False)

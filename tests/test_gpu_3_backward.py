@@ -88,7 +88,7 @@ def test_empty_rows_have_minus_inf_lse(gpu):
     assert np.all(np.isneginf(lse[empty])) and np.all(np.isfinite(lse[~empty]))
 
 
-@pytest.mark.parametrize("k", [1, 2, 4])
+@pytest.mark.parametrize("k", [1, 2, 4, 5])
 def test_transposed_plan_is_the_plan_of_the_transpose(gpu, oracle, k):
     c = W.make_config(k, with_features=False)
     N = c["N"]
@@ -100,6 +100,21 @@ def test_transposed_plan_is_the_plan_of_the_transpose(gpu, oracle, k):
         assert np.array_equal(got[key], ref[key]), key
     b = oracle.bsb(rp2, ci2, N)
     assert np.array_equal(got["cols"], b["cols"]) and np.array_equal(got["mask"], b["mask"])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_transposed_plan_of_asymmetric_patterns(gpu, oracle, seed):
+    """Random directed patterns with duplicates and empty rows: the plan of A^T
+    built from a plan of A equals the oracle's layout of A^T."""
+    rng = np.random.default_rng(500 + seed)
+    N = int(rng.integers(1, 400))
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 70), empty_frac=0.2, dup_frac=0.3)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    got = plan.transpose().export()
+    rp2, ci2 = _transpose_csr(rp, ci, N)
+    b = oracle.bsb(rp2, ci2, N)
+    for key in ("blk_off", "cols", "mask"):
+        assert np.array_equal(got[key], b[key]), key
 
 
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
