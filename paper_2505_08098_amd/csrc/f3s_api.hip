@@ -119,31 +119,14 @@ hipError_t read_scalar(T *host, const T *dev)
     return hipMemcpy(host, dev, sizeof(T), hipMemcpyDeviceToHost);
 }
 
-// Work-list piece size: aim for at most one piece's worth of blocks per
-// wavefront slot so the tail of the launch stays short; even, >= 16.
-// Piece size (even): about n_blocks / (8 x CUs) blocks, so the work list has
-// of the order of 8 items per CU, at least 16 blocks (smaller pieces help
-// the forward on tiny graphs a little but add merge launches to the
-// backward).  Never above the largest window (a larger value splits nothing
-// and only widens the bucket histogram of the work-list sort).
-int choose_piece(int64_t n_blocks, int32_t max_blocks, int device)
+// Work-list slots of a device: 8 per compute unit.
+int32_t plan_slots(int device)
 {
-    const int64_t cap = ((int64_t)(max_blocks > 2 ? max_blocks : 2) + 1) & ~1LL;
-    int64_t piece;
-    const int env = env_int("F3S_PIECE_BLOCKS", 0);
-    if (env >= 2) {
-        piece = env & ~1;
-    } else {
-        int cus = 256;
-        hipDeviceProp_t prop;
-        if (hipGetDeviceProperties(&prop, device) == hipSuccess && prop.multiProcessorCount > 0)
-            cus = prop.multiProcessorCount;
-        const int64_t slots = (int64_t)cus * 8;
-        piece = (n_blocks + slots - 1) / slots;
-        if (piece < 16) piece = 16;
-        piece = (piece + 1) & ~1LL;
-    }
-    return (int)(piece < cap ? piece : cap);
+    int cus = 256;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, device) == hipSuccess && prop.multiProcessorCount > 0)
+        cus = prop.multiProcessorCount;
+    return 8 * cus;
 }
 
 // Device-side statistics of a plan build, read back with one copy each
@@ -156,6 +139,7 @@ struct BuildStats {
     int32_t n_heavy;              // windows too large for the LDS sort
     int32_t max_blocks;
     int32_t n_blocks;
+    int32_t piece;
     int32_t n_pieces;
     int32_t n_split;
     int32_t n_items;              // total of the work-list histogram
@@ -177,16 +161,25 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     if (nnz > 0 && !col_idx) return F3S_ERR_INVALID_VALUE;
     p->nnz_csr = nnz;
 
-    // all scratch of the build in one allocation
+    // all scratch of the build in one allocation, with room for the
+    // work-list histogram at the largest piece size the block count allows
+    // (blocks <= nnz / 16 + T); a forced larger piece allocates its own
     const int64_t stage_words = mask_stage_words(nnz, T);
+    const int32_t slots = plan_slots(p->device);
+    const int32_t chunk = 64;
+    const int32_t nchunks = (T + chunk - 1) / chunk;
+    const int64_t piece_bound = ((int64_t)nnz / 16 + T + slots - 1) / slots + 18;
+    const int64_t hist_room = (piece_bound + 1) * nchunks + 1 +
+                              scan_tmp_ints((piece_bound + 1) * nchunks);
     ScratchArena tmp;
     tmp.add<BuildStats>(1);
     tmp.add<int32_t>(nnz);               // sorted distinct columns per window
     tmp.add<uint32_t>(stage_words);      // block bitmaps per window
     // u, big, is_big, bits, heavy, nb, npieces, key
     for (int k = 0; k < 8; ++k) tmp.add<int32_t>(T);
-    for (int k = 0; k < 3; ++k) tmp.add<int32_t>((int64_t)T + 1);  // tro, splits
+    for (int k = 0; k < 3; ++k) tmp.add<int32_t>((int64_t)T + 1);  // big_pos, splits
     tmp.add<int32_t>(scan_tmp_ints(T));
+    tmp.add<int32_t>(hist_room);
     HIP_TRY(tmp.alloc());
     BuildStats *st = tmp.take<BuildStats>(1);
     int32_t *tmp_cols = tmp.take<int32_t>(nnz);
@@ -196,10 +189,11 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     int32_t *heavy = tmp.take<int32_t>(T);
     int32_t *nb = tmp.take<int32_t>(T), *npieces = tmp.take<int32_t>(T);
     int32_t *key = tmp.take<int32_t>(T);
-    int32_t *tro = tmp.take<int32_t>((int64_t)T + 1);
+    int32_t *big_pos = tmp.take<int32_t>((int64_t)T + 1);
     int32_t *split_pieces = tmp.take<int32_t>((int64_t)T + 1);
     int32_t *split_one = tmp.take<int32_t>((int64_t)T + 1);
     int32_t *scan_tmp = tmp.take<int32_t>(scan_tmp_ints(T));
+    int32_t *hist_area = tmp.take<int32_t>(hist_room);
     BuildStats hs;
     HIP_TRY(hipMemsetAsync(st, 0, sizeof(BuildStats), s));
 
@@ -207,8 +201,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
     HIP_TRY(launch_window_wave(row_ptr, col_idx, N, T, tmp_cols, tmp_mask, u, is_big,
                                bits, &st->err, s));
-    HIP_TRY(launch_scan(is_big, tro, T, scan_tmp, &st->n_big, s));  // tro as scratch
-    HIP_TRY(launch_compact_big(is_big, tro, T, big, s));
+    HIP_TRY(launch_scan(is_big, big_pos, T, scan_tmp, &st->n_big, s));
+    HIP_TRY(launch_compact_big(is_big, big_pos, T, big, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
     if (hs.n_big > 0) {
@@ -238,38 +232,35 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     }
     HIP_TRY(launch_heavy_masks(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, u,
                              tmp_mask, bits, s));
-    HIP_TRY(launch_sum_i32(bits, T, &st->nnz, s));
 
-    // ---- 3. blocks per window, their prefix (tro), statistics -----------
-    HIP_TRY(launch_blocks_per_window(u, T, nb, s));
-    HIP_TRY(launch_scan(nb, tro, T, scan_tmp, &st->n_blocks, s));
-    HIP_TRY(launch_sum_i32(u, T, &st->n_unique, s));
-    HIP_TRY(launch_max_i32(nb, T, &st->max_blocks, s));
+    // ---- 3. blocks per window and statistics; work-list shape: piece size,
+    //         split windows, item count (one host round trip for all) -------
+    HIP_TRY(launch_window_stats(u, bits, T, nb, &st->n_unique, &st->nnz, &st->n_blocks,
+                                &st->max_blocks, s));
+    const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
+    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0);
+    HIP_TRY(launch_bin_keys(nb, T, &st->n_blocks, &st->max_blocks,
+                            env_int("F3S_PIECE_BLOCKS", 0), slots, reorder,
+                            &st->piece, npieces, key, split_pieces, split_one, s));
+    HIP_TRY(launch_scan(split_pieces, split_pieces, T, scan_tmp, &st->n_pieces, s));
+    HIP_TRY(launch_scan(split_one, split_one, T, scan_tmp, &st->n_split, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
     const int32_t B = hs.n_blocks;
     p->n_blocks = B;
     p->n_unique = (int64_t)hs.n_unique;
+    p->nnz = (int64_t)hs.nnz;
     p->max_blocks = hs.max_blocks;
     p->bsb_bytes = 4ll * (T + 1) + 4ll * kBlockCols * B + 4ll * kMaskWords * B;
-
-    // ---- 4. work-list shape: piece size, split windows, item count ------
-    const int32_t piece = choose_piece(B, p->max_blocks, p->device);
+    const int32_t piece = hs.piece;
     p->piece = piece;
-    const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
-    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0);
-    HIP_TRY(launch_bin_keys(nb, T, piece, reorder, npieces, key, split_pieces,
-                            split_one, s));
-    HIP_TRY(launch_scan(split_pieces, split_pieces, T, scan_tmp, &st->n_pieces, s));
-    HIP_TRY(launch_scan(split_one, split_one, T, scan_tmp, &st->n_split, s));
-    HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     p->n_pieces = hs.n_pieces;
     p->n_split = hs.n_split;
     const int64_t n_items = (int64_t)T - p->n_split + p->n_pieces;
     if (n_items > INT32_MAX) return F3S_ERR_UNSUPPORTED;
     p->n_items = (int32_t)n_items;
 
-    // ---- 5. the plan's arrays: one allocation, plus the partial buffers --
+    // ---- 4. the plan's arrays: one allocation, plus the partial buffers --
     {
         Arena a;
         a.add<int32_t>((int64_t)T + 1);
@@ -287,34 +278,33 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
         p->merges = a.take<int32_t>(3ll * p->n_split);
     }
     HIP_TRY(alloc_parts(p, part_row));
-    HIP_TRY(hipMemcpyAsync(p->blk_off, tro, sizeof(int32_t) * ((size_t)T + 1),
-                           hipMemcpyDeviceToDevice, s));
+    HIP_TRY(launch_scan(nb, p->blk_off, T, scan_tmp, nullptr, s));  // window block offsets
 
-    // ---- 6. column lists and bitmaps into their blocks --------------------
+    // ---- 5. column lists and bitmaps into their blocks --------------------
     HIP_TRY(launch_fill_windows(row_ptr, T, tmp_cols, tmp_mask, u, p->blk_off, p->cols,
                                 p->mask, s));
 
-    // ---- 7. heavy-first work list: histogram over (key, chunk), scan, scatter
-    const int32_t chunk = 64;
-    const int32_t nchunks = (T + chunk - 1) / chunk;
+    // ---- 6. heavy-first work list: histogram over (key, chunk), scan, scatter
     const int64_t cells = (int64_t)(piece + 1) * nchunks;
     if (cells >= INT32_MAX) return F3S_ERR_UNSUPPORTED;
+    int32_t *hist = hist_area, *hist_tmp = hist_area + cells + 1;
     ScratchArena hist_arena;
-    hist_arena.add<int32_t>(cells + 1);
-    hist_arena.add<int32_t>(scan_tmp_ints(cells));
-    HIP_TRY(hist_arena.alloc());
-    int32_t *hist = hist_arena.take<int32_t>(cells + 1);
-    int32_t *hist_tmp = hist_arena.take<int32_t>(scan_tmp_ints(cells));
+    if (cells + 1 + scan_tmp_ints(cells) > hist_room) {
+        hist_arena.add<int32_t>(cells + 1);
+        hist_arena.add<int32_t>(scan_tmp_ints(cells));
+        HIP_TRY(hist_arena.alloc());
+        hist = hist_arena.take<int32_t>(cells + 1);
+        hist_tmp = hist_arena.take<int32_t>(scan_tmp_ints(cells));
+    }
     HIP_TRY(hipMemsetAsync(hist, 0, (size_t)(cells + 1) * 4, s));
     HIP_TRY(launch_bin_hist(npieces, key, T, piece, chunk, nchunks, hist, s));
     HIP_TRY(launch_scan(hist, hist, (int32_t)cells, hist_tmp, &st->n_items, s));
     HIP_TRY(launch_bin_scatter(nb, p->blk_off, npieces, key, split_pieces, split_one,
                                T, piece, chunk, nchunks, hist, p->items, p->merges, s));
 
-    // ---- 8. integrity check of the finished plan ------------------------
+    // ---- 7. integrity check of the finished plan ------------------------
     HIP_TRY(launch_validate_plan(*p, &st->invalid, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
-    p->nnz = (int64_t)hs.nnz;
     if (hs.invalid || hs.n_items != p->n_items) return F3S_ERR_HIP;
     return F3S_OK;
 }

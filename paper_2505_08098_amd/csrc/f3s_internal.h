@@ -104,8 +104,12 @@ hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
                                 uint32_t *bitmap, int32_t words,
                                 int32_t *tmp_cols, int32_t *u, int32_t *err,
                                 hipStream_t s);
-hipError_t launch_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb,
-                                    hipStream_t s);
+// nb[w] = ceil(u[w] / 16) and the sums of u, bits and nb and the largest nb
+// (added / max-ed into the four outputs, zeroed by the caller).
+hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
+                               int32_t *nb, unsigned long long *sum_u,
+                               unsigned long long *sum_bits, int32_t *sum_nb,
+                               int32_t *max_nb, hipStream_t s);
 // Exclusive scan of n int32 into out[0..n], out[n] = total (in == out ok);
 // tmp: scan_tmp_ints(n) ints of workspace; total_out (may be null) also
 // receives the total.
@@ -117,15 +121,15 @@ hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t 
                                const uint32_t *tmp_mask, const int32_t *u,
                                const int32_t *blk_off, int32_t *cols, uint32_t *mask,
                                hipStream_t s);
-hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
-                          hipStream_t s);
-hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out,
-                          hipStream_t s);
-// Work list: per window piece count, bucket key, split flags.
+// Work list: the piece size (from the block count and largest window on the
+// device, see plan_piece; forced >= 2 overrides it; slots = 8 per CU) into
+// *piece_out, then per window piece count, bucket key, split flags.
 // reorder == false gives every window the same key (window order kept).
-hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
-                           int32_t *npieces, int32_t *key, int32_t *split_pieces,
-                           int32_t *split_one, hipStream_t s);
+hipError_t launch_bin_keys(const int32_t *nb, int32_t T, const int32_t *n_blocks,
+                           const int32_t *max_blocks, int32_t forced, int32_t slots,
+                           bool reorder, int32_t *piece_out, int32_t *npieces,
+                           int32_t *key, int32_t *split_pieces, int32_t *split_one,
+                           hipStream_t s);
 hipError_t launch_bin_hist(const int32_t *npieces, const int32_t *key, int32_t T,
                            int32_t piece, int32_t chunk, int32_t nchunks,
                            int32_t *hist, hipStream_t s);

@@ -472,10 +472,59 @@ __global__ __launch_bounds__(kPlanThreads) void k_heavy_compact(
     if (tid == 0) u[w] = total;
 }
 
-__global__ void k_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb)
+// Per window: blocks nb = ceil(u/16); over all windows: sum of u (distinct
+// columns), sum of bits (distinct entries), sum of nb (blocks) and the
+// largest nb.  Grid-stride, then a workgroup reduction and one atomic per
+// statistic and workgroup.
+constexpr int kStatThreads = 256;
+constexpr int kStatBlocks = 64;
+
+__global__ __launch_bounds__(kStatThreads) void k_window_stats(
+    const int32_t *u, const int32_t *bits, int32_t T, int32_t *nb,
+    unsigned long long *sum_u, unsigned long long *sum_bits, int32_t *sum_nb,
+    int32_t *max_nb)
 {
-    const int w = blockIdx.x * blockDim.x + threadIdx.x;
-    if (w < T) nb[w] = (u[w] + kBlockCols - 1) / kBlockCols;
+    __shared__ unsigned long long part[3][kStatThreads / 64];
+    __shared__ int32_t pmax[kStatThreads / 64];
+    unsigned long long su = 0, sb = 0, sn = 0;
+    int32_t mx = 0;
+    for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < T;
+         w += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t uw = u[w];
+        const int32_t b = (uw + kBlockCols - 1) / kBlockCols;
+        nb[w] = b;
+        su += (unsigned long long)uw;
+        sb += (unsigned long long)bits[w];
+        sn += (unsigned long long)b;
+        mx = max(mx, b);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        su += __shfl_xor(su, o);
+        sb += __shfl_xor(sb, o);
+        sn += __shfl_xor(sn, o);
+        mx = max(mx, __shfl_xor(mx, o));
+    }
+    const int wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        part[0][wv] = su;
+        part[1][wv] = sb;
+        part[2][wv] = sn;
+        pmax[wv] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int k = 1; k < kStatThreads / 64; ++k) {
+            su += part[0][k];
+            sb += part[1][k];
+            sn += part[2][k];
+            mx = max(mx, pmax[k]);
+        }
+        if (su) atomicAdd(sum_u, su);
+        if (sb) atomicAdd(sum_bits, sb);
+        if (sn) atomicAdd(sum_nb, (int32_t)sn);
+        if (mx) atomicMax(max_nb, mx);
+    }
 }
 
 constexpr int kScanThreads = 1024;
@@ -629,54 +678,35 @@ __global__ __launch_bounds__(256) void k_fill_windows(
     for (int k = lane; k < kMaskWords * nbw; k += 64) mdst[k] = msrc[k];
 }
 
-// Sum and maximum over n ints: grid-stride, then a workgroup reduction and
-// one atomic per workgroup (a few dozen workgroups).
-constexpr int kReduceThreads = 256;
-constexpr int kReduceBlocks = 64;
-
-__global__ __launch_bounds__(kReduceThreads) void k_sum_i32(const int32_t *in, int32_t n,
-                                                            unsigned long long *out)
+// Work-list piece size (even): about n_blocks / slots blocks (slots = 8 per
+// CU), so the work list has of the order of 8 items per CU, at least 16
+// blocks (smaller pieces help the forward on tiny graphs a little but add
+// merge launches to the backward); never above the largest window (a larger
+// value splits nothing and only widens the bucket histogram of the work-list
+// sort).  forced >= 2 overrides the estimate.
+__device__ int32_t plan_piece(int64_t n_blocks, int32_t max_blocks, int32_t forced,
+                              int32_t slots)
 {
-    __shared__ unsigned long long part[kReduceThreads / 64];
-    unsigned long long acc = 0;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
-         k += (int64_t)gridDim.x * blockDim.x)
-        acc += (unsigned long long)in[k];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
-    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned long long t = 0;
-        for (int k = 0; k < kReduceThreads / 64; ++k) t += part[k];
-        if (t) atomicAdd(out, t);
+    const int64_t cap = ((int64_t)(max_blocks > 2 ? max_blocks : 2) + 1) & ~1LL;
+    int64_t piece;
+    if (forced >= 2) {
+        piece = forced & ~1;
+    } else {
+        piece = (n_blocks + slots - 1) / slots;
+        if (piece < 16) piece = 16;
+        piece = (piece + 1) & ~1LL;
     }
+    return (int32_t)(piece < cap ? piece : cap);
 }
 
-__global__ __launch_bounds__(kReduceThreads) void k_max_i32(const int32_t *in, int32_t n,
-                                                            int32_t *out)
-{
-    __shared__ int32_t part[kReduceThreads / 64];
-    int32_t acc = 0;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n;
-         k += (int64_t)gridDim.x * blockDim.x)
-        acc = max(acc, in[k]);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) acc = max(acc, __shfl_xor(acc, o));
-    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int32_t t = 0;
-        for (int k = 0; k < kReduceThreads / 64; ++k) t = max(t, part[k]);
-        if (t) atomicMax(out, t);
-    }
-}
-
-__global__ void k_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
-                           int32_t *npieces, int32_t *key, int32_t *split_pieces,
-                           int32_t *split_one)
+__global__ void k_bin_keys(const int32_t *nb, int32_t T, const int32_t *n_blocks,
+                           const int32_t *max_blocks, int32_t forced, int32_t slots,
+                           bool reorder, int32_t *piece_out, int32_t *npieces,
+                           int32_t *key, int32_t *split_pieces, int32_t *split_one)
 {
     const int w = blockIdx.x * blockDim.x + threadIdx.x;
+    const int32_t piece = plan_piece(*n_blocks, *max_blocks, forced, slots);
+    if (w == 0) *piece_out = piece;
     if (w >= T) return;
     const int n = nb[w];
     const bool split = n > piece;
@@ -839,23 +869,31 @@ hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
     return hipGetLastError();
 }
 
-hipError_t launch_blocks_per_window(const int32_t *u, int32_t T, int32_t *nb,
-                                    hipStream_t s)
+hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
+                               int32_t *nb, unsigned long long *sum_u,
+                               unsigned long long *sum_bits, int32_t *sum_nb,
+                               int32_t *max_nb, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_blocks_per_window<<<grid_for(T, 256), 256, 0, s>>>(u, T, nb);
+    const unsigned g = grid_for(T, kStatThreads);
+    k_window_stats<<<g < kStatBlocks ? g : kStatBlocks, kStatThreads, 0, s>>>(
+        u, bits, T, nb, sum_u, sum_bits, sum_nb, max_nb);
     return hipGetLastError();
 }
 
+// Up to kScanWhole elements one workgroup walks the tiles in order (one
+// launch); above, the tiles are scanned in parallel (three launches).
+constexpr int64_t kScanWhole = 8 * (int64_t)kScanTile;
+
 int64_t scan_tmp_ints(int64_t n)
 {
-    return n <= kScanTile ? 1 : (n + kScanTile - 1) / kScanTile + 1;
+    return n <= kScanWhole ? 1 : (n + kScanTile - 1) / kScanTile + 1;
 }
 
 hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
                        int32_t *total_out, hipStream_t s)
 {
-    if (n <= kScanTile) {
+    if (n <= kScanWhole) {
         k_scan<<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total_out);
         return hipGetLastError();
     }
@@ -877,30 +915,15 @@ hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t 
     return hipGetLastError();
 }
 
-hipError_t launch_sum_i32(const int32_t *in, int32_t n, unsigned long long *out,
-                          hipStream_t s)
+hipError_t launch_bin_keys(const int32_t *nb, int32_t T, const int32_t *n_blocks,
+                           const int32_t *max_blocks, int32_t forced, int32_t slots,
+                           bool reorder, int32_t *piece_out, int32_t *npieces,
+                           int32_t *key, int32_t *split_pieces, int32_t *split_one,
+                           hipStream_t s)
 {
-    if (n == 0) return hipSuccess;
-    const unsigned g = grid_for(n, kReduceThreads);
-    k_sum_i32<<<g < kReduceBlocks ? g : kReduceBlocks, kReduceThreads, 0, s>>>(in, n, out);
-    return hipGetLastError();
-}
-
-hipError_t launch_max_i32(const int32_t *in, int32_t n, int32_t *out, hipStream_t s)
-{
-    if (n == 0) return hipSuccess;
-    const unsigned g = grid_for(n, kReduceThreads);
-    k_max_i32<<<g < kReduceBlocks ? g : kReduceBlocks, kReduceThreads, 0, s>>>(in, n, out);
-    return hipGetLastError();
-}
-
-hipError_t launch_bin_keys(const int32_t *nb, int32_t T, int32_t piece, bool reorder,
-                           int32_t *npieces, int32_t *key, int32_t *split_pieces,
-                           int32_t *split_one, hipStream_t s)
-{
-    if (T == 0) return hipSuccess;
-    k_bin_keys<<<grid_for(T, 256), 256, 0, s>>>(nb, T, piece, reorder, npieces, key,
-                                               split_pieces, split_one);
+    k_bin_keys<<<grid_for(T, 256), 256, 0, s>>>(nb, T, n_blocks, max_blocks, forced, slots,
+                                                reorder, piece_out, npieces, key,
+                                                split_pieces, split_one);
     return hipGetLastError();
 }
 

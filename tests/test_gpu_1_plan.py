@@ -123,6 +123,17 @@ def test_plan_split_windows(gpu, oracle, monkeypatch):
     assert info["piece_blocks"] == 4 and info["n_split"] > 100
 
 
+def test_plan_forced_piece_above_the_estimate(gpu, oracle, monkeypatch):
+    """A forced piece size larger than any window: capped at the largest
+    window (nothing split); its work-list histogram is larger than the one
+    the build reserves for the estimated piece size."""
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "100000")
+    c = W.make_config(2, with_features=False)
+    info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
+    assert info["n_split"] == 0
+    assert info["piece_blocks"] >= info["max_blocks"]
+
+
 def test_plan_empty_and_degenerate(gpu, oracle):
     # N = 0
     plan = _plan(gpu, np.zeros(1, dtype=np.int32), np.zeros(0, dtype=np.int32), 0)
