@@ -175,9 +175,10 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     tmp.add<BuildStats>(1);
     tmp.add<int32_t>(nnz);               // sorted distinct columns per window
     tmp.add<uint32_t>(stage_words);      // block bitmaps per window
-    // u, big, is_big, bits, heavy, nb, npieces, key
-    for (int k = 0; k < 8; ++k) tmp.add<int32_t>(T);
-    for (int k = 0; k < 3; ++k) tmp.add<int32_t>((int64_t)T + 1);  // big_pos, splits
+    // u, big, is_big, heavy, is_heavy, bits, nb, npieces, key, split_item
+    for (int k = 0; k < 10; ++k) tmp.add<int32_t>(T);
+    // big_pos, heavy_pos, split pieces, split flags
+    for (int k = 0; k < 4; ++k) tmp.add<int32_t>((int64_t)T + 1);
     tmp.add<int32_t>(scan_tmp_ints(T));
     tmp.add<int32_t>(hist_room);
     HIP_TRY(tmp.alloc());
@@ -185,11 +186,12 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     int32_t *tmp_cols = tmp.take<int32_t>(nnz);
     uint32_t *tmp_mask = tmp.take<uint32_t>(stage_words);
     int32_t *u = tmp.take<int32_t>(T), *big = tmp.take<int32_t>(T);
-    int32_t *is_big = tmp.take<int32_t>(T), *bits = tmp.take<int32_t>(T);
-    int32_t *heavy = tmp.take<int32_t>(T);
+    int32_t *is_big = tmp.take<int32_t>(T), *heavy = tmp.take<int32_t>(T);
+    int32_t *is_heavy = tmp.take<int32_t>(T), *bits = tmp.take<int32_t>(T);
     int32_t *nb = tmp.take<int32_t>(T), *npieces = tmp.take<int32_t>(T);
-    int32_t *key = tmp.take<int32_t>(T);
+    int32_t *key = tmp.take<int32_t>(T), *split_item = tmp.take<int32_t>(T);
     int32_t *big_pos = tmp.take<int32_t>((int64_t)T + 1);
+    int32_t *heavy_pos = tmp.take<int32_t>((int64_t)T + 1);
     int32_t *split_pieces = tmp.take<int32_t>((int64_t)T + 1);
     int32_t *split_one = tmp.take<int32_t>((int64_t)T + 1);
     int32_t *scan_tmp = tmp.take<int32_t>(scan_tmp_ints(T));
@@ -200,18 +202,18 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     // ---- 2. CSR check, distinct columns and bitmaps per window ----------
     HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
     HIP_TRY(launch_window_wave(row_ptr, col_idx, N, T, tmp_cols, tmp_mask, u, is_big,
-                               bits, &st->err, s));
+                               is_heavy, bits, &st->err, s));
     HIP_TRY(launch_scan(is_big, big_pos, T, scan_tmp, &st->n_big, s));
-    HIP_TRY(launch_compact_big(is_big, big_pos, T, big, s));
+    HIP_TRY(launch_scan(is_heavy, heavy_pos, T, scan_tmp, &st->n_heavy, s));
+    HIP_TRY(launch_compact_lists(is_big, big_pos, is_heavy, heavy_pos, T, big, heavy, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
-    if (hs.n_big > 0) {
-        HIP_TRY(launch_window_sort(row_ptr, col_idx, N, big, hs.n_big, tmp_cols, tmp_mask,
-                                   u, bits, heavy, &st->n_heavy, &st->err, s));
-        HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
-        if (hs.err) return F3S_ERR_INVALID_CSR;
-    }
-    if (hs.n_heavy > 0) {
+    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, big, hs.n_big, tmp_cols, tmp_mask, u,
+                               bits, &st->err, s));
+    if (hs.n_heavy > 0 && heavy_in_lds(N)) {
+        HIP_TRY(launch_heavy_lds(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, tmp_mask,
+                                 u, bits, &st->err, s));
+    } else if (hs.n_heavy > 0) {
         const int32_t words = (N + 31) / 32;
         const int64_t budget = 256ll << 20;  // bitmap workspace per batch
         int64_t per = (int64_t)words * 4;
@@ -229,9 +231,9 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
                                          words, tmp_cols, u, &st->err, s));
         }
         HIP_TRY(hipStreamSynchronize(s));  // the bitmap workspace is freed here
+        HIP_TRY(launch_heavy_masks(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, u,
+                                   tmp_mask, bits, s));
     }
-    HIP_TRY(launch_heavy_masks(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, u,
-                             tmp_mask, bits, s));
 
     // ---- 3. blocks per window and statistics; work-list shape: piece size,
     //         split windows, item count (one host round trip for all) -------
@@ -300,7 +302,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_bin_hist(npieces, key, T, piece, chunk, nchunks, hist, s));
     HIP_TRY(launch_scan(hist, hist, (int32_t)cells, hist_tmp, &st->n_items, s));
     HIP_TRY(launch_bin_scatter(nb, p->blk_off, npieces, key, split_pieces, split_one,
-                               T, piece, chunk, nchunks, hist, p->items, p->merges, s));
+                               T, piece, chunk, nchunks, hist, p->items, p->merges,
+                               split_item, p->n_split, s));
 
     // ---- 7. integrity check of the finished plan ------------------------
     HIP_TRY(launch_validate_plan(*p, &st->invalid, s));

@@ -75,24 +75,32 @@ int64_t mask_stage_words(int64_t nnz, int32_t T);
 // Per window of at most 512 entries (one wavefront each): sorted distinct
 // columns into tmp_cols at the window's CSR offset, their count into u, the
 // block bitmaps into the staging area, their set bits into bits.  Larger
-// windows get is_big = 1 and are left to launch_window_sort.
+// windows get is_big = 1 (up to 4096 entries) or is_heavy = 1.
 hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                               int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
-                              int32_t *u, int32_t *is_big, int32_t *bits, int32_t *err,
-                              hipStream_t s);
-// big[pos[w]] = w for every window with is_big[w] (pos: exclusive scan).
-hipError_t launch_compact_big(const int32_t *is_big, const int32_t *pos, int32_t T,
-                              int32_t *big, hipStream_t s);
+                              int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits,
+                              int32_t *err, hipStream_t s);
+// The flagged windows listed in window order (positions: scans of the flags).
+hipError_t launch_compact_lists(const int32_t *is_big, const int32_t *big_pos,
+                                const int32_t *is_heavy, const int32_t *heavy_pos,
+                                int32_t T, int32_t *big, int32_t *heavy, hipStream_t s);
 // The windows big[0 .. n_big): sorted distinct columns, u, bitmaps and bits
 // as above (one wavefront with 16 keys per lane up to 1024 entries, else an
-// LDS sort); windows above the LDS capacity are queued as heavy.
+// LDS sort).
 hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
                               int32_t N, const int32_t *big, int32_t n_big,
                               int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
-                              int32_t *bits, int32_t *heavy, int32_t *n_heavy,
-                              int32_t *err, hipStream_t s);
+                              int32_t *bits, int32_t *err, hipStream_t s);
+// Heavy windows when N is small enough for an N-bit LDS bitmap (heavy_in_lds):
+// columns, u, bitmaps and bits as above, one workgroup per window.
+bool heavy_in_lds(int32_t N);
+hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                            const int32_t *heavy, int32_t n_heavy, int32_t *tmp_cols,
+                            uint32_t *tmp_mask, int32_t *u, int32_t *bits, int32_t *err,
+                            hipStream_t s);
+// Otherwise: launch_heavy_compact in batches, then launch_heavy_masks.
 // Block bitmaps and bits of the windows list[0 .. count) once their columns
-// are known (the heavy windows).
+// are known.
 hipError_t launch_heavy_masks(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                             const int32_t *list, int32_t count, const int32_t *tmp_cols,
                             const int32_t *u, uint32_t *tmp_mask, int32_t *bits,
@@ -138,7 +146,8 @@ hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
                               const int32_t *slot_base, const int32_t *split_idx,
                               int32_t T, int32_t piece, int32_t chunk,
                               int32_t nchunks, int32_t *offs, WorkItem *items,
-                              int32_t *merges, hipStream_t s);
+                              int32_t *merges, int32_t *split_item, int32_t n_split,
+                              hipStream_t s);
 
 // ---- transposed pattern (transpose.hip) ----------------------------------
 // CSR of A^T (rp[N+1], ci[nnz]) from a plan's bitmaps; scratch of

@@ -215,11 +215,13 @@ __device__ __forceinline__ int32_t window_row_starts(const int32_t *row_ptr, int
 }
 
 // One wavefront (one workgroup) per window.  Windows with more than kWaveCap
-// entries are flagged in is_big for the later passes.  (No counter shared by
-// all windows: atomics on one address serialise, tens of ns each.)
+// entries are flagged in is_big (up to kSortCap entries) or is_heavy for the
+// later passes.  (No counter shared by all windows: atomics on one address
+// serialise, tens of ns each.)
 __global__ __launch_bounds__(64) void k_window_wave(
     const int32_t *row_ptr, const int32_t *col_idx, int32_t N, int32_t *tmp_cols,
-    uint32_t *tmp_mask, int32_t *u, int32_t *is_big, int32_t *bits_out, int32_t *err)
+    uint32_t *tmp_mask, int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits_out,
+    int32_t *err)
 {
     __shared__ int32_t s_cols[kWaveCap];
     __shared__ uint32_t s_mask[kWaveCap / kBlockCols * kMaskWords];
@@ -229,12 +231,15 @@ __global__ __launch_bounds__(64) void k_window_wave(
     // stops every wave here, before any column is read (is_big stays valid
     // for the scan that follows)
     if (*(volatile int32_t *)err) {
-        if (lane == 0) is_big[w] = 0;
+        if (lane == 0) is_big[w] = is_heavy[w] = 0;
         return;
     }
     int32_t beg, n;
     const int32_t rp = window_row_starts(row_ptr, N, w, lane, &beg, &n);
-    if (lane == 0) is_big[w] = n > kWaveCap;
+    if (lane == 0) {
+        is_big[w] = n > kWaveCap && n <= kSortCap;
+        is_heavy[w] = n > kSortCap;
+    }
     if (n > kWaveCap) return;
     if (n <= 64)
         window_wave<1>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols,
@@ -267,12 +272,16 @@ __global__ __launch_bounds__(64) void k_window_wave16(
                     u, bits_out, err);
 }
 
-// big[pos[w]] = w for the flagged windows (pos: exclusive scan of is_big).
-__global__ void k_compact_big(const int32_t *is_big, const int32_t *pos, int32_t T,
-                              int32_t *big)
+// big[big_pos[w]] = w and heavy[heavy_pos[w]] = w for the flagged windows
+// (positions: exclusive scans of the flags), in window order.
+__global__ void k_compact_lists(const int32_t *is_big, const int32_t *big_pos,
+                                const int32_t *is_heavy, const int32_t *heavy_pos,
+                                int32_t T, int32_t *big, int32_t *heavy)
 {
     const int w = blockIdx.x * blockDim.x + threadIdx.x;
-    if (w < T && is_big[w] && pos[w] < T) big[pos[w]] = w;
+    if (w >= T) return;
+    if (is_big[w] && big_pos[w] < T) big[big_pos[w]] = w;
+    if (is_heavy[w] && heavy_pos[w] < T) heavy[heavy_pos[w]] = w;
 }
 
 __global__ void k_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
@@ -287,10 +296,10 @@ __global__ void k_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
     if (bad) atomicOr(err, 1);
 }
 
-// Windows of the list `big` with more than kWaveCap16 entries, one
-// workgroup each: LDS bitonic sort and compaction into tmp_cols and u, then
-// the block bitmaps assembled in LDS and stored to the staging area, their
-// set bits to bits[w].  Windows above the LDS capacity are queued as heavy.
+// Windows of the list `big` with more than kWaveCap16 entries (at most
+// kSortCap), one workgroup each: LDS bitonic sort and compaction into
+// tmp_cols and u, then the block bitmaps assembled in LDS and stored to the
+// staging area, their set bits to bits[w].
 constexpr int kSortThreads = 1024;
 
 // Exclusive scan of one int per thread over a workgroup of kSortThreads.
@@ -314,8 +323,7 @@ __device__ int block_excl_scan_sort(int v, int *lds, int *total)
 
 __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *big,
-    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *heavy,
-    int32_t *n_heavy, int32_t *err)
+    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
 {
     constexpr int kChunk = kSortCap / kSortThreads;  // sorted keys per thread
     __shared__ int32_t keys[kSortCap];
@@ -328,14 +336,7 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     const int nr = min(r0 + kWindowRows, N) - r0;
     const int beg = row_ptr[r0];
     const int n = row_ptr[r0 + nr] - beg;
-    if (n <= kWaveCap16) return;  // sorted by k_window_wave16
-    if (n > kSortCap) {
-        if (tid == 0) {
-            heavy[atomicAdd(n_heavy, 1)] = w;
-            u[w] = 0;
-        }
-        return;
-    }
+    if (n <= kWaveCap16 || n > kSortCap) return;  // k_window_wave16 / heavy paths
     if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
     int p2 = 1;
     while (p2 < n) p2 <<= 1;
@@ -424,6 +425,98 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     if (tid == 0) {
         u[w] = total;
         bits_out[w] = nbits;
+    }
+}
+
+// Heavy windows (more than kSortCap entries) when N <= kLdsBitmapCols: one
+// workgroup each.  The window's columns are marked in an N-bit bitmap in LDS,
+// a prefix popcount over its words ranks them (the distinct columns in
+// order, written to tmp_cols), and every entry's compacted column is its
+// rank, so the block bitmaps need no search; they are built in LDS when they
+// fit (kHeavyMaskWords), else with atomics on the staging area.
+constexpr int kHeavyThreads = 1024;
+constexpr int kLdsBitmapCols = 1 << 17;   // 16 KB bitmap + 16 KB ranks
+constexpr int kHeavyMaskWords = 4096;     // block bitmaps held in LDS (512 blocks)
+
+__global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *heavy,
+    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
+{
+    extern __shared__ uint32_t lds[];  // [words] bitmap, [words] ranks, [kHeavyMaskWords]
+    __shared__ int32_t s_rp[kWindowRows + 1];
+    __shared__ int scan[kHeavyThreads / 64];
+    const int tid = threadIdx.x;
+    const int words = (N + 31) / 32;
+    uint32_t *bm = lds;
+    int32_t *rank = (int32_t *)(lds + words);
+    uint32_t *sm = lds + 2 * words;
+    const int w = heavy[blockIdx.x];
+    const int r0 = w * kWindowRows;
+    const int nr = min(r0 + kWindowRows, N) - r0;
+    if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
+    for (int k = tid; k < words; k += kHeavyThreads) bm[k] = 0;
+    __syncthreads();
+    const int beg = s_rp[0], n = s_rp[nr] - beg;
+    for (int e = tid; e < n; e += kHeavyThreads) {
+        const int c = col_idx[beg + e];
+        if (c < 0 || c >= N) {
+            atomicOr(err, 1);
+            continue;
+        }
+        atomicOr(&bm[c >> 5], 1u << (c & 31));
+    }
+    __syncthreads();
+    // ranks: each thread a contiguous run of words, then a workgroup scan
+    const int ch = (words + kHeavyThreads - 1) / kHeavyThreads;
+    const int lo = min(tid * ch, words), hi = min(lo + ch, words);
+    int cnt = 0;
+    for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
+    int total;
+    int off = block_excl_scan_sort(cnt, scan, &total);
+    for (int k = lo; k < hi; ++k) {
+        rank[k] = off;
+        uint32_t x = bm[k];
+        while (x) {
+            tmp_cols[beg + off++] = 32 * k + __ffs(x) - 1;
+            x &= x - 1;
+        }
+    }
+    const int nbw = (total + kBlockCols - 1) / kBlockCols;
+    const bool in_lds = kMaskWords * nbw <= kHeavyMaskWords;
+    uint32_t *gm = tmp_mask + mask_stage(beg, w);
+    uint32_t *dst = in_lds ? sm : gm;
+    for (int k = tid; k < kMaskWords * nbw; k += kHeavyThreads) dst[k] = 0;
+    __threadfence_block();  // global staging: only this workgroup's atomics (at the L2)
+    __syncthreads();
+    for (int e = tid; e < n; e += kHeavyThreads) {
+        const int c = col_idx[beg + e];
+        if (c < 0 || c >= N) continue;
+        int row = 0;
+        for (int r = 1; r < nr; ++r) row += beg + e >= s_rp[r];
+        const uint32_t below = bm[c >> 5] & ((1u << (c & 31)) - 1u);
+        const int a = rank[c >> 5] + __popc(below);
+        const int cc = a % kBlockCols;
+        const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
+        atomicOr(&dst[kMaskWords * (a / kBlockCols) + bit / 32], 1u << (bit % 32));
+    }
+    __threadfence_block();
+    __syncthreads();
+    int nb_bits = 0;
+    for (int k = tid; k < kMaskWords * nbw; k += kHeavyThreads) {
+        uint32_t m;
+        if (in_lds) {
+            m = sm[k];
+            gm[k] = m;
+        } else {
+            m = __hip_atomic_load(&gm[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        nb_bits += __popc(m);
+    }
+    int all_bits;
+    (void)block_excl_scan_sort(nb_bits, scan, &all_bits);
+    if (tid == 0) {
+        u[w] = total;
+        bits_out[w] = all_bits;
     }
 }
 
@@ -658,14 +751,12 @@ __global__ __launch_bounds__(kPlanThreads) void k_heavy_masks(
 
 // Padded column lists (sptd, -1 past the window's distinct columns) and the
 // block bitmaps copied from the staging areas to the window's blocks; one
-// wavefront per window, four per workgroup.
+// workgroup per window (a hub window has thousands of blocks).
 __global__ __launch_bounds__(256) void k_fill_windows(
-    const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols, const uint32_t *tmp_mask,
+    const int32_t *row_ptr, const int32_t *tmp_cols, const uint32_t *tmp_mask,
     const int32_t *u, const int32_t *blk_off, int32_t *cols, uint32_t *mask)
 {
-    const int lane = threadIdx.x & 63;
-    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= T) return;
+    const int w = blockIdx.x;
     const int32_t beg = row_ptr[w * kWindowRows];
     const int uw = u[w];
     const int64_t ob = blk_off[w];
@@ -674,8 +765,8 @@ __global__ __launch_bounds__(256) void k_fill_windows(
     const uint32_t *msrc = tmp_mask + mask_stage(beg, w);
     int32_t *dst = cols + kBlockCols * ob;
     uint32_t *mdst = mask + kMaskWords * ob;
-    for (int k = lane; k < kBlockCols * nbw; k += 64) dst[k] = k < uw ? src[k] : -1;
-    for (int k = lane; k < kMaskWords * nbw; k += 64) mdst[k] = msrc[k];
+    for (int k = threadIdx.x; k < kBlockCols * nbw; k += 256) dst[k] = k < uw ? src[k] : -1;
+    for (int k = threadIdx.x; k < kMaskWords * nbw; k += 256) mdst[k] = msrc[k];
 }
 
 // Work-list piece size (even): about n_blocks / slots blocks (slots = 8 per
@@ -736,7 +827,7 @@ __global__ void k_bin_scatter(const int32_t *nb, const int32_t *blk_off,
                               const int32_t *slot_base, const int32_t *split_idx,
                               int32_t T, int32_t piece, int32_t chunk,
                               int32_t nchunks, int32_t *offs, WorkItem *items,
-                              int32_t *merges)
+                              int32_t *merges, int32_t *split_item)
 {
     const int c = blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= nchunks) return;
@@ -748,19 +839,34 @@ __global__ void k_bin_scatter(const int32_t *nb, const int32_t *blk_off,
         if (n <= piece) {
             items[pos] = WorkItem{w, b0, b0 + n, -1};
         } else {
-            const int64_t pairs = (n + 1) / 2;
-            for (int k = 0; k < np; ++k) {
-                const int a = (int)((k * pairs) / np);
-                const int b = (int)(((k + 1) * pairs) / np);
-                items[pos + k] = WorkItem{w, b0 + 2 * a, b0 + min(n, 2 * b),
-                                          slot_base[w] + k};
-            }
             const int s = split_idx[w];
             merges[3 * s + 0] = w;
             merges[3 * s + 1] = slot_base[w];
             merges[3 * s + 2] = np;
+            split_item[s] = pos;  // its pieces: k_split_items
         }
         *cell = pos + np;
+    }
+}
+
+// Work items of the pieces of split window s (one wavefront per split
+// window): piece k of np covers the block pairs [floor(k*pairs/np),
+// floor((k+1)*pairs/np)) of the window, pairs = ceil(nb/2).
+__global__ __launch_bounds__(256) void k_split_items(const int32_t *merges,
+                                                     const int32_t *split_item,
+                                                     const int32_t *blk_off,
+                                                     int32_t n_split, WorkItem *items)
+{
+    const int s = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (s >= n_split) return;
+    const int w = merges[3 * s], slot = merges[3 * s + 1], np = merges[3 * s + 2];
+    const int pos = split_item[s];
+    const int b0 = blk_off[w], n = blk_off[w + 1] - b0;
+    const int64_t pairs = (n + 1) / 2;
+    for (int k = threadIdx.x & 63; k < np; k += 64) {
+        const int a = (int)((k * pairs) / np);
+        const int b = (int)(((k + 1) * pairs) / np);
+        items[pos + k] = WorkItem{w, b0 + 2 * a, b0 + min(n, 2 * b), slot + k};
     }
 }
 
@@ -815,34 +921,50 @@ int64_t mask_stage_words(int64_t nnz, int32_t T) { return (nnz >> 1) + 8ll * T +
 
 hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                               int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
-                              int32_t *u, int32_t *is_big, int32_t *bits, int32_t *err,
-                              hipStream_t s)
+                              int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits,
+                              int32_t *err, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
     k_window_wave<<<T, 64, 0, s>>>(row_ptr, col_idx, N, tmp_cols, tmp_mask, u, is_big,
-                                   bits, err);
+                                   is_heavy, bits, err);
     return hipGetLastError();
 }
 
-hipError_t launch_compact_big(const int32_t *is_big, const int32_t *pos, int32_t T,
-                              int32_t *big, hipStream_t s)
+hipError_t launch_compact_lists(const int32_t *is_big, const int32_t *big_pos,
+                                const int32_t *is_heavy, const int32_t *heavy_pos,
+                                int32_t T, int32_t *big, int32_t *heavy, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_compact_big<<<grid_for(T, 256), 256, 0, s>>>(is_big, pos, T, big);
+    k_compact_lists<<<grid_for(T, 256), 256, 0, s>>>(is_big, big_pos, is_heavy, heavy_pos,
+                                                     T, big, heavy);
     return hipGetLastError();
 }
 
 hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
                               int32_t N, const int32_t *big, int32_t n_big,
                               int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
-                              int32_t *bits, int32_t *heavy, int32_t *n_heavy,
-                              int32_t *err, hipStream_t s)
+                              int32_t *bits, int32_t *err, hipStream_t s)
 {
     if (n_big == 0) return hipSuccess;
     k_window_wave16<<<n_big, 64, 0, s>>>(row_ptr, col_idx, N, big, tmp_cols, tmp_mask, u,
                                          bits, err);
     k_window_sort<<<n_big, kSortThreads, 0, s>>>(row_ptr, col_idx, N, big, tmp_cols,
-                                                 tmp_mask, u, bits, heavy, n_heavy, err);
+                                                 tmp_mask, u, bits, err);
+    return hipGetLastError();
+}
+
+bool heavy_in_lds(int32_t N) { return N <= kLdsBitmapCols; }
+
+hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                            const int32_t *heavy, int32_t n_heavy, int32_t *tmp_cols,
+                            uint32_t *tmp_mask, int32_t *u, int32_t *bits, int32_t *err,
+                            hipStream_t s)
+{
+    if (n_heavy == 0) return hipSuccess;
+    if (!heavy_in_lds(N)) return hipErrorInvalidValue;
+    const size_t lds = (2 * (size_t)((N + 31) / 32) + kHeavyMaskWords) * 4;
+    k_heavy_lds<<<n_heavy, kHeavyThreads, lds, s>>>(row_ptr, col_idx, N, heavy, tmp_cols,
+                                                     tmp_mask, u, bits, err);
     return hipGetLastError();
 }
 
@@ -910,8 +1032,7 @@ hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t 
                                hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_fill_windows<<<grid_for(T, 4), 256, 0, s>>>(row_ptr, T, tmp_cols, tmp_mask, u,
-                                                  blk_off, cols, mask);
+    k_fill_windows<<<T, 256, 0, s>>>(row_ptr, tmp_cols, tmp_mask, u, blk_off, cols, mask);
     return hipGetLastError();
 }
 
@@ -942,12 +1063,18 @@ hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
                               const int32_t *slot_base, const int32_t *split_idx,
                               int32_t T, int32_t piece, int32_t chunk,
                               int32_t nchunks, int32_t *offs, WorkItem *items,
-                              int32_t *merges, hipStream_t s)
+                              int32_t *merges, int32_t *split_item, int32_t n_split,
+                              hipStream_t s)
 {
     if (nchunks == 0) return hipSuccess;
-    k_bin_scatter<<<grid_for(nchunks, 64), 64, 0, s>>>(
-        nb, blk_off, npieces, key, slot_base, split_idx, T, piece, chunk, nchunks,
-        offs, items, merges);
+    k_bin_scatter<<<grid_for(nchunks, 64), 64, 0, s>>>(nb, blk_off, npieces, key,
+                                                       slot_base, split_idx, T, piece,
+                                                       chunk, nchunks, offs, items,
+                                                       merges, split_item);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n_split == 0) return e;
+    k_split_items<<<grid_for(n_split, 4), 256, 0, s>>>(merges, split_item, blk_off, n_split,
+                                                      items);
     return hipGetLastError();
 }
 

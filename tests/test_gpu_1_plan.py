@@ -89,23 +89,24 @@ def _windows_of_sizes(rng, sizes, N, dup_frac=0.3):
     return rp, ci
 
 
-def test_plan_window_size_classes(gpu, oracle):
+@pytest.mark.parametrize("N", [9000, 140000])
+def test_plan_window_size_classes(gpu, oracle, N):
     """Every sorting path of the plan: one wavefront with 1, 2, 4, 8 or 16 keys
     per lane (up to 64, 128, 256, 512, 1024 entries), the workgroup LDS sort
-    (up to 4096) and the column-bitmap path above it, each at its edges."""
+    (up to 4096) and the column-bitmap paths above it (bitmap in LDS up to
+    2^17 columns, in global memory above), each at its edges."""
     rng = np.random.default_rng(11)
     sizes = [0, 1, 17, 64, 65, 100, 128, 129, 256, 257, 400, 512, 513, 1000,
-             1024, 1025, 4096, 4097, 6000, 3, 0, 64]
-    N = 9000
+             1024, 1025, 4096, 4097, 6000, 3, 0, 64, 9000]
     rp, ci = _windows_of_sizes(rng, sizes, N)
     _check_plan_against_oracle(gpu, oracle, rp, ci, N)
 
 
-@pytest.mark.parametrize("size", [100, 600, 2000, 5000])
-def test_plan_rejects_bad_column_in_each_path(gpu, size):
+@pytest.mark.parametrize("size,N", [(100, 9000), (600, 9000), (2000, 9000), (5000, 9000),
+                                    (5000, 140000)])
+def test_plan_rejects_bad_column_in_each_path(gpu, size, N):
     """An out-of-range column is reported whichever path sorts its window."""
     rng = np.random.default_rng(size)
-    N = 9000
     rp, ci = _windows_of_sizes(rng, [50, size, 20], N)
     lo, hi = int(rp[16]), int(rp[32])
     for bad in (N, -1):
