@@ -5,8 +5,8 @@
 //  2. per row window: sorted distinct columns and the window's 256-bit block
 //     bitmaps, staged at offsets fixed by the CSR (one wavefront per window
 //     with a register bitonic sort; larger windows a workgroup LDS sort;
-//     windows too large for LDS an N-bit column bitmap and popcount
-//     compaction)
+//     heavier windows an N-bit column bitmap with popcount ranks, held in
+//     LDS on graphs of up to 2^17 nodes)
 //  3. blocks per window (ceil(u/16)) and their exclusive prefix (tro)
 //  4. padded column lists (sptd) and bitmaps copied to their final blocks
 //  5. work list: windows stably sorted by block count, largest first, with
