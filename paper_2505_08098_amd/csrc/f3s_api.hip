@@ -100,6 +100,32 @@ hipError_t alloc_parts(f3s_plan_s *p, int32_t part_row)
     return hipSuccess;
 }
 
+// The plan's arrays in one allocation, laid out from its counts (T, blocks,
+// items, split windows): blk_off, cols, mask, items, merges.  Returns the
+// allocation's size in *bytes.
+hipError_t alloc_store(f3s_plan_s *p, size_t *bytes)
+{
+    using namespace f3s;
+    const int64_t B = p->n_blocks;
+    Arena a;
+    a.add<int32_t>((int64_t)p->T + 1);
+    a.add<int32_t>((int64_t)kBlockCols * B);
+    a.add<uint32_t>((int64_t)kMaskWords * B);
+    a.add<WorkItem>(p->n_items);
+    a.add<int32_t>(3ll * p->n_split);
+    hipError_t e = a.alloc();
+    if (e != hipSuccess) return e;
+    p->store = a.base;
+    p->device_bytes += (int64_t)a.cap;
+    p->blk_off = a.take<int32_t>((int64_t)p->T + 1);
+    p->cols = a.take<int32_t>((int64_t)kBlockCols * B);
+    p->mask = a.take<uint32_t>((int64_t)kMaskWords * B);
+    p->items = a.take<WorkItem>(p->n_items);
+    p->merges = a.take<int32_t>(3ll * p->n_split);
+    if (bytes) *bytes = a.cap;
+    return hipSuccess;
+}
+
 int env_int(const char *name, int dflt)
 {
     const char *v = getenv(name);
@@ -263,22 +289,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     p->n_items = (int32_t)n_items;
 
     // ---- 4. the plan's arrays: one allocation, plus the partial buffers --
-    {
-        Arena a;
-        a.add<int32_t>((int64_t)T + 1);
-        a.add<int32_t>((int64_t)kBlockCols * B);
-        a.add<uint32_t>((int64_t)kMaskWords * B);
-        a.add<WorkItem>(p->n_items);
-        a.add<int32_t>(3ll * p->n_split);
-        HIP_TRY(a.alloc());
-        p->store = a.base;
-        p->device_bytes += (int64_t)a.cap;
-        p->blk_off = a.take<int32_t>((int64_t)T + 1);
-        p->cols = a.take<int32_t>((int64_t)kBlockCols * B);
-        p->mask = a.take<uint32_t>((int64_t)kMaskWords * B);
-        p->items = a.take<WorkItem>(p->n_items);
-        p->merges = a.take<int32_t>(3ll * p->n_split);
-    }
+    HIP_TRY(alloc_store(p, nullptr));
     HIP_TRY(alloc_parts(p, part_row));
     HIP_TRY(launch_scan(nb, p->blk_off, T, scan_tmp, nullptr, s));  // window block offsets
 
@@ -320,6 +331,36 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb)
     return x < y + nb && y < x + na;
 }
 
+// A copy of plan src (same arrays, new id) whose split-window partials hold
+// part_row floats per row.
+f3s_plan_t clone_plan(const f3s_plan_s *src, int32_t part_row)
+{
+    f3s_plan_s *t = new (std::nothrow) f3s_plan_s(*src);
+    if (!t) {
+        fail(F3S_ERR_OUT_OF_MEMORY);
+        return nullptr;
+    }
+    t->nnz_csr = t->nnz;  // the pattern without duplicate entries, like A^T's CSR
+    t->store = t->part_store = nullptr;
+    t->part_o = t->part_ml = nullptr;
+    t->part_bytes = 0;
+    t->device_bytes = 0;
+    t->id = g_next_plan_id.fetch_add(1);
+    t->transpose_of = 0;
+    size_t bytes = 0;
+    hipError_t e = alloc_store(t, &bytes);
+    if (e == hipSuccess)
+        e = hipMemcpy(t->store, src->store, bytes, hipMemcpyDeviceToDevice);
+    if (e == hipSuccess) e = alloc_parts(t, part_row);
+    if (e != hipSuccess) {
+        free_plan_arrays(t);
+        delete t;
+        fail(from_hip(e));
+        return nullptr;
+    }
+    return t;
+}
+
 // Builds a plan whose split-window partials hold part_row floats per row.
 f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                      int32_t part_row)
@@ -340,15 +381,8 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
     f3s_status_t st = from_hip(hipGetDevice(&p->device));
     if (st == F3S_OK) {
         if (N == 0) {
-            Arena a;
-            a.add<int32_t>(1);
-            st = from_hip(a.alloc());
-            if (st == F3S_OK) {
-                p->store = a.base;
-                p->device_bytes += (int64_t)a.cap;
-                p->blk_off = a.take<int32_t>(1);
-                st = from_hip(hipMemset(p->blk_off, 0, sizeof(int32_t)));
-            }
+            st = from_hip(alloc_store(p, nullptr));
+            if (st == F3S_OK) st = from_hip(hipMemset(p->blk_off, 0, sizeof(int32_t)));
             p->piece = 16;
             p->part_row = part_row;
         } else {
@@ -408,7 +442,27 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
     step(hipGetDevice(&prev_device));
     step(hipSetDevice(src->device));
     f3s_plan_t t = nullptr;
+    bool symmetric = false;
     {
+        // A^T = A when every entry has its mirror: the plan of A^T is a copy
+        ScratchArena flag;
+        flag.add<int32_t>(1);
+        flag.add<int32_t>(src->n_blocks);
+        if (st == F3S_OK) step(flag.alloc());
+        if (st == F3S_OK) {
+            int32_t *asym = flag.take<int32_t>(1);
+            int32_t *win = flag.take<int32_t>(src->n_blocks);
+            int32_t h = 1;
+            step(hipMemsetAsync(asym, 0, sizeof(int32_t), nullptr));
+            step(f3s::launch_check_symmetric(*src, win, asym, nullptr));
+            step(hipMemcpy(&h, asym, sizeof(int32_t), hipMemcpyDeviceToHost));
+            symmetric = st == F3S_OK && h == 0;
+        }
+    }
+    if (symmetric) {
+        t = clone_plan(src, 2 * f3s::kMaxD);
+        if (!t) st = g_last_error;
+    } else if (st == F3S_OK) {
         // CSR of A^T from the plan's bitmaps (radix sort of the entries by
         // column)
         size_t tr_bytes = 0;

@@ -153,6 +153,10 @@ hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
 // CSR of A^T (rp[N+1], ci[nnz]) from a plan's bitmaps; scratch of
 // transpose_scratch_bytes(p) bytes.
 hipError_t transpose_scratch_bytes(const f3s_plan_s &p, size_t *bytes);
+// Sets *asym (zeroed by the caller) unless every entry (r, c) of the plan's
+// pattern has its mirror (c, r); win: scratch of n_blocks ints.
+hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
+                                  hipStream_t s);
 hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scratch_bytes,
                                 int32_t *rp, int32_t *ci, hipStream_t s);
 

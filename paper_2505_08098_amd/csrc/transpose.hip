@@ -1,4 +1,6 @@
-// CSR of the transposed pattern A^T from a plan, on the GPU, without atomics:
+// Plan of the transposed pattern A^T from a plan of A, on the GPU.  A
+// symmetric pattern (checked exactly, entry by entry) has A^T = A, so its
+// plan is a copy.  Otherwise the CSR of A^T is built without atomics:
 // the plan's block bitmaps are decoded into (column, row) pairs, the pairs
 // are radix-sorted by column (hipCUB, stable), and the row pointers of A^T
 // follow from the sorted columns by binary search.  The pattern a plan holds
@@ -88,6 +90,69 @@ __global__ void k_rows_from_sorted(const uint32_t *keys, int32_t n, int32_t N, i
     rp[c] = lo;
 }
 
+// Position of column c among the distinct columns of window v (cols padded
+// with -1 after the last one), or -1.
+__device__ int find_col(const int32_t *blk_off, const int32_t *cols, int v, int c)
+{
+    const int32_t *list = cols + (int64_t)kBlockCols * blk_off[v];
+    int lo = 0, hi = kBlockCols * (blk_off[v + 1] - blk_off[v]);
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        const int x = list[mid];
+        if (x >= 0 && x < c) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo < kBlockCols * (blk_off[v + 1] - blk_off[v]) && list[lo] == c ? lo : -1;
+}
+
+// win[b] = the window of block b; one wavefront per window.
+__global__ __launch_bounds__(256) void k_block_window(const int32_t *blk_off, int32_t T,
+                                                      int32_t *win)
+{
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= T) return;
+    for (int b = blk_off[w] + (threadIdx.x & 63); b < blk_off[w + 1]; b += 64) win[b] = w;
+}
+
+// Sets *asym when some entry (r, c) of the plan's pattern has no entry (c, r):
+// for every set bit, the row r is looked up among the distinct columns of row
+// c's window and the bit of (c, r) tested.  One thread per bitmap word over
+// all blocks (a hub window's entries spread over many waves); stops early
+// once an asymmetry is known.
+__global__ __launch_bounds__(256) void k_check_symmetric(const int32_t *blk_off,
+                                                         const int32_t *cols,
+                                                         const uint32_t *mask,
+                                                         const int32_t *win, int64_t words,
+                                                         int32_t *asym)
+{
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= words || *(volatile int32_t *)asym) return;
+    uint32_t m = mask[k];
+    if (!m) return;
+    const int64_t blk = k / kMaskWords;
+    const int word = (int)(k % kMaskWords);
+    const int w = win[blk];
+    while (m) {
+        const int bit = 32 * word + __ffs(m) - 1;
+        m &= m - 1;
+        const int r = w * kWindowRows + ((bit >> 2) & 15);
+        const int c = cols[kBlockCols * blk + 4 * (bit >> 6) + (bit & 3)];
+        const int v = c / kWindowRows;
+        const int a = find_col(blk_off, cols, v, r);
+        bool bad = a < 0;
+        if (!bad) {
+            const int cc = a % kBlockCols;
+            const int b2 = 4 * (c % kWindowRows + 16 * (cc / 4)) + (cc % 4);
+            const int64_t blk2 = blk_off[v] + a / kBlockCols;
+            bad = ((mask[kMaskWords * blk2 + b2 / 32] >> (b2 % 32)) & 1u) == 0;
+        }
+        if (bad) {
+            atomicOr(asym, 1);
+            return;
+        }
+    }
+}
+
 int key_bits(int32_t N)
 {
     int b = 1;
@@ -96,6 +161,20 @@ int key_bits(int32_t N)
 }
 
 }  // namespace
+
+hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
+                                  hipStream_t s)
+{
+    if (p.T == 0 || p.n_blocks == 0) return hipSuccess;
+    k_block_window<<<(p.T + 3) / 4, 256, 0, s>>>(p.blk_off, p.T, win);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t words = (int64_t)kMaskWords * p.n_blocks;
+    k_check_symmetric<<<(unsigned)((words + 255) / 256), 256, 0, s>>>(p.blk_off, p.cols,
+                                                                      p.mask, win, words,
+                                                                      asym);
+    return hipGetLastError();
+}
 
 // Scratch of launch_transpose_csr: keys in and out, rows in, per-window
 // counts and offsets, the scan's workspace and the radix sort's storage.

@@ -117,6 +117,35 @@ def test_transposed_plan_of_asymmetric_patterns(gpu, oracle, seed):
         assert np.array_equal(got[key], b[key]), key
 
 
+@pytest.mark.parametrize("extra", [False, True])
+def test_transposed_plan_of_symmetric_and_nearly_symmetric_patterns(gpu, oracle, extra):
+    """A symmetric pattern is its own transpose (the plan is copied); one
+    directed entry more must be caught by the symmetry check."""
+    rng = np.random.default_rng(77)
+    N = 500
+    rp, ci = W.random_csr(rng, N, max_deg=40, empty_frac=0.1, dup_frac=0.2)
+    rows = np.repeat(np.arange(N), np.diff(rp))
+    a = set(zip(rows.tolist(), ci.tolist()))
+    a |= {(c, r) for r, c in a}
+    if extra:
+        r0 = 123
+        c0 = next(c for c in range(N - 1, -1, -1) if (r0, c) not in a)
+        a.add((r0, c0))          # (c0, r0) stays absent
+    pairs = sorted(a)
+    rp_s = np.zeros(N + 1, dtype=np.int32)
+    np.add.at(rp_s, np.array([p[0] for p in pairs]) + 1, 1)
+    rp_s = np.cumsum(rp_s).astype(np.int32)
+    ci_s = np.array([p[1] for p in pairs], dtype=np.int32)
+    plan = gpu.Plan(_dev(rp_s), _dev(ci_s), N)
+    got = plan.transpose().export()
+    rp2, ci2 = _transpose_csr(rp_s, ci_s, N)
+    b = oracle.bsb(rp2, ci2, N)
+    for key in ("blk_off", "cols", "mask"):
+        assert np.array_equal(got[key], b[key]), key
+    same = all(np.array_equal(got[k], plan.export()[k]) for k in ("cols", "mask"))
+    assert same == (not extra)
+
+
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
 @pytest.mark.parametrize("N", [1, 17, 300])
 def test_gradients_random_patterns(gpu, oracle, d, N):
