@@ -236,30 +236,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     if (hs.err) return F3S_ERR_INVALID_CSR;
     HIP_TRY(launch_window_sort(row_ptr, col_idx, N, big, hs.n_big, tmp_cols, tmp_mask, u,
                                bits, &st->err, s));
-    if (hs.n_heavy > 0 && heavy_in_lds(N)) {
-        HIP_TRY(launch_heavy_lds(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, tmp_mask,
-                                 u, bits, &st->err, s));
-    } else if (hs.n_heavy > 0) {
-        const int32_t words = (N + 31) / 32;
-        const int64_t budget = 256ll << 20;  // bitmap workspace per batch
-        int64_t per = (int64_t)words * 4;
-        int32_t batch = (int32_t)(budget / per);
-        if (batch < 1) batch = 1;
-        if (batch > hs.n_heavy) batch = hs.n_heavy;
-        ScratchArena bm;
-        bm.add<uint32_t>((int64_t)batch * words);
-        HIP_TRY(bm.alloc());
-        uint32_t *bitmap = bm.take<uint32_t>((int64_t)batch * words);
-        for (int32_t first = 0; first < hs.n_heavy; first += batch) {
-            const int32_t cnt = hs.n_heavy - first < batch ? hs.n_heavy - first : batch;
-            HIP_TRY(hipMemsetAsync(bitmap, 0, (size_t)cnt * words * 4, s));
-            HIP_TRY(launch_heavy_compact(row_ptr, col_idx, N, heavy + first, cnt, bitmap,
-                                         words, tmp_cols, u, &st->err, s));
-        }
-        HIP_TRY(hipStreamSynchronize(s));  // the bitmap workspace is freed here
-        HIP_TRY(launch_heavy_masks(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, u,
-                                   tmp_mask, bits, s));
-    }
+    HIP_TRY(launch_heavy_lds(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, tmp_mask, u,
+                             bits, &st->err, s));
 
     // ---- 3. blocks per window and statistics; work-list shape: piece size,
     //         split windows, item count (one host round trip for all) -------

@@ -91,27 +91,12 @@ hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
                               int32_t N, const int32_t *big, int32_t n_big,
                               int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
                               int32_t *bits, int32_t *err, hipStream_t s);
-// Heavy windows when N is small enough for an N-bit LDS bitmap (heavy_in_lds):
-// columns, u, bitmaps and bits as above, one workgroup per window.
-bool heavy_in_lds(int32_t N);
+// Heavy windows (more than 4096 entries): columns, u, bitmaps and bits as
+// above, one workgroup per window (column bitmap in LDS, walked in chunks).
 hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                             const int32_t *heavy, int32_t n_heavy, int32_t *tmp_cols,
                             uint32_t *tmp_mask, int32_t *u, int32_t *bits, int32_t *err,
                             hipStream_t s);
-// Otherwise: launch_heavy_compact in batches, then launch_heavy_masks.
-// Block bitmaps and bits of the windows list[0 .. count) once their columns
-// are known.
-hipError_t launch_heavy_masks(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                            const int32_t *list, int32_t count, const int32_t *tmp_cols,
-                            const int32_t *u, uint32_t *tmp_mask, int32_t *bits,
-                            hipStream_t s);
-// Heavy windows heavy[first .. first+count): column bitmap of N bits each in
-// `bitmap` (zeroed by the caller), then popcount compaction.
-hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
-                                int32_t N, const int32_t *heavy, int32_t count,
-                                uint32_t *bitmap, int32_t words,
-                                int32_t *tmp_cols, int32_t *u, int32_t *err,
-                                hipStream_t s);
 // nb[w] = ceil(u[w] / 16) and the sums of u, bits and nb and the largest nb
 // (added / max-ed into the four outputs, zeroed by the caller).
 hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,

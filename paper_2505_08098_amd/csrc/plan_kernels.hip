@@ -5,8 +5,8 @@
 //  2. per row window: sorted distinct columns and the window's 256-bit block
 //     bitmaps, staged at offsets fixed by the CSR (one wavefront per window
 //     with a register bitonic sort; larger windows a workgroup LDS sort;
-//     heavier windows an N-bit column bitmap with popcount ranks, held in
-//     LDS on graphs of up to 2^17 nodes)
+//     heavier windows a column bitmap in LDS with popcount ranks, walked in
+//     chunks of 2^17 columns)
 //  3. blocks per window (ceil(u/16)) and their exclusive prefix (tro)
 //  4. padded column lists (sptd) and bitmaps copied to their final blocks
 //  5. work list: windows stably sorted by block count, largest first, with
@@ -23,26 +23,6 @@ namespace f3s {
 namespace {
 
 constexpr int kSortCap = 4096;     // entries a window may have for LDS sort
-constexpr int kPlanThreads = 256;
-
-// Exclusive scan of one int per thread over a 256-thread block.
-__device__ int block_exclusive_scan256(int v, int *lds, int *total)
-{
-    const int tid = threadIdx.x;
-    lds[tid] = v;
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {
-        int t = tid >= off ? lds[tid - off] : 0;
-        __syncthreads();
-        lds[tid] += t;
-        __syncthreads();
-    }
-    const int incl = lds[tid];
-    *total = lds[kPlanThreads - 1];
-    __syncthreads();
-    return incl - v;
-}
-
 // Staging offset (in 32-bit words) of window w's bitmaps, whose CSR entries
 // start at beg.  A window with n entries has at most ceil(n/16) blocks, 8n/16
 // + 8 words at most, and the next window's offset lies at least n/2 + 8
@@ -428,58 +408,65 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     }
 }
 
-// Heavy windows (more than kSortCap entries) when N <= kLdsBitmapCols: one
-// workgroup each.  The window's columns are marked in an N-bit bitmap in LDS,
-// a prefix popcount over its words ranks them (the distinct columns in
-// order, written to tmp_cols), and every entry's compacted column is its
-// rank, so the block bitmaps need no search; they are built in LDS when they
-// fit (kHeavyMaskWords), else with atomics on the staging area.
+// Heavy windows (more than kSortCap entries), one workgroup each.  The column
+// range is walked in chunks of kChunkCols: a chunk's columns are marked in a
+// bitmap in LDS and a prefix popcount over its words ranks them, so every
+// entry's compacted column is (distinct columns of earlier chunks) + rank +
+// popcount of the lower bits of its word; no search.  A first walk counts the
+// distinct columns (for the size of the block bitmaps), the second writes
+// them in order to tmp_cols and sets the entries' bits, in LDS when the
+// bitmaps fit (kHeavyMaskWords), else with atomics on the staging area.  On
+// graphs of up to kChunkCols nodes the first walk's bitmap is reused.
 constexpr int kHeavyThreads = 1024;
-constexpr int kLdsBitmapCols = 1 << 17;   // 16 KB bitmap + 16 KB ranks
+constexpr int kChunkCols = 1 << 17;       // 16 KB bitmap + 16 KB ranks
 constexpr int kHeavyMaskWords = 4096;     // block bitmaps held in LDS (512 blocks)
 
 __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *heavy,
     int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
 {
-    extern __shared__ uint32_t lds[];  // [words] bitmap, [words] ranks, [kHeavyMaskWords]
+    extern __shared__ uint32_t lds[];  // [cw] bitmap, [cw] ranks, [kHeavyMaskWords]
     __shared__ int32_t s_rp[kWindowRows + 1];
     __shared__ int scan[kHeavyThreads / 64];
     const int tid = threadIdx.x;
-    const int words = (N + 31) / 32;
+    const int cw = (min(N, kChunkCols) + 31) / 32;  // bitmap words of one chunk
     uint32_t *bm = lds;
-    int32_t *rank = (int32_t *)(lds + words);
-    uint32_t *sm = lds + 2 * words;
+    int32_t *rank = (int32_t *)(lds + cw);
+    uint32_t *sm = lds + 2 * cw;
     const int w = heavy[blockIdx.x];
     const int r0 = w * kWindowRows;
     const int nr = min(r0 + kWindowRows, N) - r0;
     if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
-    for (int k = tid; k < words; k += kHeavyThreads) bm[k] = 0;
     __syncthreads();
     const int beg = s_rp[0], n = s_rp[nr] - beg;
-    for (int e = tid; e < n; e += kHeavyThreads) {
-        const int c = col_idx[beg + e];
-        if (c < 0 || c >= N) {
-            atomicOr(err, 1);
-            continue;
+    const int nchunk = (N + kChunkCols - 1) / kChunkCols;
+    // marks the columns of chunk q in bm (zeroed first)
+    auto mark = [&](int q, bool report) {
+        for (int k = tid; k < cw; k += kHeavyThreads) bm[k] = 0;
+        __syncthreads();
+        const int c0 = q * kChunkCols;
+        for (int e = tid; e < n; e += kHeavyThreads) {
+            const int c = col_idx[beg + e];
+            if (c < 0 || c >= N) {
+                if (report) atomicOr(err, 1);
+                continue;
+            }
+            if (c >= c0 && c - c0 < kChunkCols)
+                atomicOr(&bm[(c - c0) >> 5], 1u << (c & 31));
         }
-        atomicOr(&bm[c >> 5], 1u << (c & 31));
-    }
-    __syncthreads();
-    // ranks: each thread a contiguous run of words, then a workgroup scan
-    const int ch = (words + kHeavyThreads - 1) / kHeavyThreads;
-    const int lo = min(tid * ch, words), hi = min(lo + ch, words);
-    int cnt = 0;
-    for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
-    int total;
-    int off = block_excl_scan_sort(cnt, scan, &total);
-    for (int k = lo; k < hi; ++k) {
-        rank[k] = off;
-        uint32_t x = bm[k];
-        while (x) {
-            tmp_cols[beg + off++] = 32 * k + __ffs(x) - 1;
-            x &= x - 1;
-        }
+        __syncthreads();
+    };
+    const int ch = (cw + kHeavyThreads - 1) / kHeavyThreads;
+    const int lo = min(tid * ch, cw), hi = min(lo + ch, cw);
+    // walk 1: distinct columns
+    int total = 0;
+    for (int q = 0; q < nchunk; ++q) {
+        mark(q, q == 0);
+        int cnt = 0;
+        for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
+        int t;
+        (void)block_excl_scan_sort(cnt, scan, &t);
+        total += t;
     }
     const int nbw = (total + kBlockCols - 1) / kBlockCols;
     const bool in_lds = kMaskWords * nbw <= kHeavyMaskWords;
@@ -488,16 +475,38 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     for (int k = tid; k < kMaskWords * nbw; k += kHeavyThreads) dst[k] = 0;
     __threadfence_block();  // global staging: only this workgroup's atomics (at the L2)
     __syncthreads();
-    for (int e = tid; e < n; e += kHeavyThreads) {
-        const int c = col_idx[beg + e];
-        if (c < 0 || c >= N) continue;
-        int row = 0;
-        for (int r = 1; r < nr; ++r) row += beg + e >= s_rp[r];
-        const uint32_t below = bm[c >> 5] & ((1u << (c & 31)) - 1u);
-        const int a = rank[c >> 5] + __popc(below);
-        const int cc = a % kBlockCols;
-        const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
-        atomicOr(&dst[kMaskWords * (a / kBlockCols) + bit / 32], 1u << (bit % 32));
+    // walk 2: ranks, distinct columns in order, the entries' bits
+    int base = 0;
+    for (int q = 0; q < nchunk; ++q) {
+        if (nchunk > 1) mark(q, false);
+        const int c0 = q * kChunkCols;
+        int cnt = 0;
+        for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
+        int t;
+        int off = base + block_excl_scan_sort(cnt, scan, &t);
+        for (int k = lo; k < hi; ++k) {
+            rank[k] = off;
+            uint32_t x = bm[k];
+            while (x) {
+                tmp_cols[beg + off++] = c0 + 32 * k + __ffs(x) - 1;
+                x &= x - 1;
+            }
+        }
+        __syncthreads();
+        for (int e = tid; e < n; e += kHeavyThreads) {
+            const int c = col_idx[beg + e];
+            if (c < c0 || c >= N || c - c0 >= kChunkCols) continue;
+            int row = 0;
+            for (int r = 1; r < nr; ++r) row += beg + e >= s_rp[r];
+            const int cl = c - c0;
+            const uint32_t below = bm[cl >> 5] & ((1u << (cl & 31)) - 1u);
+            const int a = rank[cl >> 5] + __popc(below);
+            const int cc = a % kBlockCols;
+            const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
+            atomicOr(&dst[kMaskWords * (a / kBlockCols) + bit / 32], 1u << (bit % 32));
+        }
+        base += t;
+        __syncthreads();
     }
     __threadfence_block();
     __syncthreads();
@@ -520,50 +529,6 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     }
 }
 
-__global__ __launch_bounds__(kPlanThreads) void k_heavy_compact(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-    const int32_t *heavy, uint32_t *bitmap, int32_t words, int32_t *tmp_cols,
-    int32_t *u, int32_t *err)
-{
-    __shared__ int scan[kPlanThreads];
-    const int tid = threadIdx.x;
-    const int w = heavy[blockIdx.x];
-    uint32_t *bm = bitmap + (int64_t)blockIdx.x * words;
-    const int r0 = w * kWindowRows;
-    const int r1 = min(r0 + kWindowRows, N);
-    const int beg = row_ptr[r0], end = row_ptr[r1];
-    for (int e = beg + tid; e < end; e += kPlanThreads) {
-        const int c = col_idx[e];
-        if (c < 0 || c >= N) {
-            atomicOr(err, 1);
-            continue;
-        }
-        atomicOr(&bm[c >> 5], 1u << (c & 31));
-    }
-    // the atomics and the loads below are issued by this workgroup alone and
-    // performed at the L2: workgroup-scope ordering is enough (a device-scope
-    // fence would write back the whole L2 for every block)
-    __threadfence_block();
-    __syncthreads();
-    const int ch = (words + kPlanThreads - 1) / kPlanThreads;
-    const int lo = min(tid * ch, words), hi = min(lo + ch, words);
-    int cnt = 0;
-    for (int k = lo; k < hi; ++k)
-        cnt += __popc(__hip_atomic_load(&bm[k], __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT));
-    int total;
-    int off = block_exclusive_scan256(cnt, scan, &total);
-    for (int k = lo; k < hi; ++k) {
-        uint32_t x = __hip_atomic_load(&bm[k], __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        while (x) {
-            const int b = __ffs(x) - 1;
-            tmp_cols[beg + off++] = 32 * k + b;
-            x &= x - 1;
-        }
-    }
-    if (tid == 0) u[w] = total;
-}
 
 // Per window: blocks nb = ceil(u/16); over all windows: sum of u (distinct
 // columns), sum of bits (distinct entries), sum of nb (blocks) and the
@@ -691,63 +656,6 @@ __global__ __launch_bounds__(256) void k_scan_add(int32_t *out, int32_t n,
     }
 }
 
-// Bitmaps of the heavy windows, one workgroup each, built with atomics in the
-// window's staging region: each
-// entry finds its row among the row starts and its compacted column by
-// binary search in the window's distinct columns.  The set bits go to
-// bits[w].
-__global__ __launch_bounds__(kPlanThreads) void k_heavy_masks(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *list,
-    const int32_t *tmp_cols, const int32_t *u, uint32_t *tmp_mask, int32_t *bits_out)
-{
-    __shared__ int32_t s_rp[kWindowRows + 1];
-    __shared__ int32_t s_cnt;
-    const int tid = threadIdx.x;
-    const int w = list[blockIdx.x];
-    const int r0 = w * kWindowRows;
-    const int nr = min(r0 + kWindowRows, N) - r0;
-    if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
-    if (tid == 0) s_cnt = 0;
-    const int32_t beg0 = row_ptr[r0];
-    const int32_t *uc = tmp_cols + beg0;
-    const int uw = u[w];
-    const int nbw = (uw + kBlockCols - 1) / kBlockCols;
-    uint32_t *gm = tmp_mask + mask_stage(beg0, w);
-    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads) gm[k] = 0;
-    // the stores, atomics and loads on gm are all this workgroup's and are
-    // performed at the L2: workgroup-scope ordering is enough
-    __threadfence_block();
-    __syncthreads();
-    const int beg = s_rp[0], n = s_rp[nr] - beg;
-    for (int e = tid; e < n; e += kPlanThreads) {
-        int rlo = 0, rhi = nr;  // row of entry e: the last row start <= beg + e
-        while (rhi - rlo > 1) {
-            const int mid = (rlo + rhi) >> 1;
-            if (s_rp[mid] <= beg + e) rlo = mid;
-            else rhi = mid;
-        }
-        const int c = col_idx[beg + e];
-        if (c < 0 || c >= N) continue;  // reported by the sort
-        int lo = 0, hi = uw;
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (uc[mid] < c) lo = mid + 1;
-            else hi = mid;
-        }
-        if (lo >= uw) continue;  // every valid column is in the list
-        const int cc = lo % kBlockCols;
-        const int bit = 4 * (rlo + 16 * (cc / 4)) + (cc % 4);
-        atomicOr(&gm[kMaskWords * (lo / kBlockCols) + bit / 32], 1u << (bit % 32));
-    }
-    __threadfence_block();
-    __syncthreads();
-    int cnt = 0;
-    for (int k = tid; k < kMaskWords * nbw; k += kPlanThreads)
-        cnt += __popc(__hip_atomic_load(&gm[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    if (cnt) atomicAdd(&s_cnt, cnt);  // LDS
-    __syncthreads();
-    if (tid == 0) bits_out[w] = s_cnt;
-}
 
 // Padded column lists (sptd, -1 past the window's distinct columns) and the
 // block bitmaps copied from the staging areas to the window's blocks; one
@@ -953,41 +861,15 @@ hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
     return hipGetLastError();
 }
 
-bool heavy_in_lds(int32_t N) { return N <= kLdsBitmapCols; }
-
 hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                             const int32_t *heavy, int32_t n_heavy, int32_t *tmp_cols,
                             uint32_t *tmp_mask, int32_t *u, int32_t *bits, int32_t *err,
                             hipStream_t s)
 {
     if (n_heavy == 0) return hipSuccess;
-    if (!heavy_in_lds(N)) return hipErrorInvalidValue;
-    const size_t lds = (2 * (size_t)((N + 31) / 32) + kHeavyMaskWords) * 4;
+    const size_t lds = (2 * (size_t)((min(N, kChunkCols) + 31) / 32) + kHeavyMaskWords) * 4;
     k_heavy_lds<<<n_heavy, kHeavyThreads, lds, s>>>(row_ptr, col_idx, N, heavy, tmp_cols,
                                                      tmp_mask, u, bits, err);
-    return hipGetLastError();
-}
-
-hipError_t launch_heavy_masks(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                            const int32_t *list, int32_t count, const int32_t *tmp_cols,
-                            const int32_t *u, uint32_t *tmp_mask, int32_t *bits,
-                            hipStream_t s)
-{
-    if (count == 0) return hipSuccess;
-    k_heavy_masks<<<count, kPlanThreads, 0, s>>>(row_ptr, col_idx, N, list, tmp_cols, u,
-                                               tmp_mask, bits);
-    return hipGetLastError();
-}
-
-hipError_t launch_heavy_compact(const int32_t *row_ptr, const int32_t *col_idx,
-                                int32_t N, const int32_t *heavy, int32_t count,
-                                uint32_t *bitmap, int32_t words,
-                                int32_t *tmp_cols, int32_t *u, int32_t *err,
-                                hipStream_t s)
-{
-    if (count == 0) return hipSuccess;
-    k_heavy_compact<<<count, kPlanThreads, 0, s>>>(row_ptr, col_idx, N, heavy,
-                                                   bitmap, words, tmp_cols, u, err);
     return hipGetLastError();
 }
 

@@ -93,8 +93,8 @@ def _windows_of_sizes(rng, sizes, N, dup_frac=0.3):
 def test_plan_window_size_classes(gpu, oracle, N):
     """Every sorting path of the plan: one wavefront with 1, 2, 4, 8 or 16 keys
     per lane (up to 64, 128, 256, 512, 1024 entries), the workgroup LDS sort
-    (up to 4096) and the column-bitmap paths above it (bitmap in LDS up to
-    2^17 columns, in global memory above), each at its edges."""
+    (up to 4096) and the column-bitmap path above it (one chunk of 2^17
+    columns, or several), each at its edges."""
     rng = np.random.default_rng(11)
     sizes = [0, 1, 17, 64, 65, 100, 128, 129, 256, 257, 400, 512, 513, 1000,
              1024, 1025, 4096, 4097, 6000, 3, 0, 64, 9000]
