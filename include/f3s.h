@@ -88,6 +88,25 @@ typedef struct {
 f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N);
 
 /*
+ * Device bytes of scratch a build of f3s_plan_ws needs for a pattern of N
+ * rows and nnz CSR entries on the current device (0 for negative sizes).
+ */
+size_t f3s_plan_workspace_bytes(int32_t N, int64_t nnz);
+
+/*
+ * f3s_plan with the build's scratch lent by the caller instead of allocated
+ * and freed by the library (a caching allocator can then serve repeated
+ * builds): workspace is device memory of at least
+ * f3s_plan_workspace_bytes(N, row_ptr[N]) bytes, 256-byte aligned.  The
+ * plan keeps no reference to it; the build is synchronous, so the caller
+ * may reuse or free it on return.  The plan's own arrays are still
+ * allocated by the library.  A workspace that is null, misaligned or too
+ * small gives F3S_ERR_INVALID_VALUE.  Otherwise as f3s_plan.
+ */
+f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                       void *workspace, size_t workspace_bytes);
+
+/*
  * O = softmax_rows(mask_A(scale * Q K^T)) V  (Algorithm 1, Section 3).
  *   Q, K, V  device, fp16, N x d row-major, contiguous, 16-byte aligned; they
  *            may alias each other (Q = K = V as in AGNN, Section 2.1)

@@ -76,6 +76,10 @@ def load_library():
     vp, i32 = ctypes.c_void_p, ctypes.c_int32
     L.f3s_plan.argtypes = [vp, vp, i32]
     L.f3s_plan.restype = vp
+    L.f3s_plan_workspace_bytes.argtypes = [i32, ctypes.c_int64]
+    L.f3s_plan_workspace_bytes.restype = ctypes.c_size_t
+    L.f3s_plan_ws.argtypes = [vp, vp, i32, vp, ctypes.c_size_t]
+    L.f3s_plan_ws.restype = vp
     L.f3s_run.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp]
     L.f3s_run.restype = ctypes.c_int
     L.f3s_run_mh.argtypes = [vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp]
@@ -143,10 +147,18 @@ class Plan:
         _check_device_tensor(col_idx, "col_idx", torch.int32)
         if row_ptr.numel() != int(N) + 1:
             raise ValueError("row_ptr must hold N + 1 entries")
+        ci = col_idx.data_ptr() if col_idx.numel() else None
         with torch.cuda.device(row_ptr.device):
             torch.cuda.current_stream().synchronize()
-            h = L.f3s_plan(row_ptr.data_ptr(), col_idx.data_ptr() if col_idx.numel() else None,
-                           int(N))
+            # the build's scratch from torch's caching allocator (the build is
+            # synchronous: the memory is free again when the call returns)
+            nbytes = L.f3s_plan_workspace_bytes(int(N), col_idx.numel())
+            if nbytes:
+                ws = torch.empty(nbytes, dtype=torch.uint8, device=row_ptr.device)
+                h = L.f3s_plan_ws(row_ptr.data_ptr(), ci, int(N), ws.data_ptr(), nbytes)
+                del ws
+            else:
+                h = L.f3s_plan(row_ptr.data_ptr(), ci, int(N))
         if not h:
             raise F3SError(L.f3s_last_error(), "f3s_plan")
         self._h = h

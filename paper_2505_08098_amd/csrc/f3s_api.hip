@@ -49,11 +49,13 @@ struct Arena {
     }
 };
 
-// Scratch arena freed on every exit path of a plan build.
+// Scratch arena freed on every exit path of a plan build (unless the caller
+// lent the memory).
 struct ScratchArena : Arena {
+    bool owned = true;
     ~ScratchArena()
     {
-        if (base) (void)hipFree(base);
+        if (base && owned) (void)hipFree(base);
     }
 };
 
@@ -172,8 +174,60 @@ struct BuildStats {
     int32_t invalid;              // plan integrity check
 };
 
+// Pointers into the plan build's scratch.
+struct BuildScratch {
+    BuildStats *st;
+    int32_t *tmp_cols;   // sorted distinct columns per window, at its CSR offset
+    uint32_t *tmp_mask;  // block bitmaps per window, staged
+    int32_t *u, *big, *is_big, *heavy, *is_heavy, *bits, *nb, *npieces, *key, *split_item;
+    int32_t *big_pos, *heavy_pos, *split_pieces, *split_one, *scan_tmp, *hist_area;
+    int64_t hist_room;
+};
+
+constexpr int32_t kBinChunk = 64;  // windows per histogram chunk of the work-list sort
+
+template <typename U>
+U *carve(Arena &a, bool take, int64_t n)
+{
+    if (take) return a.take<U>(n);
+    a.add<U>(n);
+    return nullptr;
+}
+
+// Lays out the build's scratch for T windows and nnz CSR entries: sizes into
+// a (take == false) or pointers out of it (take == true), in one order.  The
+// work-list histogram gets room for the largest piece size the block count
+// allows (blocks <= nnz / 16 + T); a forced larger piece allocates its own.
+void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz,
+                   int32_t slots)
+{
+    using namespace f3s;
+    const int64_t nchunks = (T + kBinChunk - 1) / kBinChunk;
+    const int64_t piece_bound = (nnz / 16 + T + slots - 1) / slots + 18;
+    b.hist_room = (piece_bound + 1) * nchunks + 1 + scan_tmp_ints((piece_bound + 1) * nchunks);
+    b.st = carve<BuildStats>(a, take, 1);
+    b.tmp_cols = carve<int32_t>(a, take, nnz);
+    b.tmp_mask = carve<uint32_t>(a, take, mask_stage_words(nnz, T));
+    int32_t **per_window[] = {&b.u, &b.big, &b.is_big, &b.heavy, &b.is_heavy,
+                              &b.bits, &b.nb, &b.npieces, &b.key, &b.split_item};
+    for (int32_t **q : per_window) *q = carve<int32_t>(a, take, T);
+    int32_t **per_window1[] = {&b.big_pos, &b.heavy_pos, &b.split_pieces, &b.split_one};
+    for (int32_t **q : per_window1) *q = carve<int32_t>(a, take, (int64_t)T + 1);
+    b.scan_tmp = carve<int32_t>(a, take, scan_tmp_ints(T));
+    b.hist_area = carve<int32_t>(a, take, b.hist_room);
+}
+
+size_t plan_workspace_bytes(int32_t N, int64_t nnz, int device)
+{
+    Arena a;
+    BuildScratch b;
+    const int32_t T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
+    carve_scratch(a, false, b, T, nnz, plan_slots(device));
+    return a.cap;
+}
+
 f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *col_idx,
-                        int32_t part_row)
+                        int32_t part_row, void *workspace, size_t workspace_bytes)
 {
     using namespace f3s;
     const hipStream_t s = nullptr;
@@ -187,41 +241,31 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     if (nnz > 0 && !col_idx) return F3S_ERR_INVALID_VALUE;
     p->nnz_csr = nnz;
 
-    // all scratch of the build in one allocation, with room for the
-    // work-list histogram at the largest piece size the block count allows
-    // (blocks <= nnz / 16 + T); a forced larger piece allocates its own
-    const int64_t stage_words = mask_stage_words(nnz, T);
+    // all scratch of the build in one allocation (or the caller's workspace)
     const int32_t slots = plan_slots(p->device);
-    const int32_t chunk = 64;
-    const int32_t nchunks = (T + chunk - 1) / chunk;
-    const int64_t piece_bound = ((int64_t)nnz / 16 + T + slots - 1) / slots + 18;
-    const int64_t hist_room = (piece_bound + 1) * nchunks + 1 +
-                              scan_tmp_ints((piece_bound + 1) * nchunks);
+    BuildScratch b;
     ScratchArena tmp;
-    tmp.add<BuildStats>(1);
-    tmp.add<int32_t>(nnz);               // sorted distinct columns per window
-    tmp.add<uint32_t>(stage_words);      // block bitmaps per window
-    // u, big, is_big, heavy, is_heavy, bits, nb, npieces, key, split_item
-    for (int k = 0; k < 10; ++k) tmp.add<int32_t>(T);
-    // big_pos, heavy_pos, split pieces, split flags
-    for (int k = 0; k < 4; ++k) tmp.add<int32_t>((int64_t)T + 1);
-    tmp.add<int32_t>(scan_tmp_ints(T));
-    tmp.add<int32_t>(hist_room);
-    HIP_TRY(tmp.alloc());
-    BuildStats *st = tmp.take<BuildStats>(1);
-    int32_t *tmp_cols = tmp.take<int32_t>(nnz);
-    uint32_t *tmp_mask = tmp.take<uint32_t>(stage_words);
-    int32_t *u = tmp.take<int32_t>(T), *big = tmp.take<int32_t>(T);
-    int32_t *is_big = tmp.take<int32_t>(T), *heavy = tmp.take<int32_t>(T);
-    int32_t *is_heavy = tmp.take<int32_t>(T), *bits = tmp.take<int32_t>(T);
-    int32_t *nb = tmp.take<int32_t>(T), *npieces = tmp.take<int32_t>(T);
-    int32_t *key = tmp.take<int32_t>(T), *split_item = tmp.take<int32_t>(T);
-    int32_t *big_pos = tmp.take<int32_t>((int64_t)T + 1);
-    int32_t *heavy_pos = tmp.take<int32_t>((int64_t)T + 1);
-    int32_t *split_pieces = tmp.take<int32_t>((int64_t)T + 1);
-    int32_t *split_one = tmp.take<int32_t>((int64_t)T + 1);
-    int32_t *scan_tmp = tmp.take<int32_t>(scan_tmp_ints(T));
-    int32_t *hist_area = tmp.take<int32_t>(hist_room);
+    carve_scratch(tmp, false, b, T, nnz, slots);
+    if (workspace) {
+        if (workspace_bytes < tmp.cap || ((uintptr_t)workspace & 255u))
+            return F3S_ERR_INVALID_VALUE;
+        tmp.base = static_cast<char *>(workspace);
+        tmp.owned = false;
+    } else {
+        HIP_TRY(tmp.alloc());
+    }
+    carve_scratch(tmp, true, b, T, nnz, slots);
+    BuildStats *st = b.st;
+    int32_t *tmp_cols = b.tmp_cols;
+    uint32_t *tmp_mask = b.tmp_mask;
+    int32_t *u = b.u, *big = b.big, *is_big = b.is_big, *heavy = b.heavy;
+    int32_t *is_heavy = b.is_heavy, *bits = b.bits, *nb = b.nb, *npieces = b.npieces;
+    int32_t *key = b.key, *split_item = b.split_item, *big_pos = b.big_pos;
+    int32_t *heavy_pos = b.heavy_pos, *split_pieces = b.split_pieces;
+    int32_t *split_one = b.split_one, *scan_tmp = b.scan_tmp, *hist_area = b.hist_area;
+    const int64_t hist_room = b.hist_room;
+    const int32_t chunk = kBinChunk;
+    const int32_t nchunks = (T + chunk - 1) / chunk;
     BuildStats hs;
     HIP_TRY(hipMemsetAsync(st, 0, sizeof(BuildStats), s));
 
@@ -341,7 +385,7 @@ f3s_plan_t clone_plan(const f3s_plan_s *src, int32_t part_row)
 
 // Builds a plan whose split-window partials hold part_row floats per row.
 f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                     int32_t part_row)
+                     int32_t part_row, void *workspace, size_t workspace_bytes)
 {
     const auto t0 = std::chrono::steady_clock::now();
     if (N < 0 || (N > 0 && !row_ptr)) {
@@ -364,7 +408,7 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
             p->piece = 16;
             p->part_row = part_row;
         } else {
-            st = build_plan(p, row_ptr, col_idx, part_row);
+            st = build_plan(p, row_ptr, col_idx, part_row, workspace, workspace_bytes);
         }
     }
     if (st != F3S_OK) {
@@ -401,7 +445,24 @@ f3s_status_t f3s_last_error(void) { return g_last_error; }
 
 f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N)
 {
-    return make_plan(row_ptr, col_idx, N, f3s::kMaxD);
+    return make_plan(row_ptr, col_idx, N, f3s::kMaxD, nullptr, 0);
+}
+
+size_t f3s_plan_workspace_bytes(int32_t N, int64_t nnz)
+{
+    int device = 0;
+    if (N < 0 || nnz < 0 || hipGetDevice(&device) != hipSuccess) return 0;
+    return plan_workspace_bytes(N, nnz, device);
+}
+
+f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                       void *workspace, size_t workspace_bytes)
+{
+    if (!workspace) {
+        fail(F3S_ERR_INVALID_VALUE);
+        return nullptr;
+    }
+    return make_plan(row_ptr, col_idx, N, f3s::kMaxD, workspace, workspace_bytes);
 }
 
 f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
@@ -458,7 +519,7 @@ f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
             // the dK/dV pass keeps two partials (dK, dV) per piece row, so a
             // launch group still holds heads with nh * d <= kMaxD
             if (st == F3S_OK) {
-                t = make_plan(rp, ci, N, 2 * f3s::kMaxD);
+                t = make_plan(rp, ci, N, 2 * f3s::kMaxD, nullptr, 0);
                 if (!t) st = g_last_error;
             }
         }

@@ -28,10 +28,18 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("f3s_plan", "f3s_run", "f3s_run_mh", "f3s_forward", "f3s_plan_transpose",
+    for n in ("f3s_plan", "f3s_plan_ws", "f3s_plan_workspace_bytes", "f3s_run",
+              "f3s_run_mh", "f3s_forward", "f3s_plan_transpose",
               "f3s_backward", "f3s_destroy", "f3s_plan_info",
               "f3s_plan_export", "f3s_last_error", "f3s_status_string"):
         assert n in names
+
+
+def test_workspace_bytes_rejects_negative_sizes(lib):
+    lib.f3s_plan_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int64]
+    lib.f3s_plan_workspace_bytes.restype = ctypes.c_size_t
+    assert lib.f3s_plan_workspace_bytes(-1, 10) == 0
+    assert lib.f3s_plan_workspace_bytes(10, -1) == 0
 
 
 def test_every_declared_symbol_is_exported(lib):

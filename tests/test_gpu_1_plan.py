@@ -160,6 +160,37 @@ def test_plan_rejects_malformed_csr(gpu, rp, ci, N):
     assert e.value.code == 2  # F3S_ERR_INVALID_CSR
 
 
+def test_plan_with_and_without_workspace(gpu):
+    """f3s_plan (library-allocated scratch) and f3s_plan_ws (lent scratch, what
+    Plan uses) build the same plan; a short or misaligned workspace is
+    rejected."""
+    import ctypes
+    L = gpu.load_library()
+    c = W.make_config(2, with_features=False)
+    dev = torch.device("cuda:0")
+    rp = torch.from_numpy(c["row_ptr"]).to(dev)
+    ci = torch.from_numpy(c["col_idx"]).to(dev)
+    N = c["N"]
+    a = gpu.Plan(rp, ci, N).export()
+    h = L.f3s_plan(rp.data_ptr(), ci.data_ptr(), N)
+    assert h
+    b = gpu.Plan._from_handle(h, dev, N).export()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    need = L.f3s_plan_workspace_bytes(N, ci.numel())
+    assert need > 4 * ci.numel()
+    ws = torch.empty(need + 512, dtype=torch.uint8, device=dev)
+    for ptr, size in ((ws.data_ptr(), need - 256), (ws.data_ptr() + 4, need),
+                      (None, need)):
+        assert not L.f3s_plan_ws(rp.data_ptr(), ci.data_ptr(), N, ptr, size)
+        assert L.f3s_last_error() == 1  # F3S_ERR_INVALID_VALUE
+    h = L.f3s_plan_ws(rp.data_ptr(), ci.data_ptr(), N, ws.data_ptr(), need)
+    assert h
+    b = gpu.Plan._from_handle(h, dev, N).export()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
 def test_plan_is_deterministic(gpu):
     c = W.make_config(2, with_features=False)
     a = _plan(gpu, c["row_ptr"], c["col_idx"], c["N"]).export()
