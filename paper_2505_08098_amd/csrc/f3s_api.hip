@@ -141,12 +141,6 @@ int env_int(const char *name, int dflt)
         if (e_ != hipSuccess) return from_hip(e_);             \
     } while (0)
 
-template <typename T>
-hipError_t read_scalar(T *host, const T *dev)
-{
-    return hipMemcpy(host, dev, sizeof(T), hipMemcpyDeviceToHost);
-}
-
 // Work-list slots of a device: 8 per compute unit.
 int32_t plan_slots(int device)
 {
