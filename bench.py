@@ -177,9 +177,15 @@ def bench_backward(args, c, plan, Q, K, V, stream, dev):
         warm.append((time.perf_counter() - t0) * 1e3)
     transpose_ms_warm = float(np.median(warm))
     rng = np.random.default_rng(np.random.SeedSequence(args.seed).spawn(4)[3])
-    G = torch.from_numpy(rng.standard_normal(tuple(Q.shape), dtype=np.float32)
-                         .astype(np.float16)).to(dev)
-    O, lse = f3s.forward(plan, Q, K, V, scale=c["scale"], stream=stream)
+    g32 = rng.standard_normal(tuple(Q.shape), dtype=np.float32)
+    if Q.dtype == torch.bfloat16:
+        from paper_2505_08098_amd import workloads as W
+        G = torch.from_numpy(W.to_bf16_bits(g32)).to(dev).view(torch.int16).view(torch.bfloat16)
+        O, lse = f3s.forward_typed(plan, Q, K, V, scale=c["scale"], want_lse=True,
+                                   stream=stream)
+    else:
+        G = torch.from_numpy(g32.astype(np.float16)).to(dev)
+        O, lse = f3s.forward(plan, Q, K, V, scale=c["scale"], stream=stream)
     for _ in range(args.warmup):
         f3s.backward(plan, plan_t, Q, K, V, O, G, lse, scale=c["scale"], stream=stream)
     torch.cuda.synchronize()
@@ -200,10 +206,10 @@ def bench_backward(args, c, plan, Q, K, V, stream, dev):
                   "(10*nnz*d) at 1 MI355X",
         "value": round(flops / (ms * 1e-3) / 1e9, 2), "unit": "GFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
-        "data": "synthetic",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": args.in_dtype, "data": "synthetic",
         "config": {"workload": c["name"], "N": c["N"], "nnz": info["nnz"], "d": d,
-                   "heads": H},
+                   "heads": H, "in_dtype": args.in_dtype},
         "ms_median": round(float(np.median(per)), 5),
         "transpose_plan_ms": round(transpose_ms, 3),
         "transpose_plan_ms_warm": round(transpose_ms_warm, 3),
@@ -247,8 +253,9 @@ def main():
                     help="after timing, run 3 plain device copies of this many MiB "
                          "(reference dispatches for scaling HBM byte counters)")
     args = ap.parse_args()
-    if args.backward and (args.in_dtype != "f16" or args.out_dtype != "f32"):
-        print(json.dumps({"error": "the backward pass takes fp16 inputs and fp32 outputs"}))
+    if args.backward and (args.in_dtype == "fp8" or args.out_dtype != "f32"):
+        print(json.dumps({"error": "the backward pass takes fp16 or bf16 inputs and "
+                                   "fp32 outputs"}))
         sys.exit(2)
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))

@@ -211,6 +211,22 @@ f3s_status_t f3s_backward(f3s_plan_t plan, f3s_plan_t plan_t, const void *Q,
                           float *dV, int32_t n_heads, int32_t d, float scale,
                           hipStream_t stream);
 
+/*
+ * f3s_backward with a choice of input type: in_dtype F3S_DTYPE_F16 (as
+ * f3s_backward) or F3S_DTYPE_BF16, the type of Q, K, V and dO (O, lse and
+ * the outputs stay fp32).  With bf16 inputs the score and dP products use
+ * the bf16 matrix product, and P and dS enter the gradient products as two
+ * bf16 terms each (about 16 significant bits), so the error stays within
+ * the fp16 scheme's bound.  Other types give F3S_ERR_UNSUPPORTED.  Layouts,
+ * alignment, d, heads and stream rules as f3s_backward.  O and lse come
+ * from f3s_forward_typed with the same inputs and an fp32 O.
+ */
+f3s_status_t f3s_backward_typed(f3s_plan_t plan, f3s_plan_t plan_t, const void *Q,
+                                const void *K, const void *V, f3s_dtype_t in_dtype,
+                                const float *O, const void *dO, const float *lse,
+                                float *row_stats, float *dQ, float *dK, float *dV,
+                                int32_t n_heads, int32_t d, float scale, hipStream_t stream);
+
 /* Release a plan and all its device memory.  NULL is a no-op. */
 void f3s_destroy(f3s_plan_t plan);
 

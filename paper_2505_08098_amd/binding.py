@@ -93,6 +93,9 @@ def load_library():
     L.f3s_plan_transpose.restype = vp
     L.f3s_backward.argtypes = [vp, vp] + [vp] * 10 + [i32, i32, ctypes.c_float, vp]
     L.f3s_backward.restype = ctypes.c_int
+    L.f3s_backward_typed.argtypes = ([vp, vp, vp, vp, vp, i32] + [vp] * 7 +
+                                     [i32, i32, ctypes.c_float, vp])
+    L.f3s_backward_typed.restype = ctypes.c_int
     L.f3s_destroy.argtypes = [vp]
     L.f3s_destroy.restype = None
     L.f3s_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
@@ -325,13 +328,16 @@ def forward_typed(plan, Q, K, V, out_dtype=torch.float32, scale=None, out=None,
 
 
 def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
-    """f3s_backward: returns (dQ, dK, dV) fp32 (the per-row (lse, delta)
-    records it needs go to a buffer allocated here)."""
+    """f3s_backward_typed: returns (dQ, dK, dV) fp32 for fp16 or bf16 Q, K, V,
+    dO (the per-row (lse, delta) records it needs go to a buffer allocated
+    here)."""
     shape = tuple(Q.shape)
     H = shape[1] if len(shape) == 3 else 1
     d = shape[-1]
+    if Q.dtype not in (torch.float16, torch.bfloat16):
+        raise TypeError("Q, K, V, dO must be float16 or bfloat16")
     for t, n in ((Q, "Q"), (K, "K"), (V, "V"), (dO, "dO")):
-        _check_device_tensor(t, n, torch.float16)
+        _check_device_tensor(t, n, Q.dtype)
         if tuple(t.shape) != shape:
             raise ValueError(f"{n} must have the shape of Q")
     _check_device_tensor(O, "O", torch.float32)
@@ -344,12 +350,13 @@ def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
         scale = 1.0 / math.sqrt(d)
     if stream is None:
         stream = torch.cuda.current_stream(Q.device)
-    rc = load_library().f3s_backward(
-        plan.handle, plan_t.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), O.data_ptr(),
-        dO.data_ptr(), lse.data_ptr(), row_stats.data_ptr(), dQ.data_ptr(), dK.data_ptr(),
-        dV.data_ptr(), int(H), int(d), float(scale), ctypes.c_void_p(stream.cuda_stream))
+    rc = load_library().f3s_backward_typed(
+        plan.handle, plan_t.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(),
+        _DTYPE_CODE[Q.dtype], O.data_ptr(), dO.data_ptr(), lse.data_ptr(),
+        row_stats.data_ptr(), dQ.data_ptr(), dK.data_ptr(), dV.data_ptr(), int(H), int(d),
+        float(scale), ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
-        raise F3SError(rc, "f3s_backward")
+        raise F3SError(rc, "f3s_backward_typed")
     return dQ, dK, dV
 
 

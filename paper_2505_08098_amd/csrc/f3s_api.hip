@@ -647,6 +647,18 @@ f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void
                           float *row_stats, float *dQ, float *dK, float *dV, int32_t n_heads,
                           int32_t d, float scale, hipStream_t stream)
 {
+    return f3s_backward_typed(p, pt, Q, K, V, F3S_DTYPE_F16, O, dO, lse, row_stats, dQ, dK,
+                              dV, n_heads, d, scale, stream);
+}
+
+f3s_status_t f3s_backward_typed(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void *K,
+                                const void *V, f3s_dtype_t in_dtype, const float *O,
+                                const void *dO, const float *lse, float *row_stats, float *dQ,
+                                float *dK, float *dV, int32_t n_heads, int32_t d, float scale,
+                                hipStream_t stream)
+{
+    if (in_dtype != F3S_DTYPE_F16 && in_dtype != F3S_DTYPE_BF16)
+        return fail(F3S_ERR_UNSUPPORTED);
     if (!p || !pt || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (pt->transpose_of != p->id || pt->N != p->N) return fail(F3S_ERR_INVALID_VALUE);
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
@@ -676,8 +688,9 @@ f3s_status_t f3s_backward(f3s_plan_t p, f3s_plan_t pt, const void *Q, const void
         for (const Span &x : out_spans)
             if (&x != &o && overlaps(o.p, o.n, x.p, x.n)) return fail(F3S_ERR_INVALID_VALUE);
     }
-    f3s_status_t st = from_hip(f3s::launch_backward(*p, *pt, Q, K, V, O, dO, lse, row_stats, dQ,
-                                                    dK, dV, n_heads, d, scale, stream));
+    auto launch = in_dtype == F3S_DTYPE_BF16 ? f3s::launch_backward_bf16 : f3s::launch_backward;
+    f3s_status_t st = from_hip(launch(*p, *pt, Q, K, V, O, dO, lse, row_stats, dQ, dK, dV,
+                                      n_heads, d, scale, stream));
     return st == F3S_OK ? F3S_OK : fail(st);
 }
 

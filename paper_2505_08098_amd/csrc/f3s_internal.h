@@ -166,11 +166,16 @@ hipError_t launch_fused_fp8(const f3s_plan_s &p, const void *Q, const void *K,
                             const void *V, void *O, bool out_f16, float *lse, int32_t H,
                             int32_t d, float scale_log2, hipStream_t s);
 
-// Gradients (see backward.hip).  pt is the plan of the transposed pattern;
-// row_stats: [N, H, 2] (base-2 lse, delta) written by the dQ pass.
+// Gradients (backward_kernel.h; fp16 inputs: backward.hip, bf16 inputs:
+// backward_bf16.hip).  pt is the plan of the transposed pattern; row_stats:
+// [N, H, 2] (base-2 lse, delta) written by the dQ pass.
 hipError_t launch_backward(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q,
                            const void *K, const void *V, const float *O, const void *G,
                            const float *lse, float *row_stats, float *dQ, float *dK, float *dV,
                            int32_t H, int32_t d, float scale, hipStream_t s);
+hipError_t launch_backward_bf16(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q,
+                                const void *K, const void *V, const float *O, const void *G,
+                                const float *lse, float *row_stats, float *dQ, float *dK,
+                                float *dV, int32_t H, int32_t d, float scale, hipStream_t s);
 
 }  // namespace f3s

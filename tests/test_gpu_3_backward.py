@@ -5,6 +5,9 @@ products, unit roundoff 2^-11; P recomputed from an lse whose normaliser
 summed fp16-rounded probabilities): relative Frobenius error <= 1e-3 per
 gradient and max-abs error <= 5e-3 * max(1, max |reference|).  Measured:
 rel-Fro ~2e-4 (the fp16 rounding of P and dS, 2^-11 relative, averaged).
+bf16 inputs (the oracle gets the same bf16 values, widened exactly): P and
+dS enter the products as two bf16 terms (~16 bits), so the same bar holds
+with room to spare.
 """
 import math
 
@@ -144,6 +147,73 @@ def test_transposed_plan_of_symmetric_and_nearly_symmetric_patterns(gpu, oracle,
         assert np.array_equal(got[key], b[key]), key
     same = all(np.array_equal(got[k], plan.export()[k]) for k in ("cols", "mask"))
     assert same == (not extra)
+
+
+def _bf16_dev(bits):
+    return _dev(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16)
+
+
+def _grad_case_bf16(f3s, oracle, rp, ci, N, Qb, Kb, Vb, Gb, scale):
+    """bf16 bit patterns in; forward (fp32 O, lse) and backward in bf16."""
+    plan = f3s.Plan(_dev(rp), _dev(ci), N)
+    plan_t = plan.transpose()
+    q, k, v, g = (_bf16_dev(x) for x in (Qb, Kb, Vb, Gb))
+    O, lse = f3s.forward_typed(plan, q, k, v, scale=scale, want_lse=True)
+    dQ, dK, dV = f3s.backward(plan, plan_t, q, k, v, O, g, lse, scale=scale)
+    torch.cuda.synchronize()
+    H = Qb.shape[1] if Qb.ndim == 3 else 1
+    wide = [oracle.widen_bf16(x) for x in (Qb, Kb, Vb, Gb)]
+    for h in range(H):
+        sl = (slice(None), h) if Qb.ndim == 3 else (slice(None),)
+        ref = oracle.attention_bwd_f64(rp, ci, *(x[sl] for x in wide), scale)
+        for name, got, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
+            _check(f"bf16 {name}[h{h}]", got.cpu().numpy()[sl], r)
+
+
+@pytest.mark.parametrize("d", [32, 64, 128, 160, 256])
+@pytest.mark.parametrize("N", [17, 300])
+def test_gradients_bf16_random_patterns(gpu, oracle, d, N):
+    rng = np.random.default_rng(3 * d + N)
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 50), empty_frac=0.1, dup_frac=0.2)
+    Qb, Kb, Vb, Gb = (W.to_bf16_bits(rng.standard_normal((N, d)).astype(np.float32))
+                      for _ in range(4))
+    _grad_case_bf16(gpu, oracle, rp, ci, N, Qb, Kb, Vb, Gb, 1.0 / math.sqrt(d))
+
+
+@pytest.mark.parametrize("H,d", [(3, 64), (2, 256)])
+def test_gradients_bf16_split_windows_and_heads(gpu, oracle, monkeypatch, H, d):
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
+    rng = np.random.default_rng(H * d)
+    N = 700
+    rp, ci = W.random_csr(rng, N, max_deg=200, empty_frac=0.05, dup_frac=0.1)
+    Qb, Kb, Vb, Gb = (W.to_bf16_bits(rng.standard_normal((N, H, d)).astype(np.float32))
+                      for _ in range(4))
+    _grad_case_bf16(gpu, oracle, rp, ci, N, Qb, Kb, Vb, Gb, 1.0 / math.sqrt(d))
+
+
+@pytest.mark.parametrize("k", [1, 4, 2])
+def test_gradients_bf16_workloads(gpu, oracle, k):
+    c = W.make_config(k, dtype="bf16")
+    print(f"workload {k} bf16 backward N={c['N']} d={c['d']}", flush=True)
+    rng = np.random.default_rng(100 + k)
+    Gb = W.to_bf16_bits(rng.standard_normal(c["Q"].shape).astype(np.float32))
+    _grad_case_bf16(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"], c["Q"], c["K"], c["V"],
+                    Gb, c["scale"])
+
+
+def test_backward_rejects_mixed_or_other_types(gpu):
+    rng = np.random.default_rng(5)
+    N, d = 40, 64
+    rp, ci = W.random_csr(rng, N, max_deg=10)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    plan_t = plan.transpose()
+    q = _dev(rng.standard_normal((N, d)).astype(np.float16))
+    O, lse = gpu.forward(plan, q, q, q)
+    with pytest.raises(TypeError):
+        gpu.backward(plan, plan_t, q, q, q, O, q.to(torch.bfloat16), lse)
+    with pytest.raises(TypeError):
+        qf = q.float()
+        gpu.backward(plan, plan_t, qf, qf, qf, O, qf, lse)
 
 
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
