@@ -111,6 +111,32 @@ int main(int argc, char **argv)
     if (!fo || fwrite(o, 4, feat, fo) != feat) return 1;
     fclose(fo);
 
+    /* the same plan built into a caller-lent workspace gives the same O */
+    const size_t ws_bytes = f3s_plan_workspace_bytes(N, (int64_t)nnz);
+    void *d_ws = NULL;
+    HIP_OK(hipMalloc(&d_ws, ws_bytes ? ws_bytes : 256));
+    f3s_plan_t plan_ws = f3s_plan_ws(d_rp, d_ci, N, d_ws, ws_bytes);
+    if (!plan_ws) {
+        fprintf(stderr, "f3s_plan_ws: %s\n", f3s_status_string(f3s_last_error()));
+        return 3;
+    }
+    float *d_o2 = NULL;
+    HIP_OK(hipMalloc((void **)&d_o2, 4 * (feat ? feat : 4)));
+    st = f3s_run(plan_ws, d_q, d_k, d_v, d_o2, d, scale, NULL);
+    HIP_OK(hipDeviceSynchronize());
+    float *o2 = malloc(4 * (feat ? feat : 1));
+    HIP_OK(hipMemcpy(o2, d_o2, 4 * feat, hipMemcpyDeviceToHost));
+    fprintf(info, "ws_run %s same %d\n", f3s_status_string(st),
+            feat == 0 || memcmp(o, o2, 4 * feat) == 0);
+    f3s_plan_t short_ws = f3s_plan_ws(d_rp, d_ci, N, d_ws, ws_bytes / 2);
+    fprintf(info, "ws_short %s %s\n", short_ws ? "plan" : "null",
+            f3s_status_string(f3s_last_error()));
+    f3s_destroy(short_ws);
+    f3s_destroy(plan_ws);
+    (void)hipFree(d_ws);
+    (void)hipFree(d_o2);
+    free(o2);
+
     /* argument errors are reported, not launched */
     st = f3s_run(plan, d_q, d_k, d_v, d_o, d + 8, scale, NULL);
     fprintf(info, "bad_d %s\n", f3s_status_string(st));

@@ -54,3 +54,5 @@ def test_c_driver_matches_oracle(gpu, oracle, tmp_path, case):
     assert info["null_plan"] == "F3S_ERR_INVALID_VALUE last_error F3S_ERR_INVALID_VALUE"
     assert info["misaligned_out"] == "F3S_ERR_INVALID_VALUE"
     assert info["bad_csr"] == "null F3S_ERR_INVALID_CSR"
+    assert info["ws_run"] == "F3S_OK same 1"          # f3s_plan_ws: identical result
+    assert info["ws_short"] == "null F3S_ERR_INVALID_VALUE"
