@@ -77,10 +77,11 @@ def traffic_from_counters(d):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(c, O_gpu, sample_rows):
+def cpu_baseline(c, O_gpu, sample_rows, threads=0):
     import numpy as np
     import oracle
-    threads = min(16, len(os.sched_getaffinity(0)))
+    if threads <= 0:
+        threads = min(16, len(os.sched_getaffinity(0)))
     r1 = min(c["N"], sample_rows)
     t0 = time.perf_counter()
     ref = oracle.attention_rows_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
@@ -237,6 +238,9 @@ def main():
                     help="heads sharing the plan (Q, K, V of shape [N, heads, d]; "
                          "fresh seeded N(0,1) features)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="threads of the oracle baseline (default: the host's cores, "
+                         "at most 16)")
     ap.add_argument("--cpu-rows", type=int, default=1 << 30,
                     help="rows of the workload in the oracle baseline sample")
     ap.add_argument("--backward", action="store_true",
@@ -398,7 +402,7 @@ def main():
     elif not args.no_cpu:
         torch.cuda.synchronize()
         O_host = O.cpu().numpy()
-        base, parity = cpu_baseline(c, O_host, args.cpu_rows)
+        base, parity = cpu_baseline(c, O_host, args.cpu_rows, args.cpu_threads)
         out["cpu_baseline"] = base
         out["parity_sample"] = parity
     else:
