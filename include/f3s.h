@@ -89,7 +89,8 @@ f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N);
 
 /*
  * Device bytes of scratch a build of f3s_plan_ws needs for a pattern of N
- * rows and nnz CSR entries on the current device (0 for negative sizes).
+ * rows and nnz CSR entries: 6 bytes per entry plus about 110 per row
+ * window (0 for negative sizes).  Host-only; calls no HIP function.
  */
 size_t f3s_plan_workspace_bytes(int32_t N, int64_t nnz);
 

@@ -164,7 +164,7 @@ struct BuildStats {
     int32_t piece;
     int32_t n_pieces;
     int32_t n_split;
-    int32_t n_items;              // total of the work-list histogram
+    int32_t n_items;              // item count from the work-list scan
     int32_t invalid;              // plan integrity check
 };
 
@@ -174,11 +174,9 @@ struct BuildScratch {
     int32_t *tmp_cols;   // sorted distinct columns per window, at its CSR offset
     uint32_t *tmp_mask;  // block bitmaps per window, staged
     int32_t *u, *big, *is_big, *heavy, *is_heavy, *bits, *nb, *npieces, *key, *split_item;
-    int32_t *big_pos, *heavy_pos, *split_pieces, *split_one, *scan_tmp, *hist_area;
-    int64_t hist_room;
+    int32_t *big_pos, *heavy_pos, *split_pieces, *split_one, *scan_tmp;
+    f3s::WorkListScratch wl;  // the work-list sort
 };
-
-constexpr int32_t kBinChunk = 64;  // windows per histogram chunk of the work-list sort
 
 template <typename U>
 U *carve(Arena &a, bool take, int64_t n)
@@ -189,16 +187,11 @@ U *carve(Arena &a, bool take, int64_t n)
 }
 
 // Lays out the build's scratch for T windows and nnz CSR entries: sizes into
-// a (take == false) or pointers out of it (take == true), in one order.  The
-// work-list histogram gets room for the largest piece size the block count
-// allows (blocks <= nnz / 16 + T); a forced larger piece allocates its own.
-void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz,
-                   int32_t slots)
+// a (take == false) or pointers out of it (take == true), in one order.
+// O(nnz + T) bytes.
+void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz)
 {
     using namespace f3s;
-    const int64_t nchunks = (T + kBinChunk - 1) / kBinChunk;
-    const int64_t piece_bound = (nnz / 16 + T + slots - 1) / slots + 18;
-    b.hist_room = (piece_bound + 1) * nchunks + 1 + scan_tmp_ints((piece_bound + 1) * nchunks);
     b.st = carve<BuildStats>(a, take, 1);
     b.tmp_cols = carve<int32_t>(a, take, nnz);
     b.tmp_mask = carve<uint32_t>(a, take, mask_stage_words(nnz, T));
@@ -207,16 +200,23 @@ void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz,
     for (int32_t **q : per_window) *q = carve<int32_t>(a, take, T);
     int32_t **per_window1[] = {&b.big_pos, &b.heavy_pos, &b.split_pieces, &b.split_one};
     for (int32_t **q : per_window1) *q = carve<int32_t>(a, take, (int64_t)T + 1);
-    b.scan_tmp = carve<int32_t>(a, take, scan_tmp_ints(T));
-    b.hist_area = carve<int32_t>(a, take, b.hist_room);
+    const int64_t wl_counts = worklist_count_ints(T);
+    b.scan_tmp = carve<int32_t>(a, take, scan_tmp_ints(T > wl_counts ? T : wl_counts));
+    b.wl.keys_a = carve<int32_t>(a, take, T);
+    b.wl.keys_b = carve<int32_t>(a, take, T);
+    b.wl.order_in = carve<int32_t>(a, take, T);
+    b.wl.order = carve<int32_t>(a, take, T);
+    b.wl.pos = carve<int32_t>(a, take, (int64_t)T + 1);
+    b.wl.counts = carve<int32_t>(a, take, wl_counts);
+    b.wl.scan_tmp = b.scan_tmp;
 }
 
-size_t plan_workspace_bytes(int32_t N, int64_t nnz, int device)
+size_t plan_workspace_bytes(int32_t N, int64_t nnz)
 {
     Arena a;
     BuildScratch b;
     const int32_t T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
-    carve_scratch(a, false, b, T, nnz, plan_slots(device));
+    carve_scratch(a, false, b, T, nnz);
     return a.cap;
 }
 
@@ -239,7 +239,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     const int32_t slots = plan_slots(p->device);
     BuildScratch b;
     ScratchArena tmp;
-    carve_scratch(tmp, false, b, T, nnz, slots);
+    carve_scratch(tmp, false, b, T, nnz);
     if (workspace) {
         if (workspace_bytes < tmp.cap || ((uintptr_t)workspace & 255u))
             return F3S_ERR_INVALID_VALUE;
@@ -248,7 +248,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     } else {
         HIP_TRY(tmp.alloc());
     }
-    carve_scratch(tmp, true, b, T, nnz, slots);
+    carve_scratch(tmp, true, b, T, nnz);
     BuildStats *st = b.st;
     int32_t *tmp_cols = b.tmp_cols;
     uint32_t *tmp_mask = b.tmp_mask;
@@ -256,10 +256,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     int32_t *is_heavy = b.is_heavy, *bits = b.bits, *nb = b.nb, *npieces = b.npieces;
     int32_t *key = b.key, *split_item = b.split_item, *big_pos = b.big_pos;
     int32_t *heavy_pos = b.heavy_pos, *split_pieces = b.split_pieces;
-    int32_t *split_one = b.split_one, *scan_tmp = b.scan_tmp, *hist_area = b.hist_area;
-    const int64_t hist_room = b.hist_room;
-    const int32_t chunk = kBinChunk;
-    const int32_t nchunks = (T + chunk - 1) / chunk;
+    int32_t *split_one = b.split_one, *scan_tmp = b.scan_tmp;
     BuildStats hs;
     HIP_TRY(hipMemsetAsync(st, 0, sizeof(BuildStats), s));
 
@@ -313,24 +310,10 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_fill_windows(row_ptr, T, tmp_cols, tmp_mask, u, p->blk_off, p->cols,
                                 p->mask, s));
 
-    // ---- 6. heavy-first work list: histogram over (key, chunk), scan, scatter
-    const int64_t cells = (int64_t)(piece + 1) * nchunks;
-    if (cells >= INT32_MAX) return F3S_ERR_UNSUPPORTED;
-    int32_t *hist = hist_area, *hist_tmp = hist_area + cells + 1;
-    ScratchArena hist_arena;
-    if (cells + 1 + scan_tmp_ints(cells) > hist_room) {
-        hist_arena.add<int32_t>(cells + 1);
-        hist_arena.add<int32_t>(scan_tmp_ints(cells));
-        HIP_TRY(hist_arena.alloc());
-        hist = hist_arena.take<int32_t>(cells + 1);
-        hist_tmp = hist_arena.take<int32_t>(scan_tmp_ints(cells));
-    }
-    HIP_TRY(hipMemsetAsync(hist, 0, (size_t)(cells + 1) * 4, s));
-    HIP_TRY(launch_bin_hist(npieces, key, T, piece, chunk, nchunks, hist, s));
-    HIP_TRY(launch_scan(hist, hist, (int32_t)cells, hist_tmp, &st->n_items, s));
-    HIP_TRY(launch_bin_scatter(nb, p->blk_off, npieces, key, split_pieces, split_one,
-                               T, piece, chunk, nchunks, hist, p->items, p->merges,
-                               split_item, p->n_split, s));
+    // ---- 6. heavy-first work list: stable sort of the windows by key ------
+    HIP_TRY(launch_worklist(key, nb, p->blk_off, npieces, split_pieces, split_one, T, piece,
+                            b.wl, p->items, p->merges, split_item, &st->n_items, s));
+    HIP_TRY(launch_split_items(p->merges, split_item, p->blk_off, p->n_split, p->items, s));
 
     // ---- 7. integrity check of the finished plan ------------------------
     HIP_TRY(launch_validate_plan(*p, &st->invalid, s));
@@ -444,9 +427,8 @@ f3s_plan_t f3s_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N)
 
 size_t f3s_plan_workspace_bytes(int32_t N, int64_t nnz)
 {
-    int device = 0;
-    if (N < 0 || nnz < 0 || hipGetDevice(&device) != hipSuccess) return 0;
-    return plan_workspace_bytes(N, nnz, device);
+    if (N < 0 || nnz < 0) return 0;
+    return plan_workspace_bytes(N, nnz);
 }
 
 f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,

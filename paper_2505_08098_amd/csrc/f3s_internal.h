@@ -123,16 +123,30 @@ hipError_t launch_bin_keys(const int32_t *nb, int32_t T, const int32_t *n_blocks
                            bool reorder, int32_t *piece_out, int32_t *npieces,
                            int32_t *key, int32_t *split_pieces, int32_t *split_one,
                            hipStream_t s);
-hipError_t launch_bin_hist(const int32_t *npieces, const int32_t *key, int32_t T,
-                           int32_t piece, int32_t chunk, int32_t nchunks,
-                           int32_t *hist, hipStream_t s);
-hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
-                              const int32_t *npieces, const int32_t *key,
-                              const int32_t *slot_base, const int32_t *split_idx,
-                              int32_t T, int32_t piece, int32_t chunk,
-                              int32_t nchunks, int32_t *offs, WorkItem *items,
-                              int32_t *merges, int32_t *split_item, int32_t n_split,
+// Pieces of the split windows: items[split_item[s] + k] for piece k of
+// split window s (merges[3s..3s+2] = window, first slot, pieces).
+hipError_t launch_split_items(const int32_t *merges, const int32_t *split_item,
+                              const int32_t *blk_off, int32_t n_split, WorkItem *items,
                               hipStream_t s);
+
+// ---- work list (worklist.hip) ----------------------------------------------
+struct WorkListScratch {
+    int32_t *keys_a, *keys_b;   // [T] each: keys between radix passes
+    int32_t *order_in;          // [T]
+    int32_t *order;             // [T] windows between radix passes
+    int32_t *pos;               // [T + 1] first item of each window in sorted order
+    int32_t *counts;            // worklist_count_ints(T): digit counts per tile
+    int32_t *scan_tmp;          // scan_tmp_ints(max(T, worklist_count_ints(T)))
+};
+int64_t worklist_count_ints(int32_t T);
+// Heavy-first work list from the keys of launch_bin_keys: whole windows as
+// items, split windows as merge records plus split_item (their pieces:
+// launch_split_items); the item count goes to *n_items_out.
+hipError_t launch_worklist(const int32_t *key, const int32_t *nb, const int32_t *blk_off,
+                           const int32_t *npieces, const int32_t *slot_base,
+                           const int32_t *split_idx, int32_t T, int32_t piece,
+                           const WorkListScratch &ws, WorkItem *items, int32_t *merges,
+                           int32_t *split_item, int32_t *n_items_out, hipStream_t s);
 
 // ---- transposed pattern (transpose.hip) ----------------------------------
 // CSR of A^T (rp[N+1], ci[nnz]) from a plan's bitmaps; scratch of

@@ -9,8 +9,9 @@
 //     chunks of 2^17 columns)
 //  3. blocks per window (ceil(u/16)) and their exclusive prefix (tro)
 //  4. padded column lists (sptd) and bitmaps copied to their final blocks
-//  5. work list: windows stably sorted by block count, largest first, with
-//     windows above `piece` blocks split into pieces of whole block pairs
+//  5. work list keys: block count per window (the stable sort, largest
+//     first, is worklist.hip's), windows above `piece` blocks split into
+//     pieces of whole block pairs
 //
 // Every kernel is deterministic: integer atomics only commute (bitwise OR,
 // counters whose final value is all that is read), and every position in
@@ -716,47 +717,6 @@ __global__ void k_bin_keys(const int32_t *nb, int32_t T, const int32_t *n_blocks
     split_one[w] = split ? 1 : 0;
 }
 
-// One thread per chunk of windows; hist is [piece + 1][nchunks], row b holds
-// the items of key (piece - b), so a flat scan orders keys largest first,
-// then chunks, then windows inside a chunk: a stable descending sort.
-__global__ void k_bin_hist(const int32_t *npieces, const int32_t *key, int32_t T,
-                           int32_t piece, int32_t chunk, int32_t nchunks,
-                           int32_t *hist)
-{
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= nchunks) return;
-    const int w1 = min(T, (c + 1) * chunk);
-    for (int w = c * chunk; w < w1; ++w)
-        hist[(int64_t)(piece - key[w]) * nchunks + c] += npieces[w];
-}
-
-__global__ void k_bin_scatter(const int32_t *nb, const int32_t *blk_off,
-                              const int32_t *npieces, const int32_t *key,
-                              const int32_t *slot_base, const int32_t *split_idx,
-                              int32_t T, int32_t piece, int32_t chunk,
-                              int32_t nchunks, int32_t *offs, WorkItem *items,
-                              int32_t *merges, int32_t *split_item)
-{
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= nchunks) return;
-    const int w1 = min(T, (c + 1) * chunk);
-    for (int w = c * chunk; w < w1; ++w) {
-        int32_t *cell = offs + (int64_t)(piece - key[w]) * nchunks + c;
-        const int pos = *cell;
-        const int n = nb[w], b0 = blk_off[w], np = npieces[w];
-        if (n <= piece) {
-            items[pos] = WorkItem{w, b0, b0 + n, -1};
-        } else {
-            const int s = split_idx[w];
-            merges[3 * s + 0] = w;
-            merges[3 * s + 1] = slot_base[w];
-            merges[3 * s + 2] = np;
-            split_item[s] = pos;  // its pieces: k_split_items
-        }
-        *cell = pos + np;
-    }
-}
-
 // Work items of the pieces of split window s (one wavefront per split
 // window): piece k of np covers the block pairs [floor(k*pairs/np),
 // floor((k+1)*pairs/np)) of the window, pairs = ceil(nb/2).
@@ -930,31 +890,11 @@ hipError_t launch_bin_keys(const int32_t *nb, int32_t T, const int32_t *n_blocks
     return hipGetLastError();
 }
 
-hipError_t launch_bin_hist(const int32_t *npieces, const int32_t *key, int32_t T,
-                           int32_t piece, int32_t chunk, int32_t nchunks,
-                           int32_t *hist, hipStream_t s)
-{
-    if (nchunks == 0) return hipSuccess;
-    k_bin_hist<<<grid_for(nchunks, 64), 64, 0, s>>>(npieces, key, T, piece, chunk,
-                                                   nchunks, hist);
-    return hipGetLastError();
-}
-
-hipError_t launch_bin_scatter(const int32_t *nb, const int32_t *blk_off,
-                              const int32_t *npieces, const int32_t *key,
-                              const int32_t *slot_base, const int32_t *split_idx,
-                              int32_t T, int32_t piece, int32_t chunk,
-                              int32_t nchunks, int32_t *offs, WorkItem *items,
-                              int32_t *merges, int32_t *split_item, int32_t n_split,
+hipError_t launch_split_items(const int32_t *merges, const int32_t *split_item,
+                              const int32_t *blk_off, int32_t n_split, WorkItem *items,
                               hipStream_t s)
 {
-    if (nchunks == 0) return hipSuccess;
-    k_bin_scatter<<<grid_for(nchunks, 64), 64, 0, s>>>(nb, blk_off, npieces, key,
-                                                       slot_base, split_idx, T, piece,
-                                                       chunk, nchunks, offs, items,
-                                                       merges, split_item);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || n_split == 0) return e;
+    if (n_split == 0) return hipSuccess;
     k_split_items<<<grid_for(n_split, 4), 256, 0, s>>>(merges, split_item, blk_off, n_split,
                                                       items);
     return hipGetLastError();

@@ -40,6 +40,11 @@ def test_workspace_bytes_rejects_negative_sizes(lib):
     lib.f3s_plan_workspace_bytes.restype = ctypes.c_size_t
     assert lib.f3s_plan_workspace_bytes(-1, 10) == 0
     assert lib.f3s_plan_workspace_bytes(10, -1) == 0
+    # host-only: linear in the entries (column staging, 4 + 2 bytes per entry)
+    a = lib.f3s_plan_workspace_bytes(1 << 20, 10_000_000)
+    b = lib.f3s_plan_workspace_bytes(1 << 20, 20_000_000)
+    assert 6 * 10_000_000 <= b - a <= 6 * 10_000_000 + 4096
+    assert lib.f3s_plan_workspace_bytes(0, 0) > 0
 
 
 def test_every_declared_symbol_is_exported(lib):

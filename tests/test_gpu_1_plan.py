@@ -126,8 +126,7 @@ def test_plan_split_windows(gpu, oracle, monkeypatch):
 
 def test_plan_forced_piece_above_the_estimate(gpu, oracle, monkeypatch):
     """A forced piece size larger than any window: capped at the largest
-    window (nothing split); its work-list histogram is larger than the one
-    the build reserves for the estimated piece size."""
+    window (nothing split), the work list is the stable sort by block count."""
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "100000")
     c = W.make_config(2, with_features=False)
     info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
