@@ -200,15 +200,15 @@ void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz)
     for (int32_t **q : per_window) *q = carve<int32_t>(a, take, T);
     int32_t **per_window1[] = {&b.big_pos, &b.heavy_pos, &b.split_pieces, &b.split_one};
     for (int32_t **q : per_window1) *q = carve<int32_t>(a, take, (int64_t)T + 1);
-    const int64_t wl_counts = worklist_count_ints(T);
-    b.scan_tmp = carve<int32_t>(a, take, scan_tmp_ints(T > wl_counts ? T : wl_counts));
-    b.wl.keys_a = carve<int32_t>(a, take, T);
-    b.wl.keys_b = carve<int32_t>(a, take, T);
-    b.wl.order_in = carve<int32_t>(a, take, T);
-    b.wl.order = carve<int32_t>(a, take, T);
+    const int64_t rc = radix_count_ints(T);
+    b.scan_tmp = carve<int32_t>(a, take, scan_tmp_ints(T > rc ? T : rc));
+    b.wl.windows = carve<int32_t>(a, take, T);
     b.wl.pos = carve<int32_t>(a, take, (int64_t)T + 1);
-    b.wl.counts = carve<int32_t>(a, take, wl_counts);
-    b.wl.scan_tmp = b.scan_tmp;
+    int32_t **radix_arrays[] = {&b.wl.radix.keys_a, &b.wl.radix.vals_a, &b.wl.radix.keys_b,
+                                &b.wl.radix.vals_b};
+    for (int32_t **q : radix_arrays) *q = carve<int32_t>(a, take, T);
+    b.wl.radix.counts = carve<int32_t>(a, take, rc);
+    b.wl.radix.scan_tmp = b.scan_tmp;
 }
 
 size_t plan_workspace_bytes(int32_t N, int64_t nnz)

@@ -129,16 +129,27 @@ hipError_t launch_split_items(const int32_t *merges, const int32_t *split_item,
                               const int32_t *blk_off, int32_t n_split, WorkItem *items,
                               hipStream_t s);
 
+// ---- radix sort (radix.hip) -------------------------------------------------
+// Stable sort of n (key, value) int32 pairs, keys in [0, max_key], ascending
+// or descending; the inputs are not written; the results end up in one of
+// the two scratch pairs (*keys_out, *vals_out say which).
+struct RadixScratch {
+    int32_t *keys_a, *vals_a, *keys_b, *vals_b;  // [n] each
+    int32_t *counts;                              // radix_count_ints(n)
+    int32_t *scan_tmp;                            // scan_tmp_ints(max(n, radix_count_ints(n)))
+};
+int64_t radix_count_ints(int32_t n);
+hipError_t launch_radix_pairs(const int32_t *keys, const int32_t *vals, int32_t n,
+                              int32_t max_key, bool descending, const RadixScratch &rs,
+                              const int32_t **keys_out, const int32_t **vals_out,
+                              hipStream_t s);
+
 // ---- work list (worklist.hip) ----------------------------------------------
 struct WorkListScratch {
-    int32_t *keys_a, *keys_b;   // [T] each: keys between radix passes
-    int32_t *order_in;          // [T]
-    int32_t *order;             // [T] windows between radix passes
-    int32_t *pos;               // [T + 1] first item of each window in sorted order
-    int32_t *counts;            // worklist_count_ints(T): digit counts per tile
-    int32_t *scan_tmp;          // scan_tmp_ints(max(T, worklist_count_ints(T)))
+    int32_t *windows;    // [T]: 0 .. T-1
+    int32_t *pos;        // [T + 1] first item of each window in sorted order
+    RadixScratch radix;  // for n = T
 };
-int64_t worklist_count_ints(int32_t T);
 // Heavy-first work list from the keys of launch_bin_keys: whole windows as
 // items, split windows as merge records plus split_item (their pieces:
 // launch_split_items); the item count goes to *n_items_out.

@@ -2,12 +2,10 @@
 // symmetric pattern (checked exactly, entry by entry) has A^T = A, so its
 // plan is a copy.  Otherwise the CSR of A^T is built without atomics:
 // the plan's block bitmaps are decoded into (column, row) pairs, the pairs
-// are radix-sorted by column (hipCUB, stable), and the row pointers of A^T
-// follow from the sorted columns by binary search.  The pattern a plan holds
+// are radix-sorted by column (radix.hip, stable), and the row pointers of
+// A^T follow from the sorted columns by binary search.  The pattern a plan holds
 // is A with duplicates merged (Section 3.1's bitmaps), so A^T has one entry
 // per set bit.
-#include <hipcub/hipcub.hpp>
-
 #include "f3s_internal.h"
 
 namespace f3s {
@@ -47,7 +45,7 @@ __global__ __launch_bounds__(256) void k_window_bits(const int32_t *blk_off,
 __global__ __launch_bounds__(256) void k_window_pairs(const int32_t *blk_off,
                                                       const int32_t *cols,
                                                       const uint32_t *mask, int32_t T,
-                                                      const int32_t *off, uint32_t *keys,
+                                                      const int32_t *off, int32_t *keys,
                                                       int32_t *rows)
 {
     const int lane = threadIdx.x & 63;
@@ -68,7 +66,7 @@ __global__ __launch_bounds__(256) void k_window_pairs(const int32_t *blk_off,
             m &= m - 1;
             const int r = (bit >> 2) & 15;             // window row
             const int c = 4 * (bit >> 6) + (bit & 3);  // block column
-            keys[pos] = (uint32_t)cols[kBlockCols * blk + c];
+            keys[pos] = cols[kBlockCols * blk + c];
             rows[pos] = w * kWindowRows + r;
             ++pos;
         }
@@ -77,7 +75,7 @@ __global__ __launch_bounds__(256) void k_window_pairs(const int32_t *blk_off,
 }
 
 // rp[c] = number of sorted keys below c, for c = 0 .. N.
-__global__ void k_rows_from_sorted(const uint32_t *keys, int32_t n, int32_t N, int32_t *rp)
+__global__ void k_rows_from_sorted(const int32_t *keys, int32_t n, int32_t N, int32_t *rp)
 {
     const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (c > N) return;
@@ -153,13 +151,6 @@ __global__ __launch_bounds__(256) void k_check_symmetric(const int32_t *blk_off,
     }
 }
 
-int key_bits(int32_t N)
-{
-    int b = 1;
-    while (b < 31 && (1ll << b) < N) ++b;
-    return b;
-}
-
 }  // namespace
 
 hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
@@ -176,20 +167,17 @@ hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *as
     return hipGetLastError();
 }
 
-// Scratch of launch_transpose_csr: keys in and out, rows in, per-window
-// counts and offsets, the scan's workspace and the radix sort's storage.
+// Scratch of launch_transpose_csr: the decoded pairs, the radix sort's two
+// buffer pairs, per-window counts and offsets, digit counts and the scans'
+// workspace.
 hipError_t transpose_scratch_bytes(const f3s_plan_s &p, size_t *bytes)
 {
-    const int32_t n = (int32_t)p.nnz;
-    size_t sort_bytes = 0;
-    hipError_t e = hipcub::DeviceRadixSort::SortPairs(
-        nullptr, sort_bytes, (const uint32_t *)nullptr, (uint32_t *)nullptr,
-        (const int32_t *)nullptr, (int32_t *)nullptr, n, 0, key_bits(p.N));
-    if (e != hipSuccess) return e;
-    auto r = [](size_t b) { return (b + 255) & ~(size_t)255; };
-    const size_t pairs = (size_t)(n > 0 ? n : 1);
-    *bytes = 3 * r(4 * pairs) + 2 * r(4 * ((size_t)p.T + 1)) +
-             r(4 * (size_t)scan_tmp_ints(p.T)) + r(sort_bytes);
+    const int64_t n = p.nnz > 0 ? p.nnz : 1;
+    const int64_t rc = radix_count_ints((int32_t)n);
+    int64_t scan = p.T > n ? p.T : n;
+    if (rc > scan) scan = rc;
+    auto r = [](int64_t ints) { return (size_t)((4 * ints + 255) & ~255ll); };
+    *bytes = 6 * r(n) + 2 * r((int64_t)p.T + 1) + r(rc) + r(scan_tmp_ints(scan));
     return hipSuccess;
 }
 
@@ -198,41 +186,47 @@ hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scrat
 {
     const int32_t n = (int32_t)p.nnz;
     const int32_t T = p.T;
-    auto r = [](size_t b) { return (b + 255) & ~(size_t)255; };
-    const size_t pairs = (size_t)(n > 0 ? n : 1);
+    const int64_t nn = n > 0 ? n : 1;
+    const int64_t rc = radix_count_ints((int32_t)nn);
+    int64_t scan = T > nn ? T : nn;
+    if (rc > scan) scan = rc;
     char *at = static_cast<char *>(scratch);
-    auto take = [&](size_t b) {
-        char *q = at;
-        at += r(b);
+    auto take = [&](int64_t ints) {
+        int32_t *q = reinterpret_cast<int32_t *>(at);
+        at += (4 * ints + 255) & ~255ll;
         return q;
     };
-    uint32_t *keys_in = (uint32_t *)take(4 * pairs);
-    uint32_t *keys_out = (uint32_t *)take(4 * pairs);
-    int32_t *rows_in = (int32_t *)take(4 * pairs);
-    int32_t *cnt = (int32_t *)take(4 * ((size_t)T + 1));
-    int32_t *off = (int32_t *)take(4 * ((size_t)T + 1));
-    int32_t *scan_tmp = (int32_t *)take(4 * (size_t)scan_tmp_ints(T));
-    const size_t used = (size_t)(at - static_cast<char *>(scratch));
-    if (used > scratch_bytes) return hipErrorInvalidValue;
-    size_t sort_bytes = scratch_bytes - used;
+    int32_t *keys_in = take(nn), *rows_in = take(nn);
+    RadixScratch rs;
+    rs.keys_a = take(nn);
+    rs.vals_a = take(nn);
+    rs.keys_b = take(nn);
+    rs.vals_b = take(nn);
+    int32_t *cnt = take((int64_t)T + 1), *off = take((int64_t)T + 1);
+    rs.counts = take(rc);
+    rs.scan_tmp = take(scan_tmp_ints(scan));
+    if ((size_t)(at - static_cast<char *>(scratch)) > scratch_bytes) return hipErrorInvalidValue;
+    hipError_t e;
     if (T > 0) {
         k_window_bits<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.mask, T, cnt);
-        hipError_t e = hipGetLastError();
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        e = launch_scan(cnt, off, T, rs.scan_tmp, nullptr, s);
         if (e != hipSuccess) return e;
-        e = launch_scan(cnt, off, T, scan_tmp, nullptr, s);
-        if (e != hipSuccess) return e;
-        k_window_pairs<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.cols, p.mask, T, off,
-                                                   keys_in, rows_in);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        k_window_pairs<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.cols, p.mask, T, off, keys_in,
+                                                   rows_in);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
+    const int32_t *sorted_cols = keys_in, *sorted_rows = rows_in;
     if (n > 0) {
-        hipError_t e = hipcub::DeviceRadixSort::SortPairs(at, sort_bytes, keys_in, keys_out,
-                                                          rows_in, ci, n, 0, key_bits(p.N), s);
+        e = launch_radix_pairs(keys_in, rows_in, n, p.N - 1, false, rs, &sorted_cols,
+                               &sorted_rows, s);
+        if (e != hipSuccess) return e;
+        e = hipMemcpyAsync(ci, sorted_rows, sizeof(int32_t) * (size_t)n,
+                           hipMemcpyDeviceToDevice, s);
         if (e != hipSuccess) return e;
     }
     k_rows_from_sorted<<<(unsigned)(((int64_t)p.N + 1 + 255) / 256), 256, 0, s>>>(
-        keys_out, n, p.N, rp);
+        sorted_cols, n, p.N, rp);
     return hipGetLastError();
 }
 
