@@ -188,6 +188,21 @@ f3s_status_t f3s_forward_typed(f3s_plan_t plan, const void *Q, const void *K, co
 f3s_plan_t f3s_plan_transpose(f3s_plan_t plan);
 
 /*
+ * Device bytes of scratch f3s_plan_transpose_ws needs for `plan` (0 for a
+ * null plan).  Host-only.
+ */
+size_t f3s_plan_transpose_workspace_bytes(f3s_plan_t plan);
+
+/*
+ * f3s_plan_transpose with its scratch lent by the caller (device memory of
+ * at least f3s_plan_transpose_workspace_bytes(plan) bytes, 256-byte
+ * aligned; no reference kept, reusable on return).  The new plan's own
+ * arrays are still allocated by the library.  A null, misaligned or short
+ * workspace gives F3S_ERR_INVALID_VALUE.
+ */
+f3s_plan_t f3s_plan_transpose_ws(f3s_plan_t plan, void *workspace, size_t workspace_bytes);
+
+/*
  * Gradients of L with respect to Q, K, V given G = dL/dO (the backward pass
  * the paper leaves to future work).  With P the forward probabilities:
  *   delta_i = G_i . O_i,  dS_ij = P_ij (G_i . V_j - delta_i)  on the pattern,

@@ -91,6 +91,10 @@ def load_library():
     L.f3s_forward_typed.restype = ctypes.c_int
     L.f3s_plan_transpose.argtypes = [vp]
     L.f3s_plan_transpose.restype = vp
+    L.f3s_plan_transpose_workspace_bytes.argtypes = [vp]
+    L.f3s_plan_transpose_workspace_bytes.restype = ctypes.c_size_t
+    L.f3s_plan_transpose_ws.argtypes = [vp, vp, ctypes.c_size_t]
+    L.f3s_plan_transpose_ws.restype = vp
     L.f3s_backward.argtypes = [vp, vp] + [vp] * 10 + [i32, i32, ctypes.c_float, vp]
     L.f3s_backward.restype = ctypes.c_int
     L.f3s_backward_typed.argtypes = ([vp, vp, vp, vp, vp, i32] + [vp] * 7 +
@@ -136,12 +140,17 @@ class Plan:
         return self
 
     def transpose(self):
-        """Plan of the transposed pattern (f3s_plan_transpose)."""
+        """Plan of the transposed pattern (f3s_plan_transpose_ws, its scratch
+        lent from torch's caching allocator)."""
         L = load_library()
         with torch.cuda.device(self.device):
-            h = L.f3s_plan_transpose(self.handle)
+            torch.cuda.current_stream().synchronize()
+            nbytes = L.f3s_plan_transpose_workspace_bytes(self.handle)
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+            h = L.f3s_plan_transpose_ws(self.handle, ws.data_ptr(), nbytes)
+            del ws
         if not h:
-            raise F3SError(L.f3s_last_error(), "f3s_plan_transpose")
+            raise F3SError(L.f3s_last_error(), "f3s_plan_transpose_ws")
         return Plan._from_handle(h, self.device, self.N)
 
     def __init__(self, row_ptr, col_idx, N):

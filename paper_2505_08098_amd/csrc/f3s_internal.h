@@ -160,15 +160,20 @@ hipError_t launch_worklist(const int32_t *key, const int32_t *nb, const int32_t 
                            int32_t *split_item, int32_t *n_items_out, hipStream_t s);
 
 // ---- transposed pattern (transpose.hip) ----------------------------------
-// CSR of A^T (rp[N+1], ci[nnz]) from a plan's bitmaps; scratch of
-// transpose_scratch_bytes(p) bytes.
-hipError_t transpose_scratch_bytes(const f3s_plan_s &p, size_t *bytes);
-// Sets *asym (zeroed by the caller) unless every entry (r, c) of the plan's
-// pattern has its mirror (c, r); win: scratch of n_blocks ints.
-hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
-                                  hipStream_t s);
+// CSR of A^T (rp[N+1], ci[nnz], each row in increasing column order) from a
+// plan's bitmaps; scratch of transpose_scratch_bytes(p) bytes.
+size_t transpose_scratch_bytes(const f3s_plan_s &p);
 hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scratch_bytes,
                                 int32_t *rp, int32_t *ci, hipStream_t s);
+// Sets *asym (zeroed by the caller) unless the plan's pattern is symmetric,
+// from the plan alone (binary searches in the windows' column lists; cheap
+// on small patterns); win: scratch of n_blocks ints.
+hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
+                                  hipStream_t s);
+// The same decision given the CSR of A^T (binary searches in its short rows;
+// cheaper on large patterns once A^T is sorted anyway).
+hipError_t launch_compare_rows(const f3s_plan_s &p, const int32_t *rpt, const int32_t *cit,
+                               int32_t *win, int32_t *asym, hipStream_t s);
 
 // Sets *err when a finished plan is internally inconsistent.
 hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s);

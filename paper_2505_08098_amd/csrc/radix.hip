@@ -1,8 +1,9 @@
 // Stable least-significant-digit radix sort of (key, value) pairs of int32,
 // keys in [0, max_key], ascending or descending, with 8-bit digits (one pass
 // per 8 bits of max_key): per tile of kTile keys a digit histogram, one scan
-// over (digit, tile), then a stable scatter in which each tile walks its keys
-// in order, 256 at a time, and ranks equal digits with wavefront ballots.
+// over (digit, tile), then a stable scatter in which each tile ranks its keys
+// (in order, 256 at a time, equal digits by wavefront ballots) into digit
+// order in LDS and writes them out run by run.
 #include "f3s_internal.h"
 
 namespace f3s {
@@ -38,21 +39,46 @@ __global__ __launch_bounds__(kRadixThreads) void k_digit_count(const int32_t *ke
     counts[(int64_t)tid * ntiles + blockIdx.x] = h[tid];
 }
 
-// Stable scatter of one tile: keys are taken in index order, 256 per step;
-// within a step a key's rank among equal digits comes from ballots (within
-// its wavefront) and the counts of the earlier wavefronts of the step.
+// Stable scatter of one tile.  The tile's keys are first placed in LDS in
+// digit order: taken in index order, 256 per step, a key's rank among equal
+// digits comes from ballots (within its wavefront) and the counts of the
+// earlier wavefronts of the step.  Then the tile is written out in that
+// order, so each digit's run of keys goes to consecutive addresses.
 __global__ __launch_bounds__(kRadixThreads) void k_digit_scatter(
     const int32_t *keys, const int32_t *vals, int32_t n, int shift, bool descending,
     int32_t ntiles, const int32_t *offs, int32_t *keys_out, int32_t *vals_out)
 {
     constexpr int kWaves = kRadixThreads / 64;
-    __shared__ int32_t run[256];           // keys of each digit placed so far
-    __shared__ int32_t wcnt[kWaves][256];  // this step's count per wave and digit
+    __shared__ int32_t s_key[kTile], s_val[kTile];  // the tile in digit order
+    __shared__ int32_t start[256];                  // first slot of each digit
+    __shared__ int32_t run[256];                    // next free slot of each digit
+    __shared__ int32_t wcnt[kWaves][256];           // this step's count per wave, digit
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    run[tid] = offs[(int64_t)tid * ntiles + blockIdx.x];
+    const int64_t base = (int64_t)blockIdx.x * kTile;
+    const int tn = (int)min((int64_t)kTile, (int64_t)n - base);
+    run[tid] = 0;
     for (int k = 0; k < kWaves; ++k) wcnt[k][tid] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kTile;
+    for (int j = 0; j < kRadixSteps; ++j) {
+        const int64_t i = base + j * kRadixThreads + tid;
+        if (i < n) atomicAdd(&run[rdigit(keys[i], shift, descending)], 1);
+    }
+    __syncthreads();
+    // exclusive scan of the tile's digit counts
+    const int cnt = run[tid];
+    start[tid] = cnt;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const int t = tid >= off ? start[tid - off] : 0;
+        __syncthreads();
+        start[tid] += t;
+        __syncthreads();
+    }
+    const int excl = start[tid] - cnt;
+    __syncthreads();
+    start[tid] = excl;
+    run[tid] = excl;
+    __syncthreads();
     const uint64_t below = (1ull << lane) - 1ull;
     for (int j = 0; j < kRadixSteps; ++j) {
         const int64_t i = base + j * kRadixThreads + tid;
@@ -70,10 +96,10 @@ __global__ __launch_bounds__(kRadixThreads) void k_digit_scatter(
         if (valid && rank == 0) wcnt[wv][d] = __popcll(peers);
         __syncthreads();
         if (valid) {
-            int before = run[d] + rank;
-            for (int k = 0; k < wv; ++k) before += wcnt[k][d];
-            keys_out[before] = key;
-            vals_out[before] = vals[i];
+            int slot = run[d] + rank;
+            for (int k = 0; k < wv; ++k) slot += wcnt[k][d];
+            s_key[slot] = key;
+            s_val[slot] = vals[i];
         }
         __syncthreads();
         int add = 0;
@@ -83,6 +109,13 @@ __global__ __launch_bounds__(kRadixThreads) void k_digit_scatter(
         }
         run[tid] += add;
         __syncthreads();
+    }
+    for (int q = tid; q < tn; q += kRadixThreads) {
+        const int32_t key = s_key[q];
+        const int d = rdigit(key, shift, descending);
+        const int64_t g = offs[(int64_t)d * ntiles + blockIdx.x] + (q - start[d]);
+        keys_out[g] = key;
+        vals_out[g] = s_val[q];
     }
 }
 

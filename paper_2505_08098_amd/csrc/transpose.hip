@@ -1,9 +1,11 @@
-// Plan of the transposed pattern A^T from a plan of A, on the GPU.  A
-// symmetric pattern (checked exactly, entry by entry) has A^T = A, so its
-// plan is a copy.  Otherwise the CSR of A^T is built without atomics:
-// the plan's block bitmaps are decoded into (column, row) pairs, the pairs
-// are radix-sorted by column (radix.hip, stable), and the row pointers of
-// A^T follow from the sorted columns by binary search.  The pattern a plan holds
+// CSR of the transposed pattern A^T from a plan of A, on the GPU, without
+// atomics: the plan's block bitmaps are decoded into (column, row) pairs,
+// the pairs are radix-sorted by column (radix.hip, stable), and the row
+// pointers of A^T follow from the sorted columns by binary search.  A^T's
+// rows come out in increasing column order (the sort is stable and the
+// pairs are decoded window by window, row-ascending within a column), so
+// looking every entry of A up in its row of A^T decides exactly whether
+// A^T = A.  The pattern a plan holds
 // is A with duplicates merged (Section 3.1's bitmaps), so A^T has one entry
 // per set bit.
 #include "f3s_internal.h"
@@ -88,6 +90,15 @@ __global__ void k_rows_from_sorted(const int32_t *keys, int32_t n, int32_t N, in
     rp[c] = lo;
 }
 
+// win[b] = the window of block b; one wavefront per window.
+__global__ __launch_bounds__(256) void k_block_window(const int32_t *blk_off, int32_t T,
+                                                      int32_t *win)
+{
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= T) return;
+    for (int b = blk_off[w] + (threadIdx.x & 63); b < blk_off[w + 1]; b += 64) win[b] = w;
+}
+
 // Position of column c among the distinct columns of window v (cols padded
 // with -1 after the last one), or -1.
 __device__ int find_col(const int32_t *blk_off, const int32_t *cols, int v, int c)
@@ -103,18 +114,10 @@ __device__ int find_col(const int32_t *blk_off, const int32_t *cols, int v, int 
     return lo < kBlockCols * (blk_off[v + 1] - blk_off[v]) && list[lo] == c ? lo : -1;
 }
 
-// win[b] = the window of block b; one wavefront per window.
-__global__ __launch_bounds__(256) void k_block_window(const int32_t *blk_off, int32_t T,
-                                                      int32_t *win)
-{
-    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= T) return;
-    for (int b = blk_off[w] + (threadIdx.x & 63); b < blk_off[w + 1]; b += 64) win[b] = w;
-}
-
-// Sets *asym when some entry (r, c) of the plan's pattern has no entry (c, r):
-// for every set bit, the row r is looked up among the distinct columns of row
-// c's window and the bit of (c, r) tested.  One thread per bitmap word over
+// Sets *asym when some entry (r, c) of the plan's pattern has no entry (c, r),
+// straight from the plan (no transposed CSR needed): for every set bit, the
+// row r is looked up among the distinct columns of row c's window and the
+// bit of (c, r) tested.  One thread per bitmap word over
 // all blocks (a hub window's entries spread over many waves); stops early
 // once an asymmetry is known.
 __global__ __launch_bounds__(256) void k_check_symmetric(const int32_t *blk_off,
@@ -151,6 +154,45 @@ __global__ __launch_bounds__(256) void k_check_symmetric(const int32_t *blk_off,
     }
 }
 
+
+// Sets *asym when some entry (r, c) of the plan's pattern A is missing from
+// row r of A^T (rpt, cit; increasing columns): binary search in that short,
+// contiguous row.  A and A^T hold the same number of entries, so A inside
+// A^T means A^T = A.  One thread per bitmap word over all blocks (a hub
+// window's entries spread over many waves); stops early once an asymmetry
+// is known.
+__global__ __launch_bounds__(256) void k_check_members(const int32_t *cols,
+                                                       const uint32_t *mask,
+                                                       const int32_t *win, int64_t words,
+                                                       const int32_t *rpt, const int32_t *cit,
+                                                       int32_t *asym)
+{
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= words || *(volatile int32_t *)asym) return;
+    uint32_t m = mask[k];
+    if (!m) return;
+    const int64_t blk = k / kMaskWords;
+    const int word = (int)(k % kMaskWords);
+    const int w = win[blk];
+    while (m) {
+        const int bit = 32 * word + __ffs(m) - 1;
+        m &= m - 1;
+        const int r = w * kWindowRows + ((bit >> 2) & 15);
+        const int c = cols[kBlockCols * blk + 4 * (bit >> 6) + (bit & 3)];
+        int lo = rpt[r], hi = rpt[r + 1];
+        const int end = hi;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (cit[mid] < c) lo = mid + 1;
+            else hi = mid;
+        }
+        if (lo >= end || cit[lo] != c) {
+            atomicOr(asym, 1);
+            return;
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
@@ -167,18 +209,28 @@ hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *as
     return hipGetLastError();
 }
 
-// Scratch of launch_transpose_csr: the decoded pairs, the radix sort's two
-// buffer pairs, per-window counts and offsets, digit counts and the scans'
-// workspace.
-hipError_t transpose_scratch_bytes(const f3s_plan_s &p, size_t *bytes)
+hipError_t launch_compare_rows(const f3s_plan_s &p, const int32_t *rpt, const int32_t *cit,
+                               int32_t *win, int32_t *asym, hipStream_t s)
+{
+    if (p.T == 0 || p.n_blocks == 0) return hipSuccess;
+    k_block_window<<<(p.T + 3) / 4, 256, 0, s>>>(p.blk_off, p.T, win);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t words = (int64_t)kMaskWords * p.n_blocks;
+    k_check_members<<<(unsigned)((words + 255) / 256), 256, 0, s>>>(p.cols, p.mask, win, words,
+                                                                    rpt, cit, asym);
+    return hipGetLastError();
+}// Scratch of launch_transpose_csr: the decoded pairs (which serve as the
+// radix sort's second buffer pair), the first buffer pair, per-window counts
+// and offsets, digit counts and the scans' workspace.
+size_t transpose_scratch_bytes(const f3s_plan_s &p)
 {
     const int64_t n = p.nnz > 0 ? p.nnz : 1;
     const int64_t rc = radix_count_ints((int32_t)n);
     int64_t scan = p.T > n ? p.T : n;
     if (rc > scan) scan = rc;
     auto r = [](int64_t ints) { return (size_t)((4 * ints + 255) & ~255ll); };
-    *bytes = 6 * r(n) + 2 * r((int64_t)p.T + 1) + r(rc) + r(scan_tmp_ints(scan));
-    return hipSuccess;
+    return 4 * r(n) + 2 * r((int64_t)p.T + 1) + r(rc) + r(scan_tmp_ints(scan));
 }
 
 hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scratch_bytes,
@@ -196,12 +248,12 @@ hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scrat
         at += (4 * ints + 255) & ~255ll;
         return q;
     };
-    int32_t *keys_in = take(nn), *rows_in = take(nn);
     RadixScratch rs;
+    int32_t *keys_in = take(nn), *rows_in = take(nn);
     rs.keys_a = take(nn);
     rs.vals_a = take(nn);
-    rs.keys_b = take(nn);
-    rs.vals_b = take(nn);
+    rs.keys_b = keys_in;  // free once the first pass has read them
+    rs.vals_b = rows_in;
     int32_t *cnt = take((int64_t)T + 1), *off = take((int64_t)T + 1);
     rs.counts = take(rc);
     rs.scan_tmp = take(scan_tmp_ints(scan));

@@ -28,7 +28,8 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("f3s_plan", "f3s_plan_ws", "f3s_plan_workspace_bytes", "f3s_run",
+    for n in ("f3s_plan", "f3s_plan_ws", "f3s_plan_workspace_bytes", "f3s_plan_transpose_ws",
+              "f3s_plan_transpose_workspace_bytes", "f3s_run",
               "f3s_run_mh", "f3s_forward", "f3s_plan_transpose",
               "f3s_backward", "f3s_backward_typed", "f3s_destroy", "f3s_plan_info",
               "f3s_plan_export", "f3s_last_error", "f3s_status_string"):

@@ -91,8 +91,10 @@ def test_empty_rows_have_minus_inf_lse(gpu):
     assert np.all(np.isneginf(lse[empty])) and np.all(np.isfinite(lse[~empty]))
 
 
-@pytest.mark.parametrize("k", [1, 2, 4, 5])
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 3])
 def test_transposed_plan_is_the_plan_of_the_transpose(gpu, oracle, k):
+    """Small symmetric patterns are checked on the plan, large ones (configs 5
+    and 3, above 8 M entries) on the sorted CSR of A^T; 5 is directed."""
     c = W.make_config(k, with_features=False)
     N = c["N"]
     plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), N)
@@ -147,6 +149,13 @@ def test_transposed_plan_of_symmetric_and_nearly_symmetric_patterns(gpu, oracle,
         assert np.array_equal(got[key], b[key]), key
     same = all(np.array_equal(got[k], plan.export()[k]) for k in ("cols", "mask"))
     assert same == (not extra)
+    # the library-allocated path (f3s_plan_transpose) gives the same plan
+    L = gpu.load_library()
+    h = L.f3s_plan_transpose(plan.handle)
+    assert h
+    alt = gpu.Plan._from_handle(h, DEV, N).export()
+    for key in got:
+        assert np.array_equal(got[key], alt[key]), key
 
 
 def _bf16_dev(bits):
@@ -214,6 +223,20 @@ def test_backward_rejects_mixed_or_other_types(gpu):
     with pytest.raises(TypeError):
         qf = q.float()
         gpu.backward(plan, plan_t, qf, qf, qf, O, qf, lse)
+
+
+def test_transpose_workspace_errors(gpu):
+    rng = np.random.default_rng(9)
+    N = 200
+    rp, ci = W.random_csr(rng, N, max_deg=30)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    L = gpu.load_library()
+    need = L.f3s_plan_transpose_workspace_bytes(plan.handle)
+    assert need > 0 and L.f3s_plan_transpose_workspace_bytes(None) == 0
+    ws = torch.empty(need + 512, dtype=torch.uint8, device=DEV)
+    for ptr, size in ((ws.data_ptr(), need - 256), (ws.data_ptr() + 4, need), (None, need)):
+        assert not L.f3s_plan_transpose_ws(plan.handle, ptr, size)
+        assert L.f3s_last_error() == 1  # F3S_ERR_INVALID_VALUE
 
 
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
