@@ -55,6 +55,43 @@ __device__ __forceinline__ int wave_excl_scan(int v, int lane, int *total)
     return incl - v;
 }
 
+// Compare-exchange of x with the x of lane ^ lj (lj a power of two below
+// 64): the smaller of the two if take_min, else the larger.  The partner's
+// value comes from cross-lane moves that stay in the vector ALU: DPP quad
+// permutations (lj = 1, 2) and row rotations (lj = 4, 8; rotation by n
+// within 16 lanes delivers lane i - n, probed on the GPU), and the gfx950
+// permlane swaps (lj = 16, 32), which give each lane the pair of its own and
+// its partner's value in some order; min and max do not depend on it.  lj
+// is a constant once the sorting network is unrolled.
+__device__ __forceinline__ int xchg_lanes(int x, int lj, int lane, bool take_min)
+{
+    int a = x, b;
+    switch (lj) {
+    case 1: b = __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false); break;  // [1,0,3,2]
+    case 2: b = __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false); break;  // [2,3,0,1]
+    case 4: {
+        const int from_below = __builtin_amdgcn_mov_dpp(x, 0x124, 0xF, 0xF, false);  // i - 4
+        const int from_above = __builtin_amdgcn_mov_dpp(x, 0x12C, 0xF, 0xF, false);  // i + 4
+        b = (lane & 4) ? from_below : from_above;
+        break;
+    }
+    case 8: b = __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false); break;  // i +- 8
+    case 16: {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        a = (int)r[0];
+        b = (int)r[1];
+        break;
+    }
+    default: {
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        a = (int)r[0];
+        b = (int)r[1];
+        break;
+    }
+    }
+    return take_min ? min(a, b) : max(a, b);
+}
+
 // Bitonic sorting network, ascending, over the 64*E keys of one wavefront:
 // key t = E*lane + i sits in x[i] of lane `lane`.  Compare distances below E
 // stay inside a lane, larger ones pair lanes lane and lane ^ (j/E).
@@ -70,8 +107,7 @@ __device__ __forceinline__ void wave_bitonic(int (&x)[E], int lane)
 #pragma unroll
                 for (int i = 0; i < E; ++i) {
                     const bool up = ((E * lane + i) & k) == 0;
-                    const int o = __shfl_xor(x[i], j / E);
-                    x[i] = lower == up ? min(x[i], o) : max(x[i], o);
+                    x[i] = xchg_lanes(x[i], j / E, lane, lower == up);
                 }
             } else {
 #pragma unroll
@@ -155,12 +191,12 @@ __device__ void window_wave(const int32_t *col_idx, int32_t N, int32_t w, int32_
         int row = 0;
 #pragma unroll
         for (int r = 1; r < kWindowRows; ++r) row += beg + e >= starts[r - 1];
-        int lo = 0, hi = total;
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (s_cols[mid] < c) lo = mid + 1;
-            else hi = mid;
-        }
+        // position of c in the distinct list (it is there): a fixed-step,
+        // branch-free search, so the E searches of a lane interleave
+        int lo = 0;
+#pragma unroll
+        for (int step = 32 * E; step > 0; step >>= 1)
+            if (lo + step <= total && s_cols[lo + step - 1] < c) lo += step;
         if (lo >= total) continue;  // every valid column is in the list
         const int cc = lo % kBlockCols;
         const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
