@@ -264,8 +264,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
     HIP_TRY(launch_window_wave(row_ptr, col_idx, N, T, tmp_cols, tmp_mask, u, is_big,
                                is_heavy, bits, &st->err, s));
-    HIP_TRY(launch_scan(is_big, big_pos, T, scan_tmp, &st->n_big, s));
-    HIP_TRY(launch_scan(is_heavy, heavy_pos, T, scan_tmp, &st->n_heavy, s));
+    HIP_TRY(launch_scan2(is_big, big_pos, &st->n_big, is_heavy, heavy_pos, &st->n_heavy, T,
+                         scan_tmp, s));
     HIP_TRY(launch_compact_lists(is_big, big_pos, is_heavy, heavy_pos, T, big, heavy, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
@@ -283,8 +283,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_bin_keys(nb, T, &st->n_blocks, &st->max_blocks,
                             env_int("F3S_PIECE_BLOCKS", 0), slots, reorder,
                             &st->piece, npieces, key, split_pieces, split_one, s));
-    HIP_TRY(launch_scan(split_pieces, split_pieces, T, scan_tmp, &st->n_pieces, s));
-    HIP_TRY(launch_scan(split_one, split_one, T, scan_tmp, &st->n_split, s));
+    HIP_TRY(launch_scan2(split_pieces, split_pieces, &st->n_pieces, split_one, split_one,
+                         &st->n_split, T, scan_tmp, s));
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
     const int32_t B = hs.n_blocks;

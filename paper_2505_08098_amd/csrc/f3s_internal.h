@@ -67,6 +67,17 @@ struct f3s_plan_s {
 
 namespace f3s {
 
+// Inclusive sum over the lanes of a wavefront (device code).
+__device__ __forceinline__ int wave_inclusive_sum(int x, int lane)
+{
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(x, off, 64);
+        if (lane >= off) x += t;
+    }
+    return x;
+}
+
 // ---- plan kernels (plan_kernels.hip) ------------------------------------
 hipError_t launch_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
                                 int32_t *err, hipStream_t s);
@@ -109,6 +120,10 @@ hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
 int64_t scan_tmp_ints(int64_t n);
 hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
                        int32_t *total_out, hipStream_t s);
+// Two independent scans of n ints each (one launch when n is small).
+hipError_t launch_scan2(const int32_t *in0, int32_t *out0, int32_t *total0,
+                        const int32_t *in1, int32_t *out1, int32_t *total1, int32_t n,
+                        int32_t *tmp, hipStream_t s);
 // Padded column lists and block bitmaps of the plan from the staging areas.
 hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,
                                const uint32_t *tmp_mask, const int32_t *u,

@@ -625,71 +625,87 @@ __global__ __launch_bounds__(kStatThreads) void k_window_stats(
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanThreads * kScanItems;
+// Up to this many elements the tile totals fit one workgroup's threads.
+constexpr int64_t kScanTwoPass = (int64_t)kScanTile * kScanThreads;
 
-// Exclusive scan of one tile of kScanTile ints per workgroup, in place or
-// not; the tile's total goes to tile_sums[tile] (when given).  With one
-// workgroup and n > kScanTile it walks the tiles in order with a carry
-// (used for the short array of tile totals), and writes out[n] = total.
-__global__ __launch_bounds__(kScanThreads) void k_scan(const int32_t *in, int32_t *out,
-                                                       int32_t n, int32_t *tile_sums,
-                                                       int32_t *total_out)
+struct ScanArray {
+    const int32_t *in;
+    int32_t *out;
+    int32_t *total;      // may be null
+    int32_t *tile_sums;  // one int per tile (several tiles only)
+};
+
+// tile_sums[tile] = sum of the tile's elements.  blockIdx.y selects one of
+// two independent arrays.
+__global__ __launch_bounds__(kScanThreads) void k_scan_reduce(ScanArray a0, ScanArray a1,
+                                                              int32_t n)
 {
-    __shared__ int32_t sh[kScanThreads];
-    const int tid = threadIdx.x;
-    const bool whole = gridDim.x == 1;
-    int carry = 0;
-    const int64_t first = whole ? 0 : (int64_t)blockIdx.x * kScanTile;
-    const int64_t last = whole ? n : min((int64_t)n, first + kScanTile);
-    for (int64_t base = first; base < last; base += kScanTile) {
-        int v[kScanItems];
-        int s = 0;
-        for (int j = 0; j < kScanItems; ++j) {
-            const int64_t idx = base + (int64_t)tid * kScanItems + j;
-            v[j] = idx < last ? in[idx] : 0;
-            s += v[j];
-        }
-        sh[tid] = s;
-        __syncthreads();
-        for (int off = 1; off < kScanThreads; off <<= 1) {
-            int t = tid >= off ? sh[tid - off] : 0;
-            __syncthreads();
-            sh[tid] += t;
-            __syncthreads();
-        }
-        int run = carry + sh[tid] - s;
-        const int tile_total = sh[kScanThreads - 1];
-        __syncthreads();
-        for (int j = 0; j < kScanItems; ++j) {
-            const int64_t idx = base + (int64_t)tid * kScanItems + j;
-            if (idx < last) out[idx] = run;
-            run += v[j];
-        }
-        carry += tile_total;
-    }
+    const ScanArray a = blockIdx.y ? a1 : a0;
+    __shared__ int32_t wave_sum[kScanThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int64_t first = ((int64_t)blockIdx.x * kScanThreads + tid) * kScanItems;
+    int own = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) own += first + j < n ? a.in[first + j] : 0;
+    const int incl = wave_inclusive_sum(own, lane);
+    if (lane == 63) wave_sum[wv] = incl;
+    __syncthreads();
     if (tid == 0) {
-        if (whole) {
-            out[n] = carry;
-            if (total_out) *total_out = carry;
-        } else {
-            tile_sums[blockIdx.x] = carry;
-        }
+        int t = 0;
+        for (int k = 0; k < kScanThreads / 64; ++k) t += wave_sum[k];
+        a.tile_sums[blockIdx.x] = t;
     }
 }
 
-// Adds the scanned tile offsets to every tile after the first and writes
-// the total.
-__global__ __launch_bounds__(256) void k_scan_add(int32_t *out, int32_t n,
-                                                  const int32_t *tile_offs, int32_t ntiles,
-                                                  int32_t *total_out)
+enum ScanCarry { kCarryNone, kCarrySumBefore, kCarryScanned };
+
+// Exclusive scan of one tile of kScanThreads * K ints per workgroup, in
+// place or not: thread t owns K consecutive elements, so one wavefront sum
+// and one barrier cover the tile.  The carry into the tile is 0 (a single
+// tile), the sum of the totals of the tiles before it (at most kScanThreads
+// of them), or the tile's entry of the already scanned totals.  The last
+// tile writes out[n] = total (and *total).  blockIdx.y selects one of two
+// independent arrays.
+template <int K, ScanCarry C>
+__global__ __launch_bounds__(kScanThreads) void k_scan(ScanArray a0, ScanArray a1, int32_t n)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) {
-        const int64_t tile = i / kScanTile;
-        if (tile > 0) out[i] += tile_offs[tile];
+    const ScanArray a = blockIdx.y ? a1 : a0;
+    __shared__ int32_t wave_sum[kScanThreads / 64], wave_carry[kScanThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int64_t first = ((int64_t)blockIdx.x * kScanThreads + tid) * K;
+    int v[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) v[j] = first + j < n ? a.in[first + j] : 0;
+    int carry_part = 0;
+    if (C == kCarrySumBefore && tid < (int)blockIdx.x) carry_part = a.tile_sums[tid];
+    int own = 0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) own += v[j];
+    const int incl = wave_inclusive_sum(own, lane);
+    if (lane == 63) wave_sum[wv] = incl;
+    if (C == kCarrySumBefore) {
+        const int c = wave_inclusive_sum(carry_part, lane);
+        if (lane == 63) wave_carry[wv] = c;
     }
-    if (i == 0) {
-        out[n] = tile_offs[ntiles];
-        if (total_out) *total_out = tile_offs[ntiles];
+    __syncthreads();
+    int before = 0, total = 0, carry = 0;
+#pragma unroll
+    for (int k = 0; k < kScanThreads / 64; ++k) {
+        const int t = wave_sum[k];
+        before += k < wv ? t : 0;
+        total += t;
+        if (C == kCarrySumBefore) carry += wave_carry[k];
+    }
+    if (C == kCarryScanned) carry = a.tile_sums[blockIdx.x];
+    int run = carry + before + incl - own;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        if (first + j < n) a.out[first + j] = run;
+        run += v[j];
+    }
+    if (tid == 0 && blockIdx.x == gridDim.x - 1) {
+        a.out[n] = carry + total;
+        if (a.total) *a.total = carry + total;
     }
 }
 
@@ -881,27 +897,61 @@ hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
     return hipGetLastError();
 }
 
-// Up to kScanWhole elements one workgroup walks the tiles in order (one
-// launch); above, the tiles are scanned in parallel (three launches).
-constexpr int64_t kScanWhole = 8 * (int64_t)kScanTile;
-
+// Up to one tile: one launch of one workgroup.  Up to kScanTwoPass: the
+// tile totals, then every tile scanned with the sum of the totals before it
+// (two launches).  Above: the tile totals, their own scan, then the tiles.
 int64_t scan_tmp_ints(int64_t n)
 {
-    return n <= kScanWhole ? 1 : (n + kScanTile - 1) / kScanTile + 1;
+    const int64_t ntiles = (n + kScanTile - 1) / kScanTile;
+    if (n <= kScanTile) return 1;
+    if (n <= kScanTwoPass) return 2 * ntiles;
+    return ntiles + 1 + scan_tmp_ints(ntiles);
+}
+
+hipError_t launch_scan_pair(ScanArray a0, ScanArray a1, int arrays, int32_t n,
+                            hipStream_t s)
+{
+    const int32_t ntiles = (int32_t)((n + kScanTile - 1) / kScanTile);
+    if (n <= kScanThreads) {
+        k_scan<1, kCarryNone><<<dim3(1, arrays), kScanThreads, 0, s>>>(a0, a1, n);
+    } else if (n <= kScanTile) {
+        k_scan<kScanItems, kCarryNone><<<dim3(1, arrays), kScanThreads, 0, s>>>(a0, a1, n);
+    } else {
+        k_scan_reduce<<<dim3(ntiles, arrays), kScanThreads, 0, s>>>(a0, a1, n);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        k_scan<kScanItems, kCarrySumBefore>
+            <<<dim3(ntiles, arrays), kScanThreads, 0, s>>>(a0, a1, n);
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
                        int32_t *total_out, hipStream_t s)
 {
-    if (n <= kScanWhole) {
-        k_scan<<<1, kScanThreads, 0, s>>>(in, out, n, nullptr, total_out);
-        return hipGetLastError();
-    }
+    ScanArray a{in, out, total_out, tmp};
+    if (n <= kScanTwoPass) return launch_scan_pair(a, a, 1, n, s);
     const int32_t ntiles = (int32_t)((n + kScanTile - 1) / kScanTile);
-    k_scan<<<ntiles, kScanThreads, 0, s>>>(in, out, n, tmp, nullptr);
-    k_scan<<<1, kScanThreads, 0, s>>>(tmp, tmp, ntiles, nullptr, nullptr);
-    k_scan_add<<<grid_for(n, 256), 256, 0, s>>>(out, n, tmp, ntiles, total_out);
+    k_scan_reduce<<<ntiles, kScanThreads, 0, s>>>(a, a, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_scan(tmp, tmp, ntiles, tmp + ntiles + 1, nullptr, s);
+    if (e != hipSuccess) return e;
+    k_scan<kScanItems, kCarryScanned><<<ntiles, kScanThreads, 0, s>>>(a, a, n);
     return hipGetLastError();
+}
+
+hipError_t launch_scan2(const int32_t *in0, int32_t *out0, int32_t *total0,
+                        const int32_t *in1, int32_t *out1, int32_t *total1, int32_t n,
+                        int32_t *tmp, hipStream_t s)
+{
+    if (n <= kScanTwoPass) {
+        const int64_t ntiles = (n + kScanTile - 1) / kScanTile;
+        return launch_scan_pair(ScanArray{in0, out0, total0, tmp},
+                                ScanArray{in1, out1, total1, tmp + ntiles}, 2, n, s);
+    }
+    hipError_t e = launch_scan(in0, out0, n, tmp, total0, s);
+    return e != hipSuccess ? e : launch_scan(in1, out1, n, tmp, total1, s);
 }
 
 hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,

@@ -2,7 +2,7 @@
 // keys in [0, max_key], ascending or descending, with 8-bit digits (one pass
 // per 8 bits of max_key): per tile of kTile keys a digit histogram, one scan
 // over (digit, tile), then a stable scatter in which each tile ranks its keys
-// (in order, 256 at a time, equal digits by wavefront ballots) into digit
+// (each wavefront its quarter, in order, equal digits by ballots) into digit
 // order in LDS and writes them out run by run.
 #include "f3s_internal.h"
 
@@ -28,93 +28,104 @@ __global__ __launch_bounds__(kRadixThreads) void k_digit_count(const int32_t *ke
 {
     __shared__ int32_t h[256];
     const int tid = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * kTile + tid;
+    int32_t key[kRadixSteps];
+#pragma unroll
+    for (int j = 0; j < kRadixSteps; ++j) {
+        const int64_t i = base + j * kRadixThreads;
+        key[j] = i < n ? keys[i] : 0;
+    }
     h[tid] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kTile;
-    for (int j = 0; j < kRadixSteps; ++j) {
-        const int64_t i = base + j * kRadixThreads + tid;
-        if (i < n) atomicAdd(&h[rdigit(keys[i], shift, descending)], 1);
-    }
+#pragma unroll
+    for (int j = 0; j < kRadixSteps; ++j)
+        if (base + j * kRadixThreads < n) atomicAdd(&h[rdigit(key[j], shift, descending)], 1);
     __syncthreads();
     counts[(int64_t)tid * ntiles + blockIdx.x] = h[tid];
 }
 
-// Stable scatter of one tile.  The tile's keys are first placed in LDS in
-// digit order: taken in index order, 256 per step, a key's rank among equal
-// digits comes from ballots (within its wavefront) and the counts of the
-// earlier wavefronts of the step.  Then the tile is written out in that
-// order, so each digit's run of keys goes to consecutive addresses.
+// Stable scatter of one tile.  Wavefront w holds elements [1024 w,
+// 1024 (w + 1)) of the tile in registers (lane l has elements 64 j + l) and
+// ranks them in order without barriers: per 64 keys, a key's rank among
+// equal digits comes from ballots, added to the wave's running count of that
+// digit in LDS.  One scan over the digits then gives each wave the first
+// slot of each digit, the tile is placed in LDS in digit order and written
+// out run by run, so each digit's keys go to consecutive addresses.
 __global__ __launch_bounds__(kRadixThreads) void k_digit_scatter(
     const int32_t *keys, const int32_t *vals, int32_t n, int shift, bool descending,
     int32_t ntiles, const int32_t *offs, int32_t *keys_out, int32_t *vals_out)
 {
     constexpr int kWaves = kRadixThreads / 64;
+    constexpr int kPerWave = kTile / kWaves;
     __shared__ int32_t s_key[kTile], s_val[kTile];  // the tile in digit order
+    __shared__ int32_t wave_digit[kWaves][256];     // count, then first slot, per wave and digit
     __shared__ int32_t start[256];                  // first slot of each digit
-    __shared__ int32_t run[256];                    // next free slot of each digit
-    __shared__ int32_t wcnt[kWaves][256];           // this step's count per wave, digit
+    __shared__ int32_t wave_sum[kWaves];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int64_t base = (int64_t)blockIdx.x * kTile;
     const int tn = (int)min((int64_t)kTile, (int64_t)n - base);
-    run[tid] = 0;
-    for (int k = 0; k < kWaves; ++k) wcnt[k][tid] = 0;
-    __syncthreads();
+    const int q0 = wv * kPerWave + lane;
+    int32_t key[kRadixSteps], val[kRadixSteps], rank[kRadixSteps];
+#pragma unroll
     for (int j = 0; j < kRadixSteps; ++j) {
-        const int64_t i = base + j * kRadixThreads + tid;
-        if (i < n) atomicAdd(&run[rdigit(keys[i], shift, descending)], 1);
+        const int q = q0 + 64 * j;
+        key[j] = q < tn ? keys[base + q] : 0;
+        val[j] = q < tn ? vals[base + q] : 0;
     }
-    __syncthreads();
-    // exclusive scan of the tile's digit counts
-    const int cnt = run[tid];
-    start[tid] = cnt;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-        const int t = tid >= off ? start[tid - off] : 0;
-        __syncthreads();
-        start[tid] += t;
-        __syncthreads();
-    }
-    const int excl = start[tid] - cnt;
-    __syncthreads();
-    start[tid] = excl;
-    run[tid] = excl;
-    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) wave_digit[wv][lane + 64 * k] = 0;
     const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
     for (int j = 0; j < kRadixSteps; ++j) {
-        const int64_t i = base + j * kRadixThreads + tid;
-        const bool valid = i < n;
-        const int32_t key = valid ? keys[i] : 0;
-        const int d = valid ? rdigit(key, shift, descending) : 0;
-        // lanes of this wave holding the same digit
+        const bool valid = q0 + 64 * j < tn;
+        const int d = rdigit(key[j], shift, descending);
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
             const uint64_t bal = __ballot(valid && ((d >> b) & 1));
             peers &= ((d >> b) & 1) ? bal : ~bal;
         }
-        const int rank = __popcll(peers & below);
-        if (valid && rank == 0) wcnt[wv][d] = __popcll(peers);
-        __syncthreads();
-        if (valid) {
-            int slot = run[d] + rank;
-            for (int k = 0; k < wv; ++k) slot += wcnt[k][d];
-            s_key[slot] = key;
-            s_val[slot] = vals[i];
-        }
-        __syncthreads();
-        int add = 0;
-        for (int k = 0; k < kWaves; ++k) {
-            add += wcnt[k][tid];
-            wcnt[k][tid] = 0;
-        }
-        run[tid] += add;
-        __syncthreads();
+        const int r = __popcll(peers & below);
+        // a wave's LDS accesses take effect in program order, so every lane
+        // reads the count before the digit's first lane updates it
+        const int prior = valid ? wave_digit[wv][d] : 0;
+        rank[j] = prior + r;
+        if (valid && r == 0) wave_digit[wv][d] = prior + __popcll(peers);
     }
+    __syncthreads();
+    // thread t: digit t's count over the tile, its first slot, each wave's
+    int c[kWaves], tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        c[w] = wave_digit[w][tid];
+        tot += c[w];
+    }
+    const int incl = wave_inclusive_sum(tot, lane);
+    if (lane == 63) wave_sum[wv] = incl;
+    __syncthreads();
+    int first = incl - tot;
+    for (int w = 0; w < wv; ++w) first += wave_sum[w];
+    start[tid] = first;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        wave_digit[w][tid] = first;
+        first += c[w];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kRadixSteps; ++j) {
+        if (q0 + 64 * j < tn) {
+            const int slot = wave_digit[wv][rdigit(key[j], shift, descending)] + rank[j];
+            s_key[slot] = key[j];
+            s_val[slot] = val[j];
+        }
+    }
+    __syncthreads();
     for (int q = tid; q < tn; q += kRadixThreads) {
-        const int32_t key = s_key[q];
-        const int d = rdigit(key, shift, descending);
+        const int32_t k = s_key[q];
+        const int d = rdigit(k, shift, descending);
         const int64_t g = offs[(int64_t)d * ntiles + blockIdx.x] + (q - start[d]);
-        keys_out[g] = key;
+        keys_out[g] = k;
         vals_out[g] = s_val[q];
     }
 }

@@ -73,6 +73,31 @@ def test_plan_heavy_window_above_lds_capacity(gpu, oracle):
     assert info["max_blocks"] > 256
 
 
+def test_plan_more_windows_than_one_scan_tile(gpu, oracle):
+    """81,250 windows, more than one scan workgroup covers (65,536), so the
+    scans over windows take the tiled path (tiles, their totals, the add)."""
+    rng = np.random.default_rng(5)
+    N = 1_300_000
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum(rng.integers(0, 4, size=N))
+    ci = rng.integers(0, N, size=int(rp[-1])).astype(np.int32)
+    info = _check_plan_against_oracle(gpu, oracle, rp, ci, N)
+    assert info["n_windows"] > 65536
+
+
+def test_plan_more_windows_than_two_scan_passes(gpu, oracle):
+    """4.2 M windows, more than a two-pass scan covers (1024 tiles of 4096
+    elements = 4,194,304), so the scans over windows scan their tile totals
+    separately (three launches)."""
+    rng = np.random.default_rng(6)
+    N = 67_200_000
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum(rng.integers(0, 2, size=N, dtype=np.int32))
+    ci = rng.integers(0, N, size=int(rp[-1]), dtype=np.int32)
+    info = _check_plan_against_oracle(gpu, oracle, rp, ci, N)
+    assert info["n_windows"] > 4_194_304
+
+
 def _windows_of_sizes(rng, sizes, N, dup_frac=0.3):
     """CSR whose window w holds sizes[w] entries spread over its 16 rows, with
     duplicates and unsorted columns; the remaining rows are empty."""
