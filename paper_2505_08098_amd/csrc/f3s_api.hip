@@ -202,7 +202,6 @@ void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz)
     for (int32_t **q : per_window1) *q = carve<int32_t>(a, take, (int64_t)T + 1);
     const int64_t rc = radix_count_ints(T);
     b.scan_tmp = carve<int32_t>(a, take, scan_tmp_ints(T > rc ? T : rc));
-    b.wl.windows = carve<int32_t>(a, take, T);
     b.wl.pos = carve<int32_t>(a, take, (int64_t)T + 1);
     int32_t **radix_arrays[] = {&b.wl.radix.keys_a, &b.wl.radix.vals_a, &b.wl.radix.keys_b,
                                 &b.wl.radix.vals_b};
@@ -264,9 +263,18 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
     HIP_TRY(launch_window_wave(row_ptr, col_idx, N, T, tmp_cols, tmp_mask, u, is_big,
                                is_heavy, bits, &st->err, s));
-    HIP_TRY(launch_scan2(is_big, big_pos, &st->n_big, is_heavy, heavy_pos, &st->n_heavy, T,
-                         scan_tmp, s));
-    HIP_TRY(launch_compact_lists(is_big, big_pos, is_heavy, heavy_pos, T, big, heavy, s));
+    {  // the flagged windows listed in window order
+        ScanArray fb, fh;
+        fb.in = is_big;
+        fb.out = big_pos;
+        fb.total = &st->n_big;
+        fb.list = big;
+        fh.in = is_heavy;
+        fh.out = heavy_pos;
+        fh.total = &st->n_heavy;
+        fh.list = heavy;
+        HIP_TRY(launch_scan2(fb, fh, T, scan_tmp, s));
+    }
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
     HIP_TRY(launch_window_sort(row_ptr, col_idx, N, big, hs.n_big, tmp_cols, tmp_mask, u,
@@ -283,8 +291,14 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_bin_keys(nb, T, &st->n_blocks, &st->max_blocks,
                             env_int("F3S_PIECE_BLOCKS", 0), slots, reorder,
                             &st->piece, npieces, key, split_pieces, split_one, s));
-    HIP_TRY(launch_scan2(split_pieces, split_pieces, &st->n_pieces, split_one, split_one,
-                         &st->n_split, T, scan_tmp, s));
+    {
+        ScanArray sp, so;
+        sp.in = sp.out = split_pieces;
+        sp.total = &st->n_pieces;
+        so.in = so.out = split_one;
+        so.total = &st->n_split;
+        HIP_TRY(launch_scan2(sp, so, T, scan_tmp, s));
+    }
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
     const int32_t B = hs.n_blocks;

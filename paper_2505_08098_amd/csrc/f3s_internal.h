@@ -91,10 +91,6 @@ hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, in
                               int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
                               int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits,
                               int32_t *err, hipStream_t s);
-// The flagged windows listed in window order (positions: scans of the flags).
-hipError_t launch_compact_lists(const int32_t *is_big, const int32_t *big_pos,
-                                const int32_t *is_heavy, const int32_t *heavy_pos,
-                                int32_t T, int32_t *big, int32_t *heavy, hipStream_t s);
 // The windows big[0 .. n_big): sorted distinct columns, u, bitmaps and bits
 // as above (one wavefront with 16 keys per lane up to 1024 entries, else an
 // LDS sort).
@@ -114,16 +110,25 @@ hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
                                int32_t *nb, unsigned long long *sum_u,
                                unsigned long long *sum_bits, int32_t *sum_nb,
                                int32_t *max_nb, hipStream_t s);
-// Exclusive scan of n int32 into out[0..n], out[n] = total (in == out ok);
-// tmp: scan_tmp_ints(n) ints of workspace; total_out (may be null) also
-// receives the total.
+// Exclusive scan of n int32 into out[0..n], out[n] = total (in == out ok).
+// Element i is in[i], or in[gather[i]] when gather is given.  With list
+// given, every nonzero element i is also listed: list[out[i]] = i (flag
+// compaction).  total (may be null) also receives the total.
+struct ScanArray {
+    const int32_t *in = nullptr;
+    const int32_t *gather = nullptr;
+    int32_t *out = nullptr;
+    int32_t *total = nullptr;
+    int32_t *list = nullptr;
+    int32_t *tile_sums = nullptr;  // set by the launcher (from tmp)
+};
+// tmp: scan_tmp_ints(n) ints of workspace.
 int64_t scan_tmp_ints(int64_t n);
+hipError_t launch_scan(ScanArray a, int32_t n, int32_t *tmp, hipStream_t s);
 hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
                        int32_t *total_out, hipStream_t s);
 // Two independent scans of n ints each (one launch when n is small).
-hipError_t launch_scan2(const int32_t *in0, int32_t *out0, int32_t *total0,
-                        const int32_t *in1, int32_t *out1, int32_t *total1, int32_t n,
-                        int32_t *tmp, hipStream_t s);
+hipError_t launch_scan2(ScanArray a0, ScanArray a1, int32_t n, int32_t *tmp, hipStream_t s);
 // Padded column lists and block bitmaps of the plan from the staging areas.
 hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,
                                const uint32_t *tmp_mask, const int32_t *u,
@@ -146,8 +151,10 @@ hipError_t launch_split_items(const int32_t *merges, const int32_t *split_item,
 
 // ---- radix sort (radix.hip) -------------------------------------------------
 // Stable sort of n (key, value) int32 pairs, keys in [0, max_key], ascending
-// or descending; the inputs are not written; the results end up in one of
-// the two scratch pairs (*keys_out, *vals_out say which).
+// or descending; vals == nullptr stands for the values 0 .. n-1 (the sort
+// then yields the sorting permutation).  The inputs are not written; the
+// results end up in one of the two scratch pairs (*keys_out, *vals_out say
+// which).
 struct RadixScratch {
     int32_t *keys_a, *vals_a, *keys_b, *vals_b;  // [n] each
     int32_t *counts;                              // radix_count_ints(n)
@@ -161,7 +168,6 @@ hipError_t launch_radix_pairs(const int32_t *keys, const int32_t *vals, int32_t 
 
 // ---- work list (worklist.hip) ----------------------------------------------
 struct WorkListScratch {
-    int32_t *windows;    // [T]: 0 .. T-1
     int32_t *pos;        // [T + 1] first item of each window in sorted order
     RadixScratch radix;  // for n = T
 };

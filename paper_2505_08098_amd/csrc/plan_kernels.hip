@@ -289,18 +289,6 @@ __global__ __launch_bounds__(64) void k_window_wave16(
                     u, bits_out, err);
 }
 
-// big[big_pos[w]] = w and heavy[heavy_pos[w]] = w for the flagged windows
-// (positions: exclusive scans of the flags), in window order.
-__global__ void k_compact_lists(const int32_t *is_big, const int32_t *big_pos,
-                                const int32_t *is_heavy, const int32_t *heavy_pos,
-                                int32_t T, int32_t *big, int32_t *heavy)
-{
-    const int w = blockIdx.x * blockDim.x + threadIdx.x;
-    if (w >= T) return;
-    if (is_big[w] && big_pos[w] < T) big[big_pos[w]] = w;
-    if (is_heavy[w] && heavy_pos[w] < T) heavy[heavy_pos[w]] = w;
-}
-
 __global__ void k_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
                                 int32_t *err)
 {
@@ -628,12 +616,10 @@ constexpr int kScanTile = kScanThreads * kScanItems;
 // Up to this many elements the tile totals fit one workgroup's threads.
 constexpr int64_t kScanTwoPass = (int64_t)kScanTile * kScanThreads;
 
-struct ScanArray {
-    const int32_t *in;
-    int32_t *out;
-    int32_t *total;      // may be null
-    int32_t *tile_sums;  // one int per tile (several tiles only)
-};
+__device__ __forceinline__ int scan_element(const ScanArray &a, int64_t i)
+{
+    return a.gather ? a.in[a.gather[i]] : a.in[i];
+}
 
 // tile_sums[tile] = sum of the tile's elements.  blockIdx.y selects one of
 // two independent arrays.
@@ -646,7 +632,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_reduce(ScanArray a0, Scan
     const int64_t first = ((int64_t)blockIdx.x * kScanThreads + tid) * kScanItems;
     int own = 0;
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) own += first + j < n ? a.in[first + j] : 0;
+    for (int j = 0; j < kScanItems; ++j) own += first + j < n ? scan_element(a, first + j) : 0;
     const int incl = wave_inclusive_sum(own, lane);
     if (lane == 63) wave_sum[wv] = incl;
     __syncthreads();
@@ -664,8 +650,8 @@ enum ScanCarry { kCarryNone, kCarrySumBefore, kCarryScanned };
 // and one barrier cover the tile.  The carry into the tile is 0 (a single
 // tile), the sum of the totals of the tiles before it (at most kScanThreads
 // of them), or the tile's entry of the already scanned totals.  The last
-// tile writes out[n] = total (and *total).  blockIdx.y selects one of two
-// independent arrays.
+// tile writes out[n] = total (and *total).  Nonzero elements are listed when
+// a list is given.  blockIdx.y selects one of two independent arrays.
 template <int K, ScanCarry C>
 __global__ __launch_bounds__(kScanThreads) void k_scan(ScanArray a0, ScanArray a1, int32_t n)
 {
@@ -675,7 +661,7 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(ScanArray a0, ScanArray a
     const int64_t first = ((int64_t)blockIdx.x * kScanThreads + tid) * K;
     int v[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) v[j] = first + j < n ? a.in[first + j] : 0;
+    for (int j = 0; j < K; ++j) v[j] = first + j < n ? scan_element(a, first + j) : 0;
     int carry_part = 0;
     if (C == kCarrySumBefore && tid < (int)blockIdx.x) carry_part = a.tile_sums[tid];
     int own = 0;
@@ -700,7 +686,10 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(ScanArray a0, ScanArray a
     int run = carry + before + incl - own;
 #pragma unroll
     for (int j = 0; j < K; ++j) {
-        if (first + j < n) a.out[first + j] = run;
+        if (first + j < n) {
+            a.out[first + j] = run;
+            if (a.list && v[j] && run < n) a.list[run] = (int32_t)(first + j);
+        }
         run += v[j];
     }
     if (tid == 0 && blockIdx.x == gridDim.x - 1) {
@@ -850,16 +839,6 @@ hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, in
     return hipGetLastError();
 }
 
-hipError_t launch_compact_lists(const int32_t *is_big, const int32_t *big_pos,
-                                const int32_t *is_heavy, const int32_t *heavy_pos,
-                                int32_t T, int32_t *big, int32_t *heavy, hipStream_t s)
-{
-    if (T == 0) return hipSuccess;
-    k_compact_lists<<<grid_for(T, 256), 256, 0, s>>>(is_big, big_pos, is_heavy, heavy_pos,
-                                                     T, big, heavy);
-    return hipGetLastError();
-}
-
 hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
                               int32_t N, const int32_t *big, int32_t n_big,
                               int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
@@ -926,10 +905,9 @@ hipError_t launch_scan_pair(ScanArray a0, ScanArray a1, int arrays, int32_t n,
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
-                       int32_t *total_out, hipStream_t s)
+hipError_t launch_scan(ScanArray a, int32_t n, int32_t *tmp, hipStream_t s)
 {
-    ScanArray a{in, out, total_out, tmp};
+    a.tile_sums = tmp;
     if (n <= kScanTwoPass) return launch_scan_pair(a, a, 1, n, s);
     const int32_t ntiles = (int32_t)((n + kScanTile - 1) / kScanTile);
     k_scan_reduce<<<ntiles, kScanThreads, 0, s>>>(a, a, n);
@@ -941,17 +919,25 @@ hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
     return hipGetLastError();
 }
 
-hipError_t launch_scan2(const int32_t *in0, int32_t *out0, int32_t *total0,
-                        const int32_t *in1, int32_t *out1, int32_t *total1, int32_t n,
-                        int32_t *tmp, hipStream_t s)
+hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
+                       int32_t *total_out, hipStream_t s)
+{
+    ScanArray a;
+    a.in = in;
+    a.out = out;
+    a.total = total_out;
+    return launch_scan(a, n, tmp, s);
+}
+
+hipError_t launch_scan2(ScanArray a0, ScanArray a1, int32_t n, int32_t *tmp, hipStream_t s)
 {
     if (n <= kScanTwoPass) {
-        const int64_t ntiles = (n + kScanTile - 1) / kScanTile;
-        return launch_scan_pair(ScanArray{in0, out0, total0, tmp},
-                                ScanArray{in1, out1, total1, tmp + ntiles}, 2, n, s);
+        a0.tile_sums = tmp;
+        a1.tile_sums = tmp + (n + kScanTile - 1) / kScanTile;
+        return launch_scan_pair(a0, a1, 2, n, s);
     }
-    hipError_t e = launch_scan(in0, out0, n, tmp, total0, s);
-    return e != hipSuccess ? e : launch_scan(in1, out1, n, tmp, total1, s);
+    hipError_t e = launch_scan(a0, n, tmp, s);
+    return e != hipSuccess ? e : launch_scan(a1, n, tmp, s);
 }
 
 hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,

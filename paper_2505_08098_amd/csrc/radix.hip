@@ -70,7 +70,7 @@ __global__ __launch_bounds__(kRadixThreads) void k_digit_scatter(
     for (int j = 0; j < kRadixSteps; ++j) {
         const int q = q0 + 64 * j;
         key[j] = q < tn ? keys[base + q] : 0;
-        val[j] = q < tn ? vals[base + q] : 0;
+        val[j] = q < tn ? (vals ? vals[base + q] : (int32_t)(base + q)) : 0;
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) wave_digit[wv][lane + 64 * k] = 0;

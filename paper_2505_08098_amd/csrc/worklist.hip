@@ -8,19 +8,6 @@
 namespace f3s {
 namespace {
 
-__global__ void k_iota(int32_t *a, int32_t n)
-{
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) a[i] = i;
-}
-
-__global__ void k_gather_pieces(const int32_t *order, const int32_t *npieces, int32_t T,
-                                int32_t *np_sorted)
-{
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < T) np_sorted[i] = npieces[order[i]];
-}
-
 // Window order[i] starts at item pos[i].
 __global__ void k_place_items(const int32_t *order, const int32_t *pos, const int32_t *nb,
                               const int32_t *blk_off, const int32_t *npieces,
@@ -57,15 +44,18 @@ hipError_t launch_worklist(const int32_t *key, const int32_t *nb, const int32_t 
                            int32_t *split_item, int32_t *n_items_out, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_iota<<<blocks_for(T, 256), 256, 0, s>>>(ws.windows, T);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    // the window indices, sorted by key (values: the indices themselves)
     const int32_t *sorted_keys = nullptr, *order = nullptr;
-    e = launch_radix_pairs(key, ws.windows, T, piece, true, ws.radix, &sorted_keys, &order, s);
+    hipError_t e = launch_radix_pairs(key, nullptr, T, piece, true, ws.radix, &sorted_keys,
+                                      &order, s);
     if (e != hipSuccess) return e;
-    k_gather_pieces<<<blocks_for(T, 256), 256, 0, s>>>(order, npieces, T, ws.pos);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    e = launch_scan(ws.pos, ws.pos, T, ws.radix.scan_tmp, n_items_out, s);
+    // first item of each window in that order: scan of its item counts
+    ScanArray a;
+    a.in = npieces;
+    a.gather = order;
+    a.out = ws.pos;
+    a.total = n_items_out;
+    e = launch_scan(a, T, ws.radix.scan_tmp, s);
     if (e != hipSuccess) return e;
     k_place_items<<<blocks_for(T, 256), 256, 0, s>>>(order, ws.pos, nb, blk_off, npieces,
                                                      slot_base, split_idx, T, piece, items,
