@@ -115,8 +115,9 @@ f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N
  *            Q, K or V; every row is overwritten (empty rows with 0)
  *   d        multiple of 32, 32 <= d <= 256
  *   scale    finite; multiplies the fp32 dot products
- *   stream   HIP stream; the call is asynchronous on it, allocates nothing
- *            and copies nothing between host and device
+ *   stream   HIP stream of the device the plan was built on (else
+ *            F3S_ERR_INVALID_VALUE); the call is asynchronous on it,
+ *            allocates nothing and copies nothing between host and device
  * Inputs must be finite.  Returns F3S_OK or an error code (no launch happens
  * on an argument error).
  */
@@ -219,7 +220,8 @@ f3s_plan_t f3s_plan_transpose_ws(f3s_plan_t plan, void *workspace, size_t worksp
  *   d             multiple of 32, 32 <= d <= 256 (as the forward)
  * P and dS enter the products as fp16 (round to nearest even).  Outputs must
  * not overlap each other or any input; 16-byte aligned (lse: 4, row_stats: 8).
- * Asynchronous on `stream`, no allocation.  Deterministic (no atomics).
+ * Asynchronous on `stream` (of the device both plans were built on, else
+ * F3S_ERR_INVALID_VALUE), no allocation.  Deterministic (no atomics).
  */
 f3s_status_t f3s_backward(f3s_plan_t plan, f3s_plan_t plan_t, const void *Q,
                           const void *K, const void *V, const float *O, const void *dO,

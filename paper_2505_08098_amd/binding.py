@@ -127,6 +127,13 @@ def _check_device_tensor(t, name, dtype):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _qkv_shape(Q):
+    """Shape of a one-head [N, d] or multi-head [N, H, d] operand."""
+    if not isinstance(Q, torch.Tensor) or Q.dim() not in (2, 3):
+        raise ValueError("Q must be [N, d] or [N, H, d]")
+    return tuple(Q.shape)
+
+
 class Plan:
     """f3s_plan on a device CSR (int32 row_ptr[N+1], int32 col_idx[nnz])."""
 
@@ -265,7 +272,7 @@ def run(plan, Q, K, V, scale=None, out=None, stream=None):
 
 def forward(plan, Q, K, V, scale=None, out=None, lse=None, stream=None):
     """f3s_forward: returns (O, lse) with lse fp32 [N] or [N, H]."""
-    shape = tuple(Q.shape)
+    shape = _qkv_shape(Q)
     H = shape[1] if len(shape) == 3 else 1
     if lse is None:
         lse = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
@@ -302,7 +309,7 @@ def forward_typed(plan, Q, K, V, out_dtype=torch.float32, scale=None, out=None,
     """f3s_forward_typed: Q, K, V fp16, bf16 or float8_e4m3fn ([N, d] or
     [N, H, d]); O of ``out_dtype`` (fp32 or fp16).  Returns (O, lse) with lse
     None unless ``want_lse`` or an ``lse`` tensor is given."""
-    shape = tuple(Q.shape)
+    shape = _qkv_shape(Q)
     H = shape[1] if len(shape) == 3 else 1
     if Q.dtype not in (torch.float16, torch.bfloat16, torch.float8_e4m3fn):
         raise TypeError(f"Q must be float16, bfloat16 or float8_e4m3fn, got {Q.dtype}")
@@ -340,7 +347,7 @@ def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
     """f3s_backward_typed: returns (dQ, dK, dV) fp32 for fp16 or bf16 Q, K, V,
     dO (the per-row (lse, delta) records it needs go to a buffer allocated
     here)."""
-    shape = tuple(Q.shape)
+    shape = _qkv_shape(Q)
     H = shape[1] if len(shape) == 3 else 1
     d = shape[-1]
     if Q.dtype not in (torch.float16, torch.bfloat16):

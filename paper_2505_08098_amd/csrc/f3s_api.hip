@@ -338,6 +338,15 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+// The plan's arrays live on one device: a launch on another device's stream
+// would read them from the wrong memory.
+bool on_plan_device(const f3s_plan_s *p, hipStream_t stream)
+{
+    int dev = -1;
+    const hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    return e == hipSuccess && dev == p->device;
+}
+
 bool overlaps(const void *a, size_t na, const void *b, size_t nb)
 {
     const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
@@ -654,6 +663,7 @@ f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const
         return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
+    if (!on_plan_device(p, stream)) return fail(F3S_ERR_INVALID_VALUE);
     if (!Q || !K || !V || !O) return fail(F3S_ERR_INVALID_VALUE);
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O))
         return fail(F3S_ERR_INVALID_VALUE);
@@ -719,6 +729,8 @@ f3s_status_t f3s_backward_typed(f3s_plan_t p, f3s_plan_t pt, const void *Q, cons
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
+    if (pt->device != p->device || !on_plan_device(p, stream))
+        return fail(F3S_ERR_INVALID_VALUE);
     const void *ins[] = {Q, K, V, dO};
     void *outs[] = {dQ, dK, dV};
     for (const void *x : ins)

@@ -161,6 +161,9 @@ struct RadixScratch {
     int32_t *scan_tmp;                            // scan_tmp_ints(max(n, radix_count_ints(n)))
 };
 int64_t radix_count_ints(int32_t n);
+// Digit passes of a sort with keys up to max_key (the results of an odd
+// count end up in keys_a / vals_a, of an even count in keys_b / vals_b).
+int radix_passes(int32_t max_key);
 hipError_t launch_radix_pairs(const int32_t *keys, const int32_t *vals, int32_t n,
                               int32_t max_key, bool descending, const RadixScratch &rs,
                               const int32_t **keys_out, const int32_t **vals_out,

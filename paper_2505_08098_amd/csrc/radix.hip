@@ -132,6 +132,13 @@ __global__ __launch_bounds__(kRadixThreads) void k_digit_scatter(
 
 }  // namespace
 
+int radix_passes(int32_t max_key)
+{
+    int passes = 1;
+    for (int shift = 8; shift < 31 && (max_key >> shift) != 0; shift += 8) ++passes;
+    return passes;
+}
+
 int64_t radix_count_ints(int32_t n)
 {
     const int64_t ntiles = (n + kTile - 1) / kTile;
@@ -148,8 +155,8 @@ hipError_t launch_radix_pairs(const int32_t *keys, const int32_t *vals, int32_t 
         const int32_t ntiles = (n + kTile - 1) / kTile;
         const int32_t cells = 256 * ntiles;
         int32_t *kout = rs.keys_a, *vout = rs.vals_a;
-        for (int shift = 0; shift == 0 || (shift < 31 && (max_key >> shift) != 0);
-             shift += 8) {
+        const int passes = radix_passes(max_key);
+        for (int shift = 0; shift < 8 * passes; shift += 8) {
             k_digit_count<<<ntiles, kRadixThreads, 0, s>>>(kin, n, shift, descending, ntiles,
                                                             rs.counts);
             hipError_t e = hipGetLastError();

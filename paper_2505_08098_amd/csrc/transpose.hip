@@ -220,7 +220,9 @@ hipError_t launch_compare_rows(const f3s_plan_s &p, const int32_t *rpt, const in
     k_check_members<<<(unsigned)((words + 255) / 256), 256, 0, s>>>(p.cols, p.mask, win, words,
                                                                     rpt, cit, asym);
     return hipGetLastError();
-}// Scratch of launch_transpose_csr: the decoded pairs (which serve as the
+}
+
+// Scratch of launch_transpose_csr: the decoded pairs (which serve as the
 // radix sort's second buffer pair), the first buffer pair, per-window counts
 // and offsets, digit counts and the scans' workspace.
 size_t transpose_scratch_bytes(const f3s_plan_s &p)
@@ -254,6 +256,9 @@ hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scrat
     rs.vals_a = take(nn);
     rs.keys_b = keys_in;  // free once the first pass has read them
     rs.vals_b = rows_in;
+    // the last pass writes the rows straight into ci: passes alternate
+    // between the buffer pairs a and b, starting with a
+    if (n > 0) (radix_passes(p.N - 1) % 2 ? rs.vals_a : rs.vals_b) = ci;
     int32_t *cnt = take((int64_t)T + 1), *off = take((int64_t)T + 1);
     rs.counts = take(rc);
     rs.scan_tmp = take(scan_tmp_ints(scan));
@@ -273,9 +278,7 @@ hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scrat
         e = launch_radix_pairs(keys_in, rows_in, n, p.N - 1, false, rs, &sorted_cols,
                                &sorted_rows, s);
         if (e != hipSuccess) return e;
-        e = hipMemcpyAsync(ci, sorted_rows, sizeof(int32_t) * (size_t)n,
-                           hipMemcpyDeviceToDevice, s);
-        if (e != hipSuccess) return e;
+        if (sorted_rows != ci) return hipErrorUnknown;  // the pass count above is wrong
     }
     k_rows_from_sorted<<<(unsigned)(((int64_t)p.N + 1 + 255) / 256), 256, 0, s>>>(
         sorted_cols, n, p.N, rp);

@@ -122,6 +122,20 @@ def test_transposed_plan_of_asymmetric_patterns(gpu, oracle, seed):
         assert np.array_equal(got[key], b[key]), key
 
 
+@pytest.mark.parametrize("N", [200, 3000, 70000])
+def test_transposed_plan_for_each_sort_depth(gpu, oracle, N):
+    """Directed patterns whose node ids need one, two and three 8-bit digit
+    passes of the column sort (the last pass writes A^T's columns in place)."""
+    rng = np.random.default_rng(N)
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 24), empty_frac=0.1, dup_frac=0.2)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    got = plan.transpose().export()
+    rp2, ci2 = _transpose_csr(rp, ci, N)
+    b = oracle.bsb(rp2, ci2, N)
+    for key in ("blk_off", "cols", "mask"):
+        assert np.array_equal(got[key], b[key]), key
+
+
 @pytest.mark.parametrize("extra", [False, True])
 def test_transposed_plan_of_symmetric_and_nearly_symmetric_patterns(gpu, oracle, extra):
     """A symmetric pattern is its own transpose (the plan is copied); one
