@@ -67,6 +67,7 @@ struct f3s_plan_s {
 
 namespace f3s {
 
+// ---- plan kernels (plan_kernels.hip) ------------------------------------
 // Inclusive sum over the lanes of a wavefront (device code).
 __device__ __forceinline__ int wave_inclusive_sum(int x, int lane)
 {
@@ -78,7 +79,6 @@ __device__ __forceinline__ int wave_inclusive_sum(int x, int lane)
     return x;
 }
 
-// ---- plan kernels (plan_kernels.hip) ------------------------------------
 hipError_t launch_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
                                 int32_t *err, hipStream_t s);
 // Staging area of the window bitmaps, in 32-bit words, for nnz CSR entries.

@@ -539,9 +539,6 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
 // Heads are launched in groups whose partial results fit the plan's scratch
 // (nh * D <= 256 floats per piece row); without split windows all heads go
 // in one launch.
-// Heads are launched in groups whose partial results fit the plan's scratch
-// (nh * D <= 256 floats per piece row); without split windows all heads go
-// in one launch.
 template <int D, int kIn, bool kOutH, bool kNarrow = false>
 hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                     const void *V, void *O, float *lse, int32_t H, float sl2,
