@@ -425,14 +425,13 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
 }
 
 // Patterns with at least this many entries check symmetry on the sorted CSR
-// of A^T (measured crossover: about 0.2 ms against 0.8 ms with 1.3 M entries,
-// 2.2 ms against 1.6 ms with 18 M).
-constexpr int64_t kSortFirstEntries = 8 << 20;
+// of A^T (F3S_SYMMETRY_SORT_FIRST overrides the count: 0 always sorts first).
+constexpr int kSortFirstEntries = 8 << 20;
 
 // Scratch of a transposition of src: the CSR of A^T, the transposition's
 // own scratch, a flag, and (with_build) the scratch of a plan build of A^T.
 struct TransposeScratch {
-    int32_t *rp, *ci, *asym, *win;
+    int32_t *rp, *ci, *asym, *win, *pre;
     void *tr, *inner;
     size_t tr_bytes, inner_bytes;
 };
@@ -446,6 +445,7 @@ void carve_transpose(Arena &a, bool take, TransposeScratch &t, const f3s_plan_s 
     t.ci = carve<int32_t>(a, take, src->nnz);
     t.asym = carve<int32_t>(a, take, 1);
     t.win = carve<int32_t>(a, take, src->n_blocks);
+    t.pre = carve<int32_t>(a, take, (int64_t)f3s::kWindowRows * src->n_blocks);
     t.tr = carve<char>(a, take, (int64_t)t.tr_bytes);
     t.inner = with_build ? carve<char>(a, take, (int64_t)t.inner_bytes) : nullptr;
 }
@@ -496,14 +496,15 @@ f3s_plan_t make_transpose(f3s_plan_t src, void *workspace, size_t workspace_byte
             int32_t h = 1;
             // symmetric?  Small patterns: checked on the plan first (no sort);
             // large ones: on A^T's sorted rows, which are needed anyway if not
-            const bool small = src->nnz < kSortFirstEntries;
+            const bool small = src->nnz < env_int("F3S_SYMMETRY_SORT_FIRST", kSortFirstEntries);
             bool have_csr = false;
             step(hipMemsetAsync(ts.asym, 0, sizeof(int32_t), nullptr));
             if (small) {
                 step(f3s::launch_check_symmetric(*src, ts.win, ts.asym, nullptr));
             } else {
                 step(f3s::launch_transpose_csr(*src, ts.tr, ts.tr_bytes, ts.rp, ts.ci, nullptr));
-                step(f3s::launch_compare_rows(*src, ts.rp, ts.ci, ts.win, ts.asym, nullptr));
+                step(f3s::launch_compare_rows(*src, ts.rp, ts.ci, ts.win, ts.pre, ts.asym,
+                                              nullptr));
                 have_csr = true;
             }
             step(hipMemcpy(&h, ts.asym, sizeof(int32_t), hipMemcpyDeviceToHost));

@@ -194,10 +194,11 @@ hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scrat
 // on small patterns); win: scratch of n_blocks ints.
 hipError_t launch_check_symmetric(const f3s_plan_s &p, int32_t *win, int32_t *asym,
                                   hipStream_t s);
-// The same decision given the CSR of A^T (binary searches in its short rows;
-// cheaper on large patterns once A^T is sorted anyway).
+// The same decision given the CSR of A^T (every row of A compared with the
+// same row of A^T, position by position; cheaper on large patterns once A^T
+// is sorted anyway).  win: n_blocks ints, pre: 16 * n_blocks ints of scratch.
 hipError_t launch_compare_rows(const f3s_plan_s &p, const int32_t *rpt, const int32_t *cit,
-                               int32_t *win, int32_t *asym, hipStream_t s);
+                               int32_t *win, int32_t *pre, int32_t *asym, hipStream_t s);
 
 // Sets *err when a finished plan is internally inconsistent.
 hipError_t launch_validate_plan(const f3s_plan_s &p, int32_t *err, hipStream_t s);

@@ -107,10 +107,24 @@ def test_transposed_plan_is_the_plan_of_the_transpose(gpu, oracle, k):
     assert np.array_equal(got["cols"], b["cols"]) and np.array_equal(got["mask"], b["mask"])
 
 
+# the symmetry check on the plan alone, or on the sorted rows of A^T (the
+# default from 8 M entries on; forced here for small patterns)
+SYMMETRY_PATHS = ["plan", "sorted"]
+
+
+def _symmetry_path(monkeypatch, path):
+    if path == "sorted":
+        monkeypatch.setenv("F3S_SYMMETRY_SORT_FIRST", "0")
+    else:
+        monkeypatch.delenv("F3S_SYMMETRY_SORT_FIRST", raising=False)
+
+
+@pytest.mark.parametrize("path", SYMMETRY_PATHS)
 @pytest.mark.parametrize("seed", range(4))
-def test_transposed_plan_of_asymmetric_patterns(gpu, oracle, seed):
+def test_transposed_plan_of_asymmetric_patterns(gpu, oracle, seed, path, monkeypatch):
     """Random directed patterns with duplicates and empty rows: the plan of A^T
     built from a plan of A equals the oracle's layout of A^T."""
+    _symmetry_path(monkeypatch, path)
     rng = np.random.default_rng(500 + seed)
     N = int(rng.integers(1, 400))
     rp, ci = W.random_csr(rng, N, max_deg=min(N, 70), empty_frac=0.2, dup_frac=0.3)
@@ -136,10 +150,13 @@ def test_transposed_plan_for_each_sort_depth(gpu, oracle, N):
         assert np.array_equal(got[key], b[key]), key
 
 
+@pytest.mark.parametrize("path", SYMMETRY_PATHS)
 @pytest.mark.parametrize("extra", [False, True])
-def test_transposed_plan_of_symmetric_and_nearly_symmetric_patterns(gpu, oracle, extra):
+def test_transposed_plan_of_symmetric_and_nearly_symmetric_patterns(gpu, oracle, extra,
+                                                                    path, monkeypatch):
     """A symmetric pattern is its own transpose (the plan is copied); one
     directed entry more must be caught by the symmetry check."""
+    _symmetry_path(monkeypatch, path)
     rng = np.random.default_rng(77)
     N = 500
     rp, ci = W.random_csr(rng, N, max_deg=40, empty_frac=0.1, dup_frac=0.2)
