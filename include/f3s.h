@@ -183,8 +183,12 @@ f3s_status_t f3s_forward_typed(f3s_plan_t plan, const void *Q, const void *K, co
  * Plan of the transposed pattern A^T, built on the GPU from `plan` alone
  * (its bitmaps list A's entries).  Needed by f3s_backward: the gradients of
  * K and V are sums over the rows that attend to a key, i.e. over the rows of
- * A^T, so each window of A^T owns its keys' gradients (no atomics).
- * Synchronous; NULL on error (f3s_last_error).  Destroy with f3s_destroy.
+ * A^T, so each window of A^T owns its keys' gradients (no atomics).  An
+ * exact symmetry check first: if A^T = A the result is a copy of the plan.
+ * The check runs on the plan for patterns below 8 M entries and on the
+ * sorted rows of A^T above (environment F3S_SYMMETRY_SORT_FIRST=<entries>
+ * moves that threshold; 0 always sorts first).  Synchronous; NULL on error
+ * (f3s_last_error).  Destroy with f3s_destroy.
  */
 f3s_plan_t f3s_plan_transpose(f3s_plan_t plan);
 
