@@ -302,10 +302,15 @@ __global__ void k_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
 }
 
 // Windows of the list `big` with more than kWaveCap16 entries (at most
-// kSortCap), one workgroup each: LDS bitonic sort and compaction into
-// tmp_cols and u, then the block bitmaps assembled in LDS and stored to the
+// kSortCap), one workgroup each: bitonic sort of kSortCap keys (the window's
+// columns padded with INT_MAX), 4 per thread in registers -- key t = 4 tid +
+// i -- so compare distances 1 and 2 stay in a thread, 4 .. 128 pair lanes of
+// a wavefront (xchg_lanes) and only the 10 steps of distance 256 and more go
+// through LDS (double-buffered: one barrier each); then compaction into
+// tmp_cols and u, and the block bitmaps assembled in LDS and stored to the
 // staging area, their set bits to bits[w].
 constexpr int kSortThreads = 1024;
+constexpr int kSortPer = kSortCap / kSortThreads;  // keys per thread
 
 // Exclusive scan of one int per thread over a workgroup of kSortThreads.
 __device__ int block_excl_scan_sort(int v, int *lds, int *total)
@@ -330,12 +335,13 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *big,
     int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
 {
-    constexpr int kChunk = kSortCap / kSortThreads;  // sorted keys per thread
-    __shared__ int32_t keys[kSortCap];
+    static_assert(kSortPer == 4, "the register network assumes 4 keys per thread");
+    __shared__ int32_t xbuf[2][kSortCap];  // cross-wave exchanges, then the distinct list
     __shared__ int scan[kSortThreads / 64];
+    __shared__ int32_t edge[kSortThreads / 64];
     __shared__ uint32_t s_mask[kSortCap / kBlockCols * kMaskWords];
     __shared__ int32_t s_rp[kWindowRows + 1];
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int w = big[blockIdx.x];
     const int r0 = w * kWindowRows;
     const int nr = min(r0 + kWindowRows, N) - r0;
@@ -343,9 +349,10 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     const int n = row_ptr[r0 + nr] - beg;
     if (n <= kWaveCap16 || n > kSortCap) return;  // k_window_wave16 / heavy paths
     if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
-    int p2 = 1;
-    while (p2 < n) p2 <<= 1;
-    for (int t = tid; t < p2; t += kSortThreads) {
+    int x[kSortPer];
+#pragma unroll
+    for (int i = 0; i < kSortPer; ++i) {
+        const int t = kSortPer * tid + i;
         int v = INT_MAX;
         if (t < n) {
             v = col_idx[beg + t];
@@ -354,46 +361,68 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
                 v = INT_MAX;
             }
         }
-        keys[t] = v;
+        x[i] = v;
     }
-    __syncthreads();
-    // bitonic sort, ascending
-    for (int k = 2; k <= p2; k <<= 1) {
+    // bitonic network, ascending
+    int buf = 0;
+#pragma unroll
+    for (int k = 2; k <= kSortCap; k <<= 1) {
+#pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int t = tid; t < p2; t += kSortThreads) {
-                const int x = t ^ j;
-                if (x > t) {
-                    const int a = keys[t], b = keys[x];
-                    const bool up = (t & k) == 0;
-                    if ((a > b) == up) {
-                        keys[t] = b;
-                        keys[x] = a;
-                    }
+            if (j >= 64 * kSortPer) {
+#pragma unroll
+                for (int i = 0; i < kSortPer; ++i) xbuf[buf][kSortPer * tid + i] = x[i];
+                __syncthreads();
+#pragma unroll
+                for (int i = 0; i < kSortPer; ++i) {
+                    const int t = kSortPer * tid + i;
+                    const int p = xbuf[buf][t ^ j];
+                    const bool take_min = ((t & j) == 0) == ((t & k) == 0);
+                    x[i] = take_min ? min(x[i], p) : max(x[i], p);
+                }
+                buf ^= 1;
+            } else if (j >= kSortPer) {
+                const int lj = j / kSortPer;
+                const bool lower = (lane & lj) == 0;
+#pragma unroll
+                for (int i = 0; i < kSortPer; ++i) {
+                    const bool up = ((kSortPer * tid + i) & k) == 0;
+                    x[i] = xchg_lanes(x[i], lj, lane, lower == up);
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < kSortPer; ++i) {
+                    if (i & j) continue;
+                    const bool up = ((kSortPer * tid + i) & k) == 0;
+                    const int a = x[i], b = x[i | j];
+                    x[i] = up ? min(a, b) : max(a, b);
+                    x[i | j] = up ? max(a, b) : min(a, b);
                 }
             }
-            __syncthreads();
         }
     }
-    // distinct values, written in order at the window's CSR offset and
-    // compacted to the front of keys (read into registers first: the scan's
-    // barriers separate every read from the compacting writes)
-    const int ch = (p2 + kSortThreads - 1) / kSortThreads;
-    const int lo = min(tid * ch, n), hi = min(lo + ch, n);
-    int v[kChunk];
+    // distinct values: key t is new if it differs from key t - 1 (the last
+    // key of the previous thread: a lane move, or across waves through LDS)
+    if (lane == 63) edge[wv] = x[kSortPer - 1];
+    __syncthreads();
+    int prev = __shfl_up(x[kSortPer - 1], 1);
+    if (lane == 0) prev = wv ? edge[wv - 1] : INT_MIN;
     uint32_t first = 0;
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j) {
-        const int k = lo + j;
-        v[j] = k < hi ? keys[k] : INT_MAX;
-        if (k < hi && v[j] != INT_MAX && (k == 0 || v[j] != keys[k - 1])) first |= 1u << j;
+    for (int i = 0; i < kSortPer; ++i) {
+        const int pv = i ? x[i - 1] : prev;
+        if (x[i] != INT_MAX && x[i] != pv) first |= 1u << i;
     }
     int total;
     int off = block_excl_scan_sort(__popc(first), scan, &total);
+    // the distinct list goes to xbuf[buf], whose last reads were separated from
+    // these writes by the scan's barriers
+    int32_t *list = xbuf[buf];
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j)
-        if (first & (1u << j)) {
-            tmp_cols[beg + off] = v[j];
-            keys[off] = v[j];
+    for (int i = 0; i < kSortPer; ++i)
+        if (first & (1u << i)) {
+            tmp_cols[beg + off] = x[i];
+            list[off] = x[i];
             ++off;
         }
     const int nbw = (total + kBlockCols - 1) / kBlockCols;
@@ -409,7 +438,7 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
         int a = 0, b = total;
         while (a < b) {
             const int mid = (a + b) >> 1;
-            if (keys[mid] < c) a = mid + 1;
+            if (list[mid] < c) a = mid + 1;
             else b = mid;
         }
         if (a >= total) continue;  // every valid column is in the list
