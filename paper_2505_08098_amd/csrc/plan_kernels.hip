@@ -469,17 +469,20 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
 // popcount of the lower bits of its word; no search.  A first walk counts the
 // distinct columns (for the size of the block bitmaps), the second writes
 // them in order to tmp_cols and sets the entries' bits, in LDS when the
-// bitmaps fit (kHeavyMaskWords), else with atomics on the staging area.  On
+// bitmaps fit (mask_words: what the LDS budget leaves after the chunk
+// bitmap and ranks), else with atomics on the staging area.  On
 // graphs of up to kChunkCols nodes the first walk's bitmap is reused.
 constexpr int kHeavyThreads = 1024;
 constexpr int kChunkCols = 1 << 17;       // 16 KB bitmap + 16 KB ranks
-constexpr int kHeavyMaskWords = 4096;     // block bitmaps held in LDS (512 blocks)
+// LDS of one workgroup: two of them (2 x 1024 threads) still fit a CU.
+constexpr int kHeavyLdsBytes = 76 * 1024;
 
 __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *heavy,
-    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
+    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err,
+    int32_t mask_words)
 {
-    extern __shared__ uint32_t lds[];  // [cw] bitmap, [cw] ranks, [kHeavyMaskWords]
+    extern __shared__ uint32_t lds[];  // [cw] bitmap, [cw] ranks, [mask_words]
     __shared__ int32_t s_rp[kWindowRows + 1];
     __shared__ int scan[kHeavyThreads / 64];
     const int tid = threadIdx.x;
@@ -494,36 +497,57 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     __syncthreads();
     const int beg = s_rp[0], n = s_rp[nr] - beg;
     const int nchunk = (N + kChunkCols - 1) / kChunkCols;
+    // A thread ORs the bits of its successive entries that land in the same
+    // word in a register, with one atomic per change of word (a window's
+    // entries often repeat a few words: banded rows, sorted rows), and
+    // follows its row incrementally.  With one column chunk each thread takes
+    // a contiguous run of entries (most repeats); with several, whose walks
+    // re-read the entries once per chunk, entries are strided over the
+    // threads so the loads stay coalesced (measured: contiguous runs cost 23%
+    // there).
+    const int per = (n + kHeavyThreads - 1) / kHeavyThreads;
+    const int e0 = nchunk == 1 ? min(tid * per, n) : tid;
+    const int e1 = nchunk == 1 ? min(e0 + per, n) : n;
+    const int es = nchunk == 1 ? 1 : kHeavyThreads;
     // marks the columns of chunk q in bm (zeroed first)
     auto mark = [&](int q, bool report) {
         for (int k = tid; k < cw; k += kHeavyThreads) bm[k] = 0;
         __syncthreads();
         const int c0 = q * kChunkCols;
-        for (int e = tid; e < n; e += kHeavyThreads) {
+        int cur = -1;
+        uint32_t acc = 0;
+        for (int e = e0; e < e1; e += es) {
             const int c = col_idx[beg + e];
             if (c < 0 || c >= N) {
                 if (report) atomicOr(err, 1);
                 continue;
             }
-            if (c >= c0 && c - c0 < kChunkCols)
-                atomicOr(&bm[(c - c0) >> 5], 1u << (c & 31));
+            if (c < c0 || c - c0 >= kChunkCols) continue;
+            const int wd = (c - c0) >> 5;
+            if (wd != cur) {
+                if (acc) atomicOr(&bm[cur], acc);
+                cur = wd;
+                acc = 0;
+            }
+            acc |= 1u << (c & 31);
         }
+        if (acc) atomicOr(&bm[cur], acc);
         __syncthreads();
     };
     const int ch = (cw + kHeavyThreads - 1) / kHeavyThreads;
     const int lo = min(tid * ch, cw), hi = min(lo + ch, cw);
     // walk 1: distinct columns
-    int total = 0;
+    int total = 0, first_off = 0;  // first_off: this thread's rank offset (one chunk)
     for (int q = 0; q < nchunk; ++q) {
         mark(q, q == 0);
         int cnt = 0;
         for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
         int t;
-        (void)block_excl_scan_sort(cnt, scan, &t);
+        first_off = block_excl_scan_sort(cnt, scan, &t);
         total += t;
     }
     const int nbw = (total + kBlockCols - 1) / kBlockCols;
-    const bool in_lds = kMaskWords * nbw <= kHeavyMaskWords;
+    const bool in_lds = kMaskWords * nbw <= mask_words;
     uint32_t *gm = tmp_mask + mask_stage(beg, w);
     uint32_t *dst = in_lds ? sm : gm;
     for (int k = tid; k < kMaskWords * nbw; k += kHeavyThreads) dst[k] = 0;
@@ -532,12 +556,17 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     // walk 2: ranks, distinct columns in order, the entries' bits
     int base = 0;
     for (int q = 0; q < nchunk; ++q) {
-        if (nchunk > 1) mark(q, false);
         const int c0 = q * kChunkCols;
-        int cnt = 0;
-        for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
-        int t;
-        int off = base + block_excl_scan_sort(cnt, scan, &t);
+        int t, off;
+        if (nchunk == 1) {  // walk 1's bitmap and offsets still hold
+            t = total;
+            off = first_off;
+        } else {
+            mark(q, false);
+            int cnt = 0;
+            for (int k = lo; k < hi; ++k) cnt += __popc(bm[k]);
+            off = base + block_excl_scan_sort(cnt, scan, &t);
+        }
         for (int k = lo; k < hi; ++k) {
             rank[k] = off;
             uint32_t x = bm[k];
@@ -547,18 +576,26 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
             }
         }
         __syncthreads();
-        for (int e = tid; e < n; e += kHeavyThreads) {
+        int row = 0, cur = -1;
+        uint32_t acc = 0;
+        for (int e = e0; e < e1; e += es) {
+            while (row + 1 < nr && beg + e >= s_rp[row + 1]) ++row;
             const int c = col_idx[beg + e];
             if (c < c0 || c >= N || c - c0 >= kChunkCols) continue;
-            int row = 0;
-            for (int r = 1; r < nr; ++r) row += beg + e >= s_rp[r];
             const int cl = c - c0;
             const uint32_t below = bm[cl >> 5] & ((1u << (cl & 31)) - 1u);
             const int a = rank[cl >> 5] + __popc(below);
             const int cc = a % kBlockCols;
             const int bit = 4 * (row + 16 * (cc / 4)) + (cc % 4);
-            atomicOr(&dst[kMaskWords * (a / kBlockCols) + bit / 32], 1u << (bit % 32));
+            const int wd = kMaskWords * (a / kBlockCols) + bit / 32;
+            if (wd != cur) {
+                if (acc) atomicOr(&dst[cur], acc);
+                cur = wd;
+                acc = 0;
+            }
+            acc |= 1u << (bit % 32);
         }
+        if (acc) atomicOr(&dst[cur], acc);
         base += t;
         __syncthreads();
     }
@@ -887,9 +924,11 @@ hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int3
                             hipStream_t s)
 {
     if (n_heavy == 0) return hipSuccess;
-    const size_t lds = (2 * (size_t)((min(N, kChunkCols) + 31) / 32) + kHeavyMaskWords) * 4;
+    const int cw = (min(N, kChunkCols) + 31) / 32;
+    const int mask_words = (kHeavyLdsBytes / 4 - 2 * cw) & ~(kMaskWords - 1);
+    const size_t lds = (size_t)(2 * cw + mask_words) * 4;
     k_heavy_lds<<<n_heavy, kHeavyThreads, lds, s>>>(row_ptr, col_idx, N, heavy, tmp_cols,
-                                                     tmp_mask, u, bits, err);
+                                                     tmp_mask, u, bits, err, mask_words);
     return hipGetLastError();
 }
 

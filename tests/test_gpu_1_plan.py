@@ -60,17 +60,20 @@ def test_plan_matches_oracle_on_random_patterns(gpu, oracle, seed):
     _check_plan_against_oracle(gpu, oracle, rp, ci, N)
 
 
-def test_plan_heavy_window_above_lds_capacity(gpu, oracle):
-    """A window with more entries than the LDS sort holds takes the bitmap path."""
+@pytest.mark.parametrize("N,per_row,min_blocks", [(40000, 600, 256), (200000, 2000, 1408)])
+def test_plan_heavy_window_above_lds_capacity(gpu, oracle, N, per_row, min_blocks):
+    """A window with more entries than the LDS sort holds takes the column-
+    bitmap path; its block bitmaps are built in LDS up to the workgroup's
+    budget (1408 blocks with two column chunks at N = 200,000) and with
+    atomics on the staging area beyond it."""
     rng = np.random.default_rng(7)
-    N = 40000
-    rows = [rng.choice(N, size=600, replace=True) if i < 16 else
+    rows = [rng.choice(N, size=per_row, replace=True) if i < 16 else
             rng.choice(N, size=3, replace=False) for i in range(N)]
     rp = np.zeros(N + 1, dtype=np.int32)
     rp[1:] = np.cumsum([len(r) for r in rows])
     ci = np.concatenate(rows).astype(np.int32)
     info = _check_plan_against_oracle(gpu, oracle, rp, ci, N)
-    assert info["max_blocks"] > 256
+    assert info["max_blocks"] > min_blocks
 
 
 def test_plan_more_windows_than_one_scan_tile(gpu, oracle):
