@@ -132,6 +132,10 @@ f3s_status_t f3s_run(f3s_plan_t plan, const void *Q, const void *K, const void *
  * is the single-head operator applied to head h of Q, K, V.  Same pointer,
  * alignment, d, scale and stream rules as f3s_run; n_heads >= 1 and
  * n_items * n_heads < 2^31.  f3s_run is f3s_run_mh with n_heads = 1.
+ * All heads run in one launch: window-major while K and V (all heads) fit
+ * the 256 MB Infinity Cache, head by head above it (environment
+ * F3S_HEAD_MAJOR_BYTES=<bytes> moves that threshold; results are identical
+ * either way).
  */
 f3s_status_t f3s_run_mh(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                         void *O, int32_t n_heads, int32_t d, float scale,

@@ -47,6 +47,8 @@
 // for split windows, the fp32 (m, l, unnormalised O) partials are written.
 #pragma once
 
+#include <stdlib.h>
+
 #include "kernel_common.h"
 
 namespace f3s {
@@ -175,7 +177,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const void *__restrict__ Kv, const void *__restrict__ Vv,
     void *__restrict__ O, float *__restrict__ part_o,
     float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
-    int32_t h0, int32_t nh, float sl2)
+    int32_t h0, int32_t nh, float sl2, bool head_major)
 {
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
@@ -191,9 +193,20 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const int lane = threadIdx.x;
     const int i = lane & 15;  // query row (accumulators) / operand row index
     const int g = lane >> 4;  // lane group: selects the reduction slots
-    // Workgroups walk the work list item-major, head-minor: the heads of one
-    // window run back to back and share its column lists and bitmaps.
-    const int item = blockIdx.x / nh, hl = blockIdx.x - item * nh;
+    // Workgroups walk the work list item-major (the heads of one window back
+    // to back: they share its column lists and bitmaps, and the lines of its
+    // K and V rows while those stay cached) or head-major (one pass over the
+    // list per head: with K and V far larger than the caches each head's
+    // gathers then stream like a single head's).
+    int item, hl;
+    if (head_major) {
+        const int n_it = gridDim.x / nh;
+        hl = blockIdx.x / n_it;
+        item = blockIdx.x - hl * n_it;
+    } else {
+        item = blockIdx.x / nh;
+        hl = blockIdx.x - item * nh;
+    }
     const int head = h0 + hl;
     const WorkItem it = items[item];
     // Row r of head h starts at r * ld + h * D (elements) in Q, K, V and O.
@@ -536,6 +549,14 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
         if (4 * q + 64 * c < D) store4<kOutH>(O, orow + 4 * q + 64 * c, acc[c] * inv);
 }
 
+// K and V bytes (all heads) above which several heads run head-major: the
+// 256 MB Infinity Cache; F3S_HEAD_MAJOR_BYTES overrides it (read at launch).
+inline uint64_t head_major_bytes()
+{
+    const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
+    return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
+}
+
 // Heads are launched in groups whose partial results fit the plan's scratch
 // (nh * D <= 256 floats per piece row); without split windows all heads go
 // in one launch.
@@ -556,9 +577,11 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
         if (p.n_items > 0) {
             const uint64_t grid = (uint64_t)p.n_items * nh;
             if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
+            const bool head_major =
+                nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_bytes();
             kern<<<(unsigned)grid, 64, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
-                                               sl2);
+                                               sl2, head_major);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }

@@ -256,9 +256,21 @@ def test_run_argument_errors(gpu):
     assert gpu.status_string(2) == "F3S_ERR_INVALID_CSR"
 
 
+def _head_order(monkeypatch, order):
+    """Workgroup order of several heads: item-major below the K/V size
+    threshold (the default for these small inputs), head-major above it
+    (forced with a threshold of 0)."""
+    if order == "head":
+        monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0")
+    else:
+        monkeypatch.delenv("F3S_HEAD_MAJOR_BYTES", raising=False)
+
+
+@pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("H,d", [(2, 64), (4, 32), (8, 64), (3, 128)])
-def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d):
+def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d, order, monkeypatch):
     """f3s_run_mh: H heads sharing one plan (Section 2.1, Eq. 4 per head)."""
+    _head_order(monkeypatch, order)
     rng = np.random.default_rng(100 + H * d)
     N = 700
     rp, ci = W.random_csr(rng, N, max_deg=60, empty_frac=0.05, dup_frac=0.1)
@@ -273,11 +285,14 @@ def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d):
         _assert_parity(O[:, h], ref)
 
 
+@pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("piece", [4, 1000000])
-def test_multi_head_equals_single_head_runs(gpu, monkeypatch, piece):
+def test_multi_head_equals_single_head_runs(gpu, monkeypatch, piece, order):
     """Head h of the multi-head call is bit-identical to a single-head call on
     the head's slice, with and without split windows (H * d > 256 also
-    exercises the head groups that bound the partial-result scratch)."""
+    exercises the head groups that bound the partial-result scratch), in
+    either workgroup order."""
+    _head_order(monkeypatch, order)
     monkeypatch.setenv("F3S_PIECE_BLOCKS", str(piece))
     c = W.make_config(2, with_features=False)
     N, H, d = c["N"], 6, 64
