@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "f3s.h"
 
@@ -68,6 +69,14 @@ struct f3s_plan_s {
 namespace f3s {
 
 // ---- plan kernels (plan_kernels.hip) ------------------------------------
+// K and V bytes (all heads) above which a launch over several heads runs
+// head by head instead of window-major: the 256 MB Infinity Cache;
+// F3S_HEAD_MAJOR_BYTES overrides it (read at launch).
+inline uint64_t head_major_threshold()
+{
+    const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
+    return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
+}
 // Inclusive sum over the lanes of a wavefront (device code).
 __device__ __forceinline__ int wave_inclusive_sum(int x, int lane)
 {

@@ -47,8 +47,6 @@
 // for split windows, the fp32 (m, l, unnormalised O) partials are written.
 #pragma once
 
-#include <stdlib.h>
-
 #include "kernel_common.h"
 
 namespace f3s {
@@ -549,14 +547,6 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
         if (4 * q + 64 * c < D) store4<kOutH>(O, orow + 4 * q + 64 * c, acc[c] * inv);
 }
 
-// K and V bytes (all heads) above which several heads run head-major: the
-// 256 MB Infinity Cache; F3S_HEAD_MAJOR_BYTES overrides it (read at launch).
-inline uint64_t head_major_bytes()
-{
-    const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
-    return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
-}
-
 // Heads are launched in groups whose partial results fit the plan's scratch
 // (nh * D <= 256 floats per piece row); without split windows all heads go
 // in one launch.
@@ -578,7 +568,7 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
             const uint64_t grid = (uint64_t)p.n_items * nh;
             if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
             const bool head_major =
-                nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_bytes();
+                nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
             kern<<<(unsigned)grid, 64, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
                                                sl2, head_major);

@@ -290,10 +290,17 @@ def test_gradients_workloads(gpu, oracle, k):
                c["scale"])
 
 
+@pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("H,d", [(3, 64), (2, 160), (2, 256)])
-def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d):
+def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order):
     """Split windows in both plans; for d > 128 the dK/dV partials of one
-    head fill a whole (double-width) partial row of the transposed plan."""
+    head fill a whole (double-width) partial row of the transposed plan.
+    Both workgroup orders of the heads (window-major, the default at this
+    size, and head by head, forced with a threshold of 0)."""
+    if order == "head":
+        monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0")
+    else:
+        monkeypatch.delenv("F3S_HEAD_MAJOR_BYTES", raising=False)
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
     rng = np.random.default_rng(12)
     N = 3000
