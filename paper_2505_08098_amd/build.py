@@ -14,6 +14,12 @@ LIB = os.path.join(HERE, "libf3s.so")
 SOURCES = ["f3s_api.hip", "plan_kernels.hip", "fused3s.hip", "fused3s_bf16.hip",
            "fused3s_fp8.hip", "fused3s_ablation.hip", "backward.hip", "backward_bf16.hip", "transpose.hip", "worklist.hip", "radix.hip"]
 
+# The plan and transposition sources are compiled as relocatable device code
+# and linked into ONE device code object: the runtime loads a code object on
+# its first kernel launch, about 0.3 ms each, which a first plan build in a
+# process would otherwise pay once per source file.
+RDC_SOURCES = {"plan_kernels.hip", "transpose.hip", "worklist.hip", "radix.hip"}
+
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
     "-Wall", "-Wno-unused-function",
@@ -38,14 +44,16 @@ def build(verbose=False, extra_flags=()):
     for src in SOURCES:
         obj = os.path.join(obj_dir, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([hipcc(), *HIPCC_FLAGS, *extra_flags, *inc, "-c",
+        rdc = ["-fgpu-rdc"] if src in RDC_SOURCES else []
+        cmds.append([hipcc(), *HIPCC_FLAGS, *rdc, *extra_flags, *inc, "-c",
                      os.path.join(HERE, "csrc", src), "-o", obj])
     jobs = max(1, min(len(cmds), os.cpu_count() or 1))
     with concurrent.futures.ThreadPoolExecutor(jobs) as pool:
         for cmd, res in zip(cmds, pool.map(_run, cmds, [verbose] * len(cmds))):
             if res.returncode != 0:
                 raise subprocess.CalledProcessError(res.returncode, cmd)
-    link = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", LIB + ".tmp", *objs]
+    link = [hipcc(), "--offload-arch=gfx950", "-fgpu-rdc", "--hip-link", "-shared", "-fPIC",
+            "-o", LIB + ".tmp", *objs]
     _run(link, verbose, check=True)
     os.replace(LIB + ".tmp", LIB)
     return LIB

@@ -20,6 +20,11 @@
 
 #include "f3s_internal.h"
 
+// Dynamic LDS of k_heavy_lds (declared at global scope: this file is also
+// built as relocatable device code, where a block-scope declaration inside
+// the anonymous namespace would name an undefined internal variable).
+extern __shared__ uint32_t f3s_heavy_lds_dyn[];
+
 namespace f3s {
 namespace {
 
@@ -482,7 +487,7 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err,
     int32_t mask_words)
 {
-    extern __shared__ uint32_t lds[];  // [cw] bitmap, [cw] ranks, [mask_words]
+    uint32_t *lds = f3s_heavy_lds_dyn;  // [cw] bitmap, [cw] ranks, [mask_words]
     __shared__ int32_t s_rp[kWindowRows + 1];
     __shared__ int scan[kHeavyThreads / 64];
     const int tid = threadIdx.x;
