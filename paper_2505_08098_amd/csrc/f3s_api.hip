@@ -141,13 +141,22 @@ int env_int(const char *name, int dflt)
         if (e_ != hipSuccess) return from_hip(e_);             \
     } while (0)
 
-// Work-list slots of a device: 8 per compute unit.
+// Work-list slots of a device: 8 per compute unit (the count is queried
+// once per device; a full property query costs tens of microseconds).
 int32_t plan_slots(int device)
 {
-    int cus = 256;
-    hipDeviceProp_t prop;
-    if (hipGetDeviceProperties(&prop, device) == hipSuccess && prop.multiProcessorCount > 0)
-        cus = prop.multiProcessorCount;
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int32_t> cached[kMaxDevices] = {};
+    if (device >= 0 && device < kMaxDevices) {
+        const int32_t c = cached[device].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) !=
+            hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    if (device >= 0 && device < kMaxDevices) cached[device].store(8 * cus);
     return 8 * cus;
 }
 
