@@ -136,12 +136,18 @@ def test_transposed_plan_of_asymmetric_patterns(gpu, oracle, seed, path, monkeyp
         assert np.array_equal(got[key], b[key]), key
 
 
-@pytest.mark.parametrize("N", [200, 3000, 70000])
+@pytest.mark.parametrize("N", [200, 3000, 70000, 17_000_000])
 def test_transposed_plan_for_each_sort_depth(gpu, oracle, N):
-    """Directed patterns whose node ids need one, two and three 8-bit digit
-    passes of the column sort (the last pass writes A^T's columns in place)."""
+    """Directed patterns whose node ids need one, two, three and four 8-bit
+    digit passes of the column sort (the last pass writes A^T's columns in
+    place, from either buffer pair)."""
     rng = np.random.default_rng(N)
-    rp, ci = W.random_csr(rng, N, max_deg=min(N, 24), empty_frac=0.1, dup_frac=0.2)
+    if N <= 100000:
+        rp, ci = W.random_csr(rng, N, max_deg=min(N, 24), empty_frac=0.1, dup_frac=0.2)
+    else:  # sparse: 0-2 entries per row, repeats possible
+        rp = np.zeros(N + 1, dtype=np.int32)
+        rp[1:] = np.cumsum(rng.integers(0, 3, size=N, dtype=np.int32))
+        ci = rng.integers(0, N, size=int(rp[-1]), dtype=np.int32)
     plan = gpu.Plan(_dev(rp), _dev(ci), N)
     got = plan.transpose().export()
     rp2, ci2 = _transpose_csr(rp, ci, N)
