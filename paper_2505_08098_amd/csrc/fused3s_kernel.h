@@ -136,6 +136,23 @@ __device__ __forceinline__ void stage_words(_Float16 *row, int m, h8 w)
         *reinterpret_cast<uint32_t *>(row + 8 * (m0 + cc) + 2 * qd) = words[cc];
 }
 
+// Orders one wave's accesses to its LDS tile.  With one wave per workgroup
+// the workgroup barrier of wave_lds_fence does it; with several waves per
+// workgroup (which run different numbers of block pairs) only this wave may
+// take part: fences at wavefront scope around a wave barrier (a wave's LDS
+// operations run in issue order, so only the compiler has to be held).
+template <int NW>
+__device__ __forceinline__ void tile_fence()
+{
+    if constexpr (NW == 1) {
+        wave_lds_fence();
+    } else {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    }
+}
+
 // v where sel is all ones, -inf where sel is zero (one bit-select).
 __device__ __forceinline__ float masked_score(float v, int sel)
 {
@@ -166,9 +183,14 @@ __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
 // gathered in 4-byte words -- consecutive lanes of a quad read consecutive
 // words of a row, each lane taking one word of each of the quad's four
 // 16-byte chunks -- instead of one 16-byte chunk per lane, i.e. the access
-// granularity without the register remapping of Section 3.4.
-template <int D, bool kWide, int kIn, bool kOutH, bool kNarrow = false>
-__global__ __launch_bounds__(64)
+// granularity without the register remapping of Section 3.4.  NW: waves
+// per workgroup sharing one work item -- each takes a contiguous share of
+// its block pairs, and the (m, l, O) partials are combined through LDS at
+// the end (the paper's split-column partition of a window among warps; used
+// for long windows, where one wave per window leaves the GPU with too few
+// waves).
+template <int D, bool kWide, int kIn, bool kOutH, bool kNarrow = false, int NW = 1>
+__global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const void *__restrict__ Qv,
@@ -186,9 +208,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     // 8-bank ranges.
     constexpr int LSK = D + 8;
     constexpr int LSV = D + 16;
-    __shared__ __attribute__((aligned(16))) _Float16 tile[32 * LSV];
+    __shared__ __attribute__((aligned(16))) _Float16 tiles[NW][32 * LSV];
+    const int wv = NW > 1 ? (int)(threadIdx.x >> 6) : 0;
+    _Float16 *const tile = tiles[wv];
 
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & 63;
     const int i = lane & 15;  // query row (accumulators) / operand row index
     const int g = lane >> 4;  // lane group: selects the reduction slots
     // Workgroups walk the work list item-major (the heads of one window back
@@ -214,7 +238,14 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const char *V = static_cast<const char *>(Vv) + (int64_t)head * D * EB;
     const int64_t ohead = (int64_t)head * D;
     const int row = it.window * kWindowRows + i;
-    const int b0 = it.blk_begin, b1 = it.blk_end;
+    // this wave's blocks: whole pairs [pa, pb) of the item's pairs
+    int b0 = it.blk_begin, b1 = it.blk_end;
+    if constexpr (NW > 1) {
+        const int pairs = (b1 - b0 + 1) >> 1;
+        const int pa = pairs * wv / NW, pb = pairs * (wv + 1) / NW;
+        b1 = min(b1, b0 + 2 * pb);
+        b0 = b0 + 2 * pa;
+    }
 
     // Q_i: lane (i, g) holds Q[row][32c + 8g .. +7] for each chunk c.  Pad
     // rows (>= N) of the last window read row N-1: their results are never
@@ -333,7 +364,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
                 *reinterpret_cast<h8 *>(dst) = kst[j];
             }
         }
-        wave_lds_fence();
+        tile_fence<NW>();
         h8 ka[NC], kb[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -347,7 +378,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
             s0 = mma_in<kIn>(ka[c], q[c], s0);
             s1 = mma_in<kIn>(kb[c], q[c], s1);
         }
-        wave_lds_fence();
+        tile_fence<NW>();
         // ---- V rows -> the same LDS tile (stride LSV, slot = neighbour) ----
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
@@ -417,7 +448,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
         m_run = m_new;
 #pragma unroll
         for (int t = 0; t < NT; ++t) o[t] *= alpha;
-        wave_lds_fence();
+        tile_fence<NW>();
         // ---- value product: A[m][slot] = V_hat[slot][16t + m] ----
         // slot order of lane group g: 4g..4g+3 (block 0), 16+4g..+3 (block 1)
         // -- the neighbours this lane's P values belong to.  Group lane s
@@ -437,7 +468,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
                 o[t] = mfma16x16x32(a, p, o[t]);
             }
         }
-        wave_lds_fence();
+        tile_fence<NW>();
     };
 
     if (b0 < b1) {
@@ -452,6 +483,40 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     // ---- finalise: full row sums, normalise, write (Algorithm 1 end) ----
     float l_tot = l_run + __shfl_xor(l_run, 16);
     l_tot += __shfl_xor(l_tot, 32);
+    if constexpr (NW > 1) {
+        // the waves' partial states: O (lane (i, g) holds columns 16t + 4g ..
+        // +3 of row i) into the wave's own tile, which 16 x D floats fit and
+        // no longer serves; then wave 0 combines them as the online softmax
+        // combines blocks (a wave without blocks has m = -inf, l = 0, O = 0)
+        __shared__ float s_m[NW][kWindowRows], s_l[NW][kWindowRows];
+        float *ot = reinterpret_cast<float *>(tile);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            *reinterpret_cast<f4 *>(ot + i * D + 16 * t + 4 * g) = o[t];
+        if (g == 0) {
+            s_m[wv][i] = m_run;
+            s_l[wv][i] = l_tot;
+        }
+        __syncthreads();
+        if (wv != 0) return;
+        float m = -__builtin_inff();
+#pragma unroll
+        for (int w = 0; w < NW; ++w) m = fmaxf(m, s_m[w][i]);
+        const float m_ref = m == -__builtin_inff() ? 0.f : m;
+        float l = 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) o[t] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const float a = __builtin_amdgcn_exp2f(s_m[w][i] - m_ref);
+            l += a * s_l[w][i];
+            const float *ow = reinterpret_cast<const float *>(tiles[w]) + i * D + 4 * g;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) o[t] += a * *reinterpret_cast<const f4 *>(ow + 16 * t);
+        }
+        m_run = m;
+        l_tot = l;
+    }
     if (it.slot < 0) {
         if (row < N) {
             const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -557,8 +622,12 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
 {
     const int32_t ld = H * D;
     const bool wide = (uint64_t)p.N * ld * elem_bytes<kIn>() > 0xFFFFFFF0ull;
-    auto kern = wide ? k_fused3s<D, true, kIn, kOutH, kNarrow>
-                     : k_fused3s<D, false, kIn, kOutH, kNarrow>;
+    // the narrow-gather ablation keeps one wave per item
+    const int nw = kNarrow ? 1 : forward_waves_per_item(p.n_blocks, p.n_items, H);
+    auto kern = nw == 4 ? (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow, kNarrow ? 1 : 4>
+                                : k_fused3s<D, false, kIn, kOutH, kNarrow, kNarrow ? 1 : 4>)
+                        : (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow>
+                                : k_fused3s<D, false, kIn, kOutH, kNarrow>);
     const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
     for (int32_t h0 = 0; h0 < H; h0 += group) {
         const int32_t nh = H - h0 < group ? H - h0 : group;
@@ -569,7 +638,7 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
             if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
             const bool head_major =
                 nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
-            kern<<<(unsigned)grid, 64, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
+            kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
                                                sl2, head_major);
             hipError_t e = hipGetLastError();

@@ -68,14 +68,38 @@ def test_workload_parity(gpu, oracle, k):
     _assert_parity(O, ref)
 
 
+@pytest.mark.parametrize("waves", ["1", "4"])
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
 @pytest.mark.parametrize("N", [1, 17, 200])
-def test_feature_sizes_and_ragged_windows(gpu, oracle, d, N):
+def test_feature_sizes_and_ragged_windows(gpu, oracle, d, N, waves, monkeypatch):
+    """Every feature size, ragged last windows, with one wave per work item
+    or four sharing it (their partials combined in LDS)."""
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     rng = np.random.default_rng(d * 1000 + N)
     rp, ci = W.random_csr(rng, N, max_deg=min(N, 70), empty_frac=0.1, dup_frac=0.2)
     Q, K, V = _qkv(rng, N, d)
     scale = 1 / math.sqrt(d)
     O, _ = _run(gpu, rp, ci, N, Q, K, V, scale)
+    _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, scale))
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_four_waves_per_item_with_split_windows(gpu, oracle, d, monkeypatch):
+    """Four waves sharing each work item, on pieces of split windows too (a
+    piece's combined partial goes to the merge launch)."""
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", "4")
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "6")
+    rng = np.random.default_rng(d + 7)
+    N = 700
+    rows = [rng.choice(N, size=400, replace=False) if i < 20 else
+            rng.choice(N, size=int(rng.integers(0, 40)), replace=False) for i in range(N)]
+    rp = np.zeros(N + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([len(r) for r in rows])
+    ci = np.concatenate(rows).astype(np.int32)
+    Q, K, V = _qkv(rng, N, d)
+    scale = 1 / math.sqrt(d)
+    O, plan = _run(gpu, rp, ci, N, Q, K, V, scale)
+    assert plan.info["n_split"] > 0
     _assert_parity(O, oracle.attention_f64(rp, ci, Q, K, V, scale))
 
 
@@ -285,14 +309,17 @@ def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d, order, monkeypatc
         _assert_parity(O[:, h], ref)
 
 
+@pytest.mark.parametrize("waves", ["1", "4"])
 @pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("piece", [4, 1000000])
-def test_multi_head_equals_single_head_runs(gpu, monkeypatch, piece, order):
+def test_multi_head_equals_single_head_runs(gpu, monkeypatch, piece, order, waves):
     """Head h of the multi-head call is bit-identical to a single-head call on
     the head's slice, with and without split windows (H * d > 256 also
     exercises the head groups that bound the partial-result scratch), in
-    either workgroup order."""
+    either workgroup order, with one or four waves per work item (fixed for
+    both calls: the combination of the waves' partials rounds differently)."""
     _head_order(monkeypatch, order)
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     monkeypatch.setenv("F3S_PIECE_BLOCKS", str(piece))
     c = W.make_config(2, with_features=False)
     N, H, d = c["N"], 6, 64
@@ -360,7 +387,9 @@ def test_split_windows_merge_all_feature_sizes(gpu, oracle, monkeypatch, d):
 def test_narrow_gather_ablation_is_bit_identical(gpu, monkeypatch, k):
     """F3S_NARROW_GATHER=1 only changes how K and V rows reach LDS (4-byte
     words instead of 16-byte chunks): same tiles, same arithmetic, so the
-    output is bit-identical; other type pairs are refused."""
+    output is bit-identical (the ablation runs one wave per work item, so the
+    reference does too); other type pairs are refused."""
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", "1")
     c = W.make_config(k)
     q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
     plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])

@@ -101,8 +101,10 @@ def test_f16_output_workloads(gpu, oracle, k):
 def test_f16_output_is_rounded_f32_output_with_split_windows_and_heads(
         gpu, monkeypatch, in_dtype):
     """Split windows (merge kernel) and head groups: fp16 O equals the fp32 O
-    rounded, and bf16-input heads equal single-head runs bit for bit."""
+    rounded, and bf16-input heads equal single-head runs bit for bit (one
+    wave per work item for both, whatever the grid sizes)."""
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", "1")
     c = W.make_config(2, with_features=False)
     N, H, d = c["N"], 5, 64
     rng = np.random.default_rng(17)
