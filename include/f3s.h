@@ -135,7 +135,10 @@ f3s_status_t f3s_run(f3s_plan_t plan, const void *Q, const void *K, const void *
  * All heads run in one launch: window-major while K and V (all heads) fit
  * the 256 MB Infinity Cache, head by head above it (environment
  * F3S_HEAD_MAJOR_BYTES=<bytes> moves that threshold; results are identical
- * either way).
+ * either way).  When a launch would have fewer waves than the GPU has SIMDs
+ * (work items x heads < 1024) four waves share each work item and combine
+ * their partial softmax states (environment F3S_WAVES_PER_ITEM=1 or 4
+ * forces one or the other; the rounding of the combination differs).
  */
 f3s_status_t f3s_run_mh(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                         void *O, int32_t n_heads, int32_t d, float scale,
