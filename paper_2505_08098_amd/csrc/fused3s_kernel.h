@@ -212,7 +212,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const int wv = NW > 1 ? (int)(threadIdx.x >> 6) : 0;
     _Float16 *const tile = tiles[wv];
 
-    const int lane = threadIdx.x & 63;
+    const int lane = NW > 1 ? (int)(threadIdx.x & 63) : (int)threadIdx.x;
     const int i = lane & 15;  // query row (accumulators) / operand row index
     const int g = lane >> 4;  // lane group: selects the reduction slots
     // Workgroups walk the work list item-major (the heads of one window back
