@@ -119,8 +119,8 @@ __device__ __forceinline__ int sanitize_slot(int ncol, int lane)
 // dQ over the row windows of A.  Lane (i, g): query row i of the window;
 // scores and dP as in the forward (S^T = K_hat Q^T, dP^T = V_hat G^T), then
 // dQ^T += K_hat^T dS^T with K_hat read transposed from LDS.
-template <int D, bool kWide, bool kBF16>
-__global__ __launch_bounds__(64)
+template <int D, bool kWide, bool kBF16, int NW = 1>
+__global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
@@ -133,10 +133,16 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     constexpr int NC = D / 32, NT = D / 16, NI = D / 16;
     constexpr int LSK = D + 16;  // K tile: operand reads and transposed reads
     constexpr int LSV = D + 8;   // V tile: operand reads only
-    __shared__ __attribute__((aligned(16))) _Float16 tK[32 * LSK];
-    __shared__ __attribute__((aligned(16))) _Float16 tV[32 * LSV];
+    __shared__ __attribute__((aligned(16))) _Float16 tKs[NW][32 * LSK];
+    __shared__ __attribute__((aligned(16))) _Float16 tVs[NW][32 * LSV];
+    // NW waves may share the work item (as in the forward): wave wv takes a
+    // contiguous share of its block pairs; the partial dQ sums meet in LDS
+    const int wv = NW > 1 ? (int)(threadIdx.x >> 6) : 0;
+    _Float16 *const tK = tKs[wv];
+    _Float16 *const tV = tVs[wv];
 
-    const int lane = threadIdx.x, i = lane & 15, g = lane >> 4;
+    const int lane = NW > 1 ? (int)(threadIdx.x & 63) : (int)threadIdx.x;
+    const int i = lane & 15, g = lane >> 4;
     // window-major, or head by head when K and V exceed the caches (as in
     // the forward)
     const int n_it = gridDim.x / nh;
@@ -152,7 +158,13 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     dQ += (int64_t)head * D;
     const int row = it.window * kWindowRows + i;
     const int rrow = min(row, N - 1);
-    const int b0 = it.blk_begin, b1 = it.blk_end;
+    int b0 = it.blk_begin, b1 = it.blk_end;
+    if constexpr (NW > 1) {
+        const int pairs = (b1 - b0 + 1) >> 1;
+        const int pa = pairs * wv / NW, pb = pairs * (wv + 1) / NW;
+        b1 = min(b1, b0 + 2 * pb);
+        b0 = b0 + 2 * pa;
+    }
 
     h8 q[NC], gq[NC];
 #pragma unroll
@@ -178,7 +190,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     dl += __shfl_xor(dl, 32);
     // one 8-byte record per row and head for the dK/dV pass, which gathers
     // it for every attending row: (base-2 log-sum-exp, delta)
-    if (g == 0 && row < N) stats[(int64_t)row * H + head] = float2{lse2, dl};
+    if (g == 0 && row < N && wv == 0) stats[(int64_t)row * H + head] = float2{lse2, dl};
 
     f4 acc[NT];
 #pragma unroll
@@ -201,7 +213,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     auto step = [&](int b, bool prefetch) {
         stage_pair<D>(tK, LSK, lane, kst);
         stage_pair<D>(tV, LSV, lane, vst);
-        wave_lds_fence();
+        tile_fence<NW>();
         f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0, d0 = s0, d1 = s0;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -248,7 +260,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
             acc[t] = bmma<kBF16>(a, dsh, acc[t]);
             if constexpr (kBF16) acc[t] = bmma<kBF16>(a, dsl, acc[t]);
         }
-        wave_lds_fence();
+        tile_fence<NW>();
     };
     if (b0 < b1) {
         load_cols(b0);
@@ -257,6 +269,24 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
         int b = b0;
         for (; b + 2 < b1; b += 2) step(b, true);
         step(b, false);
+    }
+    if constexpr (NW > 1) {
+        // partial sums into the waves' own K tiles (16 x D floats fit), then
+        // wave 0 adds them (lane (i, g) holds columns 16t + 4g .. +3 of row i)
+        float *ot = reinterpret_cast<float *>(tK);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+            *reinterpret_cast<f4 *>(ot + i * D + 16 * t + 4 * g) = acc[t];
+        __syncthreads();
+        if (wv != 0) return;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const float *ow = reinterpret_cast<const float *>(tKs[w]) + i * D + 4 * g;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[t] += *reinterpret_cast<const f4 *>(ow + 16 * t);
+        }
     }
     float *out;
     if (it.slot < 0) {
@@ -276,8 +306,8 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
 // S[query][key] = Q_hat K_w^T and dP = G_hat V_w^T come out with lane =
 // key, 4 query slots per block, i.e. directly in the B-operand layout of
 // dV^T += G_hat^T P and dK^T += Q_hat^T dS.
-template <int D, bool kWide, bool kBF16>
-__global__ __launch_bounds__(64)
+template <int D, bool kWide, bool kBF16, int NW = 1>
+__global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
@@ -289,11 +319,19 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
 {
     constexpr int NC = D / 32, NT = D / 16, NI = D / 16;
     constexpr int LS = D + 16;  // operand reads and transposed reads
-    __shared__ __attribute__((aligned(16))) _Float16 tQ[32 * LS];
-    __shared__ __attribute__((aligned(16))) _Float16 tG[32 * LS];
-    __shared__ float slse[32], sdel[32];
+    __shared__ __attribute__((aligned(16))) _Float16 tQs[NW][32 * LS];
+    __shared__ __attribute__((aligned(16))) _Float16 tGs[NW][32 * LS];
+    __shared__ float slses[NW][32], sdels[NW][32];
+    // NW waves may share the work item (as in the forward): wave wv takes a
+    // contiguous share of its block pairs; the partial dK, dV sums meet in LDS
+    const int wv = NW > 1 ? (int)(threadIdx.x >> 6) : 0;
+    _Float16 *const tQ = tQs[wv];
+    _Float16 *const tG = tGs[wv];
+    float *const slse = slses[wv];
+    float *const sdel = sdels[wv];
 
-    const int lane = threadIdx.x, i = lane & 15, g = lane >> 4;
+    const int lane = NW > 1 ? (int)(threadIdx.x & 63) : (int)threadIdx.x;
+    const int i = lane & 15, g = lane >> 4;
     // window-major, or head by head when K and V exceed the caches (as in
     // the forward)
     const int n_it = gridDim.x / nh;
@@ -309,7 +347,13 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     dV += (int64_t)head * D;
     const int key = it.window * kWindowRows + i;
     const int rkey = min(key, N - 1);
-    const int b0 = it.blk_begin, b1 = it.blk_end;
+    int b0 = it.blk_begin, b1 = it.blk_end;
+    if constexpr (NW > 1) {
+        const int pairs = (b1 - b0 + 1) >> 1;
+        const int pa = pairs * wv / NW, pb = pairs * (wv + 1) / NW;
+        b1 = min(b1, b0 + 2 * pb);
+        b0 = b0 + 2 * pa;
+    }
 
     h8 kw[NC], vw[NC];
 #pragma unroll
@@ -347,7 +391,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
             slse[lane] = lsev;
             sdel[lane] = delv;
         }
-        wave_lds_fence();
+        tile_fence<NW>();
         f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0, d0 = s0, d1 = s0;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -418,7 +462,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
             ak[t] = bmma<kBF16>(a, dsh, ak[t]);
             if constexpr (kBF16) ak[t] = bmma<kBF16>(a, dsl, ak[t]);
         }
-        wave_lds_fence();
+        tile_fence<NW>();
     };
     if (b0 < b1) {
         load_cols(b0);
@@ -427,6 +471,31 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
         int b = b0;
         for (; b + 2 < b1; b += 2) step(b, true);
         step(b, false);
+    }
+    if constexpr (NW > 1) {
+        // partial sums into the waves' own Q and G tiles (16 x D floats each
+        // fit), then wave 0 adds them
+        float *okt = reinterpret_cast<float *>(tQ);
+        float *ovt = reinterpret_cast<float *>(tG);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            *reinterpret_cast<f4 *>(okt + i * D + 16 * t + 4 * g) = ak[t];
+            *reinterpret_cast<f4 *>(ovt + i * D + 16 * t + 4 * g) = av[t];
+        }
+        __syncthreads();
+        if (wv != 0) return;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) ak[t] = av[t] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            const float *kw_ = reinterpret_cast<const float *>(tQs[w]) + i * D + 4 * g;
+            const float *vw_ = reinterpret_cast<const float *>(tGs[w]) + i * D + 4 * g;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                ak[t] += *reinterpret_cast<const f4 *>(kw_ + 16 * t);
+                av[t] += *reinterpret_cast<const f4 *>(vw_ + 16 * t);
+            }
+        }
     }
     float *ok, *ov;
     if (it.slot < 0) {
@@ -502,13 +571,15 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     const bool head_major = H > 1 && 2ull * p.N * ld * 2 > head_major_threshold();
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
-        auto kern = wide ? k_bwd_dq<D, true, kBF16> : k_bwd_dq<D, false, kBF16>;
+        const int nw = waves_per_item(p.n_blocks, p.n_items, H);
+        auto kern = nw == 4 ? (wide ? k_bwd_dq<D, true, kBF16, 4> : k_bwd_dq<D, false, kBF16, 4>)
+                            : (wide ? k_bwd_dq<D, true, kBF16> : k_bwd_dq<D, false, kBF16>);
         const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
         for (int32_t h0 = 0; h0 < H; h0 += group) {
             const int32_t nh = H - h0 < group ? H - h0 : group;
             if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
             if (p.n_items > 0) {
-                kern<<<(unsigned)((uint64_t)p.n_items * nh), 64, 0, s>>>(
+                kern<<<(unsigned)((uint64_t)p.n_items * nh), 64 * nw, 0, s>>>(
                     p.items, p.cols, p.mask, q, k, v, gr, O, lse, stats, dQ, p.part_o, p.N,
                     ld, h0, nh, sl2, scale, head_major);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -522,7 +593,10 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     }
     // dK, dV: windows of A^T; partials need 2*16*D floats per (piece, head)
     {
-        auto kern = wide ? k_bwd_dkdv<D, true, kBF16> : k_bwd_dkdv<D, false, kBF16>;
+        const int nw = waves_per_item(pt.n_blocks, pt.n_items, H);
+        auto kern = nw == 4
+                        ? (wide ? k_bwd_dkdv<D, true, kBF16, 4> : k_bwd_dkdv<D, false, kBF16, 4>)
+                        : (wide ? k_bwd_dkdv<D, true, kBF16> : k_bwd_dkdv<D, false, kBF16>);
         // the transposed plan's partial rows hold part_row floats
         const int32_t cap = pt.part_row / (2 * D);
         if (pt.n_split > 0 && cap < 1) return hipErrorInvalidValue;
@@ -531,7 +605,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             const int32_t nh = H - h0 < group ? H - h0 : group;
             if (pt.n_split > 0 && (int64_t)nh * 2 * D > pt.part_row) return hipErrorInvalidValue;
             if (pt.n_items > 0) {
-                kern<<<(unsigned)((uint64_t)pt.n_items * nh), 64, 0, s>>>(
+                kern<<<(unsigned)((uint64_t)pt.n_items * nh), 64 * nw, 0, s>>>(
                     pt.items, pt.cols, pt.mask, q, k, v, gr, stats, dK, dV, pt.part_o,
                     pt.N, ld, h0, nh, sl2, scale, head_major);
                 if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -77,13 +77,13 @@ inline uint64_t head_major_threshold()
     const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
     return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
 }
-// Waves sharing one work item of the forward: 4 when a launch would have
+// Waves sharing one work item (forward and backward): 4 when a launch would have
 // fewer waves than the GPU has SIMDs (items x heads < 1024) and the items
 // average at least 4 blocks, else 1 (with more waves the merge and the
 // per-wave Q loads cost more than the parallelism gains: measured 18%
 // slower on the 2048-window sequence workload); F3S_WAVES_PER_ITEM=1 or 4
 // forces it (read at launch).
-inline int forward_waves_per_item(int64_t n_blocks, int64_t n_items, int32_t heads)
+inline int waves_per_item(int64_t n_blocks, int64_t n_items, int32_t heads)
 {
     const char *e = getenv("F3S_WAVES_PER_ITEM");
     if (e && *e) return atoi(e) == 4 ? 4 : 1;

@@ -136,23 +136,6 @@ __device__ __forceinline__ void stage_words(_Float16 *row, int m, h8 w)
         *reinterpret_cast<uint32_t *>(row + 8 * (m0 + cc) + 2 * qd) = words[cc];
 }
 
-// Orders one wave's accesses to its LDS tile.  With one wave per workgroup
-// the workgroup barrier of wave_lds_fence does it; with several waves per
-// workgroup (which run different numbers of block pairs) only this wave may
-// take part: fences at wavefront scope around a wave barrier (a wave's LDS
-// operations run in issue order, so only the compiler has to be held).
-template <int NW>
-__device__ __forceinline__ void tile_fence()
-{
-    if constexpr (NW == 1) {
-        wave_lds_fence();
-    } else {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-    }
-}
-
 // v where sel is all ones, -inf where sel is zero (one bit-select).
 __device__ __forceinline__ float masked_score(float v, int sel)
 {
@@ -623,7 +606,7 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
     const int32_t ld = H * D;
     const bool wide = (uint64_t)p.N * ld * elem_bytes<kIn>() > 0xFFFFFFF0ull;
     // the narrow-gather ablation keeps one wave per item
-    const int nw = kNarrow ? 1 : forward_waves_per_item(p.n_blocks, p.n_items, H);
+    const int nw = kNarrow ? 1 : waves_per_item(p.n_blocks, p.n_items, H);
     auto kern = nw == 4 ? (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow, kNarrow ? 1 : 4>
                                 : k_fused3s<D, false, kIn, kOutH, kNarrow, kNarrow ? 1 : 4>)
                         : (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow>

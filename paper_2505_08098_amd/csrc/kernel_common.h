@@ -74,6 +74,23 @@ __device__ __forceinline__ void wave_lds_fence()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Orders one wave's accesses to its LDS tile.  With one wave per workgroup
+// the workgroup barrier of wave_lds_fence does it; with several waves per
+// workgroup (which run different numbers of block pairs) only this wave may
+// take part: fences at wavefront scope around a wave barrier (a wave's LDS
+// operations run in issue order, so only the compiler has to be held).
+template <int NW>
+__device__ __forceinline__ void tile_fence()
+{
+    if constexpr (NW == 1) {
+        wave_lds_fence();
+    } else {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    }
+}
+
 __device__ __forceinline__ h8 cat44(h4 lo, h4 hi)
 {
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);

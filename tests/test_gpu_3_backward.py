@@ -276,9 +276,13 @@ def test_transpose_workspace_errors(gpu):
         assert L.f3s_last_error() == 1  # F3S_ERR_INVALID_VALUE
 
 
+@pytest.mark.parametrize("waves", ["1", "4"])
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
 @pytest.mark.parametrize("N", [1, 17, 300])
-def test_gradients_random_patterns(gpu, oracle, d, N):
+def test_gradients_random_patterns(gpu, oracle, d, N, waves, monkeypatch):
+    """Every feature size, with one wave per work item or four sharing it
+    (forward and both backward passes; their partial sums combined in LDS)."""
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     rng = np.random.default_rng(d + 7 * N)
     rp, ci = W.random_csr(rng, N, max_deg=min(N, 50), empty_frac=0.1, dup_frac=0.2)
     Q, K, V, G = (rng.standard_normal((N, d)).astype(np.float16) for _ in range(4))
@@ -296,9 +300,10 @@ def test_gradients_workloads(gpu, oracle, k):
                c["scale"])
 
 
+@pytest.mark.parametrize("waves", ["1", "4"])
 @pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("H,d", [(3, 64), (2, 160), (2, 256)])
-def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order):
+def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order, waves):
     """Split windows in both plans; for d > 128 the dK/dV partials of one
     head fill a whole (double-width) partial row of the transposed plan.
     Both workgroup orders of the heads (window-major, the default at this
@@ -307,6 +312,7 @@ def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order
         monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0")
     else:
         monkeypatch.delenv("F3S_HEAD_MAJOR_BYTES", raising=False)
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
     rng = np.random.default_rng(12)
     N = 3000
