@@ -261,7 +261,7 @@ def main():
                                    "fp32 outputs"}))
         sys.exit(2)
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "bench.py measures one GPU: --gpus must be 1"}))
         sys.exit(2)
 
     import numpy as np

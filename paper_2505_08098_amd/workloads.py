@@ -28,7 +28,7 @@ import math
 
 import numpy as np
 
-CONFIGS = {
+WORKLOADS = {
     1: dict(name="er", N=1024, d=64),
     2: dict(name="cl21", N=65536, d=64),
     3: dict(name="cl25", N=1048576, d=128),
@@ -205,9 +205,9 @@ def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
 def make_config(k, seed=0, with_features=True, dtype="f16"):
     """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V);
     dtype "f16" (default), "bf16" or "fp8" selects the feature storage type."""
-    if k not in CONFIGS:
+    if k not in WORKLOADS:
         raise ValueError(f"unknown workload {k}")
-    cfg = CONFIGS[k]
+    cfg = WORKLOADS[k]
     g, f = _streams(seed)
     if k == 1:
         rp, ci = erdos_renyi(g, N=1024, avg_nbrs=15.0)
