@@ -77,11 +77,24 @@ def traffic_from_counters(d):
     return rec.get("hbm_bytes_per_launch")
 
 
+def host_threads():
+    """Threads of the oracle baseline: every core this process may run on
+    (its affinity mask), unless OMP_NUM_THREADS sets the host's CPU share
+    lower.  Returns (threads, affinity core count)."""
+    cores = len(os.sched_getaffinity(0))
+    try:
+        share = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        share = 0
+    return (min(cores, share) if share > 0 else cores), cores
+
+
 def cpu_baseline(c, O_gpu, sample_rows, threads=0):
     import numpy as np
     import oracle
+    affinity = len(os.sched_getaffinity(0))
     if threads <= 0:
-        threads = min(16, len(os.sched_getaffinity(0)))
+        threads, affinity = host_threads()
     r1 = min(c["N"], sample_rows)
     t0 = time.perf_counter()
     ref = oracle.attention_rows_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
@@ -100,10 +113,80 @@ def cpu_baseline(c, O_gpu, sample_rows, threads=0):
     diff = got - ref
     parity = dict(rows=r1, max_abs=float(np.abs(diff).max()),
                   rel_fro=float(np.linalg.norm(diff) / np.linalg.norm(ref)))
-    return dict(value=flops / dt / 1e9, unit="GFLOP/s", cores=threads, kind="oracle",
+    return dict(value=flops / dt / 1e9, unit="GFLOP/s", cores=threads,
+                affinity_cores=affinity, kind="oracle",
                 sample=f"rows 0..{r1} of the same workload ({nnz_sample} nnz, "
                        f"{dt:.2f} s wall, fp64)",
                 ms=dt * 1e3), parity
+
+
+def plan_stats(plan):
+    """The structure metrics of the paper's dataset tables for this pattern:
+    blocks per row window (mean, coefficient of variation, deciles, max),
+    distinct columns per window and non-zeros per 16x16 block."""
+    import numpy as np
+    info = plan.info
+    nb = np.diff(plan.export()["blk_off"]).astype(np.float64)
+    mean = float(nb.mean()) if nb.size else 0.0
+    dec = np.percentile(nb, [10, 20, 30, 40, 50, 60, 70, 80, 90]) if nb.size else [0] * 9
+    return {
+        "windows": int(nb.size),
+        "blocks_per_window": {
+            "mean": round(mean, 3),
+            "cv": round(float(nb.std() / mean), 4) if mean > 0 else 0.0,
+            "deciles_p10_p90": [round(float(x), 1) for x in dec],
+            "max": int(nb.max()) if nb.size else 0,
+        },
+        "unique_cols_per_window": round(info["n_unique"] / max(1, info["n_windows"]), 3),
+        "nnz_per_block": round(info["nnz"] / max(1, info["n_blocks"]), 3),
+        "block_fill": round(info["nnz"] / max(1, 256 * info["n_blocks"]), 4),
+    }
+
+
+def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, reps=5):
+    """Bandwidth ceilings measured in this process with the library's probe
+    kernels: a streaming read, copy and write over 4 GiB (16x the 256 MB
+    Infinity Cache, so DRAM serves them), and the fused kernel's own access
+    pattern on this plan without its arithmetic (f3s_probe_gather; its
+    rate counts the same algorithmic bytes).  Mean of `reps` timed calls
+    after one untimed call each."""
+    import numpy as np
+    import torch
+    import paper_2505_08098_amd as f3s
+
+    def timed(fn):
+        fn()
+        a = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+        b = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+        for k in range(reps):
+            a[k].record(stream)
+            fn()
+            b[k].record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([x.elapsed_time(y) for x, y in zip(a, b)]))
+
+    nbytes = 4 << 30
+    out = {}
+    buf = torch.empty(nbytes // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(buf)
+    sink = torch.zeros(256, dtype=torch.int32, device=dev)
+    f3s.probe_stream("write", buf, stream=stream)
+    out["stream_read_GBs"] = round(nbytes / timed(
+        lambda: f3s.probe_stream("read", buf, sink, stream=stream)) / 1e6, 1)
+    out["stream_copy_GBs"] = round(2 * nbytes / timed(
+        lambda: f3s.probe_stream("copy", buf, dst, stream=stream)) / 1e6, 1)
+    out["stream_write_GBs"] = round(nbytes / timed(
+        lambda: f3s.probe_stream("write", dst, stream=stream)) / 1e6, 1)
+    del buf, dst, sink
+    torch.cuda.empty_cache()
+    out["stream_bytes"] = nbytes
+    if Q is not None:
+        ms = timed(lambda: f3s.probe_gather(plan, Q, K, V, O, stream=stream))
+        out["pattern_gather_ms"] = round(ms, 5)
+        out["pattern_gather_GBs"] = round(alg_bytes / ms / 1e6, 1)
+        out["frac_of_pattern_gather"] = round(achieved_gbs / out["pattern_gather_GBs"], 4)
+    out["frac_of_stream_read"] = round(achieved_gbs / out["stream_read_GBs"], 4)
+    return out
 
 
 def backward_bytes(info, info_t, d, heads=1):
@@ -238,8 +321,8 @@ def main():
                          "fresh seeded N(0,1) features)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--cpu-threads", type=int, default=0,
-                    help="threads of the oracle baseline (default: the host's cores, "
-                         "at most 16)")
+                    help="threads of the oracle baseline (default: every core of the "
+                         "affinity mask, or OMP_NUM_THREADS if that is lower)")
     ap.add_argument("--cpu-rows", type=int, default=1 << 30,
                     help="rows of the workload in the oracle baseline sample")
     ap.add_argument("--backward", action="store_true",
@@ -252,6 +335,9 @@ def main():
                     help="after the timed region, calls timed one by one after a 1 GiB "
                          "scrub write each (L2 and the 256 MB Infinity Cache cold); "
                          "reported as ms_cold_mall, not in value")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the probe kernels (streaming read/copy/write over 4 GiB "
+                         "and the plan's access pattern without arithmetic)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run 3 plain device copies of this many MiB "
                          "(reference dispatches for scaling HBM byte counters)")
@@ -342,6 +428,14 @@ def main():
     achieved = alg_bytes / (ms * 1e-3) / 1e9
     issued = 1024.0 * d * H * info["n_blocks"]  # MFMA flops incl. zero padding
     traffic = traffic_from_counters(d) if H == 1 and not typed else None
+    ceilings = None
+    if not args.no_ceilings:
+        # the pattern probe reads what the fp16 -> fp32 single-head kernel reads
+        plain = H == 1 and not typed and d in (32, 64, 128, 256)
+        # (the probe writes meaningless values: it gets its own output buffer)
+        ceilings = memory_ceilings(plan, Q if plain else None, K, V,
+                                   torch.empty_like(O) if plain else None, d, achieved,
+                                   alg_bytes, stream, dev)
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -378,6 +472,7 @@ def main():
         "plan_ms_warm": round(plan_ms_warm, 3),
         "plan": {k: info[k] for k in ("n_windows", "n_unique", "n_blocks", "max_blocks",
                                       "piece_blocks", "n_items", "n_split", "n_pieces")},
+        "plan_stats": plan_stats(plan),
         "launches_per_call": 1 + (info["n_split"] > 0),
         "roofline": {
             "bound": "hbm",
@@ -386,7 +481,11 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
+            "traffic_kind": "L2-to-fabric bytes per launch (rocprofv3 FETCH_SIZE + "
+                            "WRITE_SIZE, scaled by a copy of known size): HBM reads "
+                            "and writes plus Infinity-Cache hits",
             "algorithmic_bytes_per_launch": alg_bytes,
+            "measured_ceilings": ceilings,
             "kernel": "k_fused3s<%d>" % d + (" %s->%s" % (args.in_dtype, args.out_dtype)
                                               if typed else "")
                       + (" x %d heads" % H if H > 1 else ""),

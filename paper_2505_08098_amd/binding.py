@@ -100,6 +100,14 @@ def load_library():
     L.f3s_backward_typed.argtypes = ([vp, vp, vp, vp, vp, i32] + [vp] * 7 +
                                      [i32, i32, ctypes.c_float, vp])
     L.f3s_backward_typed.restype = ctypes.c_int
+    L.f3s_probe_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
+    L.f3s_probe_read.restype = ctypes.c_int
+    L.f3s_probe_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]
+    L.f3s_probe_copy.restype = ctypes.c_int
+    L.f3s_probe_write.argtypes = [vp, ctypes.c_size_t, ctypes.c_uint32, vp]
+    L.f3s_probe_write.restype = ctypes.c_int
+    L.f3s_probe_gather.argtypes = [vp, vp, vp, vp, vp, i32, vp]
+    L.f3s_probe_gather.restype = ctypes.c_int
     L.f3s_destroy.argtypes = [vp]
     L.f3s_destroy.restype = None
     L.f3s_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
@@ -118,13 +126,18 @@ def status_string(code):
     return load_library().f3s_status_string(int(code)).decode()
 
 
-def _check_device_tensor(t, name, dtype):
+def _check_device_tensor(t, name, dtype, device=None):
+    """A contiguous device tensor of `dtype`, on `device` when one is given
+    (the library writes through the raw pointer, so a tensor on another
+    device or of another size is never handed to it)."""
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise TypeError(f"{name} must be a device tensor")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the operands on {device}")
 
 
 def _qkv_shape(Q):
@@ -245,7 +258,7 @@ def run(plan, Q, K, V, scale=None, out=None, stream=None):
     L = load_library()
     shape = tuple(Q.shape)
     for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
-        _check_device_tensor(t, n, torch.float16)
+        _check_device_tensor(t, n, torch.float16, plan.device)
         if t.dim() not in (2, 3) or t.shape[0] != plan.N:
             raise ValueError(f"{n} must be [N, d] or [N, H, d] with N = {plan.N}")
         if tuple(t.shape) != shape:
@@ -255,7 +268,7 @@ def run(plan, Q, K, V, scale=None, out=None, stream=None):
     if out is None:
         out = torch.empty(shape, dtype=torch.float32, device=Q.device)
     else:
-        _check_device_tensor(out, "out", torch.float32)
+        _check_device_tensor(out, "out", torch.float32, Q.device)
         if tuple(out.shape) != shape:
             raise ValueError("out must have the shape of Q")
     if scale is None:
@@ -274,18 +287,20 @@ def forward(plan, Q, K, V, scale=None, out=None, lse=None, stream=None):
     """f3s_forward: returns (O, lse) with lse fp32 [N] or [N, H]."""
     shape = _qkv_shape(Q)
     H = shape[1] if len(shape) == 3 else 1
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check_device_tensor(t, n, torch.float16, plan.device)
+        if tuple(t.shape) != shape or shape[0] != plan.N:
+            raise ValueError("Q, K, V must share one [N, d] / [N, H, d] shape")
     if lse is None:
         lse = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
-    _check_device_tensor(lse, "lse", torch.float32)
+    _check_device_tensor(lse, "lse", torch.float32, Q.device)
     if lse.numel() != plan.N * H:
         raise ValueError("lse must hold N * H values")
     if out is None:
         out = torch.empty(shape, dtype=torch.float32, device=Q.device)
-    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
-        _check_device_tensor(t, n, torch.float16)
-        if tuple(t.shape) != shape or shape[0] != plan.N:
-            raise ValueError("Q, K, V must share one [N, d] / [N, H, d] shape")
-    _check_device_tensor(out, "out", torch.float32)
+    _check_device_tensor(out, "out", torch.float32, Q.device)
+    if tuple(out.shape) != shape:
+        raise ValueError("out must have the shape of Q")
     d = shape[-1]
     if scale is None:
         scale = 1.0 / math.sqrt(d)
@@ -314,18 +329,18 @@ def forward_typed(plan, Q, K, V, out_dtype=torch.float32, scale=None, out=None,
     if Q.dtype not in (torch.float16, torch.bfloat16, torch.float8_e4m3fn):
         raise TypeError(f"Q must be float16, bfloat16 or float8_e4m3fn, got {Q.dtype}")
     for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
-        _check_device_tensor(t, n, Q.dtype)
+        _check_device_tensor(t, n, Q.dtype, plan.device)
         if tuple(t.shape) != shape or shape[0] != plan.N:
             raise ValueError("Q, K, V must share one [N, d] / [N, H, d] shape")
     if out is None:
         out = torch.empty(shape, dtype=out_dtype, device=Q.device)
-    _check_device_tensor(out, "out", out_dtype)
+    _check_device_tensor(out, "out", out_dtype, Q.device)
     if tuple(out.shape) != shape:
         raise ValueError("out must have the shape of Q")
     if lse is None and want_lse:
         lse = torch.empty(shape[:-1], dtype=torch.float32, device=Q.device)
     if lse is not None:
-        _check_device_tensor(lse, "lse", torch.float32)
+        _check_device_tensor(lse, "lse", torch.float32, Q.device)
         if lse.numel() != plan.N * H:
             raise ValueError("lse must hold N * H values")
     d = shape[-1]
@@ -353,11 +368,11 @@ def backward(plan, plan_t, Q, K, V, O, dO, lse, scale=None, stream=None):
     if Q.dtype not in (torch.float16, torch.bfloat16):
         raise TypeError("Q, K, V, dO must be float16 or bfloat16")
     for t, n in ((Q, "Q"), (K, "K"), (V, "V"), (dO, "dO")):
-        _check_device_tensor(t, n, Q.dtype)
-        if tuple(t.shape) != shape:
-            raise ValueError(f"{n} must have the shape of Q")
-    _check_device_tensor(O, "O", torch.float32)
-    _check_device_tensor(lse, "lse", torch.float32)
+        _check_device_tensor(t, n, Q.dtype, plan.device)
+        if tuple(t.shape) != shape or shape[0] != plan.N:
+            raise ValueError(f"{n} must have the shape of Q, with N = {plan.N} rows")
+    _check_device_tensor(O, "O", torch.float32, Q.device)
+    _check_device_tensor(lse, "lse", torch.float32, Q.device)
     if tuple(O.shape) != shape or lse.numel() != plan.N * H:
         raise ValueError("O must match Q; lse must hold N * H values")
     dQ, dK, dV = (torch.empty(shape, dtype=torch.float32, device=Q.device) for _ in range(3))
@@ -380,3 +395,51 @@ def run_raw(plan, q_ptr, k_ptr, v_ptr, o_ptr, d, scale, stream_handle):
     """f3s_run on raw device addresses (returns the status code)."""
     return load_library().f3s_run(plan.handle, q_ptr, k_ptr, v_ptr, o_ptr, int(d),
                                   float(scale), ctypes.c_void_p(stream_handle))
+
+
+def probe_stream(kind, buf, out=None, stream=None):
+    """One streaming probe over the bytes of device tensor ``buf``:
+    kind "read" (out: a uint32 device tensor of >= 256 elements, the
+    never-written sink), "copy" (out: a tensor of buf's size) or "write"."""
+    L = load_library()
+    if not isinstance(buf, torch.Tensor) or not buf.is_cuda or not buf.is_contiguous():
+        raise TypeError("buf must be a contiguous device tensor")
+    nbytes = buf.numel() * buf.element_size()
+    if stream is None:
+        stream = torch.cuda.current_stream(buf.device)
+    s = ctypes.c_void_p(stream.cuda_stream)
+    if kind == "read":
+        if out is None or out.numel() * out.element_size() < 1024 or out.device != buf.device:
+            raise ValueError("read needs a sink of at least 1 KiB on buf's device")
+        rc = L.f3s_probe_read(buf.data_ptr(), nbytes, out.data_ptr(), s)
+    elif kind == "copy":
+        if (out is None or out.numel() * out.element_size() != nbytes
+                or out.device != buf.device or not out.is_contiguous()):
+            raise ValueError("copy needs a contiguous destination of buf's size and device")
+        rc = L.f3s_probe_copy(buf.data_ptr(), out.data_ptr(), nbytes, s)
+    elif kind == "write":
+        rc = L.f3s_probe_write(buf.data_ptr(), nbytes, 0x5A5A5A5A, s)
+    else:
+        raise ValueError(f"unknown probe {kind}")
+    if rc != F3S_OK:
+        raise F3SError(rc, f"f3s_probe_{kind}")
+
+
+def probe_gather(plan, Q, K, V, out, stream=None):
+    """f3s_probe_gather: the fused kernel's memory accesses on ``plan`` for
+    fp16 Q, K, V [N, d] and fp32 out [N, d], without its arithmetic."""
+    shape = tuple(Q.shape)
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check_device_tensor(t, n, torch.float16, plan.device)
+        if t.dim() != 2 or tuple(t.shape) != shape or shape[0] != plan.N:
+            raise ValueError("Q, K, V must be [N, d]")
+    _check_device_tensor(out, "out", torch.float32, plan.device)
+    if tuple(out.shape) != shape:
+        raise ValueError("out must have the shape of Q")
+    if stream is None:
+        stream = torch.cuda.current_stream(Q.device)
+    rc = load_library().f3s_probe_gather(plan.handle, Q.data_ptr(), K.data_ptr(),
+                                         V.data_ptr(), out.data_ptr(), int(shape[1]),
+                                         ctypes.c_void_p(stream.cuda_stream))
+    if rc != F3S_OK:
+        raise F3SError(rc, "f3s_probe_gather")

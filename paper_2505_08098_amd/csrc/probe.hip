@@ -1,0 +1,227 @@
+// Memory-system probes: plain streaming kernels and the fused kernel's access
+// pattern without its arithmetic.  They give the bandwidth ceilings the fused
+// kernel is measured against (what HBM delivers to a streaming read or copy
+// on this GPU, and what the caches and HBM together deliver to a plan's
+// gathers), measured in the same process as the kernel.
+#include "f3s_probe.h"
+#include "f3s_internal.h"
+
+namespace {
+
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 16;      // 16-byte loads in flight per thread
+constexpr uint32_t kNever = 0x9E3779B9u;
+
+__device__ __forceinline__ uint32_t fold(u4 v) { return v.x ^ v.y ^ v.z ^ v.w; }
+
+// Each workgroup reads one contiguous tile of kThreads * kUnroll 16-byte
+// chunks (coalesced: chunk t + kThreads * u).  The loaded values feed a
+// store that practically never happens, which keeps every load live.
+__global__ __launch_bounds__(kThreads) void k_probe_read(const u4 *__restrict__ src,
+                                                         uint64_t n16,
+                                                         uint32_t *__restrict__ sink)
+{
+    const uint64_t base = (uint64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+    u4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const uint64_t k = base + (uint64_t)kThreads * u;
+        v[u] = k < n16 ? src[k] : u4{0u, 0u, 0u, 0u};
+    }
+    uint32_t acc = 0;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) acc ^= fold(v[u]);
+    if (acc == kNever) sink[threadIdx.x] = acc;
+}
+
+__global__ __launch_bounds__(kThreads) void k_probe_copy(const u4 *__restrict__ src,
+                                                         u4 *__restrict__ dst, uint64_t n16)
+{
+    const uint64_t base = (uint64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+    u4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const uint64_t k = base + (uint64_t)kThreads * u;
+        if (k < n16) v[u] = src[k];
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const uint64_t k = base + (uint64_t)kThreads * u;
+        if (k < n16) dst[k] = v[u];
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_probe_write(u4 *__restrict__ dst, uint64_t n16,
+                                                          uint32_t value)
+{
+    const uint64_t base = (uint64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+        const uint64_t k = base + (uint64_t)kThreads * u;
+        if (k < n16) dst[k] = u4{value, value ^ (uint32_t)u, value, (uint32_t)k};
+    }
+}
+
+// The fp16 -> fp32 fused kernel's memory accesses for one work item, with no
+// arithmetic: the item record, the window's Q rows, per block its 16 column
+// ids and 8 bitmap words, the K and V rows of every slot gathered in 16-byte
+// chunks laid flat over the lanes (a lane quad reads 64 contiguous bytes of
+// one row, padding slots re-read the block's first column), and 16 rows of
+// D fp32 written (to O for a whole window, to the piece's partial slot for a
+// piece of a split window).  Four waves share an item, wave w taking block
+// pairs w, w + 4, ...; each wave has two pairs in flight.  The written
+// values are the loaded bits folded together (garbage, but they keep every
+// load live).
+template <int D, bool kWide>
+__global__ __launch_bounds__(256) void k_probe_gather(
+    const f3s::WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
+    const uint32_t *__restrict__ mask, const char *__restrict__ Q,
+    const char *__restrict__ K, const char *__restrict__ V, float *__restrict__ O,
+    float *__restrict__ part_o, int32_t N)
+{
+    constexpr int LPR = D / 8;   // 16-byte chunks per row
+    constexpr int NI = D / 16;   // chunks per lane per 32-row tile
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const f3s::WorkItem it = items[blockIdx.x];
+    uint32_t acc = 0;
+    // Q: rows 4 wv .. 4 wv + 3 of the window (pad rows read row N - 1)
+    for (int f = lane; f < 4 * LPR; f += 64) {
+        const int r = it.window * 16 + 4 * wv + f / LPR;
+        acc ^= fold(*reinterpret_cast<const u4 *>(Q + ((int64_t)min(r, N - 1) * D) * 2 +
+                                                  16 * (f % LPR)));
+    }
+    const int b0 = it.blk_begin, b1 = it.blk_end;
+    for (int b = b0 + 2 * wv; b < b1; b += 16) {
+        // pairs b and b + 8 of this wave (the second one if it exists)
+        const int npp = b + 8 < b1 ? 2 : 1;
+        u4 kv[2][2 * NI];
+        uint32_t mw[2] = {0u, 0u};
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            if (pp >= npp) break;
+            const int bb = b + 8 * pp;
+            const int slot = lane & 31;
+            const int blk = slot < 16 ? bb : min(bb + 1, b1 - 1);
+            int c = cols[(int64_t)16 * blk + (slot & 15)];
+            const int first = cols[(int64_t)16 * blk];
+            c = c < 0 ? first : c;
+#pragma unroll
+            for (int j = 0; j < NI; ++j) {
+                const int f = lane + 64 * j;
+                const int col = __shfl(c, f / LPR);
+                if constexpr (kWide) {
+                    const int64_t off = (int64_t)col * D * 2 + 16 * (f % LPR);
+                    kv[pp][2 * j] = *reinterpret_cast<const u4 *>(K + off);
+                    kv[pp][2 * j + 1] = *reinterpret_cast<const u4 *>(V + off);
+                } else {
+                    const uint32_t off = (uint32_t)col * (uint32_t)(2 * D) + 16u * (f % LPR);
+                    kv[pp][2 * j] = *reinterpret_cast<const u4 *>(K + off);
+                    kv[pp][2 * j + 1] = *reinterpret_cast<const u4 *>(V + off);
+                }
+            }
+            mw[pp] = mask[(int64_t)8 * bb + (lane >> 3)] ^
+                     mask[(int64_t)8 * min(bb + 1, b1 - 1) + (lane >> 3)];
+        }
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp) {
+            if (pp >= npp) break;
+            acc ^= mw[pp];
+#pragma unroll
+            for (int j = 0; j < 2 * NI; ++j) acc ^= fold(kv[pp][j]);
+        }
+    }
+    // 16 x D fp32 out: wave wv writes rows 4 wv .. 4 wv + 3
+    const float val = __builtin_bit_cast(float, acc & 0x3FFFFFFFu);
+    for (int f = lane; f < 4 * (D / 4); f += 64) {
+        const int rr = 4 * wv + f / (D / 4), cc = 4 * (f % (D / 4));
+        const float4 v4 = make_float4(val, val, val, val);
+        if (it.slot < 0) {
+            const int r = it.window * 16 + rr;
+            if (r < N) *reinterpret_cast<float4 *>(O + (int64_t)r * D + cc) = v4;
+        } else {
+            *reinterpret_cast<float4 *>(part_o + ((int64_t)it.slot * 16 + rr) * D + cc) = v4;
+        }
+    }
+}
+
+template <int D>
+hipError_t launch_gather_d(const f3s_plan_s &p, const void *Q, const void *K, const void *V,
+                           float *O, hipStream_t s)
+{
+    const bool wide = (uint64_t)p.N * D * 2 > 0xFFFFFFF0ull;
+    auto kern = wide ? k_probe_gather<D, true> : k_probe_gather<D, false>;
+    kern<<<p.n_items, 256, 0, s>>>(p.items, p.cols, p.mask, static_cast<const char *>(Q),
+                                   static_cast<const char *>(K),
+                                   static_cast<const char *>(V), O, p.part_o, p.N);
+    return hipGetLastError();
+}
+
+f3s_status_t status(hipError_t e)
+{
+    return e == hipSuccess ? F3S_OK : F3S_ERR_HIP;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+unsigned tiles(uint64_t n16)
+{
+    return (unsigned)((n16 + kThreads * kUnroll - 1) / (kThreads * kUnroll));
+}
+
+}  // namespace
+
+extern "C" {
+
+f3s_status_t f3s_probe_read(const void *src, size_t bytes, uint32_t *sink, hipStream_t stream)
+{
+    if (!src || !sink || !aligned16(src) || bytes % 16 ||
+        bytes / 16 / (kThreads * kUnroll) >= 0x7FFFFFFFull)
+        return F3S_ERR_INVALID_VALUE;
+    const uint64_t n16 = bytes / 16;
+    if (n16 == 0) return F3S_OK;
+    k_probe_read<<<tiles(n16), kThreads, 0, stream>>>(static_cast<const u4 *>(src), n16, sink);
+    return status(hipGetLastError());
+}
+
+f3s_status_t f3s_probe_copy(const void *src, void *dst, size_t bytes, hipStream_t stream)
+{
+    if (!src || !dst || !aligned16(src) || !aligned16(dst) || bytes % 16 ||
+        bytes / 16 / (kThreads * kUnroll) >= 0x7FFFFFFFull)
+        return F3S_ERR_INVALID_VALUE;
+    const uint64_t n16 = bytes / 16;
+    if (n16 == 0) return F3S_OK;
+    k_probe_copy<<<tiles(n16), kThreads, 0, stream>>>(static_cast<const u4 *>(src),
+                                                       static_cast<u4 *>(dst), n16);
+    return status(hipGetLastError());
+}
+
+f3s_status_t f3s_probe_write(void *dst, size_t bytes, uint32_t value, hipStream_t stream)
+{
+    if (!dst || !aligned16(dst) || bytes % 16 ||
+        bytes / 16 / (kThreads * kUnroll) >= 0x7FFFFFFFull)
+        return F3S_ERR_INVALID_VALUE;
+    const uint64_t n16 = bytes / 16;
+    if (n16 == 0) return F3S_OK;
+    k_probe_write<<<tiles(n16), kThreads, 0, stream>>>(static_cast<u4 *>(dst), n16, value);
+    return status(hipGetLastError());
+}
+
+f3s_status_t f3s_probe_gather(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                              float *O, int32_t d, hipStream_t stream)
+{
+    if (!p || !Q || !K || !V || !O) return F3S_ERR_INVALID_VALUE;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O))
+        return F3S_ERR_INVALID_VALUE;
+    if (p->N == 0 || p->n_items == 0) return F3S_OK;
+    switch (d) {
+    case 32: return status(launch_gather_d<32>(*p, Q, K, V, O, stream));
+    case 64: return status(launch_gather_d<64>(*p, Q, K, V, O, stream));
+    case 128: return status(launch_gather_d<128>(*p, Q, K, V, O, stream));
+    case 256: return status(launch_gather_d<256>(*p, Q, K, V, O, stream));
+    default: return F3S_ERR_UNSUPPORTED;
+    }
+}
+
+}  // extern "C"

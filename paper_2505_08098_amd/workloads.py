@@ -24,6 +24,7 @@ Every generator is deterministic in its seed: one child stream of
 ``numpy.random.SeedSequence(seed)`` draws the graph, a second draws Q, K, V
 (float32 N(0,1) rounded to fp16 with round-to-nearest-even).
 """
+import functools
 import math
 
 import numpy as np
@@ -202,13 +203,11 @@ def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
                           self_loops=False, symmetric=False)
 
 
-def make_config(k, seed=0, with_features=True, dtype="f16"):
-    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V);
-    dtype "f16" (default), "bf16" or "fp8" selects the feature storage type."""
-    if k not in WORKLOADS:
-        raise ValueError(f"unknown workload {k}")
-    cfg = WORKLOADS[k]
-    g, f = _streams(seed)
+@functools.lru_cache(maxsize=2)
+def _graph(k, seed):
+    """The CSR of workload k (drawn from the graph stream only; the last two
+    are kept, the million-node graph taking tens of seconds to draw)."""
+    g, _ = _streams(seed)
     if k == 1:
         rp, ci = erdos_renyi(g, N=1024, avg_nbrs=15.0)
     elif k == 2:
@@ -219,6 +218,20 @@ def make_config(k, seed=0, with_features=True, dtype="f16"):
         rp, ci = molecules(g)
     else:
         rp, ci = sequence_window_random(g)
+    rp.flags.writeable = False
+    ci.flags.writeable = False
+    return rp, ci
+
+
+def make_config(k, seed=0, with_features=True, dtype="f16"):
+    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V);
+    dtype "f16" (default), "bf16" or "fp8" selects the feature storage type.
+    row_ptr and col_idx are fresh copies (callers may modify them)."""
+    if k not in WORKLOADS:
+        raise ValueError(f"unknown workload {k}")
+    cfg = WORKLOADS[k]
+    _, f = _streams(seed)
+    rp, ci = (a.copy() for a in _graph(k, seed))
     N = len(rp) - 1
     d = cfg["d"]
     out = dict(name=cfg["name"], N=N, d=d, scale=1.0 / math.sqrt(d),

@@ -14,6 +14,7 @@ import pytest
 import torch
 
 from paper_2505_08098_amd import workloads as W
+from _subproblem import rows_subproblem
 
 pytestmark = pytest.mark.gpu
 
@@ -280,6 +281,33 @@ def test_run_argument_errors(gpu):
     assert gpu.status_string(2) == "F3S_ERR_INVALID_CSR"
 
 
+def test_binding_rejects_wrong_out_and_lse_before_launch(gpu):
+    """A caller-supplied out or lse of the wrong shape, or an operand on
+    another device than the plan, is refused by the binding before any
+    launch (the library writes N * H * d values through the pointer)."""
+    c = W.make_config(1)
+    N, d = c["N"], c["d"]
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), N)
+    Q = _dev(c["Q"])
+    sentinel = -7.0
+    for shape in ((N - 1, d), (N, d // 2), (N, 2, d)):
+        out = torch.full(shape, sentinel, dtype=torch.float32, device=DEV)
+        with pytest.raises(ValueError):
+            gpu.forward(plan, Q, Q, Q, out=out)
+        with pytest.raises(ValueError):
+            gpu.run(plan, Q, Q, Q, out=out)
+        with pytest.raises(ValueError):
+            gpu.forward_typed(plan, Q, Q, Q, out=out)
+        torch.cuda.synchronize()
+        assert bool((out == sentinel).all())
+    with pytest.raises(ValueError):
+        gpu.forward(plan, Q, Q, Q, lse=torch.empty(N - 1, device=DEV))
+    with pytest.raises(TypeError):     # a host tensor
+        gpu.forward(plan, Q, Q, Q, out=torch.empty((N, d)))
+    with pytest.raises(TypeError):
+        gpu.forward(plan, Q, Q, Q, lse=torch.empty(N))
+
+
 def _head_order(monkeypatch, order):
     """Workgroup order of several heads: item-major below the K/V size
     threshold (the default for these small inputs), head-major above it
@@ -307,6 +335,40 @@ def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d, order, monkeypatc
     for h in range(H):
         ref = oracle.attention_f64(rp, ci, Q[:, h], K[:, h], V[:, h], scale)
         _assert_parity(O[:, h], ref)
+
+
+@pytest.mark.parametrize("k,H", [(2, 4), (5, 4), (3, 2)])
+def test_multi_head_workloads(gpu, oracle, k, H):
+    """Several heads over a workload graph (fresh seeded N(0,1) features of
+    shape [N, H, d]); each head against the oracle, on every row for the
+    smaller graphs and, for the million-node graph, on the sub-problem of
+    20,000 random rows and the 8 longest rows with their full neighbour
+    lists (the rows' outputs are exact there)."""
+    c = W.make_config(k, with_features=False)
+    rp, ci, N, d = c["row_ptr"], c["col_idx"], c["N"], c["d"]
+    rng = np.random.default_rng(40 + k)
+    X = [rng.standard_normal((N, H, d), dtype=np.float32).astype(np.float16)
+         for _ in range(3)]
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    O = gpu.run(plan, *(_dev(x) for x in X), scale=c["scale"])
+    torch.cuda.synchronize()
+    print(f"workload {k}, {H} heads, N={N} d={d}", flush=True)
+    if k == 3:
+        rows = np.unique(np.concatenate([rng.integers(0, N, size=20000),
+                                         np.argsort(np.diff(rp), kind="stable")[-8:]]))
+        mrp, mci, U = rows_subproblem(rp, ci, rows)
+        sel = torch.from_numpy(rows).to(DEV)
+        got = O.index_select(0, sel).cpu().numpy()
+        for h in range(H):
+            ref = oracle.attention_f64(mrp, mci, *(np.ascontiguousarray(x[U, h]) for x in X),
+                                       c["scale"])
+            _assert_parity(got[:, h], ref[np.searchsorted(U, rows)])
+    else:
+        O = O.cpu().numpy()
+        for h in range(H):
+            ref = oracle.attention_f64(rp, ci, *(np.ascontiguousarray(x[:, h]) for x in X),
+                                       c["scale"])
+            _assert_parity(O[:, h], ref)
 
 
 @pytest.mark.parametrize("waves", ["1", "4"])

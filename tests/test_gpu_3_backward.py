@@ -16,6 +16,7 @@ import pytest
 import torch
 
 from paper_2505_08098_amd import workloads as W
+from _subproblem import rows_attending, rows_subproblem, sample_keys
 
 pytestmark = pytest.mark.gpu
 
@@ -237,7 +238,7 @@ def test_gradients_bf16_split_windows_and_heads(gpu, oracle, monkeypatch, H, d):
     _grad_case_bf16(gpu, oracle, rp, ci, N, Qb, Kb, Vb, Gb, 1.0 / math.sqrt(d))
 
 
-@pytest.mark.parametrize("k", [1, 4, 2])
+@pytest.mark.parametrize("k", [1, 4, 2, 5])
 def test_gradients_bf16_workloads(gpu, oracle, k):
     c = W.make_config(k, dtype="bf16")
     print(f"workload {k} bf16 backward N={c['N']} d={c['d']}", flush=True)
@@ -290,7 +291,7 @@ def test_gradients_random_patterns(gpu, oracle, d, N, waves, monkeypatch):
     _grad_case(gpu, oracle, rp, ci, N, Q, K, V, G, 1 / math.sqrt(d))
 
 
-@pytest.mark.parametrize("k", [1, 4, 2])
+@pytest.mark.parametrize("k", [1, 4, 2, 5])
 def test_gradients_workloads(gpu, oracle, k):
     c = W.make_config(k)
     rng = np.random.default_rng(11)
@@ -324,6 +325,47 @@ def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order
     Q, K, V, G = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(4))
     plan, plan_t = _grad_case(gpu, oracle, rp, ci, N, Q, K, V, G, 0.125)
     assert plan.info["n_split"] > 0 and plan_t.info["n_split"] > 0
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_gradients_million_node_workload_sampled(gpu, oracle, dtype):
+    """The 1,048,576-node Chung-Lu workload (d = 128), whole backward on the
+    GPU; the oracle runs on the sub-problem of 500 random keys and the 4
+    heaviest keys (hubs of about 4,000 attending rows), every row attending
+    to them with its full neighbour list: dQ is exact there on every one of
+    those rows (about 25,000), dK and dV on the sampled keys."""
+    c = W.make_config(3, dtype=dtype)
+    rp, ci, N, scale = c["row_ptr"], c["col_idx"], c["N"], c["scale"]
+    rng = np.random.default_rng(31)
+    g32 = rng.standard_normal(c["Q"].shape, dtype=np.float32)
+    G = W.to_bf16_bits(g32) if dtype == "bf16" else g32.astype(np.float16)
+    dev = _bf16_dev if dtype == "bf16" else _dev
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    plan_t = plan.transpose()
+    q, k, v, g = (dev(x) for x in (c["Q"], c["K"], c["V"], G))
+    if dtype == "bf16":
+        O, lse = gpu.forward_typed(plan, q, k, v, scale=scale, want_lse=True)
+    else:
+        O, lse = gpu.forward(plan, q, k, v, scale=scale)
+    dQ, dK, dV = gpu.backward(plan, plan_t, q, k, v, O, g, lse, scale=scale)
+    torch.cuda.synchronize()
+    del O, lse, q, k, v, g
+    S = sample_keys(rp, ci, 500, 4, rng)
+    R = np.union1d(S, rows_attending(rp, ci, S))
+    mrp, mci, U = rows_subproblem(rp, ci, R)
+    print(f"  {dtype}: {S.size} keys, {R.size} rows, sub-problem of {U.size} nodes and "
+          f"{mci.size} entries", flush=True)
+    sub = [x[U] for x in (c["Q"], c["K"], c["V"], G)]
+    if dtype == "bf16":
+        sub = [oracle.widen_bf16(x) for x in sub]
+    ref = oracle.attention_bwd_f64(mrp, mci, *sub, scale)
+    for name, got, r, rows in (("dQ", dQ, ref[0], R), ("dK", dK, ref[1], S),
+                               ("dV", dV, ref[2], S)):
+        sel = torch.from_numpy(rows).to(DEV)
+        _check(f"{dtype} {name}", got.index_select(0, sel).cpu().numpy(),
+               r[np.searchsorted(U, rows)])
+    plan.close()
+    plan_t.close()
 
 
 def test_backward_is_deterministic(gpu):

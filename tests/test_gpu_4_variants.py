@@ -49,7 +49,7 @@ def _check(got, ref, max_abs=MAX_ABS, rel_fro=REL_FRO):
     assert ma <= max_abs and rf <= rel_fro, (ma, rf)
 
 
-@pytest.mark.parametrize("k", [1, 2, 4, 5])
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 3])
 def test_bf16_inputs_workloads(gpu, oracle, k):
     c = W.make_config(k, dtype="bf16")
     print(f"workload {k} bf16 N={c['N']} d={c['d']}", flush=True)
@@ -82,9 +82,10 @@ def test_bf16_inputs_feature_sizes(gpu, oracle, d, out_dtype):
         _check(O.float().cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("k", [1, 2, 4])
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 3])
 def test_f16_output_workloads(gpu, oracle, k):
     c = W.make_config(k)
+    print(f"workload {k} fp16 out N={c['N']} d={c['d']}", flush=True)
     plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
     q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
     O16, _ = gpu.forward_typed(plan, q, kk, v, out_dtype=torch.float16, scale=c["scale"])
@@ -187,7 +188,7 @@ def _fp8_dev(bits):
     return _dev(bits).view(torch.float8_e4m3fn)
 
 
-@pytest.mark.parametrize("k", [1, 2, 4, 5])
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 3])
 def test_fp8_inputs_workloads(gpu, oracle, k):
     c = W.make_config(k, dtype="fp8")
     print(f"workload {k} fp8 N={c['N']} d={c['d']}", flush=True)

@@ -1,0 +1,59 @@
+"""The memory-system probe kernels (f3s_probe.h) that bench.py uses for its
+measured bandwidth ceilings: the copy and write probes move exactly the bytes
+they are given, the read probe leaves its sink alone (in practice), and the
+access-pattern probe runs on every workload plan and on split windows
+without touching memory outside O and the plan's own buffers."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2505_08098_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def test_stream_probes_move_the_given_bytes(gpu):
+    n = (64 << 20) // 4 + 4 * 1000 + 4      # not a whole number of probe tiles
+    src = torch.arange(n, dtype=torch.int32, device=DEV)
+    guard = torch.full((n + 64,), -1, dtype=torch.int32, device=DEV)
+    dst = guard[:n]
+    gpu.probe_stream("copy", src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src) and bool((guard[n:] == -1).all())
+    guard.fill_(-1)
+    gpu.probe_stream("write", dst)
+    torch.cuda.synchronize()
+    assert bool((guard[n:] == -1).all()) and not bool((dst == -1).any())
+    sink = torch.zeros(256, dtype=torch.int32, device=DEV)
+    gpu.probe_stream("read", src, sink)
+    torch.cuda.synchronize()
+    with pytest.raises(ValueError):
+        gpu.probe_stream("copy", src, dst[:-4])
+    L = gpu.load_library()
+    assert L.f3s_probe_read(src.data_ptr() + 4, 64, sink.data_ptr(), None) == 1
+    assert L.f3s_probe_copy(src.data_ptr(), dst.data_ptr(), 20, None) == 1
+
+
+@pytest.mark.parametrize("k", [1, 2, 4, 5])
+def test_pattern_probe_runs_on_the_workload_plans(gpu, k, monkeypatch):
+    if k == 2:
+        monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")   # many split windows
+    c = W.make_config(k)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
+    guard = torch.full((c["N"] + 16, c["d"]), -3.0, dtype=torch.float32, device=DEV)
+    O = guard[: c["N"]]
+    gpu.probe_gather(plan, q, kk, v, O)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(O).all())
+    assert bool((guard[c["N"]:] == -3.0).all())
+    # the operator still gives its result on the same plan afterwards
+    O2 = gpu.run(plan, q, kk, v, scale=c["scale"])
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(O2).all())
