@@ -40,7 +40,9 @@ typedef enum {
     F3S_ERR_INVALID_CSR = 2,   /* row_ptr[0] != 0, decreasing, column not in [0,N) */
     F3S_ERR_UNSUPPORTED = 3,   /* d not a multiple of 32 in [32, 256]           */
     F3S_ERR_OUT_OF_MEMORY = 4, /* a device allocation failed                    */
-    F3S_ERR_HIP = 5            /* any other HIP runtime error                   */
+    F3S_ERR_HIP = 5,           /* any other HIP runtime error                   */
+    F3S_ERR_TOO_LARGE = 6      /* the call needs more than a fixed capacity of
+                                  the library (f3s_backward_noalloc)            */
 } f3s_status_t;
 
 typedef struct f3s_plan_s *f3s_plan_t;
@@ -255,6 +257,32 @@ f3s_status_t f3s_backward_typed(f3s_plan_t plan, f3s_plan_t plan_t, const void *
                                 const float *O, const void *dO, const float *lse,
                                 float *row_stats, float *dQ, float *dK, float *dV,
                                 int32_t n_heads, int32_t d, float scale, hipStream_t stream);
+
+/*
+ * f3s_backward_typed for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid hipMalloc):
+ * the per-row (base-2 lse, delta) records that f3s_backward_typed keeps in
+ * the caller's row_stats buffer live instead in a fixed array of the
+ * library, 16 MiB per device, holding f3s_backward_noalloc_max_records()
+ * = 2^21 (row, head) records; the array is looked up on the first call on
+ * a device (make one call before capturing a graph) and held until the
+ * process ends.  The call allocates nothing and never frees.
+ *   N * n_heads above 2^21 gives F3S_ERR_TOO_LARGE (nothing launched).
+ *   Every other argument, and the result, as f3s_backward_typed.
+ * All calls on one device share that device's array: two calls that
+ * overlap in time on one device (two streams, two threads) race and give
+ * wrong gradients; calls on one stream are ordered and safe.  The array's
+ * contents are written by each call before they are read (nothing has to
+ * start at zero).
+ */
+f3s_status_t f3s_backward_noalloc(f3s_plan_t plan, f3s_plan_t plan_t, const void *Q,
+                                  const void *K, const void *V, f3s_dtype_t in_dtype,
+                                  const float *O, const void *dO, const float *lse,
+                                  float *dQ, float *dK, float *dV, int32_t n_heads,
+                                  int32_t d, float scale, hipStream_t stream);
+
+/* Capacity of f3s_backward_noalloc's array in (row, head) records.  Host-only. */
+int64_t f3s_backward_noalloc_max_records(void);
 
 /* Release a plan and all its device memory.  NULL is a no-op. */
 void f3s_destroy(f3s_plan_t plan);

@@ -15,7 +15,8 @@ from . import build as _build
 
 F3S_OK = 0
 _STATUS = {0: "F3S_OK", 1: "F3S_ERR_INVALID_VALUE", 2: "F3S_ERR_INVALID_CSR",
-           3: "F3S_ERR_UNSUPPORTED", 4: "F3S_ERR_OUT_OF_MEMORY", 5: "F3S_ERR_HIP"}
+           3: "F3S_ERR_UNSUPPORTED", 4: "F3S_ERR_OUT_OF_MEMORY", 5: "F3S_ERR_HIP",
+           6: "F3S_ERR_TOO_LARGE"}
 
 
 class F3SError(RuntimeError):
@@ -100,6 +101,11 @@ def load_library():
     L.f3s_backward_typed.argtypes = ([vp, vp, vp, vp, vp, i32] + [vp] * 7 +
                                      [i32, i32, ctypes.c_float, vp])
     L.f3s_backward_typed.restype = ctypes.c_int
+    L.f3s_backward_noalloc.argtypes = ([vp, vp, vp, vp, vp, i32] + [vp] * 6 +
+                                       [i32, i32, ctypes.c_float, vp])
+    L.f3s_backward_noalloc.restype = ctypes.c_int
+    L.f3s_backward_noalloc_max_records.argtypes = []
+    L.f3s_backward_noalloc_max_records.restype = ctypes.c_int64
     L.f3s_probe_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
     L.f3s_probe_read.restype = ctypes.c_int
     L.f3s_probe_copy.argtypes = [vp, vp, ctypes.c_size_t, vp]

@@ -547,6 +547,10 @@ f3s_plan_t make_transpose(f3s_plan_t src, void *workspace, size_t workspace_byte
 
 }  // namespace
 
+namespace f3s {
+f3s_status_t record_error(f3s_status_t s) { return fail(s); }
+}  // namespace f3s
+
 extern "C" {
 
 const char *f3s_status_string(f3s_status_t status)
@@ -558,6 +562,7 @@ const char *f3s_status_string(f3s_status_t status)
     case F3S_ERR_UNSUPPORTED: return "F3S_ERR_UNSUPPORTED";
     case F3S_ERR_OUT_OF_MEMORY: return "F3S_ERR_OUT_OF_MEMORY";
     case F3S_ERR_HIP: return "F3S_ERR_HIP";
+    case F3S_ERR_TOO_LARGE: return "F3S_ERR_TOO_LARGE";
     }
     return "F3S_ERR_UNKNOWN";
 }

@@ -242,6 +242,9 @@ hipError_t launch_fused_fp8(const f3s_plan_s &p, const void *Q, const void *K,
                             const void *V, void *O, bool out_f16, float *lse, int32_t H,
                             int32_t d, float scale_log2, hipStream_t s);
 
+// Records s as this thread's last error (f3s_last_error) and returns it.
+f3s_status_t record_error(f3s_status_t s);
+
 // Gradients (backward_kernel.h; fp16 inputs: backward.hip, bf16 inputs:
 // backward_bf16.hip).  pt is the plan of the transposed pattern; row_stats:
 // [N, H, 2] (base-2 lse, delta) written by the dQ pass.

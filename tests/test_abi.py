@@ -37,6 +37,7 @@ def test_header_declares_the_boundary():
               "f3s_run_mh", "f3s_forward", "f3s_plan_transpose",
               "f3s_backward", "f3s_backward_typed", "f3s_destroy", "f3s_plan_info",
               "f3s_plan_export", "f3s_last_error", "f3s_status_string",
+              "f3s_backward_noalloc", "f3s_backward_noalloc_max_records",
               "f3s_probe_read", "f3s_probe_copy", "f3s_probe_write", "f3s_probe_gather"):
         assert n in names
 
@@ -71,6 +72,7 @@ def test_status_strings_are_host_only(lib):
     lib.f3s_status_string.argtypes = [ctypes.c_int]
     assert lib.f3s_status_string(0) == b"F3S_OK"
     assert lib.f3s_status_string(2) == b"F3S_ERR_INVALID_CSR"
+    assert lib.f3s_status_string(6) == b"F3S_ERR_TOO_LARGE"
     assert lib.f3s_status_string(99) == b"F3S_ERR_UNKNOWN"
     lib.f3s_last_error.restype = ctypes.c_int
     assert lib.f3s_last_error() == 0
