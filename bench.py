@@ -189,6 +189,141 @@ def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, r
     return out
 
 
+def dram_check(args, stream, dev, reps=10):
+    """The operator on uniform_random_graph (8,388,608 nodes, 16 random
+    neighbours + self, d = 128: K and V 17x the Infinity Cache, so the gathers
+    are served by DRAM): ms per call and algorithmic GB/s, the bandwidth the
+    kernel sustains from HBM itself.  Features: seeded N(0,1) fp16 drawn on
+    the device."""
+    import numpy as np
+    import torch
+    import paper_2505_08098_amd as f3s
+    from paper_2505_08098_amd import workloads as W
+    d = 128
+    rp, ci = W.uniform_random_graph(args.seed)
+    N = len(rp) - 1
+    plan = f3s.Plan(torch.from_numpy(rp).to(dev), torch.from_numpy(ci).to(dev), N)
+    del rp, ci
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    Q, K, V = (torch.randn((N, d), generator=gen, device=dev).half() for _ in range(3))
+    O = torch.empty((N, d), dtype=torch.float32, device=dev)
+    scale = 1.0 / math.sqrt(d)
+    for _ in range(2):
+        f3s.run(plan, Q, K, V, scale=scale, out=O, stream=stream)
+    a = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    b = [torch.cuda.Event(enable_timing=True) for _ in range(reps)]
+    for k in range(reps):
+        a[k].record(stream)
+        f3s.run(plan, Q, K, V, scale=scale, out=O, stream=stream)
+        b[k].record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([x.elapsed_time(y) for x, y in zip(a, b)]))
+    info = plan.info
+    nbytes = algorithmic_bytes(info, d)
+    gbs = nbytes / ms / 1e6
+    out = {"workload": f"uniform random graph N={N}, 16 random neighbours + self, d={d}",
+           "nnz": info["nnz"], "n_unique": info["n_unique"], "ms": round(ms, 4),
+           "algorithmic_bytes": nbytes, "achieved_GBs": round(gbs, 1),
+           "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+           "gflops_eff": round(4.0 * info["nnz"] * d / ms / 1e6, 1)}
+    plan.close()
+    del Q, K, V, O
+    torch.cuda.empty_cache()
+    return out
+
+
+def cu_balance(rec, khz):
+    """Per compute unit busy time from f3s_run_trace records (one per
+    workgroup): busy = the union of its workgroups' [start, end] intervals,
+    end = its last workgroup's end, both in microseconds from the kernel's
+    first start."""
+    import numpy as np
+    rec = rec.astype(np.uint64)
+    t0 = rec[:, 0] | (rec[:, 1] << np.uint64(32))
+    t1 = rec[:, 2] | (rec[:, 3] << np.uint64(32))
+    hw, xcc = rec[:, 4], rec[:, 5]
+    key = ((xcc & np.uint64(15)) << np.uint64(16)) | \
+          (((hw >> np.uint64(13)) & np.uint64(7)) << np.uint64(8)) | \
+          (((hw >> np.uint64(12)) & np.uint64(1)) << np.uint64(4)) | \
+          ((hw >> np.uint64(8)) & np.uint64(15))
+    base = t0.min()
+    us = 1e3 / khz
+    s = (t0 - base).astype(np.float64) * us
+    e = (t1 - base).astype(np.float64) * us
+    busy, end = [], []
+    for k in np.unique(key):
+        sel = key == k
+        order = np.argsort(s[sel], kind="stable")
+        ss, ee = s[sel][order], e[sel][order]
+        tot, cur_s, cur_e = 0.0, ss[0], ee[0]
+        for a, b in zip(ss[1:], ee[1:]):
+            if a > cur_e:
+                tot += cur_e - cur_s
+                cur_s, cur_e = a, b
+            else:
+                cur_e = max(cur_e, b)
+        busy.append(tot + cur_e - cur_s)
+        end.append(ee.max())
+    busy, end = np.array(busy), np.array(end)
+    span = float(e.max())
+
+    def st(x):
+        return {"min": round(float(x.min()), 2), "mean": round(float(x.mean()), 2),
+                "max": round(float(x.max()), 2)}
+    dur = e - s
+    q = np.percentile(dur, [10, 50, 90])
+    return {"cus": int(busy.size), "workgroups": int(rec.shape[0]), "span_us": round(span, 2),
+            "busy_us": st(busy), "end_us": st(end),
+            "busy_frac_mean": round(float(busy.mean()) / span, 4),
+            "idle_tail_us_mean": round(span - float(end.mean()), 2),
+            "workgroup_us": {"mean": round(float(dur.mean()), 3), "p10": round(float(q[0]), 3),
+                             "p50": round(float(q[1]), 3), "p90": round(float(q[2]), 3)},
+            # workgroups resident on a CU at once, averaged over its busy time
+            "resident_per_cu_mean": round(float(dur.sum()) / float(busy.sum()), 2)}
+
+
+def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
+    """Per-CU busy time of one traced forward call with the heavy-first work
+    list and with the window-order work list (F3S_NO_REORDER), the
+    load-balance comparison of the paper's row-window reordering ablation."""
+    import numpy as np
+    import torch
+    import paper_2505_08098_amd as f3s
+    out = {"metric": "per-CU busy time of one fused 3S call (f3s_run_trace)",
+           "n_gpus": 1, "config": {"workload": c["name"], "N": c["N"], "d": c["d"]},
+           "wall_clock_khz": f3s.wall_clock_khz(0), "orders": {}}
+    prev = os.environ.get("F3S_NO_REORDER")
+    for order in ("heavy_first", "window_order"):
+        if order == "window_order":
+            os.environ["F3S_NO_REORDER"] = "1"
+        else:
+            os.environ.pop("F3S_NO_REORDER", None)
+        plan = f3s.Plan(rp, ci, c["N"])
+        for _ in range(args.warmup):
+            f3s.run(plan, Q, K, V, scale=c["scale"], stream=stream)
+        ms = []
+        for _ in range(max(1, args.steps)):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            O, rec = f3s.run_trace(plan, Q, K, V, scale=c["scale"], stream=stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        r = cu_balance(rec.cpu().numpy().view(np.uint32), out["wall_clock_khz"])
+        r["ms_mean"] = round(float(np.mean(ms)), 5)
+        r["n_items"] = plan.info["n_items"]
+        r["n_split"] = plan.info["n_split"]
+        out["orders"][order] = r
+        plan.close()
+    if prev is None:
+        os.environ.pop("F3S_NO_REORDER", None)
+    else:
+        os.environ["F3S_NO_REORDER"] = prev
+    print(json.dumps(out), flush=True)
+
+
 def backward_bytes(info, info_t, d, heads=1):
     """Algorithmic bytes of one f3s_backward.  dQ pass over windows of A:
     Q, G and O rows of the window (delta = G.O is formed there) and their
@@ -204,6 +339,36 @@ def backward_bytes(info, info_t, d, heads=1):
     plan_bytes = 96 * (info["n_blocks"] + info_t["n_blocks"]) + 16 * (
         info["n_items"] + info_t["n_items"])
     return heads * (dq + dkdv) + plan_bytes
+
+
+def graph_timed(call, steps, dev):
+    """`steps` calls captured in one HIP graph (the library launches onto
+    the capturing stream; nothing in a call allocates or synchronises), one
+    untimed replay, then one replay timed with events on its stream:
+    returns (stream, ms per call), free of the host's per-launch latency."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        call()                      # one eager call on the side stream first
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=side):
+        for _ in range(steps):
+            call()
+    g.replay()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    cur = torch.cuda.current_stream(dev)
+    a.record(cur)
+    g.replay()
+    b.record(cur)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    del g
+    return cur, ms
 
 
 def cold_mall_ms(args, call, stream, dev):
@@ -269,18 +434,23 @@ def bench_backward(args, c, plan, Q, K, V, stream, dev):
     else:
         G = torch.from_numpy(g32.astype(np.float16)).to(dev)
         O, lse = f3s.forward(plan, Q, K, V, scale=c["scale"], stream=stream)
+    grads = [None]
+
+    def call():
+        grads[0] = f3s.backward(plan, plan_t, Q, K, V, O, G, lse, scale=c["scale"])
     for _ in range(args.warmup):
-        f3s.backward(plan, plan_t, Q, K, V, O, G, lse, scale=c["scale"], stream=stream)
+        call()
     torch.cuda.synchronize()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     for k in range(args.steps):
         starts[k].record(stream)
-        f3s.backward(plan, plan_t, Q, K, V, O, G, lse, scale=c["scale"], stream=stream)
+        call()
         ends[k].record(stream)
     torch.cuda.synchronize()
     per = np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
-    ms = float(per.mean())
+    ms_eager = float(per.mean())
+    ms = ms_eager if args.no_graph else graph_timed(call, args.steps, dev)[1]
     info, info_t = plan.info, plan_t.info
     flops = 10.0 * info["nnz"] * d * H  # scores recomputed + 4 products
     nbytes = backward_bytes(info, info_t, d, H)
@@ -293,7 +463,10 @@ def bench_backward(args, c, plan, Q, K, V, stream, dev):
         "dtype": args.in_dtype, "data": "synthetic",
         "config": {"workload": c["name"], "N": c["N"], "nnz": info["nnz"], "d": d,
                    "heads": H, "in_dtype": args.in_dtype},
-        "ms_median": round(float(np.median(per)), 5),
+        "ms_eager_median": round(float(np.median(per)), 5),
+        "ms_eager_per_call": round(ms_eager, 5),
+        "timing": "eager calls, events around each" if args.no_graph else
+                  "one HIP graph of the timed calls, events around its replay",
         "transpose_plan_ms": round(transpose_ms, 3),
         "transpose_plan_ms_warm": round(transpose_ms_warm, 3),
         "roofline": {"bound": "hbm", "achieved": round(nbytes / (ms * 1e-3) / 1e9, 1),
@@ -335,6 +508,12 @@ def main():
                     help="after the timed region, calls timed one by one after a 1 GiB "
                          "scrub write each (L2 and the 256 MB Infinity Cache cold); "
                          "reported as ms_cold_mall, not in value")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager calls (events around each call, host latency "
+                         "included on small workloads) instead of one HIP graph replay")
+    ap.add_argument("--cu-trace", action="store_true",
+                    help="per-CU busy time of one traced call, heavy-first and window-order "
+                         "work lists (f3s_run_trace)")
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the probe kernels (streaming read/copy/write over 4 GiB "
                          "and the plan's access pattern without arithmetic)")
@@ -383,11 +562,12 @@ def main():
     typed = args.in_dtype != "f16" or args.out_dtype != "f32"
 
     def call():
+        # on torch's current stream: the default stream, or the capturing
+        # stream while a HIP graph is recorded
         if typed:
-            f3s.forward_typed(plan, Q, K, V, out_dtype=out_dt, scale=c["scale"], out=O,
-                              stream=stream)
+            f3s.forward_typed(plan, Q, K, V, out_dtype=out_dt, scale=c["scale"], out=O)
         else:
-            f3s.run(plan, Q, K, V, scale=c["scale"], out=O, stream=stream)
+            f3s.run(plan, Q, K, V, scale=c["scale"], out=O)
     torch.cuda.synchronize()
     plan = f3s.Plan(rp, ci, N)
     info = plan.info
@@ -403,10 +583,17 @@ def main():
 
     if args.backward:
         return bench_backward(args, c, plan, Q, K, V, stream, dev)
+    if args.cu_trace:
+        if typed or H != 1:
+            print(json.dumps({"error": "--cu-trace times the one-head fp16 -> fp32 call"}))
+            sys.exit(2)
+        plan.close()
+        return bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev)
     for _ in range(args.warmup):
         call()
     torch.cuda.synchronize()
-    # timed region: events on the launch stream around each call
+    # eager calls, events on the launch stream around each call (on the small
+    # workloads these include the host's per-call latency)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -418,7 +605,19 @@ def main():
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
     per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
-    ms = float(per.mean())
+    ms_eager = float(per.mean())
+    if args.no_graph:
+        ms = ms_eager
+    else:
+        stream, ms = graph_timed(call, args.steps, dev)
+        # the graph's calls write the same O as the eager ones
+        O_eager = O.clone()
+        O.fill_(float("nan"))
+        stream, _ = graph_timed(call, 1, dev)
+        torch.cuda.synchronize()
+        if not torch.equal(O, O_eager):
+            print(json.dumps({"error": "graph replay differs from the eager call"}))
+            sys.exit(1)
     cold = cold_mall_ms(args, call, stream, dev)
 
     flops_eff = 4.0 * info["nnz"] * d * H
@@ -429,6 +628,11 @@ def main():
     issued = 1024.0 * d * H * info["n_blocks"]  # MFMA flops incl. zero padding
     traffic = traffic_from_counters(d) if H == 1 and not typed else None
     ceilings = None
+    if not args.no_ceilings and args.workload == 3 and H == 1 and not typed:
+        # the HBM-target workload also runs on a graph 8x larger that no cache holds
+        dram = dram_check(args, stream, dev)
+    else:
+        dram = None
     if not args.no_ceilings:
         # the pattern probe reads what the fp16 -> fp32 single-head kernel reads
         plain = H == 1 and not typed and d in (32, 64, 128, 256)
@@ -463,9 +667,12 @@ def main():
             "seed": args.seed,
             "parallelism": "single GPU",
         },
-        "ms_p10": round(float(np.percentile(per, 10)), 5),
-        "ms_median": round(float(np.median(per)), 5),
-        "ms_p90": round(float(np.percentile(per, 90)), 5),
+        "ms_eager_per_call": round(ms_eager, 5),
+        "timing": "eager calls, events around each" if args.no_graph else
+                  "one HIP graph of the timed calls, events around its replay",
+        "ms_eager_p10": round(float(np.percentile(per, 10)), 5),
+        "ms_eager_median": round(float(np.median(per)), 5),
+        "ms_eager_p90": round(float(np.percentile(per, 90)), 5),
         "wall_ms_per_step": round(wall_ms, 5),
         "ms_cold_mall": cold,
         "plan_ms": round(info["build_ms"], 3),
@@ -486,6 +693,7 @@ def main():
                             "and writes plus Infinity-Cache hits",
             "algorithmic_bytes_per_launch": alg_bytes,
             "measured_ceilings": ceilings,
+            "dram_scale_check": dram,
             "kernel": "k_fused3s<%d>" % d + (" %s->%s" % (args.in_dtype, args.out_dtype)
                                               if typed else "")
                       + (" x %d heads" % H if H > 1 else ""),

@@ -39,7 +39,9 @@ typedef enum {
     F3S_ERR_INVALID_VALUE = 1, /* null/misaligned pointer, bad size, aliasing   */
     F3S_ERR_INVALID_CSR = 2,   /* row_ptr[0] != 0, decreasing, column not in [0,N) */
     F3S_ERR_UNSUPPORTED = 3,   /* d not a multiple of 32 in [32, 256]           */
-    F3S_ERR_OUT_OF_MEMORY = 4, /* a device allocation failed                    */
+    F3S_ERR_OUT_OF_MEMORY = 4, /* a device allocation failed (environment
+                                  F3S_ALLOC_LIMIT_BYTES=<n> makes every
+                                  allocation above n bytes fail this way)      */
     F3S_ERR_HIP = 5,           /* any other HIP runtime error                   */
     F3S_ERR_TOO_LARGE = 6      /* the call needs more than a fixed capacity of
                                   the library (f3s_backward_noalloc)            */

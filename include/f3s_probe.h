@@ -47,6 +47,30 @@ f3s_status_t f3s_probe_write(void *dst, size_t bytes, uint32_t value, hipStream_
 f3s_status_t f3s_probe_gather(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                               float *O, int32_t d, hipStream_t stream);
 
+/*
+ * f3s_run(plan, Q, K, V, O, d, scale, stream) with a record of where and when
+ * each workgroup ran: the load-balance view of the paper's per-SM active
+ * time (Section 4.3, row-window reordering), for one head, fp16 in, fp32 out.
+ * O receives exactly f3s_run's result.  trace: device memory of at least
+ * 32 * n_items bytes (f3s_plan_info), 16-byte aligned; record k (workgroup
+ * k = work item k of the launch order) holds eight uint32:
+ *   [0], [1]  start time, low and high word   (constant clock; see
+ *   [2], [3]  end time, low and high word      f3s_wall_clock_khz)
+ *   [4]       the HW_ID register: CU id bits 8-11, shader array bit 12,
+ *             shader engine bits 13-15
+ *   [5]       the XCC_ID register (bits 0-3: which accelerator die)
+ *   [6]       workgroup index, [7] 0
+ * Patterns whose Q, K, V exceed 4 GiB give F3S_ERR_UNSUPPORTED; a short or
+ * misaligned trace buffer F3S_ERR_INVALID_VALUE.  Otherwise as f3s_run.
+ */
+f3s_status_t f3s_run_trace(f3s_plan_t plan, const void *Q, const void *K, const void *V,
+                           float *O, int32_t d, float scale, uint32_t *trace,
+                           size_t trace_bytes, hipStream_t stream);
+
+/* Frequency of the constant clock of the trace records on `device`, in kHz
+ * (0 if the query fails). */
+int32_t f3s_wall_clock_khz(int32_t device);
+
 #ifdef __cplusplus
 }
 #endif

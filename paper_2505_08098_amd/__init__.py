@@ -9,4 +9,4 @@ holds the seeded synthetic inputs.
 """
 from .binding import (F3SError, Plan, PlanInfo, backward, forward,  # noqa: F401
                       forward_typed, load_library, probe_gather, probe_stream, run,
-                      run_raw, status_string)
+                      run_raw, run_trace, status_string, wall_clock_khz)

@@ -114,6 +114,11 @@ def load_library():
     L.f3s_probe_write.restype = ctypes.c_int
     L.f3s_probe_gather.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     L.f3s_probe_gather.restype = ctypes.c_int
+    L.f3s_run_trace.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp, ctypes.c_size_t,
+                                vp]
+    L.f3s_run_trace.restype = ctypes.c_int
+    L.f3s_wall_clock_khz.argtypes = [i32]
+    L.f3s_wall_clock_khz.restype = ctypes.c_int32
     L.f3s_destroy.argtypes = [vp]
     L.f3s_destroy.restype = None
     L.f3s_plan_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
@@ -449,3 +454,37 @@ def probe_gather(plan, Q, K, V, out, stream=None):
                                          ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
         raise F3SError(rc, "f3s_probe_gather")
+
+
+def run_trace(plan, Q, K, V, scale=None, out=None, stream=None):
+    """f3s_run_trace: one-head fp16 -> fp32 forward (O as f3s_run) plus one
+    record per workgroup (start, end, compute unit); returns (O, records)
+    with records a uint32 device tensor [n_items, 8]."""
+    shape = tuple(Q.shape)
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check_device_tensor(t, n, torch.float16, plan.device)
+        if t.dim() != 2 or tuple(t.shape) != shape or shape[0] != plan.N:
+            raise ValueError("Q, K, V must be [N, d]")
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=Q.device)
+    _check_device_tensor(out, "out", torch.float32, plan.device)
+    if tuple(out.shape) != shape:
+        raise ValueError("out must have the shape of Q")
+    n = max(1, plan.info["n_items"])
+    rec = torch.zeros((n, 8), dtype=torch.int32, device=Q.device)
+    d = shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if stream is None:
+        stream = torch.cuda.current_stream(Q.device)
+    rc = load_library().f3s_run_trace(plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(),
+                                      out.data_ptr(), int(d), float(scale), rec.data_ptr(),
+                                      rec.numel() * 4, ctypes.c_void_p(stream.cuda_stream))
+    if rc != F3S_OK:
+        raise F3SError(rc, "f3s_run_trace")
+    return out, rec
+
+
+def wall_clock_khz(device=0):
+    """Frequency of the trace records' clock (kHz)."""
+    return int(load_library().f3s_wall_clock_khz(int(device)))

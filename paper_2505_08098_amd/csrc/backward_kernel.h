@@ -571,9 +571,11 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     const bool head_major = H > 1 && 2ull * p.N * ld * 2 > head_major_threshold();
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
-        const int nw = waves_per_item(p.n_blocks, p.n_items, H);
-        auto kern = nw == 4 ? (wide ? k_bwd_dq<D, true, kBF16, 4> : k_bwd_dq<D, false, kBF16, 4>)
-                            : (wide ? k_bwd_dq<D, true, kBF16> : k_bwd_dq<D, false, kBF16>);
+        const int nw = waves_per_item(p.n_blocks, p.n_items, H,
+                                      (int64_t)BwdWaves<D>::value * 1024);
+        auto kern = nw == 4   ? (wide ? k_bwd_dq<D, true, kBF16, 4> : k_bwd_dq<D, false, kBF16, 4>)
+                    : nw == 2 ? (wide ? k_bwd_dq<D, true, kBF16, 2> : k_bwd_dq<D, false, kBF16, 2>)
+                              : (wide ? k_bwd_dq<D, true, kBF16> : k_bwd_dq<D, false, kBF16>);
         const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
         for (int32_t h0 = 0; h0 < H; h0 += group) {
             const int32_t nh = H - h0 < group ? H - h0 : group;
@@ -593,9 +595,12 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     }
     // dK, dV: windows of A^T; partials need 2*16*D floats per (piece, head)
     {
-        const int nw = waves_per_item(pt.n_blocks, pt.n_items, H);
+        const int nw = waves_per_item(pt.n_blocks, pt.n_items, H,
+                                      (int64_t)BwdWaves<D>::value * 1024);
         auto kern = nw == 4
                         ? (wide ? k_bwd_dkdv<D, true, kBF16, 4> : k_bwd_dkdv<D, false, kBF16, 4>)
+                    : nw == 2
+                        ? (wide ? k_bwd_dkdv<D, true, kBF16, 2> : k_bwd_dkdv<D, false, kBF16, 2>)
                         : (wide ? k_bwd_dkdv<D, true, kBF16> : k_bwd_dkdv<D, false, kBF16>);
         // the transposed plan's partial rows hold part_row floats
         const int32_t cap = pt.part_row / (2 * D);

@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "f3s_internal.h"
+#include "f3s_probe.h"
 
 namespace {
 
@@ -27,6 +28,16 @@ f3s_status_t from_hip(hipError_t e)
     return e == hipErrorOutOfMemory ? F3S_ERR_OUT_OF_MEMORY : F3S_ERR_HIP;
 }
 
+// Largest single device allocation the library makes: F3S_ALLOC_LIMIT_BYTES
+// when set (a larger request then fails as if the device were out of
+// memory, so tests can drive every out-of-memory path from the host),
+// otherwise unlimited.
+size_t alloc_limit()
+{
+    const char *e = getenv("F3S_ALLOC_LIMIT_BYTES");
+    return e && *e ? (size_t)strtoull(e, nullptr, 10) : ~(size_t)0;
+}
+
 // One device allocation carved into 256-byte aligned pieces (the scratch of
 // one f3s_plan call, or a plan's arrays); sizing pass first (add), then one
 // hipMalloc (alloc), then the pieces in the same order (take).
@@ -39,7 +50,12 @@ struct Arena {
     {
         cap += round((size_t)(count > 0 ? count : 1) * sizeof(T));
     }
-    hipError_t alloc() { return hipMalloc((void **)&base, cap ? cap : 256); }
+    hipError_t alloc()
+    {
+        const size_t n = cap ? cap : 256;
+        if (n > alloc_limit()) return hipErrorOutOfMemory;
+        return hipMalloc((void **)&base, n);
+    }
     template <typename T>
     T *take(int64_t count)
     {
@@ -780,6 +796,43 @@ f3s_status_t f3s_run(f3s_plan_t p, const void *Q, const void *K, const void *V,
                      void *O, int32_t d, float scale, hipStream_t stream)
 {
     return f3s_run_mh(p, Q, K, V, O, 1, d, scale, stream);
+}
+
+f3s_status_t f3s_run_trace(f3s_plan_t p, const void *Q, const void *K, const void *V,
+                           float *O, int32_t d, float scale, uint32_t *trace,
+                           size_t trace_bytes, hipStream_t stream)
+{
+    if (!p) return fail(F3S_ERR_INVALID_VALUE);
+    if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
+    if (p->flags & 2) return fail(F3S_ERR_UNSUPPORTED);
+    if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
+    if (p->N == 0) return F3S_OK;
+    if (!on_plan_device(p, stream)) return fail(F3S_ERR_INVALID_VALUE);
+    if (!Q || !K || !V || !O || !trace) return fail(F3S_ERR_INVALID_VALUE);
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O) || !aligned16(trace))
+        return fail(F3S_ERR_INVALID_VALUE);
+    const size_t elems = (size_t)p->N * (size_t)d;
+    // 32-bit gather offsets only (the traced instance has no 64-bit variant)
+    if (elems * 2 > 0xFFFFFFF0ull) return fail(F3S_ERR_UNSUPPORTED);
+    const size_t need = 32ull * (size_t)p->n_items;
+    if (trace_bytes < need) return fail(F3S_ERR_INVALID_VALUE);
+    if (overlaps(O, elems * 4, Q, elems * 2) || overlaps(O, elems * 4, K, elems * 2) ||
+        overlaps(O, elems * 4, V, elems * 2) || overlaps(trace, need, O, elems * 4) ||
+        overlaps(trace, need, Q, elems * 2) || overlaps(trace, need, K, elems * 2) ||
+        overlaps(trace, need, V, elems * 2))
+        return fail(F3S_ERR_INVALID_VALUE);
+    const float sl2 = (float)((double)scale * 1.4426950408889634);
+    f3s_status_t st =
+        from_hip(f3s::launch_fused_trace(*p, Q, K, V, O, d, sl2, trace, stream));
+    return st == F3S_OK ? F3S_OK : fail(st);
+}
+
+int32_t f3s_wall_clock_khz(int32_t device)
+{
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeWallClockRate, device) != hipSuccess)
+        return 0;
+    return v;
 }
 
 }  // extern "C"

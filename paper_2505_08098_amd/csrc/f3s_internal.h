@@ -77,17 +77,27 @@ inline uint64_t head_major_threshold()
     const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
     return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
 }
-// Waves sharing one work item (forward and backward): 4 when a launch would have
-// fewer waves than the GPU has SIMDs (items x heads < 1024) and the items
-// average at least 4 blocks, else 1 (with more waves the merge and the
-// per-wave Q loads cost more than the parallelism gains: measured 18%
-// slower on the 2048-window sequence workload); F3S_WAVES_PER_ITEM=1 or 4
-// forces it (read at launch).
-inline int waves_per_item(int64_t n_blocks, int64_t n_items, int32_t heads)
+// Waves sharing one work item (forward and backward): 4 when a launch would
+// have fewer waves than the GPU has SIMDs (items x heads < 1024) and the
+// items average at least 4 blocks; else 2 when twice the waves still fit
+// the GPU at once (`resident`: the kernel's waves per SIMD x 1024 SIMDs) and
+// the items average at least 8 blocks (two pairs per wave); else 1.  More
+// waves than fit at once would run as a second round, whose tail and the
+// extra per-wave Q loads and combination cost more than the parallelism
+// gains (4 waves measured 18% slower on the 2048-window sequence workload).
+// F3S_WAVES_PER_ITEM=1, 2 or 4 forces it (read at launch).
+inline int waves_per_item(int64_t n_blocks, int64_t n_items, int32_t heads, int64_t resident)
 {
     const char *e = getenv("F3S_WAVES_PER_ITEM");
-    if (e && *e) return atoi(e) == 4 ? 4 : 1;
-    return n_items > 0 && n_items * heads < 1024 && n_blocks >= 4 * n_items ? 4 : 1;
+    if (e && *e) {
+        const int v = atoi(e);
+        return v == 4 ? 4 : v == 2 ? 2 : 1;
+    }
+    if (n_items <= 0) return 1;
+    const int64_t waves = n_items * heads;
+    if (waves < 1024 && n_blocks >= 4 * n_items) return 4;
+    if (2 * waves <= resident && n_blocks >= 8 * n_items) return 2;
+    return 1;
 }
 // Inclusive sum over the lanes of a wavefront (device code).
 __device__ __forceinline__ int wave_inclusive_sum(int x, int lane)
@@ -234,6 +244,12 @@ hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
 hipError_t launch_fused_bf16(const f3s_plan_s &p, const void *Q, const void *K,
                              const void *V, void *O, bool out_f16, float *lse, int32_t H,
                              int32_t d, float scale_log2, hipStream_t s);
+// Measurement instance of the one-head fp16 -> fp32 forward: the same result
+// in O, plus a 32-byte record per workgroup in trace (start and end times on
+// the constant clock, hardware ids of the compute unit, workgroup index).
+hipError_t launch_fused_trace(const f3s_plan_s &p, const void *Q, const void *K,
+                              const void *V, void *O, int32_t d, float sl2, uint32_t *trace,
+                              hipStream_t s);
 // Ablation: fp16 -> fp32 forward with 4-byte K/V gathers (plan flag bit 1).
 hipError_t launch_fused_narrow(const f3s_plan_s &p, const void *Q, const void *K,
                                const void *V, void *O, float *lse, int32_t H, int32_t d,

@@ -19,4 +19,12 @@ hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
                    : launch_in<kInF16, false>(p, Q, K, V, O, lse, H, d, sl2, s);
 }
 
+hipError_t launch_fused_trace(const f3s_plan_s &p, const void *Q, const void *K,
+                              const void *V, void *O, int32_t d, float sl2, uint32_t *trace,
+                              hipStream_t s)
+{
+    if (p.flags & 2) return hipErrorInvalidValue;
+    return launch_in<kInF16, false>(p, Q, K, V, O, nullptr, 1, d, sl2, s, trace);
+}
+
 }  // namespace f3s

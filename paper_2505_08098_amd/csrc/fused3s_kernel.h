@@ -72,7 +72,6 @@ constexpr int waves_per_simd()
     return WavesPerSimd<D>::value - (kIn == kInBF16 && D == 32 ? 1 : 0) -
            (kNarrow && (D == 64 || D == 96 || D == 160) ? 1 : 0);
 }
-
 // Score product for the input storage type (16-bit operands as raw bits).
 template <int kIn>
 __device__ __forceinline__ f4 mma_in(h8 a, h8 b, f4 c)
@@ -171,8 +170,12 @@ __device__ __forceinline__ void store4(void *base, int64_t idx, f4 v)
 // its block pairs, and the (m, l, O) partials are combined through LDS at
 // the end (the paper's split-column partition of a window among warps; used
 // for long windows, where one wave per window leaves the GPU with too few
-// waves).
-template <int D, bool kWide, int kIn, bool kOutH, bool kNarrow = false, int NW = 1>
+// waves).  kTrace (a measurement instance): the first thread of each
+// workgroup also records, after its outputs, when the workgroup started and
+// ended (the 100 MHz constant clock) and on which compute unit it ran, as
+// one 32-byte record per workgroup in `trace` (ordinary vector stores).
+template <int D, bool kWide, int kIn, bool kOutH, bool kNarrow = false, int NW = 1,
+          bool kTrace = false>
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
@@ -180,8 +183,10 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const void *__restrict__ Kv, const void *__restrict__ Vv,
     void *__restrict__ O, float *__restrict__ part_o,
     float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
-    int32_t h0, int32_t nh, float sl2, bool head_major)
+    int32_t h0, int32_t nh, float sl2, bool head_major, uint32_t *__restrict__ trace)
 {
+    uint64_t t_start = 0;
+    if constexpr (kTrace) t_start = wall_clock64();
     constexpr int NC = D / 32;  // 32-deep chunks of the score reduction
     constexpr int NT = D / 16;  // 16-wide output tiles of the value product
     // One LDS tile per wave, used twice per block pair with two row strides
@@ -522,6 +527,21 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
             part_ml[ps * 32 + 16 + i] = l_tot;
         }
     }
+    if constexpr (kTrace) {
+        if (threadIdx.x == 0) {
+            const uint64_t t_end = wall_clock64();
+            // HW_ID (compute unit, shader array and engine of this wave) and
+            // XCC_ID (which of the accelerator complex dies): s_getreg of
+            // hardware registers 4 and 20, all 32 / the low 16 bits
+            const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);
+            const uint32_t xcc = __builtin_amdgcn_s_getreg((15 << 11) | 20);
+            typedef uint32_t u4t __attribute__((ext_vector_type(4)));
+            u4t *rec = reinterpret_cast<u4t *>(trace + 8 * (int64_t)blockIdx.x);
+            rec[0] = u4t{(uint32_t)t_start, (uint32_t)(t_start >> 32), (uint32_t)t_end,
+                         (uint32_t)(t_end >> 32)};
+            rec[1] = u4t{hw, xcc, (uint32_t)blockIdx.x, 0u};
+        }
+    }
 }
 
 // Combines the pieces of one split window in their fixed order (so the
@@ -598,19 +618,37 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
 // Heads are launched in groups whose partial results fit the plan's scratch
 // (nh * D <= 256 floats per piece row); without split windows all heads go
 // in one launch.
+// trace (the measurement instance, fp16 -> fp32 with 32-bit addressing and
+// one head only): one 32-byte record per workgroup.
 template <int D, int kIn, bool kOutH, bool kNarrow = false>
 hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                     const void *V, void *O, float *lse, int32_t H, float sl2,
-                    hipStream_t s)
+                    hipStream_t s, uint32_t *trace = nullptr)
 {
     const int32_t ld = H * D;
     const bool wide = (uint64_t)p.N * ld * elem_bytes<kIn>() > 0xFFFFFFF0ull;
     // the narrow-gather ablation keeps one wave per item
-    const int nw = kNarrow ? 1 : waves_per_item(p.n_blocks, p.n_items, H);
-    auto kern = nw == 4 ? (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow, kNarrow ? 1 : 4>
-                                : k_fused3s<D, false, kIn, kOutH, kNarrow, kNarrow ? 1 : 4>)
-                        : (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow>
-                                : k_fused3s<D, false, kIn, kOutH, kNarrow>);
+    const int nw =
+        kNarrow ? 1
+                : waves_per_item(p.n_blocks, p.n_items, H,
+                                 (int64_t)waves_per_simd<D, kIn, kNarrow>() * 1024);
+    constexpr int W2 = kNarrow ? 1 : 2, W4 = kNarrow ? 1 : 4;
+    auto kern = nw == 4   ? (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow, W4>
+                                  : k_fused3s<D, false, kIn, kOutH, kNarrow, W4>)
+                : nw == 2 ? (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow, W2>
+                                  : k_fused3s<D, false, kIn, kOutH, kNarrow, W2>)
+                          : (wide ? k_fused3s<D, true, kIn, kOutH, kNarrow>
+                                  : k_fused3s<D, false, kIn, kOutH, kNarrow>);
+    if (trace) {
+        if constexpr (kIn == kInF16 && !kOutH && !kNarrow) {
+            if (wide || H != 1) return hipErrorInvalidValue;
+            kern = nw == 4   ? k_fused3s<D, false, kIn, kOutH, false, 4, true>
+                   : nw == 2 ? k_fused3s<D, false, kIn, kOutH, false, 2, true>
+                             : k_fused3s<D, false, kIn, kOutH, false, 1, true>;
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     const int32_t group = p.n_split > 0 ? (kMaxD / D < H ? kMaxD / D : H) : H;
     for (int32_t h0 = 0; h0 < H; h0 += group) {
         const int32_t nh = H - h0 < group ? H - h0 : group;
@@ -623,7 +661,7 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                 nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
             kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
-                                               sl2, head_major);
+                                               sl2, head_major, trace);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
@@ -640,17 +678,18 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
 // Dispatch over the feature size for one input storage type.
 template <int kIn, bool kOutH, bool kNarrow = false>
 hipError_t launch_in(const f3s_plan_s &p, const void *Q, const void *K, const void *V,
-                     void *O, float *lse, int32_t H, int32_t d, float sl2, hipStream_t s)
+                     void *O, float *lse, int32_t H, int32_t d, float sl2, hipStream_t s,
+                     uint32_t *trace = nullptr)
 {
     switch (d) {
-    case 32: return launch_d<32, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 64: return launch_d<64, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 96: return launch_d<96, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 128: return launch_d<128, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 160: return launch_d<160, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 192: return launch_d<192, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 224: return launch_d<224, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
-    case 256: return launch_d<256, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s);
+    case 32: return launch_d<32, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 64: return launch_d<64, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 96: return launch_d<96, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 128: return launch_d<128, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 160: return launch_d<160, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 192: return launch_d<192, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 224: return launch_d<224, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
+    case 256: return launch_d<256, kIn, kOutH, kNarrow>(p, Q, K, V, O, lse, H, sl2, s, trace);
     default: return hipErrorInvalidValue;
     }
 }

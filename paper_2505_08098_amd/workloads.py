@@ -241,6 +241,21 @@ def make_config(k, seed=0, with_features=True, dtype="f16"):
     return out
 
 
+def uniform_random_graph(seed=0, N=8_388_608, k=16):
+    """A graph whose gathers find no reuse in any cache: every row attends
+    to itself and k node ids drawn uniformly from [0, N) (repeats count
+    once), from the graph stream of ``seed``.  At the default size (8x the
+    million-node workload, d = 128) K and V hold 4.3 GB, 17x the 256 MB
+    Infinity Cache, so nearly every gathered row comes from DRAM: the check
+    that the operator sustains its bandwidth from HBM itself."""
+    g, _ = _streams(seed)
+    ci = np.empty((N, k + 1), dtype=np.int32)
+    ci[:, 0] = np.arange(N, dtype=np.int32)
+    ci[:, 1:] = g.integers(0, N, size=(N, k), dtype=np.int32)
+    row_ptr = (np.arange(N + 1, dtype=np.int64) * (k + 1)).astype(np.int32)
+    return row_ptr, ci.reshape(-1)
+
+
 def random_csr(rng, N, max_deg, empty_frac=0.0, dup_frac=0.0, shuffle=True):
     """Small adversarial CSR: random degrees in [0, max_deg], optional empty
     rows, optional repeated entries, columns in random order."""

@@ -92,3 +92,23 @@ def test_counters_are_used_only_for_their_feature_size():
         assert got == rec.get("hbm_bytes_per_launch")
     else:
         assert got is None
+
+
+def test_cu_balance_unions_intervals_per_cu():
+    """bench.cu_balance: busy = union of each CU's workgroup intervals, end =
+    its last end, from the first start (hand-worked records, 100 MHz)."""
+    import numpy as np
+    import bench
+    rec = np.zeros((5, 8), dtype=np.uint32)
+    rec[:, 0] = [100, 150, 100, 400, 450]          # starts (ticks)
+    rec[:, 2] = [200, 300, 300, 500, 480]          # ends
+    rec[:, 4] = [1 << 8, 1 << 8, 2 << 8, 2 << 8, 2 << 8]   # CU ids 1 and 2
+    rec[:, 5] = [0, 0, 0, 0, 0]
+    r = bench.cu_balance(rec, 100_000)             # 1 tick = 0.01 us
+    assert r["cus"] == 2 and r["workgroups"] == 5
+    assert r["span_us"] == 4.0
+    assert r["busy_us"] == {"min": 2.0, "mean": 2.5, "max": 3.0}
+    assert r["end_us"] == {"min": 2.0, "mean": 3.0, "max": 4.0}
+    # the same CU id on another die is another CU
+    rec[4, 5] = 3
+    assert bench.cu_balance(rec, 100_000)["cus"] == 3

@@ -69,12 +69,12 @@ def test_workload_parity(gpu, oracle, k):
     _assert_parity(O, ref)
 
 
-@pytest.mark.parametrize("waves", ["1", "4"])
+@pytest.mark.parametrize("waves", ["1", "2", "4"])
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
 @pytest.mark.parametrize("N", [1, 17, 200])
 def test_feature_sizes_and_ragged_windows(gpu, oracle, d, N, waves, monkeypatch):
-    """Every feature size, ragged last windows, with one wave per work item
-    or four sharing it (their partials combined in LDS)."""
+    """Every feature size, ragged last windows, with one, two or four waves per work item
+    sharing it (their partials combined in LDS)."""
     monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     rng = np.random.default_rng(d * 1000 + N)
     rp, ci = W.random_csr(rng, N, max_deg=min(N, 70), empty_frac=0.1, dup_frac=0.2)
@@ -371,14 +371,43 @@ def test_multi_head_workloads(gpu, oracle, k, H):
             _assert_parity(O[:, h], ref)
 
 
-@pytest.mark.parametrize("waves", ["1", "4"])
+def test_dram_scale_graph_sampled(gpu, oracle):
+    """The graph bench.py runs to measure the bandwidth the kernel sustains
+    from DRAM (8,388,608 nodes, self + 16 uniform random neighbours, d = 128,
+    N(0,1) fp16 features drawn on the device): the whole call on the GPU,
+    4,000 random rows and the last window against the oracle on their
+    sub-problem."""
+    rp, ci = W.uniform_random_graph(0)
+    N, d = len(rp) - 1, 128
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(0)
+    Q, K, V = (torch.randn((N, d), generator=gen, device=DEV).half() for _ in range(3))
+    O = gpu.run(plan, Q, K, V, scale=1 / math.sqrt(d))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(8)
+    rows = np.unique(np.concatenate([rng.integers(0, N, size=4000),
+                                     np.arange(N - 16, N)]))
+    mrp, mci, U = rows_subproblem(rp, ci, rows)
+    idx = torch.from_numpy(U).to(DEV)
+    q, k, v = (x.index_select(0, idx).cpu().numpy() for x in (Q, K, V))
+    ref = oracle.attention_f64(mrp, mci, q, k, v, 1 / math.sqrt(d))
+    got = O.index_select(0, torch.from_numpy(rows).to(DEV)).cpu().numpy()
+    print(f"  {rows.size} rows, sub-problem of {U.size} nodes", flush=True)
+    _assert_parity(got, ref[np.searchsorted(U, rows)])
+    plan.close()
+    del Q, K, V, O
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("waves", ["1", "2", "4"])
 @pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("piece", [4, 1000000])
 def test_multi_head_equals_single_head_runs(gpu, monkeypatch, piece, order, waves):
     """Head h of the multi-head call is bit-identical to a single-head call on
     the head's slice, with and without split windows (H * d > 256 also
     exercises the head groups that bound the partial-result scratch), in
-    either workgroup order, with one or four waves per work item (fixed for
+    either workgroup order, with one, two or four waves per work item (fixed for
     both calls: the combination of the waves' partials rounds differently)."""
     _head_order(monkeypatch, order)
     monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)

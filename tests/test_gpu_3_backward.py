@@ -277,11 +277,11 @@ def test_transpose_workspace_errors(gpu):
         assert L.f3s_last_error() == 1  # F3S_ERR_INVALID_VALUE
 
 
-@pytest.mark.parametrize("waves", ["1", "4"])
+@pytest.mark.parametrize("waves", ["1", "2", "4"])
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
 @pytest.mark.parametrize("N", [1, 17, 300])
 def test_gradients_random_patterns(gpu, oracle, d, N, waves, monkeypatch):
-    """Every feature size, with one wave per work item or four sharing it
+    """Every feature size, with one wave per work item or two or four sharing it
     (forward and both backward passes; their partial sums combined in LDS)."""
     monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     rng = np.random.default_rng(d + 7 * N)
@@ -301,7 +301,7 @@ def test_gradients_workloads(gpu, oracle, k):
                c["scale"])
 
 
-@pytest.mark.parametrize("waves", ["1", "4"])
+@pytest.mark.parametrize("waves", ["1", "2", "4"])
 @pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("H,d", [(3, 64), (2, 160), (2, 256)])
 def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order, waves):

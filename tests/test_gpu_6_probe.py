@@ -57,3 +57,30 @@ def test_pattern_probe_runs_on_the_workload_plans(gpu, k, monkeypatch):
     O2 = gpu.run(plan, q, kk, v, scale=c["scale"])
     torch.cuda.synchronize()
     assert bool(torch.isfinite(O2).all())
+
+
+@pytest.mark.parametrize("k,waves", [(1, "4"), (1, "1"), (2, "1"), (4, "1"), (5, "1")])
+def test_traced_run_equals_run_and_records_every_workgroup(gpu, k, waves, monkeypatch):
+    """f3s_run_trace writes exactly f3s_run's O (split windows and their
+    merge included) and one record per workgroup: end after start, the
+    workgroup's index, and compute-unit ids that name at most 256 CUs."""
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
+    c = W.make_config(k)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
+    ref = gpu.run(plan, q, kk, v, scale=c["scale"])
+    O, rec = gpu.run_trace(plan, q, kk, v, scale=c["scale"])
+    torch.cuda.synchronize()
+    assert torch.equal(O, ref)
+    r = rec.cpu().numpy().view(np.uint32).astype(np.uint64)
+    n = plan.info["n_items"]
+    assert r.shape == (n, 8)
+    t0 = r[:, 0] | (r[:, 1] << np.uint64(32))
+    t1 = r[:, 2] | (r[:, 3] << np.uint64(32))
+    assert np.all(t1 >= t0) and np.all(t0 > 0)
+    assert np.array_equal(r[:, 6], np.arange(n))
+    import bench
+    stats = bench.cu_balance(r.astype(np.uint32), gpu.wall_clock_khz(0))
+    print(f"  {stats}", flush=True)
+    assert 1 <= stats["cus"] <= 256
+    assert gpu.wall_clock_khz(0) > 0
