@@ -143,13 +143,14 @@ def plan_stats(plan):
     }
 
 
-def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, reps=5):
+def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, reps=20):
     """Bandwidth ceilings measured in this process with the library's probe
     kernels: a streaming read, copy and write over 4 GiB (16x the 256 MB
     Infinity Cache, so DRAM serves them), and the fused kernel's own access
     pattern on this plan without its arithmetic (f3s_probe_gather; its
-    rate counts the same algorithmic bytes).  Mean of `reps` timed calls
-    after one untimed call each."""
+    rate counts the same algorithmic bytes).  Streams: mean of `reps` timed
+    calls after one untimed call; the pattern probe: one HIP graph of `reps`
+    calls (as the operator's steps are timed)."""
     import numpy as np
     import torch
     import paper_2505_08098_amd as f3s
@@ -181,7 +182,8 @@ def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, r
     torch.cuda.empty_cache()
     out["stream_bytes"] = nbytes
     if Q is not None:
-        ms = timed(lambda: f3s.probe_gather(plan, Q, K, V, O, stream=stream))
+        # one HIP graph of `reps` probe calls, timed like the operator's steps
+        ms = graph_timed(lambda: f3s.probe_gather(plan, Q, K, V, O), reps, dev)[1]
         out["pattern_gather_ms"] = round(ms, 5)
         out["pattern_gather_GBs"] = round(alg_bytes / ms / 1e6, 1)
         out["frac_of_pattern_gather"] = round(achieved_gbs / out["pattern_gather_GBs"], 4)

@@ -43,8 +43,12 @@ typedef enum {
                                   F3S_ALLOC_LIMIT_BYTES=<n> makes every
                                   allocation above n bytes fail this way)      */
     F3S_ERR_HIP = 5,           /* any other HIP runtime error                   */
-    F3S_ERR_TOO_LARGE = 6      /* the call needs more than a fixed capacity of
+    F3S_ERR_TOO_LARGE = 6,     /* the call needs more than a fixed capacity of
                                   the library (f3s_backward_noalloc)            */
+    /* not statuses: they give the type the whole int32 range, so any int a
+       caller passes (f3s_status_string) is a valid value of the type */
+    F3S_STATUS_MIN_ = -2147483647 - 1,
+    F3S_STATUS_MAX_ = 2147483647
 } f3s_status_t;
 
 typedef struct f3s_plan_s *f3s_plan_t;
@@ -164,7 +168,11 @@ typedef enum {
     F3S_DTYPE_F16 = 0,   /* IEEE 754 binary16 */
     F3S_DTYPE_BF16 = 1,  /* bfloat16: the upper 16 bits of an IEEE binary32 */
     F3S_DTYPE_F32 = 2,   /* IEEE 754 binary32 */
-    F3S_DTYPE_FP8_E4M3 = 3  /* OCP 8-bit float e4m3 (bias 7, finite to 448, no inf) */
+    F3S_DTYPE_FP8_E4M3 = 3,  /* OCP 8-bit float e4m3 (bias 7, finite to 448, no inf) */
+    /* not types: the whole int32 range is a valid value (others are rejected
+       with F3S_ERR_UNSUPPORTED) */
+    F3S_DTYPE_MIN_ = -2147483647 - 1,
+    F3S_DTYPE_MAX_ = 2147483647
 } f3s_dtype_t;
 
 /*

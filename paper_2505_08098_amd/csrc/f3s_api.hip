@@ -214,6 +214,12 @@ U *carve(Arena &a, bool take, int64_t n)
 // Lays out the build's scratch for T windows and nnz CSR entries: sizes into
 // a (take == false) or pointers out of it (take == true), in one order.
 // O(nnz + T) bytes.
+// Row windows of an N-row pattern (64-bit sum: N may be up to 2^31 - 1).
+int32_t num_windows(int32_t N)
+{
+    return (int32_t)(((int64_t)N + f3s::kWindowRows - 1) / f3s::kWindowRows);
+}
+
 void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz)
 {
     using namespace f3s;
@@ -239,7 +245,7 @@ size_t plan_workspace_bytes(int32_t N, int64_t nnz)
 {
     Arena a;
     BuildScratch b;
-    const int32_t T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
+    const int32_t T = num_windows(N);
     carve_scratch(a, false, b, T, nnz);
     return a.cap;
 }
@@ -423,7 +429,7 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
         return nullptr;
     }
     p->N = N;
-    p->T = (N + f3s::kWindowRows - 1) / f3s::kWindowRows;
+    p->T = num_windows(N);
     p->id = g_next_plan_id.fetch_add(1);
     f3s_status_t st = from_hip(hipGetDevice(&p->device));
     if (st == F3S_OK) {
@@ -579,6 +585,7 @@ const char *f3s_status_string(f3s_status_t status)
     case F3S_ERR_OUT_OF_MEMORY: return "F3S_ERR_OUT_OF_MEMORY";
     case F3S_ERR_HIP: return "F3S_ERR_HIP";
     case F3S_ERR_TOO_LARGE: return "F3S_ERR_TOO_LARGE";
+    default: break;
     }
     return "F3S_ERR_UNKNOWN";
 }
