@@ -128,7 +128,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     const _Float16 *__restrict__ G, const float *__restrict__ O,
     const float *__restrict__ lse, float2 *__restrict__ stats, float *__restrict__ dQ,
     float *__restrict__ part, int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2,
-    float scale, bool head_major)
+    float scale, uint32_t order)
 {
     constexpr int NC = D / 32, NT = D / 16, NI = D / 16;
     constexpr int LSK = D + 16;  // K tile: operand reads and transposed reads
@@ -146,8 +146,9 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     // window-major, or head by head when K and V exceed the caches (as in
     // the forward)
     const int n_it = gridDim.x / nh;
-    const int hl = head_major ? blockIdx.x / n_it : blockIdx.x % nh;
-    const int item = head_major ? blockIdx.x - hl * n_it : blockIdx.x / nh;
+    const int wg = workgroup_position(order);
+    const int hl = (order & kOrderHead) ? wg / n_it : wg % nh;
+    const int item = (order & kOrderHead) ? wg - hl * n_it : wg / nh;
     const int head = h0 + hl, H = ld / D;
     const WorkItem it = items[item];
     Q += (int64_t)head * D;
@@ -315,7 +316,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     const _Float16 *__restrict__ G, const float2 *__restrict__ stats,
     float *__restrict__ dK, float *__restrict__ dV,
     float *__restrict__ part, int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2,
-    float scale, bool head_major)
+    float scale, uint32_t order)
 {
     constexpr int NC = D / 32, NT = D / 16, NI = D / 16;
     constexpr int LS = D + 16;  // operand reads and transposed reads
@@ -335,8 +336,9 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     // window-major, or head by head when K and V exceed the caches (as in
     // the forward)
     const int n_it = gridDim.x / nh;
-    const int hl = head_major ? blockIdx.x / n_it : blockIdx.x % nh;
-    const int item = head_major ? blockIdx.x - hl * n_it : blockIdx.x / nh;
+    const int wg = workgroup_position(order);
+    const int hl = (order & kOrderHead) ? wg / n_it : wg % nh;
+    const int item = (order & kOrderHead) ? wg - hl * n_it : wg / nh;
     const int head = h0 + hl, H = ld / D;
     const WorkItem it = items[item];
     Q += (int64_t)head * D;
@@ -569,6 +571,10 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     const auto *gr = static_cast<const _Float16 *>(G);
     hipError_t e = hipSuccess;
     const bool head_major = H > 1 && 2ull * p.N * ld * 2 > head_major_threshold();
+    const uint32_t order_a =
+        (head_major ? kOrderHead : 0u) | (xcd_chunks(p, false) ? kOrderXcd : 0u);
+    const uint32_t order_t =
+        (head_major ? kOrderHead : 0u) | (xcd_chunks(pt, false) ? kOrderXcd : 0u);
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
         const int nw = waves_per_item(p.n_blocks, p.n_items, H,
@@ -583,7 +589,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (p.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)p.n_items * nh), 64 * nw, 0, s>>>(
                     p.items, p.cols, p.mask, q, k, v, gr, O, lse, stats, dQ, p.part_o, p.N,
-                    ld, h0, nh, sl2, scale, head_major);
+                    ld, h0, nh, sl2, scale, order_a);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (p.n_split > 0) {
@@ -612,7 +618,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (pt.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)pt.n_items * nh), 64 * nw, 0, s>>>(
                     pt.items, pt.cols, pt.mask, q, k, v, gr, stats, dK, dV, pt.part_o,
-                    pt.N, ld, h0, nh, sl2, scale, head_major);
+                    pt.N, ld, h0, nh, sl2, scale, order_t);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (pt.n_split > 0) {

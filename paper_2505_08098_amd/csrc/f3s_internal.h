@@ -77,6 +77,25 @@ inline uint64_t head_major_threshold()
     const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
     return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
 }
+// Workgroup order flags of the fused kernels: heads outermost (one pass over
+// the work list per head), and consecutive ranges of the order per XCD.
+constexpr uint32_t kOrderHead = 1u;
+constexpr uint32_t kOrderXcd = 2u;
+// Whether a launch over plan p gives each XCD a consecutive range of the work
+// list.  The forward does when the items are nearly uniform (the largest at
+// most twice the mean block count, so no XCD's range is much heavier than
+// another's) and numerous (at least 2048): measured 2-3% faster on the
+// molecule and sequence workloads, while on skewed plans the ranges would
+// give the heaviest items to one XCD (1.7x slower on the million-node
+// graph).  The backward does not by default (within +-3% either way on the
+// same workloads).  F3S_XCD_CHUNKS=0 or 1 forces it for both (read at launch).
+inline bool xcd_chunks(const f3s_plan_s &p, bool forward)
+{
+    const char *e = getenv("F3S_XCD_CHUNKS");
+    if (e && *e) return atoi(e) != 0;
+    return forward && p.n_items >= 2048 &&
+           (int64_t)p.max_blocks * p.n_items <= 2 * p.n_blocks;
+}
 // Waves sharing one work item (forward and backward): 4 when a launch would
 // have fewer waves than the GPU has SIMDs (items x heads < 1024) and the
 // items average at least 4 blocks; else 2 when twice the waves still fit

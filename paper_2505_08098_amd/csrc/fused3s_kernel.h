@@ -183,7 +183,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const void *__restrict__ Kv, const void *__restrict__ Vv,
     void *__restrict__ O, float *__restrict__ part_o,
     float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
-    int32_t h0, int32_t nh, float sl2, bool head_major, uint32_t *__restrict__ trace)
+    int32_t h0, int32_t nh, float sl2, uint32_t order, uint32_t *__restrict__ trace)
 {
     uint64_t t_start = 0;
     if constexpr (kTrace) t_start = wall_clock64();
@@ -208,14 +208,15 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     // K and V rows while those stay cached) or head-major (one pass over the
     // list per head: with K and V far larger than the caches each head's
     // gathers then stream like a single head's).
+    const int wg = workgroup_position(order);
     int item, hl;
-    if (head_major) {
+    if (order & kOrderHead) {
         const int n_it = gridDim.x / nh;
-        hl = blockIdx.x / n_it;
-        item = blockIdx.x - hl * n_it;
+        hl = wg / n_it;
+        item = wg - hl * n_it;
     } else {
-        item = blockIdx.x / nh;
-        hl = blockIdx.x - item * nh;
+        item = wg / nh;
+        hl = wg - item * nh;
     }
     const int head = h0 + hl;
     const WorkItem it = items[item];
@@ -659,9 +660,11 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
             if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
             const bool head_major =
                 nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
+            const uint32_t order =
+                (head_major ? kOrderHead : 0u) | (xcd_chunks(p, true) ? kOrderXcd : 0u);
             kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
-                                               sl2, head_major, trace);
+                                               sl2, order, trace);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }

@@ -91,6 +91,21 @@ __device__ __forceinline__ void tile_fence()
     }
 }
 
+// Position of this workgroup in the launch order.  With kOrderXcd the order
+// is cut into 8 consecutive ranges, one per XCD: workgroups reach the 8 XCDs
+// round-robin (workgroup b on XCD b mod 8), so workgroup b takes position
+// (its XCD's first position) + b / 8, and neighbouring windows -- which share
+// K/V rows on banded and block-diagonal patterns -- meet in one XCD's L2.
+__device__ __forceinline__ int workgroup_position(uint32_t order)
+{
+    int wg = (int)blockIdx.x;
+    if (order & kOrderXcd) {
+        const int G = (int)gridDim.x, q = G >> 3, r = G & 7, x = wg & 7;
+        wg = x * q + min(x, r) + (wg >> 3);
+    }
+    return wg;
+}
+
 __device__ __forceinline__ h8 cat44(h4 lo, h4 hi)
 {
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);

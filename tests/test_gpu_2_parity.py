@@ -371,6 +371,28 @@ def test_multi_head_workloads(gpu, oracle, k, H):
             _assert_parity(O[:, h], ref)
 
 
+@pytest.mark.parametrize("k,H", [(5, 1), (2, 3), (4, 1)])
+def test_xcd_ranges_order_gives_identical_results(gpu, k, H, monkeypatch):
+    """Each XCD taking a consecutive range of the work list (workgroup b at
+    position (b mod 8)'s first + b / 8) only reorders independent work items:
+    O and lse are bit-identical to the round-robin order, with split windows
+    and several heads in both head orders."""
+    c = W.make_config(k, with_features=False)
+    N, d = c["N"], W.WORKLOADS[k]["d"]
+    rng = np.random.default_rng(60 + k)
+    shape = (N, H, d) if H > 1 else (N, d)
+    q, kk, v = (_dev(rng.standard_normal(shape).astype(np.float16)) for _ in range(3))
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), N)
+    for head_major in ("0", "1000000000000"):
+        monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", head_major)
+        outs = []
+        for chunks in ("0", "1"):
+            monkeypatch.setenv("F3S_XCD_CHUNKS", chunks)
+            outs.append(gpu.forward(plan, q, kk, v, scale=0.125))
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
 def test_dram_scale_graph_sampled(gpu, oracle):
     """The graph bench.py runs to measure the bandwidth the kernel sustains
     from DRAM (8,388,608 nodes, self + 16 uniform random neighbours, d = 128,
@@ -474,12 +496,13 @@ def test_split_windows_merge_all_feature_sizes(gpu, oracle, monkeypatch, d):
         assert np.abs(lse[fin, h] - reflse[fin]).max() < 2e-3
 
 
-@pytest.mark.parametrize("k", [1, 2, 4])
-def test_narrow_gather_ablation_is_bit_identical(gpu, monkeypatch, k):
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 3])
+def test_narrow_gather_ablation_is_bit_identical(gpu, oracle, monkeypatch, k):
     """F3S_NARROW_GATHER=1 only changes how K and V rows reach LDS (4-byte
     words instead of 16-byte chunks): same tiles, same arithmetic, so the
     output is bit-identical (the ablation runs one wave per work item, so the
-    reference does too); other type pairs are refused."""
+    reference does too), and it meets the oracle on every row; other type
+    pairs are refused."""
     monkeypatch.setenv("F3S_WAVES_PER_ITEM", "1")
     c = W.make_config(k)
     q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
@@ -491,6 +514,8 @@ def test_narrow_gather_ablation_is_bit_identical(gpu, monkeypatch, k):
     got, got_lse = gpu.forward(narrow, q, kk, v, scale=c["scale"])
     torch.cuda.synchronize()
     assert torch.equal(got, ref) and torch.equal(got_lse, ref_lse)
+    _assert_parity(got.cpu().numpy(), oracle.attention_f64(
+        c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"], c["scale"]))
     with pytest.raises(gpu.F3SError) as e:
         gpu.forward_typed(narrow, q, kk, v, out_dtype=torch.float16)
     assert e.value.code == 3

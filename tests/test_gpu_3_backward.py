@@ -368,6 +368,26 @@ def test_gradients_million_node_workload_sampled(gpu, oracle, dtype):
     plan_t.close()
 
 
+@pytest.mark.parametrize("k", [5, 4, 2])
+def test_backward_xcd_ranges_order_gives_identical_gradients(gpu, k, monkeypatch):
+    """Each XCD taking a consecutive range of the work list only reorders
+    independent work items of both passes: bit-identical gradients."""
+    c = W.make_config(k)
+    rng = np.random.default_rng(70 + k)
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    plan_t = plan.transpose()
+    q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
+    g = _dev(rng.standard_normal(c["Q"].shape).astype(np.float16))
+    O, lse = gpu.forward(plan, q, kk, v, scale=c["scale"])
+    outs = []
+    for chunks in ("0", "1"):
+        monkeypatch.setenv("F3S_XCD_CHUNKS", chunks)
+        outs.append(gpu.backward(plan, plan_t, q, kk, v, O, g, lse, scale=c["scale"]))
+    torch.cuda.synchronize()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 def test_backward_is_deterministic(gpu):
     c = W.make_config(2)
     rng = np.random.default_rng(13)
