@@ -287,8 +287,9 @@ def cu_balance(rec, khz):
 
 def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
     """Per-CU busy time of one traced forward call with the heavy-first work
-    list and with the window-order work list (F3S_NO_REORDER), the
-    load-balance comparison of the paper's row-window reordering ablation."""
+    list and with the window-order work list (F3S_NO_REORDER=0 and 1), the
+    load-balance comparison of the paper's row-window reordering ablation.
+    The library's own choice is one of the two (`library_order`)."""
     import numpy as np
     import torch
     import paper_2505_08098_amd as f3s
@@ -297,10 +298,7 @@ def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
            "wall_clock_khz": f3s.wall_clock_khz(0), "orders": {}}
     prev = os.environ.get("F3S_NO_REORDER")
     for order in ("heavy_first", "window_order"):
-        if order == "window_order":
-            os.environ["F3S_NO_REORDER"] = "1"
-        else:
-            os.environ.pop("F3S_NO_REORDER", None)
+        os.environ["F3S_NO_REORDER"] = "1" if order == "window_order" else "0"
         plan = f3s.Plan(rp, ci, c["N"])
         for _ in range(args.warmup):
             f3s.run(plan, Q, K, V, scale=c["scale"], stream=stream)
@@ -323,6 +321,8 @@ def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
         os.environ.pop("F3S_NO_REORDER", None)
     else:
         os.environ["F3S_NO_REORDER"] = prev
+    with f3s.Plan(rp, ci, c["N"]) as plan:
+        out["library_order"] = "window_order" if plan.info["flags"] & 1 else "heavy_first"
     print(json.dumps(out), flush=True)
 
 

@@ -65,7 +65,8 @@ typedef struct {
     int32_t n_items;       /* work items (windows or pieces) in the work list    */
     int32_t n_split;       /* windows that were split                            */
     int32_t n_pieces;      /* pieces in total (partial-result slots)             */
-    int32_t flags;         /* bit 0: work list left in window order (no reorder);
+    int32_t flags;         /* bit 0: work list in window order (forced, or
+                              chosen for nearly uniform windows; see f3s_plan);
                               bit 1: narrow K/V gathers (ablation)                */
     int64_t bsb_bytes;     /* window offsets + column lists + bitmaps            */
     int64_t device_bytes;  /* everything the plan holds on the device            */
@@ -78,7 +79,13 @@ typedef struct {
  *   F3S_PIECE_BLOCKS=<even n>  piece size of split windows (capped at the
  *                              largest window)
  *   F3S_NO_REORDER=1           work list in window order instead of
- *                              decreasing block count (Section 3.2)
+ *                              decreasing block count (Section 3.2);
+ *                              =0 always sorts.  Unset, plans of nearly
+ *                              uniform windows (at least 2048, the largest
+ *                              at most twice the mean block count) keep
+ *                              window order, which lets the forward give
+ *                              each XCD a run of neighbouring windows;
+ *                              all others are sorted
  *   F3S_NARROW_GATHER=1        the fp16 -> fp32 forward gathers K and V rows
  *                              in 4-byte words instead of 16-byte chunks (the
  *                              access granularity without the register

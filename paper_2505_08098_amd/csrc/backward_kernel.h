@@ -572,9 +572,9 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     hipError_t e = hipSuccess;
     const bool head_major = H > 1 && 2ull * p.N * ld * 2 > head_major_threshold();
     const uint32_t order_a =
-        (head_major ? kOrderHead : 0u) | (xcd_chunks(p, false) ? kOrderXcd : 0u);
+        (head_major ? kOrderHead : 0u) | (xcd_chunks(p, H) ? kOrderXcd : 0u);
     const uint32_t order_t =
-        (head_major ? kOrderHead : 0u) | (xcd_chunks(pt, false) ? kOrderXcd : 0u);
+        (head_major ? kOrderHead : 0u) | (xcd_chunks(pt, H) ? kOrderXcd : 0u);
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
         const int nw = waves_per_item(p.n_blocks, p.n_items, H,

@@ -317,7 +317,11 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     //         split windows, item count (one host round trip for all) -------
     HIP_TRY(launch_window_stats(u, bits, T, nb, &st->n_unique, &st->nnz, &st->n_blocks,
                                 &st->max_blocks, s));
-    const bool reorder = env_int("F3S_NO_REORDER", 0) == 0;
+    // F3S_NO_REORDER=1 keeps window order, =0 always sorts; unset, the order
+    // is chosen below once the block counts are known
+    const char *order_env = getenv("F3S_NO_REORDER");
+    const bool order_forced = order_env && *order_env;
+    const bool reorder = !order_forced || atoi(order_env) == 0;
     p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0);
     HIP_TRY(launch_bin_keys(nb, T, &st->n_blocks, &st->max_blocks,
                             env_int("F3S_PIECE_BLOCKS", 0), slots, reorder,
@@ -345,6 +349,15 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     const int64_t n_items = (int64_t)T - p->n_split + p->n_pieces;
     if (n_items > INT32_MAX) return F3S_ERR_UNSUPPORTED;
     p->n_items = (int32_t)n_items;
+    // Nearly uniform windows (the largest at most twice the mean, and many of
+    // them) leave the heavy-first sort nothing to balance; window order then
+    // keeps neighbouring windows -- which share K/V rows on banded and
+    // block-diagonal patterns -- next to each other in the work list, which
+    // the forward hands to each XCD as one consecutive range.
+    if (reorder && !order_forced && uniform_windows(T, B, hs.max_blocks)) {
+        HIP_TRY(hipMemsetAsync(key, 0, sizeof(int32_t) * (size_t)T, s));
+        p->flags |= 1;
+    }
 
     // ---- 4. the plan's arrays: one allocation, plus the partial buffers --
     HIP_TRY(alloc_store(p, nullptr));

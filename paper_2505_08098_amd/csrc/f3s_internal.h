@@ -81,20 +81,27 @@ inline uint64_t head_major_threshold()
 // the work list per head), and consecutive ranges of the order per XCD.
 constexpr uint32_t kOrderHead = 1u;
 constexpr uint32_t kOrderXcd = 2u;
-// Whether a launch over plan p gives each XCD a consecutive range of the work
-// list.  The forward does when the items are nearly uniform (the largest at
-// most twice the mean block count, so no XCD's range is much heavier than
-// another's) and numerous (at least 2048): measured 2-3% faster on the
-// molecule and sequence workloads, while on skewed plans the ranges would
-// give the heaviest items to one XCD (1.7x slower on the million-node
-// graph).  The backward does not by default (within +-3% either way on the
-// same workloads).  F3S_XCD_CHUNKS=0 or 1 forces it for both (read at launch).
-inline bool xcd_chunks(const f3s_plan_s &p, bool forward)
+// Plans whose windows are nearly uniform: at least 2048 windows, the largest
+// holding at most twice the mean block count.  Their work list keeps window
+// order (heavy-first sorting has nothing to balance) and the forward gives
+// each XCD a consecutive range of it.
+inline bool uniform_windows(int64_t windows, int64_t blocks, int64_t max_blocks)
+{
+    return windows >= 2048 && max_blocks * windows <= 2 * blocks;
+}
+// Whether a launch of `heads` heads over plan p gives each XCD a consecutive
+// range of the work list: for one head over a nearly uniform plan (no XCD's
+// range is then much heavier than another's).  With its window-order work
+// list the molecule batch ran 18.8 -> 15.6 us forward and 52.8 -> 45.0 us
+// backward; on skewed plans the ranges would give the heaviest items to one
+// XCD (1.7x slower on the million-node graph), and with four heads of the
+// sequence workload they measured 45% slower (unexplained), so several heads
+// keep round-robin.  F3S_XCD_CHUNKS=0 or 1 forces it (read at launch).
+inline bool xcd_chunks(const f3s_plan_s &p, int32_t heads)
 {
     const char *e = getenv("F3S_XCD_CHUNKS");
     if (e && *e) return atoi(e) != 0;
-    return forward && p.n_items >= 2048 &&
-           (int64_t)p.max_blocks * p.n_items <= 2 * p.n_blocks;
+    return heads == 1 && uniform_windows(p.n_items, p.n_blocks, p.max_blocks);
 }
 // Waves sharing one work item (forward and backward): 4 when a launch would
 // have fewer waves than the GPU has SIMDs (items x heads < 1024) and the

@@ -661,7 +661,7 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
             const bool head_major =
                 nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
             const uint32_t order =
-                (head_major ? kOrderHead : 0u) | (xcd_chunks(p, true) ? kOrderXcd : 0u);
+                (head_major ? kOrderHead : 0u) | (xcd_chunks(p, H) ? kOrderXcd : 0u);
             kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
                                                p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
                                                sl2, order, trace);

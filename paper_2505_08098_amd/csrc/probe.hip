@@ -4,7 +4,7 @@
 // on this GPU, and what the caches and HBM together deliver to a plan's
 // gathers), measured in the same process as the kernel.
 #include "f3s_probe.h"
-#include "f3s_internal.h"
+#include "kernel_common.h"
 
 namespace {
 
@@ -71,20 +71,21 @@ __global__ __launch_bounds__(kThreads) void k_probe_write(u4 *__restrict__ dst, 
 // one row, padding slots re-read the block's first column), and 16 rows of
 // D fp32 written (to O for a whole window, to the piece's partial slot for a
 // piece of a split window).  Four waves share an item, wave w taking block
-// pairs w, w + 4, ...; each wave has two pairs in flight.  The written
-// values are the loaded bits folded together (garbage, but they keep every
-// load live).
+// pairs w, w + 4, ...; each wave has two pairs in flight.  Workgroups take
+// items in the fused kernel's order (XCD ranges where it uses them).  The
+// written values are the loaded bits folded together (garbage, but they keep
+// every load live).
 template <int D, bool kWide>
 __global__ __launch_bounds__(256) void k_probe_gather(
     const f3s::WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const char *__restrict__ Q,
     const char *__restrict__ K, const char *__restrict__ V, float *__restrict__ O,
-    float *__restrict__ part_o, int32_t N)
+    float *__restrict__ part_o, int32_t N, uint32_t order)
 {
     constexpr int LPR = D / 8;   // 16-byte chunks per row
     constexpr int NI = D / 16;   // chunks per lane per 32-row tile
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const f3s::WorkItem it = items[blockIdx.x];
+    const f3s::WorkItem it = items[f3s::workgroup_position(order)];
     uint32_t acc = 0;
     // Q: rows 4 wv .. 4 wv + 3 of the window (pad rows read row N - 1)
     for (int f = lane; f < 4 * LPR; f += 64) {
@@ -154,7 +155,8 @@ hipError_t launch_gather_d(const f3s_plan_s &p, const void *Q, const void *K, co
     auto kern = wide ? k_probe_gather<D, true> : k_probe_gather<D, false>;
     kern<<<p.n_items, 256, 0, s>>>(p.items, p.cols, p.mask, static_cast<const char *>(Q),
                                    static_cast<const char *>(K),
-                                   static_cast<const char *>(V), O, p.part_o, p.N);
+                                   static_cast<const char *>(V), O, p.part_o, p.N,
+                                   f3s::xcd_chunks(p, 1) ? f3s::kOrderXcd : 0u);
     return hipGetLastError();
 }
 

@@ -226,6 +226,24 @@ def test_plan_is_deterministic(gpu):
         assert np.array_equal(a[k], b[k]), k
 
 
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_work_list_order_rule(gpu, oracle, k, monkeypatch):
+    """Unforced, the work list keeps window order exactly when the windows
+    are nearly uniform: at least 2048 of them, the largest holding at most
+    twice the mean block count (configs 4 and 5); F3S_NO_REORDER=0 sorts
+    every plan.  Both lists equal the oracle's for that order."""
+    c = W.make_config(k, with_features=False)
+    nb = oracle.bsb(c["row_ptr"], c["col_idx"], c["N"])["nb"].astype(np.int64)
+    uniform = nb.size >= 2048 and int(nb.max()) * nb.size <= 2 * int(nb.sum())
+    assert uniform == (k in (4, 5))
+    monkeypatch.delenv("F3S_NO_REORDER", raising=False)
+    info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
+    assert bool(info["flags"] & 1) == uniform
+    monkeypatch.setenv("F3S_NO_REORDER", "0")
+    info = _check_plan_against_oracle(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"])
+    assert not info["flags"] & 1
+
+
 def test_plan_without_reordering(gpu, oracle, monkeypatch):
     """Ablation switch: the work list keeps window order (Section 3.2 off)."""
     monkeypatch.setenv("F3S_NO_REORDER", "1")
