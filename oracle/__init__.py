@@ -77,6 +77,10 @@ def lib():
         L.oracle_bsb_sizes.restype = ctypes.c_int
         L.oracle_bsb_build.argtypes = [i32, vp, vp, vp, vp, vp]
         L.oracle_bsb_build.restype = ctypes.c_int
+        L.oracle_bsb_sizes_rows.argtypes = [i32, vp, vp, vp, vp, vp]
+        L.oracle_bsb_sizes_rows.restype = ctypes.c_int
+        L.oracle_bsb_build_rows.argtypes = [i32, vp, vp, vp, vp, vp, vp]
+        L.oracle_bsb_build_rows.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -240,30 +244,82 @@ def num_windows(N):
     return lib().oracle_num_windows(int(N))
 
 
-def bsb(row_ptr, col_idx, N):
+def bsb(row_ptr, col_idx, N, win_row=None):
     """Binary Sparse Block layout (Section 3.1) with r = c = 16.
+
+    ``win_row`` (T+1 ints) gives the first row of each window; by default the
+    fixed windows of Algorithm 1 (16 w, the last clipped at N).  Other
+    windows hold 1 to 16 consecutive rows (see :func:`segment_windows`).
 
     Returns a dict with ``u`` (distinct columns per window), ``nb`` (blocks
     per window), ``blk_off`` (T+1), ``cols`` (16 per block, -1 padding) and
-    ``mask`` (8 uint32 words per block; bit convention in oracle.c).
+    ``mask`` (8 uint32 words per block; bit convention in oracle.c, rows
+    counted from the window's first row).
     """
     rp, ci = _csr(row_ptr, col_idx)
-    T = num_windows(N)
+    if win_row is None:
+        T = num_windows(N)
+        wr = np.minimum(np.arange(T + 1, dtype=np.int64) * 16, N).astype(np.int32)
+    else:
+        wr = np.ascontiguousarray(win_row, dtype=np.int32)
+        T = wr.size - 1
+        if T < 0 or int(wr[-1]) != N:
+            raise ValueError("win_row must end at N")
     u = np.empty(max(T, 1), dtype=np.int32)
     nb = np.empty(max(T, 1), dtype=np.int32)
-    rc = lib().oracle_bsb_sizes(int(N), _ptr(rp), _ptr(ci), _ptr(u), _ptr(nb))
+    rc = lib().oracle_bsb_sizes_rows(int(T), _ptr(wr), _ptr(rp), _ptr(ci), _ptr(u),
+                                     _ptr(nb))
     if rc != 0:
         raise ValueError(f"oracle bsb failed (code {rc})")
     B = int(nb[:T].sum())
     blk_off = np.empty(T + 1, dtype=np.int32)
     cols = np.empty(max(16 * B, 1), dtype=np.int32)
     mask = np.empty(max(8 * B, 1), dtype=np.uint32)
-    rc = lib().oracle_bsb_build(int(N), _ptr(rp), _ptr(ci), _ptr(blk_off),
-                                _ptr(cols), _ptr(mask))
+    rc = lib().oracle_bsb_build_rows(int(T), _ptr(wr), _ptr(rp), _ptr(ci),
+                                     _ptr(blk_off), _ptr(cols), _ptr(mask))
     if rc != 0:
         raise ValueError(f"oracle bsb failed (code {rc})")
     return dict(u=u[:T], nb=nb[:T], blk_off=blk_off, cols=cols[: 16 * B],
-                mask=mask[: 8 * B])
+                mask=mask[: 8 * B], win_row=wr)
+
+
+def segment_windows(seg_ptr):
+    """Row windows aligned to the graphs of a batch.
+
+    The paper leaves the use of component boundaries in batched graphs to
+    future work (Section 4.2); this is the layout used for it here.  The rows
+    form consecutive segments (graph g: rows ``seg_ptr[g] .. seg_ptr[g+1]-1``)
+    and a window never holds part of a segment together with rows outside it,
+    except at 16-row steps inside a long segment.  Walking from row 0:
+
+    * if more than 16 rows of the current segment remain, the window is the
+      next 16 of them;
+    * otherwise the window is the rest of the segment followed by every whole
+      segment after it that still fits into 16 rows (empty segments always
+      fit).
+
+    Returns the windows' first rows followed by N (``T+1`` ints).
+    """
+    seg = [int(x) for x in seg_ptr]
+    if not seg or seg[0] != 0 or any(b < a for a, b in zip(seg, seg[1:])):
+        raise ValueError("seg_ptr must start at 0 and not decrease")
+    N = seg[-1]
+    starts = []
+    r, g = 0, 0
+    while r < N:
+        while seg[g + 1] <= r:          # the segment that holds row r
+            g += 1
+        starts.append(r)
+        if seg[g + 1] - r > 16:
+            r += 16
+            continue
+        r = seg[g + 1]                  # rest of the segment ...
+        g += 1
+        while g + 1 < len(seg) and seg[g + 1] - starts[-1] <= 16:
+            r = seg[g + 1]              # ... and the whole segments that fit
+            g += 1
+    starts.append(N)
+    return np.array(starts, dtype=np.int32)
 
 
 def worklist(nb, blk_off, piece, reorder=True):

@@ -405,16 +405,35 @@ int oracle_3s_f64_rows(int32_t N, const int32_t *row_ptr, const int32_t *col_idx
 int32_t oracle_num_windows(int32_t N) { return (N + RW - 1) / RW; }
 
 /*
+ * Row windows given by their first rows: window w covers the rows
+ * [win_row[w], win_row[w+1]), between 1 and 16 of them, in increasing order
+ * from win_row[0] = 0.  The fixed windows of Algorithm 1 are
+ * win_row[w] = 16 w (the last one clipped at N); windows aligned to the
+ * graphs of a batch (the component-aware layout Section 4.2 leaves to
+ * future work) give other starts.  Returns 0, or -2 if win_row breaks
+ * these rules.
+ */
+static int check_windows(int32_t T, const int32_t *win_row)
+{
+    if (T < 0 || win_row[0] != 0) return -2;
+    for (int32_t w = 0; w < T; ++w) {
+        int32_t n = win_row[w + 1] - win_row[w];
+        if (n < 1 || n > RW) return -2;
+    }
+    return 0;
+}
+
+/*
  * Step 2 of the construction: per window w, the sorted distinct columns that
  * hold at least one non-zero (all-zero columns removed).  Writes u[w] (count)
  * and nb[w] = ceil(u[w] / 16) (step 3: number of blocks).  Returns 0.
  */
-int oracle_bsb_sizes(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
-                     int32_t *u, int32_t *nb)
+int oracle_bsb_sizes_rows(int32_t T, const int32_t *win_row, const int32_t *row_ptr,
+                          const int32_t *col_idx, int32_t *u, int32_t *nb)
 {
-    int32_t T = oracle_num_windows(N);
+    if (check_windows(T, win_row)) return -2;
     for (int32_t w = 0; w < T; ++w) {
-        int32_t r0 = w * RW, r1 = (w + 1) * RW < N ? (w + 1) * RW : N;
+        int32_t r0 = win_row[w], r1 = win_row[w + 1];
         int64_t beg = row_ptr[r0], end = row_ptr[r1], n = end - beg;
         int64_t cnt = 0;
         if (n > 0) {
@@ -439,25 +458,28 @@ int oracle_bsb_sizes(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
  *                 gather list the paper calls sptd), -1 in padding slots
  *   mask[8*B]     one 256-bit bitmap per 16x16 block.
  * Bit convention (a storage choice; it does not change which bits are set):
- * the non-zero at window row r (0..15) and block column c (0..15) is bit
+ * the non-zero at window row r (0..15, counted from the window's first row)
+ * and block column c (0..15) is bit
  *     k = 4 * (r + 16 * (c / 4)) + (c % 4)
  * of the block, i.e. bit (k % 32) of 32-bit word (k / 32).
  */
-int oracle_bsb_build(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
-                     int32_t *blk_off, int32_t *cols, uint32_t *mask)
+int oracle_bsb_build_rows(int32_t T, const int32_t *win_row, const int32_t *row_ptr,
+                          const int32_t *col_idx, int32_t *blk_off, int32_t *cols,
+                          uint32_t *mask)
 {
-    int32_t T = oracle_num_windows(N);
+    if (check_windows(T, win_row)) return -2;
     int32_t *u = (int32_t *)malloc(sizeof(int32_t) * (T > 0 ? T : 1));
     int32_t *nb = (int32_t *)malloc(sizeof(int32_t) * (T > 0 ? T : 1));
     if (!u || !nb) { free(u); free(nb); return -6; }
-    oracle_bsb_sizes(N, row_ptr, col_idx, u, nb);
+    int rc = oracle_bsb_sizes_rows(T, win_row, row_ptr, col_idx, u, nb);
+    if (rc) { free(u); free(nb); return rc; }
     blk_off[0] = 0;
     for (int32_t w = 0; w < T; ++w) blk_off[w + 1] = blk_off[w] + nb[w];
     int64_t B = blk_off[T];
     for (int64_t k = 0; k < BC * B; ++k) cols[k] = -1;
     for (int64_t k = 0; k < 8 * B; ++k) mask[k] = 0;
     for (int32_t w = 0; w < T; ++w) {
-        int32_t r0 = w * RW, r1 = (w + 1) * RW < N ? (w + 1) * RW : N;
+        int32_t r0 = win_row[w], r1 = win_row[w + 1];
         int64_t beg = row_ptr[r0], end = row_ptr[r1], n = end - beg;
         if (n == 0) continue;
         int32_t *c = (int32_t *)malloc(sizeof(int32_t) * n);
@@ -486,4 +508,36 @@ int oracle_bsb_build(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
     free(u);
     free(nb);
     return 0;
+}
+
+/* The fixed windows of Algorithm 1: rows [16 w, min(16 w + 16, N)). */
+static int32_t *fixed_windows(int32_t N)
+{
+    int32_t T = oracle_num_windows(N);
+    int32_t *win_row = (int32_t *)malloc(sizeof(int32_t) * (T + 1));
+    if (!win_row) return NULL;
+    for (int32_t w = 0; w < T; ++w) win_row[w] = w * RW;
+    win_row[T] = N;
+    return win_row;
+}
+
+int oracle_bsb_sizes(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
+                     int32_t *u, int32_t *nb)
+{
+    int32_t *win_row = fixed_windows(N);
+    if (!win_row) return -6;
+    int rc = oracle_bsb_sizes_rows(oracle_num_windows(N), win_row, row_ptr, col_idx, u, nb);
+    free(win_row);
+    return rc;
+}
+
+int oracle_bsb_build(int32_t N, const int32_t *row_ptr, const int32_t *col_idx,
+                     int32_t *blk_off, int32_t *cols, uint32_t *mask)
+{
+    int32_t *win_row = fixed_windows(N);
+    if (!win_row) return -6;
+    int rc = oracle_bsb_build_rows(oracle_num_windows(N), win_row, row_ptr, col_idx,
+                                   blk_off, cols, mask);
+    free(win_row);
+    return rc;
 }

@@ -158,10 +158,13 @@ def _pruefer_tree(rng, n):
     return edges
 
 
-def molecules(rng, n_graphs=4096, n_min=15, n_max=45, extra=0.10):
-    """Batched molecule-like graphs as one block-diagonal CSR."""
+def molecules(rng, n_graphs=4096, n_min=15, n_max=45, extra=0.10, with_segments=False):
+    """Batched molecule-like graphs as one block-diagonal CSR.  With
+    ``with_segments`` also the graphs' first rows followed by N (the batch
+    offsets a graph library keeps beside a batch)."""
     src, dst = [], []
     base = 0
+    seg = [0]
     for _ in range(n_graphs):
         n = int(rng.integers(n_min, n_max + 1))
         tree = _pruefer_tree(rng, n)
@@ -181,7 +184,11 @@ def molecules(rng, n_graphs=4096, n_min=15, n_max=45, extra=0.10):
             src.append(base + a)
             dst.append(base + b)
         base += n
-    return csr_from_edges(base, np.array(src), np.array(dst))
+        seg.append(base)
+    rp, ci = csr_from_edges(base, np.array(src), np.array(dst))
+    if with_segments:
+        return rp, ci, np.array(seg, dtype=np.int32)
+    return rp, ci
 
 
 def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
@@ -205,9 +212,11 @@ def sequence_window_random(rng, L=32768, before=128, after=127, n_rand=64):
 
 @functools.lru_cache(maxsize=2)
 def _graph(k, seed):
-    """The CSR of workload k (drawn from the graph stream only; the last two
-    are kept, the million-node graph taking tens of seconds to draw)."""
+    """The CSR of workload k and its graph offsets (batched graphs only, else
+    None), drawn from the graph stream only; the last two are kept, the
+    million-node graph taking tens of seconds to draw."""
     g, _ = _streams(seed)
+    seg = None
     if k == 1:
         rp, ci = erdos_renyi(g, N=1024, avg_nbrs=15.0)
     elif k == 2:
@@ -215,27 +224,32 @@ def _graph(k, seed):
     elif k == 3:
         rp, ci = chung_lu(g, 1048576, 2.5, 16.0, 4096.0, permute=True)
     elif k == 4:
-        rp, ci = molecules(g)
+        rp, ci, seg = molecules(g, with_segments=True)
+        seg.flags.writeable = False
     else:
         rp, ci = sequence_window_random(g)
     rp.flags.writeable = False
     ci.flags.writeable = False
-    return rp, ci
+    return rp, ci, seg
 
 
 def make_config(k, seed=0, with_features=True, dtype="f16"):
-    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V);
+    """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V),
+    plus seg_ptr (the graphs' first rows, then N) for the batched graphs;
     dtype "f16" (default), "bf16" or "fp8" selects the feature storage type.
-    row_ptr and col_idx are fresh copies (callers may modify them)."""
+    The arrays are fresh copies (callers may modify them)."""
     if k not in WORKLOADS:
         raise ValueError(f"unknown workload {k}")
     cfg = WORKLOADS[k]
     _, f = _streams(seed)
-    rp, ci = (a.copy() for a in _graph(k, seed))
+    rp, ci, seg = _graph(k, seed)
+    rp, ci = rp.copy(), ci.copy()
     N = len(rp) - 1
     d = cfg["d"]
     out = dict(name=cfg["name"], N=N, d=d, scale=1.0 / math.sqrt(d),
                row_ptr=rp, col_idx=ci)
+    if seg is not None:
+        out["seg_ptr"] = seg.copy()
     if with_features:
         out["Q"], out["K"], out["V"] = features(f, N, d, dtype)
     return out

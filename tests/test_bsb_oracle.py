@@ -26,6 +26,7 @@ def _decode(b, N):
     """Edge set encoded by a BSB layout (inverse of the construction)."""
     edges = set()
     T = len(b["blk_off"]) - 1
+    r0s = b.get("win_row", [16 * w for w in range(T)])
     for w in range(T):
         for blk in range(b["blk_off"][w], b["blk_off"][w + 1]):
             for r in range(16):
@@ -34,7 +35,7 @@ def _decode(b, N):
                     if (int(b["mask"][8 * blk + k // 32]) >> (k % 32)) & 1:
                         col = int(b["cols"][16 * blk + c])
                         assert col >= 0, "bit set on a padding column"
-                        edges.add((16 * w + r, col))
+                        edges.add((int(r0s[w]) + r, col))
     return edges
 
 
@@ -143,3 +144,108 @@ def test_worklist_without_reordering_keeps_window_order(oracle):
     assert merges.tolist() == [[2, 0, 3]]
     sorted_items, _ = oracle.worklist(nb, blk_off, 16)
     assert sorted_items[:, 0].tolist() == [2, 2, 2, 3, 0, 4, 1]
+
+
+# ---- windows aligned to the graphs of a batch (Section 4.2's future work) ----
+
+def test_segment_windows_hand_example(oracle):
+    """Graphs of 15, 45, 3, 5, 20, 0 and 32 rows (N = 120), windows by hand:
+    [0,15) the first graph (the 45-row graph does not fit beside it);
+    [15,31) [31,47) 16-row steps of the 45-row graph, whose last 13 rows
+    [47,60) take the 3-row graph too (16 rows) but not the 5-row one;
+    [60,63) is packed: [63,68) the 5-row graph alone (the 20-row one does
+    not fit); [68,84) a 16-row step of the 20-row graph, [84,88) its last
+    4 rows with the empty graph; [88,104) [104,120) the 32-row graph."""
+    got = oracle.segment_windows([0, 15, 60, 63, 68, 88, 88, 120]).tolist()
+    assert got == [0, 15, 31, 47, 63, 68, 84, 88, 104, 120]
+
+
+def _check_segment_windows(seg, wr):
+    """The rule of segment_windows, restated as properties of the result."""
+    seg = [int(x) for x in seg]
+    N = seg[-1]
+    wr = [int(x) for x in wr]
+    assert wr[0] == 0 and wr[-1] == N
+    for a, b in zip(wr, wr[1:]):
+        assert 1 <= b - a <= 16
+        g = max(k for k in range(len(seg) - 1) if seg[k] <= a < seg[k + 1])
+        assert (a - seg[g]) % 16 == 0          # starts at a 16-row step
+        rest = seg[g + 1] - a
+        if rest > 16:
+            assert b == a + 16                 # a step inside a long graph
+        else:
+            assert b in seg                    # ends at a graph boundary ...
+            later = [s for s in seg if s > b]
+            if later:
+                assert min(later) - a > 16     # ... and the next graph did not fit
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_segment_windows_properties(oracle, seed):
+    rng = np.random.default_rng(300 + seed)
+    sizes = rng.integers(0, 50, size=int(rng.integers(1, 40)))
+    sizes[rng.random(sizes.size) < 0.2] = 0
+    sizes[rng.random(sizes.size) < 0.3] //= 8
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    if seg[-1] == 0:
+        assert oracle.segment_windows(seg).tolist() == [0]
+        return
+    _check_segment_windows(seg, oracle.segment_windows(seg))
+
+
+def test_segment_windows_molecule_batch(oracle):
+    c = W.make_config(4, with_features=False)
+    wr = oracle.segment_windows(c["seg_ptr"])
+    _check_segment_windows(c["seg_ptr"], wr)
+    # the batch is block-diagonal: a window's columns lie inside the graphs
+    # its rows belong to
+    seg = c["seg_ptr"]
+    b = oracle.bsb(c["row_ptr"], c["col_idx"], c["N"], win_row=wr)
+    g0 = np.searchsorted(seg, wr[:-1], side="right") - 1
+    g1 = np.searchsorted(seg, wr[1:] - 1, side="right") - 1
+    for w in range(len(wr) - 1):
+        lo, hi = b["blk_off"][w], b["blk_off"][w + 1]
+        cl = b["cols"][16 * lo:16 * hi]
+        cl = cl[cl >= 0]
+        assert cl.min() >= seg[g0[w]] and cl.max() < seg[g1[w] + 1]
+    assert _decode(b, c["N"]) == _edges(c["row_ptr"], c["col_idx"])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_brute_force_segment_windows(oracle, seed):
+    """Layout over windows of 1..16 rows against Python sets, and its decode."""
+    rng = np.random.default_rng(400 + seed)
+    N = int(rng.integers(1, 90))
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 40), empty_frac=0.2, dup_frac=0.3)
+    cuts = np.sort(rng.choice(np.arange(1, N), size=min(N - 1, int(rng.integers(0, 8))),
+                              replace=False)) if N > 1 else np.array([], dtype=int)
+    seg = np.concatenate([[0], cuts, [N]]).astype(np.int32)
+    wr = oracle.segment_windows(seg)
+    b = oracle.bsb(rp, ci, N, win_row=wr)
+    T = len(wr) - 1
+    assert len(b["blk_off"]) == T + 1
+    for w in range(T):
+        r0, r1 = int(wr[w]), int(wr[w + 1])
+        distinct = sorted(set(ci[rp[r0]:rp[r1]].tolist()))
+        assert b["u"][w] == len(distinct)
+        assert b["nb"][w] == -(-len(distinct) // 16)
+        lo, hi = b["blk_off"][w], b["blk_off"][w + 1]
+        slots = b["cols"][16 * lo:16 * hi].tolist()
+        assert slots == distinct + [-1] * (16 * (hi - lo) - len(distinct))
+        for blk in range(lo, hi):                # no bit beyond the window's rows
+            for r in range(r1 - r0, 16):
+                for c in range(16):
+                    k = _bit(r, c)
+                    assert not (int(b["mask"][8 * blk + k // 32]) >> (k % 32)) & 1
+    assert _decode(b, N) == _edges(rp, ci)
+
+
+def test_window_rows_reject_bad_windows(oracle):
+    rp = np.array([0, 1, 2], dtype=np.int32)
+    ci = np.array([0, 1], dtype=np.int32)
+    for wr in ([0, 0, 2], [0, 2, 1], [1, 2]):
+        with pytest.raises(ValueError):
+            oracle.bsb(rp, ci, 2, win_row=np.array(wr + ([2] if wr[-1] != 2 else []),
+                                                   dtype=np.int32))
+    with pytest.raises(ValueError):
+        oracle.segment_windows([0, 5, 3])
