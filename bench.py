@@ -285,7 +285,7 @@ def cu_balance(rec, khz):
             "resident_per_cu_mean": round(float(dur.sum()) / float(busy.sum()), 2)}
 
 
-def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
+def bench_cu_trace(args, c, make_plan, Q, K, V, stream, dev):
     """Per-CU busy time of one traced forward call with the heavy-first work
     list and with the window-order work list (F3S_NO_REORDER=0 and 1), the
     load-balance comparison of the paper's row-window reordering ablation.
@@ -294,12 +294,14 @@ def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
     import torch
     import paper_2505_08098_amd as f3s
     out = {"metric": "per-CU busy time of one fused 3S call (f3s_run_trace)",
-           "n_gpus": 1, "config": {"workload": c["name"], "N": c["N"], "d": c["d"]},
+           "n_gpus": 1, "config": {"workload": c["name"], "N": c["N"], "d": c["d"],
+                                   "windows": "aligned to the graphs" if args.segments
+                                   else "16 rows"},
            "wall_clock_khz": f3s.wall_clock_khz(0), "orders": {}}
     prev = os.environ.get("F3S_NO_REORDER")
     for order in ("heavy_first", "window_order"):
         os.environ["F3S_NO_REORDER"] = "1" if order == "window_order" else "0"
-        plan = f3s.Plan(rp, ci, c["N"])
+        plan = make_plan()
         for _ in range(args.warmup):
             f3s.run(plan, Q, K, V, scale=c["scale"], stream=stream)
         ms = []
@@ -321,7 +323,7 @@ def bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev):
         os.environ.pop("F3S_NO_REORDER", None)
     else:
         os.environ["F3S_NO_REORDER"] = prev
-    with f3s.Plan(rp, ci, c["N"]) as plan:
+    with make_plan() as plan:
         out["library_order"] = "window_order" if plan.info["flags"] & 1 else "heavy_first"
     print(json.dumps(out), flush=True)
 
@@ -519,6 +521,9 @@ def main():
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the probe kernels (streaming read/copy/write over 4 GiB "
                          "and the plan's access pattern without arithmetic)")
+    ap.add_argument("--segments", action="store_true",
+                    help="row windows aligned to the graphs of the batch "
+                         "(f3s_plan_segments; the batched-graph workload 4, forward only)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run 3 plain device copies of this many MiB "
                          "(reference dispatches for scaling HBM byte counters)")
@@ -529,6 +534,10 @@ def main():
         sys.exit(2)
     if args.gpus != 1:
         print(json.dumps({"error": "bench.py measures one GPU: --gpus must be 1"}))
+        sys.exit(2)
+    if args.segments and (args.workload != 4 or args.backward):
+        print(json.dumps({"error": "--segments needs the batched-graph workload 4 and "
+                                   "the forward pass"}))
         sys.exit(2)
 
     import numpy as np
@@ -570,14 +579,18 @@ def main():
             f3s.forward_typed(plan, Q, K, V, out_dtype=out_dt, scale=c["scale"], out=O)
         else:
             f3s.run(plan, Q, K, V, scale=c["scale"], out=O)
+    def make_plan():
+        if args.segments:
+            return f3s.Plan.segments(rp, ci, N, c["seg_ptr"])
+        return f3s.Plan(rp, ci, N)
     torch.cuda.synchronize()
-    plan = f3s.Plan(rp, ci, N)
+    plan = make_plan()
     info = plan.info
     # more builds of the same plan (median of 5): the first one in a process
     # also pays the one-time loading of the plan kernels' code
     warm = []
     for _ in range(5):
-        plan2 = f3s.Plan(rp, ci, N)
+        plan2 = make_plan()
         warm.append(plan2.info["build_ms"])
         plan2.close()
     plan_ms_warm = sorted(warm)[len(warm) // 2]
@@ -590,7 +603,7 @@ def main():
             print(json.dumps({"error": "--cu-trace times the one-head fp16 -> fp32 call"}))
             sys.exit(2)
         plan.close()
-        return bench_cu_trace(args, c, rp, ci, Q, K, V, stream, dev)
+        return bench_cu_trace(args, c, make_plan, Q, K, V, stream, dev)
     for _ in range(args.warmup):
         call()
     torch.cuda.synchronize()
@@ -666,6 +679,7 @@ def main():
             }[args.workload],
             "N": N, "nnz": info["nnz"], "d": d, "heads": H, "scale": c["scale"],
             "in_dtype": args.in_dtype, "out_dtype": args.out_dtype,
+            "windows": "aligned to the graphs" if args.segments else "16 rows",
             "seed": args.seed,
             "parallelism": "single GPU",
         },

@@ -55,7 +55,8 @@ typedef struct f3s_plan_s *f3s_plan_t;
 
 typedef struct {
     int32_t N;             /* rows (= columns) of A                              */
-    int32_t n_windows;     /* T_r = ceil(N / 16)  (Algorithm 1)                  */
+    int32_t n_windows;     /* T_r = ceil(N / 16) (Algorithm 1), or the windows
+                              of f3s_plan_segments                              */
     int64_t nnz_csr;       /* entries in the CSR, repeats included               */
     int64_t nnz;           /* distinct (row, column) pairs: the non-zeros of A   */
     int64_t n_unique;      /* sum over windows of distinct columns (bc, Table 3) */
@@ -67,7 +68,9 @@ typedef struct {
     int32_t n_pieces;      /* pieces in total (partial-result slots)             */
     int32_t flags;         /* bit 0: work list in window order (forced, or
                               chosen for nearly uniform windows; see f3s_plan);
-                              bit 1: narrow K/V gathers (ablation)                */
+                              bit 1: narrow K/V gathers (ablation);
+                              bit 2: windows aligned to the graphs of a batch
+                              (f3s_plan_segments)                               */
     int64_t bsb_bytes;     /* window offsets + column lists + bitmaps            */
     int64_t device_bytes;  /* everything the plan holds on the device            */
     double build_ms;       /* wall time of f3s_plan                              */
@@ -121,6 +124,31 @@ size_t f3s_plan_workspace_bytes(int32_t N, int64_t nnz);
  */
 f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                        void *workspace, size_t workspace_bytes);
+
+/*
+ * f3s_plan for a batch of graphs stored as one block-diagonal pattern, with
+ * row windows aligned to the graphs (the use of component boundaries that
+ * Section 4.2 leaves to future work).  Graph g holds the consecutive rows
+ * seg_ptr[g] .. seg_ptr[g+1] - 1.  Walking from row 0, a window is the next
+ * 16 rows of the current graph while more than 16 of them remain; otherwise
+ * it is the rest of that graph together with every whole graph after it
+ * that still fits into 16 rows (empty graphs always fit).  A window thus
+ * holds 1 to 16 rows and never part of a graph together with rows of
+ * another, except that a long graph's last rows may share a window with
+ * whole small graphs.  The block layout, bitmaps (rows counted from the
+ * window's first row) and work list are those of f3s_plan over these
+ * windows.
+ *   seg_ptr  HOST int32[n_segs + 1]: seg_ptr[0] == 0, non-decreasing,
+ *            seg_ptr[n_segs] == N (else F3S_ERR_INVALID_VALUE); the caller
+ *            keeps ownership
+ *   n_segs   >= 0 graphs
+ * The segments only choose the windows: the operator's result is the same
+ * for any segmentation, also when edges cross segments.  Such a plan serves
+ * f3s_run, f3s_run_mh and f3s_forward; f3s_plan_transpose and the backward
+ * calls return F3S_ERR_UNSUPPORTED for it.  Otherwise as f3s_plan.
+ */
+f3s_plan_t f3s_plan_segments(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                             const int32_t *seg_ptr, int32_t n_segs);
 
 /*
  * O = softmax_rows(mask_A(scale * Q K^T)) V  (Algorithm 1, Section 3).
@@ -324,6 +352,13 @@ f3s_status_t f3s_plan_info(f3s_plan_t plan, f3s_plan_info_t *out);
  */
 f3s_status_t f3s_plan_export(f3s_plan_t plan, int32_t *blk_off, int32_t *cols,
                              uint32_t *mask, int32_t *items, int32_t *merges);
+
+/*
+ * The first row of every window of the plan followed by N (int32[n_windows
+ * + 1], HOST buffer): 16 w for the windows of f3s_plan, the windows chosen
+ * by f3s_plan_segments for its plans.  Synchronous.
+ */
+f3s_status_t f3s_plan_window_rows(f3s_plan_t plan, int32_t *win_row);
 
 /* Status of the last failing call on this thread (F3S_OK if none). */
 f3s_status_t f3s_last_error(void);

@@ -81,6 +81,10 @@ def load_library():
     L.f3s_plan_workspace_bytes.restype = ctypes.c_size_t
     L.f3s_plan_ws.argtypes = [vp, vp, i32, vp, ctypes.c_size_t]
     L.f3s_plan_ws.restype = vp
+    L.f3s_plan_segments.argtypes = [vp, vp, i32, vp, i32]
+    L.f3s_plan_segments.restype = vp
+    L.f3s_plan_window_rows.argtypes = [vp, vp]
+    L.f3s_plan_window_rows.restype = ctypes.c_int
     L.f3s_run.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp]
     L.f3s_run.restype = ctypes.c_int
     L.f3s_run_mh.argtypes = [vp, vp, vp, vp, vp, i32, i32, ctypes.c_float, vp]
@@ -170,6 +174,39 @@ class Plan:
         self.info = self._info()
         return self
 
+    @classmethod
+    def segments(cls, row_ptr, col_idx, N, seg_ptr):
+        """f3s_plan_segments: windows aligned to the graphs of a batch, graph g
+        holding rows seg_ptr[g] .. seg_ptr[g+1] - 1 (seg_ptr: host sequence of
+        ints, first 0, last N)."""
+        import numpy as np
+        L = load_library()
+        _check_device_tensor(row_ptr, "row_ptr", torch.int32)
+        _check_device_tensor(col_idx, "col_idx", torch.int32)
+        if row_ptr.numel() != int(N) + 1:
+            raise ValueError("row_ptr must hold N + 1 entries")
+        seg = np.ascontiguousarray(seg_ptr, dtype=np.int32)
+        if seg.ndim != 1 or seg.size < 1:
+            raise ValueError("seg_ptr must be a non-empty 1-D sequence")
+        ci = col_idx.data_ptr() if col_idx.numel() else None
+        with torch.cuda.device(row_ptr.device):
+            torch.cuda.current_stream().synchronize()
+            h = L.f3s_plan_segments(row_ptr.data_ptr(), ci, int(N),
+                                    seg.ctypes.data_as(ctypes.c_void_p), int(seg.size - 1))
+        if not h:
+            raise F3SError(L.f3s_last_error(), "f3s_plan_segments")
+        return Plan._from_handle(h, row_ptr.device, N)
+
+    def window_rows(self):
+        """First row of every window, then N (host numpy int32)."""
+        import numpy as np
+        wr = np.empty(self.info["n_windows"] + 1, dtype=np.int32)
+        rc = load_library().f3s_plan_window_rows(self.handle,
+                                                 wr.ctypes.data_as(ctypes.c_void_p))
+        if rc != F3S_OK:
+            raise F3SError(rc, "f3s_plan_window_rows")
+        return wr
+
     def transpose(self):
         """Plan of the transposed pattern (f3s_plan_transpose_ws, its scratch
         lent from torch's caching allocator)."""
@@ -239,7 +276,8 @@ class Plan:
             raise F3SError(rc, "f3s_plan_export")
         return dict(blk_off=blk_off, cols=cols[: 16 * B], mask=mask[: 8 * B],
                     items=items[: 4 * inf["n_items"]].reshape(-1, 4),
-                    merges=merges[: 3 * inf["n_split"]].reshape(-1, 3))
+                    merges=merges[: 3 * inf["n_split"]].reshape(-1, 3),
+                    win_row=self.window_rows())
 
     def close(self):
         if self._h is not None:

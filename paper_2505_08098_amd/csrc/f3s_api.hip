@@ -85,6 +85,7 @@ void free_plan_arrays(f3s_plan_s *p)
     p->mask = nullptr;
     p->items = nullptr;
     p->merges = nullptr;
+    p->win_row = nullptr;
     p->part_o = nullptr;
     p->part_ml = nullptr;
 }
@@ -119,8 +120,9 @@ hipError_t alloc_parts(f3s_plan_s *p, int32_t part_row)
 }
 
 // The plan's arrays in one allocation, laid out from its counts (T, blocks,
-// items, split windows): blk_off, cols, mask, items, merges.  Returns the
-// allocation's size in *bytes.
+// items, split windows): blk_off, cols, mask, items, merges, and the window
+// rows of a plan aligned to the graphs of a batch.  Returns the allocation's
+// size in *bytes.
 hipError_t alloc_store(f3s_plan_s *p, size_t *bytes)
 {
     using namespace f3s;
@@ -131,6 +133,7 @@ hipError_t alloc_store(f3s_plan_s *p, size_t *bytes)
     a.add<uint32_t>((int64_t)kMaskWords * B);
     a.add<WorkItem>(p->n_items);
     a.add<int32_t>(3ll * p->n_split);
+    if (p->flags & 4) a.add<int32_t>((int64_t)p->T + 1);
     hipError_t e = a.alloc();
     if (e != hipSuccess) return e;
     p->store = a.base;
@@ -140,6 +143,7 @@ hipError_t alloc_store(f3s_plan_s *p, size_t *bytes)
     p->mask = a.take<uint32_t>((int64_t)kMaskWords * B);
     p->items = a.take<WorkItem>(p->n_items);
     p->merges = a.take<int32_t>(3ll * p->n_split);
+    p->win_row = (p->flags & 4) ? a.take<int32_t>((int64_t)p->T + 1) : nullptr;
     if (bytes) *bytes = a.cap;
     return hipSuccess;
 }
@@ -200,6 +204,7 @@ struct BuildScratch {
     uint32_t *tmp_mask;  // block bitmaps per window, staged
     int32_t *u, *big, *is_big, *heavy, *is_heavy, *bits, *nb, *npieces, *key, *split_item;
     int32_t *big_pos, *heavy_pos, *split_pieces, *split_one, *scan_tmp;
+    int32_t *win_row;    // the windows' first rows (null: 16-row windows)
     f3s::WorkListScratch wl;  // the work-list sort
 };
 
@@ -211,19 +216,21 @@ U *carve(Arena &a, bool take, int64_t n)
     return nullptr;
 }
 
-// Lays out the build's scratch for T windows and nnz CSR entries: sizes into
-// a (take == false) or pointers out of it (take == true), in one order.
-// O(nnz + T) bytes.
+// Lays out the build's scratch for T windows and nnz CSR entries (and the
+// windows' first rows if `rows`): sizes into a (take == false) or pointers
+// out of it (take == true), in one order.  O(nnz + T) bytes.
 // Row windows of an N-row pattern (64-bit sum: N may be up to 2^31 - 1).
 int32_t num_windows(int32_t N)
 {
     return (int32_t)(((int64_t)N + f3s::kWindowRows - 1) / f3s::kWindowRows);
 }
 
-void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz)
+void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz,
+                   bool rows = false)
 {
     using namespace f3s;
     b.st = carve<BuildStats>(a, take, 1);
+    b.win_row = rows ? carve<int32_t>(a, take, (int64_t)T + 1) : nullptr;
     b.tmp_cols = carve<int32_t>(a, take, nnz);
     b.tmp_mask = carve<uint32_t>(a, take, mask_stage_words(nnz, T));
     int32_t **per_window[] = {&b.u, &b.big, &b.is_big, &b.heavy, &b.is_heavy,
@@ -250,8 +257,11 @@ size_t plan_workspace_bytes(int32_t N, int64_t nnz)
     return a.cap;
 }
 
+// win_rows: the windows' first rows and N (T + 1 ints, host memory), or null
+// for 16-row windows.
 f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *col_idx,
-                        int32_t part_row, void *workspace, size_t workspace_bytes)
+                        int32_t part_row, void *workspace, size_t workspace_bytes,
+                        const int32_t *win_rows)
 {
     using namespace f3s;
     const hipStream_t s = nullptr;
@@ -269,7 +279,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     const int32_t slots = plan_slots(p->device);
     BuildScratch b;
     ScratchArena tmp;
-    carve_scratch(tmp, false, b, T, nnz);
+    carve_scratch(tmp, false, b, T, nnz, win_rows != nullptr);
     if (workspace) {
         if (workspace_bytes < tmp.cap || ((uintptr_t)workspace & 255u))
             return F3S_ERR_INVALID_VALUE;
@@ -278,7 +288,11 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     } else {
         HIP_TRY(tmp.alloc());
     }
-    carve_scratch(tmp, true, b, T, nnz);
+    carve_scratch(tmp, true, b, T, nnz, win_rows != nullptr);
+    const int32_t *wr = b.win_row;
+    if (wr)
+        HIP_TRY(hipMemcpy(b.win_row, win_rows, sizeof(int32_t) * ((size_t)T + 1),
+                          hipMemcpyHostToDevice));
     BuildStats *st = b.st;
     int32_t *tmp_cols = b.tmp_cols;
     uint32_t *tmp_mask = b.tmp_mask;
@@ -292,7 +306,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
 
     // ---- 2. CSR check, distinct columns and bitmaps per window ----------
     HIP_TRY(launch_check_row_ptr(row_ptr, N, nnz, &st->err, s));
-    HIP_TRY(launch_window_wave(row_ptr, col_idx, N, T, tmp_cols, tmp_mask, u, is_big,
+    HIP_TRY(launch_window_wave(row_ptr, col_idx, N, wr, T, tmp_cols, tmp_mask, u, is_big,
                                is_heavy, bits, &st->err, s));
     {  // the flagged windows listed in window order
         ScanArray fb, fh;
@@ -308,10 +322,10 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     }
     HIP_TRY(hipMemcpy(&hs, st, sizeof hs, hipMemcpyDeviceToHost));
     if (hs.err) return F3S_ERR_INVALID_CSR;
-    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, big, hs.n_big, tmp_cols, tmp_mask, u,
-                               bits, &st->err, s));
-    HIP_TRY(launch_heavy_lds(row_ptr, col_idx, N, heavy, hs.n_heavy, tmp_cols, tmp_mask, u,
-                             bits, &st->err, s));
+    HIP_TRY(launch_window_sort(row_ptr, col_idx, N, wr, big, hs.n_big, tmp_cols, tmp_mask,
+                               u, bits, &st->err, s));
+    HIP_TRY(launch_heavy_lds(row_ptr, col_idx, N, wr, heavy, hs.n_heavy, tmp_cols,
+                             tmp_mask, u, bits, &st->err, s));
 
     // ---- 3. blocks per window and statistics; work-list shape: piece size,
     //         split windows, item count (one host round trip for all) -------
@@ -322,7 +336,7 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     const char *order_env = getenv("F3S_NO_REORDER");
     const bool order_forced = order_env && *order_env;
     const bool reorder = !order_forced || atoi(order_env) == 0;
-    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0);
+    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0) | (wr ? 4 : 0);
     HIP_TRY(launch_bin_keys(nb, T, &st->n_blocks, &st->max_blocks,
                             env_int("F3S_PIECE_BLOCKS", 0), slots, reorder,
                             &st->piece, npieces, key, split_pieces, split_one, s));
@@ -363,9 +377,12 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(alloc_store(p, nullptr));
     HIP_TRY(alloc_parts(p, part_row));
     HIP_TRY(launch_scan(nb, p->blk_off, T, scan_tmp, nullptr, s));  // window block offsets
+    if (wr)
+        HIP_TRY(hipMemcpyAsync(p->win_row, wr, sizeof(int32_t) * ((size_t)T + 1),
+                               hipMemcpyDeviceToDevice, s));
 
     // ---- 5. column lists and bitmaps into their blocks --------------------
-    HIP_TRY(launch_fill_windows(row_ptr, T, tmp_cols, tmp_mask, u, p->blk_off, p->cols,
+    HIP_TRY(launch_fill_windows(row_ptr, wr, T, tmp_cols, tmp_mask, u, p->blk_off, p->cols,
                                 p->mask, s));
 
     // ---- 6. heavy-first work list: stable sort of the windows by key ------
@@ -427,9 +444,12 @@ f3s_plan_t clone_plan(const f3s_plan_s *src, int32_t part_row)
     return t;
 }
 
-// Builds a plan whose split-window partials hold part_row floats per row.
+// Builds a plan whose split-window partials hold part_row floats per row;
+// win_rows (host, T + 1 ints) gives the windows' first rows, null the 16-row
+// windows.
 f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                     int32_t part_row, void *workspace, size_t workspace_bytes)
+                     int32_t part_row, void *workspace, size_t workspace_bytes,
+                     const int32_t *win_rows = nullptr, int32_t T = 0)
 {
     const auto t0 = std::chrono::steady_clock::now();
     if (N < 0 || (N > 0 && !row_ptr)) {
@@ -442,7 +462,7 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
         return nullptr;
     }
     p->N = N;
-    p->T = num_windows(N);
+    p->T = win_rows ? T : num_windows(N);
     p->id = g_next_plan_id.fetch_add(1);
     f3s_status_t st = from_hip(hipGetDevice(&p->device));
     if (st == F3S_OK) {
@@ -452,7 +472,8 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
             p->piece = 16;
             p->part_row = part_row;
         } else {
-            st = build_plan(p, row_ptr, col_idx, part_row, workspace, workspace_bytes);
+            st = build_plan(p, row_ptr, col_idx, part_row, workspace, workspace_bytes,
+                            win_rows);
         }
     }
     if (st != F3S_OK) {
@@ -466,6 +487,33 @@ f3s_plan_t make_plan(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
     p->build_ms = std::chrono::duration<double, std::milli>(
                       std::chrono::steady_clock::now() - t0).count();
     return p;
+}
+
+// Windows aligned to the segments (the graphs of a batch; segment g holds
+// rows seg[g] .. seg[g+1] - 1): walking from row 0, a window is the next 16
+// rows of the current segment while more than 16 of them remain, otherwise
+// the rest of the segment together with every whole segment after it that
+// still fits into 16 rows.  So no window mixes part of a graph with rows of
+// another, except that a long graph's last rows may share a window with
+// whole small graphs.  Returns the windows' first rows followed by N.
+std::vector<int32_t> segment_windows(const int32_t *seg, int32_t n_segs)
+{
+    std::vector<int32_t> starts;
+    const int32_t N = seg[n_segs];
+    int32_t g = 0;
+    for (int32_t r = 0; r < N;) {
+        while (seg[g + 1] <= r) ++g;  // the segment holding row r
+        starts.push_back(r);
+        if (seg[g + 1] - r > f3s::kWindowRows) {
+            r += f3s::kWindowRows;
+            continue;
+        }
+        const int32_t first = r;
+        r = seg[++g];
+        while (g < n_segs && seg[g + 1] - first <= f3s::kWindowRows) r = seg[++g];
+    }
+    starts.push_back(N);
+    return starts;
 }
 
 // Patterns with at least this many entries check symmetry on the sorted CSR
@@ -512,6 +560,10 @@ f3s_plan_t make_transpose(f3s_plan_t src, void *workspace, size_t workspace_byte
     const auto t0 = std::chrono::steady_clock::now();
     if (!src) {
         fail(F3S_ERR_INVALID_VALUE);
+        return nullptr;
+    }
+    if (src->win_row) {  // windows aligned to graphs: forward only
+        fail(F3S_ERR_UNSUPPORTED);
         return nullptr;
     }
     f3s_status_t st = F3S_OK;
@@ -624,6 +676,43 @@ f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N
         return nullptr;
     }
     return make_plan(row_ptr, col_idx, N, f3s::kMaxD, workspace, workspace_bytes);
+}
+
+f3s_plan_t f3s_plan_segments(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
+                             const int32_t *seg_ptr, int32_t n_segs)
+{
+    if (N < 0 || !seg_ptr || n_segs < 0 || seg_ptr[0] != 0 || seg_ptr[n_segs] != N) {
+        fail(F3S_ERR_INVALID_VALUE);
+        return nullptr;
+    }
+    for (int32_t g = 0; g < n_segs; ++g) {
+        if (seg_ptr[g + 1] < seg_ptr[g]) {
+            fail(F3S_ERR_INVALID_VALUE);
+            return nullptr;
+        }
+    }
+    std::vector<int32_t> starts;
+    try {
+        starts = segment_windows(seg_ptr, n_segs);
+    } catch (const std::bad_alloc &) {
+        fail(F3S_ERR_OUT_OF_MEMORY);
+        return nullptr;
+    }
+    return make_plan(row_ptr, col_idx, N, f3s::kMaxD, nullptr, 0, starts.data(),
+                     (int32_t)starts.size() - 1);
+}
+
+f3s_status_t f3s_plan_window_rows(f3s_plan_t p, int32_t *win_row)
+{
+    if (!p || !win_row) return fail(F3S_ERR_INVALID_VALUE);
+    if (p->win_row) {
+        const f3s_status_t st = from_hip(hipMemcpy(
+            win_row, p->win_row, sizeof(int32_t) * ((size_t)p->T + 1), hipMemcpyDeviceToHost));
+        return st == F3S_OK ? F3S_OK : fail(st);
+    }
+    for (int32_t w = 0; w < p->T; ++w) win_row[w] = w * f3s::kWindowRows;
+    win_row[p->T] = p->N;
+    return F3S_OK;
 }
 
 f3s_plan_t f3s_plan_transpose(f3s_plan_t src)
@@ -777,6 +866,7 @@ f3s_status_t f3s_backward_typed(f3s_plan_t p, f3s_plan_t pt, const void *Q, cons
         return fail(F3S_ERR_UNSUPPORTED);
     if (!p || !pt || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (pt->transpose_of != p->id || pt->N != p->N) return fail(F3S_ERR_INVALID_VALUE);
+    if (p->win_row) return fail(F3S_ERR_UNSUPPORTED);  // windows aligned to graphs
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;

@@ -44,7 +44,8 @@ struct f3s_plan_s {
     int32_t n_items = 0;
     int32_t n_split = 0;
     int32_t n_pieces = 0;
-    int32_t flags = 0;           // bit 0: work list in window order; bit 1: narrow gathers
+    int32_t flags = 0;           // bit 0: work list in window order; bit 1: narrow gathers;
+                                 // bit 2: windows aligned to the graphs of a batch
     uint64_t id = 0;             // process-unique plan id
     uint64_t transpose_of = 0;   // id of the plan this one transposes (0: none)
     void *store = nullptr;       // one allocation: blk_off, cols, mask, items, merges
@@ -55,6 +56,9 @@ struct f3s_plan_s {
     uint32_t *mask = nullptr;    // [8 * n_blocks]
     f3s::WorkItem *items = nullptr;  // [n_items]
     int32_t *merges = nullptr;   // [3 * n_split]
+    int32_t *win_row = nullptr;  // [T + 1] first row of each window, then N (plans whose
+                                 // windows follow the graphs of a batch; null: window w
+                                 // is rows 16 w .. 16 w + 15)
     // Partial results of split windows for one launch group of nh heads
     // (nh * d <= kMaxD): slot (piece, head) = piece * nh + head.
     float *part_o = nullptr;     // [n_pieces * 16 * part_row]
@@ -125,6 +129,19 @@ inline int waves_per_item(int64_t n_blocks, int64_t n_items, int32_t heads, int6
     if (2 * waves <= resident && n_blocks >= 8 * n_items) return 2;
     return 1;
 }
+// First row and row count of window w: rows 16 w .. 16 w + 15 (the last
+// window clipped at N), or those given by win_row (device code).
+__device__ __forceinline__ void window_rows(const int32_t *win_row, int32_t N, int32_t w,
+                                           int32_t *r0, int32_t *nr)
+{
+    if (win_row) {
+        *r0 = win_row[w];
+        *nr = win_row[w + 1] - *r0;
+    } else {
+        *r0 = w * kWindowRows;
+        *nr = min(kWindowRows, N - *r0);
+    }
+}
 // Inclusive sum over the lanes of a wavefront (device code).
 __device__ __forceinline__ int wave_inclusive_sum(int x, int lane)
 {
@@ -144,23 +161,24 @@ int64_t mask_stage_words(int64_t nnz, int32_t T);
 // columns into tmp_cols at the window's CSR offset, their count into u, the
 // block bitmaps into the staging area, their set bits into bits.  Larger
 // windows get is_big = 1 (up to 4096 entries) or is_heavy = 1.
+// win_row: the windows' first rows (null: 16-row windows); also below.
 hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                              int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
-                              int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits,
-                              int32_t *err, hipStream_t s);
+                              const int32_t *win_row, int32_t T, int32_t *tmp_cols,
+                              uint32_t *tmp_mask, int32_t *u, int32_t *is_big,
+                              int32_t *is_heavy, int32_t *bits, int32_t *err, hipStream_t s);
 // The windows big[0 .. n_big): sorted distinct columns, u, bitmaps and bits
 // as above (one wavefront with 16 keys per lane up to 1024 entries, else an
 // LDS sort).
 hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
-                              int32_t N, const int32_t *big, int32_t n_big,
-                              int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
-                              int32_t *bits, int32_t *err, hipStream_t s);
+                              int32_t N, const int32_t *win_row, const int32_t *big,
+                              int32_t n_big, int32_t *tmp_cols, uint32_t *tmp_mask,
+                              int32_t *u, int32_t *bits, int32_t *err, hipStream_t s);
 // Heavy windows (more than 4096 entries): columns, u, bitmaps and bits as
 // above, one workgroup per window (column bitmap in LDS, walked in chunks).
 hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                            const int32_t *heavy, int32_t n_heavy, int32_t *tmp_cols,
-                            uint32_t *tmp_mask, int32_t *u, int32_t *bits, int32_t *err,
-                            hipStream_t s);
+                            const int32_t *win_row, const int32_t *heavy, int32_t n_heavy,
+                            int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+                            int32_t *bits, int32_t *err, hipStream_t s);
 // nb[w] = ceil(u[w] / 16) and the sums of u, bits and nb and the largest nb
 // (added / max-ed into the four outputs, zeroed by the caller).
 hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
@@ -187,10 +205,10 @@ hipError_t launch_scan(const int32_t *in, int32_t *out, int32_t n, int32_t *tmp,
 // Two independent scans of n ints each (one launch when n is small).
 hipError_t launch_scan2(ScanArray a0, ScanArray a1, int32_t n, int32_t *tmp, hipStream_t s);
 // Padded column lists and block bitmaps of the plan from the staging areas.
-hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,
-                               const uint32_t *tmp_mask, const int32_t *u,
-                               const int32_t *blk_off, int32_t *cols, uint32_t *mask,
-                               hipStream_t s);
+hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *win_row, int32_t T,
+                               const int32_t *tmp_cols, const uint32_t *tmp_mask,
+                               const int32_t *u, const int32_t *blk_off, int32_t *cols,
+                               uint32_t *mask, hipStream_t s);
 // Work list: the piece size (from the block count and largest window on the
 // device, see plan_piece; forced >= 2 overrides it; slots = 8 per CU) into
 // *piece_out, then per window piece count, bucket key, split flags.

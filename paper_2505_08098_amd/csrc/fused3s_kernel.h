@@ -179,8 +179,8 @@ template <int D, bool kWide, int kIn, bool kOutH, bool kNarrow = false, int NW =
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void k_fused3s(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
-    const uint32_t *__restrict__ mask, const void *__restrict__ Qv,
-    const void *__restrict__ Kv, const void *__restrict__ Vv,
+    const uint32_t *__restrict__ mask, const int32_t *__restrict__ win_row,
+    const void *__restrict__ Qv, const void *__restrict__ Kv, const void *__restrict__ Vv,
     void *__restrict__ O, float *__restrict__ part_o,
     float *__restrict__ part_ml, float *__restrict__ lse, int32_t N, int32_t ld,
     int32_t h0, int32_t nh, float sl2, uint32_t order, uint32_t *__restrict__ trace)
@@ -226,7 +226,12 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     const char *K = static_cast<const char *>(Kv) + (int64_t)head * D * EB;
     const char *V = static_cast<const char *>(Vv) + (int64_t)head * D * EB;
     const int64_t ohead = (int64_t)head * D;
-    const int row = it.window * kWindowRows + i;
+    // the window's rows: 16 from 16 w (the last window clipped at N), or
+    // those of a plan aligned to the graphs of a batch
+    int32_t r0, nr;
+    window_rows(win_row, N, it.window, &r0, &nr);
+    const int row = r0 + i;
+    const bool live = i < nr;
     // this wave's blocks: whole pairs [pa, pb) of the item's pairs
     int b0 = it.blk_begin, b1 = it.blk_end;
     if constexpr (NW > 1) {
@@ -237,11 +242,11 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     }
 
     // Q_i: lane (i, g) holds Q[row][32c + 8g .. +7] for each chunk c.  Pad
-    // rows (>= N) of the last window read row N-1: their results are never
-    // written and rows do not interact, so any finite values do.
+    // rows (past the window's last row) read its first row: their results
+    // are never written and rows do not interact, so any finite values do.
     h8 q[NC];
     {
-        const char *qp = Q + ((int64_t)min(row, N - 1) * ld + 8 * g) * EB;
+        const char *qp = Q + ((int64_t)(live ? row : r0) * ld + 8 * g) * EB;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             if constexpr (EB == 1)
@@ -507,7 +512,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
         l_tot = l;
     }
     if (it.slot < 0) {
-        if (row < N) {
+        if (live) {
             const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
             const int64_t ob = (int64_t)row * ld + ohead + 4 * g;
 #pragma unroll
@@ -557,6 +562,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
 // float4 columns 4q + 64c (c < CPT) that lie inside the row.
 template <int D, bool kOutH>
 __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merges,
+                                               const int32_t *__restrict__ win_row,
                                                const float *__restrict__ part_o,
                                                const float *__restrict__ part_ml,
                                                void *__restrict__ O,
@@ -568,8 +574,10 @@ __global__ __launch_bounds__(256) void k_merge(const int32_t *__restrict__ merge
     const int s = blockIdx.x / nh, hl = blockIdx.x - (blockIdx.x / nh) * nh;
     const int w = merges[3 * s], first = merges[3 * s + 1], np = merges[3 * s + 2];
     const int r = threadIdx.x >> 4, q = threadIdx.x & 15;
-    const int row = w * kWindowRows + r;
-    if (row >= N) return;
+    int32_t r0, nr;
+    window_rows(win_row, N, w, &r0, &nr);
+    if (r >= nr) return;
+    const int row = r0 + r;
     // partial slot of (piece k, head) = (first + k) * nh + hl
     const float *ml = part_ml + ((int64_t)first * nh + hl) * 32;
     const int64_t mstride = (int64_t)nh * 32;
@@ -662,15 +670,16 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
                 nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
             const uint32_t order =
                 (head_major ? kOrderHead : 0u) | (xcd_chunks(p, H) ? kOrderXcd : 0u);
-            kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, Q, K, V, O,
-                                               p.part_o, p.part_ml, lse, p.N, ld, h0, nh,
-                                               sl2, order, trace);
+            kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, p.win_row, Q, K,
+                                               V, O, p.part_o, p.part_ml, lse, p.N, ld, h0,
+                                               nh, sl2, order, trace);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
         if (p.n_split > 0) {
-            k_merge<D, kOutH><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.part_o, p.part_ml, O,
-                                                            lse, p.N, ld, h0, nh);
+            k_merge<D, kOutH><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.win_row, p.part_o,
+                                                            p.part_ml, O, lse, p.N, ld, h0,
+                                                            nh);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
         }

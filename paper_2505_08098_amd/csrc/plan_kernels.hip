@@ -225,11 +225,11 @@ __device__ void window_wave(const int32_t *col_idx, int32_t N, int32_t w, int32_
 
 // Loads a window's row starts into lanes 0..nr of the wave (INT_MAX above).
 __device__ __forceinline__ int32_t window_row_starts(const int32_t *row_ptr, int32_t N,
-                                                     int32_t w, int lane, int32_t *beg,
-                                                     int32_t *n)
+                                                     const int32_t *win_row, int32_t w,
+                                                     int lane, int32_t *beg, int32_t *n)
 {
-    const int r0 = w * kWindowRows;
-    const int nr = min(kWindowRows, N - r0);
+    int32_t r0, nr;
+    window_rows(win_row, N, w, &r0, &nr);
     const int32_t rp = lane <= nr ? row_ptr[r0 + lane] : INT_MAX;
     *beg = __shfl(rp, 0);
     *n = __shfl(rp, nr) - *beg;
@@ -241,9 +241,9 @@ __device__ __forceinline__ int32_t window_row_starts(const int32_t *row_ptr, int
 // later passes.  (No counter shared by all windows: atomics on one address
 // serialise, tens of ns each.)
 __global__ __launch_bounds__(64) void k_window_wave(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, int32_t *tmp_cols,
-    uint32_t *tmp_mask, int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits_out,
-    int32_t *err)
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *win_row,
+    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *is_big, int32_t *is_heavy,
+    int32_t *bits_out, int32_t *err)
 {
     __shared__ int32_t s_cols[kWaveCap];
     __shared__ uint32_t s_mask[kWaveCap / kBlockCols * kMaskWords];
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(64) void k_window_wave(
         return;
     }
     int32_t beg, n;
-    const int32_t rp = window_row_starts(row_ptr, N, w, lane, &beg, &n);
+    const int32_t rp = window_row_starts(row_ptr, N, win_row, w, lane, &beg, &n);
     if (lane == 0) {
         is_big[w] = n > kWaveCap && n <= kSortCap;
         is_heavy[w] = n > kSortCap;
@@ -280,15 +280,16 @@ __global__ __launch_bounds__(64) void k_window_wave(
 // The windows of `big` with kWaveCap < n <= kWaveCap16 entries, one wavefront
 // each with 16 keys per lane; the others are left to k_window_sort.
 __global__ __launch_bounds__(64) void k_window_wave16(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *big,
-    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *win_row,
+    const int32_t *big, int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+    int32_t *bits_out, int32_t *err)
 {
     __shared__ int32_t s_cols[kWaveCap16];
     __shared__ uint32_t s_mask[kWaveCap16 / kBlockCols * kMaskWords];
     const int lane = threadIdx.x;
     const int w = big[blockIdx.x];
     int32_t beg, n;
-    const int32_t rp = window_row_starts(row_ptr, N, w, lane, &beg, &n);
+    const int32_t rp = window_row_starts(row_ptr, N, win_row, w, lane, &beg, &n);
     if (n <= kWaveCap || n > kWaveCap16) return;
     window_wave<16>(col_idx, N, w, beg, n, rp, lane, s_cols, s_mask, tmp_cols, tmp_mask,
                     u, bits_out, err);
@@ -337,8 +338,9 @@ __device__ int block_excl_scan_sort(int v, int *lds, int *total)
 }
 
 __global__ __launch_bounds__(kSortThreads) void k_window_sort(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *big,
-    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err)
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *win_row,
+    const int32_t *big, int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+    int32_t *bits_out, int32_t *err)
 {
     static_assert(kSortPer == 4, "the register network assumes 4 keys per thread");
     __shared__ int32_t xbuf[2][kSortCap];  // cross-wave exchanges, then the distinct list
@@ -348,8 +350,8 @@ __global__ __launch_bounds__(kSortThreads) void k_window_sort(
     __shared__ int32_t s_rp[kWindowRows + 1];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int w = big[blockIdx.x];
-    const int r0 = w * kWindowRows;
-    const int nr = min(r0 + kWindowRows, N) - r0;
+    int32_t r0, nr;
+    window_rows(win_row, N, w, &r0, &nr);
     const int beg = row_ptr[r0];
     const int n = row_ptr[r0 + nr] - beg;
     if (n <= kWaveCap16 || n > kSortCap) return;  // k_window_wave16 / heavy paths
@@ -483,9 +485,9 @@ constexpr int kChunkCols = 1 << 17;       // 16 KB bitmap + 16 KB ranks
 constexpr int kHeavyLdsBytes = 76 * 1024;
 
 __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
-    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *heavy,
-    int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u, int32_t *bits_out, int32_t *err,
-    int32_t mask_words)
+    const int32_t *row_ptr, const int32_t *col_idx, int32_t N, const int32_t *win_row,
+    const int32_t *heavy, int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+    int32_t *bits_out, int32_t *err, int32_t mask_words)
 {
     uint32_t *lds = f3s_heavy_lds_dyn;  // [cw] bitmap, [cw] ranks, [mask_words]
     __shared__ int32_t s_rp[kWindowRows + 1];
@@ -496,8 +498,8 @@ __global__ __launch_bounds__(kHeavyThreads) void k_heavy_lds(
     int32_t *rank = (int32_t *)(lds + cw);
     uint32_t *sm = lds + 2 * cw;
     const int w = heavy[blockIdx.x];
-    const int r0 = w * kWindowRows;
-    const int nr = min(r0 + kWindowRows, N) - r0;
+    int32_t r0, nr;
+    window_rows(win_row, N, w, &r0, &nr);
     if (tid <= nr) s_rp[tid] = row_ptr[r0 + tid];
     __syncthreads();
     const int beg = s_rp[0], n = s_rp[nr] - beg;
@@ -774,11 +776,12 @@ __global__ __launch_bounds__(kScanThreads) void k_scan(ScanArray a0, ScanArray a
 // block bitmaps copied from the staging areas to the window's blocks; one
 // workgroup per window (a hub window has thousands of blocks).
 __global__ __launch_bounds__(256) void k_fill_windows(
-    const int32_t *row_ptr, const int32_t *tmp_cols, const uint32_t *tmp_mask,
-    const int32_t *u, const int32_t *blk_off, int32_t *cols, uint32_t *mask)
+    const int32_t *row_ptr, const int32_t *win_row, const int32_t *tmp_cols,
+    const uint32_t *tmp_mask, const int32_t *u, const int32_t *blk_off, int32_t *cols,
+    uint32_t *mask)
 {
     const int w = blockIdx.x;
-    const int32_t beg = row_ptr[w * kWindowRows];
+    const int32_t beg = row_ptr[win_row ? win_row[w] : w * kWindowRows];
     const int uw = u[w];
     const int64_t ob = blk_off[w];
     const int nbw = blk_off[w + 1] - blk_off[w];
@@ -900,40 +903,41 @@ hipError_t launch_check_row_ptr(const int32_t *row_ptr, int32_t N, int32_t nnz,
 int64_t mask_stage_words(int64_t nnz, int32_t T) { return (nnz >> 1) + 8ll * T + 8; }
 
 hipError_t launch_window_wave(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                              int32_t T, int32_t *tmp_cols, uint32_t *tmp_mask,
-                              int32_t *u, int32_t *is_big, int32_t *is_heavy, int32_t *bits,
-                              int32_t *err, hipStream_t s)
+                              const int32_t *win_row, int32_t T, int32_t *tmp_cols,
+                              uint32_t *tmp_mask, int32_t *u, int32_t *is_big,
+                              int32_t *is_heavy, int32_t *bits, int32_t *err, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_window_wave<<<T, 64, 0, s>>>(row_ptr, col_idx, N, tmp_cols, tmp_mask, u, is_big,
-                                   is_heavy, bits, err);
+    k_window_wave<<<T, 64, 0, s>>>(row_ptr, col_idx, N, win_row, tmp_cols, tmp_mask, u,
+                                   is_big, is_heavy, bits, err);
     return hipGetLastError();
 }
 
 hipError_t launch_window_sort(const int32_t *row_ptr, const int32_t *col_idx,
-                              int32_t N, const int32_t *big, int32_t n_big,
-                              int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
-                              int32_t *bits, int32_t *err, hipStream_t s)
+                              int32_t N, const int32_t *win_row, const int32_t *big,
+                              int32_t n_big, int32_t *tmp_cols, uint32_t *tmp_mask,
+                              int32_t *u, int32_t *bits, int32_t *err, hipStream_t s)
 {
     if (n_big == 0) return hipSuccess;
-    k_window_wave16<<<n_big, 64, 0, s>>>(row_ptr, col_idx, N, big, tmp_cols, tmp_mask, u,
-                                         bits, err);
-    k_window_sort<<<n_big, kSortThreads, 0, s>>>(row_ptr, col_idx, N, big, tmp_cols,
-                                                 tmp_mask, u, bits, err);
+    k_window_wave16<<<n_big, 64, 0, s>>>(row_ptr, col_idx, N, win_row, big, tmp_cols,
+                                         tmp_mask, u, bits, err);
+    k_window_sort<<<n_big, kSortThreads, 0, s>>>(row_ptr, col_idx, N, win_row, big,
+                                                 tmp_cols, tmp_mask, u, bits, err);
     return hipGetLastError();
 }
 
 hipError_t launch_heavy_lds(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
-                            const int32_t *heavy, int32_t n_heavy, int32_t *tmp_cols,
-                            uint32_t *tmp_mask, int32_t *u, int32_t *bits, int32_t *err,
-                            hipStream_t s)
+                            const int32_t *win_row, const int32_t *heavy, int32_t n_heavy,
+                            int32_t *tmp_cols, uint32_t *tmp_mask, int32_t *u,
+                            int32_t *bits, int32_t *err, hipStream_t s)
 {
     if (n_heavy == 0) return hipSuccess;
     const int cw = (min(N, kChunkCols) + 31) / 32;
     const int mask_words = (kHeavyLdsBytes / 4 - 2 * cw) & ~(kMaskWords - 1);
     const size_t lds = (size_t)(2 * cw + mask_words) * 4;
-    k_heavy_lds<<<n_heavy, kHeavyThreads, lds, s>>>(row_ptr, col_idx, N, heavy, tmp_cols,
-                                                     tmp_mask, u, bits, err, mask_words);
+    k_heavy_lds<<<n_heavy, kHeavyThreads, lds, s>>>(row_ptr, col_idx, N, win_row, heavy,
+                                                     tmp_cols, tmp_mask, u, bits, err,
+                                                     mask_words);
     return hipGetLastError();
 }
 
@@ -1013,13 +1017,14 @@ hipError_t launch_scan2(ScanArray a0, ScanArray a1, int32_t n, int32_t *tmp, hip
     return e != hipSuccess ? e : launch_scan(a1, n, tmp, s);
 }
 
-hipError_t launch_fill_windows(const int32_t *row_ptr, int32_t T, const int32_t *tmp_cols,
-                               const uint32_t *tmp_mask, const int32_t *u,
-                               const int32_t *blk_off, int32_t *cols, uint32_t *mask,
-                               hipStream_t s)
+hipError_t launch_fill_windows(const int32_t *row_ptr, const int32_t *win_row, int32_t T,
+                               const int32_t *tmp_cols, const uint32_t *tmp_mask,
+                               const int32_t *u, const int32_t *blk_off, int32_t *cols,
+                               uint32_t *mask, hipStream_t s)
 {
     if (T == 0) return hipSuccess;
-    k_fill_windows<<<T, 256, 0, s>>>(row_ptr, tmp_cols, tmp_mask, u, blk_off, cols, mask);
+    k_fill_windows<<<T, 256, 0, s>>>(row_ptr, win_row, tmp_cols, tmp_mask, u, blk_off, cols,
+                                     mask);
     return hipGetLastError();
 }
 

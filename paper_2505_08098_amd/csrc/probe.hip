@@ -78,20 +78,22 @@ __global__ __launch_bounds__(kThreads) void k_probe_write(u4 *__restrict__ dst, 
 template <int D, bool kWide>
 __global__ __launch_bounds__(256) void k_probe_gather(
     const f3s::WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
-    const uint32_t *__restrict__ mask, const char *__restrict__ Q,
-    const char *__restrict__ K, const char *__restrict__ V, float *__restrict__ O,
-    float *__restrict__ part_o, int32_t N, uint32_t order)
+    const uint32_t *__restrict__ mask, const int32_t *__restrict__ win_row,
+    const char *__restrict__ Q, const char *__restrict__ K, const char *__restrict__ V,
+    float *__restrict__ O, float *__restrict__ part_o, int32_t N, uint32_t order)
 {
     constexpr int LPR = D / 8;   // 16-byte chunks per row
     constexpr int NI = D / 16;   // chunks per lane per 32-row tile
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const f3s::WorkItem it = items[f3s::workgroup_position(order)];
+    int32_t r0, nr;
+    f3s::window_rows(win_row, N, it.window, &r0, &nr);
     uint32_t acc = 0;
-    // Q: rows 4 wv .. 4 wv + 3 of the window (pad rows read row N - 1)
+    // Q: rows 4 wv .. 4 wv + 3 of the window (pad rows read its first row)
     for (int f = lane; f < 4 * LPR; f += 64) {
-        const int r = it.window * 16 + 4 * wv + f / LPR;
-        acc ^= fold(*reinterpret_cast<const u4 *>(Q + ((int64_t)min(r, N - 1) * D) * 2 +
-                                                  16 * (f % LPR)));
+        const int r = 4 * wv + f / LPR;
+        const int64_t qrow = r0 + (r < nr ? r : 0);
+        acc ^= fold(*reinterpret_cast<const u4 *>(Q + qrow * D * 2 + 16 * (f % LPR)));
     }
     const int b0 = it.blk_begin, b1 = it.blk_end;
     for (int b = b0 + 2 * wv; b < b1; b += 16) {
@@ -139,8 +141,7 @@ __global__ __launch_bounds__(256) void k_probe_gather(
         const int rr = 4 * wv + f / (D / 4), cc = 4 * (f % (D / 4));
         const float4 v4 = make_float4(val, val, val, val);
         if (it.slot < 0) {
-            const int r = it.window * 16 + rr;
-            if (r < N) *reinterpret_cast<float4 *>(O + (int64_t)r * D + cc) = v4;
+            if (rr < nr) *reinterpret_cast<float4 *>(O + (int64_t)(r0 + rr) * D + cc) = v4;
         } else {
             *reinterpret_cast<float4 *>(part_o + ((int64_t)it.slot * 16 + rr) * D + cc) = v4;
         }
@@ -153,7 +154,8 @@ hipError_t launch_gather_d(const f3s_plan_s &p, const void *Q, const void *K, co
 {
     const bool wide = (uint64_t)p.N * D * 2 > 0xFFFFFFF0ull;
     auto kern = wide ? k_probe_gather<D, true> : k_probe_gather<D, false>;
-    kern<<<p.n_items, 256, 0, s>>>(p.items, p.cols, p.mask, static_cast<const char *>(Q),
+    kern<<<p.n_items, 256, 0, s>>>(p.items, p.cols, p.mask, p.win_row,
+                                   static_cast<const char *>(Q),
                                    static_cast<const char *>(K),
                                    static_cast<const char *>(V), O, p.part_o, p.N,
                                    f3s::xcd_chunks(p, 1) ? f3s::kOrderXcd : 0u);

@@ -70,6 +70,28 @@ int main(void)
                                NULL, NULL, NULL, 1, 64, 1.0f, NULL) == F3S_ERR_INVALID_VALUE);
     CHECK(f3s_backward_noalloc_max_records() == (int64_t)1 << 21);
     CHECK(f3s_plan_transpose(NULL) == NULL && f3s_last_error() == F3S_ERR_INVALID_VALUE);
+    CHECK(f3s_plan_window_rows(NULL, NULL) == F3S_ERR_INVALID_VALUE);
+    /* batch segmentations: malformed ones are rejected; the windows of valid
+       ones are computed (on the host) before the null CSR is rejected */
+    {
+        const int32_t bad[][4] = {{1, 2, 3, 4}, {0, 3, 2, 4}, {0, 1, 2, 3}};
+        for (int k = 0; k < 3; ++k)
+            CHECK(f3s_plan_segments(NULL, NULL, 4, bad[k], 3) == NULL &&
+                  f3s_last_error() == F3S_ERR_INVALID_VALUE);
+        CHECK(f3s_plan_segments(NULL, NULL, 4, NULL, 3) == NULL &&
+              f3s_last_error() == F3S_ERR_INVALID_VALUE);
+        CHECK(f3s_plan_segments(NULL, NULL, 4, bad[0], -1) == NULL &&
+              f3s_last_error() == F3S_ERR_INVALID_VALUE);
+        int32_t seg[40];
+        seg[0] = 0;
+        for (int g = 0; g < 39; ++g) seg[g + 1] = seg[g] + (g * 7) % 41;  /* 0 .. 40 rows */
+        const int32_t n = seg[39];
+        CHECK(f3s_plan_segments(NULL, NULL, n, seg, 39) == NULL &&
+              f3s_last_error() == F3S_ERR_INVALID_VALUE);
+        const int32_t one[2] = {0, 1 << 24};
+        CHECK(f3s_plan_segments(NULL, NULL, 1 << 24, one, 1) == NULL &&
+              f3s_last_error() == F3S_ERR_INVALID_VALUE);
+    }
     CHECK(f3s_plan_transpose_workspace_bytes(NULL) == 0);
     CHECK(f3s_plan_transpose_ws(NULL, NULL, 0) == NULL);
     CHECK(f3s_probe_read(NULL, 16, NULL, NULL) == F3S_ERR_INVALID_VALUE);
