@@ -143,14 +143,24 @@ def plan_stats(plan):
     }
 
 
-def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, reps=20):
+# Table sizes (MB) of the random-row gather sweep: inside one XCD's 4 MB L2,
+# above it, inside the 256 MB Infinity Cache, and far above it.
+GATHER_SWEEP_MB = (2, 4, 8, 16, 32, 64, 128, 256, 1024, 4096)
+
+
+def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, reps=20,
+                    kv_rows=0, row_bytes=0):
     """Bandwidth ceilings measured in this process with the library's probe
     kernels: a streaming read, copy and write over 4 GiB (16x the 256 MB
-    Infinity Cache, so DRAM serves them), and the fused kernel's own access
-    pattern on this plan without its arithmetic (f3s_probe_gather; its
-    rate counts the same algorithmic bytes).  Streams: mean of `reps` timed
-    calls after one untimed call; the pattern probe: one HIP graph of `reps`
-    calls (as the operator's steps are timed)."""
+    Infinity Cache, so DRAM serves them); uniformly random gathers of whole
+    rows of `row_bytes` (the workload's K/V row) from a table as large as K
+    and V together (`kv_rows` rows) and from tables of GATHER_SWEEP_MB
+    (f3s_probe_rows: the hardware's rate for gather-bound work with that
+    working set); and the fused kernel's own access pattern on this plan
+    without its arithmetic (f3s_probe_gather; its rate counts the same
+    algorithmic bytes).  Streams: mean of `reps` timed calls after one
+    untimed call; the gather probes: one HIP graph of `reps` calls (as the
+    operator's steps are timed)."""
     import numpy as np
     import torch
     import paper_2505_08098_amd as f3s
@@ -178,6 +188,19 @@ def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, r
         lambda: f3s.probe_stream("copy", buf, dst, stream=stream)) / 1e6, 1)
     out["stream_write_GBs"] = round(nbytes / timed(
         lambda: f3s.probe_stream("write", dst, stream=stream)) / 1e6, 1)
+    if row_bytes in (16, 32, 64, 128, 256, 512, 1024):
+        def rows_rate(n_rows):
+            # on torch's current stream: the capturing stream inside graph_timed
+            call = lambda: f3s.probe_rows(buf, n_rows, row_bytes, sink, 2048, 4)
+            nb = 2048 * 4 * 32768
+            return round(nb / graph_timed(call, reps, dev)[1] / 1e6, 1)
+        out["random_rows_bytes"] = row_bytes
+        out["random_rows_GBs_by_table_MB"] = {
+            str(mb): rows_rate((mb << 20) // row_bytes) for mb in GATHER_SWEEP_MB}
+        if 0 < kv_rows * row_bytes <= nbytes:
+            out["random_rows_table_MB"] = round(kv_rows * row_bytes / 1e6, 1)
+            out["random_rows_GBs"] = rows_rate(kv_rows)
+            out["frac_of_random_rows"] = round(achieved_gbs / out["random_rows_GBs"], 4)
     del buf, dst, sink
     torch.cuda.empty_cache()
     out["stream_bytes"] = nbytes
@@ -654,7 +677,8 @@ def main():
         # (the probe writes meaningless values: it gets its own output buffer)
         ceilings = memory_ceilings(plan, Q if plain else None, K, V,
                                    torch.empty_like(O) if plain else None, d, achieved,
-                                   alg_bytes, stream, dev)
+                                   alg_bytes, stream, dev, kv_rows=2 * N * H,
+                                   row_bytes=d * (1 if args.in_dtype == "fp8" else 2))
     out = {
         "metric": METRIC,
         "value": round(value, 2),

@@ -15,6 +15,9 @@
  *       16 x d fp32 results per work item), in the same order and
  *       granularity, with no arithmetic and more waves in flight: the
  *       ceiling of that access pattern, from the caches and HBM together.
+ *   f3s_probe_rows                    uniformly random whole-row gathers from
+ *       a table: the hardware's rate for gather-bound work whose working set
+ *       is the table, independent of the operator's own access pattern.
  * All calls are asynchronous on `stream`, allocate nothing and return
  * F3S_ERR_INVALID_VALUE for a null or misaligned (16-byte) pointer or a
  * size that is not a multiple of 16 bytes.
@@ -46,6 +49,22 @@ f3s_status_t f3s_probe_write(void *dst, size_t bytes, uint32_t value, hipStream_
  * windows) receive meaningless values. */
 f3s_status_t f3s_probe_gather(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                               float *O, int32_t d, hipStream_t stream);
+
+/*
+ * Random row gathers: `rows` rows of `row_bytes` bytes (16, 32, 64, 128, 256,
+ * 512 or 1024; else F3S_ERR_UNSUPPORTED) at table, read in 16-byte pieces by
+ * row_bytes / 16 consecutive lanes each.  The launch has `workgroups`
+ * workgroups of 256 threads; every group of lanes reads 8 * rounds rows, each
+ * chosen uniformly from the table by a fixed integer hash of the group and
+ * the step, 8 of them in flight at a time.  Every call reads exactly
+ * workgroups * rounds * 32768 bytes (each thread 16 bytes per row, 8 rows per
+ * round).  sink: device memory of 256 uint32 that the kernel may write (it
+ * practically never does).  rows >= 1 and < 2^32, workgroups in
+ * [1, 2^31 - 1], rounds >= 1.
+ */
+f3s_status_t f3s_probe_rows(const void *table, int64_t rows, int32_t row_bytes,
+                            int32_t workgroups, int32_t rounds, uint32_t *sink,
+                            hipStream_t stream);
 
 /*
  * f3s_run(plan, Q, K, V, O, d, scale, stream) with a record of where and when

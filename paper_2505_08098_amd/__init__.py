@@ -8,5 +8,5 @@ The compute path is the HIP library only (see ``binding``); ``workloads``
 holds the seeded synthetic inputs.
 """
 from .binding import (F3SError, Plan, PlanInfo, backward, forward,  # noqa: F401
-                      forward_typed, load_library, probe_gather, probe_stream, run,
-                      run_raw, run_trace, status_string, wall_clock_khz)
+                      forward_typed, load_library, probe_gather, probe_rows, probe_stream,
+                      run, run_raw, run_trace, status_string, wall_clock_khz)

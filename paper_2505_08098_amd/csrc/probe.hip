@@ -64,6 +64,43 @@ __global__ __launch_bounds__(kThreads) void k_probe_write(u4 *__restrict__ dst, 
     }
 }
 
+// A fixed integer hash (xorshift-multiply finaliser) that spreads group and
+// step indices uniformly over the table's rows.
+__device__ __forceinline__ uint32_t spread(uint32_t x)
+{
+    x ^= x >> 16;
+    x *= 0x7FEB352Du;
+    x ^= x >> 15;
+    x *= 0x846CA68Bu;
+    x ^= x >> 16;
+    return x;
+}
+
+// Random whole-row gathers: a group of L lanes reads one row of 16 L bytes
+// (16 bytes per lane) per step, 8 steps in flight, `rounds` times.
+template <int L>
+__global__ __launch_bounds__(kThreads) void k_probe_rows(const u4 *__restrict__ table,
+                                                         uint32_t rows, int32_t rounds,
+                                                         uint32_t *__restrict__ sink)
+{
+    constexpr int kInFlight = 8;
+    const uint32_t gid = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t group = gid / L, sub = gid % L;
+    uint32_t acc = 0;
+    for (int r = 0; r < rounds; ++r) {
+        u4 v[kInFlight];
+#pragma unroll
+        for (int u = 0; u < kInFlight; ++u) {
+            const uint32_t step = (uint32_t)r * kInFlight + u;
+            const uint32_t row = spread(group * 0x9E3779B1u + step * 0x85EBCA77u) % rows;
+            v[u] = table[(uint64_t)row * L + sub];
+        }
+#pragma unroll
+        for (int u = 0; u < kInFlight; ++u) acc ^= fold(v[u]);
+    }
+    if (acc == kNever) sink[threadIdx.x] = acc;
+}
+
 // The fp16 -> fp32 fused kernel's memory accesses for one work item, with no
 // arithmetic: the item record, the window's Q rows, per block its 16 column
 // ids and 8 bitmap words, the K and V rows of every slot gathered in 16-byte
@@ -209,6 +246,29 @@ f3s_status_t f3s_probe_write(void *dst, size_t bytes, uint32_t value, hipStream_
     const uint64_t n16 = bytes / 16;
     if (n16 == 0) return F3S_OK;
     k_probe_write<<<tiles(n16), kThreads, 0, stream>>>(static_cast<u4 *>(dst), n16, value);
+    return status(hipGetLastError());
+}
+
+f3s_status_t f3s_probe_rows(const void *table, int64_t rows, int32_t row_bytes,
+                            int32_t workgroups, int32_t rounds, uint32_t *sink,
+                            hipStream_t stream)
+{
+    if (!table || !sink || !aligned16(table) || rows < 1 || rows > 0xFFFFFFFFll ||
+        workgroups < 1 || rounds < 1)
+        return F3S_ERR_INVALID_VALUE;
+    const dim3 grid((unsigned)workgroups);
+    const u4 *tab = static_cast<const u4 *>(table);
+    const uint32_t n = (uint32_t)rows;
+    switch (row_bytes) {
+    case 16: k_probe_rows<1><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    case 32: k_probe_rows<2><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    case 64: k_probe_rows<4><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    case 128: k_probe_rows<8><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    case 256: k_probe_rows<16><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    case 512: k_probe_rows<32><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    case 1024: k_probe_rows<64><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    default: return F3S_ERR_UNSUPPORTED;
+    }
     return status(hipGetLastError());
 }
 

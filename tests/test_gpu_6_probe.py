@@ -40,6 +40,33 @@ def test_stream_probes_move_the_given_bytes(gpu):
     assert L.f3s_probe_copy(src.data_ptr(), dst.data_ptr(), 20, None) == 1
 
 
+@pytest.mark.parametrize("row_bytes", [16, 64, 128, 256, 1024])
+def test_row_probe_reads_only_its_table(gpu, row_bytes):
+    """f3s_probe_rows reads a table of rows * row_bytes bytes (its rows come
+    from a hash taken modulo rows), changes neither the table nor, in
+    practice, its sink, and reports the bytes it read; bad sizes are rejected
+    before any launch."""
+    rows = 1000
+    table = torch.arange(rows * row_bytes // 4, dtype=torch.int32, device=DEV)
+    sink = torch.zeros(256, dtype=torch.int32, device=DEV)
+    nbytes = gpu.probe_rows(table, rows, row_bytes, sink, workgroups=64, rounds=3)
+    torch.cuda.synchronize()
+    assert nbytes == 64 * 3 * 32768
+    assert not bool(sink.any())
+    assert torch.equal(table, torch.arange(rows * row_bytes // 4, dtype=torch.int32,
+                                           device=DEV))
+    L = gpu.load_library()
+    p, s = table.data_ptr(), sink.data_ptr()
+    assert L.f3s_probe_rows(p, rows, 48, 64, 1, s, None) == 3       # F3S_ERR_UNSUPPORTED
+    assert L.f3s_probe_rows(p, 0, row_bytes, 64, 1, s, None) == 1   # F3S_ERR_INVALID_VALUE
+    assert L.f3s_probe_rows(p, rows, row_bytes, 0, 1, s, None) == 1
+    assert L.f3s_probe_rows(p, rows, row_bytes, 64, 0, s, None) == 1
+    assert L.f3s_probe_rows(p + 4, rows, row_bytes, 64, 1, s, None) == 1
+    assert L.f3s_probe_rows(p, 1 << 32, row_bytes, 64, 1, s, None) == 1
+    with pytest.raises(ValueError):
+        gpu.probe_rows(table, rows + 1, row_bytes, sink)
+
+
 @pytest.mark.parametrize("k", [1, 2, 4, 5])
 def test_pattern_probe_runs_on_the_workload_plans(gpu, k, monkeypatch):
     if k == 2:
