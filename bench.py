@@ -191,8 +191,9 @@ def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, r
     if row_bytes in (16, 32, 64, 128, 256, 512, 1024):
         def rows_rate(n_rows):
             # on torch's current stream: the capturing stream inside graph_timed
-            call = lambda: f3s.probe_rows(buf, n_rows, row_bytes, sink, 2048, 4)
-            nb = 2048 * 4 * 32768
+            call = lambda: f3s.probe_rows(buf, n_rows, row_bytes, sink, in_flight=8,
+                                          workgroups=2048, rounds=4)
+            nb = 2048 * 4 * 8 * 4096
             return round(nb / graph_timed(call, reps, dev)[1] / 1e6, 1)
         out["random_rows_bytes"] = row_bytes
         out["random_rows_GBs_by_table_MB"] = {
@@ -212,6 +213,37 @@ def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, r
         out["frac_of_pattern_gather"] = round(achieved_gbs / out["pattern_gather_GBs"], 4)
     out["frac_of_stream_read"] = round(achieved_gbs / out["stream_read_GBs"], 4)
     return out
+
+
+def gather_sweep(dev, reps=10):
+    """f3s_probe_rows over tables of GATHER_SWEEP_MB with 64-, 128- and
+    256-byte rows, 1 to 16 rows in flight per thread and 2, 4 or 8 workgroups
+    of 256 threads per CU (about 256 MB read per call, one HIP graph of
+    `reps` calls each): what the memory system delivers to random row
+    gathers, and whether more requests in flight raise it."""
+    import torch
+    import paper_2505_08098_amd as f3s
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    buf = torch.empty((4 << 30) // 4, dtype=torch.int32, device=dev)
+    sink = torch.zeros(256, dtype=torch.int32, device=dev)
+    f3s.probe_stream("write", buf)
+    rows = []
+    for mb in GATHER_SWEEP_MB:
+        for rb in (64, 128, 256):
+            for per_cu in (2, 4, 8):
+                for u in (1, 2, 4, 8, 16):
+                    wg = per_cu * cus
+                    rounds = max(1, (256 << 20) // (wg * u * 4096))
+                    n = (mb << 20) // rb
+                    call = lambda: f3s.probe_rows(buf, n, rb, sink, in_flight=u,
+                                                  workgroups=wg, rounds=rounds)
+                    ms = graph_timed(call, reps, dev)[1]
+                    rows.append({"table_MB": mb, "row_bytes": rb, "workgroups_per_cu": per_cu,
+                                 "in_flight": u,
+                                 "GBs": round(wg * rounds * u * 4096 / ms / 1e6, 1)})
+        print(f"gather sweep: {mb} MB done", file=sys.stderr, flush=True)
+    print(json.dumps({"metric": "random whole-row gather rate (f3s_probe_rows)", "n_gpus": 1,
+                      "cus": cus, "rows": rows}), flush=True)
 
 
 def dram_check(args, stream, dev, reps=10):
@@ -544,6 +576,9 @@ def main():
     ap.add_argument("--no-ceilings", action="store_true",
                     help="skip the probe kernels (streaming read/copy/write over 4 GiB "
                          "and the plan's access pattern without arithmetic)")
+    ap.add_argument("--gather-sweep", action="store_true",
+                    help="only the random-row gather rates by table size, row size, rows "
+                         "in flight and workgroups per CU (one JSON line)")
     ap.add_argument("--segments", action="store_true",
                     help="row windows aligned to the graphs of the batch "
                          "(f3s_plan_segments; the batched-graph workload 4, forward only)")
@@ -570,6 +605,8 @@ def main():
 
     f3s.load_library()
     dev = torch.device("cuda:0")
+    if args.gather_sweep:
+        return gather_sweep(dev)
     t0 = time.perf_counter()
     c = W.make_config(args.workload, seed=args.seed, dtype=args.in_dtype)
     gen_s = time.perf_counter() - t0

@@ -52,19 +52,20 @@ f3s_status_t f3s_probe_gather(f3s_plan_t plan, const void *Q, const void *K, con
 
 /*
  * Random row gathers: `rows` rows of `row_bytes` bytes (16, 32, 64, 128, 256,
- * 512 or 1024; else F3S_ERR_UNSUPPORTED) at table, read in 16-byte pieces by
- * row_bytes / 16 consecutive lanes each.  The launch has `workgroups`
- * workgroups of 256 threads; every group of lanes reads 8 * rounds rows, each
- * chosen uniformly from the table by a fixed integer hash of the group and
- * the step, 8 of them in flight at a time.  Every call reads exactly
- * workgroups * rounds * 32768 bytes (each thread 16 bytes per row, 8 rows per
- * round).  sink: device memory of 256 uint32 that the kernel may write (it
- * practically never does).  rows >= 1 and < 2^32, workgroups in
- * [1, 2^31 - 1], rounds >= 1.
+ * 512 or 1024) at table, read in 16-byte pieces by row_bytes / 16
+ * consecutive lanes each.  The launch has `workgroups` workgroups of 256
+ * threads; every group of lanes reads in_flight * rounds rows, each chosen
+ * uniformly from the table by a fixed integer hash of the group and the
+ * step, in_flight (1, 2, 4, 8 or 16) of them in flight at a time.  Every
+ * call reads exactly workgroups * rounds * in_flight * 4096 bytes (16 bytes
+ * per thread and row).  sink: device memory of 256 uint32 that the kernel
+ * may write (it practically never does).  rows >= 1 and < 2^32, workgroups
+ * in [1, 2^31 - 1], rounds >= 1; a row size or in_flight outside the lists
+ * gives F3S_ERR_UNSUPPORTED.
  */
 f3s_status_t f3s_probe_rows(const void *table, int64_t rows, int32_t row_bytes,
-                            int32_t workgroups, int32_t rounds, uint32_t *sink,
-                            hipStream_t stream);
+                            int32_t in_flight, int32_t workgroups, int32_t rounds,
+                            uint32_t *sink, hipStream_t stream);
 
 /*
  * f3s_run(plan, Q, K, V, O, d, scale, stream) with a record of where and when

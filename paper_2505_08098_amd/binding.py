@@ -118,7 +118,7 @@ def load_library():
     L.f3s_probe_write.restype = ctypes.c_int
     L.f3s_probe_gather.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     L.f3s_probe_gather.restype = ctypes.c_int
-    L.f3s_probe_rows.argtypes = [vp, ctypes.c_int64, i32, i32, i32, vp, vp]
+    L.f3s_probe_rows.argtypes = [vp, ctypes.c_int64, i32, i32, i32, i32, vp, vp]
     L.f3s_probe_rows.restype = ctypes.c_int
     L.f3s_run_trace.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp, ctypes.c_size_t,
                                 vp]
@@ -496,10 +496,12 @@ def probe_gather(plan, Q, K, V, out, stream=None):
         raise F3SError(rc, "f3s_probe_gather")
 
 
-def probe_rows(table, rows, row_bytes, sink, workgroups=2048, rounds=8, stream=None):
+def probe_rows(table, rows, row_bytes, sink, in_flight=8, workgroups=2048, rounds=4,
+               stream=None):
     """f3s_probe_rows: random gathers of whole rows of ``row_bytes`` bytes
-    from the first ``rows`` rows of device tensor ``table``; returns the bytes
-    one call reads (workgroups * rounds * 32768)."""
+    from the first ``rows`` rows of device tensor ``table``, ``in_flight``
+    rows in flight per thread; returns the bytes one call reads
+    (workgroups * rounds * in_flight * 4096)."""
     if not isinstance(table, torch.Tensor) or not table.is_cuda or not table.is_contiguous():
         raise TypeError("table must be a contiguous device tensor")
     if int(rows) * int(row_bytes) > table.numel() * table.element_size():
@@ -510,11 +512,11 @@ def probe_rows(table, rows, row_bytes, sink, workgroups=2048, rounds=8, stream=N
     if stream is None:
         stream = torch.cuda.current_stream(table.device)
     rc = load_library().f3s_probe_rows(table.data_ptr(), int(rows), int(row_bytes),
-                                       int(workgroups), int(rounds), sink.data_ptr(),
-                                       ctypes.c_void_p(stream.cuda_stream))
+                                       int(in_flight), int(workgroups), int(rounds),
+                                       sink.data_ptr(), ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
         raise F3SError(rc, "f3s_probe_rows")
-    return int(workgroups) * int(rounds) * 32768
+    return int(workgroups) * int(rounds) * int(in_flight) * 4096
 
 
 def run_trace(plan, Q, K, V, scale=None, out=None, stream=None):

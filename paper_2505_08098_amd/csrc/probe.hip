@@ -77,13 +77,12 @@ __device__ __forceinline__ uint32_t spread(uint32_t x)
 }
 
 // Random whole-row gathers: a group of L lanes reads one row of 16 L bytes
-// (16 bytes per lane) per step, 8 steps in flight, `rounds` times.
-template <int L>
+// (16 bytes per lane) per step, kInFlight steps in flight, `rounds` times.
+template <int L, int kInFlight>
 __global__ __launch_bounds__(kThreads) void k_probe_rows(const u4 *__restrict__ table,
                                                          uint32_t rows, int32_t rounds,
                                                          uint32_t *__restrict__ sink)
 {
-    constexpr int kInFlight = 8;
     const uint32_t gid = blockIdx.x * kThreads + threadIdx.x;
     const uint32_t group = gid / L, sub = gid % L;
     uint32_t acc = 0;
@@ -204,6 +203,26 @@ f3s_status_t status(hipError_t e)
     return e == hipSuccess ? F3S_OK : F3S_ERR_HIP;
 }
 
+template <int U>
+f3s_status_t launch_rows(const void *table, int64_t rows, int32_t row_bytes,
+                         int32_t workgroups, int32_t rounds, uint32_t *sink, hipStream_t s)
+{
+    const dim3 grid((unsigned)workgroups);
+    const u4 *tab = static_cast<const u4 *>(table);
+    const uint32_t n = (uint32_t)rows;
+    switch (row_bytes) {
+    case 16: k_probe_rows<1, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    case 32: k_probe_rows<2, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    case 64: k_probe_rows<4, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    case 128: k_probe_rows<8, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    case 256: k_probe_rows<16, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    case 512: k_probe_rows<32, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    case 1024: k_probe_rows<64, U><<<grid, kThreads, 0, s>>>(tab, n, rounds, sink); break;
+    default: return F3S_ERR_UNSUPPORTED;
+    }
+    return status(hipGetLastError());
+}
+
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 unsigned tiles(uint64_t n16)
@@ -250,26 +269,20 @@ f3s_status_t f3s_probe_write(void *dst, size_t bytes, uint32_t value, hipStream_
 }
 
 f3s_status_t f3s_probe_rows(const void *table, int64_t rows, int32_t row_bytes,
-                            int32_t workgroups, int32_t rounds, uint32_t *sink,
-                            hipStream_t stream)
+                            int32_t in_flight, int32_t workgroups, int32_t rounds,
+                            uint32_t *sink, hipStream_t stream)
 {
     if (!table || !sink || !aligned16(table) || rows < 1 || rows > 0xFFFFFFFFll ||
         workgroups < 1 || rounds < 1)
         return F3S_ERR_INVALID_VALUE;
-    const dim3 grid((unsigned)workgroups);
-    const u4 *tab = static_cast<const u4 *>(table);
-    const uint32_t n = (uint32_t)rows;
-    switch (row_bytes) {
-    case 16: k_probe_rows<1><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
-    case 32: k_probe_rows<2><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
-    case 64: k_probe_rows<4><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
-    case 128: k_probe_rows<8><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
-    case 256: k_probe_rows<16><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
-    case 512: k_probe_rows<32><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
-    case 1024: k_probe_rows<64><<<grid, kThreads, 0, stream>>>(tab, n, rounds, sink); break;
+    switch (in_flight) {
+    case 1: return launch_rows<1>(table, rows, row_bytes, workgroups, rounds, sink, stream);
+    case 2: return launch_rows<2>(table, rows, row_bytes, workgroups, rounds, sink, stream);
+    case 4: return launch_rows<4>(table, rows, row_bytes, workgroups, rounds, sink, stream);
+    case 8: return launch_rows<8>(table, rows, row_bytes, workgroups, rounds, sink, stream);
+    case 16: return launch_rows<16>(table, rows, row_bytes, workgroups, rounds, sink, stream);
     default: return F3S_ERR_UNSUPPORTED;
     }
-    return status(hipGetLastError());
 }
 
 f3s_status_t f3s_probe_gather(f3s_plan_t p, const void *Q, const void *K, const void *V,

@@ -49,20 +49,23 @@ def test_row_probe_reads_only_its_table(gpu, row_bytes):
     rows = 1000
     table = torch.arange(rows * row_bytes // 4, dtype=torch.int32, device=DEV)
     sink = torch.zeros(256, dtype=torch.int32, device=DEV)
-    nbytes = gpu.probe_rows(table, rows, row_bytes, sink, workgroups=64, rounds=3)
+    for u in (1, 2, 4, 8, 16):
+        nbytes = gpu.probe_rows(table, rows, row_bytes, sink, in_flight=u, workgroups=64,
+                                rounds=3)
+        assert nbytes == 64 * 3 * u * 4096
     torch.cuda.synchronize()
-    assert nbytes == 64 * 3 * 32768
     assert not bool(sink.any())
     assert torch.equal(table, torch.arange(rows * row_bytes // 4, dtype=torch.int32,
                                            device=DEV))
     L = gpu.load_library()
     p, s = table.data_ptr(), sink.data_ptr()
-    assert L.f3s_probe_rows(p, rows, 48, 64, 1, s, None) == 3       # F3S_ERR_UNSUPPORTED
-    assert L.f3s_probe_rows(p, 0, row_bytes, 64, 1, s, None) == 1   # F3S_ERR_INVALID_VALUE
-    assert L.f3s_probe_rows(p, rows, row_bytes, 0, 1, s, None) == 1
-    assert L.f3s_probe_rows(p, rows, row_bytes, 64, 0, s, None) == 1
-    assert L.f3s_probe_rows(p + 4, rows, row_bytes, 64, 1, s, None) == 1
-    assert L.f3s_probe_rows(p, 1 << 32, row_bytes, 64, 1, s, None) == 1
+    assert L.f3s_probe_rows(p, rows, 48, 8, 64, 1, s, None) == 3         # F3S_ERR_UNSUPPORTED
+    assert L.f3s_probe_rows(p, rows, row_bytes, 3, 64, 1, s, None) == 3
+    assert L.f3s_probe_rows(p, 0, row_bytes, 8, 64, 1, s, None) == 1     # F3S_ERR_INVALID_VALUE
+    assert L.f3s_probe_rows(p, rows, row_bytes, 8, 0, 1, s, None) == 1
+    assert L.f3s_probe_rows(p, rows, row_bytes, 8, 64, 0, s, None) == 1
+    assert L.f3s_probe_rows(p + 4, rows, row_bytes, 8, 64, 1, s, None) == 1
+    assert L.f3s_probe_rows(p, 1 << 32, row_bytes, 8, 64, 1, s, None) == 1
     with pytest.raises(ValueError):
         gpu.probe_rows(table, rows + 1, row_bytes, sink)
 
