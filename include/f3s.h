@@ -144,8 +144,9 @@ f3s_plan_t f3s_plan_ws(const int32_t *row_ptr, const int32_t *col_idx, int32_t N
  *   n_segs   >= 0 graphs
  * The segments only choose the windows: the operator's result is the same
  * for any segmentation, also when edges cross segments.  Such a plan serves
- * f3s_run, f3s_run_mh and f3s_forward; f3s_plan_transpose and the backward
- * calls return F3S_ERR_UNSUPPORTED for it.  Otherwise as f3s_plan.
+ * every forward and backward call; f3s_plan_transpose gives it a plan of A^T
+ * with 16-row windows (built from the rows of A^T, never a copy).  Otherwise
+ * as f3s_plan.
  */
 f3s_plan_t f3s_plan_segments(const int32_t *row_ptr, const int32_t *col_idx, int32_t N,
                              const int32_t *seg_ptr, int32_t n_segs);
@@ -241,8 +242,9 @@ f3s_status_t f3s_forward_typed(f3s_plan_t plan, const void *Q, const void *K, co
  * exact symmetry check first: if A^T = A the result is a copy of the plan.
  * The check runs on the plan for patterns below 8 M entries and on the
  * sorted rows of A^T above (environment F3S_SYMMETRY_SORT_FIRST=<entries>
- * moves that threshold; 0 always sorts first).  Synchronous; NULL on error
- * (f3s_last_error).  Destroy with f3s_destroy.
+ * moves that threshold; 0 always sorts first).  A plan of f3s_plan_segments
+ * skips the check: its A^T always gets its own plan of 16-row windows.
+ * Synchronous; NULL on error (f3s_last_error).  Destroy with f3s_destroy.
  */
 f3s_plan_t f3s_plan_transpose(f3s_plan_t plan);
 

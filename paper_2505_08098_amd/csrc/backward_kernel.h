@@ -123,12 +123,12 @@ template <int D, bool kWide, bool kBF16, int NW = 1>
 __global__ __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
-    const uint32_t *__restrict__ mask, const _Float16 *__restrict__ Q,
-    const _Float16 *__restrict__ K, const _Float16 *__restrict__ V,
-    const _Float16 *__restrict__ G, const float *__restrict__ O,
-    const float *__restrict__ lse, float2 *__restrict__ stats, float *__restrict__ dQ,
-    float *__restrict__ part, int32_t N, int32_t ld, int32_t h0, int32_t nh, float sl2,
-    float scale, uint32_t order)
+    const uint32_t *__restrict__ mask, const int32_t *__restrict__ win_row,
+    const _Float16 *__restrict__ Q, const _Float16 *__restrict__ K,
+    const _Float16 *__restrict__ V, const _Float16 *__restrict__ G,
+    const float *__restrict__ O, const float *__restrict__ lse, float2 *__restrict__ stats,
+    float *__restrict__ dQ, float *__restrict__ part, int32_t N, int32_t ld, int32_t h0,
+    int32_t nh, float sl2, float scale, uint32_t order)
 {
     constexpr int NC = D / 32, NT = D / 16, NI = D / 16;
     constexpr int LSK = D + 16;  // K tile: operand reads and transposed reads
@@ -157,8 +157,13 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     G += (int64_t)head * D;
     O += (int64_t)head * D;
     dQ += (int64_t)head * D;
-    const int row = it.window * kWindowRows + i;
-    const int rrow = min(row, N - 1);
+    // the window's rows (16-row windows, or those of a plan aligned to the
+    // graphs of a batch); pad rows read the window's first row
+    int32_t r0, nr;
+    window_rows(win_row, N, it.window, &r0, &nr);
+    const int row = r0 + i;
+    const bool live = i < nr;
+    const int rrow = live ? row : r0;
     int b0 = it.blk_begin, b1 = it.blk_end;
     if constexpr (NW > 1) {
         const int pairs = (b1 - b0 + 1) >> 1;
@@ -191,7 +196,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     dl += __shfl_xor(dl, 32);
     // one 8-byte record per row and head for the dK/dV pass, which gathers
     // it for every attending row: (base-2 log-sum-exp, delta)
-    if (g == 0 && row < N && wv == 0) stats[(int64_t)row * H + head] = float2{lse2, dl};
+    if (g == 0 && live && wv == 0) stats[(int64_t)row * H + head] = float2{lse2, dl};
 
     f4 acc[NT];
 #pragma unroll
@@ -291,7 +296,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     }
     float *out;
     if (it.slot < 0) {
-        if (row >= N) return;
+        if (!live) return;
         out = dQ + (int64_t)row * ld;
     } else {
         const int64_t ps = (int64_t)it.slot * nh + hl;
@@ -520,6 +525,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
 // nparts outputs per (piece, head) slot, stored back to back.
 template <int D>
 __global__ __launch_bounds__(256) void k_merge_sum(const int32_t *__restrict__ merges,
+                                                   const int32_t *__restrict__ win_row,
                                                    const float *__restrict__ part,
                                                    float *__restrict__ out0,
                                                    float *__restrict__ out1, int32_t nparts,
@@ -529,8 +535,10 @@ __global__ __launch_bounds__(256) void k_merge_sum(const int32_t *__restrict__ m
     const int s = blockIdx.x / nh, hl = blockIdx.x - (blockIdx.x / nh) * nh;
     const int w = merges[3 * s], first = merges[3 * s + 1], np = merges[3 * s + 2];
     const int r = threadIdx.x >> 4, q = threadIdx.x & 15;
-    const int row = w * kWindowRows + r;
-    if (row >= N) return;
+    int32_t r0, nr;
+    window_rows(win_row, N, w, &r0, &nr);
+    if (r >= nr) return;
+    const int row = r0 + r;
     const int64_t slot_floats = (int64_t)nparts * kWindowRows * D;
     for (int pidx = 0; pidx < nparts; ++pidx) {
         float *out = (pidx == 0 ? out0 : out1) + (int64_t)row * ld + (int64_t)(h0 + hl) * D;
@@ -588,13 +596,13 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (p.n_split > 0 && (int64_t)nh * D > kMaxD) return hipErrorInvalidValue;
             if (p.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)p.n_items * nh), 64 * nw, 0, s>>>(
-                    p.items, p.cols, p.mask, q, k, v, gr, O, lse, stats, dQ, p.part_o, p.N,
-                    ld, h0, nh, sl2, scale, order_a);
+                    p.items, p.cols, p.mask, p.win_row, q, k, v, gr, O, lse, stats, dQ,
+                    p.part_o, p.N, ld, h0, nh, sl2, scale, order_a);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (p.n_split > 0) {
-                k_merge_sum<D><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.part_o, dQ,
-                                                             nullptr, 1, p.N, ld, h0, nh);
+                k_merge_sum<D><<<p.n_split * nh, 256, 0, s>>>(p.merges, p.win_row, p.part_o,
+                                                             dQ, nullptr, 1, p.N, ld, h0, nh);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
         }
@@ -622,8 +630,9 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (pt.n_split > 0) {
-                k_merge_sum<D><<<pt.n_split * nh, 256, 0, s>>>(pt.merges, pt.part_o, dK, dV,
-                                                              2, pt.N, ld, h0, nh);
+                k_merge_sum<D><<<pt.n_split * nh, 256, 0, s>>>(pt.merges, pt.win_row,
+                                                              pt.part_o, dK, dV, 2, pt.N, ld,
+                                                              h0, nh);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
         }

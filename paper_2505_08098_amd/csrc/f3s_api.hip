@@ -562,10 +562,6 @@ f3s_plan_t make_transpose(f3s_plan_t src, void *workspace, size_t workspace_byte
         fail(F3S_ERR_INVALID_VALUE);
         return nullptr;
     }
-    if (src->win_row) {  // windows aligned to graphs: forward only
-        fail(F3S_ERR_UNSUPPORTED);
-        return nullptr;
-    }
     f3s_status_t st = F3S_OK;
     auto step = [&](hipError_t e) {
         if (st == F3S_OK && e != hipSuccess) st = from_hip(e);
@@ -591,19 +587,25 @@ f3s_plan_t make_transpose(f3s_plan_t src, void *workspace, size_t workspace_byte
             carve_transpose(tmp, true, ts, src, lent);
             int32_t h = 1;
             // symmetric?  Small patterns: checked on the plan first (no sort);
-            // large ones: on A^T's sorted rows, which are needed anyway if not
+            // large ones: on A^T's sorted rows, which are needed anyway if not.
+            // A plan whose windows follow the graphs of a batch skips the check
+            // (it assumes 16-row windows): its A^T gets a plan of 16-row
+            // windows built from A^T's rows.
             const bool small = src->nnz < env_int("F3S_SYMMETRY_SORT_FIRST", kSortFirstEntries);
             bool have_csr = false;
-            step(hipMemsetAsync(ts.asym, 0, sizeof(int32_t), nullptr));
-            if (small) {
-                step(f3s::launch_check_symmetric(*src, ts.win, ts.asym, nullptr));
-            } else {
-                step(f3s::launch_transpose_csr(*src, ts.tr, ts.tr_bytes, ts.rp, ts.ci, nullptr));
-                step(f3s::launch_compare_rows(*src, ts.rp, ts.ci, ts.win, ts.pre, ts.asym,
-                                              nullptr));
-                have_csr = true;
+            if (!src->win_row) {
+                step(hipMemsetAsync(ts.asym, 0, sizeof(int32_t), nullptr));
+                if (small) {
+                    step(f3s::launch_check_symmetric(*src, ts.win, ts.asym, nullptr));
+                } else {
+                    step(f3s::launch_transpose_csr(*src, ts.tr, ts.tr_bytes, ts.rp, ts.ci,
+                                                   nullptr));
+                    step(f3s::launch_compare_rows(*src, ts.rp, ts.ci, ts.win, ts.pre,
+                                                  ts.asym, nullptr));
+                    have_csr = true;
+                }
+                step(hipMemcpy(&h, ts.asym, sizeof(int32_t), hipMemcpyDeviceToHost));
             }
-            step(hipMemcpy(&h, ts.asym, sizeof(int32_t), hipMemcpyDeviceToHost));
             if (st == F3S_OK && h == 0) {
                 t = clone_plan(src, 2 * f3s::kMaxD);
                 if (!t) st = g_last_error;
@@ -866,7 +868,7 @@ f3s_status_t f3s_backward_typed(f3s_plan_t p, f3s_plan_t pt, const void *Q, cons
         return fail(F3S_ERR_UNSUPPORTED);
     if (!p || !pt || n_heads < 1) return fail(F3S_ERR_INVALID_VALUE);
     if (pt->transpose_of != p->id || pt->N != p->N) return fail(F3S_ERR_INVALID_VALUE);
-    if (p->win_row) return fail(F3S_ERR_UNSUPPORTED);  // windows aligned to graphs
+    if (pt->win_row) return fail(F3S_ERR_UNSUPPORTED);  // A^T's plan has 16-row windows
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;

@@ -46,13 +46,17 @@ __global__ __launch_bounds__(256) void k_window_bits(const int32_t *blk_off,
 // order; one wavefront per window.
 __global__ __launch_bounds__(256) void k_window_pairs(const int32_t *blk_off,
                                                       const int32_t *cols,
-                                                      const uint32_t *mask, int32_t T,
+                                                      const uint32_t *mask,
+                                                      const int32_t *win_row, int32_t T,
                                                       const int32_t *off, int32_t *keys,
                                                       int32_t *rows)
 {
     const int lane = threadIdx.x & 63;
     const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (w >= T) return;
+    // first row of the window (16-row windows, or those of a plan aligned to
+    // the graphs of a batch)
+    const int r0 = win_row ? win_row[w] : w * kWindowRows;
     const int64_t k0 = (int64_t)kMaskWords * blk_off[w];
     const int64_t k1 = (int64_t)kMaskWords * blk_off[w + 1];
     int64_t base = off[w];
@@ -69,7 +73,7 @@ __global__ __launch_bounds__(256) void k_window_pairs(const int32_t *blk_off,
             const int r = (bit >> 2) & 15;             // window row
             const int c = 4 * (bit >> 6) + (bit & 3);  // block column
             keys[pos] = cols[kBlockCols * blk + c];
-            rows[pos] = w * kWindowRows + r;
+            rows[pos] = r0 + r;
             ++pos;
         }
         base += total;
@@ -356,8 +360,8 @@ hipError_t launch_transpose_csr(const f3s_plan_s &p, void *scratch, size_t scrat
         if ((e = hipGetLastError()) != hipSuccess) return e;
         e = launch_scan(cnt, off, T, rs.scan_tmp, nullptr, s);
         if (e != hipSuccess) return e;
-        k_window_pairs<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.cols, p.mask, T, off, keys_in,
-                                                   rows_in);
+        k_window_pairs<<<(T + 3) / 4, 256, 0, s>>>(p.blk_off, p.cols, p.mask, p.win_row, T,
+                                                   off, keys_in, rows_in);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const int32_t *sorted_cols = keys_in, *sorted_rows = rows_in;

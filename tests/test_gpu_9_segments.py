@@ -250,6 +250,82 @@ def test_segment_plan_errors(gpu):
         assert e.value.code == 1           # F3S_ERR_INVALID_VALUE
     plan = gpu.Plan.segments(_dev(rp), _dev(ci), 3, [0, 1, 3])
     assert plan.window_rows().tolist() == [0, 3]
-    with pytest.raises(gpu.F3SError) as e:
-        plan.transpose()                   # the backward needs 16-row windows
-    assert e.value.code == 3               # F3S_ERR_UNSUPPORTED
+
+
+# ---- the backward pass over a plan with graph-aligned windows ---------------
+# Gradient bar as for the 16-row plans: relative Frobenius <= 1e-3 per gradient
+# and max-abs <= 5e-3 * max(1, max |reference|) (P and dS rounded to fp16).
+
+def _check_grad(name, got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite"
+    diff = got - ref
+    nref = float(np.linalg.norm(ref))
+    rel = float(np.linalg.norm(diff)) / nref if nref > 0 else float(np.linalg.norm(diff))
+    ma = float(np.abs(diff).max()) if diff.size else 0.0
+    bound = 5e-3 * max(1.0, float(np.abs(ref).max()) if ref.size else 1.0)
+    print(f"  {name}: rel_fro={rel:.2e} max_abs={ma:.2e} (bound {bound:.2e})", flush=True)
+    assert rel <= 1e-3 and ma <= bound, (name, rel, ma)
+
+
+def _grad_case(f3s, oracle, rp, ci, N, seg, Q, K, V, G, scale, dtype=torch.float16):
+    plan = _segment_plan(f3s, rp, ci, N, seg)
+    plan_t = plan.transpose()
+    # A^T's plan has 16-row windows of its own, never a copy of the aligned plan
+    assert not (plan_t.info["flags"] & 4)
+    assert plan_t.info["n_windows"] == (N + 15) // 16
+    conv = (lambda a: _dev(a)) if dtype == torch.float16 else \
+        (lambda a: _dev(a.view(np.int16)).view(torch.bfloat16))
+    q, k, v, g = conv(Q), conv(K), conv(V), conv(G)
+    if dtype == torch.float16:
+        O, lse = f3s.forward(plan, q, k, v, scale=scale)
+    else:
+        O, lse = f3s.forward_typed(plan, q, k, v, scale=scale, want_lse=True)
+    dQ, dK, dV = f3s.backward(plan, plan_t, q, k, v, O, g, lse, scale=scale)
+    torch.cuda.synchronize()
+    if dtype == torch.float16:
+        ref = oracle.attention_bwd_f64(rp, ci, Q, K, V, G, scale)
+    else:
+        w = oracle.widen_bf16
+        ref = oracle.attention_bwd_f64(rp, ci, w(Q), w(K), w(V), w(G), scale)
+    for name, got, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
+        _check_grad(name, got.cpu().numpy(), r)
+
+
+def test_molecule_batch_gradients(gpu, oracle):
+    c = W.make_config(4)
+    G = np.random.default_rng(51).standard_normal(c["Q"].shape).astype(np.float16)
+    _grad_case(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"], c["seg_ptr"], c["Q"],
+               c["K"], c["V"], G, c["scale"])
+
+
+@pytest.mark.parametrize("waves", ["1", "2", "4"])
+def test_gradients_split_windows_of_odd_row_counts(gpu, oracle, waves, monkeypatch):
+    """The heavy windows of 5, 12 and 13 rows split into pieces (dQ partials
+    merged per window row), shared by one, two or four waves."""
+    monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "16")
+    rng = np.random.default_rng(52)
+    rp, ci, seg = _size_class_pattern(rng, N=3000)
+    N, d = len(rp) - 1, 64
+    Q, K, V, G = (rng.standard_normal((N, d)).astype(np.float16) for _ in range(4))
+    _grad_case(gpu, oracle, rp, ci, N, seg, Q, K, V, G, 0.125)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_gradients_random_segmentations(gpu, oracle, seed):
+    rng = np.random.default_rng(2200 + seed)
+    N = int(rng.integers(1, 500))
+    rp, ci = W.random_csr(rng, N, max_deg=min(N, 50), empty_frac=0.1, dup_frac=0.2)
+    d = (32, 128, 256)[seed]
+    Q, K, V, G = (rng.standard_normal((N, d)).astype(np.float16) for _ in range(4))
+    _grad_case(gpu, oracle, rp, ci, N, _random_segments(rng, N), Q, K, V, G,
+               1 / math.sqrt(d))
+
+
+def test_molecule_batch_gradients_bf16(gpu, oracle):
+    c = W.make_config(4, dtype="bf16")
+    G = W.to_bf16_bits(np.random.default_rng(53).standard_normal(c["Q"].shape,
+                                                                 dtype=np.float32))
+    _grad_case(gpu, oracle, c["row_ptr"], c["col_idx"], c["N"], c["seg_ptr"], c["Q"],
+               c["K"], c["V"], G, c["scale"], dtype=torch.bfloat16)
