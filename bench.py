@@ -279,11 +279,35 @@ def dram_check(args, stream, dev, reps=10):
     info = plan.info
     nbytes = algorithmic_bytes(info, d)
     gbs = nbytes / ms / 1e6
+    # the same accesses without arithmetic, and random 256-byte rows of K
+    # (2.1 GB, 8x the Infinity Cache): the DRAM-side ceilings of this graph
+    for _ in range(2):
+        f3s.probe_gather(plan, Q, K, V, O, stream=stream)
+    a0, b0 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record(stream)
+    for _ in range(reps):
+        f3s.probe_gather(plan, Q, K, V, O, stream=stream)
+    b0.record(stream)
+    torch.cuda.synchronize()
+    ms_probe = a0.elapsed_time(b0) / reps
+    sink = torch.zeros(256, dtype=torch.int32, device=dev)
+    rows_call = lambda: f3s.probe_rows(K, N, 2 * d, sink, in_flight=8, workgroups=2048,
+                                       rounds=16, stream=stream)
+    rows_call()
+    a0.record(stream)
+    for _ in range(reps):
+        rows_call()
+    b0.record(stream)
+    torch.cuda.synchronize()
+    rows_gbs = 2048 * 16 * 8 * 4096 / (a0.elapsed_time(b0) / reps) / 1e6
     out = {"workload": f"uniform random graph N={N}, 16 random neighbours + self, d={d}",
            "nnz": info["nnz"], "n_unique": info["n_unique"], "ms": round(ms, 4),
            "algorithmic_bytes": nbytes, "achieved_GBs": round(gbs, 1),
            "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
-           "gflops_eff": round(4.0 * info["nnz"] * d / ms / 1e6, 1)}
+           "gflops_eff": round(4.0 * info["nnz"] * d / ms / 1e6, 1),
+           "pattern_gather_ms": round(ms_probe, 4),
+           "pattern_gather_GBs": round(nbytes / ms_probe / 1e6, 1),
+           "random_rows_of_K_GBs": round(rows_gbs, 1)}
     plan.close()
     del Q, K, V, O
     torch.cuda.empty_cache()

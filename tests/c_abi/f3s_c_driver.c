@@ -137,6 +137,39 @@ int main(int argc, char **argv)
     (void)hipFree(d_o2);
     free(o2);
 
+    /* windows aligned to graphs of 7 rows each (f3s_plan_segments, host
+       offsets): same operator, so O again within the parity bar */
+    {
+        const int32_t n_segs = (N + 6) / 7;
+        int32_t *seg = malloc(sizeof(int32_t) * ((size_t)n_segs + 1));
+        for (int32_t g = 0; g <= n_segs; ++g) seg[g] = g * 7 < N ? g * 7 : N;
+        f3s_plan_t sp = f3s_plan_segments(d_rp, d_ci, N, seg, n_segs);
+        if (!sp) {
+            fprintf(stderr, "f3s_plan_segments: %s\n", f3s_status_string(f3s_last_error()));
+            return 3;
+        }
+        f3s_plan_info_t si;
+        if (f3s_plan_info(sp, &si) != F3S_OK) return 3;
+        int32_t *wr = malloc(sizeof(int32_t) * ((size_t)si.n_windows + 1));
+        if (f3s_plan_window_rows(sp, wr) != F3S_OK) return 3;
+        fprintf(info, "seg_windows %d first %d %d %d last %d\n", si.n_windows,
+                wr[0], si.n_windows > 0 ? wr[1] : -1, si.n_windows > 1 ? wr[2] : -1,
+                wr[si.n_windows]);
+        st = f3s_run(sp, d_q, d_k, d_v, d_o, d, scale, NULL);
+        HIP_OK(hipDeviceSynchronize());
+        float *os = malloc(4 * (feat ? feat : 1));
+        HIP_OK(hipMemcpy(os, d_o, 4 * feat, hipMemcpyDeviceToHost));
+        snprintf(path, sizeof path, "%s/o_seg.bin", dir);
+        FILE *fs = fopen(path, "wb");
+        if (!fs || fwrite(os, 4, feat, fs) != feat) return 1;
+        fclose(fs);
+        fprintf(info, "seg_run %s\n", f3s_status_string(st));
+        f3s_destroy(sp);
+        free(wr);
+        free(os);
+        free(seg);
+    }
+
     /* argument errors are reported, not launched */
     st = f3s_run(plan, d_q, d_k, d_v, d_o, d + 8, scale, NULL);
     fprintf(info, "bad_d %s\n", f3s_status_string(st));

@@ -25,8 +25,9 @@ def _run_driver(tmp_path, rp, ci, Q, K, V, scale):
                          capture_output=True, text=True, timeout=120)
     assert res.returncode == 0, res.stderr
     O = np.fromfile(tmp_path / "o.bin", dtype=np.float32).reshape(N, d)
+    O_seg = np.fromfile(tmp_path / "o_seg.bin", dtype=np.float32).reshape(N, d)
     info = dict(line.split(" ", 1) for line in (tmp_path / "info.txt").read_text().splitlines())
-    return O, info
+    return O, O_seg, info
 
 
 @pytest.mark.parametrize("case", ["workload1", "random_ragged"])
@@ -42,13 +43,20 @@ def test_c_driver_matches_oracle(gpu, oracle, tmp_path, case):
         rp, ci = W.random_csr(rng, N, max_deg=40, empty_frac=0.1, dup_frac=0.2)
         Q, K, V = (rng.standard_normal((N, d)).astype(np.float16) for _ in range(3))
         scale = 1 / math.sqrt(d)
-    O, info = _run_driver(tmp_path, rp, ci, Q, K, V, scale)
+    O, O_seg, info = _run_driver(tmp_path, rp, ci, Q, K, V, scale)
     ref = oracle.attention_f64(rp, ci, Q, K, V, scale)
-    err = O.astype(np.float64) - ref
-    rel = float(np.linalg.norm(err) / np.linalg.norm(ref))
-    print(f"  {case}: max_abs={np.abs(err).max():.3e} rel_fro={rel:.3e} info={info}",
-          flush=True)
-    assert np.isfinite(O).all() and np.abs(err).max() <= 5e-3 and rel <= 1e-3
+    for got in (O, O_seg):
+        err = got.astype(np.float64) - ref
+        rel = float(np.linalg.norm(err) / np.linalg.norm(ref))
+        print(f"  {case}: max_abs={np.abs(err).max():.3e} rel_fro={rel:.3e}", flush=True)
+        assert np.isfinite(got).all() and np.abs(err).max() <= 5e-3 and rel <= 1e-3
+    print(f"  info={info}", flush=True)
+    # graphs of 7 rows: two per window (14 rows), the last window the remainder
+    N = Q.shape[0]
+    wr = oracle.segment_windows(np.minimum(np.arange(0, N + 7, 7), N))
+    assert info["seg_windows"] == (f"{len(wr) - 1} first {wr[0]} {wr[1]} {wr[2]} "
+                                   f"last {wr[-1]}")
+    assert info["seg_run"] == "F3S_OK"
     assert int(info["n_windows"]) == (Q.shape[0] + 15) // 16
     assert info["bad_d"] == "F3S_ERR_UNSUPPORTED"
     assert info["null_plan"] == "F3S_ERR_INVALID_VALUE last_error F3S_ERR_INVALID_VALUE"
