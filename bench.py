@@ -604,6 +604,9 @@ def main():
     ap.add_argument("--gather-sweep", action="store_true",
                     help="only the random-row gather rates by table size, row size, rows "
                          "in flight and workgroups per CU (one JSON line)")
+    ap.add_argument("--d", type=int, default=None,
+                    help="feature size instead of the workload's (a multiple of 32 up to "
+                         "256; the paper's sweep is 64, 128, 256)")
     ap.add_argument("--segments", action="store_true",
                     help="row windows aligned to the graphs of the batch "
                          "(f3s_plan_segments; the batched-graph workload 4)")
@@ -632,7 +635,7 @@ def main():
     if args.gather_sweep:
         return gather_sweep(dev)
     t0 = time.perf_counter()
-    c = W.make_config(args.workload, seed=args.seed, dtype=args.in_dtype)
+    c = W.make_config(args.workload, seed=args.seed, dtype=args.in_dtype, d=args.d)
     gen_s = time.perf_counter() - t0
     N, d = c["N"], c["d"]
     H = args.heads
@@ -755,13 +758,13 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{c['name']}: " + {
-                1: "Erdos-Renyi N=1024, ~16 nbrs/row incl. self-loop, d=64",
-                2: "Chung-Lu N=65536, exponent 2.1, mean degree 20, cap 4096, self-loops, d=64",
+                1: "Erdos-Renyi N=1024, ~16 nbrs/row incl. self-loop",
+                2: "Chung-Lu N=65536, exponent 2.1, mean degree 20, cap 4096, self-loops",
                 3: "Chung-Lu N=1048576, exponent 2.5, mean degree 16, cap 4096, "
-                   "self-loops, permuted ids, d=128",
-                4: "4096 molecule-like graphs of 15-45 nodes, block-diagonal, d=64",
-                5: "sequence L=32768, window 256 + 64 random keys per query, d=64",
-            }[args.workload],
+                   "self-loops, permuted ids",
+                4: "4096 molecule-like graphs of 15-45 nodes, block-diagonal",
+                5: "sequence L=32768, window 256 + 64 random keys per query",
+            }[args.workload] + f", d={d}",
             "N": N, "nnz": info["nnz"], "d": d, "heads": H, "scale": c["scale"],
             "in_dtype": args.in_dtype, "out_dtype": args.out_dtype,
             "windows": "aligned to the graphs" if args.segments else "16 rows",

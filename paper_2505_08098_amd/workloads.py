@@ -233,11 +233,12 @@ def _graph(k, seed):
     return rp, ci, seg
 
 
-def make_config(k, seed=0, with_features=True, dtype="f16"):
+def make_config(k, seed=0, with_features=True, dtype="f16", d=None):
     """Workload k (1..5): dict(name, N, d, scale, row_ptr, col_idx, Q, K, V),
     plus seg_ptr (the graphs' first rows, then N) for the batched graphs;
-    dtype "f16" (default), "bf16" or "fp8" selects the feature storage type.
-    The arrays are fresh copies (callers may modify them)."""
+    dtype "f16" (default), "bf16" or "fp8" selects the feature storage type;
+    d overrides the workload's feature size (the paper varies it over 64,
+    128 and 256).  The arrays are fresh copies (callers may modify them)."""
     if k not in WORKLOADS:
         raise ValueError(f"unknown workload {k}")
     cfg = WORKLOADS[k]
@@ -245,7 +246,7 @@ def make_config(k, seed=0, with_features=True, dtype="f16"):
     rp, ci, seg = _graph(k, seed)
     rp, ci = rp.copy(), ci.copy()
     N = len(rp) - 1
-    d = cfg["d"]
+    d = cfg["d"] if d is None else int(d)
     out = dict(name=cfg["name"], N=N, d=d, scale=1.0 / math.sqrt(d),
                row_ptr=rp, col_idx=ci)
     if seg is not None:

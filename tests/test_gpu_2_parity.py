@@ -371,6 +371,28 @@ def test_multi_head_workloads(gpu, oracle, k, H):
             _assert_parity(O[:, h], ref)
 
 
+@pytest.mark.parametrize("k,d", [(3, 64), (3, 256), (2, 128), (2, 256), (4, 128), (4, 256),
+                                 (5, 128), (5, 256)])
+def test_workloads_at_other_feature_sizes(gpu, oracle, k, d):
+    """The feature-size sweep of the measurements (the paper varies d over
+    64, 128 and 256): each workload graph at the other sizes, every row, or
+    for the million-node graph the sub-problem of 20,000 random rows and the
+    8 longest rows."""
+    c = W.make_config(k, d=d)
+    rp, ci, N = c["row_ptr"], c["col_idx"], c["N"]
+    print(f"workload {k} N={N} d={d}", flush=True)
+    O, _ = _run(gpu, rp, ci, N, c["Q"], c["K"], c["V"], c["scale"])
+    if k == 3:
+        rng = np.random.default_rng(70 + d)
+        rows = np.unique(np.concatenate([rng.integers(0, N, size=20000),
+                                         np.argsort(np.diff(rp), kind="stable")[-8:]]))
+        mrp, mci, U = rows_subproblem(rp, ci, rows)
+        ref = oracle.attention_f64(mrp, mci, c["Q"][U], c["K"][U], c["V"][U], c["scale"])
+        _assert_parity(O[rows], ref[np.searchsorted(U, rows)])
+    else:
+        _assert_parity(O, oracle.attention_f64(rp, ci, c["Q"], c["K"], c["V"], c["scale"]))
+
+
 @pytest.mark.parametrize("k,H", [(5, 1), (2, 3), (4, 1)])
 def test_xcd_ranges_order_gives_identical_results(gpu, k, H, monkeypatch):
     """Each XCD taking a consecutive range of the work list (workgroup b at

@@ -327,14 +327,15 @@ def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order
     assert plan.info["n_split"] > 0 and plan_t.info["n_split"] > 0
 
 
-@pytest.mark.parametrize("dtype", ["f16", "bf16"])
-def test_gradients_million_node_workload_sampled(gpu, oracle, dtype):
-    """The 1,048,576-node Chung-Lu workload (d = 128), whole backward on the
-    GPU; the oracle runs on the sub-problem of 500 random keys and the 4
-    heaviest keys (hubs of about 4,000 attending rows), every row attending
-    to them with its full neighbour list: dQ is exact there on every one of
-    those rows (about 25,000), dK and dV on the sampled keys."""
-    c = W.make_config(3, dtype=dtype)
+@pytest.mark.parametrize("dtype,d", [("f16", 128), ("bf16", 128), ("f16", 64), ("f16", 256)])
+def test_gradients_million_node_workload_sampled(gpu, oracle, dtype, d):
+    """The 1,048,576-node Chung-Lu workload (d = 128, and 64 and 256 for the
+    feature-size sweep), whole backward on the GPU; the oracle runs on the
+    sub-problem of 500 random keys and the 4 heaviest keys (hubs of about
+    4,000 attending rows), every row attending to them with its full
+    neighbour list: dQ is exact there on every one of those rows (about
+    25,000), dK and dV on the sampled keys."""
+    c = W.make_config(3, dtype=dtype, d=d)
     rp, ci, N, scale = c["row_ptr"], c["col_idx"], c["N"], c["scale"]
     rng = np.random.default_rng(31)
     g32 = rng.standard_normal(c["Q"].shape, dtype=np.float32)
