@@ -97,3 +97,30 @@ def test_transpose_allocation_failing_leaks_nothing(gpu, monkeypatch, k):
         print(f"  limit {lim}: transpose {'built' if res[0] else 'out of memory'}", flush=True)
     assert failures >= 1 and res[-1]
     L.f3s_destroy(src)
+
+
+def test_segment_plan_allocation_failing_leaks_nothing(gpu, monkeypatch):
+    """f3s_plan_segments (the molecule batch, windows aligned to its graphs):
+    the window rows travel in the build's scratch and in the plan's arrays;
+    every failing limit gives F3S_ERR_OUT_OF_MEMORY and leaks nothing."""
+    L = gpu.load_library()
+    c = W.make_config(4, with_features=False)
+    rp, ci, N = _dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"]
+    seg = np.ascontiguousarray(c["seg_ptr"], dtype=np.int32)
+    sp = seg.ctypes.data_as(ctypes.c_void_p)
+    failures = 0
+    for lim in (0, 1 << 20, 2 << 20, 4 << 20, 1 << 30):
+        monkeypatch.setenv("F3S_ALLOC_LIMIT_BYTES", str(lim))
+        res = []
+
+        def call():
+            h = L.f3s_plan_segments(rp.data_ptr(), ci.data_ptr(), N, sp, seg.size - 1)
+            res.append(bool(h))
+            if h:
+                L.f3s_destroy(h)
+            else:
+                assert L.f3s_last_error() == F3S_ERR_OUT_OF_MEMORY, lim
+        _no_leak(call)
+        failures += not res[0]
+        print(f"  limit {lim}: plan {'built' if res[0] else 'out of memory'}", flush=True)
+    assert failures >= 2 and res[-1]
