@@ -323,6 +323,28 @@ def test_gradients_random_segmentations(gpu, oracle, seed):
                1 / math.sqrt(d))
 
 
+@pytest.mark.parametrize("order", ["item", "head"])
+def test_molecule_batch_gradients_two_heads(gpu, oracle, order, monkeypatch):
+    """Two heads sharing the aligned plan and its plan of A^T, in both head
+    orders; each head's gradients against the oracle."""
+    monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0" if order == "head" else str(1 << 40))
+    c = W.make_config(4, with_features=False)
+    N, H, d = c["N"], 2, 64
+    rng = np.random.default_rng(54)
+    Q, K, V, G = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(4))
+    plan = _segment_plan(gpu, c["row_ptr"], c["col_idx"], N, c["seg_ptr"])
+    plan_t = plan.transpose()
+    q, k, v, g = (_dev(x) for x in (Q, K, V, G))
+    O, lse = gpu.forward(plan, q, k, v, scale=0.125)
+    dQ, dK, dV = gpu.backward(plan, plan_t, q, k, v, O, g, lse, scale=0.125)
+    torch.cuda.synchronize()
+    for h in range(H):
+        ref = oracle.attention_bwd_f64(c["row_ptr"], c["col_idx"], Q[:, h], K[:, h],
+                                       V[:, h], G[:, h], 0.125)
+        for name, got, r in zip(("dQ", "dK", "dV"), (dQ, dK, dV), ref):
+            _check_grad(f"{name}[h{h}]", got.cpu().numpy()[:, h], r)
+
+
 def test_molecule_batch_gradients_bf16(gpu, oracle):
     c = W.make_config(4, dtype="bf16")
     G = W.to_bf16_bits(np.random.default_rng(53).standard_normal(c["Q"].shape,
