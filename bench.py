@@ -220,7 +220,10 @@ def gather_sweep(dev, reps=10):
     256-byte rows, 1 to 16 rows in flight per thread and 2, 4 or 8 workgroups
     of 256 threads per CU (about 256 MB read per call, one HIP graph of
     `reps` calls each): what the memory system delivers to random row
-    gathers, and whether more requests in flight raise it."""
+    gathers, and whether more requests in flight raise it.  Then, at the
+    ceilings' launch shape (8 rows in flight, 2,048 workgroups), rows of 128
+    to 1024 bytes: whether longer contiguous rows (a K row and a V row side
+    by side) are gathered at a higher byte rate."""
     import torch
     import paper_2505_08098_amd as f3s
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
@@ -242,8 +245,18 @@ def gather_sweep(dev, reps=10):
                                  "in_flight": u,
                                  "GBs": round(wg * rounds * u * 4096 / ms / 1e6, 1)})
         print(f"gather sweep: {mb} MB done", file=sys.stderr, flush=True)
+    by_size = []
+    for mb in GATHER_SWEEP_MB:
+        for rb in (128, 256, 512, 1024):
+            n = (mb << 20) // rb
+            call = lambda: f3s.probe_rows(buf, n, rb, sink, in_flight=8, workgroups=2048,
+                                          rounds=4)
+            ms = graph_timed(call, reps, dev)[1]
+            by_size.append({"table_MB": mb, "row_bytes": rb,
+                            "GBs": round(2048 * 4 * 8 * 4096 / ms / 1e6, 1)})
+    print("gather sweep: row sizes done", file=sys.stderr, flush=True)
     print(json.dumps({"metric": "random whole-row gather rate (f3s_probe_rows)", "n_gpus": 1,
-                      "cus": cus, "rows": rows}), flush=True)
+                      "cus": cus, "rows": rows, "row_sizes": by_size}), flush=True)
 
 
 def dram_check(args, stream, dev, reps=10):
