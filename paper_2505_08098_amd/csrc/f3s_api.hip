@@ -216,15 +216,15 @@ U *carve(Arena &a, bool take, int64_t n)
     return nullptr;
 }
 
-// Lays out the build's scratch for T windows and nnz CSR entries (and the
-// windows' first rows if `rows`): sizes into a (take == false) or pointers
-// out of it (take == true), in one order.  O(nnz + T) bytes.
 // Row windows of an N-row pattern (64-bit sum: N may be up to 2^31 - 1).
 int32_t num_windows(int32_t N)
 {
     return (int32_t)(((int64_t)N + f3s::kWindowRows - 1) / f3s::kWindowRows);
 }
 
+// Lays out the build's scratch for T windows and nnz CSR entries (and the
+// windows' first rows if `rows`): sizes into a (take == false) or pointers
+// out of it (take == true), in one order.  O(nnz + T) bytes.
 void carve_scratch(Arena &a, bool take, BuildScratch &b, int32_t T, int64_t nnz,
                    bool rows = false)
 {
