@@ -176,13 +176,16 @@ f3s_status_t f3s_run(f3s_plan_t plan, const void *Q, const void *K, const void *
  * is the single-head operator applied to head h of Q, K, V.  Same pointer,
  * alignment, d, scale and stream rules as f3s_run; n_heads >= 1 and
  * n_items * n_heads < 2^31.  f3s_run is f3s_run_mh with n_heads = 1.
- * All heads run in one launch: window-major while K and V (all heads) fit
- * the 256 MB Infinity Cache, head by head above it (environment
- * F3S_HEAD_MAJOR_BYTES=<bytes> moves that threshold; results are identical
+ * All heads run in one launch: head by head when K and V (all heads)
+ * exceed the 256 MB Infinity Cache or the plan's windows are nearly uniform
+ * (then each XCD takes consecutive ranges of one head's work list at a
+ * time), window-major otherwise (environment F3S_HEAD_MAJOR_BYTES=<bytes>
+ * replaces both tests with a K/V size threshold; results are identical
  * either way).  When a launch would have fewer waves than the GPU has SIMDs
- * (work items x heads < 1024) four waves share each work item and combine
- * their partial softmax states (environment F3S_WAVES_PER_ITEM=1 or 4
- * forces one or the other; the rounding of the combination differs).
+ * (work items x heads < 1024) four waves share each work item, and two when
+ * twice the waves still fit the GPU at once; they combine their partial
+ * softmax states (environment F3S_WAVES_PER_ITEM=1, 2 or 4 forces the
+ * count; the rounding of the combination differs).
  */
 f3s_status_t f3s_run_mh(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                         void *O, int32_t n_heads, int32_t d, float scale,

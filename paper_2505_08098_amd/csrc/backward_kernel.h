@@ -146,7 +146,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
     // window-major, or head by head when K and V exceed the caches (as in
     // the forward)
     const int n_it = gridDim.x / nh;
-    const int wg = workgroup_position(order);
+    const int wg = workgroup_position(order, nh);
     const int hl = (order & kOrderHead) ? wg / n_it : wg % nh;
     const int item = (order & kOrderHead) ? wg - hl * n_it : wg / nh;
     const int head = h0 + hl, H = ld / D;
@@ -341,7 +341,7 @@ __attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dkdv(
     // window-major, or head by head when K and V exceed the caches (as in
     // the forward)
     const int n_it = gridDim.x / nh;
-    const int wg = workgroup_position(order);
+    const int wg = workgroup_position(order, nh);
     const int hl = (order & kOrderHead) ? wg / n_it : wg % nh;
     const int item = (order & kOrderHead) ? wg - hl * n_it : wg / nh;
     const int head = h0 + hl, H = ld / D;
@@ -578,11 +578,13 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     const auto *v = static_cast<const _Float16 *>(V);
     const auto *gr = static_cast<const _Float16 *>(G);
     hipError_t e = hipSuccess;
-    const bool head_major = H > 1 && 2ull * p.N * ld * 2 > head_major_threshold();
-    const uint32_t order_a =
-        (head_major ? kOrderHead : 0u) | (xcd_chunks(p, H) ? kOrderXcd : 0u);
-    const uint32_t order_t =
-        (head_major ? kOrderHead : 0u) | (xcd_chunks(pt, H) ? kOrderXcd : 0u);
+    // launch order of a group of nh heads over plan q
+    const uint64_t kv_bytes = 2ull * p.N * ld * 2;
+    auto order_of = [kv_bytes](const f3s_plan_s &q, int32_t nh) -> uint32_t {
+        const bool head_major = head_major_order(q, nh, kv_bytes);
+        return (head_major ? kOrderHead : 0u) |
+               (xcd_chunks(q, nh, head_major) ? kOrderXcd : 0u);
+    };
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
         const int nw = waves_per_item(p.n_blocks, p.n_items, H,
@@ -597,7 +599,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (p.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)p.n_items * nh), 64 * nw, 0, s>>>(
                     p.items, p.cols, p.mask, p.win_row, q, k, v, gr, O, lse, stats, dQ,
-                    p.part_o, p.N, ld, h0, nh, sl2, scale, order_a);
+                    p.part_o, p.N, ld, h0, nh, sl2, scale, order_of(p, nh));
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (p.n_split > 0) {
@@ -626,7 +628,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
             if (pt.n_items > 0) {
                 kern<<<(unsigned)((uint64_t)pt.n_items * nh), 64 * nw, 0, s>>>(
                     pt.items, pt.cols, pt.mask, q, k, v, gr, stats, dK, dV, pt.part_o,
-                    pt.N, ld, h0, nh, sl2, scale, order_t);
+                    pt.N, ld, h0, nh, sl2, scale, order_of(pt, nh));
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (pt.n_split > 0) {

@@ -73,39 +73,53 @@ struct f3s_plan_s {
 namespace f3s {
 
 // ---- plan kernels (plan_kernels.hip) ------------------------------------
-// K and V bytes (all heads) above which a launch over several heads runs
-// head by head instead of window-major: the 256 MB Infinity Cache;
-// F3S_HEAD_MAJOR_BYTES overrides it (read at launch).
-inline uint64_t head_major_threshold()
-{
-    const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
-    return e && *e ? (uint64_t)strtoull(e, nullptr, 10) : (uint64_t)256 << 20;
-}
 // Workgroup order flags of the fused kernels: heads outermost (one pass over
 // the work list per head), and consecutive ranges of the order per XCD.
 constexpr uint32_t kOrderHead = 1u;
 constexpr uint32_t kOrderXcd = 2u;
 // Plans whose windows are nearly uniform: at least 2048 windows, the largest
 // holding at most twice the mean block count.  Their work list keeps window
-// order (heavy-first sorting has nothing to balance) and the forward gives
-// each XCD a consecutive range of it.
+// order (heavy-first sorting has nothing to balance), and launches of 1, 2,
+// 4 or 8 heads give each XCD a consecutive range of it.
 inline bool uniform_windows(int64_t windows, int64_t blocks, int64_t max_blocks)
 {
     return windows >= 2048 && max_blocks * windows <= 2 * blocks;
 }
-// Whether a launch of `heads` heads over plan p gives each XCD a consecutive
-// range of the work list: for one head over a nearly uniform plan (no XCD's
-// range is then much heavier than another's).  With its window-order work
-// list the molecule batch ran 18.8 -> 15.6 us forward and 52.8 -> 45.0 us
-// backward; on skewed plans the ranges would give the heaviest items to one
-// XCD (1.7x slower on the million-node graph), and with four heads of the
-// sequence workload they measured 45% slower (unexplained), so several heads
-// keep round-robin.  F3S_XCD_CHUNKS=0 or 1 forces it (read at launch).
-inline bool xcd_chunks(const f3s_plan_s &p, int32_t heads)
+// Whether a launch of nh > 1 heads over plan p, whose K and V (all heads)
+// hold kv_bytes, runs head by head instead of window-major: when K and V
+// exceed the 256 MB Infinity Cache (each head's gathers then stream like a
+// single head's), and for nearly uniform plans, whose XCD ranges then hold
+// one head's rows at a time (measured with 3, 4 and 8 heads: 5-28% faster
+// than window-major on the molecule batch and the sequence workload, equal
+// with 2).  F3S_HEAD_MAJOR_BYTES=<bytes>, when set, replaces both tests with
+// kv_bytes > bytes (read at launch).
+inline bool head_major_order(const f3s_plan_s &p, int32_t nh, uint64_t kv_bytes)
 {
+    if (nh <= 1) return false;
+    const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
+    if (e && *e) return kv_bytes > (uint64_t)strtoull(e, nullptr, 10);
+    return kv_bytes > ((uint64_t)256 << 20) ||
+           uniform_windows(p.n_items, p.n_blocks, p.max_blocks);
+}
+// Whether a launch of `heads` heads over plan p gives each XCD consecutive
+// ranges of the work list (see workgroup_position): for nearly uniform plans
+// (no XCD's range is then much heavier than another's), window-major with
+// 1, 2, 4 or 8 heads, head-major with any.  With its window-order work list
+// the molecule batch ran 18.8 -> 15.6 us forward and 52.8 -> 45.0 us
+// backward with one head, 33.7 -> 26.4 us forward with two.  On skewed plans
+// the ranges would give the heaviest items to one XCD (1.7x slower on the
+// million-node graph).  Window-major ranges over all heads of a window would
+// give every XCD the rows of every head, where round-robin order with 2, 4
+// or 8 heads leaves each XCD one head (b mod 8 fixes b mod heads): that
+// measured 45% slower with four heads of the sequence workload, so other
+// head counts keep round-robin there.  F3S_XCD_CHUNKS=0 or 1 forces the
+// choice where the ranges apply (read at launch).
+inline bool xcd_chunks(const f3s_plan_s &p, int32_t heads, bool head_major = false)
+{
+    if (heads < 1 || (!head_major && 8 % heads != 0)) return false;
     const char *e = getenv("F3S_XCD_CHUNKS");
     if (e && *e) return atoi(e) != 0;
-    return heads == 1 && uniform_windows(p.n_items, p.n_blocks, p.max_blocks);
+    return uniform_windows(p.n_items, p.n_blocks, p.max_blocks);
 }
 // Waves sharing one work item (forward and backward): 4 when a launch would
 // have fewer waves than the GPU has SIMDs (items x heads < 1024) and the

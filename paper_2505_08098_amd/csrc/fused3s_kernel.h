@@ -208,7 +208,7 @@ __attribute__((amdgpu_waves_per_eu(waves_per_simd<D, kIn, kNarrow>(), 8))) void 
     // K and V rows while those stay cached) or head-major (one pass over the
     // list per head: with K and V far larger than the caches each head's
     // gathers then stream like a single head's).
-    const int wg = workgroup_position(order);
+    const int wg = workgroup_position(order, nh);
     int item, hl;
     if (order & kOrderHead) {
         const int n_it = gridDim.x / nh;
@@ -667,9 +667,9 @@ hipError_t launch_d(const f3s_plan_s &p, const void *Q, const void *K,
             const uint64_t grid = (uint64_t)p.n_items * nh;
             if (grid > 0x7FFFFFFFull) return hipErrorInvalidConfiguration;
             const bool head_major =
-                nh > 1 && 2ull * p.N * ld * elem_bytes<kIn>() > head_major_threshold();
-            const uint32_t order =
-                (head_major ? kOrderHead : 0u) | (xcd_chunks(p, H) ? kOrderXcd : 0u);
+                head_major_order(p, nh, 2ull * p.N * ld * elem_bytes<kIn>());
+            const uint32_t order = (head_major ? kOrderHead : 0u) |
+                                   (xcd_chunks(p, nh, head_major) ? kOrderXcd : 0u);
             kern<<<(unsigned)grid, 64 * nw, 0, s>>>(p.items, p.cols, p.mask, p.win_row, Q, K,
                                                V, O, p.part_o, p.part_ml, lse, p.N, ld, h0,
                                                nh, sl2, order, trace);

@@ -91,19 +91,35 @@ __device__ __forceinline__ void tile_fence()
     }
 }
 
-// Position of this workgroup in the launch order.  With kOrderXcd the order
-// is cut into 8 consecutive ranges, one per XCD: workgroups reach the 8 XCDs
-// round-robin (workgroup b on XCD b mod 8), so workgroup b takes position
-// (its XCD's first position) + b / 8, and neighbouring windows -- which share
-// K/V rows on banded and block-diagonal patterns -- meet in one XCD's L2.
-__device__ __forceinline__ int workgroup_position(uint32_t order)
+// Position of this workgroup in the launch order: window-major (item * nh
+// + head) or, with kOrderHead, head-major (head * items + item).
+// Workgroups reach the 8 XCDs round-robin (workgroup b on XCD b mod 8).
+// With kOrderXcd the XCDs cut a work list into consecutive ranges, so that
+// neighbouring windows -- which share K/V rows on banded and block-diagonal
+// patterns -- meet in one XCD's L2:
+// - window-major with nh dividing 8: XCD x serves head x mod nh only, and the
+//   8 / nh XCDs of a head split its list: XCD x takes items (its range's
+//   first) + b / 8;
+// - head-major (any nh): the heads' lists follow one another in launch
+//   order, and within head h's list the workgroup with index t = b - h *
+//   items takes item (range t mod 8's first) + t / 8: whatever XCD t mod 8
+//   maps to for that head, each XCD walks one consecutive range per head.
+// Each range gets exactly as many workgroups as it holds items, so the map is
+// one-to-one.
+__device__ __forceinline__ int workgroup_position(uint32_t order, int nh)
 {
     int wg = (int)blockIdx.x;
-    if (order & kOrderXcd) {
-        const int G = (int)gridDim.x, q = G >> 3, r = G & 7, x = wg & 7;
-        wg = x * q + min(x, r) + (wg >> 3);
+    if (!(order & kOrderXcd) || nh < 1) return wg;
+    const int n_it = (int)gridDim.x / nh;
+    if (order & kOrderHead) {
+        const int h = wg / n_it, t = wg - h * n_it;
+        const int q = n_it >> 3, r = n_it & 7, y = t & 7;
+        return h * n_it + y * q + min(y, r) + (t >> 3);
     }
-    return wg;
+    if (8 % nh != 0) return wg;
+    const int x = wg & 7, per = 8 / nh, h = x % nh, k = x / nh;
+    const int q = n_it / per, r = n_it % per;
+    return (k * q + min(k, r) + (wg >> 3)) * nh + h;
 }
 
 __device__ __forceinline__ h8 cat44(h4 lo, h4 hi)

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256) void k_probe_gather(
     constexpr int LPR = D / 8;   // 16-byte chunks per row
     constexpr int NI = D / 16;   // chunks per lane per 32-row tile
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const f3s::WorkItem it = items[f3s::workgroup_position(order)];
+    const f3s::WorkItem it = items[f3s::workgroup_position(order, 1)];
     int32_t r0, nr;
     f3s::window_rows(win_row, N, it.window, &r0, &nr);
     uint32_t acc = 0;

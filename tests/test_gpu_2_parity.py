@@ -309,13 +309,12 @@ def test_binding_rejects_wrong_out_and_lse_before_launch(gpu):
 
 
 def _head_order(monkeypatch, order):
-    """Workgroup order of several heads: item-major below the K/V size
-    threshold (the default for these small inputs), head-major above it
-    (forced with a threshold of 0)."""
+    """Workgroup order of several heads, forced either way: item-major (a
+    K/V size threshold no input reaches) or head-major (a threshold of 0)."""
     if order == "head":
         monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0")
     else:
-        monkeypatch.delenv("F3S_HEAD_MAJOR_BYTES", raising=False)
+        monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", str(1 << 40))
 
 
 @pytest.mark.parametrize("order", ["item", "head"])
@@ -337,7 +336,7 @@ def test_multi_head_matches_oracle_per_head(gpu, oracle, H, d, order, monkeypatc
         _assert_parity(O[:, h], ref)
 
 
-@pytest.mark.parametrize("k,H", [(2, 4), (5, 4), (3, 2)])
+@pytest.mark.parametrize("k,H", [(2, 4), (5, 4), (3, 2), (4, 2), (4, 4), (5, 8)])
 def test_multi_head_workloads(gpu, oracle, k, H):
     """Several heads over a workload graph (fresh seeded N(0,1) features of
     shape [N, H, d]); each head against the oracle, on every row for the
@@ -393,12 +392,14 @@ def test_workloads_at_other_feature_sizes(gpu, oracle, k, d):
         _assert_parity(O, oracle.attention_f64(rp, ci, c["Q"], c["K"], c["V"], c["scale"]))
 
 
-@pytest.mark.parametrize("k,H", [(5, 1), (2, 3), (4, 1)])
+@pytest.mark.parametrize("k,H", [(5, 1), (2, 3), (4, 1), (4, 2), (2, 4), (5, 8), (4, 3)])
 def test_xcd_ranges_order_gives_identical_results(gpu, k, H, monkeypatch):
-    """Each XCD taking a consecutive range of the work list (workgroup b at
-    position (b mod 8)'s first + b / 8) only reorders independent work items:
-    O and lse are bit-identical to the round-robin order, with split windows
-    and several heads in both head orders."""
+    """Each XCD taking a consecutive range of the work list (with 2, 4 or 8
+    heads, of one head's list) only reorders independent work items: O and
+    lse are bit-identical to the round-robin order, with split windows (a
+    merge launch follows) and several heads in both head orders (window-major
+    with 3 heads keeps round-robin order; head by head takes ranges of each
+    head's list with any head count)."""
     c = W.make_config(k, with_features=False)
     N, d = c["N"], W.WORKLOADS[k]["d"]
     rng = np.random.default_rng(60 + k)

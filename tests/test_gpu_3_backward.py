@@ -312,7 +312,7 @@ def test_gradients_split_windows_and_heads(gpu, oracle, monkeypatch, H, d, order
     if order == "head":
         monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0")
     else:
-        monkeypatch.delenv("F3S_HEAD_MAJOR_BYTES", raising=False)
+        monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", str(1 << 40))
     monkeypatch.setenv("F3S_WAVES_PER_ITEM", waves)
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
     rng = np.random.default_rng(12)
@@ -369,24 +369,31 @@ def test_gradients_million_node_workload_sampled(gpu, oracle, dtype, d):
     plan_t.close()
 
 
-@pytest.mark.parametrize("k", [5, 4, 2])
-def test_backward_xcd_ranges_order_gives_identical_gradients(gpu, k, monkeypatch):
-    """Each XCD taking a consecutive range of the work list only reorders
+@pytest.mark.parametrize("k,H", [(5, 1), (4, 1), (2, 1), (4, 4), (2, 2)])
+def test_backward_xcd_ranges_order_gives_identical_gradients(gpu, k, H, monkeypatch):
+    """Each XCD taking a consecutive range of the work list (with several
+    heads, of one head's list, window-major or head by head) only reorders
     independent work items of both passes: bit-identical gradients."""
     c = W.make_config(k)
     rng = np.random.default_rng(70 + k)
     plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
     plan_t = plan.transpose()
-    q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
-    g = _dev(rng.standard_normal(c["Q"].shape).astype(np.float16))
+    if H == 1:
+        q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
+    else:
+        shape = (c["N"], H, c["Q"].shape[1])
+        q, kk, v = (_dev(rng.standard_normal(shape).astype(np.float16)) for _ in range(3))
+    g = _dev(rng.standard_normal(tuple(q.shape)).astype(np.float16))
     O, lse = gpu.forward(plan, q, kk, v, scale=c["scale"])
-    outs = []
-    for chunks in ("0", "1"):
-        monkeypatch.setenv("F3S_XCD_CHUNKS", chunks)
-        outs.append(gpu.backward(plan, plan_t, q, kk, v, O, g, lse, scale=c["scale"]))
-    torch.cuda.synchronize()
-    for a, b in zip(*outs):
-        assert torch.equal(a, b)
+    for head_major in ("0", "1000000000000"):
+        monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", head_major)
+        outs = []
+        for chunks in ("0", "1"):
+            monkeypatch.setenv("F3S_XCD_CHUNKS", chunks)
+            outs.append(gpu.backward(plan, plan_t, q, kk, v, O, g, lse, scale=c["scale"]))
+        torch.cuda.synchronize()
+        for a, b in zip(*outs):
+            assert torch.equal(a, b)
 
 
 def test_backward_is_deterministic(gpu):
