@@ -86,9 +86,9 @@ typedef struct {
  *                              =0 always sorts.  Unset, plans of nearly
  *                              uniform windows (at least 2048, the largest
  *                              at most twice the mean block count) keep
- *                              window order, which lets the forward give
- *                              each XCD a run of neighbouring windows;
- *                              all others are sorted
+ *                              window order, which lets the forward and
+ *                              backward give each XCD runs of
+ *                              neighbouring windows; all others are sorted
  *   F3S_NARROW_GATHER=1        the fp16 -> fp32 forward gathers K and V rows
  *                              in 4-byte words instead of 16-byte chunks (the
  *                              access granularity without the register
