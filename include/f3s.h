@@ -177,11 +177,11 @@ f3s_status_t f3s_run(f3s_plan_t plan, const void *Q, const void *K, const void *
  * alignment, d, scale and stream rules as f3s_run; n_heads >= 1 and
  * n_items * n_heads < 2^31.  f3s_run is f3s_run_mh with n_heads = 1.
  * All heads run in one launch: head by head when K and V (all heads)
- * exceed the 256 MB Infinity Cache or the plan's windows are nearly uniform
- * (then each XCD takes consecutive ranges of one head's work list at a
- * time), window-major otherwise (environment F3S_HEAD_MAJOR_BYTES=<bytes>
- * replaces both tests with a K/V size threshold; results are identical
- * either way).  When a launch would have fewer waves than the GPU has SIMDs
+ * exceed the 256 MB Infinity Cache, when n_heads does not divide 8, or when
+ * the plan's windows are nearly uniform (then each XCD takes consecutive
+ * ranges of one head's work list at a time), window-major otherwise
+ * (environment F3S_HEAD_MAJOR_BYTES=<bytes> replaces these tests with a K/V
+ * size threshold; results are identical either way).  When a launch would have fewer waves than the GPU has SIMDs
  * (work items x heads < 1024) four waves share each work item, and two when
  * twice the waves still fit the GPU at once; they combine their partial
  * softmax states (environment F3S_WAVES_PER_ITEM=1, 2 or 4 forces the

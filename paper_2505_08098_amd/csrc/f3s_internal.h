@@ -86,19 +86,28 @@ inline bool uniform_windows(int64_t windows, int64_t blocks, int64_t max_blocks)
     return windows >= 2048 && max_blocks * windows <= 2 * blocks;
 }
 // Whether a launch of nh > 1 heads over plan p, whose K and V (all heads)
-// hold kv_bytes, runs head by head instead of window-major: when K and V
-// exceed the 256 MB Infinity Cache (each head's gathers then stream like a
-// single head's), and for nearly uniform plans, whose XCD ranges then hold
-// one head's rows at a time (measured with 3, 4 and 8 heads: 5-28% faster
-// than window-major on the molecule batch and the sequence workload, equal
-// with 2).  F3S_HEAD_MAJOR_BYTES=<bytes>, when set, replaces both tests with
-// kv_bytes > bytes (read at launch).
+// hold kv_bytes, runs head by head instead of window-major (item * nh +
+// head).  Window-major order shares a window's column lists and bitmaps
+// among its heads, and with nh = 2, 4 or 8 round-robin dispatch still leaves
+// each XCD one head (b mod 8 fixes b mod nh).  Head by head wins
+// - when K and V exceed the 256 MB Infinity Cache: each head's gathers then
+//   stream like a single head's;
+// - when nh does not divide 8: window-major order then gives every XCD the
+//   rows of every head (hub-heavy Chung-Lu graph, 3 heads: 97.1 -> 88.7 us
+//   forward, 245.7 -> 226.7 us backward);
+// - on nearly uniform plans, whose XCD ranges then hold one head's rows at a
+//   time (3, 4 and 8 heads: 5-28% faster on the molecule batch and the
+//   sequence workload; equal with 2).
+// Window-major stays for skewed plans with 2, 4 or 8 heads (hub-heavy graph,
+// 4 heads: 108.6 against 113.8 us head by head).  F3S_HEAD_MAJOR_BYTES=
+// <bytes>, when set, replaces all three tests with kv_bytes > bytes (read at
+// launch).
 inline bool head_major_order(const f3s_plan_s &p, int32_t nh, uint64_t kv_bytes)
 {
     if (nh <= 1) return false;
     const char *e = getenv("F3S_HEAD_MAJOR_BYTES");
     if (e && *e) return kv_bytes > (uint64_t)strtoull(e, nullptr, 10);
-    return kv_bytes > ((uint64_t)256 << 20) ||
+    return kv_bytes > ((uint64_t)256 << 20) || 8 % nh != 0 ||
            uniform_windows(p.n_items, p.n_blocks, p.max_blocks);
 }
 // Whether a launch of `heads` heads over plan p gives each XCD consecutive
