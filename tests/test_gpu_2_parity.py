@@ -392,7 +392,8 @@ def test_workloads_at_other_feature_sizes(gpu, oracle, k, d):
         _assert_parity(O, oracle.attention_f64(rp, ci, c["Q"], c["K"], c["V"], c["scale"]))
 
 
-@pytest.mark.parametrize("k,H", [(5, 1), (2, 3), (4, 1), (4, 2), (2, 4), (5, 8), (4, 3)])
+@pytest.mark.parametrize("k,H", [(5, 1), (2, 3), (4, 1), (4, 2), (2, 4), (5, 8), (4, 3),
+                                 (5, 6), (1, 16)])
 def test_xcd_ranges_order_gives_identical_results(gpu, k, H, monkeypatch):
     """Each XCD taking a consecutive range of the work list (with 2, 4 or 8
     heads, of one head's list) only reorders independent work items: O and
