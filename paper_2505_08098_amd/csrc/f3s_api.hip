@@ -368,10 +368,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     // keeps neighbouring windows -- which share K/V rows on banded and
     // block-diagonal patterns -- next to each other in the work list, which
     // the forward hands to each XCD as one consecutive range.
-    if (reorder && !order_forced && uniform_windows(T, B, hs.max_blocks)) {
-        HIP_TRY(hipMemsetAsync(key, 0, sizeof(int32_t) * (size_t)T, s));
-        p->flags |= 1;
-    }
+    if (reorder && !order_forced && uniform_windows(T, B, hs.max_blocks)) p->flags |= 1;
+    const bool window_order = (p->flags & 1) != 0;
 
     // ---- 4. the plan's arrays: one allocation, plus the partial buffers --
     HIP_TRY(alloc_store(p, nullptr));
@@ -385,9 +383,11 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     HIP_TRY(launch_fill_windows(row_ptr, wr, T, tmp_cols, tmp_mask, u, p->blk_off, p->cols,
                                 p->mask, s));
 
-    // ---- 6. heavy-first work list: stable sort of the windows by key ------
+    // ---- 6. work list: windows stably sorted by key, heavy first (or kept
+    //         in window order) ----------------------------------------------
     HIP_TRY(launch_worklist(key, nb, p->blk_off, npieces, split_pieces, split_one, T, piece,
-                            b.wl, p->items, p->merges, split_item, &st->n_items, s));
+                            window_order, b.wl, p->items, p->merges, split_item,
+                            &st->n_items, s));
     HIP_TRY(launch_split_items(p->merges, split_item, p->blk_off, p->n_split, p->items, s));
 
     // ---- 7. integrity check of the finished plan ------------------------

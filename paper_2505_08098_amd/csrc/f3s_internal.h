@@ -274,12 +274,15 @@ struct WorkListScratch {
 };
 // Heavy-first work list from the keys of launch_bin_keys: whole windows as
 // items, split windows as merge records plus split_item (their pieces:
-// launch_split_items); the item count goes to *n_items_out.
+// launch_split_items); the item count goes to *n_items_out.  window_order:
+// the list keeps window order (what the stable sort gives when every key
+// is equal), so key is not read and no sort is launched.
 hipError_t launch_worklist(const int32_t *key, const int32_t *nb, const int32_t *blk_off,
                            const int32_t *npieces, const int32_t *slot_base,
                            const int32_t *split_idx, int32_t T, int32_t piece,
-                           const WorkListScratch &ws, WorkItem *items, int32_t *merges,
-                           int32_t *split_item, int32_t *n_items_out, hipStream_t s);
+                           bool window_order, const WorkListScratch &ws, WorkItem *items,
+                           int32_t *merges, int32_t *split_item, int32_t *n_items_out,
+                           hipStream_t s);
 
 // ---- transposed pattern (transpose.hip) ----------------------------------
 // CSR of A^T (rp[N+1], ci[nnz], each row in increasing column order) from a

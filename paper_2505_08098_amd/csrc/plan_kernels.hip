@@ -686,6 +686,9 @@ __global__ __launch_bounds__(kStatThreads) void k_window_stats(
 constexpr int kScanThreads = 1024;
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanThreads * kScanItems;
+// Up to this many elements one workgroup scans them in one launch, 16 per
+// thread (a second launch costs more than the longer tile).
+constexpr int kScanOneLaunch = kScanThreads * 16;
 // Up to this many elements the tile totals fit one workgroup's threads.
 constexpr int64_t kScanTwoPass = (int64_t)kScanTile * kScanThreads;
 
@@ -953,9 +956,10 @@ hipError_t launch_window_stats(const int32_t *u, const int32_t *bits, int32_t T,
     return hipGetLastError();
 }
 
-// Up to one tile: one launch of one workgroup.  Up to kScanTwoPass: the
-// tile totals, then every tile scanned with the sum of the totals before it
-// (two launches).  Above: the tile totals, their own scan, then the tiles.
+// Up to kScanOneLaunch elements: one launch of one workgroup.  Up to
+// kScanTwoPass: the tile totals, then every tile scanned with the sum of the
+// totals before it (two launches).  Above: the tile totals, their own scan,
+// then the tiles.
 int64_t scan_tmp_ints(int64_t n)
 {
     const int64_t ntiles = (n + kScanTile - 1) / kScanTile;
@@ -972,6 +976,9 @@ hipError_t launch_scan_pair(ScanArray a0, ScanArray a1, int arrays, int32_t n,
         k_scan<1, kCarryNone><<<dim3(1, arrays), kScanThreads, 0, s>>>(a0, a1, n);
     } else if (n <= kScanTile) {
         k_scan<kScanItems, kCarryNone><<<dim3(1, arrays), kScanThreads, 0, s>>>(a0, a1, n);
+    } else if (n <= kScanOneLaunch) {
+        k_scan<kScanOneLaunch / kScanThreads, kCarryNone>
+            <<<dim3(1, arrays), kScanThreads, 0, s>>>(a0, a1, n);
     } else {
         k_scan_reduce<<<dim3(ntiles, arrays), kScanThreads, 0, s>>>(a0, a1, n);
         hipError_t e = hipGetLastError();

@@ -8,7 +8,7 @@
 namespace f3s {
 namespace {
 
-// Window order[i] starts at item pos[i].
+// Window order[i] (window i without an order) starts at item pos[i].
 __global__ void k_place_items(const int32_t *order, const int32_t *pos, const int32_t *nb,
                               const int32_t *blk_off, const int32_t *npieces,
                               const int32_t *slot_base, const int32_t *split_idx, int32_t T,
@@ -17,7 +17,7 @@ __global__ void k_place_items(const int32_t *order, const int32_t *pos, const in
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= T) return;
-    const int w = order[i], p = pos[i];
+    const int w = order ? order[i] : i, p = pos[i];
     const int n = nb[w], b0 = blk_off[w];
     if (n <= piece) {
         items[p] = WorkItem{w, b0, b0 + n, -1};
@@ -40,15 +40,19 @@ inline unsigned blocks_for(int64_t n, int threads)
 hipError_t launch_worklist(const int32_t *key, const int32_t *nb, const int32_t *blk_off,
                            const int32_t *npieces, const int32_t *slot_base,
                            const int32_t *split_idx, int32_t T, int32_t piece,
-                           const WorkListScratch &ws, WorkItem *items, int32_t *merges,
-                           int32_t *split_item, int32_t *n_items_out, hipStream_t s)
+                           bool window_order, const WorkListScratch &ws, WorkItem *items,
+                           int32_t *merges, int32_t *split_item, int32_t *n_items_out,
+                           hipStream_t s)
 {
     if (T == 0) return hipSuccess;
     // the window indices, sorted by key (values: the indices themselves)
     const int32_t *sorted_keys = nullptr, *order = nullptr;
-    hipError_t e = launch_radix_pairs(key, nullptr, T, piece, true, ws.radix, &sorted_keys,
-                                      &order, s);
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    if (!window_order) {
+        e = launch_radix_pairs(key, nullptr, T, piece, true, ws.radix, &sorted_keys, &order,
+                               s);
+        if (e != hipSuccess) return e;
+    }
     // first item of each window in that order: scan of its item counts
     ScanArray a;
     a.in = npieces;
