@@ -70,7 +70,8 @@ typedef struct {
                               chosen for nearly uniform windows; see f3s_plan);
                               bit 1: narrow K/V gathers (ablation);
                               bit 2: windows aligned to the graphs of a batch
-                              (f3s_plan_segments)                               */
+                              (f3s_plan_segments);
+                              bit 3: split-row forward (ablation)                */
     int64_t bsb_bytes;     /* window offsets + column lists + bitmaps            */
     int64_t device_bytes;  /* everything the plan holds on the device            */
     double build_ms;       /* wall time of f3s_plan                              */
@@ -94,6 +95,15 @@ typedef struct {
  *                              access granularity without the register
  *                              remapping of Section 3.4); other type pairs
  *                              then return F3S_ERR_UNSUPPORTED
+ *   F3S_SPLIT_ROW=1            the fp16 -> fp32 forward partitions each
+ *                              window among 2 or 4 waves by feature slices
+ *                              (split-row score product summed through LDS
+ *                              once per block pair, split-column value
+ *                              product; Section 3.3) instead of by block
+ *                              pairs; d must be a multiple of 64 and Q/K/V
+ *                              below 4 GiB, and other type pairs, other d
+ *                              or F3S_NARROW_GATHER=1 together with it
+ *                              return F3S_ERR_UNSUPPORTED
  *   row_ptr  int32[N+1], row_ptr[0] == 0, non-decreasing
  *   col_idx  int32[row_ptr[N]], every entry in [0, N); order inside a row is
  *            free and repeated entries count once (A is binary, Section 3.1)

@@ -336,7 +336,8 @@ f3s_status_t build_plan(f3s_plan_s *p, const int32_t *row_ptr, const int32_t *co
     const char *order_env = getenv("F3S_NO_REORDER");
     const bool order_forced = order_env && *order_env;
     const bool reorder = !order_forced || atoi(order_env) == 0;
-    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0) | (wr ? 4 : 0);
+    p->flags = (reorder ? 0 : 1) | (env_int("F3S_NARROW_GATHER", 0) ? 2 : 0) | (wr ? 4 : 0) |
+               (env_int("F3S_SPLIT_ROW", 0) ? 8 : 0);
     HIP_TRY(launch_bin_keys(nb, T, &st->n_blocks, &st->max_blocks,
                             env_int("F3S_PIECE_BLOCKS", 0), slots, reorder,
                             &st->piece, npieces, key, split_pieces, split_one, s));
@@ -800,8 +801,13 @@ f3s_status_t f3s_forward_typed(f3s_plan_t p, const void *Q, const void *K, const
         return fail(F3S_ERR_UNSUPPORTED);
     if (out_dtype != F3S_DTYPE_F32 && out_dtype != F3S_DTYPE_F16)
         return fail(F3S_ERR_UNSUPPORTED);
-    // the narrow-gather ablation exists for fp16 -> fp32 only
-    if ((p->flags & 2) && (in_dtype != F3S_DTYPE_F16 || out_dtype != F3S_DTYPE_F32))
+    // the narrow-gather ablation exists for fp16 -> fp32 only, the split-row
+    // one also only for d a multiple of 64 and 32-bit addressing; not both
+    if ((p->flags & 10) && (in_dtype != F3S_DTYPE_F16 || out_dtype != F3S_DTYPE_F32))
+        return fail(F3S_ERR_UNSUPPORTED);
+    if ((p->flags & 8) && ((p->flags & 2) || d % 64 != 0 ||
+                           (uint64_t)p->N * (uint64_t)n_heads * (uint64_t)d * 2u >
+                               0xFFFFFFF0ull))
         return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
@@ -916,7 +922,7 @@ f3s_status_t f3s_run_trace(f3s_plan_t p, const void *Q, const void *K, const voi
 {
     if (!p) return fail(F3S_ERR_INVALID_VALUE);
     if (d < 32 || d > f3s::kMaxD || d % 32 != 0) return fail(F3S_ERR_UNSUPPORTED);
-    if (p->flags & 2) return fail(F3S_ERR_UNSUPPORTED);
+    if (p->flags & 10) return fail(F3S_ERR_UNSUPPORTED);
     if (!isfinite(scale)) return fail(F3S_ERR_INVALID_VALUE);
     if (p->N == 0) return F3S_OK;
     if (!on_plan_device(p, stream)) return fail(F3S_ERR_INVALID_VALUE);

@@ -45,7 +45,8 @@ struct f3s_plan_s {
     int32_t n_split = 0;
     int32_t n_pieces = 0;
     int32_t flags = 0;           // bit 0: work list in window order; bit 1: narrow gathers;
-                                 // bit 2: windows aligned to the graphs of a batch
+                                 // bit 2: windows aligned to the graphs of a batch;
+                                 // bit 3: split-row forward (ablation)
     uint64_t id = 0;             // process-unique plan id
     uint64_t transpose_of = 0;   // id of the plan this one transposes (0: none)
     void *store = nullptr;       // one allocation: blk_off, cols, mask, items, merges
@@ -324,6 +325,11 @@ hipError_t launch_fused_trace(const f3s_plan_s &p, const void *Q, const void *K,
 hipError_t launch_fused_narrow(const f3s_plan_s &p, const void *Q, const void *K,
                                const void *V, void *O, float *lse, int32_t H, int32_t d,
                                float scale_log2, hipStream_t s);
+// Ablation: fp16 -> fp32 forward with the split-row partition of a window
+// among its waves (plan flag bit 3; d a multiple of 64, 32-bit addressing).
+hipError_t launch_fused_split_row(const f3s_plan_s &p, const void *Q, const void *K,
+                                  const void *V, float *O, float *lse, int32_t H, int32_t d,
+                                  float scale_log2, hipStream_t s);
 hipError_t launch_fused_fp8(const f3s_plan_s &p, const void *Q, const void *K,
                             const void *V, void *O, bool out_f16, float *lse, int32_t H,
                             int32_t d, float scale_log2, hipStream_t s);

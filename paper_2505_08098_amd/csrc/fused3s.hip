@@ -15,6 +15,10 @@ hipError_t launch_fused(const f3s_plan_s &p, const void *Q, const void *K,
         if (out_f16) return hipErrorInvalidValue;
         return launch_fused_narrow(p, Q, K, V, O, lse, H, d, sl2, s);
     }
+    if (p.flags & 8) {
+        if (out_f16) return hipErrorInvalidValue;
+        return launch_fused_split_row(p, Q, K, V, static_cast<float *>(O), lse, H, d, sl2, s);
+    }
     return out_f16 ? launch_in<kInF16, true>(p, Q, K, V, O, lse, H, d, sl2, s)
                    : launch_in<kInF16, false>(p, Q, K, V, O, lse, H, d, sl2, s);
 }
@@ -23,7 +27,7 @@ hipError_t launch_fused_trace(const f3s_plan_s &p, const void *Q, const void *K,
                               const void *V, void *O, int32_t d, float sl2, uint32_t *trace,
                               hipStream_t s)
 {
-    if (p.flags & 2) return hipErrorInvalidValue;
+    if (p.flags & 10) return hipErrorInvalidValue;
     return launch_in<kInF16, false>(p, Q, K, V, O, nullptr, 1, d, sl2, s, trace);
 }
 

@@ -545,6 +545,89 @@ def test_narrow_gather_ablation_is_bit_identical(gpu, oracle, monkeypatch, k):
     assert e.value.code == 3
 
 
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 3])
+def test_split_row_ablation_matches_oracle(gpu, oracle, monkeypatch, k):
+    """F3S_SPLIT_ROW=1 (the paper's split-row partition): the waves of a work
+    item split the feature dimension -- partial scores summed through LDS
+    once per block pair, each wave's own output columns -- instead of the
+    block pairs.  Same plan arrays; only the order of the score's partial
+    sums differs from the default kernel, so it meets the oracle on every
+    row; other type pairs are refused."""
+    c = W.make_config(k)
+    q, kk, v = (_dev(c[x]) for x in ("Q", "K", "V"))
+    plan = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    ref_gpu, _ = gpu.forward(plan, q, kk, v, scale=c["scale"])
+    monkeypatch.setenv("F3S_SPLIT_ROW", "1")
+    sr = gpu.Plan(_dev(c["row_ptr"]), _dev(c["col_idx"]), c["N"])
+    assert sr.info["flags"] & 8
+    for key in ("n_blocks", "n_items", "n_split"):
+        assert sr.info[key] == plan.info[key]
+    got, got_lse = gpu.forward(sr, q, kk, v, scale=c["scale"])
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.attention_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                                        c["scale"], want_lse=True)
+    _assert_parity(got.cpu().numpy(), ref)
+    got_lse = got_lse.cpu().numpy()
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isfinite(got_lse), fin)
+    assert np.abs(got_lse[fin] - ref_lse[fin]).max() < 2e-3
+    # a different rounding of a score can move a probability's fp16 rounding
+    # by one unit, so the two kernels agree to the parity bound, not bit for bit
+    assert float((got - ref_gpu).abs().max()) <= MAX_ABS
+    with pytest.raises(gpu.F3SError) as e:
+        gpu.forward_typed(sr, q, kk, v, out_dtype=torch.float16)
+    assert e.value.code == 3
+
+
+@pytest.mark.parametrize("d,H", [(64, 3), (128, 2), (192, 1), (256, 1)])
+def test_split_row_ablation_heads_split_windows_ragged(gpu, oracle, monkeypatch, d, H):
+    """The split-row instance at every feature size it takes (2 waves at
+    d = 64 and 192, 4 at 128 and 256), with several heads, split windows
+    (merge launch) and a ragged last window, against the oracle per head."""
+    rng = np.random.default_rng(300 + d + H)
+    N = 1003
+    rp, ci = W.random_csr(rng, N, max_deg=300, empty_frac=0.05, dup_frac=0.1)
+    Q, K, V = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(3))
+    monkeypatch.setenv("F3S_SPLIT_ROW", "1")
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "4")
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    assert plan.info["flags"] & 8 and plan.info["n_split"] > 0
+    O, lse = gpu.forward(plan, _dev(Q), _dev(K), _dev(V), scale=1 / math.sqrt(d))
+    torch.cuda.synchronize()
+    O, lse = O.cpu().numpy(), lse.cpu().numpy()
+    for h in range(H):
+        ref, reflse = oracle.attention_f64(rp, ci, np.ascontiguousarray(Q[:, h]),
+                                           np.ascontiguousarray(K[:, h]),
+                                           np.ascontiguousarray(V[:, h]), 1 / math.sqrt(d),
+                                           want_lse=True)
+        _assert_parity(O[:, h], ref)
+        fin = np.isfinite(reflse)
+        assert np.array_equal(np.isfinite(lse[:, h]), fin)
+        assert np.abs(lse[fin, h] - reflse[fin]).max() < 2e-3
+
+
+def test_split_row_ablation_refuses_other_shapes(gpu, monkeypatch):
+    """d not a multiple of 64, or the narrow-gather ablation as well: refused
+    before any launch (F3S_ERR_UNSUPPORTED)."""
+    rng = np.random.default_rng(5)
+    N = 64
+    rp, ci = W.random_csr(rng, N, max_deg=8)
+    monkeypatch.setenv("F3S_SPLIT_ROW", "1")
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    for d in (32, 96, 160, 224):
+        q = _dev(rng.standard_normal((N, d)).astype(np.float16))
+        with pytest.raises(gpu.F3SError) as e:
+            gpu.forward(plan, q, q, q)
+        assert e.value.code == 3
+    monkeypatch.setenv("F3S_NARROW_GATHER", "1")
+    both = gpu.Plan(_dev(rp), _dev(ci), N)
+    assert both.info["flags"] & 10 == 10
+    q = _dev(rng.standard_normal((N, 64)).astype(np.float16))
+    with pytest.raises(gpu.F3SError) as e:
+        gpu.forward(both, q, q, q)
+    assert e.value.code == 3
+
+
 def _sample_rows_reference(oracle, rp, ci, S, Q, K, V, scale):
     """Oracle rows S of a large problem: the rows S and their neighbours are
     copied into a small problem (neighbour-only rows empty) and the oracle
