@@ -70,6 +70,10 @@ template <> struct BwdWaves<32> { static constexpr int value = 4; };
 template <> struct BwdWaves<64> { static constexpr int value = 2; };
 template <> struct BwdWaves<96> { static constexpr int value = 2; };
 template <> struct BwdWaves<128> { static constexpr int value = 2; };
+// The dQ pass holds fewer registers than the dK/dV pass: at d = 64 it fits
+// four waves per SIMD (128 VGPRs) without spilling.
+template <int D> struct BwdDqWaves { static constexpr int value = BwdWaves<D>::value; };
+template <> struct BwdDqWaves<64> { static constexpr int value = 4; };
 
 // Row-contiguous gather of the 32 rows (two blocks) of a block pair from two
 // row-major fp16 matrices A and B (same rows): chunk f = lane + 64 j is row
@@ -121,7 +125,7 @@ __device__ __forceinline__ int sanitize_slot(int ncol, int lane)
 // dQ^T += K_hat^T dS^T with K_hat read transposed from LDS.
 template <int D, bool kWide, bool kBF16, int NW = 1>
 __global__ __launch_bounds__(64 * NW)
-__attribute__((amdgpu_waves_per_eu(BwdWaves<D>::value, 8))) void k_bwd_dq(
+__attribute__((amdgpu_waves_per_eu(BwdDqWaves<D>::value, 8))) void k_bwd_dq(
     const WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
     const uint32_t *__restrict__ mask, const int32_t *__restrict__ win_row,
     const _Float16 *__restrict__ Q, const _Float16 *__restrict__ K,
@@ -588,7 +592,7 @@ hipError_t launch_bwd_d(const f3s_plan_s &p, const f3s_plan_s &pt, const void *Q
     // dQ: windows of A; partials need 16*D floats per (piece, head)
     {
         const int nw = waves_per_item(p.n_blocks, p.n_items, H,
-                                      (int64_t)BwdWaves<D>::value * 1024);
+                                      (int64_t)BwdDqWaves<D>::value * 1024);
         auto kern = nw == 4   ? (wide ? k_bwd_dq<D, true, kBF16, 4> : k_bwd_dq<D, false, kBF16, 4>)
                     : nw == 2 ? (wide ? k_bwd_dq<D, true, kBF16, 2> : k_bwd_dq<D, false, kBF16, 2>)
                               : (wide ? k_bwd_dq<D, true, kBF16> : k_bwd_dq<D, false, kBF16>);
