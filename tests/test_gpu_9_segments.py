@@ -173,6 +173,22 @@ def test_molecule_batch_forward(gpu, oracle):
     assert np.abs(lse.cpu().numpy() - reflse).max() < 1e-3
 
 
+def test_molecule_batch_forward_split_row(gpu, oracle, monkeypatch):
+    """The split-row ablation instance (F3S_SPLIT_ROW=1) over windows aligned
+    to the graphs: it reads each window's rows from the plan like the
+    default kernel, and meets the oracle on every row."""
+    monkeypatch.setenv("F3S_SPLIT_ROW", "1")
+    c = W.make_config(4)
+    plan = _segment_plan(gpu, c["row_ptr"], c["col_idx"], c["N"], c["seg_ptr"])
+    assert plan.info["flags"] & 12 == 12
+    O, lse = gpu.forward(plan, _dev(c["Q"]), _dev(c["K"]), _dev(c["V"]), scale=c["scale"])
+    torch.cuda.synchronize()
+    ref, reflse = oracle.attention_f64(c["row_ptr"], c["col_idx"], c["Q"], c["K"], c["V"],
+                                       c["scale"], want_lse=True)
+    _check(O.cpu().numpy(), ref)
+    assert np.abs(lse.cpu().numpy() - reflse).max() < 1e-3
+
+
 @pytest.mark.parametrize("order", ["item", "head"])
 def test_molecule_batch_multi_head(gpu, oracle, order, monkeypatch):
     monkeypatch.setenv("F3S_HEAD_MAJOR_BYTES", "0" if order == "head" else str(1 << 40))
