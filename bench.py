@@ -77,6 +77,14 @@ def traffic_from_counters(d):
     return rec.get("hbm_bytes_per_launch")
 
 
+def library_switches():
+    """The library's F3S_* environment switches (ablations and tuning) set for
+    this run, as {"switches": {...}}, or {} when none is set: a line measured
+    under an ablation says so."""
+    sw = {k: v for k, v in sorted(os.environ.items()) if k.startswith("F3S_")}
+    return {"switches": sw} if sw else {}
+
+
 def host_threads():
     """Threads of the oracle baseline: every core this process may run on
     (its affinity mask), unless OMP_NUM_THREADS sets the host's CPU share
@@ -559,7 +567,7 @@ def bench_backward(args, c, plan, Q, K, V, stream, dev):
         "dtype": args.in_dtype, "data": "synthetic",
         "config": {"workload": c["name"], "N": c["N"], "nnz": info["nnz"], "d": d,
                    "windows": "aligned to the graphs" if args.segments else "16 rows",
-                   "heads": H, "in_dtype": args.in_dtype},
+                   "heads": H, "in_dtype": args.in_dtype, **library_switches()},
         "ms_eager_median": round(float(np.median(per)), 5),
         "ms_eager_per_call": round(ms_eager, 5),
         "timing": "eager calls, events around each" if args.no_graph else
@@ -783,6 +791,7 @@ def main():
             "windows": "aligned to the graphs" if args.segments else "16 rows",
             "seed": args.seed,
             "parallelism": "single GPU",
+            **library_switches(),
         },
         "ms_eager_per_call": round(ms_eager, 5),
         "timing": "eager calls, events around each" if args.no_graph else

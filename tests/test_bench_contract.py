@@ -112,3 +112,15 @@ def test_cu_balance_unions_intervals_per_cu():
     # the same CU id on another die is another CU
     rec[4, 5] = 3
     assert bench.cu_balance(rec, 100_000)["cus"] == 3
+
+
+def test_library_switches_are_reported(monkeypatch):
+    """A bench line measured under one of the library's F3S_* switches names
+    it in its config; without any, the config carries no switches entry."""
+    for k in [k for k in os.environ if k.startswith("F3S_")]:
+        monkeypatch.delenv(k)
+    assert bench.library_switches() == {}
+    monkeypatch.setenv("F3S_SPLIT_ROW", "1")
+    monkeypatch.setenv("F3S_PIECE_BLOCKS", "8")
+    assert bench.library_switches() == {
+        "switches": {"F3S_PIECE_BLOCKS": "8", "F3S_SPLIT_ROW": "1"}}
