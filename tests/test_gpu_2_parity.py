@@ -495,17 +495,23 @@ def ctypes_stream():
 
 
 @pytest.mark.parametrize("d", [32, 64, 96, 128, 160, 192, 224, 256])
-def test_split_windows_merge_all_feature_sizes(gpu, oracle, monkeypatch, d):
+@pytest.mark.parametrize("many", [False, True])
+def test_split_windows_merge_all_feature_sizes(gpu, oracle, monkeypatch, d, many):
     """Pieces of 2 blocks: every window above 2 blocks is split and merged
     (the merge kernel's column coverage differs for d = 32, 96, 160, 224);
-    two heads share each launch where 2 * d <= 256."""
+    two heads share each launch where 2 * d <= 256.  `many`: windows of up to
+    ~60 blocks, so some have more than 16 pieces (several rounds of the merge's
+    loads)."""
     monkeypatch.setenv("F3S_PIECE_BLOCKS", "2")
-    rng = np.random.default_rng(500 + d)
-    N, H = 300, 2
-    rp, ci = W.random_csr(rng, N, max_deg=80, empty_frac=0.05, dup_frac=0.1)
+    rng = np.random.default_rng(500 + d + (7 if many else 0))
+    N, H = (1003, 2) if many else (300, 2)
+    rp, ci = W.random_csr(rng, N, max_deg=300 if many else 80, empty_frac=0.05,
+                          dup_frac=0.1)
     Q, K, V = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(3))
     plan = gpu.Plan(_dev(rp), _dev(ci), N)
     assert plan.info["n_split"] > 0
+    max_pieces = -(-plan.info["max_blocks"] // plan.info["piece_blocks"])
+    assert (max_pieces > 16) == many
     O, lse = gpu.forward(plan, _dev(Q), _dev(K), _dev(V), scale=1 / math.sqrt(d))
     torch.cuda.synchronize()
     O, lse = O.cpu().numpy(), lse.cpu().numpy()
