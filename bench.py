@@ -219,6 +219,11 @@ def memory_ceilings(plan, Q, K, V, O, d, achieved_gbs, alg_bytes, stream, dev, r
         out["pattern_gather_ms"] = round(ms, 5)
         out["pattern_gather_GBs"] = round(alg_bytes / ms / 1e6, 1)
         out["frac_of_pattern_gather"] = round(achieved_gbs / out["pattern_gather_GBs"], 4)
+        if d <= 128 and Q.shape[0] * d * 2 <= 0xFFFFFFF0:
+            # the same accesses into LDS, rows in flight bounded by the hardware only
+            ms = graph_timed(lambda: f3s.probe_gather(plan, Q, K, V, O, lds=True), reps,
+                             dev)[1]
+            out["pattern_gather_lds_ms"] = round(ms, 5)
     out["frac_of_stream_read"] = round(achieved_gbs / out["stream_read_GBs"], 4)
     return out
 
@@ -311,6 +316,15 @@ def dram_check(args, stream, dev, reps=10):
     b0.record(stream)
     torch.cuda.synchronize()
     ms_probe = a0.elapsed_time(b0) / reps
+    # the same accesses into LDS with no limit on the rows in flight
+    for _ in range(2):
+        f3s.probe_gather(plan, Q, K, V, O, stream=stream, lds=True)
+    a0.record(stream)
+    for _ in range(reps):
+        f3s.probe_gather(plan, Q, K, V, O, stream=stream, lds=True)
+    b0.record(stream)
+    torch.cuda.synchronize()
+    ms_probe_lds = a0.elapsed_time(b0) / reps
     sink = torch.zeros(256, dtype=torch.int32, device=dev)
     rows_call = lambda: f3s.probe_rows(K, N, 2 * d, sink, in_flight=8, workgroups=2048,
                                        rounds=16, stream=stream)
@@ -328,6 +342,7 @@ def dram_check(args, stream, dev, reps=10):
            "gflops_eff": round(4.0 * info["nnz"] * d / ms / 1e6, 1),
            "pattern_gather_ms": round(ms_probe, 4),
            "pattern_gather_GBs": round(nbytes / ms_probe / 1e6, 1),
+           "pattern_gather_lds_ms": round(ms_probe_lds, 4),
            "random_rows_of_K_GBs": round(rows_gbs, 1)}
     plan.close()
     del Q, K, V, O

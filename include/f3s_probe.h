@@ -15,6 +15,9 @@
  *       16 x d fp32 results per work item), in the same order and
  *       granularity, with no arithmetic and more waves in flight: the
  *       ceiling of that access pattern, from the caches and HBM together.
+ *   f3s_probe_gather_lds              the same accesses with the K and V
+ *       rows loaded straight into LDS and never waited for: the pattern's
+ *       rate with as many rows in flight as the hardware allows.
  *   f3s_probe_rows                    uniformly random whole-row gathers from
  *       a table: the hardware's rate for gather-bound work whose working set
  *       is the table, independent of the operator's own access pattern.
@@ -49,6 +52,17 @@ f3s_status_t f3s_probe_write(void *dst, size_t bytes, uint32_t value, hipStream_
  * windows) receive meaningless values. */
 f3s_status_t f3s_probe_gather(f3s_plan_t plan, const void *Q, const void *K, const void *V,
                               float *O, int32_t d, hipStream_t stream);
+
+/* f3s_probe_gather with the K and V chunks loaded into LDS (16 bytes per
+ * lane, global-to-LDS loads) instead of registers: each wave issues the
+ * loads of its block pairs one pair after another without waiting for any,
+ * all into one LDS area that is read once at the end, so nothing but the
+ * hardware's count of outstanding loads bounds the rows in flight.  An upper
+ * bound for a kernel that gathers into LDS, which must keep each pair there
+ * until it is used.  d in {32, 64, 128} and Q, K, V below 4 GiB, else
+ * F3S_ERR_UNSUPPORTED.  O receives meaningless values. */
+f3s_status_t f3s_probe_gather_lds(f3s_plan_t plan, const void *Q, const void *K,
+                                  const void *V, float *O, int32_t d, hipStream_t stream);
 
 /*
  * Random row gathers: `rows` rows of `row_bytes` bytes (16, 32, 64, 128, 256,

@@ -118,6 +118,8 @@ def load_library():
     L.f3s_probe_write.restype = ctypes.c_int
     L.f3s_probe_gather.argtypes = [vp, vp, vp, vp, vp, i32, vp]
     L.f3s_probe_gather.restype = ctypes.c_int
+    L.f3s_probe_gather_lds.argtypes = [vp, vp, vp, vp, vp, i32, vp]
+    L.f3s_probe_gather_lds.restype = ctypes.c_int
     L.f3s_probe_rows.argtypes = [vp, ctypes.c_int64, i32, i32, i32, i32, vp, vp]
     L.f3s_probe_rows.restype = ctypes.c_int
     L.f3s_run_trace.argtypes = [vp, vp, vp, vp, vp, i32, ctypes.c_float, vp, ctypes.c_size_t,
@@ -476,9 +478,11 @@ def probe_stream(kind, buf, out=None, stream=None):
         raise F3SError(rc, f"f3s_probe_{kind}")
 
 
-def probe_gather(plan, Q, K, V, out, stream=None):
+def probe_gather(plan, Q, K, V, out, stream=None, lds=False):
     """f3s_probe_gather: the fused kernel's memory accesses on ``plan`` for
-    fp16 Q, K, V [N, d] and fp32 out [N, d], without its arithmetic."""
+    fp16 Q, K, V [N, d] and fp32 out [N, d], without its arithmetic
+    (``lds``: f3s_probe_gather_lds, the K and V rows loaded into LDS with no
+    limit on the rows in flight)."""
     shape = tuple(Q.shape)
     for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
         _check_device_tensor(t, n, torch.float16, plan.device)
@@ -489,11 +493,12 @@ def probe_gather(plan, Q, K, V, out, stream=None):
         raise ValueError("out must have the shape of Q")
     if stream is None:
         stream = torch.cuda.current_stream(Q.device)
-    rc = load_library().f3s_probe_gather(plan.handle, Q.data_ptr(), K.data_ptr(),
-                                         V.data_ptr(), out.data_ptr(), int(shape[1]),
-                                         ctypes.c_void_p(stream.cuda_stream))
+    L = load_library()
+    fn = L.f3s_probe_gather_lds if lds else L.f3s_probe_gather
+    rc = fn(plan.handle, Q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(),
+            int(shape[1]), ctypes.c_void_p(stream.cuda_stream))
     if rc != F3S_OK:
-        raise F3SError(rc, "f3s_probe_gather")
+        raise F3SError(rc, "f3s_probe_gather_lds" if lds else "f3s_probe_gather")
 
 
 def probe_rows(table, rows, row_bytes, sink, in_flight=8, workgroups=2048, rounds=4,

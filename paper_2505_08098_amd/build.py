@@ -12,7 +12,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libf3s.so")
 SOURCES = ["f3s_api.hip", "plan_kernels.hip", "fused3s.hip", "fused3s_bf16.hip",
-           "fused3s_fp8.hip", "fused3s_ablation.hip", "fused3s_split_row.hip", "backward.hip", "backward_bf16.hip", "backward_noalloc.hip", "probe.hip",
+           "fused3s_fp8.hip", "fused3s_ablation.hip", "fused3s_split_row.hip",
+           "backward.hip", "backward_bf16.hip", "backward_noalloc.hip", "probe.hip",
            "transpose.hip", "worklist.hip", "radix.hip"]
 
 # The plan and transposition sources are compiled as relocatable device code

@@ -184,6 +184,88 @@ __global__ __launch_bounds__(256) void k_probe_gather(
     }
 }
 
+// The same accesses with the K and V chunks loaded straight into LDS
+// (global_load_lds, 16 bytes per lane: one instruction fills a 1 KB run of
+// the wave's LDS area, lane l at byte 16 l).  The wave walks pairs w, w + 4,
+// ... of the item one after another and never waits for them: every pair
+// overwrites the same 2 NI KB area, which nothing reads back until the end
+// (one word per lane), so the only limit on the rows in flight is the
+// hardware's count of outstanding loads.  This is the rate of the access
+// pattern with unbounded depth, an upper bound for any kernel that gathers
+// the rows into LDS and has to keep each pair there until it is consumed.
+// 32-bit offsets only; D <= 128 (the four waves' areas, 8 D bytes each per
+// 16-byte chunk column, fill at most 64 KB).
+template <int D>
+__global__ __launch_bounds__(256) void k_probe_gather_lds(
+    const f3s::WorkItem *__restrict__ items, const int32_t *__restrict__ cols,
+    const uint32_t *__restrict__ mask, const int32_t *__restrict__ win_row,
+    const char *__restrict__ Q, const char *__restrict__ K, const char *__restrict__ V,
+    float *__restrict__ O, float *__restrict__ part_o, int32_t N, uint32_t order)
+{
+    constexpr int LPR = D / 8;            // 16-byte chunks per row
+    constexpr int NI = D / 16;            // chunks per lane per 32-row tile
+    constexpr int AREA = 2 * NI * 1024;   // a pair's K and V rows, bytes
+    typedef __attribute__((address_space(3))) void lds_void;
+    __shared__ __attribute__((aligned(16))) char lds[4][AREA];
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const f3s::WorkItem it = items[f3s::workgroup_position(order, 1)];
+    int32_t r0, nr;
+    f3s::window_rows(win_row, N, it.window, &r0, &nr);
+    uint32_t acc = 0;
+    for (int f = lane; f < 4 * LPR; f += 64) {
+        const int r = 4 * wv + f / LPR;
+        const int64_t qrow = r0 + (r < nr ? r : 0);
+        acc ^= fold(*reinterpret_cast<const u4 *>(Q + qrow * D * 2 + 16 * (f % LPR)));
+    }
+    const int b0 = it.blk_begin, b1 = it.blk_end;
+    for (int b = b0 + 2 * wv; b < b1; b += 8) {
+        const int slot = lane & 31;
+        const int blk = slot < 16 ? b : min(b + 1, b1 - 1);
+        int c = cols[(int64_t)16 * blk + (slot & 15)];
+        const int first = cols[(int64_t)16 * blk];
+        c = c < 0 ? first : c;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int f = lane + 64 * j;
+            const int col = __shfl(c, f / LPR);
+            const uint32_t off = (uint32_t)col * (uint32_t)(2 * D) + 16u * (f % LPR);
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(K + off),
+                                             (lds_void *)&lds[wv][2 * j * 1024], 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(static_cast<const void *>(V + off),
+                                             (lds_void *)&lds[wv][(2 * j + 1) * 1024], 16, 0,
+                                             0);
+        }
+        acc ^= mask[(int64_t)8 * b + (lane >> 3)] ^
+               mask[(int64_t)8 * min(b + 1, b1 - 1) + (lane >> 3)];
+    }
+    // every load done before the area is read (the compiler does not track
+    // loads into LDS)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    acc ^= reinterpret_cast<const uint32_t *>(lds[wv])[lane];
+    const float val = __builtin_bit_cast(float, acc & 0x3FFFFFFFu);
+    for (int f = lane; f < 4 * (D / 4); f += 64) {
+        const int rr = 4 * wv + f / (D / 4), cc = 4 * (f % (D / 4));
+        const float4 v4 = make_float4(val, val, val, val);
+        if (it.slot < 0) {
+            if (rr < nr) *reinterpret_cast<float4 *>(O + (int64_t)(r0 + rr) * D + cc) = v4;
+        } else {
+            *reinterpret_cast<float4 *>(part_o + ((int64_t)it.slot * 16 + rr) * D + cc) = v4;
+        }
+    }
+}
+
+template <int D>
+hipError_t launch_gather_lds_d(const f3s_plan_s &p, const void *Q, const void *K,
+                               const void *V, float *O, hipStream_t s)
+{
+    k_probe_gather_lds<D><<<p.n_items, 256, 0, s>>>(
+        p.items, p.cols, p.mask, p.win_row, static_cast<const char *>(Q),
+        static_cast<const char *>(K), static_cast<const char *>(V), O, p.part_o, p.N,
+        f3s::xcd_chunks(p, 1) ? f3s::kOrderXcd : 0u);
+    return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_gather_d(const f3s_plan_s &p, const void *Q, const void *K, const void *V,
                            float *O, hipStream_t s)
@@ -298,6 +380,22 @@ f3s_status_t f3s_probe_gather(f3s_plan_t p, const void *Q, const void *K, const 
     case 128: return status(launch_gather_d<128>(*p, Q, K, V, O, stream));
     case 256: return status(launch_gather_d<256>(*p, Q, K, V, O, stream));
     default: return F3S_ERR_UNSUPPORTED;
+    }
+}
+
+f3s_status_t f3s_probe_gather_lds(f3s_plan_t p, const void *Q, const void *K,
+                                  const void *V, float *O, int32_t d, hipStream_t stream)
+{
+    if (!p || !Q || !K || !V || !O) return F3S_ERR_INVALID_VALUE;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O))
+        return F3S_ERR_INVALID_VALUE;
+    if (d != 32 && d != 64 && d != 128) return F3S_ERR_UNSUPPORTED;
+    if ((uint64_t)p->N * (uint64_t)d * 2u > 0xFFFFFFF0ull) return F3S_ERR_UNSUPPORTED;
+    if (p->N == 0 || p->n_items == 0) return F3S_OK;
+    switch (d) {
+    case 32: return status(launch_gather_lds_d<32>(*p, Q, K, V, O, stream));
+    case 64: return status(launch_gather_lds_d<64>(*p, Q, K, V, O, stream));
+    default: return status(launch_gather_lds_d<128>(*p, Q, K, V, O, stream));
     }
 }
 

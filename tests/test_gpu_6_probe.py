@@ -83,6 +83,12 @@ def test_pattern_probe_runs_on_the_workload_plans(gpu, k, monkeypatch):
     torch.cuda.synchronize()
     assert bool(torch.isfinite(O).all())
     assert bool((guard[c["N"]:] == -3.0).all())
+    # the same accesses loaded into LDS
+    O.fill_(-3.0)
+    gpu.probe_gather(plan, q, kk, v, O, lds=True)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(O).all())
+    assert bool((guard[c["N"]:] == -3.0).all())
     # the operator still gives its result on the same plan afterwards
     O2 = gpu.run(plan, q, kk, v, scale=c["scale"])
     torch.cuda.synchronize()
@@ -114,3 +120,24 @@ def test_traced_run_equals_run_and_records_every_workgroup(gpu, k, waves, monkey
     print(f"  {stats}", flush=True)
     assert 1 <= stats["cus"] <= 256
     assert gpu.wall_clock_khz(0) > 0
+
+
+def test_lds_pattern_probe_argument_errors(gpu):
+    """f3s_probe_gather_lds takes d = 32, 64 or 128 (its LDS areas) and
+    refuses other feature sizes before any launch."""
+    rng = np.random.default_rng(11)
+    N = 64
+    rp, ci = W.random_csr(rng, N, max_deg=8)
+    plan = gpu.Plan(_dev(rp), _dev(ci), N)
+    L = gpu.load_library()
+    for d, want in ((256, 3), (96, 3), (48, 3)):
+        q = torch.zeros((N, d), dtype=torch.float16, device=DEV)
+        o = torch.zeros((N, d), dtype=torch.float32, device=DEV)
+        assert L.f3s_probe_gather_lds(plan.handle, q.data_ptr(), q.data_ptr(), q.data_ptr(),
+                                      o.data_ptr(), d, None) == want
+    q = torch.zeros((N, 64), dtype=torch.float16, device=DEV)
+    o = torch.zeros((N, 64), dtype=torch.float32, device=DEV)
+    assert L.f3s_probe_gather_lds(plan.handle, q.data_ptr() + 4, q.data_ptr(), q.data_ptr(),
+                                  o.data_ptr(), 64, None) == 1
+    assert L.f3s_probe_gather_lds(None, q.data_ptr(), q.data_ptr(), q.data_ptr(),
+                                  o.data_ptr(), 64, None) == 1
