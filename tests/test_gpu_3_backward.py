@@ -301,6 +301,21 @@ def test_gradients_workloads(gpu, oracle, k):
                c["scale"])
 
 
+@pytest.mark.parametrize("k,H", [(2, 2), (4, 3), (5, 2)])
+def test_gradients_workloads_several_heads(gpu, oracle, k, H):
+    """Several heads of a workload in one backward call, every head against
+    the oracle: the hub-heavy graph with split windows and window-major
+    order, the molecule batch and the sequence workload head by head over
+    their nearly uniform plans (with XCD ranges, and on the sequence
+    workload two waves per item in the dQ pass)."""
+    c = W.make_config(k, with_features=False)
+    N, d = c["N"], 64
+    rng = np.random.default_rng(40 + k)
+    Q, K, V, G = (rng.standard_normal((N, H, d)).astype(np.float16) for _ in range(4))
+    print(f"workload {k} N={N} heads={H}", flush=True)
+    _grad_case(gpu, oracle, c["row_ptr"], c["col_idx"], N, Q, K, V, G, 1 / math.sqrt(d))
+
+
 @pytest.mark.parametrize("waves", ["1", "2", "4"])
 @pytest.mark.parametrize("order", ["item", "head"])
 @pytest.mark.parametrize("H,d", [(3, 64), (2, 160), (2, 256)])
