@@ -50,6 +50,30 @@ def test_algorithmic_bytes_is_the_sum_over_windows(d, heads):
         int(per_window8.sum())
 
 
+@pytest.mark.parametrize("d,heads", [(64, 1), (128, 2)])
+def test_backward_bytes_is_the_sum_over_both_passes(d, heads):
+    # dQ pass, per 16-row window of A with u_w distinct columns (per head):
+    # Q and G rows 2 * 16*d*2, O rows 16*d*4 (delta = G.O), lse 16*4, K and V
+    # rows 2*2*d*u_w, dQ written 16*d*4, one 8-byte (lse, delta) record per
+    # row written.  dK/dV pass, per window of A^T with v_w distinct columns:
+    # K and V rows 2 * 16*d*2, Q and G rows 2*2*d*v_w plus an 8-byte record
+    # per column, dK and dV written 2 * 16*d*4.  Plan data of both plans:
+    # 96 B per block and 16 B per work item.
+    rng = np.random.default_rng(9)
+    T = 23
+    N = 16 * T
+    u = rng.integers(1, 200, size=T).astype(np.int64)
+    v = rng.integers(1, 200, size=T).astype(np.int64)
+    bu, bv = (u + 15) // 16, (v + 15) // 16
+    per_w_dq = (16 * d * 2 * 2 + 16 * d * 4 + 16 * 4 + 4 * d * u + 16 * d * 4 + 16 * 8)
+    per_w_dkdv = (16 * d * 2 * 2 + 4 * d * v + 8 * v + 2 * 16 * d * 4)
+    want = heads * int(per_w_dq.sum() + per_w_dkdv.sum()) + \
+        96 * int(bu.sum() + bv.sum()) + 16 * 2 * T
+    info = {"N": N, "n_unique": int(u.sum()), "n_blocks": int(bu.sum()), "n_items": T}
+    info_t = {"N": N, "n_unique": int(v.sum()), "n_blocks": int(bv.sum()), "n_items": T}
+    assert bench.backward_bytes(info, info_t, d, heads) == want
+
+
 def _copy_sources(tmp_path):
     for p in bench.KERNEL_SOURCES:
         dst = tmp_path / os.path.relpath(p, ROOT)
