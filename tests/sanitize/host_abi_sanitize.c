@@ -98,6 +98,8 @@ int main(void)
     CHECK(f3s_probe_copy(NULL, NULL, 16, NULL) == F3S_ERR_INVALID_VALUE);
     CHECK(f3s_probe_write(NULL, 16, 0u, NULL) == F3S_ERR_INVALID_VALUE);
     CHECK(f3s_probe_gather(NULL, NULL, NULL, NULL, NULL, 64, NULL) == F3S_ERR_INVALID_VALUE);
+    CHECK(f3s_probe_gather_lds(NULL, NULL, NULL, NULL, NULL, 64, NULL) ==
+          F3S_ERR_INVALID_VALUE);
     CHECK(f3s_probe_rows(NULL, 16, 128, 8, 1, 1, NULL, NULL) == F3S_ERR_INVALID_VALUE);
     CHECK(f3s_run_trace(NULL, NULL, NULL, NULL, NULL, 64, 1.0f, NULL, 0, NULL) ==
           F3S_ERR_INVALID_VALUE);
